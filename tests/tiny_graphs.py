@@ -1,0 +1,142 @@
+"""Small dgir graphs covering every op kind and attribute of the vocabulary,
+plus shrunken versions of the five workloads and of the paper's example.
+Sized so that perturbation over every leaf element and autograd over every
+output element finish in seconds."""
+
+from __future__ import annotations
+
+from paper_2609_19611_amd.workloads import (GraphText, c5_reference_text, c5_variant_text,
+                                            paper_kernel_text, paper_reference_text)
+
+
+def _g(leaves, ops, out, shape):
+    g = GraphText()
+    for n, s in leaves:
+        g.leaf(n, s)
+    for name, kind, operands, attrs in ops:
+        g.op(name, kind, *operands, **attrs)
+    g.output(out, shape)
+    return g.text()
+
+
+def catalogue():
+    """name -> (dgir text, masks) where masks says whether a saturating or
+    selecting op may hide a dependence from perturbation."""
+    G = {}
+    G["matmul2d"] = (_g([("A", [3, 4]), ("B", [4, 2])], [("y", "matmul", ["A", "B"], {})], "y", [3, 2]), False)
+    G["matmul_bcast"] = (_g([("A", [2, 1, 3, 4]), ("B", [3, 4, 2])],
+                            [("y", "matmul", ["A", "B"], {})], "y", [2, 3, 3, 2]), False)
+    G["linear"] = (_g([("x", [2, 3, 4]), ("W", [5, 4]), ("b", [5])],
+                      [("y", "linear", ["x", "W", "b"], {})], "y", [2, 3, 5]), False)
+    G["conv1d_groups"] = (_g([("x", [2, 4, 7]), ("W", [6, 2, 3]), ("b", [6])],
+                             [("y", "conv", ["x", "W", "b"], dict(stride=[2], pad=[1], dilation=[2], groups=2))],
+                             "y", [2, 6, 3]), False)
+    G["conv2d_asym"] = (_g([("x", [1, 2, 5, 6]), ("W", [3, 2, 3, 2])],
+                           [("y", "conv", ["x", "W"], dict(stride=[1, 2], pad=[1, 0], dilation=[1, 1], groups=1))],
+                           "y", [1, 3, 5, 3]), False)
+    G["conv3d_groups"] = (_g([("x", [1, 2, 3, 4, 4]), ("W", [2, 1, 2, 2, 3]), ("b", [2])],
+                             [("y", "conv", ["x", "W", "b"], dict(stride=[1, 1, 1], pad=[0, 1, 1], dilation=[1, 1, 1], groups=2))],
+                             "y", [1, 2, 2, 5, 4]), False)
+    G["convT1d_groups"] = (_g([("x", [1, 4, 5]), ("W", [4, 3, 3]), ("b", [6])],
+                              [("y", "conv_transpose", ["x", "W", "b"],
+                                dict(stride=[2], pad=[1], output_padding=[1], dilation=[1], groups=2))],
+                              "y", [1, 6, 10]), False)
+    G["convT2d_dil"] = (_g([("x", [1, 3, 3, 4]), ("W", [3, 2, 3, 2])],
+                           [("y", "conv_transpose", ["x", "W"],
+                             dict(stride=[2, 3], pad=[1, 0], output_padding=[1, 2], dilation=[1, 2], groups=1))],
+                           "y", [1, 2, 6, 14]), False)
+    G["convT3d"] = (_g([("x", [1, 2, 2, 3, 3]), ("W", [2, 2, 3, 3, 3]), ("b", [2])],
+                       [("y", "conv_transpose", ["x", "W", "b"],
+                         dict(stride=[2, 2, 2], pad=[1, 1, 1], output_padding=[1, 1, 1], dilation=[1, 1, 1], groups=1))],
+                       "y", [1, 2, 4, 6, 6]), False)
+    G["maxpool2d"] = (_g([("x", [1, 2, 5, 5])],
+                         [("y", "max_pool", ["x"], dict(kernel=[3, 3], stride=[2, 2], pad=[1, 1], dilation=[1, 1]))],
+                         "y", [1, 2, 3, 3]), True)
+    G["maxpool2d_dil"] = (_g([("x", [1, 1, 7, 7])],
+                             [("y", "max_pool", ["x"], dict(kernel=[2, 2], stride=[1, 1], pad=[0, 0], dilation=[2, 2]))],
+                             "y", [1, 1, 5, 5]), True)
+    G["avgpool1d"] = (_g([("x", [2, 3, 7])],
+                         [("y", "avg_pool", ["x"], dict(kernel=[3], stride=[2], pad=[1], dilation=[1]))],
+                         "y", [2, 3, 4]), False)
+    G["unary_chain"] = (_g([("x", [2, 3])],
+                           [("a", "exp", ["x"], {}), ("b", "tanh", ["a"], {}), ("c", "sigmoid", ["b"], {}),
+                            ("d", "square", ["c"], {}), ("e", "gelu", ["d"], {}), ("y", "neg", ["e"], {})],
+                           "y", [2, 3]), False)
+    G["binary_bcast"] = (_g([("x", [2, 1, 3]), ("z", [4, 1])],
+                            [("a", "add", ["x", "z"], {}), ("b", "mul", ["a", "z"], {}), ("c", "sub", ["b", "x"], {}),
+                             ("y", "div", ["c", "x"], {})],
+                            "y", [2, 4, 3]), False)
+    G["self_product"] = (_g([("x", [3, 2]), ("w", [2])],
+                            [("a", "mul", ["x", "x"], {}), ("b", "add", ["a", "x"], {}), ("y", "mul", ["b", "w"], {})],
+                            "y", [3, 2]), False)
+    G["maxmin"] = (_g([("x", [3, 4]), ("z", [4]), ("u", [3, 1])],
+                      [("a", "maximum", ["x", "z"], {}), ("y", "minimum", ["a", "u"], {})],
+                      "y", [3, 4]), True)
+    # min(max(x, z), x) == x: z is read (syntactic footprint) but cannot
+    # change the value (semantic footprint); perturbation must give a subset.
+    G["select_absorb"] = (_g([("x", [2, 3]), ("z", [3])],
+                             [("a", "maximum", ["x", "z"], {}), ("y", "minimum", ["a", "x"], {})],
+                             "y", [2, 3]), True)
+    G["reductions"] = (_g([("x", [2, 3, 4])],
+                          [("a", "sum", ["x"], dict(dims=[0, 2], keepdim=1)), ("b", "mul", ["a", "x"], {}),
+                           ("c", "mean", ["b"], dict(dims=[1], keepdim=0)), ("y", "prod", ["c"], dict(dims=[-1], keepdim=1))],
+                          "y", [2, 1]), False)
+    G["amax_full"] = (_g([("x", [2, 3]), ("z", [2, 3])],
+                         [("a", "add", ["x", "z"], {}), ("y", "amax", ["a"], dict(dims=[0, 1], keepdim=0))],
+                         "y", [1]), True)
+    G["softmax"] = (_g([("x", [2, 3, 4])], [("y", "softmax", ["x"], dict(dim=1))], "y", [2, 3, 4]), False)
+    G["log_softmax"] = (_g([("x", [3, 5])], [("y", "log_softmax", ["x"], dict(dim=-1))], "y", [3, 5]), False)
+    G["group_norm"] = (_g([("x", [2, 4, 3]), ("g", [4]), ("b", [4])],
+                          [("y", "group_norm", ["x", "g", "b"], dict(groups=2))], "y", [2, 4, 3]), False)
+    G["group_norm_plain"] = (_g([("x", [1, 6, 2, 2])],
+                                [("y", "group_norm", ["x"], dict(groups=3))], "y", [1, 6, 2, 2]), False)
+    G["batch_norm"] = (_g([("x", [3, 2, 2]), ("g", [2]), ("b", [2])],
+                          [("y", "batch_norm", ["x", "g", "b"], {})], "y", [3, 2, 2]), False)
+    G["layer_norm"] = (_g([("x", [2, 3, 2]), ("g", [3, 2]), ("b", [3, 2])],
+                          [("y", "layer_norm", ["x", "g", "b"], dict(ndims=2))], "y", [2, 3, 2]), False)
+    G["channel_affine"] = (_g([("x", [2, 3, 2]), ("s", [3]), ("t", [3])],
+                              [("y", "channel_affine", ["x", "s", "t"], {})], "y", [2, 3, 2]), False)
+    G["views"] = (_g([("x", [2, 3, 4]), ("z", [4, 1])],
+                     [("a", "slice", ["x"], dict(dim=2, start=1, end=4, step=2)),
+                      ("b", "permute", ["a"], dict(dims=[2, 0, 1])),
+                      ("c", "reshape", ["b"], dict(shape=[4, 3])),
+                      ("d", "expand", ["z"], dict(shape=[2, 4, 3])),
+                      ("y", "add", ["c", "d"], {})],
+                     "y", [2, 4, 3]), False)
+    G["gather_exact_div"] = (_g([("x", [2, 4]), ("w", [3])],
+                                [("y", "affine_gather", ["x", "w"],
+                                  dict(shape=[2, 8], window=[3], idx0=["o0", "(o1+1-w0)/2"], idx1=["w0"], mult=[1, 1]))],
+                                "y", [2, 8]), False)
+    G["gather_floor_flat"] = (_g([("x", [3, 5]), ("v", [2, 3])],
+                                 [("y", "affine_gather", ["x", "v"],
+                                   dict(shape=[4, 3], window=[2, 3], flat=[1, 5],
+                                        idx0=["(o0+w0)//2", "2*o1-w1+1"], idx1=["w0", "w1"], mult=[2, 1]))],
+                                 "y", [4, 3]), False)
+    G["diamond"] = (_g([("x", [2, 3]), ("W", [3, 3])],
+                       [("t", "matmul", ["x", "W"], {}), ("a", "tanh", ["t"], {}), ("b", "sigmoid", ["t"], {}),
+                        ("c", "add", ["a", "b"], {}), ("d", "softmax", ["c"], dict(dim=1)), ("y", "mul", ["d", "t"], {})],
+                       "y", [2, 3]), False)
+    # Shrunken workloads.
+    G["c1"] = (_g([("A", [8, 16]), ("B", [16, 8])],
+                  [("C", "matmul", ["A", "B"], {}), ("R", "relu", ["C"], {}), ("y", "sum", ["R"], dict(dims=[1], keepdim=0))],
+                  "y", [8]), True)
+    G["c2_small"] = (_g([("x", [2, 3, 6, 6]), ("W", [4, 3, 3, 3]), ("conv_b", [4]), ("bias", [4, 1, 1])],
+                        [("t1", "conv", ["x", "W", "conv_b"], dict(stride=[1, 1], pad=[1, 1], dilation=[1, 1], groups=1)),
+                         ("t2", "add", ["t1", "bias"], {}), ("t3", "gelu", ["t2"], {}),
+                         ("y", "max_pool", ["t3"], dict(kernel=[2, 2], stride=[2, 2], pad=[0, 0], dilation=[1, 1]))],
+                        "y", [2, 4, 3, 3]), True)
+    G["c3_small"] = (_g([("x", [1, 2, 3, 3, 4]), ("W", [2, 3, 3, 3, 3]), ("b", [3])],
+                        [("t1", "conv_transpose", ["x", "W", "b"],
+                          dict(stride=[2, 2, 2], pad=[1, 1, 1], output_padding=[1, 1, 1], dilation=[1, 1, 1], groups=1)),
+                         ("t2", "mean", ["t1"], dict(dims=[1], keepdim=0)), ("y", "softmax", ["t2"], dict(dim=3))],
+                        "y", [1, 6, 6, 8]), False)
+    G["c4_small"] = (_g([("x", [3, 8]), ("W", [8, 6]), ("bias", [6]), ("gamma", [6]), ("beta", [6])],
+                        [("h", "matmul", ["x", "W"], {}), ("h2", "add", ["h", "bias"], {}),
+                         ("gn", "group_norm", ["h2", "gamma", "beta"], dict(groups=2)), ("ht", "hardtanh", ["gn"], {}),
+                         ("xs", "slice", ["x"], dict(dim=1, start=0, end=6, step=1)), ("y", "add", ["ht", "xs"], {})],
+                        "y", [3, 6]), True)
+    G["c5_small_ref"] = (c5_reference_text(n=1, c=2, hw=3, co=2), True)
+    G["c5_small_var"] = (c5_variant_text(n=1, c=2, hw=3, co=2, splits=3), True)
+    G["paper_ref_small"] = (paper_reference_text(N=2, C=3, H=4, W=2), True)
+    G["paper_kernel_small"] = (paper_kernel_text(N=2, C=3, H=4, W=2, h_limit=2), True)
+    return G
