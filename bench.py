@@ -1,0 +1,198 @@
+"""Benchmark of batched backward dataflow enumeration on one MI355X.
+
+One step is one pass of the enumeration hot path over the workload's
+location list, with the locations already resident in device memory:
+the sizes kernel (per-location plan + row sizes), the device-wide scan of
+the offsets, and the fill kernel writing the CSR rows.  The default workload
+is the GEMM -> GroupNorm -> Hardtanh -> residual graph with all 65,536
+output locations enumerated (4,366,401,536 entries, 34.9 GB of rows per
+step); --workload selects another configuration (c5 times the two-graph
+comparator over the clean split-K variant and the 16 fault variants).
+
+Prints one JSON line.  Values are synthetic and irrelevant: footprints are
+data independent, so only shapes are used.
+"""
+
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import subprocess
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
+
+
+def parse_args():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=10)
+    p.add_argument("--warmup", type=int, default=3)
+    p.add_argument("--workload", default="c4", choices=["c1", "c2", "c3", "c4", "c5"])
+    p.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the oracle sample")
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    return p.parse_args()
+
+
+def git_sha():
+    try:
+        return subprocess.check_output(["git", "rev-parse", "--short", "HEAD"], cwd=ROOT,
+                                       stderr=subprocess.DEVNULL).decode().strip()
+    except Exception:
+        return None
+
+
+def cpu_baseline(workload, text_a, text_b, locs, target_s):
+    """The oracle, as it stands, on a bounded prefix of the same location list."""
+    import oracle
+    threads = min(16, os.cpu_count() or 1)
+    if workload == "c5":
+        ga, gb = oracle.Graph(text_a), oracle.Graph(text_b)
+        m = 256
+        while True:
+            t0 = time.perf_counter()
+            oracle.compare(ga, gb, locs[:m], threads=threads)
+            dt = time.perf_counter() - t0
+            if dt * 4 > target_s or m >= len(locs):
+                break
+            m = min(len(locs), int(m * max(2.0, 0.8 * target_s / max(dt, 1e-3))))
+        return {"value": m / dt, "unit": "locations/s", "cores": threads, "kind": "oracle",
+                "sample": f"first {m} of {len(locs)} locations, one compare (clean variant)",
+                "seconds": round(dt, 3)}
+    g = oracle.Graph(text_a)
+    m = 16
+    while True:
+        t0 = time.perf_counter()
+        off, _, _ = g.enumerate(locs[:m], threads=threads)
+        dt = time.perf_counter() - t0
+        if dt * 4 > target_s or m >= len(locs):
+            break
+        m = min(len(locs), int(m * max(2.0, 0.8 * target_s / max(dt, 1e-3))))
+    return {"value": float(off[-1]) / dt, "unit": "entries/s", "cores": threads, "kind": "oracle",
+            "sample": f"first {m} of {len(locs)} locations", "locations_per_s": m / dt,
+            "seconds": round(dt, 3)}
+
+
+def main():
+    args = parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU; --gpus {args.gpus} is not supported: each GPU would run an "
+              "independent shard of the location list (no collective on the hot path), so the whole-job "
+              "rate is N times the one-GPU rate measured here.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2609_19611_amd import binding as B
+    from paper_2609_19611_amd import workloads as W
+
+    cfg = W.CONFIGS[args.workload]
+    text = cfg["text"]()
+    locs = W.config_locations(args.workload)
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+    d_locs = torch.as_tensor(locs, dtype=torch.int64, device=dev)
+    n = len(locs)
+    g = B.dg_graph_parse(text)
+    info = B.dg_graph_info(g)
+
+    if args.workload == "c5":
+        variants = [B.dg_graph_parse(W.c5_variant_text())] + [B.dg_graph_parse(W.c5_variant_text(fault=f))
+                                                              for f in W.c5_faults()]
+        ws = torch.empty(max(B.dg_workspace_size(g, n), 1), dtype=torch.uint8, device=dev)
+        status = torch.empty(n, dtype=torch.uint8, device=dev)
+        mism = torch.empty(n, dtype=torch.int64, device=dev)
+
+        def step():
+            k = 0
+            for v in variants:
+                k += B.dg_compare(g, v, d_locs, status, mism, ws)
+            return k
+
+        for _ in range(args.warmup):
+            step()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(args.steps):
+            mismatches = step()
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t0
+        ms = elapsed * 1000 / args.steps
+        compares = len(variants)
+        value = n * compares / (elapsed / args.steps)
+        line = {
+            "metric": "output locations/sec compared (two-graph footprint check)",
+            "value": value, "unit": "locations/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+            "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u32",
+            "data": "synthetic (shapes only; footprints are data independent)",
+            "config": {"workload": "c5: " + cfg["desc"], "locations": n, "compares_per_step": compares,
+                       "mismatching_locations_last_step": int(mismatches)},
+            "roofline": {"bound": "alu", "achieved": None, "peak": None, "unit": None, "frac": None,
+                         "traffic": None},
+        }
+        if not args.no_cpu_baseline:
+            line["cpu_baseline"] = cpu_baseline("c5", text, W.c5_variant_text(), locs, args.cpu_seconds)
+        line["git"] = git_sha()
+        print(json.dumps(line), flush=True)
+        return
+
+    ws = torch.empty(max(B.dg_workspace_size(g, n), 1), dtype=torch.uint8, device=dev)
+    offsets = torch.empty(n + 1, dtype=torch.int64, device=dev)
+    total = B.dg_enumerate_sizes(g, d_locs, offsets, ws)
+    ids = torch.empty(max(total, 1), dtype=torch.int32, device=dev)
+    cnt = torch.empty(max(total, 1), dtype=torch.int32, device=dev)
+    fill_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+               for _ in range(args.steps)]
+
+    def step(i=None):
+        t = B.dg_enumerate_sizes(g, d_locs, offsets, ws)
+        if i is not None:
+            fill_ev[i][0].record(stream)
+        B.dg_enumerate_fill(g, d_locs, offsets, ids, cnt, ws)
+        if i is not None:
+            fill_ev[i][1].record(stream)
+        return t
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        t = step(i)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    assert t == total
+    fill_ms = float(np.mean([a.elapsed_time(b) for a, b in fill_ev]))
+    ms = elapsed * 1000 / args.steps
+    # Algorithmic bytes per location: 8 (location) + 8 (offset) + 8 per entry
+    # (uint32 id + uint32 count).
+    alg_bytes = 16 * n + 8 * total
+    achieved = alg_bytes / (fill_ms * 1e-3) / 1e9
+    line = {
+        "metric": "footprint entries/sec enumerated (with output locations/sec and % of HBM peak)",
+        "value": total / (elapsed / args.steps), "unit": "entries/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "u32",
+        "data": "synthetic (shapes only; footprints are data independent)",
+        "config": {"workload": f"{args.workload}: " + cfg["desc"], "locations": n, "entries_per_step": total,
+                   "locations_per_s": n / (elapsed / args.steps), "block_threads": info["block_threads"],
+                   "lds_bytes": info["lds_bytes"]},
+        "roofline": {"bound": "hbm", "kernel": "k_fill", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None, "fill_ms": fill_ms,
+                     "algorithmic_bytes": alg_bytes},
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(args.workload, text, None, locs, args.cpu_seconds)
+    line["git"] = git_sha()
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,232 @@
+/*
+ * dirigo_rocm.h -- batched backward dataflow enumeration on MI355X (gfx950).
+ *
+ * For a fixed-shape tensor-op graph in SSA form and a list of output
+ * locations, each call returns the exact input-element footprint of every
+ * location together with per-element path counts (Sec. 3.4 of "The
+ * Output-Space Hypothesis: Enumerative Equivalence Checking for Tensor
+ * Programs", "Per-element equations" and "Back-projection"):
+ *
+ *   res(y[l]) substitutes each op's per-element equation f_k backwards until
+ *   only input (leaf) elements remain; the footprint of l is the set of leaf
+ *   elements occurring in res(y[l]) and the path count of a leaf element is
+ *   its number of occurrences.
+ *
+ * Conventions shared by every call:
+ *  - A location is a flat row-major index into the output's logical shape
+ *    (Sec. 3.3 "Setup": R_y maps flat indices of y).
+ *  - A leaf element's global id is base[leaf] + its row-major flat index,
+ *    where base is the running element count in leaf declaration order.
+ *  - A row lists its leaf elements by ascending global id.  Rows are stored
+ *    as CSR: offsets[n+1] (int64) plus two parallel arrays ids[] and
+ *    counts[] (uint32, structure of arrays).
+ *  - Values never matter: footprints are data independent (Sec. 2, Sec. 3.4
+ *    "Flipping the quantifiers"); tensors have shapes only.
+ *  - The dataflow reading of each op (which elements it reads and how
+ *    often) follows the Torch lowerings of Sec. 3.3: each tensor element is
+ *    one variable; activations are uninterpreted functions of their operand;
+ *    selects (max, min, clamp) read each operand once; constants (padding,
+ *    eps, 1/n) are not variables; softmax reads its slice once and l once
+ *    more; a normalisation with statistics set S reads x[s] |S| + 2 times,
+ *    x[l] once more, and its affine parameters once.
+ *
+ * Memory and streams: every device pointer argument is caller-owned device
+ * memory (for example a torch tensor's data pointer); `stream` is a
+ * hipStream_t passed as void* (NULL = the default stream).  The library
+ * allocates no device memory in these calls except the compiled graph
+ * itself (a few KB), which each graph handle uploads once per device on its
+ * first use and frees in dg_graph_destroy.  Scratch space is the caller's
+ * workspace, sized by dg_workspace_size.
+ *
+ * Errors: every call returns a dg_status; 0 is success, negative values are
+ * errors and dg_last_error() returns a message for the calling thread.  No
+ * C++ exception crosses this interface.
+ *
+ * Thread safety: a dg_graph is immutable after construction and may be used
+ * from several host threads and streams at once.  Calls that share one
+ * workspace buffer must not overlap in time.
+ */
+#ifndef DIRIGO_ROCM_H
+#define DIRIGO_ROCM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t dg_status;
+
+#define DG_OK 0
+#define DG_E_INVALID_ARG (-1)    /* null pointer, negative size, bad index */
+#define DG_E_PARSE (-2)          /* malformed dgir text */
+#define DG_E_SHAPE (-3)          /* inconsistent shapes or attributes */
+#define DG_E_UNSUPPORTED_OP (-4) /* op kind, or a form of it, not handled */
+#define DG_E_RANGE (-5)          /* a location outside [0, output numel) */
+#define DG_E_OVERFLOW (-6)       /* leaf elements >= 2^32, or a path count
+                                    that does not fit 32 bits */
+#define DG_E_SIGNATURE (-7)      /* compare: leaves or output shape differ */
+#define DG_E_WORKSPACE (-8)      /* workspace missing or too small */
+#define DG_E_HIP (-9)            /* HIP runtime error (message attached) */
+#define DG_E_CAPACITY (-10)      /* the per-location plan of this graph does
+                                    not fit the device's local data share */
+
+#define DG_MAX_RANK 8
+#define DG_NAME_LEN 64
+
+typedef struct dg_graph dg_graph;
+
+/* ------------------------------------------------------------------------
+ * Graph construction.
+ * ------------------------------------------------------------------------
+ * dg_graph_parse: builds a graph from dgir v1 text (`len` bytes, not
+ * necessarily NUL-terminated):
+ *
+ *     dgir 1
+ *     leaf <name> <d0,d1,...>
+ *     op <name> <kind> <operand> [<operand> ...] [; key=value ...]
+ *     output <name> <d0,d1,...>
+ *
+ * Ops are in SSA order (each writes one new tensor and reads earlier ones,
+ * Sec. 3.4 "Per-element equations"); the output line names the checked
+ * tensor and states its shape, which must equal the inferred one.  Op kinds:
+ *   matmul A B                     batched, NumPy-broadcast batch dims
+ *   linear x W [b]                 y = x W^T + b, W is [out, in]
+ *   conv x W [b]                   stride= pad= dilation= groups=
+ *   conv_transpose x W [b]         stride= pad= output_padding= dilation= groups=
+ *   max_pool x | avg_pool x        kernel= stride= pad= dilation=
+ *   relu gelu gelu_tanh hardtanh clamp sigmoid tanh exp log log1p square sqrt
+ *   rsqrt neg abs identity contiguous silu softplus erf scale leaky_relu elu
+ *   reciprocal x                   elementwise unary
+ *   add sub mul div maximum minimum pow a b   broadcasting binary
+ *   sum mean amax amin prod max min x        dims= keepdim=
+ *   softmax x | log_softmax x      dim=
+ *   group_norm x [g b] groups= | batch_norm x [g b] | layer_norm x [g b] ndims=
+ *   channel_affine x scale shift   x * scale[c] + shift[c], c = dim 1
+ *   slice x dim= start= end= step= | permute x dims= | reshape x shape= |
+ *   expand x shape=
+ *   affine_gather a [b ...]        shape= window= flat=lo,hi idx0=... mult=...
+ *     the inverted affine write set of a custom kernel (Sec. 3.4: with the
+ *     written location fixed, every read index is affine): for every window
+ *     point w whose row-major flat index lies in [lo, hi), operand j is read
+ *     at index idxj(o, w) with multiplicity mult[j], provided every operand
+ *     index of that point is in range (and exactly divisible where written
+ *     "(expr)/s"; "(expr)//s" floors).  Expressions are sums of c*o<k>,
+ *     c*w<k> and integers.
+ * Returns DG_E_PARSE, DG_E_SHAPE, DG_E_UNSUPPORTED_OP or DG_E_OVERFLOW
+ * (leaf elements >= 2^32, or a static path-count bound beyond 64 bits) on
+ * failure; *out is set only on success and is owned by the caller, who
+ * releases it with dg_graph_destroy.
+ */
+dg_status dg_graph_parse(const char* text, size_t len, dg_graph** out);
+
+/* dg_graph_build: the same graph from descriptors instead of text.
+ * tensors[0..nt) are the leaves in declaration order (name, rank, shape);
+ * ops[0..nops) are in SSA order; op i writes tensor nt + i, and operand
+ * indices refer to that numbering; `attrs` is the text after ';' in the
+ * dgir form (may be NULL).  output_tensor indexes the same numbering. */
+typedef struct {
+  const char* name;
+  int32_t rank;
+  const int64_t* shape;
+} dg_tensor_desc;
+
+typedef struct {
+  const char* name;   /* name of the tensor the op writes */
+  const char* kind;
+  int32_t n_inputs;
+  const int32_t* inputs;
+  const char* attrs;
+} dg_op_desc;
+
+dg_status dg_graph_build(const dg_tensor_desc* tensors, int32_t nt, const dg_op_desc* ops, int32_t nops,
+                         int32_t output_tensor, dg_graph** out);
+
+/* Releases a graph and its per-device copies; NULL is ignored.  Must not
+ * be called while work using the graph is still queued on a stream. */
+void dg_graph_destroy(dg_graph* g);
+
+/* ------------------------------------------------------------------------
+ * Introspection (host only; no device work).
+ * ------------------------------------------------------------------------ */
+typedef struct {
+  int32_t n_leaves;
+  int32_t output_rank;
+  int64_t output_shape[DG_MAX_RANK];
+  int64_t output_numel;
+  uint64_t leaf_total;        /* total leaf elements (global id space) */
+  int64_t max_row_size;       /* static upper bound on one row's entries */
+  double count_bound;         /* static upper bound on one path count */
+  int32_t n_instructions;     /* per-location plan length */
+  int32_t lds_bytes;          /* local data share one location needs */
+  int32_t block_threads;      /* threads working on one location */
+  int32_t max_leaf_terms;     /* separable terms of the busiest leaf */
+} dg_graph_info_t;
+
+dg_status dg_graph_info(const dg_graph* g, dg_graph_info_t* out);
+
+typedef struct {
+  char name[DG_NAME_LEN];
+  int32_t rank;
+  int64_t shape[DG_MAX_RANK];
+  uint64_t base;   /* global id of the leaf's element 0 */
+  int64_t numel;
+} dg_leaf_info_t;
+
+/* Leaf i in declaration order, 0 <= i < n_leaves. */
+dg_status dg_graph_leaf(const dg_graph* g, int32_t i, dg_leaf_info_t* out);
+
+/* ------------------------------------------------------------------------
+ * Enumeration.
+ * ------------------------------------------------------------------------
+ * dg_workspace_size: bytes of device workspace that dg_enumerate_sizes,
+ * dg_enumerate_fill and dg_compare need for n_locs locations (the same
+ * buffer serves all three; for dg_compare pass the larger of the two
+ * graphs' sizes). */
+dg_status dg_workspace_size(const dg_graph* g, int64_t n_locs, size_t* bytes);
+
+/* dg_enumerate_sizes: row sizes and CSR offsets.
+ *   d_locs[n]        device, int64 flat output locations (any order,
+ *                    duplicates allowed: each gets its own row)
+ *   d_offsets[n+1]   device, written: d_offsets[0] = 0 and d_offsets[i+1]
+ *                    = d_offsets[i] + |row i|
+ *   d_ws             device workspace of dg_workspace_size bytes
+ *   h_total          host, written: d_offsets[n] (the number of entries)
+ * Synchronous: returns after the stream has finished this work.  Returns
+ * DG_E_RANGE if a location is outside the output and DG_E_OVERFLOW if a
+ * path count does not fit 32 bits; d_offsets is then unspecified.
+ * n == 0 writes d_offsets[0] = 0 and *h_total = 0. */
+dg_status dg_enumerate_sizes(const dg_graph* g, const int64_t* d_locs, int64_t n, int64_t* d_offsets,
+                             void* d_ws, int64_t* h_total, void* stream);
+
+/* dg_enumerate_fill: writes row i to d_ids / d_counts at positions
+ * [d_offsets[i], d_offsets[i+1]).  d_offsets must come from
+ * dg_enumerate_sizes on the same graph and locations (a caller chunking a
+ * large list passes a slice of d_locs and that slice's own offsets, which
+ * start at 0).  d_ids and d_counts hold d_offsets[n] entries each.
+ * Asynchronous on `stream`. */
+dg_status dg_enumerate_fill(const dg_graph* g, const int64_t* d_locs, int64_t n, const int64_t* d_offsets,
+                            uint32_t* d_ids, uint32_t* d_counts, void* d_ws, void* stream);
+
+/* dg_compare: footprints of two graphs, location by location (Sec. 3.4:
+ * e_A and e_B at the same l; the two programs read the same leaves and
+ * write outputs of the same shape, as MERGE's input/output matching of
+ * Sec. 3.2 requires, else DG_E_SIGNATURE).
+ *   d_status[n]      device, written: 0 rows equal, 1 the id sets differ,
+ *                    2 same ids but some count differs
+ *   d_mismatch[n]    device, written: the positions i (into d_locs) with
+ *                    d_status[i] != 0, ascending
+ *   h_n_mismatch     host, written: how many positions were written
+ * Synchronous.  DG_E_RANGE / DG_E_OVERFLOW as for dg_enumerate_sizes. */
+dg_status dg_compare(const dg_graph* a, const dg_graph* b, const int64_t* d_locs, int64_t n, uint8_t* d_status,
+                     int64_t* d_mismatch, int64_t* h_n_mismatch, void* d_ws, void* stream);
+
+/* Message of the calling thread's last failed call ("" if none). */
+const char* dg_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* DIRIGO_ROCM_H */

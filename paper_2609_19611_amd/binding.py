@@ -1,0 +1,269 @@
+"""ctypes binding of libdirigo_rocm.so.
+
+The functions named ``dg_*`` take the C ABI's arguments (device buffers as
+torch tensors, streams as torch streams) and only marshal them; every step
+of the enumeration runs in the library's HIP kernels.  ``enumerate_locations``
+and ``compare_locations`` are conveniences that allocate the outputs with torch and call
+the ``dg_*`` functions in order.
+
+Importing this module fails loudly if the library has not been built.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import torch
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "lib", "libdirigo_rocm.so")
+HEADER = os.path.join(os.path.dirname(HERE), "include", "dirigo_rocm.h")
+
+DG_OK = 0
+STATUS_NAMES = {
+    -1: "DG_E_INVALID_ARG", -2: "DG_E_PARSE", -3: "DG_E_SHAPE", -4: "DG_E_UNSUPPORTED_OP", -5: "DG_E_RANGE",
+    -6: "DG_E_OVERFLOW", -7: "DG_E_SIGNATURE", -8: "DG_E_WORKSPACE", -9: "DG_E_HIP", -10: "DG_E_CAPACITY",
+}
+MAX_RANK = 8
+
+
+class DgError(RuntimeError):
+    def __init__(self, code: int, message: str):
+        super().__init__(f"{STATUS_NAMES.get(code, code)}: {message}")
+        self.code = code
+        self.name = STATUS_NAMES.get(code, str(code))
+
+
+class GraphInfo(ctypes.Structure):
+    _fields_ = [
+        ("n_leaves", ctypes.c_int32),
+        ("output_rank", ctypes.c_int32),
+        ("output_shape", ctypes.c_int64 * MAX_RANK),
+        ("output_numel", ctypes.c_int64),
+        ("leaf_total", ctypes.c_uint64),
+        ("max_row_size", ctypes.c_int64),
+        ("count_bound", ctypes.c_double),
+        ("n_instructions", ctypes.c_int32),
+        ("lds_bytes", ctypes.c_int32),
+        ("block_threads", ctypes.c_int32),
+        ("max_leaf_terms", ctypes.c_int32),
+    ]
+
+
+class LeafInfo(ctypes.Structure):
+    _fields_ = [
+        ("name", ctypes.c_char * 64),
+        ("rank", ctypes.c_int32),
+        ("shape", ctypes.c_int64 * MAX_RANK),
+        ("base", ctypes.c_uint64),
+        ("numel", ctypes.c_int64),
+    ]
+
+
+class TensorDesc(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char_p), ("rank", ctypes.c_int32), ("shape", ctypes.POINTER(ctypes.c_int64))]
+
+
+class OpDesc(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char_p), ("kind", ctypes.c_char_p), ("n_inputs", ctypes.c_int32),
+                ("inputs", ctypes.POINTER(ctypes.c_int32)), ("attrs", ctypes.c_char_p)]
+
+
+def _load():
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is not built: run `python -m paper_2609_19611_amd.build` "
+                           "(or __graft_entry__.build()) first")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    sig = {
+        "dg_graph_parse": ([ctypes.c_char_p, sz, ctypes.POINTER(P)], i32),
+        "dg_graph_build": ([P, i32, P, i32, i32, ctypes.POINTER(P)], i32),
+        "dg_graph_destroy": ([P], None),
+        "dg_graph_info": ([P, ctypes.POINTER(GraphInfo)], i32),
+        "dg_graph_leaf": ([P, i32, ctypes.POINTER(LeafInfo)], i32),
+        "dg_workspace_size": ([P, i64, ctypes.POINTER(sz)], i32),
+        "dg_enumerate_sizes": ([P, P, i64, P, P, ctypes.POINTER(i64), P], i32),
+        "dg_enumerate_fill": ([P, P, i64, P, P, P, P, P], i32),
+        "dg_compare": ([P, P, P, i64, P, P, ctypes.POINTER(i64), P, P], i32),
+        "dg_last_error": ([], ctypes.c_char_p),
+    }
+    for name, (args, res) in sig.items():
+        fn = getattr(lib, name)
+        fn.argtypes = args
+        fn.restype = res
+    return lib
+
+
+_lib = _load()
+
+
+def _check(rc: int) -> None:
+    if rc != DG_OK:
+        raise DgError(rc, _lib.dg_last_error().decode())
+
+
+def header_symbols() -> list[str]:
+    """Names of the functions include/dirigo_rocm.h declares."""
+    text = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:dg_status|void|const char\*)\s+(dg_\w+)\s*\(", text, re.M)))
+
+
+def _ptr(t: torch.Tensor | None) -> int | None:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream) -> int | None:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream
+
+
+class Graph:
+    """An owned dg_graph handle."""
+
+    def __init__(self, handle):
+        self._h = handle
+
+    def __del__(self):
+        h = getattr(self, "_h", None)
+        if h:
+            _lib.dg_graph_destroy(h)
+            self._h = None
+
+    @property
+    def handle(self):
+        return self._h
+
+
+def dg_graph_parse(text: str) -> Graph:
+    data = text.encode()
+    h = ctypes.c_void_p()
+    _check(_lib.dg_graph_parse(data, len(data), ctypes.byref(h)))
+    return Graph(h)
+
+
+def dg_graph_build(leaves, ops, output: int) -> Graph:
+    """leaves: [(name, shape)]; ops: [(name, kind, [input indices], attrs)]."""
+    keep = []
+    td = (TensorDesc * len(leaves))()
+    for i, (name, shape) in enumerate(leaves):
+        arr = (ctypes.c_int64 * len(shape))(*shape)
+        keep.append(arr)
+        td[i] = TensorDesc(name.encode(), len(shape), arr)
+    od = (OpDesc * max(1, len(ops)))()
+    for i, (name, kind, ins, attrs) in enumerate(ops):
+        arr = (ctypes.c_int32 * max(1, len(ins)))(*ins)
+        keep.append(arr)
+        od[i] = OpDesc(name.encode(), kind.encode(), len(ins), arr, (attrs or "").encode())
+    h = ctypes.c_void_p()
+    _check(_lib.dg_graph_build(td, len(leaves), od, len(ops), output, ctypes.byref(h)))
+    return Graph(h)
+
+
+def dg_graph_info(g: Graph) -> dict:
+    info = GraphInfo()
+    _check(_lib.dg_graph_info(g.handle, ctypes.byref(info)))
+    return {
+        "n_leaves": info.n_leaves,
+        "output_shape": tuple(info.output_shape[: info.output_rank]),
+        "output_numel": info.output_numel,
+        "leaf_total": info.leaf_total,
+        "max_row_size": info.max_row_size,
+        "count_bound": info.count_bound,
+        "n_instructions": info.n_instructions,
+        "lds_bytes": info.lds_bytes,
+        "block_threads": info.block_threads,
+        "max_leaf_terms": info.max_leaf_terms,
+    }
+
+
+def dg_graph_leaf(g: Graph, i: int) -> dict:
+    li = LeafInfo()
+    _check(_lib.dg_graph_leaf(g.handle, i, ctypes.byref(li)))
+    return {"name": li.name.decode(), "shape": tuple(li.shape[: li.rank]), "base": li.base, "numel": li.numel}
+
+
+def dg_workspace_size(g: Graph, n_locs: int) -> int:
+    b = ctypes.c_size_t()
+    _check(_lib.dg_workspace_size(g.handle, n_locs, ctypes.byref(b)))
+    return b.value
+
+
+def _dev_i64(t: torch.Tensor, what: str) -> None:
+    if not t.is_cuda or t.dtype != torch.int64 or not t.is_contiguous():
+        raise ValueError(f"{what} must be a contiguous int64 device tensor")
+
+
+def dg_enumerate_sizes(g: Graph, d_locs: torch.Tensor, d_offsets: torch.Tensor, d_ws: torch.Tensor,
+                       stream=None) -> int:
+    n = d_locs.numel()
+    _dev_i64(d_locs, "locations")
+    _dev_i64(d_offsets, "offsets")
+    if d_offsets.numel() < n + 1:
+        raise ValueError("offsets needs n + 1 entries")
+    total = ctypes.c_int64()
+    _check(_lib.dg_enumerate_sizes(g.handle, _ptr(d_locs), n, _ptr(d_offsets), _ptr(d_ws), ctypes.byref(total),
+                                   _stream(stream)))
+    return total.value
+
+
+def dg_enumerate_fill(g: Graph, d_locs: torch.Tensor, d_offsets: torch.Tensor, d_ids: torch.Tensor,
+                      d_counts: torch.Tensor, d_ws: torch.Tensor, stream=None) -> None:
+    n = d_locs.numel()
+    for t, what in ((d_ids, "ids"), (d_counts, "counts")):
+        if not t.is_cuda or t.dtype not in (torch.int32, torch.uint32) or not t.is_contiguous():
+            raise ValueError(f"{what} must be a contiguous 32-bit device tensor")
+    _check(_lib.dg_enumerate_fill(g.handle, _ptr(d_locs), n, _ptr(d_offsets), _ptr(d_ids), _ptr(d_counts),
+                                  _ptr(d_ws), _stream(stream)))
+
+
+def dg_compare(a: Graph, b: Graph, d_locs: torch.Tensor, d_status: torch.Tensor, d_mismatch: torch.Tensor,
+               d_ws: torch.Tensor, stream=None) -> int:
+    n = d_locs.numel()
+    _dev_i64(d_locs, "locations")
+    if d_status.dtype != torch.uint8 or d_status.numel() < n:
+        raise ValueError("status must be a uint8 device tensor of n entries")
+    _dev_i64(d_mismatch, "mismatch")
+    nm = ctypes.c_int64()
+    _check(_lib.dg_compare(a.handle, b.handle, _ptr(d_locs), n, _ptr(d_status), _ptr(d_mismatch),
+                           ctypes.byref(nm), _ptr(d_ws), _stream(stream)))
+    return nm.value
+
+
+def dg_last_error() -> str:
+    return _lib.dg_last_error().decode()
+
+
+# ---------------------------------------------------------------- helpers --
+def workspace(g: Graph, n: int, device=None) -> torch.Tensor:
+    return torch.empty(max(1, dg_workspace_size(g, n)), dtype=torch.uint8, device=device or "cuda")
+
+
+def enumerate_locations(g: Graph, locs, stream=None):
+    """(offsets int64[n+1], ids int32[total], counts int32[total]) on the device.
+    ids and counts hold uint32 values in int32 storage."""
+    d_locs = locs if isinstance(locs, torch.Tensor) else torch.as_tensor(locs, dtype=torch.int64)
+    d_locs = d_locs.to(device="cuda", dtype=torch.int64).contiguous()
+    n = d_locs.numel()
+    ws = workspace(g, n, d_locs.device)
+    offsets = torch.empty(n + 1, dtype=torch.int64, device=d_locs.device)
+    total = dg_enumerate_sizes(g, d_locs, offsets, ws, stream)
+    ids = torch.empty(max(1, total), dtype=torch.int32, device=d_locs.device)
+    cnt = torch.empty(max(1, total), dtype=torch.int32, device=d_locs.device)
+    dg_enumerate_fill(g, d_locs, offsets, ids, cnt, ws, stream)
+    return offsets, ids[:total], cnt[:total]
+
+
+def compare_locations(a: Graph, b: Graph, locs, stream=None):
+    """(status uint8[n], mismatch positions int64[k]) on the device."""
+    d_locs = locs if isinstance(locs, torch.Tensor) else torch.as_tensor(locs, dtype=torch.int64)
+    d_locs = d_locs.to(device="cuda", dtype=torch.int64).contiguous()
+    n = d_locs.numel()
+    ws = torch.empty(max(dg_workspace_size(a, n), dg_workspace_size(b, n), 1), dtype=torch.uint8,
+                     device=d_locs.device)
+    status = torch.empty(max(1, n), dtype=torch.uint8, device=d_locs.device)
+    mism = torch.empty(max(1, n), dtype=torch.int64, device=d_locs.device)
+    k = dg_compare(a, b, d_locs, status, mism, ws, stream)
+    return status[:n], mism[:k]

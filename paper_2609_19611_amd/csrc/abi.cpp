@@ -1,0 +1,319 @@
+// C ABI of libdirigo_rocm (declared in include/dirigo_rocm.h).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <new>
+#include <string>
+
+#include "../../include/dirigo_rocm.h"
+#include "compile.h"
+#include "graph.h"
+#include "kernels.h"
+
+struct dg_graph {
+  dg::GraphIR ir;
+  dg::Plan plan;
+  int block = 64;
+  uint32_t lds = 0;
+  std::mutex mu;
+  std::map<int, uint8_t*> dev_blob;  // compiled plan per device
+};
+
+namespace {
+
+thread_local std::string g_last_error;
+
+dg_status set_error(dg_status code, const std::string& msg) {
+  g_last_error = msg;
+  return code;
+}
+
+dg_status hip_error(hipError_t e, const char* where) {
+  return set_error(DG_E_HIP, std::string(where) + ": " + hipGetErrorString(e));
+}
+
+#define DG_HIP(call, where)              \
+  do {                                   \
+    hipError_t e_ = (call);              \
+    if (e_ != hipSuccess) return hip_error(e_, where); \
+  } while (0)
+
+int max_lds_per_block() {
+  int dev = 0, v = 65536;
+  if (hipGetDevice(&dev) == hipSuccess) {
+    int x = 0;
+    if (hipDeviceGetAttribute(&x, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) == hipSuccess && x > 0) v = x;
+  }
+  return v;
+}
+
+// Finishes a freshly parsed graph: compile, pick the block size and the LDS
+// footprint of one location.
+dg_status finalize(dg_graph* g) {
+  g->plan = dg::compile_plan(g->ir);
+  g->block = g->plan.max_row_size >= 4096 ? 256 : 64;
+  g->lds = dg::plan_lds_bytes(g->plan);
+  return DG_OK;
+}
+
+dg_status device_blob(const dg_graph* cg, const uint8_t** out) {
+  dg_graph* g = const_cast<dg_graph*>(cg);
+  int dev = 0;
+  DG_HIP(hipGetDevice(&dev), "hipGetDevice");
+  std::lock_guard<std::mutex> lock(g->mu);
+  auto it = g->dev_blob.find(dev);
+  if (it != g->dev_blob.end()) {
+    *out = it->second;
+    return DG_OK;
+  }
+  void* p = nullptr;
+  const size_t bytes = g->plan.blob.size();
+  DG_HIP(hipMalloc(&p, bytes), "hipMalloc(plan)");
+  hipError_t e = hipMemcpy(p, g->plan.blob.data(), bytes, hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    (void)hipFree(p);
+    return hip_error(e, "hipMemcpy(plan)");
+  }
+  g->dev_blob[dev] = static_cast<uint8_t*>(p);
+  *out = static_cast<uint8_t*>(p);
+  return DG_OK;
+}
+
+struct WsLayout {
+  size_t err, sums, flags, total;
+};
+
+WsLayout ws_layout(int64_t n) {
+  WsLayout w;
+  w.err = 0;
+  w.sums = 256;
+  w.flags = w.sums + 8 * (size_t)dgk::scan_temp_entries(n < 0 ? 0 : n);
+  w.flags = (w.flags + 255) & ~size_t(255);
+  w.total = w.flags + 8 * (size_t)((n < 0 ? 0 : n) + 1);
+  w.total = (w.total + 255) & ~size_t(255);
+  return w;
+}
+
+dg_status device_errors(uint32_t bits) {
+  if (bits & DGP_ERR_RANGE) return set_error(DG_E_RANGE, "a location lies outside the output tensor");
+  if (bits & DGP_ERR_OVERFLOW) return set_error(DG_E_OVERFLOW, "a path count does not fit 32 bits");
+  if (bits & DGP_ERR_CAPACITY)
+    return set_error(DG_E_CAPACITY, "a per-location factor outgrew its compiled capacity");
+  if (bits & DGP_ERR_SIZE) return set_error(DG_E_INVALID_ARG, "offsets do not match this graph and locations");
+  return DG_OK;
+}
+
+template <class F>
+dg_status guarded(F f) {
+  try {
+    return f();
+  } catch (const dg::Failure& e) {
+    return set_error(e.code, e.what());
+  } catch (const std::bad_alloc&) {
+    return set_error(DG_E_INVALID_ARG, "out of host memory");
+  } catch (const std::exception& e) {
+    return set_error(DG_E_INVALID_ARG, e.what());
+  }
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* dg_last_error(void) { return g_last_error.c_str(); }
+
+dg_status dg_graph_parse(const char* text, size_t len, dg_graph** out) {
+  if (!text || !out) return set_error(DG_E_INVALID_ARG, "null argument");
+  return guarded([&]() -> dg_status {
+    dg_graph* g = new dg_graph;
+    try {
+      g->ir = dg::parse_dgir(std::string(text, len));
+      finalize(g);
+    } catch (...) {
+      delete g;
+      throw;
+    }
+    *out = g;
+    return DG_OK;
+  });
+}
+
+dg_status dg_graph_build(const dg_tensor_desc* tensors, int32_t nt, const dg_op_desc* ops, int32_t nops,
+                         int32_t output_tensor, dg_graph** out) {
+  if (!out || nt <= 0 || nops < 0 || !tensors || (nops > 0 && !ops))
+    return set_error(DG_E_INVALID_ARG, "bad descriptor arguments");
+  return guarded([&]() -> dg_status {
+    dg_graph* g = new dg_graph;
+    try {
+      for (int32_t i = 0; i < nt; ++i) {
+        const dg_tensor_desc& t = tensors[i];
+        if (!t.name || !t.shape || t.rank <= 0 || t.rank > DG_MAX_RANK)
+          throw dg::Failure(DG_E_INVALID_ARG, "bad tensor descriptor " + std::to_string(i));
+        dg::add_leaf(g->ir, t.name, dg::Dims(t.shape, t.shape + t.rank));
+      }
+      for (int32_t i = 0; i < nops; ++i) {
+        const dg_op_desc& o = ops[i];
+        if (!o.name || !o.kind || o.n_inputs < 0 || (o.n_inputs > 0 && !o.inputs))
+          throw dg::Failure(DG_E_INVALID_ARG, "bad op descriptor " + std::to_string(i));
+        std::vector<int> in(o.inputs, o.inputs + o.n_inputs);
+        for (int t : in)
+          if (t < 0 || t >= nt + i) throw dg::Failure(DG_E_INVALID_ARG, "op operand refers to a later tensor");
+        dg::add_op(g->ir, o.name, o.kind, in, o.attrs ? o.attrs : "");
+      }
+      dg::set_output(g->ir, output_tensor, nullptr);
+      dg::finish(g->ir);
+      finalize(g);
+    } catch (...) {
+      delete g;
+      throw;
+    }
+    *out = g;
+    return DG_OK;
+  });
+}
+
+void dg_graph_destroy(dg_graph* g) {
+  if (!g) return;
+  int cur = 0;
+  bool have = hipGetDevice(&cur) == hipSuccess;
+  for (auto& kv : g->dev_blob) {
+    if (hipSetDevice(kv.first) == hipSuccess) (void)hipFree(kv.second);
+  }
+  if (have) (void)hipSetDevice(cur);
+  delete g;
+}
+
+dg_status dg_graph_info(const dg_graph* g, dg_graph_info_t* out) {
+  if (!g || !out) return set_error(DG_E_INVALID_ARG, "null argument");
+  std::memset(out, 0, sizeof(*out));
+  const dg::Tensor& o = g->ir.tensors[g->ir.output];
+  out->n_leaves = (int32_t)g->ir.leaves.size();
+  out->output_rank = (int32_t)o.shape.size();
+  for (size_t d = 0; d < o.shape.size(); ++d) out->output_shape[d] = o.shape[d];
+  out->output_numel = dg::numel(o.shape);
+  out->leaf_total = g->ir.leaf_total;
+  out->max_row_size = g->plan.max_row_size;
+  out->count_bound = g->plan.count_bound;
+  out->n_instructions = g->plan.header().ninstr;
+  out->lds_bytes = (int32_t)g->lds;
+  out->block_threads = g->block;
+  out->max_leaf_terms = g->plan.max_leaf_terms;
+  return DG_OK;
+}
+
+dg_status dg_graph_leaf(const dg_graph* g, int32_t i, dg_leaf_info_t* out) {
+  if (!g || !out) return set_error(DG_E_INVALID_ARG, "null argument");
+  if (i < 0 || i >= (int32_t)g->ir.leaves.size()) return set_error(DG_E_INVALID_ARG, "leaf index out of range");
+  std::memset(out, 0, sizeof(*out));
+  const dg::Tensor& t = g->ir.tensors[g->ir.leaves[i]];
+  std::snprintf(out->name, DG_NAME_LEN, "%s", t.name.c_str());
+  out->rank = (int32_t)t.shape.size();
+  for (size_t d = 0; d < t.shape.size(); ++d) out->shape[d] = t.shape[d];
+  out->base = t.base;
+  out->numel = dg::numel(t.shape);
+  return DG_OK;
+}
+
+dg_status dg_workspace_size(const dg_graph* g, int64_t n_locs, size_t* bytes) {
+  if (!g || !bytes || n_locs < 0) return set_error(DG_E_INVALID_ARG, "bad argument");
+  *bytes = ws_layout(n_locs).total;
+  return DG_OK;
+}
+
+dg_status dg_enumerate_sizes(const dg_graph* g, const int64_t* d_locs, int64_t n, int64_t* d_offsets, void* d_ws,
+                             int64_t* h_total, void* stream) {
+  if (!g || !d_offsets || !h_total || n < 0 || (n > 0 && !d_locs)) return set_error(DG_E_INVALID_ARG, "bad argument");
+  if (!d_ws) return set_error(DG_E_WORKSPACE, "workspace is required");
+  if (g->lds > (uint32_t)max_lds_per_block())
+    return set_error(DG_E_CAPACITY, "one location needs " + std::to_string(g->lds) + " bytes of LDS");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const uint8_t* blob = nullptr;
+  dg_status st = device_blob(g, &blob);
+  if (st != DG_OK) return st;
+  WsLayout w = ws_layout(n);
+  uint8_t* ws = static_cast<uint8_t*>(d_ws);
+  uint32_t* err = reinterpret_cast<uint32_t*>(ws + w.err);
+  DG_HIP(dgk::launch_zero(err, s), "zero");
+  DG_HIP(dgk::launch_sizes(blob, d_locs, n, d_offsets, err, g->block, g->lds, s), "sizes kernel");
+  DG_HIP(dgk::launch_scan(d_offsets, n, reinterpret_cast<int64_t*>(ws + w.sums), s), "scan");
+  int64_t total = 0;
+  uint32_t bits = 0;
+  DG_HIP(hipMemcpyAsync(&total, d_offsets + n, sizeof(int64_t), hipMemcpyDeviceToHost, s), "copy total");
+  DG_HIP(hipMemcpyAsync(&bits, err, sizeof(uint32_t), hipMemcpyDeviceToHost, s), "copy flags");
+  DG_HIP(hipStreamSynchronize(s), "sizes sync");
+  st = device_errors(bits);
+  if (st != DG_OK) return st;
+  *h_total = total;
+  return DG_OK;
+}
+
+dg_status dg_enumerate_fill(const dg_graph* g, const int64_t* d_locs, int64_t n, const int64_t* d_offsets,
+                            uint32_t* d_ids, uint32_t* d_counts, void* d_ws, void* stream) {
+  if (!g || n < 0 || (n > 0 && (!d_locs || !d_offsets || !d_ids || !d_counts)))
+    return set_error(DG_E_INVALID_ARG, "bad argument");
+  if (!d_ws) return set_error(DG_E_WORKSPACE, "workspace is required");
+  if (n == 0) return DG_OK;
+  if (g->lds > (uint32_t)max_lds_per_block())
+    return set_error(DG_E_CAPACITY, "one location needs " + std::to_string(g->lds) + " bytes of LDS");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const uint8_t* blob = nullptr;
+  dg_status st = device_blob(g, &blob);
+  if (st != DG_OK) return st;
+  uint32_t* err = reinterpret_cast<uint32_t*>(static_cast<uint8_t*>(d_ws) + ws_layout(n).err);
+  DG_HIP(dgk::launch_zero(err, s), "zero");
+  DG_HIP(dgk::launch_fill(blob, d_locs, n, d_offsets, d_ids, d_counts, err, g->block, g->lds, s), "fill kernel");
+  return DG_OK;
+}
+
+dg_status dg_compare(const dg_graph* a, const dg_graph* b, const int64_t* d_locs, int64_t n, uint8_t* d_status,
+                     int64_t* d_mismatch, int64_t* h_n_mismatch, void* d_ws, void* stream) {
+  if (!a || !b || !h_n_mismatch || n < 0 || (n > 0 && (!d_locs || !d_status || !d_mismatch)))
+    return set_error(DG_E_INVALID_ARG, "bad argument");
+  if (!d_ws) return set_error(DG_E_WORKSPACE, "workspace is required");
+  return guarded([&]() -> dg_status {
+    // MERGE's input/output matching: same leaves (names, shapes, order) and
+    // the same output shape.
+    const dg::GraphIR &A = a->ir, &B = b->ir;
+    if (A.leaves.size() != B.leaves.size()) return set_error(DG_E_SIGNATURE, "leaf count differs");
+    for (size_t i = 0; i < A.leaves.size(); ++i) {
+      const dg::Tensor &x = A.tensors[A.leaves[i]], &y = B.tensors[B.leaves[i]];
+      if (x.name != y.name || x.shape != y.shape)
+        return set_error(DG_E_SIGNATURE, "leaf " + std::to_string(i) + " ('" + x.name + "') differs");
+    }
+    if (A.tensors[A.output].shape != B.tensors[B.output].shape)
+      return set_error(DG_E_SIGNATURE, "output shape differs");
+    dgc::PairPlan pp;
+    dg::pair_plan(a->plan, b->plan, &pp);
+    if (pp.lds_bytes > (uint32_t)max_lds_per_block())
+      return set_error(DG_E_CAPACITY, "comparison needs " + std::to_string(pp.lds_bytes) + " bytes of LDS");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const uint8_t *ba = nullptr, *bb = nullptr;
+    dg_status st = device_blob(a, &ba);
+    if (st != DG_OK) return st;
+    st = device_blob(b, &bb);
+    if (st != DG_OK) return st;
+    WsLayout w = ws_layout(n);
+    uint8_t* ws = static_cast<uint8_t*>(d_ws);
+    uint32_t* err = reinterpret_cast<uint32_t*>(ws + w.err);
+    int64_t* flags = reinterpret_cast<int64_t*>(ws + w.flags);
+    DG_HIP(dgk::launch_zero(err, s), "zero");
+    int block = std::max(a->block, b->block);
+    DG_HIP(dgk::launch_compare(ba, bb, pp, d_locs, n, d_status, flags, err, block, s), "compare kernel");
+    DG_HIP(dgk::launch_scan(flags, n, reinterpret_cast<int64_t*>(ws + w.sums), s), "scan");
+    DG_HIP(dgk::launch_scatter_mismatch(d_status, flags, n, d_mismatch, s), "scatter");
+    int64_t total = 0;
+    uint32_t bits = 0;
+    DG_HIP(hipMemcpyAsync(&total, flags + n, sizeof(int64_t), hipMemcpyDeviceToHost, s), "copy count");
+    DG_HIP(hipMemcpyAsync(&bits, err, sizeof(uint32_t), hipMemcpyDeviceToHost, s), "copy flags");
+    DG_HIP(hipStreamSynchronize(s), "compare sync");
+    st = device_errors(bits);
+    if (st != DG_OK) return st;
+    *h_n_mismatch = total;
+    return DG_OK;
+  });
+}
+
+}  // extern "C"

@@ -1,0 +1,695 @@
+// Host compiler: graph IR -> per-location plan of separable terms.
+//
+// The back-projection res(y[l]) of Sec. 3.4 is evaluated symbolically once
+// for a generic location.  The path-count function of each reached tensor is
+// a sum of terms coef * prod_d f_d(i_d).  Substituting op k's per-element
+// equation into a term of T_k: for a read group (window box W, operands) and
+// an operand r, the count at r's index is
+//     sum over output coords o and window points w with r's index = i and
+//     every operand index valid, of coef * prod_a f_a(o_a).
+// The variables (o_a, w_b) split into components linked by the validity
+// predicates and by r's own index functions; each component carries at most
+// one dimension of r (else the dataflow is not separable and the graph is
+// rejected), so the sum factors into one vector per dimension of r times
+// scalar sums.  Terms that agree in all but one factor are merged, which
+// keeps the term count small (e.g. a softmax row plus its own element, or a
+// normalisation's statistics set plus its own element).
+#include "compile.h"
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <map>
+#include <numeric>
+#include <sstream>
+
+#include "../../include/dirigo_rocm.h"
+
+namespace dg {
+
+namespace {
+
+[[noreturn]] void fail(int code, const std::string& m) { throw Failure(code, m); }
+
+const int kMaxTensorTerms = 64;
+const int64_t kLincombFullDim = 4096;  // dims up to this size get full-extent merged factors
+const int64_t kMaxTableEntries = 8192;
+const int64_t kMaxTableWords = 24576;
+
+int64_t floor_div(int64_t a, int64_t b) {
+  int64_t q = a / b;
+  if ((a % b) != 0 && ((a < 0) != (b < 0))) --q;
+  return q;
+}
+int64_t ceil_div(int64_t a, int64_t b) { return -floor_div(-a, b); }
+
+struct Coef {
+  uint64_t k = 1;
+  std::vector<int> slots;  // scalar slots, multiplied
+};
+
+struct SymTerm {
+  Coef coef;
+  std::vector<int> f;  // factor slot per dim
+};
+
+struct UnionFind {
+  std::vector<int> p;
+  explicit UnionFind(int n) : p(n) { std::iota(p.begin(), p.end(), 0); }
+  int find(int x) { return p[x] == x ? x : p[x] = find(p[x]); }
+  void unite(int a, int b) { p[find(a)] = find(b); }
+};
+
+std::pair<int64_t, int64_t> fn_range(const IndexFn& f, const std::vector<int64_t>& vmin,
+                                     const std::vector<int64_t>& vmax) {
+  int64_t lo = f.c, hi = f.c;
+  for (const auto& t : f.terms) {
+    int64_t a = floor_div(vmin[t.var], t.vdiv), b = floor_div(vmax[t.var], t.vdiv);
+    if (t.coef >= 0) {
+      lo += t.coef * a;
+      hi += t.coef * b;
+    } else {
+      lo += t.coef * b;
+      hi += t.coef * a;
+    }
+  }
+  if (f.mode == 1) return {ceil_div(lo, f.s), floor_div(hi, f.s)};
+  if (f.mode == 2) return {floor_div(lo, f.s), floor_div(hi, f.s)};
+  return {lo, hi};
+}
+
+// Largest magnitude of any partial sum while evaluating f (int32 safety).
+int64_t fn_magnitude(const IndexFn& f, const std::vector<int64_t>& vmin, const std::vector<int64_t>& vmax) {
+  int64_t m = std::llabs(f.c);
+  for (const auto& t : f.terms) {
+    int64_t v = std::max(std::llabs(vmin[t.var]), std::llabs(vmax[t.var]));
+    m += std::llabs(t.coef) * (v / t.vdiv + 1);
+  }
+  return m;
+}
+
+bool fn_uses(const IndexFn& f, int v) {
+  for (const auto& t : f.terms)
+    if (t.var == v) return true;
+  return false;
+}
+
+double sat(double x) { return std::isfinite(x) ? x : 1e300; }
+
+class Compiler {
+ public:
+  explicit Compiler(const GraphIR& g) : g_(g) {}
+  Plan run();
+
+ private:
+  const GraphIR& g_;
+  std::vector<DgpInstr> ins_;
+  std::vector<DgpFactor> fac_;
+  std::vector<double> fbound_;
+  std::vector<double> sbound_;
+  std::map<std::string, int> memo_;
+  std::vector<std::vector<SymTerm>> terms_;
+
+  int new_factor(int64_t cap, int64_t size, double bound) {
+    DgpFactor f{};
+    f.cap = (int32_t)std::max<int64_t>(1, cap);
+    f.size = (int32_t)size;
+    fac_.push_back(f);
+    fbound_.push_back(sat(bound));
+    return (int)fac_.size() - 1;
+  }
+  int new_scalar(double bound) {
+    sbound_.push_back(sat(bound));
+    return (int)sbound_.size() - 1;
+  }
+  DgpInstr blank(int opcode) {
+    DgpInstr i;
+    std::memset(&i, 0, sizeof(i));
+    i.opcode = opcode;
+    i.f1 = i.f2 = i.k1 = i.k2 = -1;
+    return i;
+  }
+
+  int root_factor(int a) {
+    std::string key = "ROOT " + std::to_string(a);
+    auto it = memo_.find(key);
+    if (it != memo_.end()) return it->second;
+    int f = new_factor(1, g_.tensors[g_.output].shape[a], 1.0);
+    DgpInstr i = blank(DGP_ROOT);
+    i.dst = f;
+    i.a = a;
+    ins_.push_back(i);
+    return memo_[key] = f;
+  }
+
+  int const_factor(int64_t v, int64_t size) {
+    std::string key = "CONST " + std::to_string(v) + " " + std::to_string(size);
+    auto it = memo_.find(key);
+    if (it != memo_.end()) return it->second;
+    int f = new_factor(1, size, 1.0);
+    DgpInstr i = blank(DGP_CONST);
+    i.dst = f;
+    i.a = (int32_t)v;
+    ins_.push_back(i);
+    return memo_[key] = f;
+  }
+
+  double coef_bound(const Coef& c) {
+    double b = (double)c.k;
+    for (int s : c.slots) b *= sbound_[s];
+    return sat(b);
+  }
+
+  // Materialises the product of a coefficient's scalar slots: (slot or -1, constant).
+  std::pair<int, uint64_t> coef_slot(const Coef& c) {
+    if (c.slots.empty()) return {-1, c.k};
+    if (c.slots.size() == 1) return {c.slots[0], c.k};
+    std::vector<int> s = c.slots;
+    std::sort(s.begin(), s.end());
+    std::ostringstream key;
+    key << "SMUL";
+    for (int x : s) key << " " << x;
+    auto it = memo_.find(key.str());
+    int slot;
+    if (it != memo_.end()) {
+      slot = it->second;
+    } else {
+      if (s.size() > 8) fail(DG_E_UNSUPPORTED_OP, "coefficient with more than 8 scalar factors");
+      double b = 1;
+      for (int x : s) b *= sbound_[x];
+      slot = new_scalar(b);
+      DgpInstr i = blank(DGP_SMUL);
+      i.dst = slot;
+      i.dst_is_scalar = 1;
+      i.ns = (int32_t)s.size();
+      for (size_t q = 0; q < s.size(); ++q) i.s[q] = s[q];
+      i.cst = 1;
+      ins_.push_back(i);
+      memo_[key.str()] = slot;
+    }
+    return {slot, c.k};
+  }
+
+  Coef coef_add(const Coef& a, const Coef& b) {
+    if (a.slots.empty() && b.slots.empty()) {
+      uint64_t k;
+      if (!__builtin_add_overflow(a.k, b.k, &k)) return Coef{k, {}};
+    }
+    auto sa = coef_slot(a), sb = coef_slot(b);
+    std::ostringstream key;
+    key << "SADD " << sa.first << " " << sa.second << " " << sb.first << " " << sb.second;
+    auto it = memo_.find(key.str());
+    int slot;
+    if (it != memo_.end()) {
+      slot = it->second;
+    } else {
+      slot = new_scalar(coef_bound(a) + coef_bound(b));
+      DgpInstr i = blank(DGP_SADD);
+      i.dst = slot;
+      i.dst_is_scalar = 1;
+      i.f1 = sa.first;
+      i.c1 = sa.second;
+      i.f2 = sb.first;
+      i.c2 = sb.second;
+      ins_.push_back(i);
+      memo_[key.str()] = slot;
+    }
+    return Coef{1, {slot}};
+  }
+
+  int lincomb(int f1, const Coef& c1, int f2, const Coef& c2, int64_t size) {
+    auto s1 = coef_slot(c1), s2 = coef_slot(c2);
+    std::ostringstream key;
+    key << "LIN " << f1 << " " << s1.first << " " << s1.second << " " << f2 << " " << s2.first << " " << s2.second
+        << " " << size;
+    auto it = memo_.find(key.str());
+    if (it != memo_.end()) return it->second;
+    int64_t cap = size <= kLincombFullDim ? size : std::min<int64_t>(size, (int64_t)fac_[f1].cap + fac_[f2].cap);
+    int f = new_factor(cap, size, fbound_[f1] * coef_bound(c1) + fbound_[f2] * coef_bound(c2));
+    DgpInstr i = blank(DGP_LINCOMB);
+    i.dst = f;
+    i.f1 = f1;
+    i.k1 = s1.first;
+    i.c1 = s1.second;
+    i.f2 = f2;
+    i.k2 = s2.first;
+    i.c2 = s2.second;
+    ins_.push_back(i);
+    return memo_[key.str()] = f;
+  }
+
+  // Merges terms equal in all factors (coefficients add) or in all but one
+  // (that factor becomes a linear combination).  `shape` is the tensor's.
+  void merge_terms(std::vector<SymTerm>& ts, const Dims& shape) {
+    bool again = true;
+    while (again) {
+      again = false;
+      for (size_t i = 0; i < ts.size() && !again; ++i) {
+        for (size_t j = i + 1; j < ts.size() && !again; ++j) {
+          int ndiff = 0, dim = -1;
+          for (size_t d = 0; d < ts[i].f.size(); ++d)
+            if (ts[i].f[d] != ts[j].f[d]) {
+              ++ndiff;
+              dim = (int)d;
+            }
+          if (ndiff == 0) {
+            ts[i].coef = coef_add(ts[i].coef, ts[j].coef);
+          } else if (ndiff == 1) {
+            ts[i].f[dim] = lincomb(ts[i].f[dim], ts[i].coef, ts[j].f[dim], ts[j].coef, shape[dim]);
+            ts[i].coef = Coef{1, {}};
+          } else {
+            continue;
+          }
+          ts.erase(ts.begin() + j);
+          again = true;
+        }
+      }
+    }
+  }
+
+  DgpIFn to_dev(const IndexFn& f, const std::vector<int>& local, int64_t size) {
+    DgpIFn d;
+    std::memset(&d, 0, sizeof(d));
+    if (f.terms.size() > DGP_MAX_FTERMS) fail(DG_E_UNSUPPORTED_OP, "index function with more than 4 terms");
+    d.nterm = (int32_t)f.terms.size();
+    for (size_t q = 0; q < f.terms.size(); ++q) {
+      d.var[q] = local[f.terms[q].var];
+      d.coef[q] = (int32_t)f.terms[q].coef;
+      d.vdiv[q] = (int32_t)f.terms[q].vdiv;
+    }
+    d.c = (int32_t)f.c;
+    d.mode = f.mode;
+    d.s = (int32_t)f.s;
+    d.size = (int32_t)size;
+    return d;
+  }
+
+  static void key_fn(std::ostringstream& k, const IndexFn& f, const std::vector<int>& local, int64_t size) {
+    k << "[" << f.c << "," << f.mode << "," << f.s << "," << size;
+    for (const auto& t : f.terms) k << ";" << local[t.var] << "," << t.coef << "," << t.vdiv;
+    k << "]";
+  }
+
+  // Sum over one component.  Returns a factor slot (target != nullptr) or a
+  // scalar slot; a component of window variables without predicates and
+  // without a target folds into `folded` and returns -1.
+  int component(const SymTerm& t, const std::vector<int>& vars, const std::vector<const IndexFn*>& preds,
+                const std::vector<int64_t>& psize, const IndexFn* target, int64_t tsize, int R,
+                const ReadGroup& G, uint64_t* folded) {
+    // Identity transfer: the target index is exactly one output coordinate.
+    if (target && preds.empty() && vars.size() == 1 && vars[0] < R && target->terms.size() == 1 &&
+        target->terms[0].coef == 1 && target->terms[0].vdiv == 1 && target->c == 0 && target->mode == 0)
+      return t.f[vars[0]];
+    bool window_only = true;
+    for (int v : vars)
+      if (v < R) window_only = false;
+    if (!target && window_only && preds.empty()) {
+      uint64_t n = 1;
+      for (int v : vars) n *= (uint64_t)(G.whi[v - R] - G.wlo[v - R]);
+      *folded = n;
+      return -1;
+    }
+    if (vars.size() > DGP_MAX_VARS) fail(DG_E_UNSUPPORTED_OP, "component with more than 8 variables");
+    if (preds.size() > DGP_MAX_PREDS) fail(DG_E_UNSUPPORTED_OP, "component with more than 12 predicates");
+    int nv_total = R + (int)G.wlo.size();
+    std::vector<int> local(nv_total, -1);
+    for (size_t q = 0; q < vars.size(); ++q) local[vars[q]] = (int)q;
+    std::ostringstream key;
+    key << "COMP";
+    double points = 1, weight = 1;
+    std::vector<int64_t> width(vars.size());
+    for (size_t q = 0; q < vars.size(); ++q) {
+      int v = vars[q];
+      if (v < R) {
+        key << " o" << t.f[v];
+        width[q] = fac_[t.f[v]].cap;
+        weight *= fbound_[t.f[v]];
+      } else {
+        key << " w" << G.wlo[v - R] << ":" << G.whi[v - R];
+        width[q] = G.whi[v - R] - G.wlo[v - R];
+      }
+      points *= (double)width[q];
+    }
+    if (points > 2147483647.0) fail(DG_E_UNSUPPORTED_OP, "component sum over more than 2^31 points");
+    key << " P";
+    for (size_t p = 0; p < preds.size(); ++p) key_fn(key, *preds[p], local, psize[p]);
+    if (target) {
+      key << " T";
+      key_fn(key, *target, local, tsize);
+    } else {
+      key << " S";
+    }
+    auto it = memo_.find(key.str());
+    if (it != memo_.end()) return it->second;
+
+    DgpInstr i = blank(DGP_COMP);
+    i.nvar = (int32_t)vars.size();
+    for (size_t q = 0; q < vars.size(); ++q) {
+      int v = vars[q];
+      if (v < R) {
+        i.var_src[q] = t.f[v];
+      } else {
+        i.var_src[q] = -1;
+        i.wlo[q] = (int32_t)G.wlo[v - R];
+        i.whi[q] = (int32_t)G.whi[v - R];
+      }
+    }
+    i.npred = (int32_t)preds.size();
+    for (size_t p = 0; p < preds.size(); ++p) i.pred[p] = to_dev(*preds[p], local, psize[p]);
+    int slot;
+    if (target) {
+      // Capacity: how many integer values the target can take over the
+      // variables' ranges (widths from the static factor capacities).
+      int64_t span = 0;
+      for (const auto& tm : target->terms) {
+        int64_t w = width[local[tm.var]];
+        span += std::llabs(tm.coef) * ceil_div(w - 1, tm.vdiv);
+      }
+      int64_t count = (target->mode ? ceil_div(span, target->s) : span) + 1;
+      slot = new_factor(std::min(count, tsize), tsize, points * weight);
+      i.target = to_dev(*target, local, tsize);
+      i.dst_is_scalar = 0;
+    } else {
+      slot = new_scalar(points * weight);
+      i.dst_is_scalar = 1;
+    }
+    i.dst = slot;
+    ins_.push_back(i);
+    return memo_[key.str()] = slot;
+  }
+
+  void propagate(const SymTerm& t, const OpNode& op, const ReadGroup& G) {
+    const Dims& oshape = g_.tensors[op.out].shape;
+    int R = (int)oshape.size(), Q = (int)G.wlo.size(), NV = R + Q;
+    std::vector<int64_t> vmin(NV), vmax(NV);
+    for (int a = 0; a < R; ++a) {
+      vmin[a] = 0;
+      vmax[a] = oshape[a] - 1;
+    }
+    for (int b = 0; b < Q; ++b) {
+      if (G.whi[b] <= G.wlo[b]) return;  // empty window: reads nothing
+      vmin[R + b] = G.wlo[b];
+      vmax[R + b] = G.whi[b] - 1;
+    }
+    // Validity predicates of the whole group (joint over the operands).
+    std::vector<const IndexFn*> preds;
+    std::vector<int64_t> psize;
+    for (const Operand& r : G.ops) {
+      const Dims& s = g_.tensors[r.tensor].shape;
+      for (size_t d = 0; d < s.size(); ++d) {
+        const IndexFn& f = r.idx[d];
+        if (fn_magnitude(f, vmin, vmax) >= (int64_t(1) << 30))
+          fail(DG_E_UNSUPPORTED_OP, op.kind + ": index arithmetic exceeds 32 bits");
+        if (f.terms.empty()) {
+          int64_t v = f.c;
+          if (f.mode == 1 && floor_div(v, f.s) * f.s != v) return;
+          if (f.mode) v = floor_div(v, f.s);
+          if (v < 0 || v >= s[d]) return;  // constant index out of range: nothing is read
+          continue;
+        }
+        auto rg = fn_range(f, vmin, vmax);
+        bool trivial = (f.mode != 1 || f.s == 1) && rg.first >= 0 && rg.second <= s[d] - 1;
+        if (!trivial) {
+          preds.push_back(&f);
+          psize.push_back(s[d]);
+        }
+      }
+    }
+    for (const Operand& r : G.ops) {
+      const Dims& s = g_.tensors[r.tensor].shape;
+      UnionFind uf(NV);
+      for (const IndexFn* p : preds)
+        for (size_t q = 1; q < p->terms.size(); ++q) uf.unite(p->terms[0].var, p->terms[q].var);
+      for (const IndexFn& f : r.idx)
+        for (size_t q = 1; q < f.terms.size(); ++q) uf.unite(f.terms[0].var, f.terms[q].var);
+      // Group variables by component.
+      std::map<int, std::vector<int>> comp_vars;
+      for (int v = 0; v < NV; ++v) comp_vars[uf.find(v)].push_back(v);
+      std::map<int, int> comp_dim;  // component root -> dim of r
+      SymTerm out;
+      out.coef = t.coef;
+      out.f.assign(s.size(), -1);
+      uint64_t kmul = r.mult;
+      for (size_t d = 0; d < s.size(); ++d) {
+        const IndexFn& f = r.idx[d];
+        if (f.terms.empty()) {
+          int64_t v = f.mode ? floor_div(f.c, f.s) : f.c;
+          out.f[d] = const_factor(v, s[d]);
+          continue;
+        }
+        int root = uf.find(f.terms[0].var);
+        if (comp_dim.count(root))
+          fail(DG_E_UNSUPPORTED_OP, op.kind + ": dims " + std::to_string(comp_dim[root]) + " and " +
+                                        std::to_string(d) + " of an operand depend on one coupled set of "
+                                        "variables (dataflow not separable)");
+        comp_dim[root] = (int)d;
+      }
+      for (auto& cv : comp_vars) {
+        int root = cv.first;
+        std::vector<const IndexFn*> cp;
+        std::vector<int64_t> cs;
+        for (size_t p = 0; p < preds.size(); ++p)
+          if (uf.find(preds[p]->terms[0].var) == root) {
+            cp.push_back(preds[p]);
+            cs.push_back(psize[p]);
+          }
+        uint64_t folded = 1;
+        auto dit = comp_dim.find(root);
+        if (dit != comp_dim.end()) {
+          int d = dit->second;
+          out.f[d] = component(t, cv.second, cp, cs, &r.idx[d], s[d], R, G, &folded);
+        } else {
+          int slot = component(t, cv.second, cp, cs, nullptr, 0, R, G, &folded);
+          if (slot >= 0) out.coef.slots.push_back(slot);
+          else if (__builtin_mul_overflow(kmul, folded, &kmul))
+            fail(DG_E_OVERFLOW, "static path-count bound exceeds 64 bits");
+        }
+      }
+      if (__builtin_mul_overflow(out.coef.k, kmul, &out.coef.k))
+        fail(DG_E_OVERFLOW, "static path-count bound exceeds 64 bits");
+      terms_[r.tensor].push_back(out);
+    }
+  }
+};
+
+Plan Compiler::run() {
+  const GraphIR& g = g_;
+  terms_.assign(g.tensors.size(), {});
+  const Dims& oshape = g.tensors[g.output].shape;
+  SymTerm root;
+  for (size_t a = 0; a < oshape.size(); ++a) root.f.push_back(root_factor((int)a));
+  terms_[g.output].push_back(root);
+  for (int k = (int)g.ops.size() - 1; k >= 0; --k) {
+    const OpNode& op = g.ops[k];
+    std::vector<SymTerm> ts;
+    ts.swap(terms_[op.out]);
+    if (ts.empty()) continue;
+    merge_terms(ts, g.tensors[op.out].shape);
+    if ((int)ts.size() > kMaxTensorTerms)
+      fail(DG_E_UNSUPPORTED_OP, "tensor '" + g.tensors[op.out].name + "' needs more than 64 separable terms");
+    for (const SymTerm& t : ts)
+      for (const ReadGroup& G : op.groups) propagate(t, op, G);
+  }
+
+  std::vector<DgpLeaf> leaves;
+  std::vector<DgpTerm> dterms;
+  Plan plan;
+  int64_t max_row = 0, emit_entries = 0, union_entries = 0;
+  double cbound = 0;
+  for (int li = 0; li < (int)g.leaves.size(); ++li) {
+    const Tensor& T = g.tensors[g.leaves[li]];
+    std::vector<SymTerm>& ts = terms_[g.leaves[li]];
+    merge_terms(ts, T.shape);
+    if ((int)ts.size() > DGP_MAX_LEAF_TERMS)
+      fail(DG_E_UNSUPPORTED_OP, "leaf '" + T.name + "' needs more than 32 separable terms");
+    DgpLeaf L;
+    std::memset(&L, 0, sizeof(L));
+    L.rank = (int32_t)T.shape.size();
+    L.nterm = (int32_t)ts.size();
+    L.term0 = (int32_t)dterms.size();
+    L.base = (uint32_t)T.base;
+    uint64_t stride = 1;
+    for (int d = L.rank - 1; d >= 0; --d) {
+      L.shape[d] = (int32_t)T.shape[d];
+      L.stride[d] = (uint32_t)stride;
+      stride *= (uint64_t)T.shape[d];
+    }
+    double lb = 0;
+    for (const SymTerm& t : ts) {
+      DgpTerm dt;
+      std::memset(&dt, 0, sizeof(dt));
+      auto cs = coef_slot(t.coef);
+      dt.coef_slot = cs.first;
+      dt.coef_const = cs.second;
+      double b = coef_bound(t.coef);
+      for (int d = 0; d < L.rank; ++d) {
+        dt.factor[d] = t.f[d];
+        b *= fbound_[t.f[d]];
+      }
+      lb += b;
+      dterms.push_back(dt);
+    }
+    cbound = std::max(cbound, lb);
+    int64_t ucount = 0, cells = ts.empty() ? 0 : 1;
+    for (int d = 0; d < L.rank; ++d) {
+      int64_t u = 0;
+      for (const SymTerm& t : ts) u += fac_[t.f[d]].cap;
+      u = std::min<int64_t>(u, T.shape[d]);
+      L.ucap[d] = (int32_t)std::max<int64_t>(u, 1);
+      ucount += L.ucap[d];
+      cells *= L.ucap[d];
+    }
+    max_row += cells;
+    // Emission tables: dims [0, split) outer, [split, rank) inner.
+    int best = -1;
+    int64_t best_entries = 0;
+    for (int s = 0; s <= L.rank; ++s) {
+      int64_t o = 1, in = 1;
+      for (int d = 0; d < s; ++d) o *= L.ucap[d];
+      for (int d = s; d < L.rank; ++d) in *= L.ucap[d];
+      if (o > kMaxTableEntries || in > kMaxTableEntries) continue;
+      if (best < 0 || o + in < best_entries) {
+        best = s;
+        best_entries = o + in;
+        L.outer_cap = (int32_t)o;
+        L.inner_cap = (int32_t)in;
+      }
+    }
+    int64_t words = best_entries * (1 + std::max<int64_t>(1, ts.size()));
+    if (best < 0 || words > kMaxTableWords) {
+      L.split = -1;  // per-cell decomposition, no tables
+      L.outer_cap = L.inner_cap = 0;
+      words = 0;
+    } else {
+      L.split = best;
+    }
+    emit_entries = std::max(emit_entries, words);
+    union_entries = std::max(union_entries, ucount);
+    leaves.push_back(L);
+    plan.max_leaf_terms = std::max(plan.max_leaf_terms, (int)ts.size());
+  }
+  if (cbound > 9.2e18) fail(DG_E_OVERFLOW, "static path-count bound exceeds 2^63");
+  for (double b : fbound_)
+    if (b > 9.2e18) fail(DG_E_OVERFLOW, "static path-count bound exceeds 2^63");
+  for (double b : sbound_)
+    if (b > 9.2e18) fail(DG_E_OVERFLOW, "static path-count bound exceeds 2^63");
+
+  // Factor value offsets.
+  int64_t fval = 0;
+  for (auto& f : fac_) {
+    f.off = (int32_t)fval;
+    fval += f.cap;
+  }
+  DgpHeader h;
+  std::memset(&h, 0, sizeof(h));
+  h.magic = DGP_MAGIC;
+  h.out_rank = (int32_t)oshape.size();
+  h.out_numel = numel(oshape);
+  int64_t st = 1;
+  for (int d = h.out_rank - 1; d >= 0; --d) {
+    h.out_shape[d] = oshape[d];
+    h.out_stride[d] = st;
+    st *= oshape[d];
+  }
+  h.ninstr = (int32_t)ins_.size();
+  h.nfactor = (int32_t)fac_.size();
+  h.nscalar = (int32_t)sbound_.size();
+  h.nleaf = (int32_t)leaves.size();
+  h.nterm = (int32_t)dterms.size();
+  h.fval_entries = (int32_t)fval;
+  h.max_leaf_terms = plan.max_leaf_terms;
+  h.emit_entries = (int32_t)emit_entries;
+  h.union_entries = (int32_t)union_entries;
+  size_t off = (sizeof(DgpHeader) + 15) & ~size_t(15);
+  h.instr_off = (int32_t)off;
+  off += ins_.size() * sizeof(DgpInstr);
+  off = (off + 15) & ~size_t(15);
+  h.factor_off = (int32_t)off;
+  off += fac_.size() * sizeof(DgpFactor);
+  off = (off + 15) & ~size_t(15);
+  h.leaf_off = (int32_t)off;
+  off += leaves.size() * sizeof(DgpLeaf);
+  off = (off + 15) & ~size_t(15);
+  h.term_off = (int32_t)off;
+  off += dterms.size() * sizeof(DgpTerm);
+  h.blob_bytes = (int32_t)off;
+  plan.blob.assign(off, 0);
+  std::memcpy(plan.blob.data(), &h, sizeof(h));
+  if (!ins_.empty()) std::memcpy(plan.blob.data() + h.instr_off, ins_.data(), ins_.size() * sizeof(DgpInstr));
+  if (!fac_.empty()) std::memcpy(plan.blob.data() + h.factor_off, fac_.data(), fac_.size() * sizeof(DgpFactor));
+  if (!leaves.empty()) std::memcpy(plan.blob.data() + h.leaf_off, leaves.data(), leaves.size() * sizeof(DgpLeaf));
+  if (!dterms.empty()) std::memcpy(plan.blob.data() + h.term_off, dterms.data(), dterms.size() * sizeof(DgpTerm));
+  plan.max_row_size = max_row;
+  plan.count_bound = cbound;
+  return plan;
+}
+
+}  // namespace
+
+Plan compile_plan(const GraphIR& g) { return Compiler(g).run(); }
+
+uint32_t plan_lds_bytes(const Plan& p) {
+  const DgpHeader& h = p.header();
+  dgc::PlanLayout PL = dgc::plan_layout(&h, 0);
+  dgc::EmitLayout E = dgc::emit_layout(PL.end, h.max_leaf_terms, h.union_entries, h.emit_entries);
+  return (E.end + 15u) & ~15u;
+}
+
+void pair_plan(const Plan& a, const Plan& b, dgc::PairPlan* pp) {
+  const DgpHeader& ha = a.header();
+  const DgpHeader& hb = b.header();
+  if (ha.nleaf != hb.nleaf) fail(DG_E_SIGNATURE, "leaf count differs");
+  if (ha.nleaf > 16) fail(DG_E_UNSUPPORTED_OP, "compare supports at most 16 leaves");
+  std::memset(pp, 0, sizeof(*pp));
+  pp->nleaf = ha.nleaf;
+  const DgpLeaf* la = reinterpret_cast<const DgpLeaf*>(a.blob.data() + ha.leaf_off);
+  const DgpLeaf* lb = reinterpret_cast<const DgpLeaf*>(b.blob.data() + hb.leaf_off);
+  int64_t emit = 0, uni = 0;
+  for (int l = 0; l < ha.nleaf; ++l) {
+    const DgpLeaf &x = la[l], &y = lb[l];
+    int T = x.nterm + y.nterm;
+    pp->max_terms = std::max(pp->max_terms, T);
+    dgc::LeafShape& S = pp->leaf[l];
+    int64_t ucount = 0;
+    for (int d = 0; d < DGP_MAX_RANK; ++d) {
+      if (d < x.rank) {
+        int64_t u = (x.nterm > 0 ? (int64_t)x.ucap[d] : 0) + (y.nterm > 0 ? (int64_t)y.ucap[d] : 0);
+        u = std::min<int64_t>(u, x.shape[d]);
+        S.ucap[d] = (int32_t)std::max<int64_t>(u, 1);
+        ucount += S.ucap[d];
+      } else {
+        S.ucap[d] = 1;
+      }
+    }
+    int best = -1;
+    int64_t best_e = 0;
+    for (int s = 0; s <= x.rank; ++s) {
+      int64_t o = 1, in = 1;
+      for (int d = 0; d < s; ++d) o *= S.ucap[d];
+      for (int d = s; d < x.rank; ++d) in *= S.ucap[d];
+      if (o > kMaxTableEntries || in > kMaxTableEntries) continue;
+      if (best < 0 || o + in < best_e) {
+        best = s;
+        best_e = o + in;
+      }
+    }
+    int64_t words = best_e * (1 + std::max(T, 1));
+    if (best < 0 || words > kMaxTableWords) {
+      S.split = -1;
+      words = 0;
+    } else {
+      S.split = best;
+    }
+    emit = std::max(emit, words);
+    uni = std::max(uni, ucount);
+  }
+  pp->union_entries = (int32_t)uni;
+  pp->emit_entries = (int32_t)emit;
+  dgc::PlanLayout PA = dgc::plan_layout(&ha, 0);
+  pp->plan_b = dgc::align8(PA.end);
+  dgc::PlanLayout PB = dgc::plan_layout(&hb, pp->plan_b);
+  dgc::EmitLayout E = dgc::emit_layout(PB.end, pp->max_terms, pp->union_entries, pp->emit_entries);
+  pp->lds_bytes = (E.end + 15u) & ~15u;
+}
+
+}  // namespace dg

@@ -1,0 +1,34 @@
+// Host compiler: graph IR -> per-location plan (program.h).
+#pragma once
+#include <cstdint>
+#include <vector>
+
+#include "core.h"
+#include "graph.h"
+#include "program.h"
+
+namespace dg {
+
+struct Plan {
+  std::vector<uint8_t> blob;  // DgpHeader followed by the instruction, factor, leaf and term arrays
+  int64_t max_row_size = 0;   // static bound on entries per row
+  double count_bound = 0;     // static bound on one path count
+  int max_leaf_terms = 0;
+
+  const DgpHeader& header() const { return *reinterpret_cast<const DgpHeader*>(blob.data()); }
+};
+
+// Compiles the back-projection of one (symbolic) output location.  Throws
+// Failure(DG_E_UNSUPPORTED_OP) for graphs whose dataflow is not separable
+// (an operand with two dims fed by one coupled set of variables) and
+// Failure(DG_E_OVERFLOW) if the static path-count bound exceeds 2^63.
+Plan compile_plan(const GraphIR& g);
+
+// Local data share bytes one location of this plan needs.
+uint32_t plan_lds_bytes(const Plan& p);
+
+// Combined per-leaf emission shapes and LDS layout for comparing two plans
+// location by location (same leaves in the same order).
+void pair_plan(const Plan& a, const Plan& b, dgc::PairPlan* out);
+
+}  // namespace dg

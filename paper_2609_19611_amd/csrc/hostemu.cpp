@@ -1,0 +1,123 @@
+// Host emulation of the device kernels, for CPU tests only.
+//
+// Runs the same per-location plan (compile.cpp) and the same block code
+// (core.h) with a block of one thread on the host, so the compiler and the
+// kernel logic can be checked against the oracle without a GPU.  The
+// library's entry points never call this; it is built as a separate test
+// library.
+#include <cstdint>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/dirigo_rocm.h"
+#include "compile.h"
+#include "core.h"
+#include "graph.h"
+
+namespace {
+
+struct HostCtx {
+  int tid() const { return 0; }
+  int nthreads() const { return 1; }
+  void sync() const {}
+  void atomic_add(uint64_t* p, uint64_t v) const { *p += v; }
+  void atomic_max(uint64_t* p, uint64_t v) const {
+    if (v > *p) *p = v;
+  }
+  void store(uint32_t* p, uint32_t v) const { *p = v; }
+  uint32_t prefix(bool f, uint32_t* total) const {
+    *total = f ? 1u : 0u;
+    return 0u;
+  }
+  bool any(bool f) const { return f; }
+};
+
+thread_local std::string g_err;
+
+int fail_with(const dg::Failure& e) {
+  g_err = e.what();
+  return e.code;
+}
+
+int bits_status(uint32_t bits) {
+  if (bits & DGP_ERR_RANGE) { g_err = "location out of range"; return DG_E_RANGE; }
+  if (bits & DGP_ERR_OVERFLOW) { g_err = "path count overflow"; return DG_E_OVERFLOW; }
+  if (bits & DGP_ERR_CAPACITY) { g_err = "capacity exceeded"; return DG_E_CAPACITY; }
+  if (bits & DGP_ERR_SIZE) { g_err = "row size mismatch"; return DG_E_INVALID_ARG; }
+  return 0;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* dgh_error(void) { return g_err.c_str(); }
+
+// Row sizes into offsets[0..n] (running totals).
+int dgh_sizes(const char* text, int64_t len, const int64_t* locs, int64_t n, int64_t* offsets) {
+  try {
+    dg::GraphIR ir = dg::parse_dgir(std::string(text, (size_t)len));
+    dg::Plan plan = dg::compile_plan(ir);
+    std::vector<uint64_t> area((dg::plan_lds_bytes(plan) + 7) / 8 + 1);
+    HostCtx c;
+    uint32_t err = 0;
+    offsets[0] = 0;
+    for (int64_t i = 0; i < n; ++i) {
+      std::memset(area.data(), 0xA5, area.size() * 8);  // no reliance on zeroed LDS
+      uint64_t r = dgc::location_row<HostCtx, dgc::EMIT_COUNT>(c, plan.blob.data(), locs[i],
+                                                               reinterpret_cast<uint8_t*>(area.data()), nullptr,
+                                                               nullptr, 0, &err);
+      offsets[i + 1] = offsets[i] + (int64_t)r;
+    }
+    return bits_status(err);
+  } catch (const dg::Failure& e) {
+    return fail_with(e);
+  }
+}
+
+int dgh_fill(const char* text, int64_t len, const int64_t* locs, int64_t n, const int64_t* offsets, uint32_t* ids,
+             uint32_t* cnt) {
+  try {
+    dg::GraphIR ir = dg::parse_dgir(std::string(text, (size_t)len));
+    dg::Plan plan = dg::compile_plan(ir);
+    std::vector<uint64_t> area((dg::plan_lds_bytes(plan) + 7) / 8 + 1);
+    HostCtx c;
+    uint32_t err = 0;
+    for (int64_t i = 0; i < n; ++i) {
+      std::memset(area.data(), 0x5A, area.size() * 8);
+      uint64_t r = dgc::location_row<HostCtx, dgc::EMIT_FILL>(c, plan.blob.data(), locs[i],
+                                                              reinterpret_cast<uint8_t*>(area.data()),
+                                                              ids + offsets[i], cnt + offsets[i],
+                                                              (uint64_t)(offsets[i + 1] - offsets[i]), &err);
+      if ((int64_t)r != offsets[i + 1] - offsets[i]) err |= DGP_ERR_SIZE;
+    }
+    return bits_status(err);
+  } catch (const dg::Failure& e) {
+    return fail_with(e);
+  }
+}
+
+int dgh_compare(const char* ta, int64_t la, const char* tb, int64_t lb, const int64_t* locs, int64_t n,
+                uint8_t* status) {
+  try {
+    dg::GraphIR ia = dg::parse_dgir(std::string(ta, (size_t)la));
+    dg::GraphIR ib = dg::parse_dgir(std::string(tb, (size_t)lb));
+    dg::Plan pa = dg::compile_plan(ia), pb = dg::compile_plan(ib);
+    dgc::PairPlan pp;
+    dg::pair_plan(pa, pb, &pp);
+    std::vector<uint64_t> area(pp.lds_bytes / 8 + 1);
+    HostCtx c;
+    uint32_t err = 0;
+    for (int64_t i = 0; i < n; ++i) {
+      std::memset(area.data(), 0x33, area.size() * 8);
+      status[i] = (uint8_t)dgc::location_compare(c, pa.blob.data(), pb.blob.data(), pp, locs[i],
+                                                 reinterpret_cast<uint8_t*>(area.data()), &err);
+    }
+    return bits_status(err);
+  } catch (const dg::Failure& e) {
+    return fail_with(e);
+  }
+}
+
+}  // extern "C"

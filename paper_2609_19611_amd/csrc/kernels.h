@@ -1,0 +1,24 @@
+// Launchers of the HIP kernels (kernels.hip), called by the C ABI.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "core.h"
+
+namespace dgk {
+
+hipError_t launch_sizes(const uint8_t* blob, const int64_t* locs, int64_t n, int64_t* offsets, uint32_t* err,
+                        int block, uint32_t lds, hipStream_t s);
+hipError_t launch_fill(const uint8_t* blob, const int64_t* locs, int64_t n, const int64_t* offsets, uint32_t* ids,
+                       uint32_t* cnt, uint32_t* err, int block, uint32_t lds, hipStream_t s);
+hipError_t launch_compare(const uint8_t* blob_a, const uint8_t* blob_b, const dgc::PairPlan& pp, const int64_t* locs,
+                          int64_t n, uint8_t* status, int64_t* flags, uint32_t* err, int block, hipStream_t s);
+// In-place scan: v[1..n] holds sizes on entry, running totals on exit, v[0] = 0.
+hipError_t launch_scan(int64_t* v, int64_t n, int64_t* sums, hipStream_t s);
+int64_t scan_temp_entries(int64_t n);
+// Clears one error word (a kernel, so it may be recorded in a captured graph).
+hipError_t launch_zero(uint32_t* p, hipStream_t s);
+hipError_t launch_scatter_mismatch(const uint8_t* status, const int64_t* pos, int64_t n, int64_t* out,
+                                   hipStream_t s);
+
+}  // namespace dgk

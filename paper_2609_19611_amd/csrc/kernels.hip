@@ -1,0 +1,282 @@
+// HIP kernels for gfx950: per-location plan execution and CSR emission
+// (one block per location), the device-wide scan of row sizes, and the
+// two-graph comparator with mismatch compaction.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#define DGC __device__ __forceinline__
+#include "core.h"
+#include "kernels.h"
+
+namespace {
+
+// Block context for core.h: BLOCK threads cooperating on one location.
+template <int BLOCK>
+struct DevCtx {
+  uint32_t* wsum;  // LDS, BLOCK / 64 words
+  DGC int tid() const { return (int)threadIdx.x; }
+  DGC int nthreads() const { return BLOCK; }
+  DGC void sync() const { __syncthreads(); }
+  DGC void atomic_add(uint64_t* p, uint64_t v) const {
+    atomicAdd(reinterpret_cast<unsigned long long*>(p), (unsigned long long)v);
+  }
+  DGC void atomic_max(uint64_t* p, uint64_t v) const {
+    atomicMax(reinterpret_cast<unsigned long long*>(p), (unsigned long long)v);
+  }
+  DGC void store(uint32_t* p, uint32_t v) const { __builtin_nontemporal_store(v, p); }
+  // Exclusive count of set flags among lower threads of the block, and the
+  // block total.  Ends with every thread past a barrier.
+  DGC uint32_t prefix(bool f, uint32_t* total) const {
+    const uint64_t m = __ballot(f);
+    const uint32_t lane = threadIdx.x & 63u;
+    const uint32_t pre = (uint32_t)__popcll(m & ((1ull << lane) - 1ull));
+    if (BLOCK == 64) {
+      *total = (uint32_t)__popcll(m);
+      return pre;
+    }
+    const uint32_t wave = threadIdx.x >> 6;
+    __syncthreads();
+    if (lane == 0) wsum[wave] = (uint32_t)__popcll(m);
+    __syncthreads();
+    uint32_t before = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < BLOCK / 64; ++w) {
+      uint32_t x = wsum[w];
+      before += (w < (int)wave) ? x : 0u;
+      tot += x;
+    }
+    *total = tot;
+    return before + pre;
+  }
+  DGC bool any(bool f) const { return __syncthreads_or(f) != 0; }
+};
+
+extern __shared__ uint64_t dg_smem[];
+
+template <int BLOCK>
+__global__ __launch_bounds__(BLOCK) void k_sizes(const uint8_t* __restrict__ blob, const int64_t* __restrict__ locs,
+                                                 int64_t n, int64_t* __restrict__ offsets, uint32_t* __restrict__ err) {
+  __shared__ uint32_t wsum[BLOCK / 64];
+  const int64_t i = blockIdx.x;
+  if (i >= n) return;
+  DevCtx<BLOCK> c{wsum};
+  uint32_t e = 0;
+  uint8_t* area = reinterpret_cast<uint8_t*>(dg_smem);
+  const uint64_t rows =
+      dgc::location_row<DevCtx<BLOCK>, dgc::EMIT_COUNT>(c, blob, locs[i], area, nullptr, nullptr, 0, &e);
+  if (threadIdx.x == 0) offsets[i + 1] = (int64_t)rows;
+  if (e) atomicOr(err, e);
+}
+
+template <int BLOCK>
+__global__ __launch_bounds__(BLOCK) void k_fill(const uint8_t* __restrict__ blob, const int64_t* __restrict__ locs,
+                                                int64_t n, const int64_t* __restrict__ offsets,
+                                                uint32_t* __restrict__ ids, uint32_t* __restrict__ cnt,
+                                                uint32_t* __restrict__ err) {
+  __shared__ uint32_t wsum[BLOCK / 64];
+  const int64_t i = blockIdx.x;
+  if (i >= n) return;
+  DevCtx<BLOCK> c{wsum};
+  uint32_t e = 0;
+  uint8_t* area = reinterpret_cast<uint8_t*>(dg_smem);
+  const int64_t start = offsets[i];
+  const int64_t room = offsets[i + 1] - start;
+  // Writes stay inside [offsets[i], offsets[i+1]) whatever this row's size.
+  const uint64_t rows = dgc::location_row<DevCtx<BLOCK>, dgc::EMIT_FILL>(
+      c, blob, locs[i], area, ids + start, cnt + start, room > 0 ? (uint64_t)room : 0ull, &e);
+  if (threadIdx.x == 0 && (int64_t)rows != room) e |= DGP_ERR_SIZE;
+  if (e) atomicOr(err, e);
+}
+
+template <int BLOCK>
+__global__ __launch_bounds__(BLOCK) void k_compare(const uint8_t* __restrict__ blob_a,
+                                                   const uint8_t* __restrict__ blob_b, dgc::PairPlan pp,
+                                                   const int64_t* __restrict__ locs, int64_t n,
+                                                   uint8_t* __restrict__ status, int64_t* __restrict__ flags,
+                                                   uint32_t* __restrict__ err) {
+  __shared__ uint32_t wsum[BLOCK / 64];
+  const int64_t i = blockIdx.x;
+  if (i >= n) return;
+  DevCtx<BLOCK> c{wsum};
+  uint32_t e = 0;
+  uint8_t* area = reinterpret_cast<uint8_t*>(dg_smem);
+  const uint32_t s = dgc::location_compare(c, blob_a, blob_b, pp, locs[i], area, &e);
+  if (threadIdx.x == 0) {
+    status[i] = (uint8_t)s;
+    flags[i + 1] = s != 0 ? 1 : 0;
+  }
+  if (e) atomicOr(err, e);
+}
+
+// ---- device-wide inclusive scan of v[1..n] (v[0] = 0 on exit) ---------------
+constexpr int SCAN_THREADS = 256;
+constexpr int SCAN_ITEMS = 4;
+constexpr int SCAN_TILE = SCAN_THREADS * SCAN_ITEMS;
+
+__device__ __forceinline__ int64_t block_inclusive_scan(int64_t x, int64_t* sh, int64_t* total) {
+  // Wave-level scan with shuffles, then across the 4 waves.
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    int64_t y = __shfl_up(x, o, 64);
+    if (lane >= o) x += y;
+  }
+  if (lane == 63) sh[wave] = x;
+  __syncthreads();
+  int64_t before = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < SCAN_THREADS / 64; ++w) {
+    int64_t s = sh[w];
+    before += (w < wave) ? s : 0;
+    tot += s;
+  }
+  __syncthreads();
+  *total = tot;
+  return x + before;
+}
+
+__global__ __launch_bounds__(SCAN_THREADS) void k_scan_reduce(const int64_t* __restrict__ v, int64_t n,
+                                                              int64_t* __restrict__ sums) {
+  __shared__ int64_t sh[SCAN_THREADS / 64];
+  const int64_t base = (int64_t)blockIdx.x * SCAN_TILE;
+  int64_t s = 0;
+#pragma unroll
+  for (int k = 0; k < SCAN_ITEMS; ++k) {
+    int64_t i = base + (int64_t)threadIdx.x * SCAN_ITEMS + k;
+    if (i < n) s += v[1 + i];
+  }
+  int64_t tot;
+  block_inclusive_scan(s, sh, &tot);
+  if (threadIdx.x == 0) sums[blockIdx.x] = tot;
+}
+
+// One block scans the tile sums (exclusive, in place).
+__global__ __launch_bounds__(SCAN_THREADS) void k_scan_sums(int64_t* __restrict__ sums, int64_t m) {
+  __shared__ int64_t sh[SCAN_THREADS / 64];
+  int64_t carry = 0;
+  for (int64_t b = 0; b < m; b += SCAN_THREADS) {
+    int64_t i = b + threadIdx.x;
+    int64_t x = i < m ? sums[i] : 0;
+    int64_t tot;
+    int64_t inc = block_inclusive_scan(x, sh, &tot);
+    if (i < m) sums[i] = carry + inc - x;
+    carry += tot;
+  }
+}
+
+__global__ __launch_bounds__(SCAN_THREADS) void k_scan_apply(int64_t* __restrict__ v, int64_t n,
+                                                             const int64_t* __restrict__ sums) {
+  __shared__ int64_t sh[SCAN_THREADS / 64];
+  const int64_t base = (int64_t)blockIdx.x * SCAN_TILE;
+  int64_t x[SCAN_ITEMS];
+  int64_t s = 0;
+#pragma unroll
+  for (int k = 0; k < SCAN_ITEMS; ++k) {
+    int64_t i = base + (int64_t)threadIdx.x * SCAN_ITEMS + k;
+    x[k] = i < n ? v[1 + i] : 0;
+    s += x[k];
+  }
+  int64_t tot;
+  int64_t inc = block_inclusive_scan(s, sh, &tot);
+  int64_t run = sums[blockIdx.x] + inc - s;
+#pragma unroll
+  for (int k = 0; k < SCAN_ITEMS; ++k) {
+    int64_t i = base + (int64_t)threadIdx.x * SCAN_ITEMS + k;
+    run += x[k];
+    if (i < n) v[1 + i] = run;
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) v[0] = 0;
+}
+
+__global__ void k_scatter_mismatch(const uint8_t* __restrict__ status, const int64_t* __restrict__ pos, int64_t n,
+                                   int64_t* __restrict__ out) {
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n && status[i] != 0) out[pos[i]] = i;
+}
+
+__global__ void k_zero_offsets(int64_t* __restrict__ v) { v[0] = 0; }
+
+__global__ void k_zero_word(uint32_t* __restrict__ p) { *p = 0u; }
+
+template <class K>
+hipError_t allow_lds(K kernel, uint32_t bytes) {
+  if (bytes <= 65536u) return hipSuccess;
+  return hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
+                             (int)bytes);
+}
+
+}  // namespace
+
+namespace dgk {
+
+hipError_t launch_sizes(const uint8_t* blob, const int64_t* locs, int64_t n, int64_t* offsets, uint32_t* err,
+                        int block, uint32_t lds, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipError_t e;
+  if (block == 256) {
+    if ((e = allow_lds(k_sizes<256>, lds)) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_sizes<256>, dim3((unsigned)n), dim3(256), lds, s, blob, locs, n, offsets, err);
+  } else {
+    if ((e = allow_lds(k_sizes<64>, lds)) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_sizes<64>, dim3((unsigned)n), dim3(64), lds, s, blob, locs, n, offsets, err);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_fill(const uint8_t* blob, const int64_t* locs, int64_t n, const int64_t* offsets, uint32_t* ids,
+                       uint32_t* cnt, uint32_t* err, int block, uint32_t lds, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipError_t e;
+  if (block == 256) {
+    if ((e = allow_lds(k_fill<256>, lds)) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_fill<256>, dim3((unsigned)n), dim3(256), lds, s, blob, locs, n, offsets, ids, cnt, err);
+  } else {
+    if ((e = allow_lds(k_fill<64>, lds)) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_fill<64>, dim3((unsigned)n), dim3(64), lds, s, blob, locs, n, offsets, ids, cnt, err);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_compare(const uint8_t* blob_a, const uint8_t* blob_b, const dgc::PairPlan& pp, const int64_t* locs,
+                          int64_t n, uint8_t* status, int64_t* flags, uint32_t* err, int block, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipError_t e;
+  if (block == 256) {
+    if ((e = allow_lds(k_compare<256>, pp.lds_bytes)) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_compare<256>, dim3((unsigned)n), dim3(256), pp.lds_bytes, s, blob_a, blob_b, pp, locs, n,
+                       status, flags, err);
+  } else {
+    if ((e = allow_lds(k_compare<64>, pp.lds_bytes)) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_compare<64>, dim3((unsigned)n), dim3(64), pp.lds_bytes, s, blob_a, blob_b, pp, locs, n,
+                       status, flags, err);
+  }
+  return hipGetLastError();
+}
+
+int64_t scan_temp_entries(int64_t n) { return (n + SCAN_TILE - 1) / SCAN_TILE + 1; }
+
+hipError_t launch_zero(uint32_t* p, hipStream_t s) {
+  hipLaunchKernelGGL(k_zero_word, dim3(1), dim3(1), 0, s, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_scan(int64_t* v, int64_t n, int64_t* sums, hipStream_t s) {
+  if (n <= 0) {
+    hipLaunchKernelGGL(k_zero_offsets, dim3(1), dim3(1), 0, s, v);
+    return hipGetLastError();
+  }
+  const int64_t tiles = (n + SCAN_TILE - 1) / SCAN_TILE;
+  hipLaunchKernelGGL(k_scan_reduce, dim3((unsigned)tiles), dim3(SCAN_THREADS), 0, s, v, n, sums);
+  hipLaunchKernelGGL(k_scan_sums, dim3(1), dim3(SCAN_THREADS), 0, s, sums, tiles);
+  hipLaunchKernelGGL(k_scan_apply, dim3((unsigned)tiles), dim3(SCAN_THREADS), 0, s, v, n, sums);
+  return hipGetLastError();
+}
+
+hipError_t launch_scatter_mismatch(const uint8_t* status, const int64_t* pos, int64_t n, int64_t* out,
+                                   hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_scatter_mismatch, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, status, pos, n, out);
+  return hipGetLastError();
+}
+
+}  // namespace dgk

@@ -1,0 +1,59 @@
+"""Wrapper of the host-emulation test library (one-thread blocks on the CPU
+running the library's compiled plans and block code)."""
+
+import ctypes
+import os
+
+import numpy as np
+
+LIB = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "paper_2609_19611_amd", "lib",
+                   "libdirigo_hostemu.so")
+_lib = None
+
+
+class HostEmuError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"{code}: {msg}")
+        self.code = code
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB):
+            from paper_2609_19611_amd import build
+            build.build_hostemu()
+        _lib = ctypes.CDLL(LIB)
+        _lib.dgh_error.restype = ctypes.c_char_p
+        P, i64 = ctypes.c_void_p, ctypes.c_int64
+        _lib.dgh_sizes.argtypes = [ctypes.c_char_p, i64, P, i64, P]
+        _lib.dgh_fill.argtypes = [ctypes.c_char_p, i64, P, i64, P, P, P]
+        _lib.dgh_compare.argtypes = [ctypes.c_char_p, i64, ctypes.c_char_p, i64, P, i64, P]
+    return _lib
+
+
+def enumerate(text, locs):
+    L = lib()
+    t = text.encode()
+    locs = np.ascontiguousarray(np.asarray(locs, dtype=np.int64))
+    off = np.zeros(len(locs) + 1, dtype=np.int64)
+    rc = L.dgh_sizes(t, len(t), locs.ctypes.data, len(locs), off.ctypes.data)
+    if rc:
+        raise HostEmuError(rc, L.dgh_error().decode())
+    ids = np.zeros(max(1, off[-1]), dtype=np.uint32)
+    cnt = np.zeros(max(1, off[-1]), dtype=np.uint32)
+    rc = L.dgh_fill(t, len(t), locs.ctypes.data, len(locs), off.ctypes.data, ids.ctypes.data, cnt.ctypes.data)
+    if rc:
+        raise HostEmuError(rc, L.dgh_error().decode())
+    return off, ids[: off[-1]], cnt[: off[-1]]
+
+
+def compare(text_a, text_b, locs):
+    L = lib()
+    a, b = text_a.encode(), text_b.encode()
+    locs = np.ascontiguousarray(np.asarray(locs, dtype=np.int64))
+    st = np.zeros(max(1, len(locs)), dtype=np.uint8)
+    rc = L.dgh_compare(a, len(a), b, len(b), locs.ctypes.data, len(locs), st.ctypes.data)
+    if rc:
+        raise HostEmuError(rc, L.dgh_error().decode())
+    return st[: len(locs)]

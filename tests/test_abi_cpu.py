@@ -1,0 +1,108 @@
+"""CPU checks of the C ABI library: it loads, exports every symbol the header
+declares, and its host-only calls (parse, build, info, leaf, workspace size)
+behave, including every error path that needs no device."""
+
+import ctypes
+
+import numpy as np
+import pytest
+
+import oracle
+import tiny_graphs
+from paper_2609_19611_amd import binding as B
+from paper_2609_19611_amd import workloads as W
+
+CAT = tiny_graphs.catalogue()
+
+
+def test_library_exports_every_header_symbol():
+    names = B.header_symbols()
+    assert len(names) == 10
+    lib = ctypes.CDLL(B.LIB_PATH)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+@pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4", "c5"])
+def test_info_of_workloads(name):
+    text = W.CONFIGS[name]["text"]()
+    g = B.dg_graph_parse(text)
+    info = B.dg_graph_info(g)
+    og = oracle.Graph(text)
+    assert info["output_shape"] == og.output_shape
+    assert info["output_numel"] == og.output_numel
+    assert info["leaf_total"] == og.leaf_total
+    assert info["n_leaves"] == len(og.leaves)
+    for i, leaf in enumerate(og.leaves):
+        li = B.dg_graph_leaf(g, i)
+        assert (li["name"], li["shape"], li["base"], li["numel"]) == (leaf.name, leaf.shape, leaf.base, leaf.numel)
+    # Static bounds hold for sampled rows.
+    locs = W.config_locations(name)[:: max(1, len(W.config_locations(name)) // 5)][:5]
+    off, ids, cnt = og.enumerate(locs, threads=4)
+    assert info["max_row_size"] >= int(np.diff(off).max())
+    assert info["count_bound"] >= int(cnt.max())
+    assert info["lds_bytes"] <= 160 * 1024
+    assert info["block_threads"] in (64, 256)
+
+
+def test_build_matches_parse():
+    leaves = [("x", [16, 3, 32, 32]), ("W", [16, 3, 3, 3]), ("conv_b", [16]), ("bias", [16, 1, 1])]
+    ops = [("t1", "conv", [0, 1, 2], "stride=1,1 pad=1,1 dilation=1,1 groups=1"),
+           ("t2", "add", [4, 3], ""), ("t3", "gelu", [5], ""),
+           ("y", "max_pool", [6], "kernel=2,2 stride=2,2")]
+    gb = B.dg_graph_build(leaves, ops, 7)
+    gp = B.dg_graph_parse(W.c2_text())
+    assert B.dg_graph_info(gb) == B.dg_graph_info(gp)
+
+
+@pytest.mark.parametrize("text,code", [
+    ("leaf x 2\noutput x 2\n", "DG_E_PARSE"),
+    ("dgir 1\nleaf x 2,0\noutput x 2,0\n", "DG_E_SHAPE"),
+    ("dgir 1\nleaf x 2\nop y frobnicate x\noutput y 2\n", "DG_E_UNSUPPORTED_OP"),
+    ("dgir 1\nleaf x 2,3\nleaf z 4\nop y add x z\noutput y 2,3\n", "DG_E_SHAPE"),
+    ("dgir 1\nleaf x 2\nop y relu q\noutput y 2\n", "DG_E_PARSE"),
+    ("dgir 1\nleaf x 2\nop y relu x\noutput y 3\n", "DG_E_SHAPE"),
+    ("dgir 1\nleaf x 2\nop y relu x\n", "DG_E_PARSE"),
+    ("dgir 1\nleaf x 65536,65536\noutput x 65536,65536\n", "DG_E_OVERFLOW"),
+    ("dgir 1\nleaf x 2,3\nop y affine_gather x ; shape=2 idx0=o0+,o1\noutput y 2\n", "DG_E_PARSE"),
+    ("dgir 1\nleaf x 2,3\nop y affine_gather x ; shape=2 idx0=o0\noutput y 2\n", "DG_E_SHAPE"),
+    ("dgir 1\nleaf x 2,3\nop y conv x x\noutput y 2\n", "DG_E_SHAPE"),
+])
+def test_parse_errors(text, code):
+    with pytest.raises(B.DgError) as e:
+        B.dg_graph_parse(text)
+    assert e.value.name == code
+    assert B.dg_last_error()
+
+
+@pytest.mark.parametrize("name", sorted(tiny_graphs.NONSEPARABLE))
+def test_nonseparable_graphs_are_rejected(name):
+    with pytest.raises(B.DgError) as e:
+        B.dg_graph_parse(CAT[name][0])
+    assert e.value.name == "DG_E_UNSUPPORTED_OP"
+
+
+def test_static_overflow_rejected():
+    # Ten nested layer norms over 65536 elements: the bound passes 2^63.
+    ops = []
+    prev = "x"
+    for i in range(10):
+        ops.append((f"n{i}", "layer_norm", [prev], dict(ndims=1)))
+        prev = f"n{i}"
+    txt = tiny_graphs._g([("x", [1, 65536])], ops, prev, [1, 65536])
+    with pytest.raises(B.DgError) as e:
+        B.dg_graph_parse(txt)
+    assert e.value.name == "DG_E_OVERFLOW"
+
+
+def test_workspace_size_grows_with_n():
+    g = B.dg_graph_parse(W.c1_text())
+    a, b, c = (B.dg_workspace_size(g, n) for n in (0, 1000, 1_000_000))
+    assert 0 < a <= b <= c
+    assert c >= 8 * 1_000_001
+
+
+def test_header_documents_every_status():
+    text = open(B.HEADER).read()
+    for code in B.STATUS_NAMES.values():
+        assert code in text

@@ -1,0 +1,209 @@
+"""GPU parity: the HIP library against the CPU oracle, bit for bit.
+
+Every call goes through the C ABI (paper_2609_19611_amd.binding).  Small
+graphs are compared at every output location; the five workloads run at
+their full sizes in the same launch configuration the benchmark times, with
+sampled rows checked against the oracle and closed-form properties checked
+at every location.
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import tiny_graphs
+from paper_2609_19611_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+CAT = tiny_graphs.catalogue()
+SEPARABLE = sorted(set(CAT) - tiny_graphs.NONSEPARABLE)
+
+
+@pytest.fixture(scope="module")
+def B():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_19611_amd import binding
+    return binding
+
+
+def rows_to_host(off, ids, cnt, positions):
+    """Rows at the given positions: (lengths, ids, counts) as numpy, taken
+    slice by slice on the device."""
+    off_h = off.cpu().numpy()
+    out = []
+    for p in positions:
+        a, b = int(off_h[p]), int(off_h[p + 1])
+        out.append((ids[a:b].cpu().numpy().view(np.uint32), cnt[a:b].cpu().numpy().view(np.uint32)))
+    return off_h, out
+
+
+def oracle_rows(text, locs, threads=8):
+    off, ids, cnt = oracle.Graph(text).enumerate(locs, threads=threads)
+    return [(ids[off[i]:off[i + 1]], cnt[off[i]:off[i + 1]]) for i in range(len(locs))]
+
+
+def check_rows_sorted(off, ids):
+    """Within every row ids strictly increase (checked on the device)."""
+    if ids.numel() < 2:
+        return
+    chunk = 1 << 28
+    starts = torch.zeros(ids.numel(), dtype=torch.bool, device=ids.device)
+    inner = off[1:-1]
+    starts[inner[inner < ids.numel()]] = True
+    for a in range(1, ids.numel(), chunk):
+        b = min(ids.numel(), a + chunk)
+        cur = ids[a:b].to(torch.int64) & 0xFFFFFFFF
+        prev = ids[a - 1:b - 1].to(torch.int64) & 0xFFFFFFFF
+        assert bool(((cur > prev) | starts[a:b]).all())
+
+
+@pytest.mark.parametrize("name", SEPARABLE)
+def test_catalogue_all_locations(B, name):
+    text = CAT[name][0]
+    g = B.dg_graph_parse(text)
+    og = oracle.Graph(text)
+    locs = list(range(og.output_numel))
+    off, ids, cnt = B.enumerate_locations(g, locs)
+    ro, io, co = og.enumerate(locs)
+    assert np.array_equal(off.cpu().numpy(), ro)
+    assert np.array_equal(ids.cpu().numpy().view(np.uint32), io)
+    assert np.array_equal(cnt.cpu().numpy().view(np.uint32), co)
+
+
+def test_c1_all(B):
+    text = W.c1_text()
+    off, ids, cnt = B.enumerate_locations(B.dg_graph_parse(text), W.config_locations("c1"))
+    ro, io, co = oracle.Graph(text).enumerate(range(8))
+    assert np.array_equal(off.cpu().numpy(), ro)
+    assert np.array_equal(ids.cpu().numpy().view(np.uint32), io)
+    assert np.array_equal(cnt.cpu().numpy().view(np.uint32), co)
+
+
+def test_c2_all_4096(B):
+    text = W.c2_text()
+    locs = W.config_locations("c2")
+    off, ids, cnt = B.enumerate_locations(B.dg_graph_parse(text), locs)
+    ro, io, co = oracle.Graph(text).enumerate(locs, threads=8)
+    assert np.array_equal(off.cpu().numpy(), ro)
+    assert np.array_equal(ids.cpu().numpy().view(np.uint32), io)
+    assert np.array_equal(cnt.cpu().numpy().view(np.uint32), co)
+
+
+def test_c3_full(B):
+    text = W.c3_text()
+    locs = W.config_locations("c3")
+    off, ids, cnt = B.enumerate_locations(B.dg_graph_parse(text), locs)
+    la = np.asarray(locs)
+    d, h = (la // 4096) % 32, (la // 64) % 64
+    td = np.where((d % 2 == 1) & (d <= 29), 2, 1)
+    th = np.where((h % 2 == 1) & (h <= 61), 2, 1)
+    off_h = off.cpu().numpy()
+    assert np.array_equal(np.diff(off_h), 7168 * td * th + 64)
+    check_rows_sorted(off, ids)
+    rng = np.random.default_rng(3)
+    pos = sorted(set(rng.choice(len(locs), 24, replace=False).tolist()) | {0, len(locs) - 1})
+    _, got = rows_to_host(off, ids, cnt, pos)
+    want = oracle_rows(text, [locs[p] for p in pos])
+    for (gi, gc), (wi, wc) in zip(got, want):
+        assert np.array_equal(gi, wi) and np.array_equal(gc, wc)
+
+
+def test_c4_full(B):
+    text = W.c4_text()
+    locs = W.config_locations("c4")
+    off, ids, cnt = B.enumerate_locations(B.dg_graph_parse(text), locs)
+    off_h = off.cpu().numpy()
+    assert np.all(np.diff(off_h) == 66626)
+    assert off_h[-1] == 4366401536
+    rng = np.random.default_rng(4)
+    pos = sorted(set(rng.choice(len(locs), 6, replace=False).tolist()) | {0, len(locs) - 1})
+    _, got = rows_to_host(off, ids, cnt, pos)
+    want = oracle_rows(text, [locs[p] for p in pos])
+    for (gi, gc), (wi, wc) in zip(got, want):
+        assert np.array_equal(gi, wi) and np.array_equal(gc, wc)
+    # Counts take only the closed-form values.
+    vals = torch.unique(cnt[: 66626 * 64])
+    assert set(vals.cpu().tolist()) == {1, 66, 67, 4225, 4226}
+
+
+def test_c5_clean_and_faults(B):
+    ref_text = W.c5_reference_text()
+    ref = B.dg_graph_parse(ref_text)
+    locs = W.config_locations("c5")
+    d_locs = torch.as_tensor(locs, dtype=torch.int64, device="cuda")
+    status, mism = B.compare_locations(ref, B.dg_graph_parse(W.c5_variant_text()), d_locs)
+    assert mism.numel() == 0 and int(status.max()) == 0
+    og_ref = oracle.Graph(ref_text)
+    rng = np.random.default_rng(5)
+    sample = np.sort(rng.choice(len(locs), 160, replace=False))
+    for f in W.c5_faults():
+        vt = W.c5_variant_text(fault=f)
+        status, mism = B.compare_locations(ref, B.dg_graph_parse(vt), d_locs)
+        st = status.cpu().numpy()
+        assert np.array_equal(mism.cpu().numpy(), np.nonzero(st)[0]), f
+        want = oracle.compare(og_ref, oracle.Graph(vt), [locs[i] for i in sample], threads=8)
+        assert np.array_equal(st[sample], want), f
+        assert st.any(), f
+
+
+def test_paper_example(B):
+    a = B.dg_graph_parse(W.paper_kernel_text())
+    b = B.dg_graph_parse(W.paper_reference_text())
+    status, mism = B.compare_locations(a, b, [11596, 0])
+    assert status.cpu().tolist() == [1, 1] and mism.cpu().tolist() == [0, 1]
+    off_a, _, _ = B.enumerate_locations(a, [11596])
+    off_b, _, _ = B.enumerate_locations(b, [11596])
+    assert int(off_a[1]) == 513 and int(off_b[1]) == 1025
+
+
+def test_compare_small_graphs_against_oracle(B):
+    ref = W.c5_reference_text(n=2, c=4, hw=6, co=3)
+    locs = list(range(2 * 3 * 6 * 6))
+    g_ref, o_ref = B.dg_graph_parse(ref), oracle.Graph(ref)
+    for f in W.c5_faults():
+        vt = W.c5_variant_text(fault=f, n=2, c=4, hw=6, co=3)
+        st, _ = B.compare_locations(g_ref, B.dg_graph_parse(vt), locs)
+        assert np.array_equal(st.cpu().numpy(), oracle.compare(o_ref, oracle.Graph(vt), locs)), f
+    a = CAT["self_product"][0]
+    b = tiny_graphs._g([("x", [3, 2]), ("w", [2])], [("a", "add", ["x", "x"], {}), ("y", "mul", ["a", "w"], {})],
+                       "y", [3, 2])
+    st, _ = B.compare_locations(B.dg_graph_parse(a), B.dg_graph_parse(b), range(6))
+    assert st.cpu().tolist() == [2] * 6
+
+
+def test_edge_cases(B):
+    g = B.dg_graph_parse(W.c2_text())
+    off, ids, cnt = B.enumerate_locations(g, torch.empty(0, dtype=torch.int64))
+    assert off.cpu().tolist() == [0] and ids.numel() == 0
+    locs = [65535, 3, 3, 40000, 0, 3]
+    off, ids, cnt = B.enumerate_locations(g, locs)
+    ro, io, co = oracle.Graph(W.c2_text()).enumerate(locs)
+    assert np.array_equal(off.cpu().numpy(), ro)
+    assert np.array_equal(ids.cpu().numpy().view(np.uint32), io)
+    with pytest.raises(B.DgError) as e:
+        B.enumerate_locations(g, [0, 65536])
+    assert e.value.name == "DG_E_RANGE"
+    with pytest.raises(B.DgError) as e:
+        B.enumerate_locations(g, [-1])
+    assert e.value.name == "DG_E_RANGE"
+    txt = tiny_graphs._g([("x", [1, 4096])],
+                         [("a", "layer_norm", ["x"], dict(ndims=1)), ("b", "layer_norm", ["a"], dict(ndims=1)),
+                          ("y", "layer_norm", ["b"], dict(ndims=1))], "y", [1, 4096])
+    with pytest.raises(B.DgError) as e:
+        B.enumerate_locations(B.dg_graph_parse(txt), [0])
+    assert e.value.name == "DG_E_OVERFLOW"
+    with pytest.raises(B.DgError) as e:
+        B.compare_locations(g, B.dg_graph_parse(W.c1_text()), [0])
+    assert e.value.name == "DG_E_SIGNATURE"
+
+
+def test_repeatable(B):
+    g = B.dg_graph_parse(W.c3_text())
+    locs = W.config_locations("c3")[:2048]
+    a = B.enumerate_locations(g, locs)
+    b = B.enumerate_locations(g, locs)
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)

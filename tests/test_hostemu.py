@@ -1,0 +1,89 @@
+"""CPU checks of the library's compiler and block code.
+
+The host-emulation test library runs the compiled per-location plans and
+the same block code as the GPU kernels with a block of one host thread; its
+rows must equal the oracle's bit for bit.  (The GPU parity tests in
+test_gpu_parity.py check the real kernels.)
+"""
+
+import numpy as np
+import pytest
+
+import hostemu
+import oracle
+import tiny_graphs
+from paper_2609_19611_amd import workloads as W
+
+CAT = tiny_graphs.catalogue()
+SEPARABLE = sorted(set(CAT) - tiny_graphs.NONSEPARABLE)
+
+
+def assert_same(a, b):
+    for x, y in zip(a, b):
+        assert np.array_equal(np.asarray(x), np.asarray(y))
+
+
+@pytest.mark.parametrize("name", SEPARABLE)
+def test_catalogue_matches_oracle(name):
+    text = CAT[name][0]
+    g = oracle.Graph(text)
+    locs = list(range(g.output_numel))
+    assert_same(hostemu.enumerate(text, locs), g.enumerate(locs))
+
+
+@pytest.mark.parametrize("name", sorted(tiny_graphs.NONSEPARABLE))
+def test_nonseparable_rejected(name):
+    with pytest.raises(hostemu.HostEmuError) as e:
+        hostemu.enumerate(CAT[name][0], [0])
+    assert e.value.code == -4
+
+
+@pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4", "c5"])
+def test_workload_samples_match_oracle(name):
+    text = W.CONFIGS[name]["text"]()
+    locs = W.config_locations(name)
+    rng = np.random.default_rng(7)
+    k = {"c1": 8, "c2": 64, "c3": 6, "c4": 3, "c5": 24}[name]
+    pick = sorted(set(rng.choice(locs, size=min(k, len(locs)), replace=False).tolist()) | {locs[0], locs[-1]})
+    assert_same(hostemu.enumerate(text, pick), oracle.Graph(text).enumerate(pick, threads=4))
+
+
+def test_unsorted_and_duplicate_locations():
+    text = W.c2_text()
+    locs = [65535, 3, 3, 40000, 0, 3]
+    assert_same(hostemu.enumerate(text, locs), oracle.Graph(text).enumerate(locs))
+
+
+def test_compare_clean_and_faults():
+    ref = W.c5_reference_text(n=2, c=4, hw=6, co=3)
+    locs = list(range(2 * 3 * 6 * 6))
+    assert not hostemu.compare(ref, W.c5_variant_text(n=2, c=4, hw=6, co=3), locs).any()
+    g_ref = oracle.Graph(ref)
+    for f in W.c5_faults():
+        var = W.c5_variant_text(fault=f, n=2, c=4, hw=6, co=3)
+        assert np.array_equal(hostemu.compare(ref, var, locs), oracle.compare(g_ref, oracle.Graph(var), locs)), f
+
+
+def test_compare_status_two():
+    a = CAT["self_product"][0]
+    b = tiny_graphs._g([("x", [3, 2]), ("w", [2])], [("a", "add", ["x", "x"], {}), ("y", "mul", ["a", "w"], {})],
+                       "y", [3, 2])
+    assert list(hostemu.compare(a, b, range(6))) == [2] * 6
+    assert list(hostemu.compare(a, a, range(6))) == [0] * 6
+
+
+def test_paper_example():
+    st = hostemu.compare(W.paper_kernel_text(), W.paper_reference_text(), [11596, 0, 131071])
+    assert list(st) == [1, 1, 1]
+
+
+def test_range_and_overflow_errors():
+    with pytest.raises(hostemu.HostEmuError) as e:
+        hostemu.enumerate(W.c1_text(), [8])
+    assert e.value.code == -5
+    txt = tiny_graphs._g([("x", [1, 4096])],
+                         [("a", "layer_norm", ["x"], dict(ndims=1)), ("b", "layer_norm", ["a"], dict(ndims=1)),
+                          ("y", "layer_norm", ["b"], dict(ndims=1))], "y", [1, 4096])
+    with pytest.raises(hostemu.HostEmuError) as e:
+        hostemu.enumerate(txt, [0])
+    assert e.value.code == -6

@@ -19,6 +19,13 @@ def _g(leaves, ops, out, shape):
     return g.text()
 
 
+# Graphs whose dataflow the separable plan cannot express: a grouped
+# transposed convolution (its weight's first two dims are both fed by the
+# output channel) and a reshape that merges dims.  The oracle handles them;
+# the library rejects them with DG_E_UNSUPPORTED_OP.
+NONSEPARABLE = {"convT1d_groups", "views"}
+
+
 def catalogue():
     """name -> (dgir text, masks) where masks says whether a saturating or
     selecting op may hide a dependence from perturbation."""
@@ -103,6 +110,18 @@ def catalogue():
                       ("d", "expand", ["z"], dict(shape=[2, 4, 3])),
                       ("y", "add", ["c", "d"], {})],
                      "y", [2, 4, 3]), False)
+    G["convT1d"] = (_g([("x", [2, 3, 5]), ("W", [3, 2, 4]), ("b", [2])],
+                       [("y", "conv_transpose", ["x", "W", "b"],
+                         dict(stride=[3], pad=[2], output_padding=[1], dilation=[1], groups=1))],
+                       "y", [2, 2, 13]), False)
+    G["views_sep"] = (_g([("x", [2, 3, 4]), ("z", [4, 1])],
+                         [("a", "slice", ["x"], dict(dim=2, start=1, end=4, step=2)),
+                          ("b", "permute", ["a"], dict(dims=[2, 0, 1])),
+                          ("c", "reshape", ["b"], dict(shape=[2, 1, 2, 3])),
+                          ("d", "expand", ["z"], dict(shape=[2, 4, 3])),
+                          ("e", "reshape", ["d"], dict(shape=[2, 4, 1, 3])),
+                          ("y", "add", ["c", "e"], {})],
+                         "y", [2, 4, 2, 3]), False)
     G["gather_exact_div"] = (_g([("x", [2, 4]), ("w", [3])],
                                 [("y", "affine_gather", ["x", "w"],
                                   dict(shape=[2, 8], window=[3], idx0=["o0", "(o1+1-w0)/2"], idx1=["w0"], mult=[1, 1]))],
