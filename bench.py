@@ -38,7 +38,38 @@ def parse_args():
     p.add_argument("--workload", default="c4", choices=["c1", "c2", "c3", "c4", "c5"])
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the oracle sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--two-pass", action="store_true",
+                   help="time dg_enumerate_sizes + dg_enumerate_fill instead of the single-pass dg_enumerate")
+    p.add_argument("--copy-gib", type=float, default=0.0,
+                   help="instead of the workload, time a plain device copy of this many GiB (HBM calibration)")
     return p.parse_args()
+
+
+def copy_calibration(gib, steps, warmup):
+    """Device-to-device copy and a write-only fill of a known size: measured
+    HBM bandwidth, and the reference dispatches for scaling the FETCH_SIZE /
+    WRITE_SIZE counters."""
+    import torch
+    n = int(gib * (1 << 30)) // 4
+    src = torch.ones(n, dtype=torch.int32, device="cuda")
+    dst = torch.empty_like(src)
+
+    def timed(fn):
+        for _ in range(warmup):
+            fn()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+        torch.cuda.synchronize()
+        for a, b in ev:
+            a.record()
+            fn()
+            b.record()
+        torch.cuda.synchronize()
+        return float(np.median([a.elapsed_time(b) for a, b in ev]))
+
+    ms_copy = timed(lambda: dst.copy_(src))
+    ms_fill = timed(lambda: dst.fill_(7))
+    print(json.dumps({"bytes": n * 4, "copy_ms": ms_copy, "copy_GBps_read_plus_write": 2 * n * 4 / (ms_copy * 1e-3) / 1e9,
+                      "fill_ms": ms_fill, "fill_GBps_write": n * 4 / (ms_fill * 1e-3) / 1e9}), flush=True)
 
 
 def git_sha():
@@ -60,9 +91,9 @@ def cpu_baseline(workload, text_a, text_b, locs, target_s):
             t0 = time.perf_counter()
             oracle.compare(ga, gb, locs[:m], threads=threads)
             dt = time.perf_counter() - t0
-            if dt * 4 > target_s or m >= len(locs):
+            if dt > 0.5 * target_s or m >= len(locs):
                 break
-            m = min(len(locs), int(m * max(2.0, 0.8 * target_s / max(dt, 1e-3))))
+            m = min(len(locs), int(m * min(64.0, max(2.0, 0.8 * target_s / max(dt, 1e-3)))))
         return {"value": m / dt, "unit": "locations/s", "cores": threads, "kind": "oracle",
                 "sample": f"first {m} of {len(locs)} locations, one compare (clean variant)",
                 "seconds": round(dt, 3)}
@@ -72,9 +103,9 @@ def cpu_baseline(workload, text_a, text_b, locs, target_s):
         t0 = time.perf_counter()
         off, _, _ = g.enumerate(locs[:m], threads=threads)
         dt = time.perf_counter() - t0
-        if dt * 4 > target_s or m >= len(locs):
+        if dt > 0.5 * target_s or m >= len(locs):
             break
-        m = min(len(locs), int(m * max(2.0, 0.8 * target_s / max(dt, 1e-3))))
+        m = min(len(locs), int(m * min(64.0, max(2.0, 0.8 * target_s / max(dt, 1e-3)))))
     return {"value": float(off[-1]) / dt, "unit": "entries/s", "cores": threads, "kind": "oracle",
             "sample": f"first {m} of {len(locs)} locations", "locations_per_s": m / dt,
             "seconds": round(dt, 3)}
@@ -87,6 +118,10 @@ def main():
               "independent shard of the location list (no collective on the hot path), so the whole-job "
               "rate is N times the one-GPU rate measured here.", file=sys.stderr)
         sys.exit(2)
+
+    if args.copy_gib > 0:
+        copy_calibration(args.copy_gib, args.steps, args.warmup)
+        return
 
     import torch
     from paper_2609_19611_amd import binding as B
@@ -145,36 +180,56 @@ def main():
 
     ws = torch.empty(max(B.dg_workspace_size(g, n), 1), dtype=torch.uint8, device=dev)
     offsets = torch.empty(n + 1, dtype=torch.int64, device=dev)
+    # Size the output buffers once (untimed); every timed step then computes
+    # the offsets and rows from scratch.
     total = B.dg_enumerate_sizes(g, d_locs, offsets, ws)
     ids = torch.empty(max(total, 1), dtype=torch.int32, device=dev)
     cnt = torch.empty(max(total, 1), dtype=torch.int32, device=dev)
-    fill_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+    kern_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
                for _ in range(args.steps)]
 
-    def step(i=None):
-        t = B.dg_enumerate_sizes(g, d_locs, offsets, ws)
-        if i is not None:
-            fill_ev[i][0].record(stream)
-        B.dg_enumerate_fill(g, d_locs, offsets, ids, cnt, ws)
-        if i is not None:
-            fill_ev[i][1].record(stream)
-        return t
+    if args.two_pass:
+        kernel = "k_fill"
 
-    for _ in range(args.warmup):
+        def step(i=None):
+            t = B.dg_enumerate_sizes(g, d_locs, offsets, ws)
+            if i is not None:
+                kern_ev[i][0].record(stream)
+            B.dg_enumerate_fill(g, d_locs, offsets, ids, cnt, ws)
+            if i is not None:
+                kern_ev[i][1].record(stream)
+            return t
+    else:
+        kernel = "k_enumerate"
+
+        def step(i=None):
+            if i is not None:
+                kern_ev[i][0].record(stream)
+            t = B.dg_enumerate(g, d_locs, offsets, ids, cnt, ws)
+            if i is not None:
+                kern_ev[i][1].record(stream)
+            return t
+
+    for _ in range(max(1, args.warmup)):
         step()
     torch.cuda.synchronize()
+    # The first call compiled the graph's specialised kernels (unless
+    # DIRIGO_JIT=0); the timed kernel is named accordingly.
+    specialized = B.dg_graph_info(g)["specialized"] == 1
+    if specialized:
+        kernel = "dg_" + kernel[2:]
     t0 = time.perf_counter()
     for i in range(args.steps):
         t = step(i)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     assert t == total
-    fill_ms = float(np.mean([a.elapsed_time(b) for a, b in fill_ev]))
+    kern_ms = float(np.mean([a.elapsed_time(b) for a, b in kern_ev]))
     ms = elapsed * 1000 / args.steps
     # Algorithmic bytes per location: 8 (location) + 8 (offset) + 8 per entry
     # (uint32 id + uint32 count).
     alg_bytes = 16 * n + 8 * total
-    achieved = alg_bytes / (fill_ms * 1e-3) / 1e9
+    achieved = alg_bytes / (kern_ms * 1e-3) / 1e9
     line = {
         "metric": "footprint entries/sec enumerated (with output locations/sec and % of HBM peak)",
         "value": total / (elapsed / args.steps), "unit": "entries/s", "n_gpus": 1, "steps": args.steps,
@@ -183,9 +238,10 @@ def main():
         "data": "synthetic (shapes only; footprints are data independent)",
         "config": {"workload": f"{args.workload}: " + cfg["desc"], "locations": n, "entries_per_step": total,
                    "locations_per_s": n / (elapsed / args.steps), "block_threads": info["block_threads"],
-                   "lds_bytes": info["lds_bytes"]},
-        "roofline": {"bound": "hbm", "kernel": "k_fill", "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None, "fill_ms": fill_ms,
+                   "lds_bytes": info["lds_bytes"], "path": "two-pass" if args.two_pass else "single-pass",
+                   "kernels": "specialized" if specialized else "interpreted"},
+        "roofline": {"bound": "hbm", "kernel": kernel, "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBS, "traffic": None, "kernel_ms": kern_ms,
                      "algorithmic_bytes": alg_bytes},
     }
     if not args.no_cpu_baseline:

@@ -42,6 +42,11 @@
  * errors and dg_last_error() returns a message for the calling thread.  No
  * C++ exception crosses this interface.
  *
+ * Specialisation: on its first device call, a graph compiles kernels
+ * specialised to its plan (hipRTC, a few seconds, cached per process);
+ * setting the environment variable DIRIGO_JIT=0 keeps the precompiled
+ * kernels, which run the same code on the plan as data.
+ *
  * Thread safety: a dg_graph is immutable after construction and may be used
  * from several host threads and streams at once.  Calls that share one
  * workspace buffer must not overlap in time.
@@ -71,6 +76,8 @@ typedef int32_t dg_status;
 #define DG_E_HIP (-9)            /* HIP runtime error (message attached) */
 #define DG_E_CAPACITY (-10)      /* the per-location plan of this graph does
                                     not fit the device's local data share */
+#define DG_E_BUFFER (-11)        /* dg_enumerate: the rows need more entries
+                                    than the output buffers hold */
 
 #define DG_MAX_RANK 8
 #define DG_NAME_LEN 64
@@ -162,6 +169,10 @@ typedef struct {
   int32_t lds_bytes;          /* local data share one location needs */
   int32_t block_threads;      /* threads working on one location */
   int32_t max_leaf_terms;     /* separable terms of the busiest leaf */
+  int32_t specialized;        /* kernels specialised for this graph on the
+                                 current device: 1 loaded, 0 off or failed
+                                 (the precompiled kernels run the plan),
+                                 -1 not used on this device yet */
 } dg_graph_info_t;
 
 dg_status dg_graph_info(const dg_graph* g, dg_graph_info_t* out);
@@ -208,6 +219,23 @@ dg_status dg_enumerate_sizes(const dg_graph* g, const int64_t* d_locs, int64_t n
  * Asynchronous on `stream`. */
 dg_status dg_enumerate_fill(const dg_graph* g, const int64_t* d_locs, int64_t n, const int64_t* d_offsets,
                             uint32_t* d_ids, uint32_t* d_counts, void* d_ws, void* stream);
+
+/* dg_enumerate: sizes, offsets and rows in one pass over the locations.
+ * Each location's plan runs once; a block finds its row offset by a
+ * decoupled look-back over its predecessors' row sizes.
+ *   d_locs[n]        device, int64 flat output locations (as above)
+ *   d_offsets[n+1]   device, written as by dg_enumerate_sizes
+ *   d_ids, d_counts  device, `capacity` uint32 entries each; row i is written
+ *                    at [d_offsets[i], d_offsets[i+1]) when that range lies
+ *                    below `capacity`
+ *   h_total          host, written: d_offsets[n]
+ * Synchronous.  Returns DG_E_BUFFER when *h_total > capacity: the offsets
+ * and *h_total are then valid, the rows past `capacity` are not written,
+ * and the call can be repeated with larger buffers.  DG_E_RANGE and
+ * DG_E_OVERFLOW as for dg_enumerate_sizes.  A caller that knows the total
+ * (the same graph and locations as an earlier call) needs this one call. */
+dg_status dg_enumerate(const dg_graph* g, const int64_t* d_locs, int64_t n, int64_t* d_offsets, uint32_t* d_ids,
+                       uint32_t* d_counts, int64_t capacity, void* d_ws, int64_t* h_total, void* stream);
 
 /* dg_compare: footprints of two graphs, location by location (Sec. 3.4:
  * e_A and e_B at the same l; the two programs read the same leaves and

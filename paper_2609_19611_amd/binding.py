@@ -25,6 +25,7 @@ DG_OK = 0
 STATUS_NAMES = {
     -1: "DG_E_INVALID_ARG", -2: "DG_E_PARSE", -3: "DG_E_SHAPE", -4: "DG_E_UNSUPPORTED_OP", -5: "DG_E_RANGE",
     -6: "DG_E_OVERFLOW", -7: "DG_E_SIGNATURE", -8: "DG_E_WORKSPACE", -9: "DG_E_HIP", -10: "DG_E_CAPACITY",
+    -11: "DG_E_BUFFER",
 }
 MAX_RANK = 8
 
@@ -49,6 +50,7 @@ class GraphInfo(ctypes.Structure):
         ("lds_bytes", ctypes.c_int32),
         ("block_threads", ctypes.c_int32),
         ("max_leaf_terms", ctypes.c_int32),
+        ("specialized", ctypes.c_int32),
     ]
 
 
@@ -86,6 +88,7 @@ def _load():
         "dg_workspace_size": ([P, i64, ctypes.POINTER(sz)], i32),
         "dg_enumerate_sizes": ([P, P, i64, P, P, ctypes.POINTER(i64), P], i32),
         "dg_enumerate_fill": ([P, P, i64, P, P, P, P, P], i32),
+        "dg_enumerate": ([P, P, i64, P, P, P, i64, P, ctypes.POINTER(i64), P], i32),
         "dg_compare": ([P, P, P, i64, P, P, ctypes.POINTER(i64), P, P], i32),
         "dg_last_error": ([], ctypes.c_char_p),
     }
@@ -176,6 +179,7 @@ def dg_graph_info(g: Graph) -> dict:
         "lds_bytes": info.lds_bytes,
         "block_threads": info.block_threads,
         "max_leaf_terms": info.max_leaf_terms,
+        "specialized": info.specialized,
     }
 
 
@@ -217,6 +221,26 @@ def dg_enumerate_fill(g: Graph, d_locs: torch.Tensor, d_offsets: torch.Tensor, d
             raise ValueError(f"{what} must be a contiguous 32-bit device tensor")
     _check(_lib.dg_enumerate_fill(g.handle, _ptr(d_locs), n, _ptr(d_offsets), _ptr(d_ids), _ptr(d_counts),
                                   _ptr(d_ws), _stream(stream)))
+
+
+def dg_enumerate(g: Graph, d_locs: torch.Tensor, d_offsets: torch.Tensor, d_ids: torch.Tensor,
+                 d_counts: torch.Tensor, d_ws: torch.Tensor, stream=None) -> int:
+    """Single pass: offsets and rows; capacity is the size of d_ids/d_counts.
+    Returns the total; raises DgError(DG_E_BUFFER) if the rows do not fit
+    (the offsets are then valid)."""
+    n = d_locs.numel()
+    _dev_i64(d_locs, "locations")
+    _dev_i64(d_offsets, "offsets")
+    if d_offsets.numel() < n + 1:
+        raise ValueError("offsets needs n + 1 entries")
+    cap = min(d_ids.numel(), d_counts.numel())
+    for t, what in ((d_ids, "ids"), (d_counts, "counts")):
+        if not t.is_cuda or t.dtype not in (torch.int32, torch.uint32) or not t.is_contiguous():
+            raise ValueError(f"{what} must be a contiguous 32-bit device tensor")
+    total = ctypes.c_int64()
+    _check(_lib.dg_enumerate(g.handle, _ptr(d_locs), n, _ptr(d_offsets), _ptr(d_ids), _ptr(d_counts), cap,
+                             _ptr(d_ws), ctypes.byref(total), _stream(stream)))
+    return total.value
 
 
 def dg_compare(a: Graph, b: Graph, d_locs: torch.Tensor, d_status: torch.Tensor, d_mismatch: torch.Tensor,

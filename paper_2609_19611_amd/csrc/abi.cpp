@@ -4,6 +4,7 @@
 #include <algorithm>
 #include <cstring>
 #include <map>
+#include <cstdlib>
 #include <mutex>
 #include <new>
 #include <string>
@@ -11,7 +12,16 @@
 #include "../../include/dirigo_rocm.h"
 #include "compile.h"
 #include "graph.h"
+#include "jit.h"
 #include "kernels.h"
+
+// Specialised kernels of a graph on one device.
+struct DevKernels {
+  bool tried = false;
+  bool ok = false;
+  dg::JitModule jm;
+  std::string log;
+};
 
 struct dg_graph {
   dg::GraphIR ir;
@@ -20,6 +30,7 @@ struct dg_graph {
   uint32_t lds = 0;
   std::mutex mu;
   std::map<int, uint8_t*> dev_blob;  // compiled plan per device
+  std::map<int, DevKernels> jit;     // specialised kernels per device
 };
 
 namespace {
@@ -55,7 +66,12 @@ int max_lds_per_block() {
 dg_status finalize(dg_graph* g) {
   g->plan = dg::compile_plan(g->ir);
   g->block = g->plan.max_row_size >= 4096 ? 256 : 64;
-  g->lds = dg::plan_lds_bytes(g->plan);
+  // Tuning override of the block size (specialised kernels only).
+  if (const char* e = std::getenv("DIRIGO_BLOCK")) {
+    const int b = std::atoi(e);
+    if (b == 64 || b == 128 || b == 256 || b == 512 || b == 1024) g->block = b;
+  }
+  g->lds = dg::plan_lds_bytes(g->plan, g->block);
   return DG_OK;
 }
 
@@ -82,14 +98,40 @@ dg_status device_blob(const dg_graph* cg, const uint8_t** out) {
   return DG_OK;
 }
 
+// The graph's specialised kernels on the current device, compiled on first
+// use; nullptr when specialisation is off or failed (the precompiled
+// kernels then run the plan).
+const dg::JitModule* graph_jit(const dg_graph* cg) {
+  if (!dg::jit_enabled()) return nullptr;
+  dg_graph* g = const_cast<dg_graph*>(cg);
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return nullptr;
+  std::lock_guard<std::mutex> lock(g->mu);
+  DevKernels& k = g->jit[dev];
+  if (!k.tried) {
+    k.tried = true;
+    k.ok = dg::jit_load(dg::jit_enum_source(g->plan, g->block), &k.jm, &k.log) && k.jm.sizes && k.jm.fill &&
+           k.jm.enumerate;
+  }
+  return k.ok ? &k.jm : nullptr;
+}
+
+hipError_t launch_module(hipFunction_t f, int64_t n, int block, uint32_t lds, hipStream_t s, void** args) {
+  if (n <= 0) return hipSuccess;
+  return hipModuleLaunchKernel(f, (unsigned)n, 1, 1, (unsigned)block, 1, 1, lds, s, args, nullptr);
+}
+
 struct WsLayout {
-  size_t err, sums, flags, total;
+  size_t err, ticket, pair, sums, flags, total;
 };
 
+// Workspace: error word | comparison pair plan | scan tile sums | flags.
 WsLayout ws_layout(int64_t n) {
   WsLayout w;
   w.err = 0;
-  w.sums = 256;
+  w.ticket = 8;
+  w.pair = 256;
+  w.sums = (w.pair + sizeof(dgc::PairPlan) + 255) & ~size_t(255);
   w.flags = w.sums + 8 * (size_t)dgk::scan_temp_entries(n < 0 ? 0 : n);
   w.flags = (w.flags + 255) & ~size_t(255);
   w.total = w.flags + 8 * (size_t)((n < 0 ? 0 : n) + 1);
@@ -103,6 +145,8 @@ dg_status device_errors(uint32_t bits) {
   if (bits & DGP_ERR_CAPACITY)
     return set_error(DG_E_CAPACITY, "a per-location factor outgrew its compiled capacity");
   if (bits & DGP_ERR_SIZE) return set_error(DG_E_INVALID_ARG, "offsets do not match this graph and locations");
+  if (bits & DGP_ERR_TIMEOUT) return set_error(DG_E_HIP, "single pass: a predecessor's row size never arrived");
+  if (bits & DGP_ERR_BUFFER) return set_error(DG_E_BUFFER, "the rows need more entries than the output buffers hold");
   return DG_OK;
 }
 
@@ -201,6 +245,18 @@ dg_status dg_graph_info(const dg_graph* g, dg_graph_info_t* out) {
   out->lds_bytes = (int32_t)g->lds;
   out->block_threads = g->block;
   out->max_leaf_terms = g->plan.max_leaf_terms;
+  out->specialized = -1;
+  if (!dg::jit_enabled()) {
+    out->specialized = 0;
+  } else {
+    int dev = 0;
+    if (hipGetDevice(&dev) == hipSuccess) {
+      dg_graph* mg = const_cast<dg_graph*>(g);
+      std::lock_guard<std::mutex> lock(mg->mu);
+      auto it = mg->jit.find(dev);
+      if (it != mg->jit.end() && it->second.tried) out->specialized = it->second.ok ? 1 : 0;
+    }
+  }
   return DG_OK;
 }
 
@@ -237,7 +293,12 @@ dg_status dg_enumerate_sizes(const dg_graph* g, const int64_t* d_locs, int64_t n
   uint8_t* ws = static_cast<uint8_t*>(d_ws);
   uint32_t* err = reinterpret_cast<uint32_t*>(ws + w.err);
   DG_HIP(dgk::launch_zero(err, s), "zero");
-  DG_HIP(dgk::launch_sizes(blob, d_locs, n, d_offsets, err, g->block, g->lds, s), "sizes kernel");
+  if (const dg::JitModule* jm = graph_jit(g)) {
+    void* args[] = {(void*)&d_locs, &n, &d_offsets, &err};
+    DG_HIP(launch_module(jm->sizes, n, g->block, g->lds, s, args), "sizes kernel");
+  } else {
+    DG_HIP(dgk::launch_sizes(blob, d_locs, n, d_offsets, err, g->block, g->lds, s), "sizes kernel");
+  }
   DG_HIP(dgk::launch_scan(d_offsets, n, reinterpret_cast<int64_t*>(ws + w.sums), s), "scan");
   int64_t total = 0;
   uint32_t bits = 0;
@@ -264,8 +325,57 @@ dg_status dg_enumerate_fill(const dg_graph* g, const int64_t* d_locs, int64_t n,
   if (st != DG_OK) return st;
   uint32_t* err = reinterpret_cast<uint32_t*>(static_cast<uint8_t*>(d_ws) + ws_layout(n).err);
   DG_HIP(dgk::launch_zero(err, s), "zero");
-  DG_HIP(dgk::launch_fill(blob, d_locs, n, d_offsets, d_ids, d_counts, err, g->block, g->lds, s), "fill kernel");
+  if (const dg::JitModule* jm = graph_jit(g)) {
+    void* args[] = {(void*)&d_locs, &n, (void*)&d_offsets, &d_ids, &d_counts, &err};
+    DG_HIP(launch_module(jm->fill, n, g->block, g->lds, s, args), "fill kernel");
+  } else {
+    DG_HIP(dgk::launch_fill(blob, d_locs, n, d_offsets, d_ids, d_counts, err, g->block, g->lds, s), "fill kernel");
+  }
   return DG_OK;
+}
+
+dg_status dg_enumerate(const dg_graph* g, const int64_t* d_locs, int64_t n, int64_t* d_offsets, uint32_t* d_ids,
+                       uint32_t* d_counts, int64_t capacity, void* d_ws, int64_t* h_total, void* stream) {
+  if (!g || !d_offsets || !h_total || n < 0 || capacity < 0 || (n > 0 && !d_locs) ||
+      (capacity > 0 && (!d_ids || !d_counts)))
+    return set_error(DG_E_INVALID_ARG, "bad argument");
+  if (!d_ws) return set_error(DG_E_WORKSPACE, "workspace is required");
+  if (g->lds > (uint32_t)max_lds_per_block())
+    return set_error(DG_E_CAPACITY, "one location needs " + std::to_string(g->lds) + " bytes of LDS");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (n == 0) {
+    DG_HIP(dgk::launch_scan(d_offsets, 0, nullptr, s), "offsets");
+    DG_HIP(hipStreamSynchronize(s), "sync");
+    *h_total = 0;
+    return DG_OK;
+  }
+  const uint8_t* blob = nullptr;
+  dg_status st = device_blob(g, &blob);
+  if (st != DG_OK) return st;
+  WsLayout w = ws_layout(n);
+  uint8_t* ws = static_cast<uint8_t*>(d_ws);
+  uint32_t* err = reinterpret_cast<uint32_t*>(ws + w.err);
+  DG_HIP(dgk::launch_zero(err, s), "zero");
+  uint64_t* status = reinterpret_cast<uint64_t*>(ws + w.flags);
+  uint64_t* ticket = reinterpret_cast<uint64_t*>(ws + w.ticket);
+  uint64_t cap = (uint64_t)capacity;
+  if (const dg::JitModule* jm = graph_jit(g)) {
+    DG_HIP(dgk::launch_zero_u64(status, n, s), "zero status");
+    DG_HIP(dgk::launch_zero_u64(ticket, 1, s), "zero ticket");
+    void* args[] = {(void*)&d_locs, &n, &d_offsets, &d_ids, &d_counts, &cap, &status, &ticket, &err};
+    DG_HIP(launch_module(jm->enumerate, n, g->block, g->lds, s, args), "enumerate kernel");
+  } else {
+    DG_HIP(dgk::launch_enumerate(blob, d_locs, n, d_offsets, d_ids, d_counts, cap, status, ticket, err, g->block,
+                                 g->lds, s),
+           "enumerate kernel");
+  }
+  int64_t total = 0;
+  uint32_t bits = 0;
+  DG_HIP(hipMemcpyAsync(&total, d_offsets + n, sizeof(int64_t), hipMemcpyDeviceToHost, s), "copy total");
+  DG_HIP(hipMemcpyAsync(&bits, err, sizeof(uint32_t), hipMemcpyDeviceToHost, s), "copy flags");
+  DG_HIP(hipStreamSynchronize(s), "enumerate sync");
+  *h_total = total;
+  return device_errors(bits);
 }
 
 dg_status dg_compare(const dg_graph* a, const dg_graph* b, const int64_t* d_locs, int64_t n, uint8_t* d_status,
@@ -285,8 +395,11 @@ dg_status dg_compare(const dg_graph* a, const dg_graph* b, const int64_t* d_locs
     }
     if (A.tensors[A.output].shape != B.tensors[B.output].shape)
       return set_error(DG_E_SIGNATURE, "output shape differs");
+    // Comparison rows are compared in LDS, not written: one wave per
+    // location keeps its many barriers cheap.
+    const int block = 64;
     dgc::PairPlan pp;
-    dg::pair_plan(a->plan, b->plan, &pp);
+    dg::pair_plan(a->plan, b->plan, block, &pp);
     if (pp.lds_bytes > (uint32_t)max_lds_per_block())
       return set_error(DG_E_CAPACITY, "comparison needs " + std::to_string(pp.lds_bytes) + " bytes of LDS");
     hipStream_t s = static_cast<hipStream_t>(stream);
@@ -300,8 +413,11 @@ dg_status dg_compare(const dg_graph* a, const dg_graph* b, const int64_t* d_locs
     uint32_t* err = reinterpret_cast<uint32_t*>(ws + w.err);
     int64_t* flags = reinterpret_cast<int64_t*>(ws + w.flags);
     DG_HIP(dgk::launch_zero(err, s), "zero");
-    int block = std::max(a->block, b->block);
-    DG_HIP(dgk::launch_compare(ba, bb, pp, d_locs, n, d_status, flags, err, block, s), "compare kernel");
+    dgc::PairPlan* d_pp = reinterpret_cast<dgc::PairPlan*>(ws + w.pair);
+    // Pageable source: the copy has completed when the call returns.
+    DG_HIP(hipMemcpyAsync(d_pp, &pp, sizeof(pp), hipMemcpyHostToDevice, s), "copy pair plan");
+    DG_HIP(dgk::launch_compare(ba, bb, d_pp, pp.lds_bytes, d_locs, n, d_status, flags, err, block, s),
+           "compare kernel");
     DG_HIP(dgk::launch_scan(flags, n, reinterpret_cast<int64_t*>(ws + w.sums), s), "scan");
     DG_HIP(dgk::launch_scatter_mismatch(d_status, flags, n, d_mismatch, s), "scatter");
     int64_t total = 0;

@@ -574,6 +574,59 @@ Plan Compiler::run() {
   for (double b : sbound_)
     if (b > 9.2e18) fail(DG_E_OVERFLOW, "static path-count bound exceeds 2^63");
 
+  // Levels: an instruction runs one level after the latest instruction it
+  // reads; within a level the order is free.  Component sums over more than
+  // two variables get a level of their own.
+  const int nins = (int)ins_.size();
+  std::vector<int> fprod(fac_.size(), -1), sprod(sbound_.size(), -1), lev(nins, 0);
+  for (int k = 0; k < nins; ++k) {
+    const DgpInstr& I = ins_[k];
+    auto dep_f = [&](int f) {
+      if (f >= 0 && fprod[f] >= 0) lev[k] = std::max(lev[k], lev[fprod[f]] + 1);
+    };
+    auto dep_s = [&](int x) {
+      if (x >= 0 && sprod[x] >= 0) lev[k] = std::max(lev[k], lev[sprod[x]] + 1);
+    };
+    if (I.opcode == DGP_COMP) {
+      for (int q = 0; q < I.nvar; ++q) dep_f(I.var_src[q]);
+    } else if (I.opcode == DGP_LINCOMB) {
+      dep_f(I.f1);
+      dep_f(I.f2);
+      dep_s(I.k1);
+      dep_s(I.k2);
+    } else if (I.opcode == DGP_SMUL) {
+      for (int q = 0; q < I.ns; ++q) dep_s(I.s[q]);
+    } else if (I.opcode == DGP_SADD) {
+      dep_s(I.f1);
+      dep_s(I.f2);
+    }
+    if (I.dst_is_scalar) sprod[I.dst] = k;
+    else fprod[I.dst] = k;
+  }
+  int serial_vars = 0;
+  std::vector<std::pair<std::pair<int, int>, int>> order;  // ((level, serial rank), instruction)
+  for (int k = 0; k < nins; ++k) {
+    bool serial = ins_[k].opcode == DGP_COMP && ins_[k].nvar > 2;
+    if (serial) serial_vars = std::max(serial_vars, (int)ins_[k].nvar);
+    order.push_back({{lev[k], serial ? k + 1 : 0}, k});
+  }
+  std::stable_sort(order.begin(), order.end(),
+                   [](const std::pair<std::pair<int, int>, int>& a, const std::pair<std::pair<int, int>, int>& b) {
+                     return a.first < b.first;
+                   });
+  std::vector<DgpInstr> sorted;
+  std::vector<int32_t> level_start;
+  std::pair<int, int> cur{-1, -1};
+  for (auto& o : order) {
+    if (o.first != cur) {
+      level_start.push_back((int32_t)sorted.size());
+      cur = o.first;
+    }
+    sorted.push_back(ins_[o.second]);
+  }
+  level_start.push_back((int32_t)sorted.size());
+  ins_.swap(sorted);
+
   // Factor value offsets.
   int64_t fval = 0;
   for (auto& f : fac_) {
@@ -600,6 +653,8 @@ Plan Compiler::run() {
   h.max_leaf_terms = plan.max_leaf_terms;
   h.emit_entries = (int32_t)emit_entries;
   h.union_entries = (int32_t)union_entries;
+  h.nlevel = (int32_t)level_start.size() - 1;
+  h.serial_vars = serial_vars;
   size_t off = (sizeof(DgpHeader) + 15) & ~size_t(15);
   h.instr_off = (int32_t)off;
   off += ins_.size() * sizeof(DgpInstr);
@@ -612,6 +667,9 @@ Plan Compiler::run() {
   off = (off + 15) & ~size_t(15);
   h.term_off = (int32_t)off;
   off += dterms.size() * sizeof(DgpTerm);
+  off = (off + 15) & ~size_t(15);
+  h.level_off = (int32_t)off;
+  off += level_start.size() * sizeof(int32_t);
   h.blob_bytes = (int32_t)off;
   plan.blob.assign(off, 0);
   std::memcpy(plan.blob.data(), &h, sizeof(h));
@@ -619,6 +677,7 @@ Plan Compiler::run() {
   if (!fac_.empty()) std::memcpy(plan.blob.data() + h.factor_off, fac_.data(), fac_.size() * sizeof(DgpFactor));
   if (!leaves.empty()) std::memcpy(plan.blob.data() + h.leaf_off, leaves.data(), leaves.size() * sizeof(DgpLeaf));
   if (!dterms.empty()) std::memcpy(plan.blob.data() + h.term_off, dterms.data(), dterms.size() * sizeof(DgpTerm));
+  std::memcpy(plan.blob.data() + h.level_off, level_start.data(), level_start.size() * sizeof(int32_t));
   plan.max_row_size = max_row;
   plan.count_bound = cbound;
   return plan;
@@ -628,14 +687,14 @@ Plan Compiler::run() {
 
 Plan compile_plan(const GraphIR& g) { return Compiler(g).run(); }
 
-uint32_t plan_lds_bytes(const Plan& p) {
+uint32_t plan_lds_bytes(const Plan& p, int nthreads) {
   const DgpHeader& h = p.header();
-  dgc::PlanLayout PL = dgc::plan_layout(&h, 0);
+  dgc::PlanLayout PL = dgc::plan_layout(&h, dgc::vars_bytes(h.serial_vars, nthreads));
   dgc::EmitLayout E = dgc::emit_layout(PL.end, h.max_leaf_terms, h.union_entries, h.emit_entries);
   return (E.end + 15u) & ~15u;
 }
 
-void pair_plan(const Plan& a, const Plan& b, dgc::PairPlan* pp) {
+void pair_plan(const Plan& a, const Plan& b, int nthreads, dgc::PairPlan* pp) {
   const DgpHeader& ha = a.header();
   const DgpHeader& hb = b.header();
   if (ha.nleaf != hb.nleaf) fail(DG_E_SIGNATURE, "leaf count differs");
@@ -685,11 +744,84 @@ void pair_plan(const Plan& a, const Plan& b, dgc::PairPlan* pp) {
   }
   pp->union_entries = (int32_t)uni;
   pp->emit_entries = (int32_t)emit;
-  dgc::PlanLayout PA = dgc::plan_layout(&ha, 0);
+  pp->nthreads = nthreads;
+  pp->vars = dgc::vars_bytes(std::max(ha.serial_vars, hb.serial_vars), nthreads);
+  dgc::PlanLayout PA = dgc::plan_layout(&ha, pp->vars);
   pp->plan_b = dgc::align8(PA.end);
   dgc::PlanLayout PB = dgc::plan_layout(&hb, pp->plan_b);
   dgc::EmitLayout E = dgc::emit_layout(PB.end, pp->max_terms, pp->union_entries, pp->emit_entries);
   pp->lds_bytes = (E.end + 15u) & ~15u;
+}
+
+}  // namespace dg
+
+namespace dg {
+
+namespace {
+std::string fn_text(const DgpIFn& f) {
+  std::ostringstream o;
+  o << "(";
+  for (int q = 0; q < f.nterm; ++q) {
+    if (q) o << " + ";
+    o << f.coef[q] << "*v" << f.var[q];
+    if (f.vdiv[q] != 1) o << "/" << f.vdiv[q];
+  }
+  o << " + " << f.c << ")";
+  if (f.mode == 1) o << " /exact " << f.s;
+  if (f.mode == 2) o << " //" << f.s;
+  o << " in [0," << f.size << ")";
+  return o.str();
+}
+}  // namespace
+
+std::string plan_listing(const Plan& p) {
+  const DgpHeader& h = p.header();
+  const DgpInstr* ins = reinterpret_cast<const DgpInstr*>(p.blob.data() + h.instr_off);
+  const DgpFactor* fac = reinterpret_cast<const DgpFactor*>(p.blob.data() + h.factor_off);
+  const DgpLeaf* lv = reinterpret_cast<const DgpLeaf*>(p.blob.data() + h.leaf_off);
+  const DgpTerm* tm = reinterpret_cast<const DgpTerm*>(p.blob.data() + h.term_off);
+  std::ostringstream o;
+  o << "instructions " << h.ninstr << ", factors " << h.nfactor << " (" << h.fval_entries << " values), scalars "
+    << h.nscalar << "\n";
+  const int32_t* ls = reinterpret_cast<const int32_t*>(p.blob.data() + h.level_off);
+  for (int k = 0; k < h.ninstr; ++k) {
+    for (int g = 0; g < h.nlevel; ++g)
+      if (ls[g] == k) o << "-- level " << g << "\n";
+    const DgpInstr& I = ins[k];
+    std::string dst = I.dst_is_scalar ? "s" + std::to_string(I.dst)
+                                      : "f" + std::to_string(I.dst) + "[cap " + std::to_string(fac[I.dst].cap) + "]";
+    o << k << ": ";
+    switch (I.opcode) {
+      case DGP_ROOT: o << dst << " = ROOT dim " << I.a; break;
+      case DGP_CONST: o << dst << " = CONST " << I.a; break;
+      case DGP_COMP:
+        o << dst << " = COMP vars";
+        for (int q = 0; q < I.nvar; ++q) {
+          if (I.var_src[q] >= 0) o << " v" << q << "=f" << I.var_src[q];
+          else o << " v" << q << "=[" << I.wlo[q] << "," << I.whi[q] << ")";
+        }
+        for (int e = 0; e < I.npred; ++e) o << " | pred " << fn_text(I.pred[e]);
+        if (!I.dst_is_scalar) o << " | target " << fn_text(I.target);
+        break;
+      case DGP_LINCOMB:
+        o << dst << " = LINCOMB s" << I.k1 << "*" << I.c1 << "*f" << I.f1 << " + s" << I.k2 << "*" << I.c2 << "*f" << I.f2;
+        break;
+      case DGP_SMUL: o << dst << " = SMUL " << I.cst; for (int q = 0; q < I.ns; ++q) o << " *s" << I.s[q]; break;
+      case DGP_SADD: o << dst << " = SADD s" << I.f1 << "*" << I.c1 << " + s" << I.f2 << "*" << I.c2; break;
+    }
+    o << "\n";
+  }
+  for (int l = 0; l < h.nleaf; ++l) {
+    o << "leaf " << l << " rank " << lv[l].rank << " split " << lv[l].split << " terms " << lv[l].nterm << ":";
+    for (int t = 0; t < lv[l].nterm; ++t) {
+      const DgpTerm& T = tm[lv[l].term0 + t];
+      o << " [s" << T.coef_slot << "*" << T.coef_const;
+      for (int d = 0; d < lv[l].rank; ++d) o << " f" << T.factor[d];
+      o << "]";
+    }
+    o << "\n";
+  }
+  return o.str();
 }
 
 }  // namespace dg

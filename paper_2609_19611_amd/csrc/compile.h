@@ -1,6 +1,7 @@
 // Host compiler: graph IR -> per-location plan (program.h).
 #pragma once
 #include <cstdint>
+#include <string>
 #include <vector>
 
 #include "core.h"
@@ -24,11 +25,15 @@ struct Plan {
 // Failure(DG_E_OVERFLOW) if the static path-count bound exceeds 2^63.
 Plan compile_plan(const GraphIR& g);
 
-// Local data share bytes one location of this plan needs.
-uint32_t plan_lds_bytes(const Plan& p);
+// Local data share bytes one location of this plan needs with a block of
+// `nthreads` threads.
+uint32_t plan_lds_bytes(const Plan& p, int nthreads);
 
 // Combined per-leaf emission shapes and LDS layout for comparing two plans
 // location by location (same leaves in the same order).
-void pair_plan(const Plan& a, const Plan& b, dgc::PairPlan* out);
+void pair_plan(const Plan& a, const Plan& b, int nthreads, dgc::PairPlan* out);
+
+// Text listing of a plan's instructions and leaf terms.
+std::string plan_listing(const Plan& p);
 
 }  // namespace dg

@@ -14,6 +14,10 @@
 //   3. the grid is split into an outer and an inner table of (id part,
 //      count part) pairs, so that each entry costs two LDS reads, one add
 //      and one multiply before its two coalesced stores.
+//
+// Small per-thread arrays are only ever indexed with compile-time indices
+// (fully unrolled loops, select chains) so they stay in registers; values
+// that are the same for the whole block live in LDS.
 #pragma once
 #include <stdint.h>
 
@@ -25,11 +29,34 @@
 #define DGC inline
 #endif
 
+#if defined(__HIP_DEVICE_COMPILE__)
+#define DG_UNROLL _Pragma("unroll")
+#else
+#define DG_UNROLL
+#endif
+
+// Loops whose trip counts come from the compiled plan (levels,
+// instructions, leaves, terms, dims, predicates).  The kernels specialised
+// for one graph see the plan as constant data and unroll them completely;
+// the precompiled kernels leave them as loops.
+#if defined(DG_JIT)
+#define DG_PLAN_UNROLL _Pragma("unroll")
+#else
+#define DG_PLAN_UNROLL
+#endif
+
 namespace dgc {
 
 // ---------------------------------------------------------------- layout --
 struct PlanLayout {
-  uint32_t scal, fmeta, fval, end;  // byte offsets in the block's LDS area
+  uint32_t scal, fmeta, fval, fstat, end;  // byte offsets in the block's LDS area
+};
+
+// Per factor, after the plan has run: how many of its values are nonzero
+// and the largest value.
+struct FStat {
+  uint64_t nnz;
+  uint64_t vmax;
 };
 
 // Per-leaf emission view of one separable term.
@@ -38,24 +65,45 @@ struct TermRef {
   int32_t lo[DGP_MAX_RANK];
   int32_t len[DGP_MAX_RANK];
   uint32_t off[DGP_MAX_RANK];  // uint64 index of the factor's values in the LDS area
+  int32_t fid[DGP_MAX_RANK];   // factor of each dim
+};
+
+// Values shared by the block while one leaf is emitted.
+struct LeafHdr {
+  int32_t u[DGP_MAX_RANK];      // union length per dim
+  int32_t uoff[DGP_MAX_RANK];   // offset of the dim's union list
+  int32_t hlo[DGP_MAX_RANK];    // first coordinate of the dim's hull
+  int32_t dense[DGP_MAX_RANK];  // every hull coordinate is nonzero: no list, x = hlo + i
+  uint64_t cnt[DGP_MAX_RANK];   // nonzero coordinates per dim (block total)
+  uint64_t umax[DGP_MAX_RANK];  // largest factor value on the union (single term)
 };
 
 struct EmitLayout {
-  uint32_t terms;    // TermRef[max_terms]
-  uint32_t ulist;    // int32[union_entries]
-  uint32_t tables;   // uint32[emit_entries]
-  uint32_t scratch;  // uint64[2 * 64 + 8]
+  uint32_t terms;   // TermRef[max_terms]
+  uint32_t ulist;   // int32[union_entries]
+  uint32_t tables;  // uint32[emit_entries]
+  uint32_t hdr;     // LeafHdr
+  uint32_t tmax;    // uint64[2 * max_terms]: per-term largest outer / inner table value
   uint32_t end;
 };
 
 DGC uint32_t align8(uint32_t x) { return (x + 7u) & ~7u; }
+
+// Component-sum scratch at the start of the area, used by sums over more
+// than two variables: the block-uniform lower bound, length and factor
+// offset of each variable (3 x 8 words), then each thread's variable
+// values, variable-major so that a wave reads consecutive banks.
+DGC uint32_t vars_bytes(int serial_vars, int nthreads) {
+  return serial_vars > 0 ? align8(4u * (uint32_t)(3 * DGP_MAX_VARS + serial_vars * nthreads)) : 0u;
+}
 
 DGC PlanLayout plan_layout(const DgpHeader* h, uint32_t base) {
   PlanLayout L;
   L.scal = align8(base);
   L.fmeta = L.scal + 8u * (uint32_t)h->nscalar;
   L.fval = L.fmeta + 8u * (uint32_t)h->nfactor;
-  L.end = L.fval + 8u * (uint32_t)h->fval_entries;
+  L.fstat = L.fval + 8u * (uint32_t)h->fval_entries;
+  L.end = L.fstat + (uint32_t)sizeof(FStat) * (uint32_t)h->nfactor;
   return L;
 }
 
@@ -64,8 +112,9 @@ DGC EmitLayout emit_layout(uint32_t base, int32_t max_terms, int32_t union_entri
   E.terms = align8(base);
   E.ulist = E.terms + (uint32_t)sizeof(TermRef) * (uint32_t)(max_terms > 0 ? max_terms : 1);
   E.tables = align8(E.ulist + 4u * (uint32_t)union_entries);
-  E.scratch = align8(E.tables + 4u * (uint32_t)emit_entries);
-  E.end = E.scratch + 8u * (2u * 64u + 8u);
+  E.hdr = align8(E.tables + 4u * (uint32_t)emit_entries);
+  E.tmax = E.hdr + (uint32_t)sizeof(LeafHdr);
+  E.end = E.tmax + 16u * (uint32_t)(max_terms > 0 ? max_terms : 1);
   return E;
 }
 
@@ -83,13 +132,16 @@ DGC int32_t fdiv(int32_t a, int32_t b) {
   return q;
 }
 
-// Evaluates an index function at variable values v; false if an exact
-// division does not divide or the result is outside [0, size).
-DGC bool ifn_eval(const DgpIFn& f, const int32_t* v, int32_t* out) {
+// Evaluates an index function at the calling thread's variable values
+// (vt[k * nt] is variable k); false if an exact division does not divide or
+// the result is outside [0, size).
+DGC bool ifn_eval(const DgpIFn& f, const int32_t* vt, int nt, int32_t* out) {
   int32_t x = f.c;
-  for (int q = 0; q < f.nterm; ++q) {
-    int32_t vv = v[f.var[q]];
-    if (f.vdiv[q] != 1) vv = vv / f.vdiv[q];  // variables are non-negative
+  const int n = f.nterm;
+  for (int q = 0; q < n; ++q) {
+    int32_t vv = vt[f.var[q] * nt];
+    const int32_t d = f.vdiv[q];
+    if (d != 1) vv = vv / d;  // variables are non-negative
     x += f.coef[q] * vv;
   }
   if (f.mode == 1) {
@@ -102,11 +154,13 @@ DGC bool ifn_eval(const DgpIFn& f, const int32_t* v, int32_t* out) {
   return x >= 0 && x < f.size;
 }
 
-// Range of an index function over variables v in [vlo, vlo + vn).
+// Range of an index function over variables k in [vlo[k], vlo[k] + vn[k]).
 DGC void ifn_range(const DgpIFn& f, const int32_t* vlo, const int32_t* vn, int32_t* lo, int32_t* hi) {
   int32_t a = f.c, b = f.c;
-  for (int q = 0; q < f.nterm; ++q) {
-    int32_t x0 = vlo[f.var[q]], x1 = vlo[f.var[q]] + vn[f.var[q]] - 1;
+  const int n = f.nterm;
+  for (int q = 0; q < n; ++q) {
+    int32_t x0 = vlo[f.var[q]];
+    int32_t x1 = x0 + vn[f.var[q]] - 1;
     if (f.vdiv[q] != 1) {
       x0 /= f.vdiv[q];
       x1 /= f.vdiv[q];
@@ -137,151 +191,367 @@ DGC uint64_t mul_sat(uint64_t a, uint64_t b) {
 }
 
 // ------------------------------------------------------------ plan_exec --
+// Index function of a component with at most two variables (v0, v1).
+DGC bool ifn_eval2(const DgpIFn& f, int32_t v0, int32_t v1, int32_t* out) {
+  int32_t x = f.c;
+  const int n = f.nterm;
+  DG_PLAN_UNROLL
+  for (int q = 0; q < n; ++q) {
+    int32_t vv = f.var[q] == 0 ? v0 : v1;
+    const int32_t d = f.vdiv[q];
+    if (d != 1) vv = vv / d;
+    x += f.coef[q] * vv;
+  }
+  if (f.mode == 1) {
+    if (x % f.s != 0) return false;
+    x = x / f.s;
+  } else if (f.mode == 2) {
+    x = fdiv(x, f.s);
+  }
+  *out = x;
+  return x >= 0 && x < f.size;
+}
+
+DGC void ifn_range2(const DgpIFn& f, int32_t lo0, int32_t n0, int32_t lo1, int32_t n1, int32_t* lo, int32_t* hi) {
+  int32_t a = f.c, b = f.c;
+  const int n = f.nterm;
+  DG_PLAN_UNROLL
+  for (int q = 0; q < n; ++q) {
+    int32_t x0 = f.var[q] == 0 ? lo0 : lo1;
+    int32_t x1 = x0 + (f.var[q] == 0 ? n0 : n1) - 1;
+    if (f.vdiv[q] != 1) {
+      x0 /= f.vdiv[q];
+      x1 /= f.vdiv[q];
+    }
+    if (f.coef[q] >= 0) {
+      a += f.coef[q] * x0;
+      b += f.coef[q] * x1;
+    } else {
+      a += f.coef[q] * x1;
+      b += f.coef[q] * x0;
+    }
+  }
+  if (f.mode == 1) {
+    a = -fdiv(-a, f.s);
+    b = fdiv(b, f.s);
+  } else if (f.mode == 2) {
+    a = fdiv(a, f.s);
+    b = fdiv(b, f.s);
+  }
+  *lo = a;
+  *hi = b;
+}
+
+// Variable ranges of a component with at most two variables.
+struct Vars2 {
+  int32_t lo0, n0, f0, lo1, n1, f1;  // f: factor value offset, -1 for a window variable
+};
+
+DGC Vars2 vars2(const DgpInstr& I, const int32_t* meta, const DgpFactor* fac) {
+  Vars2 v;
+  v.lo0 = 0;
+  v.n0 = 1;
+  v.f0 = -1;
+  v.lo1 = 0;
+  v.n1 = 1;
+  v.f1 = -1;
+  if (I.nvar >= 1) {
+    const int s0 = I.var_src[0];
+    if (s0 >= 0) {
+      v.lo0 = meta[2 * s0];
+      v.n0 = meta[2 * s0 + 1];
+      v.f0 = fac[s0].off;
+    } else {
+      v.lo0 = I.wlo[0];
+      v.n0 = I.whi[0] - I.wlo[0];
+    }
+  }
+  if (I.nvar >= 2) {
+    const int s1 = I.var_src[1];
+    if (s1 >= 0) {
+      v.lo1 = meta[2 * s1];
+      v.n1 = meta[2 * s1 + 1];
+      v.f1 = fac[s1].off;
+    } else {
+      v.lo1 = I.wlo[1];
+      v.n1 = I.whi[1] - I.wlo[1];
+    }
+  }
+  return v;
+}
+
+// Target range of a component sum clipped to its factor (len 0 if empty).
+DGC void target_range(const DgpIFn& t, int32_t lo, int32_t hi, uint32_t P, const DgpFactor& F, int32_t* tlo,
+                      int32_t* tlen, uint32_t* err) {
+  if (lo < 0) lo = 0;
+  if (hi > F.size - 1) hi = F.size - 1;
+  int32_t len = (P == 0 || hi < lo) ? 0 : hi - lo + 1;
+  if (len > F.cap) {
+    *err |= DGP_ERR_CAPACITY;
+    len = F.cap;
+  }
+  *tlo = lo;
+  *tlen = len;
+}
+
+// Runs the compiled instructions of one location, level by level: phase 1
+// sets up every instruction of the level (factor ranges, zeroed outputs,
+// and the instructions that need no accumulation), phase 2 accumulates the
+// component sums.  One barrier ends each phase.
 template <class C>
 DGC void plan_exec(C& c, const uint8_t* blob, int64_t loc, uint8_t* area, const PlanLayout& PL, uint32_t* err) {
   const DgpHeader* h = (const DgpHeader*)blob;
   const DgpInstr* ins = (const DgpInstr*)(blob + h->instr_off);
   const DgpFactor* fac = (const DgpFactor*)(blob + h->factor_off);
+  const int32_t* level = (const int32_t*)(blob + h->level_off);
   uint64_t* scal = (uint64_t*)(area + PL.scal);
   int32_t* meta = (int32_t*)(area + PL.fmeta);
   uint64_t* fval = (uint64_t*)(area + PL.fval);
   const int tid = c.tid(), nt = c.nthreads();
-  for (int k = 0; k < h->ninstr; ++k) {
-    const DgpInstr& I = ins[k];
-    const int op = I.opcode;
-    if (op == DGP_ROOT || op == DGP_CONST) {
-      if (tid == 0) {
-        int32_t x;
-        if (op == DGP_ROOT) x = (int32_t)((loc / h->out_stride[I.a]) % h->out_shape[I.a]);
-        else x = I.a;
-        meta[2 * I.dst] = x;
-        meta[2 * I.dst + 1] = 1;
-        fval[fac[I.dst].off] = 1;
-      }
-    } else if (op == DGP_COMP) {
-      const int nv = I.nvar;
-      int32_t vlo[DGP_MAX_VARS], vn[DGP_MAX_VARS];
-      uint32_t P = 1;
-      for (int q = 0; q < nv; ++q) {
-        int src = I.var_src[q];
-        if (src >= 0) {
-          vlo[q] = meta[2 * src];
-          vn[q] = meta[2 * src + 1];
-        } else {
-          vlo[q] = I.wlo[q];
-          vn[q] = I.whi[q] - I.wlo[q];
+  // Scratch of the sums over more than two variables.
+  int32_t* vlo = (int32_t*)area;
+  int32_t* vn = vlo + DGP_MAX_VARS;
+  int32_t* foff = vn + DGP_MAX_VARS;
+  int32_t* vt = foff + DGP_MAX_VARS + tid;
+  FStat* st = (FStat*)(area + PL.fstat);
+  for (int f = tid; f < h->nfactor; f += nt) {
+    st[f].nnz = 0;
+    st[f].vmax = 0;
+  }
+  const int nlevel = h->nlevel;
+  DG_PLAN_UNROLL
+  for (int g = 0; g < nlevel; ++g) {
+    const int k0 = level[g], k1 = level[g + 1];
+    // ---- phase 1
+    DG_PLAN_UNROLL
+    for (int k = k0; k < k1; ++k) {
+      const DgpInstr& I = ins[k];
+      const int op = I.opcode;
+      if (op == DGP_COMP) {
+        if (I.nvar <= 2) {
+          const Vars2 V = vars2(I, meta, fac);
+          const uint32_t P = (uint32_t)V.n0 * (uint32_t)V.n1;
+          if (!I.dst_is_scalar) {
+            int32_t lo, hi, tlo, tlen;
+            ifn_range2(I.target, V.lo0, V.n0, V.lo1, V.n1, &lo, &hi);
+            target_range(I.target, lo, hi, P, fac[I.dst], &tlo, &tlen, err);
+            if (tid == 0) {
+              meta[2 * I.dst] = tlo;
+              meta[2 * I.dst + 1] = tlen;
+            }
+            uint64_t* dv = fval + fac[I.dst].off;
+            for (int i = tid; i < tlen; i += nt) dv[i] = 0;
+          } else if (tid == 0) {
+            scal[I.dst] = 0;
+          }
+        } else if (tid == 0) {
+          // Serial level: publish the variable ranges and the target range.
+          uint32_t P = 1;
+          for (int q = 0; q < I.nvar; ++q) {
+            const int src = I.var_src[q];
+            if (src >= 0) {
+              vlo[q] = meta[2 * src];
+              vn[q] = meta[2 * src + 1];
+              foff[q] = fac[src].off;
+            } else {
+              vlo[q] = I.wlo[q];
+              vn[q] = I.whi[q] - I.wlo[q];
+              foff[q] = -1;
+            }
+            P *= (uint32_t)vn[q];
+          }
+          if (!I.dst_is_scalar) {
+            int32_t lo, hi, tlo, tlen;
+            ifn_range(I.target, vlo, vn, &lo, &hi);
+            target_range(I.target, lo, hi, P, fac[I.dst], &tlo, &tlen, err);
+            meta[2 * I.dst] = tlo;
+            meta[2 * I.dst + 1] = tlen;
+          } else {
+            scal[I.dst] = 0;
+          }
         }
-        P *= (uint32_t)vn[q];
-      }
-      int32_t tlo = 0, tlen = 0;
-      uint64_t* dv = nullptr;
-      if (!I.dst_is_scalar) {
-        const DgpFactor F = fac[I.dst];
-        int32_t hi;
-        ifn_range(I.target, vlo, vn, &tlo, &hi);
-        if (tlo < 0) tlo = 0;
-        if (hi > F.size - 1) hi = F.size - 1;
-        tlen = (P == 0 || hi < tlo) ? 0 : hi - tlo + 1;
-        if (tlen > F.cap) {
-          *err |= DGP_ERR_CAPACITY;
-          tlen = F.cap;
-        }
-        dv = fval + F.off;
+      } else if (op == DGP_ROOT || op == DGP_CONST) {
         if (tid == 0) {
-          meta[2 * I.dst] = tlo;
-          meta[2 * I.dst + 1] = tlen;
+          int32_t x;
+          if (op == DGP_ROOT) x = (int32_t)((loc / h->out_stride[I.a]) % h->out_shape[I.a]);
+          else x = I.a;
+          meta[2 * I.dst] = x;
+          meta[2 * I.dst + 1] = 1;
+          fval[fac[I.dst].off] = 1;
         }
-        for (int i = tid; i < tlen; i += nt) dv[i] = 0;
-      } else if (tid == 0) {
-        scal[I.dst] = 0;
-      }
-      c.sync();
-      uint64_t acc = 0;
-      for (uint32_t p = (uint32_t)tid; p < P; p += (uint32_t)nt) {
-        int32_t v[DGP_MAX_VARS];
-        uint32_t rem = p;
-        uint64_t w = 1;
-        for (int q = nv - 1; q >= 0; --q) {
-          uint32_t n = (uint32_t)vn[q];
-          uint32_t r = rem % n;
-          rem /= n;
-          v[q] = vlo[q] + (int32_t)r;
-          int src = I.var_src[q];
-          if (src >= 0) w *= fval[fac[src].off + r];
-        }
-        if (w == 0) continue;
-        bool ok = true;
-        for (int e = 0; e < I.npred && ok; ++e) {
-          int32_t t;
-          ok = ifn_eval(I.pred[e], v, &t);
-        }
-        if (!ok) continue;
-        if (dv) {
-          int32_t t;
-          if (!ifn_eval(I.target, v, &t) || t < tlo || t >= tlo + tlen) continue;
-          c.atomic_add(&dv[t - tlo], w);
+      } else if (op == DGP_LINCOMB) {
+        const int32_t lo1 = meta[2 * I.f1], n1 = meta[2 * I.f1 + 1];
+        const int32_t lo2 = meta[2 * I.f2], n2 = meta[2 * I.f2 + 1];
+        const uint64_t k1s = (I.k1 < 0 ? 1ull : scal[I.k1]) * I.c1;
+        const uint64_t k2s = (I.k2 < 0 ? 1ull : scal[I.k2]) * I.c2;
+        int32_t lo, hi;
+        if (n1 == 0 && n2 == 0) {
+          lo = 0;
+          hi = 0;
+        } else if (n1 == 0) {
+          lo = lo2;
+          hi = lo2 + n2;
+        } else if (n2 == 0) {
+          lo = lo1;
+          hi = lo1 + n1;
         } else {
-          acc += w;
+          lo = lo1 < lo2 ? lo1 : lo2;
+          hi = (lo1 + n1) > (lo2 + n2) ? (lo1 + n1) : (lo2 + n2);
+        }
+        int32_t len = hi - lo;
+        const DgpFactor F = fac[I.dst];
+        if (len > F.cap) {
+          *err |= DGP_ERR_CAPACITY;
+          len = F.cap;
+        }
+        const uint64_t* a1 = fval + fac[I.f1].off;
+        const uint64_t* a2 = fval + fac[I.f2].off;
+        uint64_t* dv = fval + F.off;
+        if (tid == 0) {
+          meta[2 * I.dst] = lo;
+          meta[2 * I.dst + 1] = len;
+        }
+        for (int i = tid; i < len; i += nt) {
+          const int32_t x = lo + i;
+          uint64_t sum = 0;
+          if (x - lo1 >= 0 && x - lo1 < n1) sum += k1s * a1[x - lo1];
+          if (x - lo2 >= 0 && x - lo2 < n2) sum += k2s * a2[x - lo2];
+          dv[i] = sum;
+        }
+      } else if (op == DGP_SMUL) {
+        if (tid == 0) {
+          uint64_t v = I.cst;
+          DG_PLAN_UNROLL
+          for (int q = 0; q < I.ns; ++q) v *= scal[I.s[q]];
+          scal[I.dst] = v;
+        }
+      } else if (op == DGP_SADD) {
+        if (tid == 0) {
+          const uint64_t a = (I.f1 < 0 ? 1ull : scal[I.f1]) * I.c1;
+          const uint64_t b = (I.f2 < 0 ? 1ull : scal[I.f2]) * I.c2;
+          scal[I.dst] = a + b;
         }
       }
-      if (!dv && acc) c.atomic_add(&scal[I.dst], acc);
-    } else if (op == DGP_LINCOMB) {
-      int32_t lo1 = meta[2 * I.f1], n1 = meta[2 * I.f1 + 1];
-      int32_t lo2 = meta[2 * I.f2], n2 = meta[2 * I.f2 + 1];
-      uint64_t k1 = (I.k1 < 0 ? 1ull : scal[I.k1]) * I.c1;
-      uint64_t k2 = (I.k2 < 0 ? 1ull : scal[I.k2]) * I.c2;
-      int32_t lo, hi;
-      if (n1 == 0 && n2 == 0) {
-        lo = 0;
-        hi = 0;
-      } else if (n1 == 0) {
-        lo = lo2;
-        hi = lo2 + n2;
-      } else if (n2 == 0) {
-        lo = lo1;
-        hi = lo1 + n1;
+    }
+    c.sync();
+    // ---- phase 2
+    DG_PLAN_UNROLL
+    for (int k = k0; k < k1; ++k) {
+      const DgpInstr& I = ins[k];
+      if (I.opcode != DGP_COMP) continue;
+      const bool to_factor = !I.dst_is_scalar;
+      const int npred = I.npred;
+      uint64_t* dv = to_factor ? fval + fac[I.dst].off : nullptr;
+      int32_t tlo = 0, tlen = 0;
+      if (to_factor) {
+        tlo = meta[2 * I.dst];
+        tlen = meta[2 * I.dst + 1];
+      }
+      uint64_t acc = 0;
+      if (I.nvar <= 2) {
+        const Vars2 V = vars2(I, meta, fac);
+        const uint32_t n1 = (uint32_t)V.n1;
+        const uint32_t P = (uint32_t)V.n0 * n1;
+        for (uint32_t p = (uint32_t)tid; p < P; p += (uint32_t)nt) {
+          const uint32_t i0 = n1 == 1 ? p : p / n1;
+          const uint32_t i1 = p - i0 * n1;
+          const int32_t v0 = V.lo0 + (int32_t)i0, v1 = V.lo1 + (int32_t)i1;
+          uint64_t w = 1;
+          if (V.f0 >= 0) w = fval[V.f0 + (int32_t)i0];
+          if (V.f1 >= 0) w *= fval[V.f1 + (int32_t)i1];
+          if (w == 0) continue;
+          bool ok = true;
+          DG_PLAN_UNROLL
+          for (int e = 0; e < npred; ++e) {
+            int32_t t;
+            ok = ok && ifn_eval2(I.pred[e], v0, v1, &t);
+          }
+          if (!ok) continue;
+          if (to_factor) {
+            int32_t t;
+            if (!ifn_eval2(I.target, v0, v1, &t) || t < tlo || t >= tlo + tlen) continue;
+            c.atomic_add(&dv[t - tlo], w);
+          } else {
+            acc += w;
+          }
+        }
       } else {
-        lo = lo1 < lo2 ? lo1 : lo2;
-        hi = (lo1 + n1) > (lo2 + n2) ? (lo1 + n1) : (lo2 + n2);
+        // Serial level (the only instruction): zero the target, then sum.
+        const int nv = I.nvar;
+        if (to_factor)
+          for (int i = tid; i < tlen; i += nt) dv[i] = 0;
+        c.sync();
+        uint32_t P = 1;
+        for (int q = 0; q < nv; ++q) P *= (uint32_t)vn[q];
+        for (uint32_t p = (uint32_t)tid; p < P; p += (uint32_t)nt) {
+          uint32_t rem = p;
+          uint64_t w = 1;
+          for (int q = nv - 1; q >= 0; --q) {
+            const uint32_t n = (uint32_t)vn[q];
+            const uint32_t r = rem % n;
+            rem /= n;
+            vt[q * nt] = vlo[q] + (int32_t)r;
+            const int32_t fo = foff[q];
+            if (fo >= 0) w *= fval[fo + (int32_t)r];
+          }
+          if (w == 0) continue;
+          bool ok = true;
+          for (int e = 0; e < npred && ok; ++e) {
+            int32_t t;
+            ok = ifn_eval(I.pred[e], vt, nt, &t);
+          }
+          if (!ok) continue;
+          if (to_factor) {
+            int32_t t;
+            if (!ifn_eval(I.target, vt, nt, &t) || t < tlo || t >= tlo + tlen) continue;
+            c.atomic_add(&dv[t - tlo], w);
+          } else {
+            acc += w;
+          }
+        }
       }
-      int32_t len = hi - lo;
-      const DgpFactor F = fac[I.dst];
-      if (len > F.cap) {
-        *err |= DGP_ERR_CAPACITY;
-        len = F.cap;
-      }
-      const uint64_t* a1 = fval + fac[I.f1].off;
-      const uint64_t* a2 = fval + fac[I.f2].off;
-      uint64_t* dv = fval + F.off;
-      if (tid == 0) {
-        meta[2 * I.dst] = lo;
-        meta[2 * I.dst + 1] = len;
-      }
-      for (int i = tid; i < len; i += nt) {
-        int32_t x = lo + i;
-        uint64_t s = 0;
-        if (x - lo1 >= 0 && x - lo1 < n1) s += k1 * a1[x - lo1];
-        if (x - lo2 >= 0 && x - lo2 < n2) s += k2 * a2[x - lo2];
-        dv[i] = s;
-      }
-    } else if (op == DGP_SMUL) {
-      if (tid == 0) {
-        uint64_t v = I.cst;
-        for (int q = 0; q < I.ns; ++q) v *= scal[I.s[q]];
-        scal[I.dst] = v;
-      }
-    } else if (op == DGP_SADD) {
-      if (tid == 0) {
-        uint64_t a = (I.f1 < 0 ? 1ull : scal[I.f1]) * I.c1;
-        uint64_t b = (I.f2 < 0 ? 1ull : scal[I.f2]) * I.c2;
-        scal[I.dst] = a + b;
-      }
+      if (!to_factor && acc) c.atomic_add(&scal[I.dst], acc);
     }
     c.sync();
   }
 }
 
-// Fills TermRef[t0 .. t0 + L.nterm) for leaf `leaf` of a plan.
+// Nonzero count and largest value of every factor (after plan_exec, whose
+// last barrier also published the zeroed statistics).  A single-term leaf is
+// the outer product of its factors, so these give its entry count and its
+// largest path count without touching the leaf.
+template <class C>
+DGC void factor_stats(C& c, const uint8_t* blob, uint8_t* area, const PlanLayout& PL) {
+  const DgpHeader* h = (const DgpHeader*)blob;
+  const DgpFactor* fac = (const DgpFactor*)(blob + h->factor_off);
+  const int32_t* meta = (const int32_t*)(area + PL.fmeta);
+  const uint64_t* fval = (const uint64_t*)(area + PL.fval);
+  FStat* st = (FStat*)(area + PL.fstat);
+  const int tid = c.tid(), nt = c.nthreads();
+  const int wave_base = tid & ~63;
+  const int nf = h->nfactor;
+  DG_PLAN_UNROLL
+  for (int f = 0; f < nf; ++f) {
+    const int32_t len = meta[2 * f + 1];
+    if (wave_base >= len) continue;  // uniform per wave
+    const uint64_t* v = fval + fac[f].off;
+    uint64_t cnt = 0, mx = 0;
+    for (int32_t x = tid; x < len; x += nt) {
+      const uint64_t a = v[x];
+      cnt += a != 0 ? 1u : 0u;
+      mx = a > mx ? a : mx;
+    }
+    cnt = c.wave_sum(cnt);
+    mx = c.wave_max(mx);
+    if ((tid & 63) == 0) {
+      if (cnt) c.atomic_add(&st[f].nnz, cnt);
+      if (mx) c.atomic_max(&st[f].vmax, mx);
+    }
+  }
+  c.sync();
+}
+
+// Fills TermRef[0 .. nterm) for leaf `leaf` of a plan.
 template <class C>
 DGC void leaf_terms(C& c, const uint8_t* blob, int leaf, uint8_t* area, const PlanLayout& PL, TermRef* out) {
   const DgpHeader* h = (const DgpHeader*)blob;
@@ -290,62 +560,124 @@ DGC void leaf_terms(C& c, const uint8_t* blob, int leaf, uint8_t* area, const Pl
   const DgpFactor* fac = (const DgpFactor*)(blob + h->factor_off);
   const uint64_t* scal = (const uint64_t*)(area + PL.scal);
   const int32_t* meta = (const int32_t*)(area + PL.fmeta);
+  const int rank = L->rank;
   for (int t = c.tid(); t < L->nterm; t += c.nthreads()) {
-    TermRef r;
-    r.coef = (T[t].coef_slot < 0 ? 1ull : scal[T[t].coef_slot]) * T[t].coef_const;
-    for (int d = 0; d < L->rank; ++d) {
-      int f = T[t].factor[d];
-      r.lo[d] = meta[2 * f];
-      r.len[d] = meta[2 * f + 1];
-      r.off[d] = (PL.fval >> 3) + (uint32_t)fac[f].off;
+    TermRef* r = out + t;
+    r->coef = (T[t].coef_slot < 0 ? 1ull : scal[T[t].coef_slot]) * T[t].coef_const;
+    DG_PLAN_UNROLL
+    for (int d = 0; d < rank; ++d) {
+      const int f = T[t].factor[d];
+      r->lo[d] = meta[2 * f];
+      r->len[d] = meta[2 * f + 1];
+      r->off[d] = (PL.fval >> 3) + (uint32_t)fac[f].off;
+      r->fid[d] = f;
     }
-    out[t] = r;
   }
 }
 
 DGC uint64_t term_val(const TermRef& r, int d, int32_t x, const uint64_t* area64) {
-  int32_t i = x - r.lo[d];
+  const int32_t i = x - r.lo[d];
   return (i >= 0 && i < r.len[d]) ? area64[r.off[d] + (uint32_t)i] : 0ull;
 }
 
-// Builds the sorted union of nonzero coordinates per dim over terms [0, nterm).
-// Returns false (leaf empty) if some dim has no nonzero coordinate.
+// Hull [lo, hi) of dim d over the terms' ranges (hi <= lo if all empty).
+DGC void term_hull(const TermRef* terms, int nterm, int d, int32_t* lo, int32_t* hi) {
+  int32_t a = 0x7fffffff, b = -0x7fffffff;
+  DG_PLAN_UNROLL
+  for (int t = 0; t < nterm; ++t) {
+    const int32_t l = terms[t].lo[d], n = terms[t].len[d];
+    if (n <= 0) continue;
+    if (l < a) a = l;
+    if (l + n > b) b = l + n;
+  }
+  *lo = a;
+  *hi = b;
+}
+
+// Per dim, the union of the terms' nonzero coordinates: its size, whether it
+// is the whole hull (dense: coordinate i of the union is hlo + i) and, for
+// the other dims when `lists` is set, the sorted coordinates in `ulist`.
+// Also the largest factor value per dim (used for a single term).  Returns
+// false (leaf empty) if some dim has no nonzero coordinate.
+//
+// With `st` (a single term), the factor statistics give the counts and the
+// counting pass is skipped.
 template <class C>
 DGC bool build_union(C& c, const TermRef* terms, int nterm, int rank, const int32_t* ucap, int32_t* ulist,
-                     int32_t* u, uint8_t* area, uint32_t* err) {
+                     LeafHdr* H, bool lists, uint8_t* area, const FStat* st, uint32_t* err) {
   const uint64_t* a64 = (const uint64_t*)area;
   const int tid = c.tid(), nt = c.nthreads();
+  if (!st) {
+    for (int i = tid; i < DGP_MAX_RANK; i += nt) {
+      H->cnt[i] = 0;
+      H->umax[i] = 0;
+    }
+    c.sync();
+    // Counts: one pass over every dim, one barrier.
+    DG_PLAN_UNROLL
+    for (int d = 0; d < rank; ++d) {
+      int32_t hlo, hhi;
+      term_hull(terms, nterm, d, &hlo, &hhi);
+      uint64_t cnt = 0, vmax = 0;
+      for (int32_t x = hlo + tid; x < hhi; x += nt) {
+        bool nz = false;
+        DG_PLAN_UNROLL
+        for (int t = 0; t < nterm; ++t) {
+          const uint64_t v = term_val(terms[t], d, x, a64);
+          nz = nz || v != 0;
+          if (v > vmax) vmax = v;
+        }
+        cnt += nz ? 1u : 0u;
+      }
+      if (cnt) c.atomic_add(&H->cnt[d], cnt);
+      if (vmax) c.atomic_max(&H->umax[d], vmax);
+    }
+    c.sync();
+  }
   bool empty = false;
   int32_t base_off = 0;
+  DG_PLAN_UNROLL
   for (int d = 0; d < rank; ++d) {
-    int32_t hlo = 0x7fffffff, hhi = -0x7fffffff;
-    for (int t = 0; t < nterm; ++t) {
-      if (terms[t].len[d] <= 0) continue;
-      if (terms[t].lo[d] < hlo) hlo = terms[t].lo[d];
-      if (terms[t].lo[d] + terms[t].len[d] > hhi) hhi = terms[t].lo[d] + terms[t].len[d];
-    }
-    int32_t count = 0;
-    int32_t* ul = ulist + base_off;
-    for (int32_t chunk = hlo; chunk < hhi; chunk += nt) {
-      int32_t x = chunk + tid;
-      bool nz = false;
-      if (x < hhi)
-        for (int t = 0; t < nterm && !nz; ++t) nz = term_val(terms[t], d, x, a64) != 0;
-      uint32_t tot;
-      uint32_t pre = c.prefix(nz, &tot);
-      if (nz && count + (int32_t)pre < ucap[d]) ul[count + (int32_t)pre] = x;
-      count += (int32_t)tot;
-    }
-    if (count > ucap[d]) {
+    int32_t hlo, hhi;
+    term_hull(terms, nterm, d, &hlo, &hhi);
+    int32_t count = st ? (int32_t)st[terms[0].fid[d]].nnz : (int32_t)H->cnt[d];
+    const bool dense = count > 0 && count == hhi - hlo;
+    const int32_t cap = ucap[d];
+    if (!dense && count > cap) {
       *err |= DGP_ERR_CAPACITY;
-      count = ucap[d];
+      count = cap;
     }
-    u[d] = count;
+    if (tid == 0) {
+      H->u[d] = count;
+      H->uoff[d] = base_off;
+      H->hlo[d] = hlo;
+      H->dense[d] = dense ? 1 : 0;
+    }
     if (count == 0) empty = true;
-    base_off += ucap[d];
+    if (lists && !dense && count > 0) {
+      // Ordered compaction of the nonzero coordinates.
+      int32_t* ul = ulist + base_off;
+      int32_t done = 0;
+      for (int32_t chunk = hlo; chunk < hhi; chunk += nt) {
+        const int32_t x = chunk + tid;
+        bool nz = false;
+        if (x < hhi)
+          for (int t = 0; t < nterm && !nz; ++t) nz = term_val(terms[t], d, x, a64) != 0;
+        uint32_t tot;
+        const uint32_t pre = c.prefix(nz, &tot);
+        if (nz && done + (int32_t)pre < cap) ul[done + (int32_t)pre] = x;
+        done += (int32_t)tot;
+      }
+    }
+    base_off += cap;
   }
   c.sync();
   return !empty;
+}
+
+// Coordinate of union entry i of dim d.
+DGC int32_t ucoord(const LeafHdr* H, const int32_t* ulist, int d, int32_t i) {
+  return H->dense[d] ? H->hlo[d] + i : ulist[H->uoff[d] + i];
 }
 
 // Mode of a leaf pass.
@@ -357,6 +689,47 @@ struct LeafGeom {
   uint32_t stride[DGP_MAX_RANK];
 };
 
+// Builds one table: entries r < n over dims [d0, d1); entry = (id part,
+// count part of every term).  Records each term's largest value in tmax.
+template <class C>
+DGC void build_table(C& c, const LeafGeom& G, const TermRef* terms, int nterm, const int32_t* ulist,
+                     const LeafHdr* H, int d0, int d1, bool with_base, uint32_t n, uint32_t* tab, uint64_t* tmax,
+                     const uint64_t* a64) {
+  const int W = 1 + nterm;
+  int32_t u[DGP_MAX_RANK];
+  DG_UNROLL
+  for (int d = 0; d < DGP_MAX_RANK; ++d) u[d] = H->u[d];
+  for (uint32_t r = (uint32_t)c.tid(); r < n; r += (uint32_t)c.nthreads()) {
+    uint32_t rem = r;
+    int32_t x[DGP_MAX_RANK];
+    uint32_t pos = with_base ? G.base : 0u;
+    DG_UNROLL
+    for (int d = DGP_MAX_RANK - 1; d >= 0; --d) {
+      x[d] = 0;
+      if (d >= d0 && d < d1) {
+        const uint32_t i = rem % (uint32_t)u[d];
+        rem /= (uint32_t)u[d];
+        x[d] = ucoord(H, ulist, d, (int32_t)i);
+        pos += (uint32_t)x[d] * G.stride[d];
+      }
+    }
+    tab[(uint64_t)r * W] = pos;
+    DG_PLAN_UNROLL
+    for (int t = 0; t < nterm; ++t) {
+      uint64_t v = with_base ? terms[t].coef : 1ull;
+      DG_UNROLL
+      for (int d = 0; d < DGP_MAX_RANK; ++d)
+        if (d >= d0 && d < d1 && v) v = mul_sat(v, term_val(terms[t], d, x[d], a64));
+      tab[(uint64_t)r * W + 1 + t] = v > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)v;
+      if (v) c.atomic_max(&tmax[t], v);
+    }
+  }
+}
+
+DGC bool prod_overflows(uint64_t a, uint64_t b) {
+  return a && b && (a > 0xFFFFFFFFull || b > 0xFFFFFFFFull || a * b > 0xFFFFFFFFull);
+}
+
 // One leaf of one location.  Terms [0, na) belong to graph A (the graph
 // being enumerated), terms [na, na + nb) to graph B (compare only).
 //   EMIT_COUNT:   returns the number of nonzero entries.
@@ -365,111 +738,116 @@ struct LeafGeom {
 //   `room` bounds the entries EMIT_FILL may write at ids/cnt; a leaf that
 //   would need more raises DGP_ERR_SIZE and writes nothing past it.
 template <class C, int MODE>
-DGC uint64_t leaf_pass(C& c, const LeafGeom& G, const LeafShape& S, const TermRef* terms, int na, int nb,
-                       uint8_t* area, const EmitLayout& E, uint32_t* ids, uint32_t* cnt, uint64_t room,
-                       uint32_t* err) {
+DGC uint64_t leaf_pass(C& c, const LeafGeom& G, int split, const int32_t* ucap, const TermRef* terms, int na,
+                       int nb, uint8_t* area, const EmitLayout& E, const FStat* st, uint32_t* ids, uint32_t* cnt,
+                       uint64_t room, uint32_t* err) {
   const int tid = c.tid(), nt = c.nthreads();
   const int nterm = na + nb;
   const int rank = G.rank;
   if (MODE != EMIT_COMPARE && na == 0) return 0;
   if (MODE == EMIT_COMPARE && nterm == 0) return 0;
   int32_t* ulist = (int32_t*)(area + E.ulist);
-  int32_t u[DGP_MAX_RANK];
-  if (!build_union(c, terms, nterm, rank, S.ucap, ulist, u, area, err)) {
-    // Some dim has no nonzero coordinate in any term: the leaf is absent
-    // from both rows.
-    return 0;
-  }
+  LeafHdr* H = (LeafHdr*)(area + E.hdr);
   const uint64_t* a64 = (const uint64_t*)area;
-  int32_t uoff[DGP_MAX_RANK];
-  {
-    int32_t o = 0;
-    for (int d = 0; d < rank; ++d) {
-      uoff[d] = o;
-      o += S.ucap[d];
+  const bool single = MODE != EMIT_COMPARE && nterm == 1;
+  // A single term with a zero coefficient is identically zero.
+  if (single && terms[0].coef == 0) return 0;
+  // A single term needs no union lists to be counted, and its per-dim
+  // counts are the factor statistics.
+  if (!build_union(c, terms, nterm, rank, ucap, ulist, H, !(single && MODE == EMIT_COUNT), area,
+                   single ? st : nullptr, err))
+    return 0;
+  int32_t u[DGP_MAX_RANK];
+  DG_UNROLL
+  for (int d = 0; d < DGP_MAX_RANK; ++d) u[d] = d < rank ? H->u[d] : 1;
+
+  if (single && MODE == EMIT_COUNT) {
+    // Every cell of a single term's grid is an entry; the largest count is
+    // the coefficient times the largest value of each factor.
+    uint64_t total = 1, mx = terms[0].coef;
+    DG_UNROLL
+    for (int d = 0; d < DGP_MAX_RANK; ++d) {
+      total *= (uint64_t)u[d];
+      if (d < rank) mx = mul_sat(mx, st ? st[terms[0].fid[d]].vmax : H->umax[d]);
     }
+    if (mx > 0xFFFFFFFFull) *err |= DGP_ERR_OVERFLOW;
+    c.sync();
+    return total;
   }
-  uint64_t* scratch = (uint64_t*)(area + E.scratch);
-  const int split = S.split;
 
   if (split >= 0) {
-    // Outer table over dims [0, split), inner over [split, rank); an entry is
-    // (id part, count part per term).
+    // Outer table over dims [0, split), inner over [split, rank).
     const int W = 1 + nterm;
     uint32_t O = 1, In = 1;
-    for (int d = 0; d < split; ++d) O *= (uint32_t)u[d];
-    for (int d = split; d < rank; ++d) In *= (uint32_t)u[d];
+    DG_UNROLL
+    for (int d = 0; d < DGP_MAX_RANK; ++d) {
+      if (d < split) O *= (uint32_t)u[d];
+      else if (d < rank) In *= (uint32_t)u[d];
+    }
     uint32_t* otab = (uint32_t*)(area + E.tables);
     uint32_t* itab = otab + (uint64_t)O * W;
-    for (int i = tid; i < 2 * nterm; i += nt) scratch[i] = 0;
+    uint64_t* tmax = (uint64_t*)(area + E.tmax);
+    for (int i = tid; i < 2 * nterm; i += nt) tmax[i] = 0;
     c.sync();
-    for (int side = 0; side < 2; ++side) {
-      const int d0 = side == 0 ? 0 : split, d1 = side == 0 ? split : rank;
-      const uint32_t n = side == 0 ? O : In;
-      uint32_t* tab = side == 0 ? otab : itab;
-      for (uint32_t r = (uint32_t)tid; r < n; r += (uint32_t)nt) {
-        uint32_t rem = r;
-        int32_t x[DGP_MAX_RANK];
-        uint32_t pos = side == 0 ? G.base : 0u;
-        for (int d = d1 - 1; d >= d0; --d) {
-          uint32_t i = rem % (uint32_t)u[d];
-          rem /= (uint32_t)u[d];
-          x[d] = ulist[uoff[d] + (int32_t)i];
-          pos += (uint32_t)x[d] * G.stride[d];
-        }
-        tab[(uint64_t)r * W] = pos;
-        for (int t = 0; t < nterm; ++t) {
-          uint64_t v = side == 0 ? terms[t].coef : 1ull;
-          for (int d = d0; d < d1 && v; ++d) v = mul_sat(v, term_val(terms[t], d, x[d], a64));
-          tab[(uint64_t)r * W + 1 + t] = v > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)v;
-          if (v) c.atomic_max(&scratch[2 * t + side], v);
-        }
-      }
-    }
+    build_table(c, G, terms, nterm, ulist, H, 0, split, true, O, otab, tmax, a64);
+    build_table(c, G, terms, nterm, ulist, H, split, rank, false, In, itab, tmax + nterm, a64);
     c.sync();
     // A term whose largest outer and inner parts multiply past 32 bits has a
     // real cell with that count.
-    for (int t = tid; t < nterm; t += nt) {
-      uint64_t a = scratch[2 * t], b = scratch[2 * t + 1];
-      if (a && b && (a > 0xFFFFFFFFull || b > 0xFFFFFFFFull || a * b > 0xFFFFFFFFull)) *err |= DGP_ERR_OVERFLOW;
-    }
+    for (int t = tid; t < nterm; t += nt)
+      if (prod_overflows(tmax[t], tmax[nterm + t])) *err |= DGP_ERR_OVERFLOW;
     const uint64_t total = (uint64_t)O * In;
-    if (MODE == EMIT_COUNT && nterm == 1) return total;
     if (MODE == EMIT_FILL && nterm == 1) {
-      // Dense single-term grid: every cell is an entry, in order.
+      // Dense single-term grid: every cell is an entry, in order.  Lanes are
+      // shifted so that each wave's stores cover whole aligned 256-byte
+      // blocks of the id array.
       if (total > room) *err |= DGP_ERR_SIZE;
-      const uint32_t tot32 = (uint32_t)(total < room ? total : room);
-      const uint32_t step = (uint32_t)nt;
-      const uint32_t dr = step / In, dj = step % In;
-      uint32_t p = (uint32_t)tid;
-      uint32_t r = p / In, j = p % In;
-      for (; p < tot32; p += step) {
-        const uint32_t* o = otab + (uint64_t)r * 2;
-        const uint32_t* q = itab + (uint64_t)j * 2;
-        c.store(&ids[p], o[0] + q[0]);
-        c.store(&cnt[p], o[1] * q[1]);
-        j += dj;
-        r += dr;
-        if (j >= In) {
-          j -= In;
-          ++r;
+      const int64_t tot = (int64_t)(total < room ? total : room);
+      // (Shift by the entries that precede ids in its 256-byte block; the
+      // shift stays below the block width, so p + step >= 0 below.)
+      const int64_t head = nt >= 64 ? (int64_t)((((uintptr_t)ids) >> 2) & 63u) : 0;
+      const int64_t step = nt;
+      int64_t p = (int64_t)tid - head;
+      if (p >= 0 && p < tot) {
+        const uint32_t r = (uint32_t)(p / In), j = (uint32_t)(p % In);
+        c.store(&ids[p], otab[2 * (uint64_t)r] + itab[2 * (uint64_t)j]);
+        c.store(&cnt[p], otab[2 * (uint64_t)r + 1] * itab[2 * (uint64_t)j + 1]);
+      }
+      p += step;
+      if (p < tot) {
+        uint32_t r = (uint32_t)(p / In), j = (uint32_t)(p % In);
+        const uint32_t dr = (uint32_t)(step / In), dj = (uint32_t)(step % In);
+        for (; p < tot; p += step) {
+          const uint32_t* o = otab + 2 * (uint64_t)r;
+          const uint32_t* q = itab + 2 * (uint64_t)j;
+          c.store(&ids[p], o[0] + q[0]);
+          c.store(&cnt[p], o[1] * q[1]);
+          j += dj;
+          r += dr;
+          if (j >= In) {
+            j -= In;
+            ++r;
+          }
         }
       }
+      c.sync();
       return total;
     }
     // Several terms: evaluate each cell, keep the nonzero ones in order.
     uint64_t written = 0;
     uint32_t flags = 0;
     for (uint64_t chunk = 0; chunk < total; chunk += (uint64_t)nt) {
-      uint64_t p = chunk + (uint64_t)tid;
+      const uint64_t p = chunk + (uint64_t)tid;
       uint64_t ca = 0, cb = 0;
       uint32_t pos = 0;
       if (p < total) {
-        uint32_t r = (uint32_t)(p / In), j = (uint32_t)(p % In);
+        const uint32_t r = (uint32_t)(p / In), j = (uint32_t)(p % In);
         const uint32_t* o = otab + (uint64_t)r * W;
         const uint32_t* q = itab + (uint64_t)j * W;
         pos = o[0] + q[0];
+        DG_PLAN_UNROLL
         for (int t = 0; t < na; ++t) ca += (uint64_t)o[1 + t] * q[1 + t];
+        DG_PLAN_UNROLL
         for (int t = na; t < nterm; ++t) cb += (uint64_t)o[1 + t] * q[1 + t];
       }
       if (MODE == EMIT_COMPARE) {
@@ -478,9 +856,9 @@ DGC uint64_t leaf_pass(C& c, const LeafGeom& G, const LeafShape& S, const TermRe
         if (c.any((flags & 1u) != 0)) return 1;
       } else {
         if (ca > 0xFFFFFFFFull) *err |= DGP_ERR_OVERFLOW;
-        bool nz = ca != 0;
+        const bool nz = ca != 0;
         uint32_t tot;
-        uint32_t pre = c.prefix(nz, &tot);
+        const uint32_t pre = c.prefix(nz, &tot);
         if (MODE == EMIT_FILL && nz) {
           if (written + pre < room) {
             c.store(&ids[written + pre], pos);
@@ -493,30 +871,39 @@ DGC uint64_t leaf_pass(C& c, const LeafGeom& G, const LeafShape& S, const TermRe
       }
     }
     if (MODE == EMIT_COMPARE) return c.any((flags & 2u) != 0) ? 2 : 0;
+    c.sync();
     return written;
   }
 
   // No tables: decompose every cell of the union grid.
   uint64_t total = 1;
-  for (int d = 0; d < rank; ++d) total *= (uint64_t)u[d];
+  DG_UNROLL
+  for (int d = 0; d < DGP_MAX_RANK; ++d) total *= (uint64_t)u[d];
   uint64_t written = 0;
   uint32_t flags = 0;
   for (uint64_t chunk = 0; chunk < total; chunk += (uint64_t)nt) {
-    uint64_t p = chunk + (uint64_t)tid;
+    const uint64_t p = chunk + (uint64_t)tid;
     uint64_t ca = 0, cb = 0;
     uint32_t pos = G.base;
     if (p < total) {
       int32_t x[DGP_MAX_RANK];
       uint64_t rem = p;
-      for (int d = rank - 1; d >= 0; --d) {
-        uint64_t i = rem % (uint64_t)u[d];
-        rem /= (uint64_t)u[d];
-        x[d] = ulist[uoff[d] + (int32_t)i];
-        pos += (uint32_t)x[d] * G.stride[d];
+      DG_UNROLL
+      for (int d = DGP_MAX_RANK - 1; d >= 0; --d) {
+        x[d] = 0;
+        if (d < rank) {
+          const uint64_t i = rem % (uint64_t)u[d];
+          rem /= (uint64_t)u[d];
+          x[d] = ucoord(H, ulist, d, (int32_t)i);
+          pos += (uint32_t)x[d] * G.stride[d];
+        }
       }
+      DG_PLAN_UNROLL
       for (int t = 0; t < nterm; ++t) {
         uint64_t v = terms[t].coef;
-        for (int d = 0; d < rank && v; ++d) v = mul_sat(v, term_val(terms[t], d, x[d], a64));
+        DG_UNROLL
+        for (int d = 0; d < DGP_MAX_RANK; ++d)
+          if (d < rank && v) v = mul_sat(v, term_val(terms[t], d, x[d], a64));
         if (t < na) ca = (ca + v < ca) ? ~0ull : ca + v;
         else cb = (cb + v < cb) ? ~0ull : cb + v;
       }
@@ -527,9 +914,9 @@ DGC uint64_t leaf_pass(C& c, const LeafGeom& G, const LeafShape& S, const TermRe
       if (c.any((flags & 1u) != 0)) return 1;
     } else {
       if (ca > 0xFFFFFFFFull) *err |= DGP_ERR_OVERFLOW;
-      bool nz = ca != 0;
+      const bool nz = ca != 0;
       uint32_t tot;
-      uint32_t pre = c.prefix(nz, &tot);
+      const uint32_t pre = c.prefix(nz, &tot);
       if (MODE == EMIT_FILL && nz) {
         if (written + pre < room) {
           c.store(&ids[written + pre], pos);
@@ -542,6 +929,7 @@ DGC uint64_t leaf_pass(C& c, const LeafGeom& G, const LeafShape& S, const TermRe
     }
   }
   if (MODE == EMIT_COMPARE) return c.any((flags & 2u) != 0) ? 2 : 0;
+  c.sync();
   return written;
 }
 
@@ -549,15 +937,69 @@ DGC LeafGeom leaf_geom(const DgpLeaf& L) {
   LeafGeom G;
   G.rank = L.rank;
   G.base = L.base;
+  DG_UNROLL
   for (int d = 0; d < DGP_MAX_RANK; ++d) G.stride[d] = d < L.rank ? L.stride[d] : 0u;
   return G;
 }
 
-DGC LeafShape leaf_shape(const DgpLeaf& L) {
-  LeafShape S;
-  S.split = L.split;
-  for (int d = 0; d < DGP_MAX_RANK; ++d) S.ucap[d] = d < L.rank ? L.ucap[d] : 1;
-  return S;
+// Runs the plan of one location; false (and DGP_ERR_RANGE) if the location
+// lies outside the output.
+template <class C>
+DGC bool location_plan(C& c, const uint8_t* blob, int64_t loc, uint8_t* area, uint32_t* err) {
+  const DgpHeader* h = (const DgpHeader*)blob;
+  if (loc < 0 || loc >= h->out_numel) {
+    *err |= DGP_ERR_RANGE;
+    return false;
+  }
+  const PlanLayout PL = plan_layout(h, vars_bytes(h->serial_vars, c.nthreads()));
+  plan_exec(c, blob, loc, area, PL, err);
+  factor_stats(c, blob, area, PL);
+  return true;
+}
+
+// Leaf passes over a plan already in LDS: the row size (EMIT_COUNT) or the
+// row itself (EMIT_FILL, at most `room` entries written at ids/cnt).
+template <class C, int MODE>
+DGC uint64_t location_leaves(C& c, const uint8_t* blob, uint8_t* area, uint32_t* ids, uint32_t* cnt, uint64_t room,
+                             uint32_t* err) {
+  const DgpHeader* h = (const DgpHeader*)blob;
+  const PlanLayout PL = plan_layout(h, vars_bytes(h->serial_vars, c.nthreads()));
+  const EmitLayout E = emit_layout(PL.end, h->max_leaf_terms, h->union_entries, h->emit_entries);
+  const DgpLeaf* leaves = (const DgpLeaf*)(blob + h->leaf_off);
+  const DgpTerm* T0 = (const DgpTerm*)(blob + h->term_off);
+  const uint64_t* scal = (const uint64_t*)(area + PL.scal);
+  const FStat* st = (const FStat*)(area + PL.fstat);
+  TermRef* terms = (TermRef*)(area + E.terms);
+  uint64_t off = 0;
+  const int nleaf = h->nleaf;
+  DG_PLAN_UNROLL
+  for (int l = 0; l < nleaf; ++l) {
+    const DgpLeaf& L = leaves[l];
+    if (L.nterm == 0) continue;
+    if (MODE == EMIT_COUNT && L.nterm == 1) {
+      // Entry count of a single term: the product of its factors' nonzero
+      // counts (every thread computes it from the statistics, no barrier).
+      const DgpTerm& T = T0[L.term0];
+      const uint64_t coef = (T.coef_slot < 0 ? 1ull : scal[T.coef_slot]) * T.coef_const;
+      if (coef == 0) continue;
+      uint64_t n = 1, mx = coef;
+      DG_PLAN_UNROLL
+      for (int d = 0; d < L.rank; ++d) {
+        n *= st[T.factor[d]].nnz;
+        mx = mul_sat(mx, st[T.factor[d]].vmax);
+      }
+      if (n && mx > 0xFFFFFFFFull) *err |= DGP_ERR_OVERFLOW;
+      off += n;
+      continue;
+    }
+    leaf_terms(c, blob, l, area, PL, terms);
+    c.sync();
+    off += leaf_pass<C, MODE>(c, leaf_geom(L), L.split, L.ucap, terms, L.nterm, 0, area, E, st,
+                               ids ? ids + off : nullptr, cnt ? cnt + off : nullptr, off < room ? room - off : 0,
+                               err);
+    c.sync();
+  }
+  return off;
 }
 
 // Row size (EMIT_COUNT) or row contents (EMIT_FILL, at most `room` entries
@@ -565,28 +1007,8 @@ DGC LeafShape leaf_shape(const DgpLeaf& L) {
 template <class C, int MODE>
 DGC uint64_t location_row(C& c, const uint8_t* blob, int64_t loc, uint8_t* area, uint32_t* ids, uint32_t* cnt,
                           uint64_t room, uint32_t* err) {
-  const DgpHeader* h = (const DgpHeader*)blob;
-  if (loc < 0 || loc >= h->out_numel) {
-    *err |= DGP_ERR_RANGE;
-    return 0;
-  }
-  const PlanLayout PL = plan_layout(h, 0);
-  const EmitLayout E = emit_layout(PL.end, h->max_leaf_terms, h->union_entries, h->emit_entries);
-  plan_exec(c, blob, loc, area, PL, err);
-  const DgpLeaf* leaves = (const DgpLeaf*)(blob + h->leaf_off);
-  TermRef* terms = (TermRef*)(area + E.terms);
-  uint64_t off = 0;
-  for (int l = 0; l < h->nleaf; ++l) {
-    const DgpLeaf L = leaves[l];
-    if (L.nterm == 0) continue;
-    leaf_terms(c, blob, l, area, PL, terms);
-    c.sync();
-    off += leaf_pass<C, MODE>(c, leaf_geom(L), leaf_shape(L), terms, L.nterm, 0, area, E,
-                               ids ? ids + off : nullptr, cnt ? cnt + off : nullptr, off < room ? room - off : 0,
-                               err);
-    c.sync();
-  }
-  return off;
+  if (!location_plan(c, blob, loc, area, err)) return 0;
+  return location_leaves<C, MODE>(c, blob, area, ids, cnt, room, err);
 }
 
 // Per-leaf combined emission shapes of a two-graph comparison.
@@ -595,13 +1017,16 @@ struct PairPlan {
   int32_t max_terms;
   int32_t union_entries;
   int32_t emit_entries;
-  uint32_t plan_b;  // byte offset of graph B's plan area
+  uint32_t plan_b;  // byte offset of graph B's plan area (for `nthreads`)
+  int32_t nthreads;
+  uint32_t vars;    // bytes of component-sum scratch before graph A's plan area
   uint32_t lds_bytes;
   LeafShape leaf[16];
 };
 
+// PP lives in global memory (the kernels read it from the workspace).
 template <class C>
-DGC uint32_t location_compare(C& c, const uint8_t* blob_a, const uint8_t* blob_b, const PairPlan& PP, int64_t loc,
+DGC uint32_t location_compare(C& c, const uint8_t* blob_a, const uint8_t* blob_b, const PairPlan* PP, int64_t loc,
                               uint8_t* area, uint32_t* err) {
   const DgpHeader* ha = (const DgpHeader*)blob_a;
   const DgpHeader* hb = (const DgpHeader*)blob_b;
@@ -609,23 +1034,25 @@ DGC uint32_t location_compare(C& c, const uint8_t* blob_a, const uint8_t* blob_b
     *err |= DGP_ERR_RANGE;
     return 0;
   }
-  const PlanLayout PA = plan_layout(ha, 0);
-  const PlanLayout PB = plan_layout(hb, PP.plan_b);
-  const EmitLayout E = emit_layout(PB.end, PP.max_terms, PP.union_entries, PP.emit_entries);
+  const PlanLayout PA = plan_layout(ha, PP->vars);
+  const PlanLayout PB = plan_layout(hb, PP->plan_b);
+  const EmitLayout E = emit_layout(PB.end, PP->max_terms, PP->union_entries, PP->emit_entries);
   plan_exec(c, blob_a, loc, area, PA, err);
   plan_exec(c, blob_b, loc, area, PB, err);
   const DgpLeaf* la = (const DgpLeaf*)(blob_a + ha->leaf_off);
   const DgpLeaf* lb = (const DgpLeaf*)(blob_b + hb->leaf_off);
   TermRef* terms = (TermRef*)(area + E.terms);
   uint32_t status = 0;
-  for (int l = 0; l < PP.nleaf; ++l) {
-    const DgpLeaf A = la[l], B = lb[l];
-    if (A.nterm + B.nterm == 0) continue;
+  const int nleaf = PP->nleaf;
+  for (int l = 0; l < nleaf; ++l) {
+    const int na = la[l].nterm, nb = lb[l].nterm;
+    if (na + nb == 0) continue;
     leaf_terms(c, blob_a, l, area, PA, terms);
-    leaf_terms(c, blob_b, l, area, PB, terms + A.nterm);
+    leaf_terms(c, blob_b, l, area, PB, terms + na);
     c.sync();
-    uint32_t s = (uint32_t)leaf_pass<C, EMIT_COMPARE>(c, leaf_geom(A), PP.leaf[l], terms, A.nterm, B.nterm, area,
-                                                      E, nullptr, nullptr, 0, err);
+    const uint32_t s = (uint32_t)leaf_pass<C, EMIT_COMPARE>(c, leaf_geom(la[l]), PP->leaf[l].split,
+                                                            PP->leaf[l].ucap, terms, na, nb, area, E, nullptr,
+                                                            nullptr, nullptr, 0, err);
     c.sync();
     if (s == 1) return 1;
     if (s == 2) status = 2;

@@ -14,6 +14,7 @@
 #include "compile.h"
 #include "core.h"
 #include "graph.h"
+#include "jit.h"
 
 namespace {
 
@@ -31,6 +32,8 @@ struct HostCtx {
     return 0u;
   }
   bool any(bool f) const { return f; }
+  uint64_t wave_sum(uint64_t v) const { return v; }
+  uint64_t wave_max(uint64_t v) const { return v; }
 };
 
 thread_local std::string g_err;
@@ -59,7 +62,7 @@ int dgh_sizes(const char* text, int64_t len, const int64_t* locs, int64_t n, int
   try {
     dg::GraphIR ir = dg::parse_dgir(std::string(text, (size_t)len));
     dg::Plan plan = dg::compile_plan(ir);
-    std::vector<uint64_t> area((dg::plan_lds_bytes(plan) + 7) / 8 + 1);
+    std::vector<uint64_t> area((dg::plan_lds_bytes(plan, 1) + 7) / 8 + 1);
     HostCtx c;
     uint32_t err = 0;
     offsets[0] = 0;
@@ -81,7 +84,7 @@ int dgh_fill(const char* text, int64_t len, const int64_t* locs, int64_t n, cons
   try {
     dg::GraphIR ir = dg::parse_dgir(std::string(text, (size_t)len));
     dg::Plan plan = dg::compile_plan(ir);
-    std::vector<uint64_t> area((dg::plan_lds_bytes(plan) + 7) / 8 + 1);
+    std::vector<uint64_t> area((dg::plan_lds_bytes(plan, 1) + 7) / 8 + 1);
     HostCtx c;
     uint32_t err = 0;
     for (int64_t i = 0; i < n; ++i) {
@@ -105,16 +108,42 @@ int dgh_compare(const char* ta, int64_t la, const char* tb, int64_t lb, const in
     dg::GraphIR ib = dg::parse_dgir(std::string(tb, (size_t)lb));
     dg::Plan pa = dg::compile_plan(ia), pb = dg::compile_plan(ib);
     dgc::PairPlan pp;
-    dg::pair_plan(pa, pb, &pp);
+    dg::pair_plan(pa, pb, 1, &pp);
     std::vector<uint64_t> area(pp.lds_bytes / 8 + 1);
     HostCtx c;
     uint32_t err = 0;
     for (int64_t i = 0; i < n; ++i) {
       std::memset(area.data(), 0x33, area.size() * 8);
-      status[i] = (uint8_t)dgc::location_compare(c, pa.blob.data(), pb.blob.data(), pp, locs[i],
+      status[i] = (uint8_t)dgc::location_compare(c, pa.blob.data(), pb.blob.data(), &pp, locs[i],
                                                  reinterpret_cast<uint8_t*>(area.data()), &err);
     }
     return bits_status(err);
+  } catch (const dg::Failure& e) {
+    return fail_with(e);
+  }
+}
+
+// Source of the specialised kernels of a graph (for tests and tuning).
+int dgh_jit_source(const char* text, int64_t len, int block, char* out, int64_t cap) {
+  try {
+    dg::GraphIR ir = dg::parse_dgir(std::string(text, (size_t)len));
+    dg::Plan plan = dg::compile_plan(ir);
+    std::string s = dg::jit_enum_source(plan, block);
+    snprintf(out, (size_t)cap, "%s", s.c_str());
+    return (int)s.size();
+  } catch (const dg::Failure& e) {
+    return fail_with(e);
+  }
+}
+
+// Human-readable listing of a graph's compiled plan (for tests and tuning).
+int dgh_dump(const char* text, int64_t len, char* out, int64_t cap) {
+  try {
+    dg::GraphIR ir = dg::parse_dgir(std::string(text, (size_t)len));
+    dg::Plan plan = dg::compile_plan(ir);
+    std::string s = dg::plan_listing(plan);
+    snprintf(out, (size_t)cap, "%s", s.c_str());
+    return (int)s.size();
   } catch (const dg::Failure& e) {
     return fail_with(e);
   }

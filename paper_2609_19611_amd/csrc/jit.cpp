@@ -1,0 +1,121 @@
+// Run-time specialisation of the per-location kernels (see jit.h).
+#include "jit.h"
+
+#include <hip/hiprtc.h>
+
+#include <cstdlib>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <sstream>
+
+namespace dg {
+
+// Text of program.h, core.h and kernels_dev.h, embedded at build time.
+extern const char* const kJitProgramH;
+extern const char* const kJitCoreH;
+extern const char* const kJitKernelsDevH;
+
+namespace {
+
+std::mutex g_mu;
+std::map<std::string, std::vector<char>> g_code;                    // source -> code object
+std::map<std::pair<int, std::string>, hipModule_t> g_modules;       // (device, source) -> module
+
+bool compile(const std::string& src, std::vector<char>* code, std::string* log) {
+  hiprtcProgram prog;
+  const char* headers[] = {kJitProgramH, kJitCoreH, kJitKernelsDevH};
+  const char* names[] = {"program.h", "core.h", "kernels_dev.h"};
+  if (hiprtcCreateProgram(&prog, src.c_str(), "dg_plan.hip", 3, headers, names) != HIPRTC_SUCCESS) {
+    *log = "hiprtcCreateProgram failed";
+    return false;
+  }
+  // Same code-generation footing as the precompiled kernels: packed FP32
+  // instructions stay off.
+  const char* opts[] = {"--offload-arch=gfx950", "-O3",     "-std=c++17",      "-mllvm",
+                        "-amdgpu-early-inline-all=true",   "-Wno-pass-failed", "-Xclang",
+                        "-target-feature",                 "-Xclang",          "-packed-fp32-ops"};
+  hiprtcResult r = hiprtcCompileProgram(prog, (int)(sizeof(opts) / sizeof(opts[0])), opts);
+  size_t n = 0;
+  hiprtcGetProgramLogSize(prog, &n);
+  if (n > 1) {
+    std::string l(n, '\0');
+    hiprtcGetProgramLog(prog, &l[0]);
+    *log = l;
+  }
+  if (r != HIPRTC_SUCCESS) {
+    hiprtcDestroyProgram(&prog);
+    return false;
+  }
+  size_t sz = 0;
+  hiprtcGetCodeSize(prog, &sz);
+  code->resize(sz);
+  hiprtcGetCode(prog, code->data());
+  hiprtcDestroyProgram(&prog);
+  return true;
+}
+
+}  // namespace
+
+bool jit_enabled() {
+  const char* e = std::getenv("DIRIGO_JIT");
+  return !(e && std::strcmp(e, "0") == 0);
+}
+
+bool jit_load(const std::string& source, JitModule* out, std::string* log) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    *log = "hipGetDevice failed";
+    return false;
+  }
+  std::vector<char> code;
+  {
+    std::lock_guard<std::mutex> lock(g_mu);
+    auto mit = g_modules.find({dev, source});
+    if (mit != g_modules.end()) {
+      out->mod = mit->second;
+    } else {
+      auto it = g_code.find(source);
+      if (it != g_code.end()) code = it->second;
+    }
+  }
+  if (!out->mod) {
+    if (code.empty()) {
+      if (!compile(source, &code, log)) return false;
+      std::lock_guard<std::mutex> lock(g_mu);
+      g_code[source] = code;
+    }
+    hipModule_t m = nullptr;
+    hipError_t e = hipModuleLoadData(&m, code.data());
+    if (e != hipSuccess) {
+      *log = std::string("hipModuleLoadData: ") + hipGetErrorString(e);
+      return false;
+    }
+    std::lock_guard<std::mutex> lock(g_mu);
+    auto mit = g_modules.find({dev, source});
+    if (mit != g_modules.end()) {
+      (void)hipModuleUnload(m);
+      out->mod = mit->second;
+    } else {
+      g_modules[{dev, source}] = m;
+      out->mod = m;
+    }
+  }
+  // A module holds either the enumeration kernels or the comparison kernel;
+  // a name it lacks leaves a null function.  The failed lookup also sets
+  // the thread's last HIP error, which is cleared here so that it is not
+  // reported by the next launch check.
+  auto get = [&](const char* name, hipFunction_t* f) {
+    if (hipModuleGetFunction(f, out->mod, name) != hipSuccess) {
+      *f = nullptr;
+      (void)hipGetLastError();
+    }
+  };
+  get("dg_sizes", &out->sizes);
+  get("dg_fill", &out->fill);
+  get("dg_enumerate", &out->enumerate);
+  get("dg_compare", &out->compare);
+  return true;
+}
+
+}  // namespace dg

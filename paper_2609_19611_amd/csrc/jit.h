@@ -1,0 +1,45 @@
+// Per-graph specialised kernels, compiled at run time with hipRTC.
+//
+// The compiled plan of a graph (or of a pair of graphs for a comparison) is
+// written into a small HIP source as __constant__ data and the kernel bodies
+// of kernels_dev.h are instantiated against it, so every instruction field,
+// op dispatch and trip count is a compile-time constant.  Code objects are
+// cached per process by source text; modules are loaded per device.
+#pragma once
+
+#include <cstdint>
+#include <memory>
+#include <string>
+#include <vector>
+
+#include "compile.h"
+
+namespace dg {
+
+// Source of the specialised enumeration kernels (dg_sizes, dg_fill,
+// dg_enumerate) of one plan for blocks of `block` threads.
+std::string jit_enum_source(const Plan& p, int block);
+// Source of the specialised comparison kernel (dg_compare) of a pair.
+std::string jit_compare_source(const Plan& a, const Plan& b, const dgc::PairPlan& pp, int block);
+
+}  // namespace dg
+
+#if defined(__HIP_PLATFORM_AMD__) || defined(__HIPCC__)
+#include <hip/hip_runtime.h>
+
+namespace dg {
+
+// Compiles (or takes from the cache) and loads on the current device.
+// Returns true and the module; on failure a message in *log.
+struct JitModule {
+  hipModule_t mod = nullptr;
+  hipFunction_t sizes = nullptr, fill = nullptr, enumerate = nullptr, compare = nullptr;
+};
+bool jit_load(const std::string& source, JitModule* out, std::string* log);
+
+// Whether run-time specialisation is enabled (environment DIRIGO_JIT=0
+// turns it off; the precompiled kernels then run every graph).
+bool jit_enabled();
+
+}  // namespace dg
+#endif

@@ -1,0 +1,64 @@
+// Sources of the per-graph specialised kernels (see jit.h).  Host-only
+// code: no HIP runtime calls.
+#include <cstring>
+#include <sstream>
+
+#include "jit.h"
+
+namespace dg {
+
+namespace {
+
+void emit_bytes(std::ostringstream& o, const char* name, const std::vector<uint8_t>& b) {
+  o << "static __constant__ __attribute__((aligned(16))) const unsigned char " << name << "[" << b.size()
+    << "] = {";
+  for (size_t i = 0; i < b.size(); ++i) {
+    if (i % 32 == 0) o << "\n";
+    o << (unsigned)b[i] << ",";
+  }
+  o << "};\n";
+}
+
+const char* kPrelude =
+    "#define DG_JIT 1\n"
+    "#define DGC __device__ __forceinline__\n"
+    "#include \"kernels_dev.h\"\n";
+
+}  // namespace
+
+std::string jit_enum_source(const Plan& p, int block) {
+  std::ostringstream o;
+  o << kPrelude;
+  emit_bytes(o, "dg_plan", p.blob);
+  o << "#define DG_B " << block << "\n"
+    << "extern \"C\" __global__ __launch_bounds__(DG_B) void dg_sizes(const int64_t* __restrict__ locs, int64_t n,\n"
+    << "    int64_t* __restrict__ offsets, uint32_t* __restrict__ err) {\n"
+    << "  dgk_dev::sizes_body<DG_B>(dg_plan, locs, n, offsets, err);\n}\n"
+    << "extern \"C\" __global__ __launch_bounds__(DG_B) void dg_fill(const int64_t* __restrict__ locs, int64_t n,\n"
+    << "    const int64_t* __restrict__ offsets, uint32_t* __restrict__ ids, uint32_t* __restrict__ cnt,\n"
+    << "    uint32_t* __restrict__ err) {\n"
+    << "  dgk_dev::fill_body<DG_B>(dg_plan, locs, n, offsets, ids, cnt, err);\n}\n"
+    << "extern \"C\" __global__ __launch_bounds__(DG_B) void dg_enumerate(const int64_t* __restrict__ locs, int64_t n,\n"
+    << "    int64_t* __restrict__ offsets, uint32_t* __restrict__ ids, uint32_t* __restrict__ cnt, uint64_t capacity,\n"
+    << "    uint64_t* __restrict__ status, unsigned long long* __restrict__ ticket, uint32_t* __restrict__ err) {\n"
+    << "  dgk_dev::enumerate_body<DG_B>(dg_plan, locs, n, offsets, ids, cnt, capacity, status, ticket, err);\n}\n";
+  return o.str();
+}
+
+std::string jit_compare_source(const Plan& a, const Plan& b, const dgc::PairPlan& pp, int block) {
+  std::ostringstream o;
+  o << kPrelude;
+  emit_bytes(o, "dg_plan_a", a.blob);
+  emit_bytes(o, "dg_plan_b", b.blob);
+  std::vector<uint8_t> ppb(sizeof(pp));
+  std::memcpy(ppb.data(), &pp, sizeof(pp));
+  emit_bytes(o, "dg_pair", ppb);
+  o << "#define DG_B " << block << "\n"
+    << "extern \"C\" __global__ __launch_bounds__(DG_B) void dg_compare(const int64_t* __restrict__ locs, int64_t n,\n"
+    << "    uint8_t* __restrict__ status, int64_t* __restrict__ flags, uint32_t* __restrict__ err) {\n"
+    << "  dgk_dev::compare_body<DG_B>(dg_plan_a, dg_plan_b, (const dgc::PairPlan*)dg_pair, locs, n, status, flags,"
+       " err);\n}\n";
+  return o.str();
+}
+
+}  // namespace dg

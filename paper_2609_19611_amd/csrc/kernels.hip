@@ -5,67 +5,17 @@
 #include <stdint.h>
 
 #define DGC __device__ __forceinline__
-#include "core.h"
+#include "kernels_dev.h"
 #include "kernels.h"
 
 namespace {
 
-// Block context for core.h: BLOCK threads cooperating on one location.
-template <int BLOCK>
-struct DevCtx {
-  uint32_t* wsum;  // LDS, BLOCK / 64 words
-  DGC int tid() const { return (int)threadIdx.x; }
-  DGC int nthreads() const { return BLOCK; }
-  DGC void sync() const { __syncthreads(); }
-  DGC void atomic_add(uint64_t* p, uint64_t v) const {
-    atomicAdd(reinterpret_cast<unsigned long long*>(p), (unsigned long long)v);
-  }
-  DGC void atomic_max(uint64_t* p, uint64_t v) const {
-    atomicMax(reinterpret_cast<unsigned long long*>(p), (unsigned long long)v);
-  }
-  DGC void store(uint32_t* p, uint32_t v) const { __builtin_nontemporal_store(v, p); }
-  // Exclusive count of set flags among lower threads of the block, and the
-  // block total.  Ends with every thread past a barrier.
-  DGC uint32_t prefix(bool f, uint32_t* total) const {
-    const uint64_t m = __ballot(f);
-    const uint32_t lane = threadIdx.x & 63u;
-    const uint32_t pre = (uint32_t)__popcll(m & ((1ull << lane) - 1ull));
-    if (BLOCK == 64) {
-      *total = (uint32_t)__popcll(m);
-      return pre;
-    }
-    const uint32_t wave = threadIdx.x >> 6;
-    __syncthreads();
-    if (lane == 0) wsum[wave] = (uint32_t)__popcll(m);
-    __syncthreads();
-    uint32_t before = 0, tot = 0;
-#pragma unroll
-    for (int w = 0; w < BLOCK / 64; ++w) {
-      uint32_t x = wsum[w];
-      before += (w < (int)wave) ? x : 0u;
-      tot += x;
-    }
-    *total = tot;
-    return before + pre;
-  }
-  DGC bool any(bool f) const { return __syncthreads_or(f) != 0; }
-};
-
-extern __shared__ uint64_t dg_smem[];
+using dgk_dev::DevCtx;
 
 template <int BLOCK>
 __global__ __launch_bounds__(BLOCK) void k_sizes(const uint8_t* __restrict__ blob, const int64_t* __restrict__ locs,
                                                  int64_t n, int64_t* __restrict__ offsets, uint32_t* __restrict__ err) {
-  __shared__ uint32_t wsum[BLOCK / 64];
-  const int64_t i = blockIdx.x;
-  if (i >= n) return;
-  DevCtx<BLOCK> c{wsum};
-  uint32_t e = 0;
-  uint8_t* area = reinterpret_cast<uint8_t*>(dg_smem);
-  const uint64_t rows =
-      dgc::location_row<DevCtx<BLOCK>, dgc::EMIT_COUNT>(c, blob, locs[i], area, nullptr, nullptr, 0, &e);
-  if (threadIdx.x == 0) offsets[i + 1] = (int64_t)rows;
-  if (e) atomicOr(err, e);
+  dgk_dev::sizes_body<BLOCK>(blob, locs, n, offsets, err);
 }
 
 template <int BLOCK>
@@ -73,39 +23,33 @@ __global__ __launch_bounds__(BLOCK) void k_fill(const uint8_t* __restrict__ blob
                                                 int64_t n, const int64_t* __restrict__ offsets,
                                                 uint32_t* __restrict__ ids, uint32_t* __restrict__ cnt,
                                                 uint32_t* __restrict__ err) {
-  __shared__ uint32_t wsum[BLOCK / 64];
-  const int64_t i = blockIdx.x;
-  if (i >= n) return;
-  DevCtx<BLOCK> c{wsum};
-  uint32_t e = 0;
-  uint8_t* area = reinterpret_cast<uint8_t*>(dg_smem);
-  const int64_t start = offsets[i];
-  const int64_t room = offsets[i + 1] - start;
-  // Writes stay inside [offsets[i], offsets[i+1]) whatever this row's size.
-  const uint64_t rows = dgc::location_row<DevCtx<BLOCK>, dgc::EMIT_FILL>(
-      c, blob, locs[i], area, ids + start, cnt + start, room > 0 ? (uint64_t)room : 0ull, &e);
-  if (threadIdx.x == 0 && (int64_t)rows != room) e |= DGP_ERR_SIZE;
-  if (e) atomicOr(err, e);
+  dgk_dev::fill_body<BLOCK>(blob, locs, n, offsets, ids, cnt, err);
 }
 
 template <int BLOCK>
 __global__ __launch_bounds__(BLOCK) void k_compare(const uint8_t* __restrict__ blob_a,
-                                                   const uint8_t* __restrict__ blob_b, dgc::PairPlan pp,
+                                                   const uint8_t* __restrict__ blob_b,
+                                                   const dgc::PairPlan* __restrict__ pp,
                                                    const int64_t* __restrict__ locs, int64_t n,
                                                    uint8_t* __restrict__ status, int64_t* __restrict__ flags,
                                                    uint32_t* __restrict__ err) {
-  __shared__ uint32_t wsum[BLOCK / 64];
-  const int64_t i = blockIdx.x;
-  if (i >= n) return;
-  DevCtx<BLOCK> c{wsum};
-  uint32_t e = 0;
-  uint8_t* area = reinterpret_cast<uint8_t*>(dg_smem);
-  const uint32_t s = dgc::location_compare(c, blob_a, blob_b, pp, locs[i], area, &e);
-  if (threadIdx.x == 0) {
-    status[i] = (uint8_t)s;
-    flags[i + 1] = s != 0 ? 1 : 0;
-  }
-  if (e) atomicOr(err, e);
+  dgk_dev::compare_body<BLOCK>(blob_a, blob_b, pp, locs, n, status, flags, err);
+}
+
+template <int BLOCK>
+__global__ __launch_bounds__(BLOCK) void k_enumerate(const uint8_t* __restrict__ blob,
+                                                     const int64_t* __restrict__ locs, int64_t n,
+                                                     int64_t* __restrict__ offsets, uint32_t* __restrict__ ids,
+                                                     uint32_t* __restrict__ cnt, uint64_t capacity,
+                                                     uint64_t* __restrict__ status,
+                                                     unsigned long long* __restrict__ ticket,
+                                                     uint32_t* __restrict__ err) {
+  dgk_dev::enumerate_body<BLOCK>(blob, locs, n, offsets, ids, cnt, capacity, status, ticket, err);
+}
+
+__global__ void k_zero_u64(uint64_t* __restrict__ p, int64_t count) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < count) p[i] = 0ull;
 }
 
 // ---- device-wide inclusive scan of v[1..n] (v[0] = 0 on exit) ---------------
@@ -212,6 +156,7 @@ namespace dgk {
 hipError_t launch_sizes(const uint8_t* blob, const int64_t* locs, int64_t n, int64_t* offsets, uint32_t* err,
                         int block, uint32_t lds, hipStream_t s) {
   if (n <= 0) return hipSuccess;
+  if (block != 64 && block != 256) return hipErrorInvalidConfiguration;
   hipError_t e;
   if (block == 256) {
     if ((e = allow_lds(k_sizes<256>, lds)) != hipSuccess) return e;
@@ -226,6 +171,7 @@ hipError_t launch_sizes(const uint8_t* blob, const int64_t* locs, int64_t n, int
 hipError_t launch_fill(const uint8_t* blob, const int64_t* locs, int64_t n, const int64_t* offsets, uint32_t* ids,
                        uint32_t* cnt, uint32_t* err, int block, uint32_t lds, hipStream_t s) {
   if (n <= 0) return hipSuccess;
+  if (block != 64 && block != 256) return hipErrorInvalidConfiguration;
   hipError_t e;
   if (block == 256) {
     if ((e = allow_lds(k_fill<256>, lds)) != hipSuccess) return e;
@@ -237,23 +183,53 @@ hipError_t launch_fill(const uint8_t* blob, const int64_t* locs, int64_t n, cons
   return hipGetLastError();
 }
 
-hipError_t launch_compare(const uint8_t* blob_a, const uint8_t* blob_b, const dgc::PairPlan& pp, const int64_t* locs,
-                          int64_t n, uint8_t* status, int64_t* flags, uint32_t* err, int block, hipStream_t s) {
+hipError_t launch_compare(const uint8_t* blob_a, const uint8_t* blob_b, const dgc::PairPlan* pp, uint32_t lds,
+                          const int64_t* locs, int64_t n, uint8_t* status, int64_t* flags, uint32_t* err, int block,
+                          hipStream_t s) {
   if (n <= 0) return hipSuccess;
   hipError_t e;
   if (block == 256) {
-    if ((e = allow_lds(k_compare<256>, pp.lds_bytes)) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_compare<256>, dim3((unsigned)n), dim3(256), pp.lds_bytes, s, blob_a, blob_b, pp, locs, n,
-                       status, flags, err);
+    if ((e = allow_lds(k_compare<256>, lds)) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_compare<256>, dim3((unsigned)n), dim3(256), lds, s, blob_a, blob_b, pp, locs, n, status,
+                       flags, err);
   } else {
-    if ((e = allow_lds(k_compare<64>, pp.lds_bytes)) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_compare<64>, dim3((unsigned)n), dim3(64), pp.lds_bytes, s, blob_a, blob_b, pp, locs, n,
-                       status, flags, err);
+    if ((e = allow_lds(k_compare<64>, lds)) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_compare<64>, dim3((unsigned)n), dim3(64), lds, s, blob_a, blob_b, pp, locs, n, status, flags,
+                       err);
   }
   return hipGetLastError();
 }
 
 int64_t scan_temp_entries(int64_t n) { return (n + SCAN_TILE - 1) / SCAN_TILE + 1; }
+
+hipError_t launch_enumerate(const uint8_t* blob, const int64_t* locs, int64_t n, int64_t* offsets, uint32_t* ids,
+                            uint32_t* cnt, uint64_t capacity, uint64_t* status, uint64_t* ticket, uint32_t* err,
+                            int block, uint32_t lds, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  if (block != 64 && block != 256) return hipErrorInvalidConfiguration;
+  // Clear the look-back status words and the ticket (status holds n words,
+  // the ticket one more).
+  hipLaunchKernelGGL(k_zero_u64, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, status, n);
+  hipLaunchKernelGGL(k_zero_u64, dim3(1), dim3(1), 0, s, ticket, (int64_t)1);
+  hipError_t e;
+  unsigned long long* t = reinterpret_cast<unsigned long long*>(ticket);
+  if (block == 256) {
+    if ((e = allow_lds(k_enumerate<256>, lds)) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_enumerate<256>, dim3((unsigned)n), dim3(256), lds, s, blob, locs, n, offsets, ids, cnt,
+                       capacity, status, t, err);
+  } else {
+    if ((e = allow_lds(k_enumerate<64>, lds)) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_enumerate<64>, dim3((unsigned)n), dim3(64), lds, s, blob, locs, n, offsets, ids, cnt,
+                       capacity, status, t, err);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_zero_u64(uint64_t* p, int64_t count, hipStream_t s) {
+  if (count <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_zero_u64, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, s, p, count);
+  return hipGetLastError();
+}
 
 hipError_t launch_zero(uint32_t* p, hipStream_t s) {
   hipLaunchKernelGGL(k_zero_word, dim3(1), dim3(1), 0, s, p);

@@ -1,0 +1,216 @@
+// Device code shared by the precompiled kernels (kernels.hip) and the
+// per-graph specialised kernels built at run time (jit.cpp): the block
+// context for core.h and the bodies of the per-location kernels.  Each body
+// takes the compiled plan as a pointer; the specialised kernels pass a
+// pointer to a __constant__ copy of the plan so that every instruction field,
+// op dispatch and trip count folds to a constant.
+#pragma once
+#include <stdint.h>
+
+#include "core.h"
+
+namespace dgk_dev {
+
+// Block context for core.h: BLOCK threads cooperating on one location.
+template <int BLOCK>
+struct DevCtx {
+  uint32_t* wsum;  // LDS, BLOCK / 64 words
+  DGC int tid() const { return (int)threadIdx.x; }
+  DGC int nthreads() const { return BLOCK; }
+  DGC void sync() const { __syncthreads(); }
+  DGC void atomic_add(uint64_t* p, uint64_t v) const {
+    atomicAdd(reinterpret_cast<unsigned long long*>(p), (unsigned long long)v);
+  }
+  DGC void atomic_max(uint64_t* p, uint64_t v) const {
+    atomicMax(reinterpret_cast<unsigned long long*>(p), (unsigned long long)v);
+  }
+  DGC void store(uint32_t* p, uint32_t v) const { __builtin_nontemporal_store(v, p); }
+  // Exclusive count of set flags among lower threads of the block, and the
+  // block total.  Ends with every thread past a barrier.
+  DGC uint32_t prefix(bool f, uint32_t* total) const {
+    const uint64_t m = __ballot(f);
+    const uint32_t lane = threadIdx.x & 63u;
+    const uint32_t pre = (uint32_t)__popcll(m & ((1ull << lane) - 1ull));
+    if (BLOCK == 64) {
+      *total = (uint32_t)__popcll(m);
+      return pre;
+    }
+    const uint32_t wave = threadIdx.x >> 6;
+    __syncthreads();
+    if (lane == 0) wsum[wave] = (uint32_t)__popcll(m);
+    __syncthreads();
+    uint32_t before = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < BLOCK / 64; ++w) {
+      uint32_t x = wsum[w];
+      before += (w < (int)wave) ? x : 0u;
+      tot += x;
+    }
+    *total = tot;
+    return before + pre;
+  }
+  DGC bool any(bool f) const { return __syncthreads_or(f) != 0; }
+  // Sum and maximum over the 64 lanes of the calling wave (all lanes active).
+  DGC uint64_t wave_sum(uint64_t v) const {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+  }
+  DGC uint64_t wave_max(uint64_t v) const {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const uint64_t w = __shfl_xor(v, o, 64);
+      v = w > v ? w : v;
+    }
+    return v;
+  }
+};
+
+extern __shared__ uint64_t dg_smem[];
+
+template <int BLOCK>
+DGC void sizes_body(const uint8_t* __restrict__ blob, const int64_t* __restrict__ locs,
+                                                 int64_t n, int64_t* __restrict__ offsets, uint32_t* __restrict__ err) {
+  __shared__ uint32_t wsum[BLOCK / 64];
+  const int64_t i = blockIdx.x;
+  if (i >= n) return;
+  DevCtx<BLOCK> c{wsum};
+  uint32_t e = 0;
+  uint8_t* area = reinterpret_cast<uint8_t*>(dg_smem);
+  const uint64_t rows =
+      dgc::location_row<DevCtx<BLOCK>, dgc::EMIT_COUNT>(c, blob, locs[i], area, nullptr, nullptr, 0, &e);
+  if (threadIdx.x == 0) offsets[i + 1] = (int64_t)rows;
+  if (e) atomicOr(err, e);
+}
+
+template <int BLOCK>
+DGC void fill_body(const uint8_t* __restrict__ blob, const int64_t* __restrict__ locs,
+                                                int64_t n, const int64_t* __restrict__ offsets,
+                                                uint32_t* __restrict__ ids, uint32_t* __restrict__ cnt,
+                                                uint32_t* __restrict__ err) {
+  __shared__ uint32_t wsum[BLOCK / 64];
+  const int64_t i = blockIdx.x;
+  if (i >= n) return;
+  DevCtx<BLOCK> c{wsum};
+  uint32_t e = 0;
+  uint8_t* area = reinterpret_cast<uint8_t*>(dg_smem);
+  const int64_t start = offsets[i];
+  const int64_t room = offsets[i + 1] - start;
+  // Writes stay inside [offsets[i], offsets[i+1]) whatever this row's size.
+  const uint64_t rows = dgc::location_row<DevCtx<BLOCK>, dgc::EMIT_FILL>(
+      c, blob, locs[i], area, ids + start, cnt + start, room > 0 ? (uint64_t)room : 0ull, &e);
+  if (threadIdx.x == 0 && (int64_t)rows != room) e |= DGP_ERR_SIZE;
+  if (e) atomicOr(err, e);
+}
+
+template <int BLOCK>
+DGC void compare_body(const uint8_t* __restrict__ blob_a,
+                                                   const uint8_t* __restrict__ blob_b,
+                                                   const dgc::PairPlan* __restrict__ pp,
+                                                   const int64_t* __restrict__ locs, int64_t n,
+                                                   uint8_t* __restrict__ status, int64_t* __restrict__ flags,
+                                                   uint32_t* __restrict__ err) {
+  __shared__ uint32_t wsum[BLOCK / 64];
+  const int64_t i = blockIdx.x;
+  if (i >= n) return;
+  DevCtx<BLOCK> c{wsum};
+  uint32_t e = 0;
+  uint8_t* area = reinterpret_cast<uint8_t*>(dg_smem);
+  const uint32_t s = dgc::location_compare(c, blob_a, blob_b, pp, locs[i], area, &e);
+  if (threadIdx.x == 0) {
+    status[i] = (uint8_t)s;
+    flags[i + 1] = s != 0 ? 1 : 0;
+  }
+  if (e) atomicOr(err, e);
+}
+
+// ---- single pass: sizes, offsets by decoupled look-back, rows -------------
+// status[i]: bits 62-63 = 0 not ready, 1 row size of i, 2 offsets[i+1];
+// bits 0-61 the value.  A reader needs nothing but the word itself, so the
+// accesses are relaxed atomics at device scope (they bypass the non-coherent
+// per-XCD caches without invalidating them).  A block takes its location index from a ticket
+// counter, so every lower index belongs to a block that is already running
+// and the look-back always finishes; the wait is bounded anyway.
+constexpr uint64_t ST_SIZE = 1ull << 62, ST_PREFIX = 2ull << 62, ST_VALUE = (1ull << 62) - 1;
+constexpr uint32_t LOOKBACK_SPIN_LIMIT = 1u << 24;
+
+template <int BLOCK>
+DGC void enumerate_body(const uint8_t* __restrict__ blob,
+                                                     const int64_t* __restrict__ locs, int64_t n,
+                                                     int64_t* __restrict__ offsets, uint32_t* __restrict__ ids,
+                                                     uint32_t* __restrict__ cnt, uint64_t capacity,
+                                                     uint64_t* __restrict__ status,
+                                                     unsigned long long* __restrict__ ticket,
+                                                     uint32_t* __restrict__ err) {
+  __shared__ uint32_t wsum[BLOCK / 64];
+  __shared__ int64_t sh_i;
+  __shared__ uint64_t sh_off;
+  if (threadIdx.x == 0) sh_i = (int64_t)atomicAdd(ticket, 1ull);
+  __syncthreads();
+  const int64_t i = sh_i;
+  if (i >= n) return;
+  DevCtx<BLOCK> c{wsum};
+  uint32_t e = 0;
+  uint8_t* area = reinterpret_cast<uint8_t*>(dg_smem);
+  const bool ok = dgc::location_plan(c, blob, locs[i], area, &e);
+  const uint64_t size = ok ? dgc::location_leaves<DevCtx<BLOCK>, dgc::EMIT_COUNT>(c, blob, area, nullptr, nullptr,
+                                                                                   0, &e)
+                           : 0ull;
+  if (threadIdx.x < 64) {
+    // Wave 0 publishes this row's size, then looks back 64 predecessors at a
+    // time: the nearest one whose running total is published ends the walk,
+    // the row sizes above it are added.  Only those must have arrived.
+    const int lane = (int)threadIdx.x;
+    if (lane == 0) {
+      __hip_atomic_store(&status[i], (i == 0 ? ST_PREFIX : ST_SIZE) | size, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+    }
+    uint64_t before = 0;
+    int64_t hi = i;  // window [hi - 64, hi)
+    uint32_t spins = 0;
+    while (hi > 0) {
+      const int64_t j = hi - 64 + lane;
+      const uint64_t st =
+          j >= 0 ? __hip_atomic_load(&status[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : ST_PREFIX;
+      const uint64_t tag = st & ~ST_VALUE;
+      const uint64_t pmask = __ballot(tag == ST_PREFIX);
+      const int top = pmask ? 63 - __clzll((long long)pmask) : -1;
+      const uint64_t waiting = __ballot(tag == 0) & (top >= 0 ? ~((2ull << top) - 1ull) : ~0ull);
+      if (waiting) {
+        if (++spins > LOOKBACK_SPIN_LIMIT) {
+          e |= DGP_ERR_TIMEOUT;
+          break;
+        }
+        __builtin_amdgcn_s_sleep(1);
+        continue;
+      }
+      uint64_t v = lane >= top ? (st & ST_VALUE) : 0ull;
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+      before += v;
+      if (top >= 0) break;
+      hi -= 64;
+    }
+    if (lane == 0) {
+      if (i > 0)
+        __hip_atomic_store(&status[i], ST_PREFIX | (before + size), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      offsets[i] = (int64_t)before;
+      if (i == n - 1) offsets[n] = (int64_t)(before + size);
+      sh_off = before;
+    }
+  }
+  __syncthreads();
+  const uint64_t off = sh_off;
+  if (ok && size > 0) {
+    if (off + size <= capacity) {
+      const uint64_t rows = dgc::location_leaves<DevCtx<BLOCK>, dgc::EMIT_FILL>(c, blob, area, ids + off, cnt + off,
+                                                                              size, &e);
+      if (threadIdx.x == 0 && rows != size) e |= DGP_ERR_SIZE;
+    } else if (threadIdx.x == 0) {
+      e |= DGP_ERR_BUFFER;
+    }
+  }
+  if (e) atomicOr(err, e);
+}
+
+}  // namespace dgk_dev

@@ -112,6 +112,16 @@ struct DgpHeader {
   int32_t max_leaf_terms;
   int32_t emit_entries;  // table area (uint32 words) for the largest leaf
   int32_t union_entries; // union-list area (int32) for the largest leaf
+  // Instructions are grouped into levels: a level only reads values written
+  // by earlier levels, so the block synchronises once per phase of a level
+  // instead of once per instruction.  level_off: byte offset of int32
+  // level_start[nlevel + 1] (instruction index of each level's first
+  // instruction).  A component sum over more than two variables runs in a
+  // level of its own and keeps its variables in LDS (serial_vars: the
+  // largest such variable count, 0 if none).
+  int32_t nlevel;
+  int32_t level_off;
+  int32_t serial_vars;
   int32_t pad;
 };
 
@@ -122,3 +132,5 @@ struct DgpHeader {
 #define DGP_ERR_OVERFLOW 2u   // a path count does not fit 32 bits
 #define DGP_ERR_CAPACITY 4u   // a factor or union outgrew its static capacity
 #define DGP_ERR_SIZE 8u       // fill found a row size different from the sizes pass
+#define DGP_ERR_BUFFER 16u    // single pass: the rows do not fit the output buffers
+#define DGP_ERR_TIMEOUT 32u   // single pass: a predecessor's row size never arrived

@@ -61,7 +61,9 @@ def check_rows_sorted(off, ids):
 
 
 @pytest.mark.parametrize("name", SEPARABLE)
-def test_catalogue_all_locations(B, name):
+@pytest.mark.parametrize("kernels", ["specialized", "interpreted"])
+def test_catalogue_all_locations(B, name, kernels, monkeypatch):
+    monkeypatch.setenv("DIRIGO_JIT", "1" if kernels == "specialized" else "0")
     text = CAT[name][0]
     g = B.dg_graph_parse(text)
     og = oracle.Graph(text)
@@ -71,6 +73,18 @@ def test_catalogue_all_locations(B, name):
     assert np.array_equal(off.cpu().numpy(), ro)
     assert np.array_equal(ids.cpu().numpy().view(np.uint32), io)
     assert np.array_equal(cnt.cpu().numpy().view(np.uint32), co)
+
+
+def test_specialized_kernels_load(B, monkeypatch):
+    """With specialisation on (the default), a graph's first device call
+    compiles and loads its own kernels; with DIRIGO_JIT=0 it never does."""
+    monkeypatch.delenv("DIRIGO_JIT", raising=False)
+    g = B.dg_graph_parse(W.c2_text())
+    assert B.dg_graph_info(g)["specialized"] == -1
+    B.enumerate_locations(g, [0, 1, 2])
+    assert B.dg_graph_info(g)["specialized"] == 1
+    monkeypatch.setenv("DIRIGO_JIT", "0")
+    assert B.dg_graph_info(B.dg_graph_parse(W.c1_text()))["specialized"] == 0
 
 
 def test_c1_all(B):
@@ -207,3 +221,79 @@ def test_repeatable(B):
     b = B.enumerate_locations(g, locs)
     for x, y in zip(a, b):
         assert torch.equal(x, y)
+
+
+def _fused(B, g, locs):
+    d_locs = torch.as_tensor(locs, dtype=torch.int64, device="cuda")
+    n = d_locs.numel()
+    ws = B.workspace(g, n)
+    off = torch.empty(n + 1, dtype=torch.int64, device="cuda")
+    total = B.dg_enumerate_sizes(g, d_locs, off, ws)
+    ids = torch.empty(max(total, 1), dtype=torch.int32, device="cuda")
+    cnt = torch.empty(max(total, 1), dtype=torch.int32, device="cuda")
+    off2 = torch.full((n + 1,), -7, dtype=torch.int64, device="cuda")
+    t2 = B.dg_enumerate(g, d_locs, off2, ids, cnt, ws)
+    assert t2 == total and torch.equal(off, off2)
+    return off2, ids[:total], cnt[:total]
+
+
+@pytest.mark.parametrize("name", ["c1", "c2", "c3"])
+def test_single_pass_equals_two_pass(B, name):
+    text = W.CONFIGS[name]["text"]()
+    g = B.dg_graph_parse(text)
+    locs = W.config_locations(name)
+    a = B.enumerate_locations(g, locs)
+    b = _fused(B, g, locs)
+    for x, y in zip(a, b):
+        assert torch.equal(x, y)
+
+
+def test_single_pass_c4_against_oracle(B):
+    text = W.c4_text()
+    g = B.dg_graph_parse(text)
+    locs = W.config_locations("c4")
+    off, ids, cnt = _fused(B, g, locs)
+    assert int(off[-1]) == 4366401536
+    assert bool((off[1:] - off[:-1] == 66626).all())
+    pos = [0, 1, 31337, len(locs) - 1]
+    _, got = rows_to_host(off, ids, cnt, pos)
+    want = oracle_rows(text, [locs[p] for p in pos])
+    for (gi, gc), (wi, wc) in zip(got, want):
+        assert np.array_equal(gi, wi) and np.array_equal(gc, wc)
+
+
+@pytest.mark.parametrize("name", ["c5_small_var", "conv3d_groups", "gather_floor_flat", "diamond"])
+@pytest.mark.parametrize("kernels", ["specialized", "interpreted"])
+def test_single_pass_catalogue(B, name, kernels, monkeypatch):
+    monkeypatch.setenv("DIRIGO_JIT", "1" if kernels == "specialized" else "0")
+    text = CAT[name][0]
+    og = oracle.Graph(text)
+    locs = list(range(og.output_numel))[::-1]  # descending order, still one row per location
+    off, ids, cnt = _fused(B, B.dg_graph_parse(text), locs)
+    ro, io, co = og.enumerate(locs)
+    assert np.array_equal(off.cpu().numpy(), ro)
+    assert np.array_equal(ids.cpu().numpy().view(np.uint32), io)
+    assert np.array_equal(cnt.cpu().numpy().view(np.uint32), co)
+
+
+def test_single_pass_small_buffer(B):
+    text = W.c2_text()
+    g = B.dg_graph_parse(text)
+    locs = W.config_locations("c2")[:300]
+    d_locs = torch.as_tensor(locs, dtype=torch.int64, device="cuda")
+    ws = B.workspace(g, len(locs))
+    off = torch.empty(len(locs) + 1, dtype=torch.int64, device="cuda")
+    ro, io, co = oracle.Graph(text).enumerate(locs)
+    cap = int(ro[150])  # room for exactly the first 150 rows
+    guard = 4096
+    ids = torch.full((cap + guard,), -1, dtype=torch.int32, device="cuda")
+    cnt = torch.full((cap + guard,), -1, dtype=torch.int32, device="cuda")
+    with pytest.raises(B.DgError) as e:
+        B.dg_enumerate(g, d_locs, off, ids[:cap], cnt[:cap], ws)
+    assert e.value.name == "DG_E_BUFFER"
+    assert np.array_equal(off.cpu().numpy(), ro)
+    assert np.array_equal(ids[:cap].cpu().numpy().view(np.uint32), io[:cap])
+    assert bool((ids[cap:] == -1).all()) and bool((cnt[cap:] == -1).all())
+    # n = 0
+    off0 = torch.full((1,), 5, dtype=torch.int64, device="cuda")
+    assert B.dg_enumerate(g, d_locs[:0], off0, ids, cnt, ws) == 0 and int(off0[0]) == 0
