@@ -515,6 +515,8 @@ Plan Compiler::run() {
       stride *= (uint64_t)T.shape[d];
     }
     double lb = 0;
+    if (ts.size() == 1)
+      for (int d = 0; d < L.rank; ++d) fac_[ts[0].f[d]].stat = 1;
     for (const SymTerm& t : ts) {
       DgpTerm dt;
       std::memset(&dt, 0, sizeof(dt));

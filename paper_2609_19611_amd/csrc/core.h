@@ -75,7 +75,10 @@ struct LeafHdr {
   int32_t hlo[DGP_MAX_RANK];    // first coordinate of the dim's hull
   int32_t dense[DGP_MAX_RANK];  // every hull coordinate is nonzero: no list, x = hlo + i
   uint64_t cnt[DGP_MAX_RANK];   // nonzero coordinates per dim (block total)
-  uint64_t umax[DGP_MAX_RANK];  // largest factor value on the union (single term)
+  uint64_t umax[DGP_MAX_RANK];  // largest factor value on the union (several terms)
+  int32_t ok;                   // the prepared leaf has entries
+  uint32_t O, In;               // outer and inner table lengths
+  int32_t pad;
 };
 
 struct EmitLayout {
@@ -185,9 +188,8 @@ DGC void ifn_range(const DgpIFn& f, const int32_t* vlo, const int32_t* vn, int32
 }
 
 DGC uint64_t mul_sat(uint64_t a, uint64_t b) {
-  if (a == 0 || b == 0) return 0;
-  if (a > ~0ull / b) return ~0ull;
-  return a * b;
+  uint64_t r;
+  return __builtin_mul_overflow(a, b, &r) ? ~0ull : r;
 }
 
 // ------------------------------------------------------------ plan_exec --
@@ -510,16 +512,17 @@ DGC void plan_exec(C& c, const uint8_t* blob, int64_t loc, uint8_t* area, const 
           }
         }
       }
-      if (!to_factor && acc) c.atomic_add(&scal[I.dst], acc);
+      if (!to_factor) c.reduce_add(&scal[I.dst], acc);
     }
     c.sync();
   }
 }
 
-// Nonzero count and largest value of every factor (after plan_exec, whose
-// last barrier also published the zeroed statistics).  A single-term leaf is
-// the outer product of its factors, so these give its entry count and its
-// largest path count without touching the leaf.
+// Nonzero count and largest value of the factors used by single-term leaves
+// (after plan_exec, whose last barrier also published the zeroed
+// statistics).  A single-term leaf is the outer product of its factors, so
+// these give its entry count and its largest path count without touching
+// the leaf.
 template <class C>
 DGC void factor_stats(C& c, const uint8_t* blob, uint8_t* area, const PlanLayout& PL) {
   const DgpHeader* h = (const DgpHeader*)blob;
@@ -528,12 +531,11 @@ DGC void factor_stats(C& c, const uint8_t* blob, uint8_t* area, const PlanLayout
   const uint64_t* fval = (const uint64_t*)(area + PL.fval);
   FStat* st = (FStat*)(area + PL.fstat);
   const int tid = c.tid(), nt = c.nthreads();
-  const int wave_base = tid & ~63;
   const int nf = h->nfactor;
   DG_PLAN_UNROLL
   for (int f = 0; f < nf; ++f) {
+    if (!fac[f].stat) continue;
     const int32_t len = meta[2 * f + 1];
-    if (wave_base >= len) continue;  // uniform per wave
     const uint64_t* v = fval + fac[f].off;
     uint64_t cnt = 0, mx = 0;
     for (int32_t x = tid; x < len; x += nt) {
@@ -541,12 +543,8 @@ DGC void factor_stats(C& c, const uint8_t* blob, uint8_t* area, const PlanLayout
       cnt += a != 0 ? 1u : 0u;
       mx = a > mx ? a : mx;
     }
-    cnt = c.wave_sum(cnt);
-    mx = c.wave_max(mx);
-    if ((tid & 63) == 0) {
-      if (cnt) c.atomic_add(&st[f].nnz, cnt);
-      if (mx) c.atomic_max(&st[f].vmax, mx);
-    }
+    c.reduce_add(&st[f].nnz, cnt);
+    c.reduce_max(&st[f].vmax, mx);
   }
   c.sync();
 }
@@ -629,8 +627,8 @@ DGC bool build_union(C& c, const TermRef* terms, int nterm, int rank, const int3
         }
         cnt += nz ? 1u : 0u;
       }
-      if (cnt) c.atomic_add(&H->cnt[d], cnt);
-      if (vmax) c.atomic_max(&H->umax[d], vmax);
+      c.reduce_add(&H->cnt[d], cnt);
+      c.reduce_max(&H->umax[d], vmax);
     }
     c.sync();
   }
@@ -699,6 +697,7 @@ DGC void build_table(C& c, const LeafGeom& G, const TermRef* terms, int nterm, c
   int32_t u[DGP_MAX_RANK];
   DG_UNROLL
   for (int d = 0; d < DGP_MAX_RANK; ++d) u[d] = H->u[d];
+  uint64_t m1 = 0;  // a single term's largest value, combined once per wave
   for (uint32_t r = (uint32_t)c.tid(); r < n; r += (uint32_t)c.nthreads()) {
     uint32_t rem = r;
     int32_t x[DGP_MAX_RANK];
@@ -721,81 +720,94 @@ DGC void build_table(C& c, const LeafGeom& G, const TermRef* terms, int nterm, c
       for (int d = 0; d < DGP_MAX_RANK; ++d)
         if (d >= d0 && d < d1 && v) v = mul_sat(v, term_val(terms[t], d, x[d], a64));
       tab[(uint64_t)r * W + 1 + t] = v > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)v;
-      if (v) c.atomic_max(&tmax[t], v);
+      if (nterm == 1) m1 = v > m1 ? v : m1;
+      else if (v) c.atomic_max(&tmax[t], v);
     }
   }
+  if (nterm == 1) c.reduce_max(&tmax[0], m1);
 }
 
 DGC bool prod_overflows(uint64_t a, uint64_t b) {
   return a && b && (a > 0xFFFFFFFFull || b > 0xFFFFFFFFull || a * b > 0xFFFFFFFFull);
 }
 
-// One leaf of one location.  Terms [0, na) belong to graph A (the graph
-// being enumerated), terms [na, na + nb) to graph B (compare only).
+// Prepares one leaf of one location for emission (block `w`).  Terms [0, na) belong to graph A (the graph being enumerated),
+// terms [na, na + nb) to graph B (compare only).  Forms the union of the
+// terms' nonzero coordinates and, with a split, the outer and inner tables,
+// and publishes in the leaf header: ok (0 when the leaf has no entry), the
+// union lengths, and the table lengths O and In.
+template <class W, int MODE>
+DGC void leaf_prepare(W& w, const LeafGeom& G, int split, const int32_t* ucap, const TermRef* terms, int na, int nb,
+                      uint8_t* area, const EmitLayout& E, const FStat* st, uint32_t* err) {
+  const int tid = w.tid(), nt = w.nthreads();
+  const int nterm = na + nb;
+  const int rank = G.rank;
+  int32_t* ulist = (int32_t*)(area + E.ulist);
+  LeafHdr* H = (LeafHdr*)(area + E.hdr);
+  const uint64_t* a64 = (const uint64_t*)area;
+  const bool single = MODE != EMIT_COMPARE && nterm == 1;
+  bool ok = nterm > 0 && !(MODE != EMIT_COMPARE && na == 0);
+  // A single term with a zero coefficient is identically zero.
+  if (ok && single && terms[0].coef == 0) ok = false;
+  // A single term's per-dim counts are the factor statistics.
+  if (ok) ok = build_union(w, terms, nterm, rank, ucap, ulist, H, true, area, single ? st : nullptr, err);
+  uint32_t O = 1, In = 1;
+  if (ok && split >= 0) {
+    // Outer table over dims [0, split), inner over [split, rank).
+    int32_t u[DGP_MAX_RANK];
+    DG_UNROLL
+    for (int d = 0; d < DGP_MAX_RANK; ++d) u[d] = d < rank ? H->u[d] : 1;
+    DG_UNROLL
+    for (int d = 0; d < DGP_MAX_RANK; ++d) {
+      if (d < split) O *= (uint32_t)u[d];
+      else if (d < rank) In *= (uint32_t)u[d];
+    }
+    const int Wd = 1 + nterm;
+    uint32_t* otab = (uint32_t*)(area + E.tables);
+    uint32_t* itab = otab + (uint64_t)O * Wd;
+    uint64_t* tmax = (uint64_t*)(area + E.tmax);
+    for (int i = tid; i < 2 * nterm; i += nt) tmax[i] = 0;
+    w.sync();
+    build_table(w, G, terms, nterm, ulist, H, 0, split, true, O, otab, tmax, a64);
+    build_table(w, G, terms, nterm, ulist, H, split, rank, false, In, itab, tmax + nterm, a64);
+    w.sync();
+    // A term whose largest outer and inner parts multiply past 32 bits has a
+    // real cell with that count.
+    for (int t = tid; t < nterm; t += nt)
+      if (prod_overflows(tmax[t], tmax[nterm + t])) *err |= DGP_ERR_OVERFLOW;
+  }
+  if (tid == 0) {
+    H->ok = ok ? 1 : 0;
+    H->O = O;
+    H->In = In;
+  }
+}
+
+// Emits one prepared leaf (block `c`).
 //   EMIT_COUNT:   returns the number of nonzero entries.
 //   EMIT_FILL:    writes them at ids/cnt and returns their number.
 //   EMIT_COMPARE: returns 0 equal, 1 nonzero sets differ, 2 counts differ.
 //   `room` bounds the entries EMIT_FILL may write at ids/cnt; a leaf that
 //   would need more raises DGP_ERR_SIZE and writes nothing past it.
 template <class C, int MODE>
-DGC uint64_t leaf_pass(C& c, const LeafGeom& G, int split, const int32_t* ucap, const TermRef* terms, int na,
-                       int nb, uint8_t* area, const EmitLayout& E, const FStat* st, uint32_t* ids, uint32_t* cnt,
-                       uint64_t room, uint32_t* err) {
+DGC uint64_t leaf_emit(C& c, const LeafGeom& G, int split, const TermRef* terms, int na, int nb, uint8_t* area,
+                       const EmitLayout& E, uint32_t* ids, uint32_t* cnt, uint64_t room, uint32_t* err) {
   const int tid = c.tid(), nt = c.nthreads();
   const int nterm = na + nb;
   const int rank = G.rank;
-  if (MODE != EMIT_COMPARE && na == 0) return 0;
-  if (MODE == EMIT_COMPARE && nterm == 0) return 0;
-  int32_t* ulist = (int32_t*)(area + E.ulist);
-  LeafHdr* H = (LeafHdr*)(area + E.hdr);
+  const int32_t* ulist = (const int32_t*)(area + E.ulist);
+  const LeafHdr* H = (const LeafHdr*)(area + E.hdr);
   const uint64_t* a64 = (const uint64_t*)area;
-  const bool single = MODE != EMIT_COMPARE && nterm == 1;
-  // A single term with a zero coefficient is identically zero.
-  if (single && terms[0].coef == 0) return 0;
-  // A single term needs no union lists to be counted, and its per-dim
-  // counts are the factor statistics.
-  if (!build_union(c, terms, nterm, rank, ucap, ulist, H, !(single && MODE == EMIT_COUNT), area,
-                   single ? st : nullptr, err))
-    return 0;
+  if (!H->ok) return 0;
   int32_t u[DGP_MAX_RANK];
   DG_UNROLL
   for (int d = 0; d < DGP_MAX_RANK; ++d) u[d] = d < rank ? H->u[d] : 1;
 
-  if (single && MODE == EMIT_COUNT) {
-    // Every cell of a single term's grid is an entry; the largest count is
-    // the coefficient times the largest value of each factor.
-    uint64_t total = 1, mx = terms[0].coef;
-    DG_UNROLL
-    for (int d = 0; d < DGP_MAX_RANK; ++d) {
-      total *= (uint64_t)u[d];
-      if (d < rank) mx = mul_sat(mx, st ? st[terms[0].fid[d]].vmax : H->umax[d]);
-    }
-    if (mx > 0xFFFFFFFFull) *err |= DGP_ERR_OVERFLOW;
-    c.sync();
-    return total;
-  }
-
   if (split >= 0) {
-    // Outer table over dims [0, split), inner over [split, rank).
     const int W = 1 + nterm;
-    uint32_t O = 1, In = 1;
-    DG_UNROLL
-    for (int d = 0; d < DGP_MAX_RANK; ++d) {
-      if (d < split) O *= (uint32_t)u[d];
-      else if (d < rank) In *= (uint32_t)u[d];
-    }
-    uint32_t* otab = (uint32_t*)(area + E.tables);
-    uint32_t* itab = otab + (uint64_t)O * W;
-    uint64_t* tmax = (uint64_t*)(area + E.tmax);
-    for (int i = tid; i < 2 * nterm; i += nt) tmax[i] = 0;
-    c.sync();
-    build_table(c, G, terms, nterm, ulist, H, 0, split, true, O, otab, tmax, a64);
-    build_table(c, G, terms, nterm, ulist, H, split, rank, false, In, itab, tmax + nterm, a64);
-    c.sync();
-    // A term whose largest outer and inner parts multiply past 32 bits has a
-    // real cell with that count.
-    for (int t = tid; t < nterm; t += nt)
-      if (prod_overflows(tmax[t], tmax[nterm + t])) *err |= DGP_ERR_OVERFLOW;
+    const uint32_t O = H->O, In = H->In;
+    const uint32_t* otab = (const uint32_t*)(area + E.tables);
+    const uint32_t* itab = otab + (uint64_t)O * W;
     const uint64_t total = (uint64_t)O * In;
     if (MODE == EMIT_FILL && nterm == 1) {
       // Dense single-term grid: every cell is an entry, in order.  Lanes are
@@ -830,7 +842,6 @@ DGC uint64_t leaf_pass(C& c, const LeafGeom& G, int split, const int32_t* ucap, 
           }
         }
       }
-      c.sync();
       return total;
     }
     // Several terms: evaluate each cell, keep the nonzero ones in order.
@@ -841,7 +852,8 @@ DGC uint64_t leaf_pass(C& c, const LeafGeom& G, int split, const int32_t* ucap, 
       uint64_t ca = 0, cb = 0;
       uint32_t pos = 0;
       if (p < total) {
-        const uint32_t r = (uint32_t)(p / In), j = (uint32_t)(p % In);
+        // (A leaf has fewer than 2^32 elements, so cell indices fit 32 bits.)
+        const uint32_t r = (uint32_t)p / In, j = (uint32_t)p - r * In;
         const uint32_t* o = otab + (uint64_t)r * W;
         const uint32_t* q = itab + (uint64_t)j * W;
         pos = o[0] + q[0];
@@ -871,7 +883,6 @@ DGC uint64_t leaf_pass(C& c, const LeafGeom& G, int split, const int32_t* ucap, 
       }
     }
     if (MODE == EMIT_COMPARE) return c.any((flags & 2u) != 0) ? 2 : 0;
-    c.sync();
     return written;
   }
 
@@ -887,13 +898,13 @@ DGC uint64_t leaf_pass(C& c, const LeafGeom& G, int split, const int32_t* ucap, 
     uint32_t pos = G.base;
     if (p < total) {
       int32_t x[DGP_MAX_RANK];
-      uint64_t rem = p;
+      uint32_t rem = (uint32_t)p;  // (fewer than 2^32 cells)
       DG_UNROLL
       for (int d = DGP_MAX_RANK - 1; d >= 0; --d) {
         x[d] = 0;
         if (d < rank) {
-          const uint64_t i = rem % (uint64_t)u[d];
-          rem /= (uint64_t)u[d];
+          const uint32_t i = rem % (uint32_t)u[d];
+          rem /= (uint32_t)u[d];
           x[d] = ucoord(H, ulist, d, (int32_t)i);
           pos += (uint32_t)x[d] * G.stride[d];
         }
@@ -929,7 +940,6 @@ DGC uint64_t leaf_pass(C& c, const LeafGeom& G, int split, const int32_t* ucap, 
     }
   }
   if (MODE == EMIT_COMPARE) return c.any((flags & 2u) != 0) ? 2 : 0;
-  c.sync();
   return written;
 }
 
@@ -942,26 +952,42 @@ DGC LeafGeom leaf_geom(const DgpLeaf& L) {
   return G;
 }
 
-// Runs the plan of one location; false (and DGP_ERR_RANGE) if the location
-// lies outside the output.
-template <class C>
-DGC bool location_plan(C& c, const uint8_t* blob, int64_t loc, uint8_t* area, uint32_t* err) {
+// ---------------------------------------------------------------- drivers --
+DGC bool location_in_range(const uint8_t* blob, int64_t loc) {
   const DgpHeader* h = (const DgpHeader*)blob;
-  if (loc < 0 || loc >= h->out_numel) {
-    *err |= DGP_ERR_RANGE;
-    return false;
-  }
+  return loc >= 0 && loc < h->out_numel;
+}
+
+// Runs the plan of one (in-range) location and the factor statistics.
+template <class C>
+DGC void location_plan(C& c, const uint8_t* blob, int64_t loc, uint8_t* area, uint32_t* err) {
+  const DgpHeader* h = (const DgpHeader*)blob;
   const PlanLayout PL = plan_layout(h, vars_bytes(h->serial_vars, c.nthreads()));
   plan_exec(c, blob, loc, area, PL, err);
   factor_stats(c, blob, area, PL);
-  return true;
 }
 
-// Leaf passes over a plan already in LDS: the row size (EMIT_COUNT) or the
-// row itself (EMIT_FILL, at most `room` entries written at ids/cnt).
-template <class C, int MODE>
+// Where a row goes: the emission calls `place` once, right before it writes
+// the row's first entry (or at the end if the row has none), after the
+// first leaf to emit has been prepared.  It returns the row's offset in
+// ids/cnt and whether the row may be written.  The single-pass kernel finds
+// its offset there, so that the wait for its predecessors overlaps the
+// preparation of its first leaf.
+struct PlaceAt {
+  uint64_t off;
+  template <class C>
+  DGC uint64_t operator()(C&, bool* go) const {
+    *go = true;
+    return off;
+  }
+};
+
+// Leaf passes over a plan already in LDS (the block has synchronised since
+// the plan): the row size (EMIT_COUNT) or the row itself (EMIT_FILL, at most
+// `room` entries written at ids/cnt + place()).
+template <class C, int MODE, class Place>
 DGC uint64_t location_leaves(C& c, const uint8_t* blob, uint8_t* area, uint32_t* ids, uint32_t* cnt, uint64_t room,
-                             uint32_t* err) {
+                             uint32_t* err, Place& place) {
   const DgpHeader* h = (const DgpHeader*)blob;
   const PlanLayout PL = plan_layout(h, vars_bytes(h->serial_vars, c.nthreads()));
   const EmitLayout E = emit_layout(PL.end, h->max_leaf_terms, h->union_entries, h->emit_entries);
@@ -970,7 +996,8 @@ DGC uint64_t location_leaves(C& c, const uint8_t* blob, uint8_t* area, uint32_t*
   const uint64_t* scal = (const uint64_t*)(area + PL.scal);
   const FStat* st = (const FStat*)(area + PL.fstat);
   TermRef* terms = (TermRef*)(area + E.terms);
-  uint64_t off = 0;
+  uint64_t off = 0, base = 0;
+  bool placed = false, go = true;
   const int nleaf = h->nleaf;
   DG_PLAN_UNROLL
   for (int l = 0; l < nleaf; ++l) {
@@ -992,23 +1019,38 @@ DGC uint64_t location_leaves(C& c, const uint8_t* blob, uint8_t* area, uint32_t*
       off += n;
       continue;
     }
+    const LeafGeom G = leaf_geom(L);
     leaf_terms(c, blob, l, area, PL, terms);
     c.sync();
-    off += leaf_pass<C, MODE>(c, leaf_geom(L), L.split, L.ucap, terms, L.nterm, 0, area, E, st,
-                               ids ? ids + off : nullptr, cnt ? cnt + off : nullptr, off < room ? room - off : 0,
-                               err);
+    leaf_prepare<C, MODE>(c, G, L.split, L.ucap, terms, L.nterm, 0, area, E, st, err);
+    c.sync();
+    if (!placed) {
+      base = place(c, &go);
+      placed = true;
+      if (!go) break;
+    }
+    off += leaf_emit<C, MODE>(c, G, L.split, terms, L.nterm, 0, area, E, ids ? ids + base + off : nullptr,
+                              cnt ? cnt + base + off : nullptr, off < room ? room - off : 0, err);
     c.sync();
   }
+  if (!placed) place(c, &go);
   return off;
 }
 
 // Row size (EMIT_COUNT) or row contents (EMIT_FILL, at most `room` entries
-// written at ids/cnt) of one location.
+// written at ids/cnt) of one location; 0 and DGP_ERR_RANGE when the
+// location lies outside the output.
 template <class C, int MODE>
 DGC uint64_t location_row(C& c, const uint8_t* blob, int64_t loc, uint8_t* area, uint32_t* ids, uint32_t* cnt,
                           uint64_t room, uint32_t* err) {
-  if (!location_plan(c, blob, loc, area, err)) return 0;
-  return location_leaves<C, MODE>(c, blob, area, ids, cnt, room, err);
+  if (!location_in_range(blob, loc)) {
+    *err |= DGP_ERR_RANGE;
+    return 0;
+  }
+  location_plan(c, blob, loc, area, err);
+  c.sync();
+  PlaceAt at{0};
+  return location_leaves<C, MODE>(c, blob, area, ids, cnt, room, err, at);
 }
 
 // Per-leaf combined emission shapes of a two-graph comparison.
@@ -1030,7 +1072,7 @@ DGC uint32_t location_compare(C& c, const uint8_t* blob_a, const uint8_t* blob_b
                               uint8_t* area, uint32_t* err) {
   const DgpHeader* ha = (const DgpHeader*)blob_a;
   const DgpHeader* hb = (const DgpHeader*)blob_b;
-  if (loc < 0 || loc >= ha->out_numel) {
+  if (!location_in_range(blob_a, loc)) {
     *err |= DGP_ERR_RANGE;
     return 0;
   }
@@ -1047,11 +1089,13 @@ DGC uint32_t location_compare(C& c, const uint8_t* blob_a, const uint8_t* blob_b
   for (int l = 0; l < nleaf; ++l) {
     const int na = la[l].nterm, nb = lb[l].nterm;
     if (na + nb == 0) continue;
+    const LeafGeom G = leaf_geom(la[l]);
     leaf_terms(c, blob_a, l, area, PA, terms);
     leaf_terms(c, blob_b, l, area, PB, terms + na);
     c.sync();
-    const uint32_t s = (uint32_t)leaf_pass<C, EMIT_COMPARE>(c, leaf_geom(la[l]), PP->leaf[l].split,
-                                                            PP->leaf[l].ucap, terms, na, nb, area, E, nullptr,
+    leaf_prepare<C, EMIT_COMPARE>(c, G, PP->leaf[l].split, PP->leaf[l].ucap, terms, na, nb, area, E, nullptr, err);
+    c.sync();
+    const uint32_t s = (uint32_t)leaf_emit<C, EMIT_COMPARE>(c, G, PP->leaf[l].split, terms, na, nb, area, E,
                                                             nullptr, nullptr, 0, err);
     c.sync();
     if (s == 1) return 1;

@@ -7,6 +7,7 @@
 // library.
 #include <cstdint>
 #include <cstring>
+#include <cstdlib>
 #include <string>
 #include <vector>
 
@@ -27,13 +28,15 @@ struct HostCtx {
     if (v > *p) *p = v;
   }
   void store(uint32_t* p, uint32_t v) const { *p = v; }
+  void reduce_add(uint64_t* p, uint64_t v) const { *p += v; }
+  void reduce_max(uint64_t* p, uint64_t v) const {
+    if (v > *p) *p = v;
+  }
   uint32_t prefix(bool f, uint32_t* total) const {
     *total = f ? 1u : 0u;
     return 0u;
   }
   bool any(bool f) const { return f; }
-  uint64_t wave_sum(uint64_t v) const { return v; }
-  uint64_t wave_max(uint64_t v) const { return v; }
 };
 
 thread_local std::string g_err;

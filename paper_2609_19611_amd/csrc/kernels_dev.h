@@ -25,6 +25,32 @@ struct DevCtx {
     atomicMax(reinterpret_cast<unsigned long long*>(p), (unsigned long long)v);
   }
   DGC void store(uint32_t* p, uint32_t v) const { __builtin_nontemporal_store(v, p); }
+  // Adds (or takes the maximum of) every thread's v into *p with four LDS
+  // atomics per wave instead of one per thread: DPP lane permutes (xor 1,
+  // xor 2, mirror within 8, mirror within 16) leave every row of 16 lanes
+  // holding its total, which the row's first lane adds.  Called by all
+  // lanes of the wave.
+  DGC void reduce_add(uint64_t* p, uint64_t v) const {
+    v += dpp64<0xB1>(v);
+    v += dpp64<0x4E>(v);
+    v += dpp64<0x141>(v);
+    v += dpp64<0x140>(v);
+    if ((threadIdx.x & 15u) == 0 && v) atomic_add(p, v);
+  }
+  DGC void reduce_max(uint64_t* p, uint64_t v) const {
+    v = umax(v, dpp64<0xB1>(v));
+    v = umax(v, dpp64<0x4E>(v));
+    v = umax(v, dpp64<0x141>(v));
+    v = umax(v, dpp64<0x140>(v));
+    if ((threadIdx.x & 15u) == 0 && v) atomic_max(p, v);
+  }
+  DGC static uint64_t umax(uint64_t a, uint64_t b) { return a > b ? a : b; }
+  template <int CTRL>
+  DGC static uint64_t dpp64(uint64_t v) {
+    const uint32_t lo = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)v, CTRL, 0xf, 0xf, false);
+    const uint32_t hi = (uint32_t)__builtin_amdgcn_update_dpp(0, (int)(uint32_t)(v >> 32), CTRL, 0xf, 0xf, false);
+    return ((uint64_t)hi << 32) | lo;
+  }
   // Exclusive count of set flags among lower threads of the block, and the
   // block total.  Ends with every thread past a barrier.
   DGC uint32_t prefix(bool f, uint32_t* total) const {
@@ -50,20 +76,6 @@ struct DevCtx {
     return before + pre;
   }
   DGC bool any(bool f) const { return __syncthreads_or(f) != 0; }
-  // Sum and maximum over the 64 lanes of the calling wave (all lanes active).
-  DGC uint64_t wave_sum(uint64_t v) const {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-    return v;
-  }
-  DGC uint64_t wave_max(uint64_t v) const {
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) {
-      const uint64_t w = __shfl_xor(v, o, 64);
-      v = w > v ? w : v;
-    }
-    return v;
-  }
 };
 
 extern __shared__ uint64_t dg_smem[];
@@ -134,6 +146,67 @@ DGC void compare_body(const uint8_t* __restrict__ blob_a,
 constexpr uint64_t ST_SIZE = 1ull << 62, ST_PREFIX = 2ull << 62, ST_VALUE = (1ull << 62) - 1;
 constexpr uint32_t LOOKBACK_SPIN_LIMIT = 1u << 24;
 
+// Offset of row i by decoupled look-back (wave 0), once the row's own size
+// has been published: the nearest predecessor whose running total is
+// published ends the walk, the row sizes above it are added; only those must
+// have arrived.  Publishes row i's running total, writes offsets[i] (and
+// offsets[n] for the last row) and tells the block whether the row fits in
+// `capacity` entries.  Called by every thread of the block.
+template <int BLOCK>
+struct LookBack {
+  uint64_t* status;
+  int64_t i, n;
+  uint64_t size, capacity;
+  int64_t* offsets;
+  uint64_t* sh_off;
+  uint32_t* e;
+  bool fits = false;
+  DGC uint64_t operator()(DevCtx<BLOCK>&, bool* go) {
+    if (threadIdx.x < 64) {
+      const int lane = (int)threadIdx.x;
+      uint64_t before = 0;
+      int64_t hi = i;  // window [hi - 64, hi)
+      uint32_t spins = 0;
+      while (hi > 0) {
+        const int64_t j = hi - 64 + lane;
+        const uint64_t st =
+            j >= 0 ? __hip_atomic_load(&status[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : ST_PREFIX;
+        const uint64_t tag = st & ~ST_VALUE;
+        const uint64_t pmask = __ballot(tag == ST_PREFIX);
+        const int top = pmask ? 63 - __clzll((long long)pmask) : -1;
+        const uint64_t waiting = __ballot(tag == 0) & (top >= 0 ? ~((2ull << top) - 1ull) : ~0ull);
+        if (waiting) {
+          if (++spins > LOOKBACK_SPIN_LIMIT) {
+            *e |= DGP_ERR_TIMEOUT;
+            break;
+          }
+          __builtin_amdgcn_s_sleep(1);
+          continue;
+        }
+        uint64_t v = lane >= top ? (st & ST_VALUE) : 0ull;
+#pragma unroll
+        for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+        before += v;
+        if (top >= 0) break;
+        hi -= 64;
+      }
+      if (lane == 0) {
+        if (i > 0)
+          __hip_atomic_store(&status[i], ST_PREFIX | (before + size), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        offsets[i] = (int64_t)before;
+        if (i == n - 1) offsets[n] = (int64_t)(before + size);
+        *sh_off = before;
+      }
+    }
+    __syncthreads();
+    const uint64_t off = *sh_off;
+    fits = off + size <= capacity;
+    if (!fits && threadIdx.x == 0 && size > 0) *e |= DGP_ERR_BUFFER;
+    *go = fits;
+    return off;
+  }
+};
+
 template <int BLOCK>
 DGC void enumerate_body(const uint8_t* __restrict__ blob,
                                                      const int64_t* __restrict__ locs, int64_t n,
@@ -152,63 +225,27 @@ DGC void enumerate_body(const uint8_t* __restrict__ blob,
   DevCtx<BLOCK> c{wsum};
   uint32_t e = 0;
   uint8_t* area = reinterpret_cast<uint8_t*>(dg_smem);
-  const bool ok = dgc::location_plan(c, blob, locs[i], area, &e);
-  const uint64_t size = ok ? dgc::location_leaves<DevCtx<BLOCK>, dgc::EMIT_COUNT>(c, blob, area, nullptr, nullptr,
-                                                                                   0, &e)
-                           : 0ull;
-  if (threadIdx.x < 64) {
-    // Wave 0 publishes this row's size, then looks back 64 predecessors at a
-    // time: the nearest one whose running total is published ends the walk,
-    // the row sizes above it are added.  Only those must have arrived.
-    const int lane = (int)threadIdx.x;
-    if (lane == 0) {
-      __hip_atomic_store(&status[i], (i == 0 ? ST_PREFIX : ST_SIZE) | size, __ATOMIC_RELAXED,
-                         __HIP_MEMORY_SCOPE_AGENT);
-    }
-    uint64_t before = 0;
-    int64_t hi = i;  // window [hi - 64, hi)
-    uint32_t spins = 0;
-    while (hi > 0) {
-      const int64_t j = hi - 64 + lane;
-      const uint64_t st =
-          j >= 0 ? __hip_atomic_load(&status[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : ST_PREFIX;
-      const uint64_t tag = st & ~ST_VALUE;
-      const uint64_t pmask = __ballot(tag == ST_PREFIX);
-      const int top = pmask ? 63 - __clzll((long long)pmask) : -1;
-      const uint64_t waiting = __ballot(tag == 0) & (top >= 0 ? ~((2ull << top) - 1ull) : ~0ull);
-      if (waiting) {
-        if (++spins > LOOKBACK_SPIN_LIMIT) {
-          e |= DGP_ERR_TIMEOUT;
-          break;
-        }
-        __builtin_amdgcn_s_sleep(1);
-        continue;
-      }
-      uint64_t v = lane >= top ? (st & ST_VALUE) : 0ull;
-#pragma unroll
-      for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
-      before += v;
-      if (top >= 0) break;
-      hi -= 64;
-    }
-    if (lane == 0) {
-      if (i > 0)
-        __hip_atomic_store(&status[i], ST_PREFIX | (before + size), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      offsets[i] = (int64_t)before;
-      if (i == n - 1) offsets[n] = (int64_t)(before + size);
-      sh_off = before;
-    }
-  }
+  const int64_t loc = locs[i];
+  const bool ok = dgc::location_in_range(blob, loc);
+  if (!ok) e |= DGP_ERR_RANGE;
+  if (ok) dgc::location_plan(c, blob, loc, area, &e);
   __syncthreads();
-  const uint64_t off = sh_off;
+  dgc::PlaceAt none{0};
+  const uint64_t size =
+      ok ? dgc::location_leaves<DevCtx<BLOCK>, dgc::EMIT_COUNT>(c, blob, area, nullptr, nullptr, 0, &e, none) : 0ull;
+  if (threadIdx.x == 0) {
+    __hip_atomic_store(&status[i], (i == 0 ? ST_PREFIX : ST_SIZE) | size, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  // The row's offset is looked up once its first leaf is prepared (or at
+  // once when it has nothing to write).
+  LookBack<BLOCK> place{status, i, n, size, capacity, offsets, &sh_off, &e};
   if (ok && size > 0) {
-    if (off + size <= capacity) {
-      const uint64_t rows = dgc::location_leaves<DevCtx<BLOCK>, dgc::EMIT_FILL>(c, blob, area, ids + off, cnt + off,
-                                                                              size, &e);
-      if (threadIdx.x == 0 && rows != size) e |= DGP_ERR_SIZE;
-    } else if (threadIdx.x == 0) {
-      e |= DGP_ERR_BUFFER;
-    }
+    const uint64_t rows =
+        dgc::location_leaves<DevCtx<BLOCK>, dgc::EMIT_FILL>(c, blob, area, ids, cnt, size, &e, place);
+    if (threadIdx.x == 0 && place.fits && rows != size) e |= DGP_ERR_SIZE;
+  } else {
+    bool go;
+    place(c, &go);
   }
   if (e) atomicOr(err, e);
 }

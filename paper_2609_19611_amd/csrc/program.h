@@ -74,7 +74,7 @@ struct DgpFactor {
   int32_t cap;   // capacity (entries)
   int32_t off;   // offset of the values in the factor-value area (in uint64 units)
   int32_t size;  // extent of the tensor dimension the factor lives on
-  int32_t pad;
+  int32_t stat;  // 1: used by a single-term leaf (its nonzero count and maximum are taken)
 };
 
 // One separable term of a leaf: coef = (coef_slot < 0 ? 1 : scalar) * coef_const.
