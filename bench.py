@@ -72,6 +72,31 @@ def copy_calibration(gib, steps, warmup):
                       "fill_ms": ms_fill, "fill_GBps_write": n * 4 / (ms_fill * 1e-3) / 1e9}), flush=True)
 
 
+KERNEL_SOURCES = ["program.h", "core.h", "kernels_dev.h", "jit_source.cpp", "jit.cpp", "compile.cpp", "graph.cpp"]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "dg_enumerate_hbm_traffic.txt")
+
+
+def measured_traffic(workload):
+    """HBM bytes per dg_enumerate launch from the committed rocprofv3 counter
+    summary (FETCH_SIZE and WRITE_SIZE scaled by a copy of known size), or
+    None when the kernel sources have changed since it was taken."""
+    import hashlib
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, "paper_2609_19611_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    stored, traffic = None, None
+    for line in open(TRAFFIC_FILE):
+        parts = line.split()
+        if len(parts) == 2 and parts[0] == "kernel_sources_sha256":
+            stored = parts[1]
+        if len(parts) == 3 and parts[0] == "traffic_bytes_per_launch" and parts[1] == workload:
+            traffic = int(parts[2])
+    return traffic if stored == h.hexdigest() else None
+
+
 def git_sha():
     try:
         return subprocess.check_output(["git", "rev-parse", "--short", "HEAD"], cwd=ROOT,
@@ -241,8 +266,10 @@ def main():
                    "lds_bytes": info["lds_bytes"], "path": "two-pass" if args.two_pass else "single-pass",
                    "kernels": "specialized" if specialized else "interpreted"},
         "roofline": {"bound": "hbm", "kernel": kernel, "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": achieved / HBM_PEAK_GBS, "traffic": None, "kernel_ms": kern_ms,
-                     "algorithmic_bytes": alg_bytes},
+                     "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": measured_traffic(args.workload) if kernel == "dg_enumerate" else None,
+                     "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE x2 + WRITE_SIZE x1)",
+                     "kernel_ms": kern_ms, "algorithmic_bytes": alg_bytes},
     }
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(args.workload, text, None, locs, args.cpu_seconds)
