@@ -2,6 +2,8 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
+#include <tuple>
 #include <cstring>
 #include <map>
 #include <cstdlib>
@@ -31,6 +33,10 @@ struct dg_graph {
   std::mutex mu;
   std::map<int, uint8_t*> dev_blob;  // compiled plan per device
   std::map<int, DevKernels> jit;     // specialised kernels per device
+  uint64_t serial = 0;               // unique per graph in the process
+  // Specialised comparison kernels with another graph: (device, other's
+  // serial, block) -> kernels.
+  std::map<std::tuple<int, uint64_t, int>, DevKernels> pair_jit;
 };
 
 namespace {
@@ -64,6 +70,8 @@ int max_lds_per_block() {
 // Finishes a freshly parsed graph: compile, pick the block size and the LDS
 // footprint of one location.
 dg_status finalize(dg_graph* g) {
+  static std::atomic<uint64_t> next_serial{1};
+  g->serial = next_serial++;
   g->plan = dg::compile_plan(g->ir);
   g->block = g->plan.max_row_size >= 4096 ? 256 : 64;
   // Tuning override of the block size (specialised kernels only).
@@ -112,6 +120,22 @@ const dg::JitModule* graph_jit(const dg_graph* cg) {
     k.tried = true;
     k.ok = dg::jit_load(dg::jit_enum_source(g->plan, g->block), &k.jm, &k.log) && k.jm.sizes && k.jm.fill &&
            k.jm.enumerate;
+  }
+  return k.ok ? &k.jm : nullptr;
+}
+
+// Specialised comparison kernel of the pair (a, b) on the current device;
+// nullptr when specialisation is off or failed.
+const dg::JitModule* pair_jit(const dg_graph* ca, const dg_graph* b, const dgc::PairPlan& pp, int block) {
+  if (!dg::jit_enabled()) return nullptr;
+  dg_graph* a = const_cast<dg_graph*>(ca);
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return nullptr;
+  std::lock_guard<std::mutex> lock(a->mu);
+  DevKernels& k = a->pair_jit[std::make_tuple(dev, b->serial, block)];
+  if (!k.tried) {
+    k.tried = true;
+    k.ok = dg::jit_load(dg::jit_compare_source(a->plan, b->plan, pp, block), &k.jm, &k.log) && k.jm.compare;
   }
   return k.ok ? &k.jm : nullptr;
 }
@@ -397,7 +421,11 @@ dg_status dg_compare(const dg_graph* a, const dg_graph* b, const int64_t* d_locs
       return set_error(DG_E_SIGNATURE, "output shape differs");
     // Comparison rows are compared in LDS, not written: one wave per
     // location keeps its many barriers cheap.
-    const int block = 64;
+    int block = 64;
+    if (const char* e = std::getenv("DIRIGO_CMP_BLOCK")) {
+      const int v = std::atoi(e);
+      if (v == 64 || v == 128 || v == 256) block = v;
+    }
     dgc::PairPlan pp;
     dg::pair_plan(a->plan, b->plan, block, &pp);
     if (pp.lds_bytes > (uint32_t)max_lds_per_block())
@@ -413,11 +441,17 @@ dg_status dg_compare(const dg_graph* a, const dg_graph* b, const int64_t* d_locs
     uint32_t* err = reinterpret_cast<uint32_t*>(ws + w.err);
     int64_t* flags = reinterpret_cast<int64_t*>(ws + w.flags);
     DG_HIP(dgk::launch_zero(err, s), "zero");
-    dgc::PairPlan* d_pp = reinterpret_cast<dgc::PairPlan*>(ws + w.pair);
-    // Pageable source: the copy has completed when the call returns.
-    DG_HIP(hipMemcpyAsync(d_pp, &pp, sizeof(pp), hipMemcpyHostToDevice, s), "copy pair plan");
-    DG_HIP(dgk::launch_compare(ba, bb, d_pp, pp.lds_bytes, d_locs, n, d_status, flags, err, block, s),
-           "compare kernel");
+    if (const dg::JitModule* jm = pair_jit(a, b, pp, block)) {
+      void* args[] = {(void*)&d_locs, &n, &d_status, &flags, &err};
+      DG_HIP(launch_module(jm->compare, n, block, pp.lds_bytes, s, args), "compare kernel");
+    } else {
+      if (block != 64 && block != 256) return set_error(DG_E_INVALID_ARG, "block size needs specialised kernels");
+      dgc::PairPlan* d_pp = reinterpret_cast<dgc::PairPlan*>(ws + w.pair);
+      // Pageable source: the copy has completed when the call returns.
+      DG_HIP(hipMemcpyAsync(d_pp, &pp, sizeof(pp), hipMemcpyHostToDevice, s), "copy pair plan");
+      DG_HIP(dgk::launch_compare(ba, bb, d_pp, pp.lds_bytes, d_locs, n, d_status, flags, err, block, s),
+             "compare kernel");
+    }
     DG_HIP(dgk::launch_scan(flags, n, reinterpret_cast<int64_t*>(ws + w.sums), s), "scan");
     DG_HIP(dgk::launch_scatter_mismatch(d_status, flags, n, d_mismatch, s), "scatter");
     int64_t total = 0;

@@ -96,6 +96,70 @@ bool fn_uses(const IndexFn& f, int v) {
 
 double sat(double x) { return std::isfinite(x) ? x : 1e300; }
 
+// ------------------------------------------------- anchored coordinate ranges
+// Static capacities of factors and of a leaf's per-dim unions.  A factor's
+// range is bounded relative to a linear form of the output coordinates (see
+// FactorPos); merging factors with the same form (a linear combination, a
+// union of terms) then costs the hull of their offsets instead of the whole
+// dimension.  The bounds mirror the device's range computation (core.h
+// ifn_range, target_range): each index term is bounded on its own, floor
+// divisions widen by (q - 1) / q, clamping to the tensor only shrinks.
+
+Frac frac(int64_t n, int64_t d = 1) {
+  if (d < 0) {
+    n = -n;
+    d = -d;
+  }
+  int64_t g = std::gcd(n < 0 ? -n : n, d);
+  if (g > 1) {
+    n /= g;
+    d /= g;
+  }
+  return Frac{n, d};
+}
+Frac operator+(Frac a, Frac b) { return frac(a.n * b.d + b.n * a.d, a.d * b.d); }
+Frac operator-(Frac a, Frac b) { return frac(a.n * b.d - b.n * a.d, a.d * b.d); }
+Frac operator*(Frac a, int64_t k) { return frac(a.n * k, a.d); }
+Frac operator/(Frac a, int64_t k) { return frac(a.n, a.d * k); }
+bool operator<(Frac a, Frac b) { return a.n * b.d < b.n * a.d; }
+bool operator==(Frac a, Frac b) { return a.n == b.n && a.d == b.d; }
+int64_t floor_frac(Frac a) { return floor_div(a.n, a.d); }
+
+using Anchor = std::vector<std::pair<int, Frac>>;
+
+Anchor anchor_axpy(const Anchor& x, Frac k, const Anchor& y) {  // x + k*y
+  std::map<int, Frac> m;
+  for (const auto& e : x) m[e.first] = e.second;
+  for (const auto& e : y) {
+    Frac v = m.count(e.first) ? m[e.first] : Frac{0, 1};
+    m[e.first] = v + Frac{e.second.n * k.n, 1} / (e.second.d * k.d);
+  }
+  Anchor r;
+  for (const auto& e : m)
+    if (e.second.n != 0) r.push_back({e.first, frac(e.second.n, e.second.d)});
+  return r;
+}
+
+bool same_anchor(const Anchor& a, const Anchor& b) {
+  if (a.size() != b.size()) return false;
+  for (size_t i = 0; i < a.size(); ++i)
+    if (a[i].first != b[i].first || !(a[i].second == b[i].second)) return false;
+  return true;
+}
+
+// Coordinates a hull of positions can span; -1 when unbounded (unknown
+// position or different anchors).
+int64_t hull_bound(const std::vector<const FactorPos*>& ps) {
+  if (ps.empty()) return -1;
+  Frac lo = ps[0]->lo, hi = ps[0]->hi;
+  for (const FactorPos* p : ps) {
+    if (!p->known || !same_anchor(p->a, ps[0]->a)) return -1;
+    if (p->lo < lo) lo = p->lo;
+    if (hi < p->hi) hi = p->hi;
+  }
+  return floor_frac(hi - lo) + 1;
+}
+
 class Compiler {
  public:
   explicit Compiler(const GraphIR& g) : g_(g) {}
@@ -105,6 +169,7 @@ class Compiler {
   const GraphIR& g_;
   std::vector<DgpInstr> ins_;
   std::vector<DgpFactor> fac_;
+  std::vector<FactorPos> pos_;
   std::vector<double> fbound_;
   std::vector<double> sbound_;
   std::map<std::string, int> memo_;
@@ -115,6 +180,7 @@ class Compiler {
     f.cap = (int32_t)std::max<int64_t>(1, cap);
     f.size = (int32_t)size;
     fac_.push_back(f);
+    pos_.push_back(FactorPos{});
     fbound_.push_back(sat(bound));
     return (int)fac_.size() - 1;
   }
@@ -135,6 +201,8 @@ class Compiler {
     auto it = memo_.find(key);
     if (it != memo_.end()) return it->second;
     int f = new_factor(1, g_.tensors[g_.output].shape[a], 1.0);
+    pos_[f].known = true;
+    pos_[f].a = {{a, Frac{1, 1}}};
     DgpInstr i = blank(DGP_ROOT);
     i.dst = f;
     i.a = a;
@@ -147,6 +215,8 @@ class Compiler {
     auto it = memo_.find(key);
     if (it != memo_.end()) return it->second;
     int f = new_factor(1, size, 1.0);
+    pos_[f].known = true;
+    pos_[f].lo = pos_[f].hi = frac(v);
     DgpInstr i = blank(DGP_CONST);
     i.dst = f;
     i.a = (int32_t)v;
@@ -225,7 +295,16 @@ class Compiler {
     auto it = memo_.find(key.str());
     if (it != memo_.end()) return it->second;
     int64_t cap = size <= kLincombFullDim ? size : std::min<int64_t>(size, (int64_t)fac_[f1].cap + fac_[f2].cap);
+    const int64_t hb = hull_bound({&pos_[f1], &pos_[f2]});
+    if (hb > 0) cap = std::min(cap, hb);
+    FactorPos hp;
+    if (hb > 0) {
+      hp = pos_[f1];
+      if (pos_[f2].lo < hp.lo) hp.lo = pos_[f2].lo;
+      if (hp.hi < pos_[f2].hi) hp.hi = pos_[f2].hi;
+    }
     int f = new_factor(cap, size, fbound_[f1] * coef_bound(c1) + fbound_[f2] * coef_bound(c2));
+    pos_[f] = hp;
     DgpInstr i = blank(DGP_LINCOMB);
     i.dst = f;
     i.f1 = f1;
@@ -288,6 +367,60 @@ class Compiler {
     k << "[" << f.c << "," << f.mode << "," << f.s << "," << size;
     for (const auto& t : f.terms) k << ";" << local[t.var] << "," << t.coef << "," << t.vdiv;
     k << "]";
+  }
+
+  // Position of a component's target index (see FactorPos), from the
+  // positions of its factor variables and the ranges of its window
+  // variables.
+  FactorPos target_pos(const IndexFn& f, const SymTerm& t, const std::vector<int>& vars, int R, const ReadGroup& G) {
+    FactorPos r;
+    Anchor A;
+    Frac L = frac(f.c), H = frac(f.c);
+    for (const auto& tm : f.terms) {
+      const int v = tm.var;
+      if (std::find(vars.begin(), vars.end(), v) == vars.end()) return FactorPos{};
+      Anchor va;
+      Frac vlo, vhi;
+      bool may_be_negative = false;
+      if (v < R) {
+        const FactorPos& p = pos_[t.f[v]];
+        if (!p.known) return FactorPos{};
+        va = p.a;
+        vlo = p.lo;
+        vhi = p.hi;
+      } else {
+        vlo = frac(G.wlo[v - R]);
+        vhi = frac(G.whi[v - R] - 1);
+        may_be_negative = G.wlo[v - R] < 0;
+      }
+      const int64_t q = tm.vdiv;
+      Frac lo = vlo, hi = vhi;
+      if (q != 1) {
+        // Device: truncating division of a value in [vlo, vhi].
+        const Frac w = frac(q - 1, q);
+        lo = vlo / q - w;
+        hi = may_be_negative ? vhi / q + w : vhi / q;
+      }
+      A = anchor_axpy(A, frac(tm.coef, q), va);
+      if (tm.coef >= 0) {
+        L = L + lo * tm.coef;
+        H = H + hi * tm.coef;
+      } else {
+        L = L + hi * tm.coef;
+        H = H + lo * tm.coef;
+      }
+    }
+    if (f.mode == 1 || f.mode == 2) {
+      A = anchor_axpy(Anchor{}, frac(1, f.s), A);
+      L = L / f.s;
+      H = H / f.s;
+      if (f.mode == 2) L = L - frac(f.s - 1, f.s);
+    }
+    r.known = true;
+    r.a = A;
+    r.lo = L;
+    r.hi = H;
+    return r;
   }
 
   // Sum over one component.  Returns a factor slot (target != nullptr) or a
@@ -366,7 +499,10 @@ class Compiler {
         span += std::llabs(tm.coef) * ceil_div(w - 1, tm.vdiv);
       }
       int64_t count = (target->mode ? ceil_div(span, target->s) : span) + 1;
+      FactorPos tp = target_pos(*target, t, vars, R, G);
+      if (tp.known) count = std::min(count, floor_frac(tp.hi - tp.lo) + 1);
       slot = new_factor(std::min(count, tsize), tsize, points * weight);
+      pos_[slot] = tp;
       i.target = to_dev(*target, local, tsize);
       i.dst_is_scalar = 0;
     } else {
@@ -535,7 +671,13 @@ Plan Compiler::run() {
     int64_t ucount = 0, cells = ts.empty() ? 0 : 1;
     for (int d = 0; d < L.rank; ++d) {
       int64_t u = 0;
-      for (const SymTerm& t : ts) u += fac_[t.f[d]].cap;
+      std::vector<const FactorPos*> ps;
+      for (const SymTerm& t : ts) {
+        u += fac_[t.f[d]].cap;
+        ps.push_back(&pos_[t.f[d]]);
+      }
+      const int64_t hb = hull_bound(ps);
+      if (hb > 0) u = std::min(u, hb);
       u = std::min<int64_t>(u, T.shape[d]);
       L.ucap[d] = (int32_t)std::max<int64_t>(u, 1);
       ucount += L.ucap[d];
@@ -682,6 +824,7 @@ Plan Compiler::run() {
   std::memcpy(plan.blob.data() + h.level_off, level_start.data(), level_start.size() * sizeof(int32_t));
   plan.max_row_size = max_row;
   plan.count_bound = cbound;
+  plan.fpos = pos_;
   return plan;
 }
 
@@ -705,6 +848,8 @@ void pair_plan(const Plan& a, const Plan& b, int nthreads, dgc::PairPlan* pp) {
   pp->nleaf = ha.nleaf;
   const DgpLeaf* la = reinterpret_cast<const DgpLeaf*>(a.blob.data() + ha.leaf_off);
   const DgpLeaf* lb = reinterpret_cast<const DgpLeaf*>(b.blob.data() + hb.leaf_off);
+  const DgpTerm* ta = reinterpret_cast<const DgpTerm*>(a.blob.data() + ha.term_off);
+  const DgpTerm* tb = reinterpret_cast<const DgpTerm*>(b.blob.data() + hb.term_off);
   int64_t emit = 0, uni = 0;
   for (int l = 0; l < ha.nleaf; ++l) {
     const DgpLeaf &x = la[l], &y = lb[l];
@@ -715,6 +860,13 @@ void pair_plan(const Plan& a, const Plan& b, int nthreads, dgc::PairPlan* pp) {
     for (int d = 0; d < DGP_MAX_RANK; ++d) {
       if (d < x.rank) {
         int64_t u = (x.nterm > 0 ? (int64_t)x.ucap[d] : 0) + (y.nterm > 0 ? (int64_t)y.ucap[d] : 0);
+        // Both graphs' positions are anchored on the same output
+        // coordinates, so their union is bounded by the joint hull.
+        std::vector<const FactorPos*> ps;
+        for (int t = 0; t < x.nterm; ++t) ps.push_back(&a.fpos[ta[x.term0 + t].factor[d]]);
+        for (int t = 0; t < y.nterm; ++t) ps.push_back(&b.fpos[tb[y.term0 + t].factor[d]]);
+        const int64_t hb = hull_bound(ps);
+        if (hb > 0) u = std::min(u, hb);
         u = std::min<int64_t>(u, x.shape[d]);
         S.ucap[d] = (int32_t)std::max<int64_t>(u, 1);
         ucount += S.ucap[d];

@@ -10,11 +10,28 @@
 
 namespace dg {
 
+// Exact rational number (small numerators and denominators).
+struct Frac {
+  int64_t n = 0, d = 1;
+};
+
+// Where a factor's coordinate range can lie, for every location: each value
+// v it covers satisfies  A(r) + lo <= v <= A(r) + hi,  with A a rational
+// linear form in the output coordinates r (root dim -> coefficient).  Two
+// factors with the same A have a hull of at most floor(hi - lo) + 1
+// coordinates however the location moves.
+struct FactorPos {
+  bool known = false;
+  std::vector<std::pair<int, Frac>> a;  // sorted by root dim, no zero coefficients
+  Frac lo, hi;
+};
+
 struct Plan {
   std::vector<uint8_t> blob;  // DgpHeader followed by the instruction, factor, leaf and term arrays
   int64_t max_row_size = 0;   // static bound on entries per row
   double count_bound = 0;     // static bound on one path count
   int max_leaf_terms = 0;
+  std::vector<FactorPos> fpos;  // per factor (host side only)
 
   const DgpHeader& header() const { return *reinterpret_cast<const DgpHeader*>(blob.data()); }
 };

@@ -139,6 +139,31 @@ int dgh_jit_source(const char* text, int64_t len, int block, char* out, int64_t 
   }
 }
 
+// Source of the specialised comparison kernel of a pair of graphs.
+int dgh_jit_compare_source(const char* ta, int64_t la, const char* tb, int64_t lb, int block, char* out,
+                           int64_t cap) {
+  try {
+    dg::GraphIR ia = dg::parse_dgir(std::string(ta, (size_t)la));
+    dg::GraphIR ib = dg::parse_dgir(std::string(tb, (size_t)lb));
+    dg::Plan pa = dg::compile_plan(ia), pb = dg::compile_plan(ib);
+    dgc::PairPlan pp;
+    dg::pair_plan(pa, pb, block, &pp);
+    std::string s = dg::jit_compare_source(pa, pb, pp, block);
+    snprintf(out, (size_t)cap, "%s", s.c_str());
+    return (int)s.size();
+  } catch (const dg::Failure& e) {
+    return fail_with(e);
+  }
+}
+
+// hipRTC options of the specialised kernels, space separated.
+int dgh_jit_options(char* out, int64_t cap) {
+  std::string s;
+  for (const char* const* o = dg::jit_compile_options(); *o; ++o) s += std::string(s.empty() ? "" : " ") + *o;
+  snprintf(out, (size_t)cap, "%s", s.c_str());
+  return (int)s.size();
+}
+
 // Human-readable listing of a graph's compiled plan (for tests and tuning).
 int dgh_dump(const char* text, int64_t len, char* out, int64_t cap) {
   try {

@@ -30,12 +30,10 @@ bool compile(const std::string& src, std::vector<char>* code, std::string* log) 
     *log = "hiprtcCreateProgram failed";
     return false;
   }
-  // Same code-generation footing as the precompiled kernels: packed FP32
-  // instructions stay off.
-  const char* opts[] = {"--offload-arch=gfx950", "-O3",     "-std=c++17",      "-mllvm",
-                        "-amdgpu-early-inline-all=true",   "-Wno-pass-failed", "-Xclang",
-                        "-target-feature",                 "-Xclang",          "-packed-fp32-ops"};
-  hiprtcResult r = hiprtcCompileProgram(prog, (int)(sizeof(opts) / sizeof(opts[0])), opts);
+  const char* const* opts = jit_compile_options();
+  int nopt = 0;
+  while (opts[nopt]) ++nopt;
+  hiprtcResult r = hiprtcCompileProgram(prog, nopt, const_cast<const char**>(opts));
   size_t n = 0;
   hiprtcGetProgramLogSize(prog, &n);
   if (n > 1) {

@@ -22,6 +22,9 @@ std::string jit_enum_source(const Plan& p, int block);
 // Source of the specialised comparison kernel (dg_compare) of a pair.
 std::string jit_compare_source(const Plan& a, const Plan& b, const dgc::PairPlan& pp, int block);
 
+// hipRTC options of the specialised kernels (null-terminated list).
+const char* const* jit_compile_options();
+
 }  // namespace dg
 
 #if defined(__HIP_PLATFORM_AMD__) || defined(__HIPCC__)

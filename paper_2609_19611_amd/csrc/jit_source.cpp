@@ -24,7 +24,16 @@ const char* kPrelude =
     "#define DGC __device__ __forceinline__\n"
     "#include \"kernels_dev.h\"\n";
 
+// Same code-generation footing as the precompiled kernels: packed FP32
+// instructions stay off.
+const char* const kOptions[] = {"--offload-arch=gfx950", "-O3",     "-std=c++17",      "-mllvm",
+                                "-amdgpu-early-inline-all=true",   "-Wno-pass-failed", "-Xclang",
+                                "-target-feature",                 "-Xclang",          "-packed-fp32-ops",
+                                nullptr};
+
 }  // namespace
+
+const char* const* jit_compile_options() { return kOptions; }
 
 std::string jit_enum_source(const Plan& p, int block) {
   std::ostringstream o;

@@ -1,0 +1,98 @@
+"""The per-graph specialised kernels compile (hipRTC cross-compiles for
+gfx950 without a GPU): the sources the library generates for the workloads
+and for a comparison pair, with the library's own options and headers, and
+no private (scratch) memory in the resulting kernels."""
+
+import ctypes
+import os
+import re
+import subprocess
+import tempfile
+
+import pytest
+
+import hostemu
+from paper_2609_19611_amd import workloads as W
+
+CSRC = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "paper_2609_19611_amd", "csrc")
+HIPRTC = "/opt/rocm/lib/libhiprtc.so"
+READELF = "/opt/rocm/llvm/bin/llvm-readelf"
+
+pytestmark = pytest.mark.skipif(not os.path.exists(HIPRTC), reason="hipRTC not installed")
+
+
+def _rtc():
+    L = ctypes.CDLL(HIPRTC)
+    P = ctypes.c_void_p
+    L.hiprtcCreateProgram.argtypes = [ctypes.POINTER(P), ctypes.c_char_p, ctypes.c_char_p, ctypes.c_int,
+                                      ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(ctypes.c_char_p)]
+    L.hiprtcCompileProgram.argtypes = [P, ctypes.c_int, ctypes.POINTER(ctypes.c_char_p)]
+    L.hiprtcGetCodeSize.argtypes = [P, ctypes.POINTER(ctypes.c_size_t)]
+    L.hiprtcGetCode.argtypes = [P, ctypes.c_char_p]
+    L.hiprtcGetProgramLogSize.argtypes = [P, ctypes.POINTER(ctypes.c_size_t)]
+    L.hiprtcGetProgramLog.argtypes = [P, ctypes.c_char_p]
+    L.hiprtcDestroyProgram.argtypes = [ctypes.POINTER(P)]
+    return L
+
+
+def _compile(src):
+    L = _rtc()
+    names = ["program.h", "core.h", "kernels_dev.h"]
+    texts = [open(os.path.join(CSRC, n), "rb").read() for n in names]
+    hdr = (ctypes.c_char_p * 3)(*texts)
+    nm = (ctypes.c_char_p * 3)(*[n.encode() for n in names])
+    prog = ctypes.c_void_p()
+    assert L.hiprtcCreateProgram(ctypes.byref(prog), src.encode(), b"dg_plan.hip", 3, hdr, nm) == 0
+    buf = ctypes.create_string_buffer(4096)
+    hostemu.lib().dgh_jit_options(buf, 4096)
+    opts = buf.value.decode().split()
+    arr = (ctypes.c_char_p * len(opts))(*[o.encode() for o in opts])
+    rc = L.hiprtcCompileProgram(prog, len(opts), arr)
+    n = ctypes.c_size_t()
+    L.hiprtcGetProgramLogSize(prog, ctypes.byref(n))
+    log = ctypes.create_string_buffer(max(1, n.value))
+    L.hiprtcGetProgramLog(prog, log)
+    assert rc == 0, log.value.decode()[-2000:]
+    L.hiprtcGetCodeSize(prog, ctypes.byref(n))
+    code = ctypes.create_string_buffer(n.value)
+    L.hiprtcGetCode(prog, code)
+    L.hiprtcDestroyProgram(ctypes.byref(prog))
+    return code.raw
+
+
+def _kernel_notes(code):
+    """(name, private segment bytes) of every kernel in a code object."""
+    with tempfile.NamedTemporaryFile(suffix=".co") as f:
+        f.write(code)
+        f.flush()
+        out = subprocess.run([READELF, "--notes", f.name], capture_output=True, text=True).stdout
+    names = re.findall(r"^\s+\.name:\s+(\S+)", out, re.M)
+    priv = [int(x) for x in re.findall(r"\.private_segment_fixed_size:\s+(\d+)", out)]
+    return list(zip(names, priv))
+
+
+def _source(fn, *args):
+    buf = ctypes.create_string_buffer(1 << 24)
+    n = fn(*args, buf, 1 << 24)
+    assert n > 0, hostemu.lib().dgh_error().decode()
+    return buf.value.decode()
+
+
+@pytest.mark.parametrize("name,block", [("c1", 64), ("c3", 256), ("c4", 256)])
+def test_enumeration_kernels_compile(name, block):
+    t = W.CONFIGS[name]["text"]().encode()
+    src = _source(hostemu.lib().dgh_jit_source, t, len(t), block)
+    code = _compile(src)
+    notes = _kernel_notes(code)
+    assert {n for n, _ in notes} >= {"dg_sizes", "dg_fill", "dg_enumerate"}
+    if os.path.exists(READELF):
+        assert all(p == 0 for _, p in notes), notes
+
+
+def test_comparison_kernel_compiles():
+    a = W.c5_reference_text(n=2, c=4, hw=6, co=3).encode()
+    b = W.c5_variant_text(fault=W.c5_faults()[0], n=2, c=4, hw=6, co=3).encode()
+    src = _source(hostemu.lib().dgh_jit_compare_source, a, len(a), b, len(b), 64)
+    notes = _kernel_notes(_compile(src))
+    assert [n for n, _ in notes] == ["dg_compare"]
+    assert all(p == 0 for _, p in notes), notes
