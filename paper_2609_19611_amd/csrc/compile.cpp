@@ -799,6 +799,9 @@ Plan Compiler::run() {
   h.union_entries = (int32_t)union_entries;
   h.nlevel = (int32_t)level_start.size() - 1;
   h.serial_vars = serial_vars;
+  // (Bounds are products and sums of integers; below 2^53 doubles hold
+  // them exactly.)
+  h.no_overflow = cbound <= 4294967295.0 ? 1 : 0;
   size_t off = (sizeof(DgpHeader) + 15) & ~size_t(15);
   h.instr_off = (int32_t)off;
   off += ins_.size() * sizeof(DgpInstr);

@@ -75,10 +75,9 @@ struct LeafHdr {
   int32_t hlo[DGP_MAX_RANK];    // first coordinate of the dim's hull
   int32_t dense[DGP_MAX_RANK];  // every hull coordinate is nonzero: no list, x = hlo + i
   uint64_t cnt[DGP_MAX_RANK];   // nonzero coordinates per dim (block total)
-  uint64_t umax[DGP_MAX_RANK];  // largest factor value on the union (several terms)
   int32_t ok;                   // the prepared leaf has entries
   uint32_t O, In;               // outer and inner table lengths
-  int32_t pad;
+  int32_t notab;                // cells are evaluated from the factors directly (no tables)
 };
 
 struct EmitLayout {
@@ -532,19 +531,29 @@ DGC void factor_stats(C& c, const uint8_t* blob, uint8_t* area, const PlanLayout
   FStat* st = (FStat*)(area + PL.fstat);
   const int tid = c.tid(), nt = c.nthreads();
   const int nf = h->nfactor;
+  // Factors of at most 64 values are taken by one wave each, in turn.
+  const int nwave = nt >= 64 ? nt / 64 : 1;
+  const int wave = nt >= 64 ? tid / 64 : 0;
+  int small = 0;
   DG_PLAN_UNROLL
   for (int f = 0; f < nf; ++f) {
     if (!fac[f].stat) continue;
+    int32_t x0 = tid, step = nt;
+    if (nt >= 64 && fac[f].cap <= 64) {
+      if (small++ % nwave != wave) continue;
+      x0 = tid & 63;
+      step = 64;
+    }
     const int32_t len = meta[2 * f + 1];
     const uint64_t* v = fval + fac[f].off;
     uint64_t cnt = 0, mx = 0;
-    for (int32_t x = tid; x < len; x += nt) {
+    for (int32_t x = x0; x < len; x += step) {
       const uint64_t a = v[x];
       cnt += a != 0 ? 1u : 0u;
       mx = a > mx ? a : mx;
     }
     c.reduce_add(&st[f].nnz, cnt);
-    c.reduce_max(&st[f].vmax, mx);
+    if (!h->no_overflow) c.reduce_max(&st[f].vmax, mx);
   }
   c.sync();
 }
@@ -595,8 +604,7 @@ DGC void term_hull(const TermRef* terms, int nterm, int d, int32_t* lo, int32_t*
 // Per dim, the union of the terms' nonzero coordinates: its size, whether it
 // is the whole hull (dense: coordinate i of the union is hlo + i) and, for
 // the other dims when `lists` is set, the sorted coordinates in `ulist`.
-// Also the largest factor value per dim (used for a single term).  Returns
-// false (leaf empty) if some dim has no nonzero coordinate.
+// Returns false (leaf empty) if some dim has no nonzero coordinate.
 //
 // With `st` (a single term), the factor statistics give the counts and the
 // counting pass is skipped.
@@ -606,29 +614,21 @@ DGC bool build_union(C& c, const TermRef* terms, int nterm, int rank, const int3
   const uint64_t* a64 = (const uint64_t*)area;
   const int tid = c.tid(), nt = c.nthreads();
   if (!st) {
-    for (int i = tid; i < DGP_MAX_RANK; i += nt) {
-      H->cnt[i] = 0;
-      H->umax[i] = 0;
-    }
+    for (int i = tid; i < DGP_MAX_RANK; i += nt) H->cnt[i] = 0;
     c.sync();
     // Counts: one pass over every dim, one barrier.
     DG_PLAN_UNROLL
     for (int d = 0; d < rank; ++d) {
       int32_t hlo, hhi;
       term_hull(terms, nterm, d, &hlo, &hhi);
-      uint64_t cnt = 0, vmax = 0;
+      uint64_t cnt = 0;
       for (int32_t x = hlo + tid; x < hhi; x += nt) {
         bool nz = false;
         DG_PLAN_UNROLL
-        for (int t = 0; t < nterm; ++t) {
-          const uint64_t v = term_val(terms[t], d, x, a64);
-          nz = nz || v != 0;
-          if (v > vmax) vmax = v;
-        }
+        for (int t = 0; t < nterm; ++t) nz = nz || term_val(terms[t], d, x, a64) != 0;
         cnt += nz ? 1u : 0u;
       }
       c.reduce_add(&H->cnt[d], cnt);
-      c.reduce_max(&H->umax[d], vmax);
     }
     c.sync();
   }
@@ -688,7 +688,8 @@ struct LeafGeom {
 };
 
 // Builds one table: entries r < n over dims [d0, d1); entry = (id part,
-// count part of every term).  Records each term's largest value in tmax.
+// count part of every term).  With `tmax`, records each term's largest
+// value there (per-thread maxima, combined once per wave and term).
 template <class C>
 DGC void build_table(C& c, const LeafGeom& G, const TermRef* terms, int nterm, const int32_t* ulist,
                      const LeafHdr* H, int d0, int d1, bool with_base, uint32_t n, uint32_t* tab, uint64_t* tmax,
@@ -697,11 +698,9 @@ DGC void build_table(C& c, const LeafGeom& G, const TermRef* terms, int nterm, c
   int32_t u[DGP_MAX_RANK];
   DG_UNROLL
   for (int d = 0; d < DGP_MAX_RANK; ++d) u[d] = H->u[d];
-  uint64_t m1 = 0;  // a single term's largest value, combined once per wave
-  for (uint32_t r = (uint32_t)c.tid(); r < n; r += (uint32_t)c.nthreads()) {
+  // Coordinates of entry r (row-major over the union lists of [d0, d1)).
+  auto coords = [&](uint32_t r, int32_t* x) {
     uint32_t rem = r;
-    int32_t x[DGP_MAX_RANK];
-    uint32_t pos = with_base ? G.base : 0u;
     DG_UNROLL
     for (int d = DGP_MAX_RANK - 1; d >= 0; --d) {
       x[d] = 0;
@@ -709,22 +708,54 @@ DGC void build_table(C& c, const LeafGeom& G, const TermRef* terms, int nterm, c
         const uint32_t i = rem % (uint32_t)u[d];
         rem /= (uint32_t)u[d];
         x[d] = ucoord(H, ulist, d, (int32_t)i);
-        pos += (uint32_t)x[d] * G.stride[d];
       }
     }
+  };
+  if (nterm == 1) {
+    // One pass: id part and count part together.
+    uint64_t m = 0;
+    for (uint32_t r = (uint32_t)c.tid(); r < n; r += (uint32_t)c.nthreads()) {
+      int32_t x[DGP_MAX_RANK];
+      coords(r, x);
+      uint32_t pos = with_base ? G.base : 0u;
+      uint64_t v = with_base ? terms[0].coef : 1ull;
+      DG_UNROLL
+      for (int d = 0; d < DGP_MAX_RANK; ++d)
+        if (d >= d0 && d < d1) {
+          pos += (uint32_t)x[d] * G.stride[d];
+          if (v) v = mul_sat(v, term_val(terms[0], d, x[d], a64));
+        }
+      tab[2 * (uint64_t)r] = pos;
+      tab[2 * (uint64_t)r + 1] = v > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)v;
+      m = v > m ? v : m;
+    }
+    if (tmax) c.reduce_max(&tmax[0], m);
+    return;
+  }
+  for (uint32_t r = (uint32_t)c.tid(); r < n; r += (uint32_t)c.nthreads()) {
+    int32_t x[DGP_MAX_RANK];
+    coords(r, x);
+    uint32_t pos = with_base ? G.base : 0u;
+    DG_UNROLL
+    for (int d = 0; d < DGP_MAX_RANK; ++d)
+      if (d >= d0 && d < d1) pos += (uint32_t)x[d] * G.stride[d];
     tab[(uint64_t)r * W] = pos;
-    DG_PLAN_UNROLL
-    for (int t = 0; t < nterm; ++t) {
+  }
+  DG_PLAN_UNROLL
+  for (int t = 0; t < nterm; ++t) {
+    uint64_t m = 0;
+    for (uint32_t r = (uint32_t)c.tid(); r < n; r += (uint32_t)c.nthreads()) {
+      int32_t x[DGP_MAX_RANK];
+      coords(r, x);
       uint64_t v = with_base ? terms[t].coef : 1ull;
       DG_UNROLL
       for (int d = 0; d < DGP_MAX_RANK; ++d)
         if (d >= d0 && d < d1 && v) v = mul_sat(v, term_val(terms[t], d, x[d], a64));
       tab[(uint64_t)r * W + 1 + t] = v > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)v;
-      if (nterm == 1) m1 = v > m1 ? v : m1;
-      else if (v) c.atomic_max(&tmax[t], v);
+      m = v > m ? v : m;
     }
+    if (tmax) c.reduce_max(&tmax[t], m);
   }
-  if (nterm == 1) c.reduce_max(&tmax[0], m1);
 }
 
 DGC bool prod_overflows(uint64_t a, uint64_t b) {
@@ -738,7 +769,7 @@ DGC bool prod_overflows(uint64_t a, uint64_t b) {
 // union lengths, and the table lengths O and In.
 template <class W, int MODE>
 DGC void leaf_prepare(W& w, const LeafGeom& G, int split, const int32_t* ucap, const TermRef* terms, int na, int nb,
-                      uint8_t* area, const EmitLayout& E, const FStat* st, uint32_t* err) {
+                      uint8_t* area, const EmitLayout& E, const FStat* st, bool checks, uint32_t* err) {
   const int tid = w.tid(), nt = w.nthreads();
   const int nterm = na + nb;
   const int rank = G.rank;
@@ -749,10 +780,50 @@ DGC void leaf_prepare(W& w, const LeafGeom& G, int split, const int32_t* ucap, c
   bool ok = nterm > 0 && !(MODE != EMIT_COMPARE && na == 0);
   // A single term with a zero coefficient is identically zero.
   if (ok && single && terms[0].coef == 0) ok = false;
+  bool hull = false;
+  if (ok && MODE == EMIT_COMPARE) {
+    // A comparison needs no ordered union: it evaluates both graphs on the
+    // hull grid of all terms (cells outside every support are zero on both
+    // sides), as long as each hull fits the union's capacity.
+    bool fits = true, empty = false;
+    DG_PLAN_UNROLL
+    for (int d = 0; d < rank; ++d) {
+      int32_t hlo, hhi;
+      term_hull(terms, nterm, d, &hlo, &hhi);
+      if (hhi <= hlo) empty = true;
+      else if (hhi - hlo > ucap[d]) fits = false;
+    }
+    if (empty) {
+      ok = false;
+      hull = true;
+    } else if (fits) {
+      if (tid == 0) {
+        DG_PLAN_UNROLL
+        for (int d = 0; d < rank; ++d) {
+          int32_t hlo, hhi;
+          term_hull(terms, nterm, d, &hlo, &hhi);
+          H->u[d] = hhi - hlo;
+          H->hlo[d] = hlo;
+          H->dense[d] = 1;
+        }
+      }
+      w.sync();
+      hull = true;
+    }
+  }
   // A single term's per-dim counts are the factor statistics.
-  if (ok) ok = build_union(w, terms, nterm, rank, ucap, ulist, H, true, area, single ? st : nullptr, err);
+  if (ok && !hull) ok = build_union(w, terms, nterm, rank, ucap, ulist, H, true, area, single ? st : nullptr, err);
+  // A comparison grid that one pass of the block covers is evaluated from
+  // the factors directly: tables would cost more than they save.
+  bool notab = split < 0;
+  if (ok && MODE == EMIT_COMPARE && hull) {
+    uint64_t cells = 1;
+    DG_PLAN_UNROLL
+    for (int d = 0; d < rank; ++d) cells *= (uint64_t)H->u[d];
+    if (cells <= (uint64_t)nt) notab = true;
+  }
   uint32_t O = 1, In = 1;
-  if (ok && split >= 0) {
+  if (ok && !notab) {
     // Outer table over dims [0, split), inner over [split, rank).
     int32_t u[DGP_MAX_RANK];
     DG_UNROLL
@@ -765,21 +836,25 @@ DGC void leaf_prepare(W& w, const LeafGeom& G, int split, const int32_t* ucap, c
     const int Wd = 1 + nterm;
     uint32_t* otab = (uint32_t*)(area + E.tables);
     uint32_t* itab = otab + (uint64_t)O * Wd;
-    uint64_t* tmax = (uint64_t*)(area + E.tmax);
-    for (int i = tid; i < 2 * nterm; i += nt) tmax[i] = 0;
-    w.sync();
+    uint64_t* tmax = checks ? (uint64_t*)(area + E.tmax) : nullptr;
+    if (checks) {
+      for (int i = tid; i < 2 * nterm; i += nt) tmax[i] = 0;
+      w.sync();
+    }
     build_table(w, G, terms, nterm, ulist, H, 0, split, true, O, otab, tmax, a64);
-    build_table(w, G, terms, nterm, ulist, H, split, rank, false, In, itab, tmax + nterm, a64);
+    build_table(w, G, terms, nterm, ulist, H, split, rank, false, In, itab, checks ? tmax + nterm : nullptr, a64);
     w.sync();
     // A term whose largest outer and inner parts multiply past 32 bits has a
     // real cell with that count.
-    for (int t = tid; t < nterm; t += nt)
-      if (prod_overflows(tmax[t], tmax[nterm + t])) *err |= DGP_ERR_OVERFLOW;
+    if (checks)
+      for (int t = tid; t < nterm; t += nt)
+        if (prod_overflows(tmax[t], tmax[nterm + t])) *err |= DGP_ERR_OVERFLOW;
   }
   if (tid == 0) {
     H->ok = ok ? 1 : 0;
     H->O = O;
     H->In = In;
+    H->notab = notab ? 1 : 0;
   }
 }
 
@@ -803,7 +878,7 @@ DGC uint64_t leaf_emit(C& c, const LeafGeom& G, int split, const TermRef* terms,
   DG_UNROLL
   for (int d = 0; d < DGP_MAX_RANK; ++d) u[d] = d < rank ? H->u[d] : 1;
 
-  if (split >= 0) {
+  if (!H->notab) {
     const int W = 1 + nterm;
     const uint32_t O = H->O, In = H->In;
     const uint32_t* otab = (const uint32_t*)(area + E.tables);
@@ -1013,16 +1088,16 @@ DGC uint64_t location_leaves(C& c, const uint8_t* blob, uint8_t* area, uint32_t*
       DG_PLAN_UNROLL
       for (int d = 0; d < L.rank; ++d) {
         n *= st[T.factor[d]].nnz;
-        mx = mul_sat(mx, st[T.factor[d]].vmax);
+        if (!h->no_overflow) mx = mul_sat(mx, st[T.factor[d]].vmax);
       }
-      if (n && mx > 0xFFFFFFFFull) *err |= DGP_ERR_OVERFLOW;
+      if (!h->no_overflow && n && mx > 0xFFFFFFFFull) *err |= DGP_ERR_OVERFLOW;
       off += n;
       continue;
     }
     const LeafGeom G = leaf_geom(L);
     leaf_terms(c, blob, l, area, PL, terms);
     c.sync();
-    leaf_prepare<C, MODE>(c, G, L.split, L.ucap, terms, L.nterm, 0, area, E, st, err);
+    leaf_prepare<C, MODE>(c, G, L.split, L.ucap, terms, L.nterm, 0, area, E, st, !h->no_overflow, err);
     c.sync();
     if (!placed) {
       base = place(c, &go);
@@ -1081,6 +1156,7 @@ DGC uint32_t location_compare(C& c, const uint8_t* blob_a, const uint8_t* blob_b
   const EmitLayout E = emit_layout(PB.end, PP->max_terms, PP->union_entries, PP->emit_entries);
   plan_exec(c, blob_a, loc, area, PA, err);
   plan_exec(c, blob_b, loc, area, PB, err);
+  const bool checks = !(ha->no_overflow && hb->no_overflow);
   const DgpLeaf* la = (const DgpLeaf*)(blob_a + ha->leaf_off);
   const DgpLeaf* lb = (const DgpLeaf*)(blob_b + hb->leaf_off);
   TermRef* terms = (TermRef*)(area + E.terms);
@@ -1093,7 +1169,8 @@ DGC uint32_t location_compare(C& c, const uint8_t* blob_a, const uint8_t* blob_b
     leaf_terms(c, blob_a, l, area, PA, terms);
     leaf_terms(c, blob_b, l, area, PB, terms + na);
     c.sync();
-    leaf_prepare<C, EMIT_COMPARE>(c, G, PP->leaf[l].split, PP->leaf[l].ucap, terms, na, nb, area, E, nullptr, err);
+    leaf_prepare<C, EMIT_COMPARE>(c, G, PP->leaf[l].split, PP->leaf[l].ucap, terms, na, nb, area, E, nullptr,
+                                  checks, err);
     c.sync();
     const uint32_t s = (uint32_t)leaf_emit<C, EMIT_COMPARE>(c, G, PP->leaf[l].split, terms, na, nb, area, E,
                                                             nullptr, nullptr, 0, err);

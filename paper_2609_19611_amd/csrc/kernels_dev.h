@@ -25,12 +25,19 @@ struct DevCtx {
     atomicMax(reinterpret_cast<unsigned long long*>(p), (unsigned long long)v);
   }
   DGC void store(uint32_t* p, uint32_t v) const { __builtin_nontemporal_store(v, p); }
-  // Adds (or takes the maximum of) every thread's v into *p with four LDS
-  // atomics per wave instead of one per thread: DPP lane permutes (xor 1,
-  // xor 2, mirror within 8, mirror within 16) leave every row of 16 lanes
-  // holding its total, which the row's first lane adds.  Called by all
+  // Adds (or takes the maximum of) every thread's v into *p with at most
+  // four LDS atomics per wave instead of one per thread: DPP lane permutes
+  // (xor 1, xor 2, mirror within 8, mirror within 16) leave every row of 16
+  // lanes holding its total, which the row's first lane adds.  A wave with
+  // no nonzero value, or a single one, skips the permutes.  Called by all
   // lanes of the wave.
   DGC void reduce_add(uint64_t* p, uint64_t v) const {
+    const uint64_t m = __ballot(v != 0);
+    if (m == 0) return;
+    if ((m & (m - 1)) == 0) {  // one contributor
+      if (v) atomic_add(p, v);
+      return;
+    }
     v += dpp64<0xB1>(v);
     v += dpp64<0x4E>(v);
     v += dpp64<0x141>(v);
@@ -38,6 +45,12 @@ struct DevCtx {
     if ((threadIdx.x & 15u) == 0 && v) atomic_add(p, v);
   }
   DGC void reduce_max(uint64_t* p, uint64_t v) const {
+    const uint64_t m = __ballot(v != 0);
+    if (m == 0) return;
+    if ((m & (m - 1)) == 0) {  // one contributor
+      if (v) atomic_max(p, v);
+      return;
+    }
     v = umax(v, dpp64<0xB1>(v));
     v = umax(v, dpp64<0x4E>(v));
     v = umax(v, dpp64<0x141>(v));

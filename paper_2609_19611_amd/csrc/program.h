@@ -122,7 +122,9 @@ struct DgpHeader {
   int32_t nlevel;
   int32_t level_off;
   int32_t serial_vars;
-  int32_t pad;
+  // 1 when the static bound on every path count is below 2^32: the
+  // run-time overflow checks (factor and table maxima) are then skipped.
+  int32_t no_overflow;
 };
 
 #define DGP_MAGIC 0x44475031u  // "DGP1"
