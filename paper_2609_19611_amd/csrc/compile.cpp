@@ -170,6 +170,10 @@ class Compiler {
   std::vector<DgpInstr> ins_;
   std::vector<DgpFactor> fac_;
   std::vector<FactorPos> pos_;
+  // Per factor: number of coordinates it covers when every value is 1 and
+  // the range does not depend on the location (a single point: ROOT,
+  // CONST; a window mapped one-to-one: length of its clamped image), else 0.
+  std::vector<int64_t> unit_len_;
   std::vector<double> fbound_;
   std::vector<double> sbound_;
   std::map<std::string, int> memo_;
@@ -181,6 +185,7 @@ class Compiler {
     f.size = (int32_t)size;
     fac_.push_back(f);
     pos_.push_back(FactorPos{});
+    unit_len_.push_back(0);
     fbound_.push_back(sat(bound));
     return (int)fac_.size() - 1;
   }
@@ -201,6 +206,7 @@ class Compiler {
     auto it = memo_.find(key);
     if (it != memo_.end()) return it->second;
     int f = new_factor(1, g_.tensors[g_.output].shape[a], 1.0);
+    unit_len_[f] = 1;
     pos_[f].known = true;
     pos_[f].a = {{a, Frac{1, 1}}};
     DgpInstr i = blank(DGP_ROOT);
@@ -215,6 +221,7 @@ class Compiler {
     auto it = memo_.find(key);
     if (it != memo_.end()) return it->second;
     int f = new_factor(1, size, 1.0);
+    unit_len_[f] = 1;
     pos_[f].known = true;
     pos_[f].lo = pos_[f].hi = frac(v);
     DgpInstr i = blank(DGP_CONST);
@@ -433,14 +440,21 @@ class Compiler {
     if (target && preds.empty() && vars.size() == 1 && vars[0] < R && target->terms.size() == 1 &&
         target->terms[0].coef == 1 && target->terms[0].vdiv == 1 && target->c == 0 && target->mode == 0)
       return t.f[vars[0]];
-    bool window_only = true;
-    for (int v : vars)
-      if (v < R) window_only = false;
-    if (!target && window_only && preds.empty()) {
+    // A sum without predicates or target over window variables and over
+    // factors whose values are all 1 on a location-independent number of
+    // coordinates is that product of counts: fold it into the coefficient.
+    if (!target && preds.empty()) {
       uint64_t n = 1;
-      for (int v : vars) n *= (uint64_t)(G.whi[v - R] - G.wlo[v - R]);
-      *folded = n;
-      return -1;
+      bool foldable = true;
+      for (int v : vars) {
+        const int64_t k = v < R ? unit_len_[t.f[v]] : G.whi[v - R] - G.wlo[v - R];
+        if (k <= 0) foldable = false;
+        else n *= (uint64_t)k;
+      }
+      if (foldable) {
+        *folded = n;
+        return -1;
+      }
     }
     if (vars.size() > DGP_MAX_VARS) fail(DG_E_UNSUPPORTED_OP, "component with more than 8 variables");
     if (preds.size() > DGP_MAX_PREDS) fail(DG_E_UNSUPPORTED_OP, "component with more than 12 predicates");
@@ -503,6 +517,14 @@ class Compiler {
       if (tp.known) count = std::min(count, floor_frac(tp.hi - tp.lo) + 1);
       slot = new_factor(std::min(count, tsize), tsize, points * weight);
       pos_[slot] = tp;
+      if (preds.empty() && vars.size() == 1 && vars[0] >= R && target->mode == 0 && target->terms.size() == 1 &&
+          target->terms[0].vdiv == 1 && (target->terms[0].coef == 1 || target->terms[0].coef == -1)) {
+        // Each window point lands on its own coordinate with count 1.
+        const int64_t a = target->terms[0].coef * G.wlo[vars[0] - R] + target->c;
+        const int64_t b = target->terms[0].coef * (G.whi[vars[0] - R] - 1) + target->c;
+        const int64_t lo = std::max<int64_t>(0, std::min(a, b)), hi = std::min<int64_t>(tsize - 1, std::max(a, b));
+        unit_len_[slot] = hi >= lo ? hi - lo + 1 : 0;
+      }
       i.target = to_dev(*target, local, tsize);
       i.dst_is_scalar = 0;
     } else {
