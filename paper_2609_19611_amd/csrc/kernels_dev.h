@@ -158,6 +158,7 @@ DGC void compare_body(const uint8_t* __restrict__ blob_a,
 // and the look-back always finishes; the wait is bounded anyway.
 constexpr uint64_t ST_SIZE = 1ull << 62, ST_PREFIX = 2ull << 62, ST_VALUE = (1ull << 62) - 1;
 constexpr uint32_t LOOKBACK_SPIN_LIMIT = 1u << 24;
+constexpr int LB_WORDS = 1;  // status words read per lane and step
 
 // Offset of row i by decoupled look-back (wave 0), once the row's own size
 // has been published: the nearest predecessor whose running total is
@@ -176,18 +177,28 @@ struct LookBack {
   bool fits = false;
   DGC uint64_t operator()(DevCtx<BLOCK>&, bool* go) {
     if (threadIdx.x < 64) {
+      // Each lane reads LB_WORDS consecutive status words, so one step of
+      // the wave covers 64 * LB_WORDS predecessors.
       const int lane = (int)threadIdx.x;
       uint64_t before = 0;
-      int64_t hi = i;  // window [hi - 64, hi)
+      int64_t hi = i;  // window [hi - 64 * LB_WORDS, hi)
       uint32_t spins = 0;
       while (hi > 0) {
-        const int64_t j = hi - 64 + lane;
-        const uint64_t st =
-            j >= 0 ? __hip_atomic_load(&status[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : ST_PREFIX;
-        const uint64_t tag = st & ~ST_VALUE;
-        const uint64_t pmask = __ballot(tag == ST_PREFIX);
+        const int64_t base = hi - 64 * LB_WORDS + (int64_t)lane * LB_WORDS;
+        uint64_t st[LB_WORDS];
+        int kp = -1;  // this lane's highest word holding a running total
+#pragma unroll
+        for (int k = 0; k < LB_WORDS; ++k) {
+          const int64_t j = base + k;
+          st[k] = j >= 0 ? __hip_atomic_load(&status[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : ST_PREFIX;
+          if ((st[k] & ~ST_VALUE) == ST_PREFIX) kp = k;
+        }
+        bool missing = false;  // a word above kp has not arrived
+#pragma unroll
+        for (int k = 0; k < LB_WORDS; ++k) missing = missing || (k > kp && (st[k] & ~ST_VALUE) == 0);
+        const uint64_t pmask = __ballot(kp >= 0);
         const int top = pmask ? 63 - __clzll((long long)pmask) : -1;
-        const uint64_t waiting = __ballot(tag == 0) & (top >= 0 ? ~((2ull << top) - 1ull) : ~0ull);
+        const uint64_t waiting = __ballot(missing) & (top >= 0 ? ~((1ull << top) - 1ull) : ~0ull);
         if (waiting) {
           if (++spins > LOOKBACK_SPIN_LIMIT) {
             *e |= DGP_ERR_TIMEOUT;
@@ -196,12 +207,15 @@ struct LookBack {
           __builtin_amdgcn_s_sleep(1);
           continue;
         }
-        uint64_t v = lane >= top ? (st & ST_VALUE) : 0ull;
+        uint64_t v = 0;
+#pragma unroll
+        for (int k = 0; k < LB_WORDS; ++k)
+          if (lane > top || (lane == top && k >= kp)) v += st[k] & ST_VALUE;
 #pragma unroll
         for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
         before += v;
         if (top >= 0) break;
-        hi -= 64;
+        hi -= 64 * LB_WORDS;
       }
       if (lane == 0) {
         if (i > 0)

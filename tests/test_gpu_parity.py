@@ -297,3 +297,31 @@ def test_single_pass_small_buffer(B):
     # n = 0
     off0 = torch.full((1,), 5, dtype=torch.int64, device="cuda")
     assert B.dg_enumerate(g, d_locs[:0], off0, ids, cnt, ws) == 0 and int(off0[0]) == 0
+
+
+@pytest.mark.parametrize("K", [4096, 6144])
+@pytest.mark.parametrize("kernels", ["specialized", "interpreted"])
+def test_large_lds_graphs(B, K, kernels, monkeypatch):
+    """Graphs whose location needs more than 64 KB of LDS (a long
+    contraction): both kernel kinds launch with the larger allocation."""
+    monkeypatch.setenv("DIRIGO_JIT", "1" if kernels == "specialized" else "0")
+    text = tiny_graphs._g([("x", [2, K]), ("W", [K, 3])], [("y", "matmul", ["x", "W"], {})], "y", [2, 3])
+    g = B.dg_graph_parse(text)
+    assert B.dg_graph_info(g)["lds_bytes"] > 65536
+    locs = list(range(6))
+    off, ids, cnt = B.enumerate_locations(g, locs)
+    ro, io, co = oracle.Graph(text).enumerate(locs)
+    assert np.array_equal(off.cpu().numpy(), ro)
+    assert np.array_equal(ids.cpu().numpy().view(np.uint32), io)
+    assert np.array_equal(cnt.cpu().numpy().view(np.uint32), co)
+    off2, ids2, cnt2 = _fused(B, g, locs)
+    assert torch.equal(off, off2) and torch.equal(ids, ids2) and torch.equal(cnt, cnt2)
+
+
+def test_lds_beyond_the_device_is_rejected(B):
+    text = tiny_graphs._g([("x", [2, 8192]), ("W", [8192, 3])], [("y", "matmul", ["x", "W"], {})], "y", [2, 3])
+    g = B.dg_graph_parse(text)
+    assert B.dg_graph_info(g)["lds_bytes"] > 160 * 1024
+    with pytest.raises(B.DgError) as e:
+        B.enumerate_locations(g, [0])
+    assert e.value.name == "DG_E_CAPACITY"
