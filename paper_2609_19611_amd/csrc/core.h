@@ -895,20 +895,25 @@ DGC uint64_t leaf_emit(C& c, const LeafGeom& G, int split, const TermRef* terms,
       const int64_t head = nt >= 64 ? (int64_t)((((uintptr_t)ids) >> 2) & 63u) : 0;
       const int64_t step = nt;
       int64_t p = (int64_t)tid - head;
+      // (Single-term entries are 8-byte aligned (id part, count part)
+      // pairs: one 64-bit LDS read each, which keeps a wave's reads free of
+      // bank conflicts.)
+      const uint64_t* otab2 = (const uint64_t*)otab;
+      const uint64_t* itab2 = (const uint64_t*)itab;
       if (p >= 0 && p < tot) {
         const uint32_t r = (uint32_t)(p / In), j = (uint32_t)(p % In);
-        c.store(&ids[p], otab[2 * (uint64_t)r] + itab[2 * (uint64_t)j]);
-        c.store(&cnt[p], otab[2 * (uint64_t)r + 1] * itab[2 * (uint64_t)j + 1]);
+        const uint64_t o = otab2[r], q = itab2[j];
+        c.store(&ids[p], (uint32_t)o + (uint32_t)q);
+        c.store(&cnt[p], (uint32_t)(o >> 32) * (uint32_t)(q >> 32));
       }
       p += step;
       if (p < tot) {
         uint32_t r = (uint32_t)(p / In), j = (uint32_t)(p % In);
         const uint32_t dr = (uint32_t)(step / In), dj = (uint32_t)(step % In);
         for (; p < tot; p += step) {
-          const uint32_t* o = otab + 2 * (uint64_t)r;
-          const uint32_t* q = itab + 2 * (uint64_t)j;
-          c.store(&ids[p], o[0] + q[0]);
-          c.store(&cnt[p], o[1] * q[1]);
+          const uint64_t o = otab2[r], q = itab2[j];
+          c.store(&ids[p], (uint32_t)o + (uint32_t)q);
+          c.store(&cnt[p], (uint32_t)(o >> 32) * (uint32_t)(q >> 32));
           j += dj;
           r += dr;
           if (j >= In) {
