@@ -237,6 +237,15 @@ dg_status dg_enumerate_fill(const dg_graph* g, const int64_t* d_locs, int64_t n,
 dg_status dg_enumerate(const dg_graph* g, const int64_t* d_locs, int64_t n, int64_t* d_offsets, uint32_t* d_ids,
                        uint32_t* d_counts, int64_t capacity, void* d_ws, int64_t* h_total, void* stream);
 
+/* dg_enumerate_range: dg_enumerate over the contiguous flat locations
+ * first, first + 1, ..., first + n - 1 (row i belongs to location
+ * first + i), with no location list: a whole output, or a chunk of it, is
+ * enumerated by walking [0, numel) in ranges.  DG_E_RANGE if the range
+ * leaves the output (checked before any work).  Otherwise as dg_enumerate;
+ * the workspace is dg_workspace_size(g, n). */
+dg_status dg_enumerate_range(const dg_graph* g, int64_t first, int64_t n, int64_t* d_offsets, uint32_t* d_ids,
+                             uint32_t* d_counts, int64_t capacity, void* d_ws, int64_t* h_total, void* stream);
+
 /* dg_compare: footprints of two graphs, location by location (Sec. 3.4:
  * e_A and e_B at the same l; the two programs read the same leaves and
  * write outputs of the same shape, as MERGE's input/output matching of
@@ -249,6 +258,25 @@ dg_status dg_enumerate(const dg_graph* g, const int64_t* d_locs, int64_t n, int6
  * Synchronous.  DG_E_RANGE / DG_E_OVERFLOW as for dg_enumerate_sizes. */
 dg_status dg_compare(const dg_graph* a, const dg_graph* b, const int64_t* d_locs, int64_t n, uint8_t* d_status,
                      int64_t* d_mismatch, int64_t* h_n_mismatch, void* d_ws, void* stream);
+
+/* dg_compare_range: dg_compare over the contiguous flat locations first,
+ * ..., first + n - 1 (the full-output verification of Sec. 5, RQ4, is
+ * first = 0, n = numel), with a budget (Sec. 3.4, "Enumeration and
+ * budgets": stop once a bug is found).
+ *   max_mismatch     0: compare every location.  k > 0: once k mismatching
+ *                    locations have been found, locations whose comparison
+ *                    has not started yet are skipped and get status 3; at
+ *                    least min(k, number of mismatching locations) are
+ *                    reported, which ones depends on scheduling
+ *   d_status[n]      device, written: 0, 1, 2 as for dg_compare, 3 skipped
+ *   d_mismatch[n]    device, written: positions i (location first + i) with
+ *                    status 1 or 2, ascending
+ *   h_n_mismatch     host, written: how many positions were written
+ * DG_E_RANGE if the range leaves the output (checked before any work).
+ * Synchronous.  The workspace is dg_workspace_size(a, n). */
+dg_status dg_compare_range(const dg_graph* a, const dg_graph* b, int64_t first, int64_t n, int64_t max_mismatch,
+                           uint8_t* d_status, int64_t* d_mismatch, int64_t* h_n_mismatch, void* d_ws,
+                           void* stream);
 
 /* Message of the calling thread's last failed call ("" if none). */
 const char* dg_last_error(void);

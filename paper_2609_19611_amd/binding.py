@@ -90,6 +90,8 @@ def _load():
         "dg_enumerate_fill": ([P, P, i64, P, P, P, P, P], i32),
         "dg_enumerate": ([P, P, i64, P, P, P, i64, P, ctypes.POINTER(i64), P], i32),
         "dg_compare": ([P, P, P, i64, P, P, ctypes.POINTER(i64), P, P], i32),
+        "dg_enumerate_range": ([P, i64, i64, P, P, P, i64, P, ctypes.POINTER(i64), P], i32),
+        "dg_compare_range": ([P, P, i64, i64, i64, P, P, ctypes.POINTER(i64), P, P], i32),
         "dg_last_error": ([], ctypes.c_char_p),
     }
     for name, (args, res) in sig.items():
@@ -253,6 +255,38 @@ def dg_compare(a: Graph, b: Graph, d_locs: torch.Tensor, d_status: torch.Tensor,
     nm = ctypes.c_int64()
     _check(_lib.dg_compare(a.handle, b.handle, _ptr(d_locs), n, _ptr(d_status), _ptr(d_mismatch),
                            ctypes.byref(nm), _ptr(d_ws), _stream(stream)))
+    return nm.value
+
+
+def dg_enumerate_range(g: Graph, first: int, n: int, d_offsets: torch.Tensor, d_ids: torch.Tensor,
+                       d_counts: torch.Tensor, d_ws: torch.Tensor, stream=None) -> int:
+    """Single pass over the flat locations first .. first + n - 1."""
+    _dev_i64(d_offsets, "offsets")
+    if d_offsets.numel() < n + 1:
+        raise ValueError("offsets needs n + 1 entries")
+    cap = min(d_ids.numel(), d_counts.numel())
+    for t, what in ((d_ids, "ids"), (d_counts, "counts")):
+        if not t.is_cuda or t.dtype not in (torch.int32, torch.uint32) or not t.is_contiguous():
+            raise ValueError(f"{what} must be a contiguous 32-bit device tensor")
+    total = ctypes.c_int64()
+    _check(_lib.dg_enumerate_range(g.handle, first, n, _ptr(d_offsets), _ptr(d_ids), _ptr(d_counts), cap,
+                                   _ptr(d_ws), ctypes.byref(total), _stream(stream)))
+    return total.value
+
+
+def dg_compare_range(a: Graph, b: Graph, first: int, n: int, d_status: torch.Tensor, d_mismatch: torch.Tensor,
+                     d_ws: torch.Tensor, max_mismatch: int = 0, stream=None) -> int:
+    """Compare over the flat locations first .. first + n - 1; with
+    max_mismatch > 0 locations not started once that many mismatches were
+    found get status 3.  Returns the number of mismatch positions written."""
+    if d_status.dtype != torch.uint8 or d_status.numel() < n or not d_status.is_cuda:
+        raise ValueError("status must be a uint8 device tensor of n entries")
+    _dev_i64(d_mismatch, "mismatch")
+    if d_mismatch.numel() < n:
+        raise ValueError("mismatch needs n entries")
+    nm = ctypes.c_int64()
+    _check(_lib.dg_compare_range(a.handle, b.handle, first, n, max_mismatch, _ptr(d_status), _ptr(d_mismatch),
+                                 ctypes.byref(nm), _ptr(d_ws), _stream(stream)))
     return nm.value
 
 

@@ -146,7 +146,7 @@ hipError_t launch_module(hipFunction_t f, int64_t n, int block, uint32_t lds, hi
 }
 
 struct WsLayout {
-  size_t err, ticket, pair, sums, flags, total;
+  size_t err, ticket, found, pair, sums, flags, total;
 };
 
 // Workspace: error word | comparison pair plan | scan tile sums | flags.
@@ -154,6 +154,7 @@ WsLayout ws_layout(int64_t n) {
   WsLayout w;
   w.err = 0;
   w.ticket = 8;
+  w.found = 16;
   w.pair = 256;
   w.sums = (w.pair + sizeof(dgc::PairPlan) + 255) & ~size_t(255);
   w.flags = w.sums + 8 * (size_t)dgk::scan_temp_entries(n < 0 ? 0 : n);
@@ -317,11 +318,12 @@ dg_status dg_enumerate_sizes(const dg_graph* g, const int64_t* d_locs, int64_t n
   uint8_t* ws = static_cast<uint8_t*>(d_ws);
   uint32_t* err = reinterpret_cast<uint32_t*>(ws + w.err);
   DG_HIP(dgk::launch_zero(err, s), "zero");
+  dgc::LocSrc src{d_locs, 0};
   if (const dg::JitModule* jm = graph_jit(g)) {
-    void* args[] = {(void*)&d_locs, &n, &d_offsets, &err};
+    void* args[] = {&src, &n, &d_offsets, &err};
     DG_HIP(launch_module(jm->sizes, n, g->block, g->lds, s, args), "sizes kernel");
   } else {
-    DG_HIP(dgk::launch_sizes(blob, d_locs, n, d_offsets, err, g->block, g->lds, s), "sizes kernel");
+    DG_HIP(dgk::launch_sizes(blob, src, n, d_offsets, err, g->block, g->lds, s), "sizes kernel");
   }
   DG_HIP(dgk::launch_scan(d_offsets, n, reinterpret_cast<int64_t*>(ws + w.sums), s), "scan");
   int64_t total = 0;
@@ -349,20 +351,21 @@ dg_status dg_enumerate_fill(const dg_graph* g, const int64_t* d_locs, int64_t n,
   if (st != DG_OK) return st;
   uint32_t* err = reinterpret_cast<uint32_t*>(static_cast<uint8_t*>(d_ws) + ws_layout(n).err);
   DG_HIP(dgk::launch_zero(err, s), "zero");
+  dgc::LocSrc src{d_locs, 0};
   if (const dg::JitModule* jm = graph_jit(g)) {
-    void* args[] = {(void*)&d_locs, &n, (void*)&d_offsets, &d_ids, &d_counts, &err};
+    void* args[] = {&src, &n, (void*)&d_offsets, &d_ids, &d_counts, &err};
     DG_HIP(launch_module(jm->fill, n, g->block, g->lds, s, args), "fill kernel");
   } else {
-    DG_HIP(dgk::launch_fill(blob, d_locs, n, d_offsets, d_ids, d_counts, err, g->block, g->lds, s), "fill kernel");
+    DG_HIP(dgk::launch_fill(blob, src, n, d_offsets, d_ids, d_counts, err, g->block, g->lds, s), "fill kernel");
   }
   return DG_OK;
 }
 
-dg_status dg_enumerate(const dg_graph* g, const int64_t* d_locs, int64_t n, int64_t* d_offsets, uint32_t* d_ids,
-                       uint32_t* d_counts, int64_t capacity, void* d_ws, int64_t* h_total, void* stream) {
-  if (!g || !d_offsets || !h_total || n < 0 || capacity < 0 || (n > 0 && !d_locs) ||
-      (capacity > 0 && (!d_ids || !d_counts)))
-    return set_error(DG_E_INVALID_ARG, "bad argument");
+namespace {
+
+// Single pass over the locations of `src` (a list or a flat range).
+dg_status enumerate_impl(const dg_graph* g, dgc::LocSrc src, int64_t n, int64_t* d_offsets, uint32_t* d_ids,
+                         uint32_t* d_counts, int64_t capacity, void* d_ws, int64_t* h_total, void* stream) {
   if (!d_ws) return set_error(DG_E_WORKSPACE, "workspace is required");
   if (g->lds > (uint32_t)max_lds_per_block())
     return set_error(DG_E_CAPACITY, "one location needs " + std::to_string(g->lds) + " bytes of LDS");
@@ -386,10 +389,10 @@ dg_status dg_enumerate(const dg_graph* g, const int64_t* d_locs, int64_t n, int6
   if (const dg::JitModule* jm = graph_jit(g)) {
     DG_HIP(dgk::launch_zero_u64(status, n, s), "zero status");
     DG_HIP(dgk::launch_zero_u64(ticket, 1, s), "zero ticket");
-    void* args[] = {(void*)&d_locs, &n, &d_offsets, &d_ids, &d_counts, &cap, &status, &ticket, &err};
+    void* args[] = {&src, &n, &d_offsets, &d_ids, &d_counts, &cap, &status, &ticket, &err};
     DG_HIP(launch_module(jm->enumerate, n, g->block, g->lds, s, args), "enumerate kernel");
   } else {
-    DG_HIP(dgk::launch_enumerate(blob, d_locs, n, d_offsets, d_ids, d_counts, cap, status, ticket, err, g->block,
+    DG_HIP(dgk::launch_enumerate(blob, src, n, d_offsets, d_ids, d_counts, cap, status, ticket, err, g->block,
                                  g->lds, s),
            "enumerate kernel");
   }
@@ -402,10 +405,35 @@ dg_status dg_enumerate(const dg_graph* g, const int64_t* d_locs, int64_t n, int6
   return device_errors(bits);
 }
 
-dg_status dg_compare(const dg_graph* a, const dg_graph* b, const int64_t* d_locs, int64_t n, uint8_t* d_status,
-                     int64_t* d_mismatch, int64_t* h_n_mismatch, void* d_ws, void* stream) {
-  if (!a || !b || !h_n_mismatch || n < 0 || (n > 0 && (!d_locs || !d_status || !d_mismatch)))
+// Whether [first, first + n) lies inside the output of g.
+bool range_ok(const dg_graph* g, int64_t first, int64_t n) {
+  const int64_t numel = g->plan.header().out_numel;
+  return first >= 0 && n >= 0 && first <= numel && n <= numel - first;
+}
+
+}  // namespace
+
+dg_status dg_enumerate(const dg_graph* g, const int64_t* d_locs, int64_t n, int64_t* d_offsets, uint32_t* d_ids,
+                       uint32_t* d_counts, int64_t capacity, void* d_ws, int64_t* h_total, void* stream) {
+  if (!g || !d_offsets || !h_total || n < 0 || capacity < 0 || (n > 0 && !d_locs) ||
+      (capacity > 0 && (!d_ids || !d_counts)))
     return set_error(DG_E_INVALID_ARG, "bad argument");
+  return enumerate_impl(g, dgc::LocSrc{d_locs, 0}, n, d_offsets, d_ids, d_counts, capacity, d_ws, h_total, stream);
+}
+
+dg_status dg_enumerate_range(const dg_graph* g, int64_t first, int64_t n, int64_t* d_offsets, uint32_t* d_ids,
+                             uint32_t* d_counts, int64_t capacity, void* d_ws, int64_t* h_total, void* stream) {
+  if (!g || !d_offsets || !h_total || n < 0 || capacity < 0 || (capacity > 0 && (!d_ids || !d_counts)))
+    return set_error(DG_E_INVALID_ARG, "bad argument");
+  if (!range_ok(g, first, n)) return set_error(DG_E_RANGE, "the location range leaves the output");
+  return enumerate_impl(g, dgc::LocSrc{nullptr, first}, n, d_offsets, d_ids, d_counts, capacity, d_ws, h_total,
+                        stream);
+}
+
+namespace {
+
+dg_status compare_impl(const dg_graph* a, const dg_graph* b, dgc::LocSrc src, int64_t n, uint64_t limit,
+                       uint8_t* d_status, int64_t* d_mismatch, int64_t* h_n_mismatch, void* d_ws, void* stream) {
   if (!d_ws) return set_error(DG_E_WORKSPACE, "workspace is required");
   return guarded([&]() -> dg_status {
     // MERGE's input/output matching: same leaves (names, shapes, order) and
@@ -441,15 +469,17 @@ dg_status dg_compare(const dg_graph* a, const dg_graph* b, const int64_t* d_locs
     uint32_t* err = reinterpret_cast<uint32_t*>(ws + w.err);
     int64_t* flags = reinterpret_cast<int64_t*>(ws + w.flags);
     DG_HIP(dgk::launch_zero(err, s), "zero");
+    uint64_t* found = reinterpret_cast<uint64_t*>(ws + w.found);
+    DG_HIP(dgk::launch_zero_u64(found, 1, s), "zero count");
     if (const dg::JitModule* jm = pair_jit(a, b, pp, block)) {
-      void* args[] = {(void*)&d_locs, &n, &d_status, &flags, &err};
+      void* args[] = {&src, &n, &d_status, &flags, &found, &limit, &err};
       DG_HIP(launch_module(jm->compare, n, block, pp.lds_bytes, s, args), "compare kernel");
     } else {
       if (block != 64 && block != 256) return set_error(DG_E_INVALID_ARG, "block size needs specialised kernels");
       dgc::PairPlan* d_pp = reinterpret_cast<dgc::PairPlan*>(ws + w.pair);
       // Pageable source: the copy has completed when the call returns.
       DG_HIP(hipMemcpyAsync(d_pp, &pp, sizeof(pp), hipMemcpyHostToDevice, s), "copy pair plan");
-      DG_HIP(dgk::launch_compare(ba, bb, d_pp, pp.lds_bytes, d_locs, n, d_status, flags, err, block, s),
+      DG_HIP(dgk::launch_compare(ba, bb, d_pp, pp.lds_bytes, src, n, d_status, flags, found, limit, err, block, s),
              "compare kernel");
     }
     DG_HIP(dgk::launch_scan(flags, n, reinterpret_cast<int64_t*>(ws + w.sums), s), "scan");
@@ -464,6 +494,25 @@ dg_status dg_compare(const dg_graph* a, const dg_graph* b, const int64_t* d_locs
     *h_n_mismatch = total;
     return DG_OK;
   });
+}
+
+}  // namespace
+
+dg_status dg_compare(const dg_graph* a, const dg_graph* b, const int64_t* d_locs, int64_t n, uint8_t* d_status,
+                     int64_t* d_mismatch, int64_t* h_n_mismatch, void* d_ws, void* stream) {
+  if (!a || !b || !h_n_mismatch || n < 0 || (n > 0 && (!d_locs || !d_status || !d_mismatch)))
+    return set_error(DG_E_INVALID_ARG, "bad argument");
+  return compare_impl(a, b, dgc::LocSrc{d_locs, 0}, n, 0, d_status, d_mismatch, h_n_mismatch, d_ws, stream);
+}
+
+dg_status dg_compare_range(const dg_graph* a, const dg_graph* b, int64_t first, int64_t n, int64_t max_mismatch,
+                           uint8_t* d_status, int64_t* d_mismatch, int64_t* h_n_mismatch, void* d_ws,
+                           void* stream) {
+  if (!a || !b || !h_n_mismatch || n < 0 || max_mismatch < 0 || (n > 0 && (!d_status || !d_mismatch)))
+    return set_error(DG_E_INVALID_ARG, "bad argument");
+  if (!range_ok(a, first, n)) return set_error(DG_E_RANGE, "the location range leaves the output");
+  return compare_impl(a, b, dgc::LocSrc{nullptr, first}, n, (uint64_t)max_mismatch, d_status, d_mismatch,
+                      h_n_mismatch, d_ws, stream);
 }
 
 }  // extern "C"

@@ -1033,6 +1033,14 @@ DGC LeafGeom leaf_geom(const DgpLeaf& L) {
 }
 
 // ---------------------------------------------------------------- drivers --
+// Where the locations of a launch come from: an explicit list, or (list
+// null) the contiguous flat range first, first + 1, ...
+struct LocSrc {
+  const int64_t* locs;
+  int64_t first;
+};
+DGC int64_t loc_at(const LocSrc& s, int64_t i) { return s.locs ? s.locs[i] : s.first + i; }
+
 DGC bool location_in_range(const uint8_t* blob, int64_t loc) {
   const DgpHeader* h = (const DgpHeader*)blob;
   return loc >= 0 && loc < h->out_numel;

@@ -40,14 +40,14 @@ std::string jit_enum_source(const Plan& p, int block) {
   o << kPrelude;
   emit_bytes(o, "dg_plan", p.blob);
   o << "#define DG_B " << block << "\n"
-    << "extern \"C\" __global__ __launch_bounds__(DG_B) void dg_sizes(const int64_t* __restrict__ locs, int64_t n,\n"
+    << "extern \"C\" __global__ __launch_bounds__(DG_B) void dg_sizes(dgc::LocSrc locs, int64_t n,\n"
     << "    int64_t* __restrict__ offsets, uint32_t* __restrict__ err) {\n"
     << "  dgk_dev::sizes_body<DG_B>(dg_plan, locs, n, offsets, err);\n}\n"
-    << "extern \"C\" __global__ __launch_bounds__(DG_B) void dg_fill(const int64_t* __restrict__ locs, int64_t n,\n"
+    << "extern \"C\" __global__ __launch_bounds__(DG_B) void dg_fill(dgc::LocSrc locs, int64_t n,\n"
     << "    const int64_t* __restrict__ offsets, uint32_t* __restrict__ ids, uint32_t* __restrict__ cnt,\n"
     << "    uint32_t* __restrict__ err) {\n"
     << "  dgk_dev::fill_body<DG_B>(dg_plan, locs, n, offsets, ids, cnt, err);\n}\n"
-    << "extern \"C\" __global__ __launch_bounds__(DG_B) void dg_enumerate(const int64_t* __restrict__ locs, int64_t n,\n"
+    << "extern \"C\" __global__ __launch_bounds__(DG_B) void dg_enumerate(dgc::LocSrc locs, int64_t n,\n"
     << "    int64_t* __restrict__ offsets, uint32_t* __restrict__ ids, uint32_t* __restrict__ cnt, uint64_t capacity,\n"
     << "    uint64_t* __restrict__ status, unsigned long long* __restrict__ ticket, uint32_t* __restrict__ err) {\n"
     << "  dgk_dev::enumerate_body<DG_B>(dg_plan, locs, n, offsets, ids, cnt, capacity, status, ticket, err);\n}\n";
@@ -63,10 +63,11 @@ std::string jit_compare_source(const Plan& a, const Plan& b, const dgc::PairPlan
   std::memcpy(ppb.data(), &pp, sizeof(pp));
   emit_bytes(o, "dg_pair", ppb);
   o << "#define DG_B " << block << "\n"
-    << "extern \"C\" __global__ __launch_bounds__(DG_B) void dg_compare(const int64_t* __restrict__ locs, int64_t n,\n"
-    << "    uint8_t* __restrict__ status, int64_t* __restrict__ flags, uint32_t* __restrict__ err) {\n"
+    << "extern \"C\" __global__ __launch_bounds__(DG_B) void dg_compare(dgc::LocSrc locs, int64_t n,\n"
+    << "    uint8_t* __restrict__ status, int64_t* __restrict__ flags, unsigned long long* __restrict__ found,\n"
+    << "    uint64_t limit, uint32_t* __restrict__ err) {\n"
     << "  dgk_dev::compare_body<DG_B>(dg_plan_a, dg_plan_b, (const dgc::PairPlan*)dg_pair, locs, n, status, flags,"
-       " err);\n}\n";
+       " found, limit, err);\n}\n";
   return o.str();
 }
 

@@ -7,20 +7,22 @@
 
 namespace dgk {
 
-hipError_t launch_sizes(const uint8_t* blob, const int64_t* locs, int64_t n, int64_t* offsets, uint32_t* err,
+hipError_t launch_sizes(const uint8_t* blob, dgc::LocSrc locs, int64_t n, int64_t* offsets, uint32_t* err,
                         int block, uint32_t lds, hipStream_t s);
-hipError_t launch_fill(const uint8_t* blob, const int64_t* locs, int64_t n, const int64_t* offsets, uint32_t* ids,
+hipError_t launch_fill(const uint8_t* blob, dgc::LocSrc locs, int64_t n, const int64_t* offsets, uint32_t* ids,
                        uint32_t* cnt, uint32_t* err, int block, uint32_t lds, hipStream_t s);
-// pp: device copy of the pair plan; lds: pp's lds_bytes.
+// pp: device copy of the pair plan; lds: pp's lds_bytes.  found: a word
+// counting mismatching locations (cleared by the caller); with limit > 0,
+// locations that start after `limit` mismatches were found are skipped.
 hipError_t launch_compare(const uint8_t* blob_a, const uint8_t* blob_b, const dgc::PairPlan* pp, uint32_t lds,
-                          const int64_t* locs, int64_t n, uint8_t* status, int64_t* flags, uint32_t* err, int block,
-                          hipStream_t s);
+                          dgc::LocSrc locs, int64_t n, uint8_t* status, int64_t* flags, uint64_t* found,
+                          uint64_t limit, uint32_t* err, int block, hipStream_t s);
 // In-place scan: v[1..n] holds sizes on entry, running totals on exit, v[0] = 0.
 hipError_t launch_scan(int64_t* v, int64_t n, int64_t* sums, hipStream_t s);
 int64_t scan_temp_entries(int64_t n);
 // Single pass over n locations: offsets[0..n] and the rows (written only
 // where they fit `capacity` entries).  status: n words, ticket: one word.
-hipError_t launch_enumerate(const uint8_t* blob, const int64_t* locs, int64_t n, int64_t* offsets, uint32_t* ids,
+hipError_t launch_enumerate(const uint8_t* blob, dgc::LocSrc locs, int64_t n, int64_t* offsets, uint32_t* ids,
                             uint32_t* cnt, uint64_t capacity, uint64_t* status, uint64_t* ticket, uint32_t* err,
                             int block, uint32_t lds, hipStream_t s);
 // Clears count 64-bit words.

@@ -13,14 +13,14 @@ namespace {
 using dgk_dev::DevCtx;
 
 template <int BLOCK>
-__global__ __launch_bounds__(BLOCK) void k_sizes(const uint8_t* __restrict__ blob, const int64_t* __restrict__ locs,
-                                                 int64_t n, int64_t* __restrict__ offsets, uint32_t* __restrict__ err) {
+__global__ __launch_bounds__(BLOCK) void k_sizes(const uint8_t* __restrict__ blob, dgc::LocSrc locs, int64_t n,
+                                                 int64_t* __restrict__ offsets, uint32_t* __restrict__ err) {
   dgk_dev::sizes_body<BLOCK>(blob, locs, n, offsets, err);
 }
 
 template <int BLOCK>
-__global__ __launch_bounds__(BLOCK) void k_fill(const uint8_t* __restrict__ blob, const int64_t* __restrict__ locs,
-                                                int64_t n, const int64_t* __restrict__ offsets,
+__global__ __launch_bounds__(BLOCK) void k_fill(const uint8_t* __restrict__ blob, dgc::LocSrc locs, int64_t n,
+                                                const int64_t* __restrict__ offsets,
                                                 uint32_t* __restrict__ ids, uint32_t* __restrict__ cnt,
                                                 uint32_t* __restrict__ err) {
   dgk_dev::fill_body<BLOCK>(blob, locs, n, offsets, ids, cnt, err);
@@ -29,16 +29,15 @@ __global__ __launch_bounds__(BLOCK) void k_fill(const uint8_t* __restrict__ blob
 template <int BLOCK>
 __global__ __launch_bounds__(BLOCK) void k_compare(const uint8_t* __restrict__ blob_a,
                                                    const uint8_t* __restrict__ blob_b,
-                                                   const dgc::PairPlan* __restrict__ pp,
-                                                   const int64_t* __restrict__ locs, int64_t n,
-                                                   uint8_t* __restrict__ status, int64_t* __restrict__ flags,
-                                                   uint32_t* __restrict__ err) {
-  dgk_dev::compare_body<BLOCK>(blob_a, blob_b, pp, locs, n, status, flags, err);
+                                                   const dgc::PairPlan* __restrict__ pp, dgc::LocSrc locs,
+                                                   int64_t n, uint8_t* __restrict__ status,
+                                                   int64_t* __restrict__ flags, unsigned long long* __restrict__ found,
+                                                   uint64_t limit, uint32_t* __restrict__ err) {
+  dgk_dev::compare_body<BLOCK>(blob_a, blob_b, pp, locs, n, status, flags, found, limit, err);
 }
 
 template <int BLOCK>
-__global__ __launch_bounds__(BLOCK) void k_enumerate(const uint8_t* __restrict__ blob,
-                                                     const int64_t* __restrict__ locs, int64_t n,
+__global__ __launch_bounds__(BLOCK) void k_enumerate(const uint8_t* __restrict__ blob, dgc::LocSrc locs, int64_t n,
                                                      int64_t* __restrict__ offsets, uint32_t* __restrict__ ids,
                                                      uint32_t* __restrict__ cnt, uint64_t capacity,
                                                      uint64_t* __restrict__ status,
@@ -135,7 +134,7 @@ __global__ __launch_bounds__(SCAN_THREADS) void k_scan_apply(int64_t* __restrict
 __global__ void k_scatter_mismatch(const uint8_t* __restrict__ status, const int64_t* __restrict__ pos, int64_t n,
                                    int64_t* __restrict__ out) {
   int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n && status[i] != 0) out[pos[i]] = i;
+  if (i < n && (status[i] == 1 || status[i] == 2)) out[pos[i]] = i;
 }
 
 __global__ void k_zero_offsets(int64_t* __restrict__ v) { v[0] = 0; }
@@ -153,7 +152,7 @@ hipError_t allow_lds(K kernel, uint32_t bytes) {
 
 namespace dgk {
 
-hipError_t launch_sizes(const uint8_t* blob, const int64_t* locs, int64_t n, int64_t* offsets, uint32_t* err,
+hipError_t launch_sizes(const uint8_t* blob, dgc::LocSrc locs, int64_t n, int64_t* offsets, uint32_t* err,
                         int block, uint32_t lds, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   if (block != 64 && block != 256) return hipErrorInvalidConfiguration;
@@ -168,7 +167,7 @@ hipError_t launch_sizes(const uint8_t* blob, const int64_t* locs, int64_t n, int
   return hipGetLastError();
 }
 
-hipError_t launch_fill(const uint8_t* blob, const int64_t* locs, int64_t n, const int64_t* offsets, uint32_t* ids,
+hipError_t launch_fill(const uint8_t* blob, dgc::LocSrc locs, int64_t n, const int64_t* offsets, uint32_t* ids,
                        uint32_t* cnt, uint32_t* err, int block, uint32_t lds, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   if (block != 64 && block != 256) return hipErrorInvalidConfiguration;
@@ -184,25 +183,26 @@ hipError_t launch_fill(const uint8_t* blob, const int64_t* locs, int64_t n, cons
 }
 
 hipError_t launch_compare(const uint8_t* blob_a, const uint8_t* blob_b, const dgc::PairPlan* pp, uint32_t lds,
-                          const int64_t* locs, int64_t n, uint8_t* status, int64_t* flags, uint32_t* err, int block,
-                          hipStream_t s) {
+                          dgc::LocSrc locs, int64_t n, uint8_t* status, int64_t* flags, uint64_t* found,
+                          uint64_t limit, uint32_t* err, int block, hipStream_t s) {
+  unsigned long long* fnd = reinterpret_cast<unsigned long long*>(found);
   if (n <= 0) return hipSuccess;
   hipError_t e;
   if (block == 256) {
     if ((e = allow_lds(k_compare<256>, lds)) != hipSuccess) return e;
     hipLaunchKernelGGL(k_compare<256>, dim3((unsigned)n), dim3(256), lds, s, blob_a, blob_b, pp, locs, n, status,
-                       flags, err);
+                       flags, fnd, limit, err);
   } else {
     if ((e = allow_lds(k_compare<64>, lds)) != hipSuccess) return e;
     hipLaunchKernelGGL(k_compare<64>, dim3((unsigned)n), dim3(64), lds, s, blob_a, blob_b, pp, locs, n, status, flags,
-                       err);
+                       fnd, limit, err);
   }
   return hipGetLastError();
 }
 
 int64_t scan_temp_entries(int64_t n) { return (n + SCAN_TILE - 1) / SCAN_TILE + 1; }
 
-hipError_t launch_enumerate(const uint8_t* blob, const int64_t* locs, int64_t n, int64_t* offsets, uint32_t* ids,
+hipError_t launch_enumerate(const uint8_t* blob, dgc::LocSrc locs, int64_t n, int64_t* offsets, uint32_t* ids,
                             uint32_t* cnt, uint64_t capacity, uint64_t* status, uint64_t* ticket, uint32_t* err,
                             int block, uint32_t lds, hipStream_t s) {
   if (n <= 0) return hipSuccess;

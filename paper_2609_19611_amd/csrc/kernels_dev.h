@@ -94,8 +94,8 @@ struct DevCtx {
 extern __shared__ uint64_t dg_smem[];
 
 template <int BLOCK>
-DGC void sizes_body(const uint8_t* __restrict__ blob, const int64_t* __restrict__ locs,
-                                                 int64_t n, int64_t* __restrict__ offsets, uint32_t* __restrict__ err) {
+DGC void sizes_body(const uint8_t* __restrict__ blob, dgc::LocSrc locs, int64_t n,
+                    int64_t* __restrict__ offsets, uint32_t* __restrict__ err) {
   __shared__ uint32_t wsum[BLOCK / 64];
   const int64_t i = blockIdx.x;
   if (i >= n) return;
@@ -103,16 +103,15 @@ DGC void sizes_body(const uint8_t* __restrict__ blob, const int64_t* __restrict_
   uint32_t e = 0;
   uint8_t* area = reinterpret_cast<uint8_t*>(dg_smem);
   const uint64_t rows =
-      dgc::location_row<DevCtx<BLOCK>, dgc::EMIT_COUNT>(c, blob, locs[i], area, nullptr, nullptr, 0, &e);
+      dgc::location_row<DevCtx<BLOCK>, dgc::EMIT_COUNT>(c, blob, dgc::loc_at(locs, i), area, nullptr, nullptr, 0, &e);
   if (threadIdx.x == 0) offsets[i + 1] = (int64_t)rows;
   if (e) atomicOr(err, e);
 }
 
 template <int BLOCK>
-DGC void fill_body(const uint8_t* __restrict__ blob, const int64_t* __restrict__ locs,
-                                                int64_t n, const int64_t* __restrict__ offsets,
-                                                uint32_t* __restrict__ ids, uint32_t* __restrict__ cnt,
-                                                uint32_t* __restrict__ err) {
+DGC void fill_body(const uint8_t* __restrict__ blob, dgc::LocSrc locs, int64_t n,
+                   const int64_t* __restrict__ offsets, uint32_t* __restrict__ ids, uint32_t* __restrict__ cnt,
+                   uint32_t* __restrict__ err) {
   __shared__ uint32_t wsum[BLOCK / 64];
   const int64_t i = blockIdx.x;
   if (i >= n) return;
@@ -123,28 +122,42 @@ DGC void fill_body(const uint8_t* __restrict__ blob, const int64_t* __restrict__
   const int64_t room = offsets[i + 1] - start;
   // Writes stay inside [offsets[i], offsets[i+1]) whatever this row's size.
   const uint64_t rows = dgc::location_row<DevCtx<BLOCK>, dgc::EMIT_FILL>(
-      c, blob, locs[i], area, ids + start, cnt + start, room > 0 ? (uint64_t)room : 0ull, &e);
+      c, blob, dgc::loc_at(locs, i), area, ids + start, cnt + start, room > 0 ? (uint64_t)room : 0ull, &e);
   if (threadIdx.x == 0 && (int64_t)rows != room) e |= DGP_ERR_SIZE;
   if (e) atomicOr(err, e);
 }
 
+// Status of a location the comparison skipped because `limit` mismatching
+// locations had already been found.
+constexpr uint8_t CMP_SKIPPED = 3;
+
 template <int BLOCK>
-DGC void compare_body(const uint8_t* __restrict__ blob_a,
-                                                   const uint8_t* __restrict__ blob_b,
-                                                   const dgc::PairPlan* __restrict__ pp,
-                                                   const int64_t* __restrict__ locs, int64_t n,
-                                                   uint8_t* __restrict__ status, int64_t* __restrict__ flags,
-                                                   uint32_t* __restrict__ err) {
+DGC void compare_body(const uint8_t* __restrict__ blob_a, const uint8_t* __restrict__ blob_b,
+                      const dgc::PairPlan* __restrict__ pp, dgc::LocSrc locs, int64_t n,
+                      uint8_t* __restrict__ status, int64_t* __restrict__ flags, unsigned long long* __restrict__ found,
+                      uint64_t limit, uint32_t* __restrict__ err) {
   __shared__ uint32_t wsum[BLOCK / 64];
+  __shared__ int skip;
   const int64_t i = blockIdx.x;
   if (i >= n) return;
+  if (threadIdx.x == 0)
+    skip = limit != 0 && __hip_atomic_load(found, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= limit;
+  __syncthreads();
+  if (skip) {
+    if (threadIdx.x == 0) {
+      status[i] = CMP_SKIPPED;
+      flags[i + 1] = 0;
+    }
+    return;
+  }
   DevCtx<BLOCK> c{wsum};
   uint32_t e = 0;
   uint8_t* area = reinterpret_cast<uint8_t*>(dg_smem);
-  const uint32_t s = dgc::location_compare(c, blob_a, blob_b, pp, locs[i], area, &e);
+  const uint32_t s = dgc::location_compare(c, blob_a, blob_b, pp, dgc::loc_at(locs, i), area, &e);
   if (threadIdx.x == 0) {
     status[i] = (uint8_t)s;
     flags[i + 1] = s != 0 ? 1 : 0;
+    if (s != 0 && limit != 0) atomicAdd(found, 1ull);
   }
   if (e) atomicOr(err, e);
 }
@@ -235,8 +248,7 @@ struct LookBack {
 };
 
 template <int BLOCK>
-DGC void enumerate_body(const uint8_t* __restrict__ blob,
-                                                     const int64_t* __restrict__ locs, int64_t n,
+DGC void enumerate_body(const uint8_t* __restrict__ blob, dgc::LocSrc locs, int64_t n,
                                                      int64_t* __restrict__ offsets, uint32_t* __restrict__ ids,
                                                      uint32_t* __restrict__ cnt, uint64_t capacity,
                                                      uint64_t* __restrict__ status,
@@ -252,7 +264,7 @@ DGC void enumerate_body(const uint8_t* __restrict__ blob,
   DevCtx<BLOCK> c{wsum};
   uint32_t e = 0;
   uint8_t* area = reinterpret_cast<uint8_t*>(dg_smem);
-  const int64_t loc = locs[i];
+  const int64_t loc = dgc::loc_at(locs, i);
   const bool ok = dgc::location_in_range(blob, loc);
   if (!ok) e |= DGP_ERR_RANGE;
   if (ok) dgc::location_plan(c, blob, loc, area, &e);

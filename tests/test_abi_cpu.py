@@ -17,7 +17,7 @@ CAT = tiny_graphs.catalogue()
 
 def test_library_exports_every_header_symbol():
     names = B.header_symbols()
-    assert len(names) == 11
+    assert len(names) == 13
     lib = ctypes.CDLL(B.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -106,3 +106,16 @@ def test_header_documents_every_status():
     text = open(B.HEADER).read()
     for code in B.STATUS_NAMES.values():
         assert code in text
+
+
+def test_ranges_outside_the_output_are_rejected_before_any_work():
+    g = B.dg_graph_parse(W.c1_text())  # output [8]
+    fake = ctypes.c_void_p(0x1000)  # never dereferenced: the range is checked first
+    total = ctypes.c_int64()
+    for first, n in ((-1, 2), (7, 2), (9, 0), (0, 9)):
+        rc = B._lib.dg_enumerate_range(g.handle, first, n, fake, fake, fake, 16, fake, ctypes.byref(total), None)
+        assert B.STATUS_NAMES[rc] == "DG_E_RANGE", (first, n)
+        rc = B._lib.dg_compare_range(g.handle, g.handle, first, n, 0, fake, fake, ctypes.byref(total), fake, None)
+        assert B.STATUS_NAMES[rc] == "DG_E_RANGE", (first, n)
+    rc = B._lib.dg_compare_range(g.handle, g.handle, 0, 4, -1, fake, fake, ctypes.byref(total), fake, None)
+    assert B.STATUS_NAMES[rc] == "DG_E_INVALID_ARG"

@@ -325,3 +325,86 @@ def test_lds_beyond_the_device_is_rejected(B):
     with pytest.raises(B.DgError) as e:
         B.enumerate_locations(g, [0])
     assert e.value.name == "DG_E_CAPACITY"
+
+
+def test_range_enumeration_equals_list(B):
+    text = W.c2_text()
+    g = B.dg_graph_parse(text)
+    first, n = 1000, 3000
+    a = B.enumerate_locations(g, list(range(first, first + n)))
+    ws = B.workspace(g, n)
+    off = torch.empty(n + 1, dtype=torch.int64, device="cuda")
+    ids = torch.empty(int(a[0][-1]), dtype=torch.int32, device="cuda")
+    cnt = torch.empty_like(ids)
+    total = B.dg_enumerate_range(g, first, n, off, ids, cnt, ws)
+    assert total == int(a[0][-1])
+    assert torch.equal(off, a[0]) and torch.equal(ids, a[1]) and torch.equal(cnt, a[2])
+    # the whole output of the GEMM + GroupNorm graph, by range
+    g4 = B.dg_graph_parse(W.c4_text())
+    n4 = 128 * 512
+    ws4 = B.workspace(g4, n4)
+    off4 = torch.empty(n4 + 1, dtype=torch.int64, device="cuda")
+    ids4 = torch.empty(4366401536, dtype=torch.int32, device="cuda")
+    cnt4 = torch.empty_like(ids4)
+    assert B.dg_enumerate_range(g4, 0, n4, off4, ids4, cnt4, ws4) == 4366401536
+    assert bool((off4[1:] - off4[:-1] == 66626).all())
+    pos = [0, 777, n4 - 1]
+    _, got = rows_to_host(off4, ids4, cnt4, pos)
+    want = oracle_rows(W.c4_text(), pos)
+    for (gi, gc), (wi, wc) in zip(got, want):
+        assert np.array_equal(gi, wi) and np.array_equal(gc, wc)
+    del ids4, cnt4
+
+
+def test_range_compare_and_mismatch_limit(B):
+    ref_text = W.c5_reference_text(n=2, c=4, hw=6, co=3)
+    ref = B.dg_graph_parse(ref_text)
+    numel = 2 * 3 * 6 * 6
+    ws = B.workspace(ref, numel)
+    status = torch.empty(numel, dtype=torch.uint8, device="cuda")
+    mism = torch.empty(numel, dtype=torch.int64, device="cuda")
+    og_ref = oracle.Graph(ref_text)
+    for f in W.c5_faults()[:8]:
+        vt = W.c5_variant_text(fault=f, n=2, c=4, hw=6, co=3)
+        var = B.dg_graph_parse(vt)
+        want = oracle.compare(og_ref, oracle.Graph(vt), list(range(numel)))
+        k = B.dg_compare_range(ref, var, 0, numel, status, mism, ws)
+        st = status.cpu().numpy()
+        assert np.array_equal(st, want), f
+        assert np.array_equal(mism[:k].cpu().numpy(), np.nonzero(want)[0])
+        # a sub-range reports positions relative to its first location
+        k = B.dg_compare_range(ref, var, 50, 100, status, mism, ws)
+        assert np.array_equal(status[:100].cpu().numpy(), want[50:150])
+        assert np.array_equal(mism[:k].cpu().numpy(), np.nonzero(want[50:150])[0])
+        # with a budget: every reported status is right, skipped ones are 3
+        nbad = int((want != 0).sum())
+        for limit in (1, 5):
+            k = B.dg_compare_range(ref, var, 0, numel, status, mism, ws, max_mismatch=limit)
+            st = status.cpu().numpy()
+            done = st != 3
+            assert np.array_equal(st[done], want[done]), (f, limit)
+            assert int(((st == 1) | (st == 2)).sum()) >= min(limit, nbad)
+            assert np.array_equal(mism[:k].cpu().numpy(), np.nonzero((st == 1) | (st == 2))[0])
+            if nbad == 0:
+                assert not (st == 3).any()
+
+
+def test_full_output_verification_of_the_split_k_variant(B):
+    """Every one of the 33,554,432 output locations of the conv2d pair: the
+    clean split-K NHWC variant is footprint-equivalent to the reference."""
+    ref = B.dg_graph_parse(W.c5_reference_text())
+    var = B.dg_graph_parse(W.c5_variant_text())
+    numel = 64 * 128 * 64 * 64
+    ws = B.workspace(ref, numel)
+    status = torch.empty(numel, dtype=torch.uint8, device="cuda")
+    mism = torch.empty(numel, dtype=torch.int64, device="cuda")
+    assert B.dg_compare_range(ref, var, 0, numel, status, mism, ws) == 0
+    assert int(status.max()) == 0
+    # a faulty variant stops early under a budget of one mismatch
+    bad = B.dg_graph_parse(W.c5_variant_text(fault=W.c5_faults()[0]))
+    k = B.dg_compare_range(ref, bad, 0, numel, status, mism, ws, max_mismatch=1)
+    assert k >= 1
+    first = int(mism[0])
+    want = oracle.compare(oracle.Graph(W.c5_reference_text()), oracle.Graph(W.c5_variant_text(fault=W.c5_faults()[0])),
+                          [first])
+    assert want[0] == int(status[first]) != 0
