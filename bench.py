@@ -40,6 +40,9 @@ def parse_args():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--two-pass", action="store_true",
                    help="time dg_enumerate_sizes + dg_enumerate_fill instead of the single-pass dg_enumerate")
+    p.add_argument("--full-output", action="store_true",
+                   help="c5 only: compare every output location (dg_compare_range over all 33,554,432) instead of "
+                        "the sampled list; the faulty variants stop at their first mismatch")
     p.add_argument("--copy-gib", type=float, default=0.0,
                    help="instead of the workload, time a plain device copy of this many GiB (HBM calibration)")
     return p.parse_args()
@@ -166,14 +169,26 @@ def main():
     if args.workload == "c5":
         variants = [B.dg_graph_parse(W.c5_variant_text())] + [B.dg_graph_parse(W.c5_variant_text(fault=f))
                                                               for f in W.c5_faults()]
+        if args.full_output:
+            n = info["output_numel"]
         ws = torch.empty(max(B.dg_workspace_size(g, n), 1), dtype=torch.uint8, device=dev)
         status = torch.empty(n, dtype=torch.uint8, device=dev)
         mism = torch.empty(n, dtype=torch.int64, device=dev)
 
+        if args.full_output:
+            # A step verifies the clean variant at every output location;
+            # the faulty variants, timed apart, stop at their first mismatch.
+            variants_timed = variants[:1]
+        else:
+            variants_timed = variants
+
         def step():
             k = 0
-            for v in variants:
-                k += B.dg_compare(g, v, d_locs, status, mism, ws)
+            for v in variants_timed:
+                if args.full_output:
+                    k += B.dg_compare_range(g, v, 0, n, status, mism, ws)
+                else:
+                    k += B.dg_compare(g, v, d_locs, status, mism, ws)
             return k
 
         for _ in range(args.warmup):
@@ -185,15 +200,26 @@ def main():
         torch.cuda.synchronize()
         elapsed = time.perf_counter() - t0
         ms = elapsed * 1000 / args.steps
-        compares = len(variants)
+        compares = len(variants_timed)
         value = n * compares / (elapsed / args.steps)
+        extra = {}
+        if args.full_output:
+            fault_ms = []
+            for v in variants[1:]:
+                torch.cuda.synchronize()
+                t1 = time.perf_counter()
+                B.dg_compare_range(g, v, 0, n, status, mism, ws, max_mismatch=1)
+                fault_ms.append((time.perf_counter() - t1) * 1000)
+            extra = {"faulty_variants": len(fault_ms), "ms_to_first_mismatch_mean": float(np.mean(fault_ms)),
+                     "ms_to_first_mismatch_max": float(np.max(fault_ms))}
         line = {
             "metric": "output locations/sec compared (two-graph footprint check)",
             "value": value, "unit": "locations/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
             "ms_per_step": ms, "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u32",
             "data": "synthetic (shapes only; footprints are data independent)",
-            "config": {"workload": "c5: " + cfg["desc"], "locations": n, "compares_per_step": compares,
-                       "mismatching_locations_last_step": int(mismatches)},
+            "config": {"workload": "c5: " + cfg["desc"] + (" (full output)" if args.full_output else ""),
+                       "locations": n, "compares_per_step": compares,
+                       "mismatching_locations_last_step": int(mismatches), **extra},
             "roofline": {"bound": "alu", "achieved": None, "peak": None, "unit": None, "frac": None,
                          "traffic": None},
         }
