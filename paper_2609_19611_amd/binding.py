@@ -25,7 +25,7 @@ DG_OK = 0
 STATUS_NAMES = {
     -1: "DG_E_INVALID_ARG", -2: "DG_E_PARSE", -3: "DG_E_SHAPE", -4: "DG_E_UNSUPPORTED_OP", -5: "DG_E_RANGE",
     -6: "DG_E_OVERFLOW", -7: "DG_E_SIGNATURE", -8: "DG_E_WORKSPACE", -9: "DG_E_HIP", -10: "DG_E_CAPACITY",
-    -11: "DG_E_BUFFER",
+    -11: "DG_E_BUFFER", -12: "DG_E_STOPPED",
 }
 MAX_RANK = 8
 
@@ -73,6 +73,11 @@ class OpDesc(ctypes.Structure):
                 ("inputs", ctypes.POINTER(ctypes.c_int32)), ("attrs", ctypes.c_char_p)]
 
 
+# dg_chunk_fn(user, first, n, d_offsets, d_ids, d_counts, total, stream)
+CHUNK_FN = ctypes.CFUNCTYPE(ctypes.c_int32, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_void_p,
+                            ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p)
+
+
 def _load():
     if not os.path.exists(LIB_PATH):
         raise RuntimeError(f"{LIB_PATH} is not built: run `python -m paper_2609_19611_amd.build` "
@@ -92,6 +97,7 @@ def _load():
         "dg_compare": ([P, P, P, i64, P, P, ctypes.POINTER(i64), P, P], i32),
         "dg_enumerate_range": ([P, i64, i64, P, P, P, i64, P, ctypes.POINTER(i64), P], i32),
         "dg_compare_range": ([P, P, i64, i64, i64, P, P, ctypes.POINTER(i64), P, P], i32),
+        "dg_enumerate_stream": ([P, i64, i64, P, sz, i64, CHUNK_FN, P, P, P], i32),
         "dg_last_error": ([], ctypes.c_char_p),
     }
     for name, (args, res) in sig.items():
@@ -288,6 +294,52 @@ def dg_compare_range(a: Graph, b: Graph, first: int, n: int, d_status: torch.Ten
     _check(_lib.dg_compare_range(a.handle, b.handle, first, n, max_mismatch, _ptr(d_status), _ptr(d_mismatch),
                                  ctypes.byref(nm), _ptr(d_ws), _stream(stream)))
     return nm.value
+
+
+class _DeviceArray:
+    """A device pointer viewed as a torch tensor (no copy)."""
+
+    def __init__(self, ptr: int, n: int, typestr: str):
+        self.__cuda_array_interface__ = {"shape": (n,), "typestr": typestr, "data": (ptr, False), "version": 3}
+
+
+def device_view(ptr: int, n: int, dtype: torch.dtype) -> torch.Tensor:
+    typestr = {torch.int64: "<i8", torch.int32: "<i4", torch.uint8: "|u1"}[dtype]
+    if n == 0:
+        return torch.empty(0, dtype=dtype, device="cuda")
+    return torch.as_tensor(_DeviceArray(ptr, n, typestr), device="cuda")
+
+
+def dg_enumerate_stream(g: Graph, first: int, n: int, d_buf: torch.Tensor, max_chunk: int, consume,
+                        streams=None) -> None:
+    """Streams rows of locations first .. first + n - 1 through the two halves
+    of d_buf.  consume(first, offsets, ids, counts, stream) gets each chunk
+    as device tensors (views into d_buf, valid until it returns and the
+    work it enqueued on `stream` has finished); a truthy return stops."""
+    if not d_buf.is_cuda or not d_buf.is_contiguous():
+        raise ValueError("the buffer must be a contiguous device tensor")
+    sa, sb = streams if streams is not None else (torch.cuda.Stream(), torch.cuda.Stream())
+    by_handle = {int(sa.cuda_stream): sa, int(sb.cuda_stream): sb}
+    errors = []
+
+    def trampoline(user, first_, n_, d_off, d_ids, d_cnt, total, stream):
+        try:
+            off = device_view(d_off, n_ + 1, torch.int64)
+            ids = device_view(d_ids, total, torch.int32)
+            cnt = device_view(d_cnt, total, torch.int32)
+            s = by_handle.get(int(stream or 0))
+            with torch.cuda.stream(s):
+                return 1 if consume(first_, off, ids, cnt, s) else 0
+        except Exception as e:  # reported after the call returns
+            errors.append(e)
+            return 1
+
+    cb = CHUNK_FN(trampoline)
+    rc = _lib.dg_enumerate_stream(g.handle, first, n, _ptr(d_buf), d_buf.numel() * d_buf.element_size(), max_chunk,
+                                  cb, None, sa.cuda_stream, sb.cuda_stream)
+    if errors:
+        raise errors[0]
+    _check(rc)
 
 
 def dg_last_error() -> str:

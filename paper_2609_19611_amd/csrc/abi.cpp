@@ -4,6 +4,7 @@
 #include <algorithm>
 #include <atomic>
 #include <tuple>
+#include <vector>
 #include <cstring>
 #include <map>
 #include <cstdlib>
@@ -428,6 +429,64 @@ dg_status dg_enumerate_range(const dg_graph* g, int64_t first, int64_t n, int64_
   if (!range_ok(g, first, n)) return set_error(DG_E_RANGE, "the location range leaves the output");
   return enumerate_impl(g, dgc::LocSrc{nullptr, first}, n, d_offsets, d_ids, d_counts, capacity, d_ws, h_total,
                         stream);
+}
+
+dg_status dg_enumerate_stream(const dg_graph* g, int64_t first, int64_t n, void* d_buf, size_t buf_bytes,
+                              int64_t max_chunk, dg_chunk_fn fn, void* user, void* stream_a, void* stream_b) {
+  if (!g || !d_buf || !fn || n < 0 || max_chunk <= 0) return set_error(DG_E_INVALID_ARG, "bad argument");
+  if (!range_ok(g, first, n)) return set_error(DG_E_RANGE, "the location range leaves the output");
+  return guarded([&]() -> dg_status {
+    // Each half: offsets[max_chunk + 1] | workspace | ids | counts.
+    const size_t half = (buf_bytes / 2) & ~size_t(255);
+    const size_t off_bytes = (8 * (size_t)(max_chunk + 1) + 255) & ~size_t(255);
+    const size_t ws_bytes = (ws_layout(max_chunk).total + 255) & ~size_t(255);
+    if (half <= off_bytes + ws_bytes + 512) return set_error(DG_E_BUFFER, "buffer too small for one chunk");
+    const int64_t cap = (int64_t)((half - off_bytes - ws_bytes) / 8) & ~int64_t(63);
+    hipStream_t st[2] = {static_cast<hipStream_t>(stream_a), static_cast<hipStream_t>(stream_b)};
+    bool used[2] = {false, false};
+    int64_t pos = first, chunk = max_chunk;
+    std::vector<int64_t> h_off;
+    int c = 0;
+    dg_status rc = DG_OK;
+    while (pos < first + n) {
+      const int h = c & 1;
+      uint8_t* base = static_cast<uint8_t*>(d_buf) + h * half;
+      int64_t* d_off = reinterpret_cast<int64_t*>(base);
+      void* ws = base + off_bytes;
+      uint32_t* ids = reinterpret_cast<uint32_t*>(base + off_bytes + ws_bytes);
+      uint32_t* cnt = ids + cap;
+      // The consumer of the chunk that last used this half has finished.
+      if (used[h]) DG_HIP(hipStreamSynchronize(st[h]), "consumer sync");
+      int64_t m = std::min(chunk, first + n - pos), total = 0;
+      dg_status e = enumerate_impl(g, dgc::LocSrc{nullptr, pos}, m, d_off, ids, cnt, cap, ws, &total, st[h]);
+      if (e == DG_E_BUFFER) {
+        // The rows of the longest prefix below `cap` are complete.
+        h_off.resize((size_t)m + 1);
+        DG_HIP(hipMemcpy(h_off.data(), d_off, 8 * (size_t)(m + 1), hipMemcpyDeviceToHost), "copy offsets");
+        const int64_t k = (int64_t)(std::upper_bound(h_off.begin(), h_off.end(), cap) - h_off.begin()) - 1;
+        if (k <= 0) {
+          rc = set_error(DG_E_BUFFER, "one location's row does not fit half of the buffer");
+          break;
+        }
+        m = k;
+        total = h_off[(size_t)k];
+        chunk = k;
+      } else if (e != DG_OK) {
+        rc = e;
+        break;
+      }
+      used[h] = true;
+      if (fn(user, pos, m, d_off, ids, cnt, total, st[h]) != 0) {
+        rc = set_error(DG_E_STOPPED, "the chunk consumer stopped the stream");
+        break;
+      }
+      pos += m;
+      ++c;
+    }
+    for (int h = 0; h < 2; ++h)
+      if (used[h]) DG_HIP(hipStreamSynchronize(st[h]), "final sync");
+    return rc;
+  });
 }
 
 namespace {

@@ -408,3 +408,49 @@ def test_full_output_verification_of_the_split_k_variant(B):
     want = oracle.compare(oracle.Graph(W.c5_reference_text()), oracle.Graph(W.c5_variant_text(fault=W.c5_faults()[0])),
                           [first])
     assert want[0] == int(status[first]) != 0
+
+
+def test_streamed_enumeration_matches_one_pass(B):
+    """A whole output streamed through two small buffer halves (chunks cut
+    where the rows stop fitting) gives the one-pass CSR, chunk by chunk."""
+    text = W.c2_text()
+    g = B.dg_graph_parse(text)
+    numel = 16 * 16 * 16 * 16
+    ws = B.workspace(g, numel)
+    off = torch.empty(numel + 1, dtype=torch.int64, device="cuda")
+    ids = torch.empty(numel * 80, dtype=torch.int32, device="cuda")
+    cnt = torch.empty_like(ids)
+    total = B.dg_enumerate_range(g, 0, numel, off, ids, cnt, ws)
+    want_off = off.cpu().numpy()
+    want_ids = ids[:total].cpu().numpy()
+    want_cnt = cnt[:total].cpu().numpy()
+    buf = torch.empty(2 * (1 << 20), dtype=torch.uint8, device="cuda")
+    chunks = []
+
+    def consume(first, o, i, c, stream):
+        chunks.append((first, o.cpu().numpy().copy(), i.cpu().numpy().copy(), c.cpu().numpy().copy()))
+
+    B.dg_enumerate_stream(g, 0, numel, buf, 8192, consume)
+    assert len(chunks) > 8
+    pos = 0
+    for first, o, i, c in chunks:
+        assert first == pos
+        m = len(o) - 1
+        base = want_off[pos]
+        assert np.array_equal(o, want_off[pos:pos + m + 1] - base)
+        assert np.array_equal(i, want_ids[base:base + o[-1]]) and np.array_equal(c, want_cnt[base:base + o[-1]])
+        pos += m
+    assert pos == numel
+    # a consumer can stop the stream
+    seen = []
+    with pytest.raises(B.DgError) as e:
+        B.dg_enumerate_stream(g, 0, numel, buf, 4096, lambda *a: seen.append(1) or len(seen) == 2)
+    assert e.value.name == "DG_E_STOPPED" and len(seen) == 2
+    # halves of 64 entries: the first row (56 entries, a corner) fits, the
+    # second (65) does not
+    got = []
+    with pytest.raises(B.DgError) as e:
+        B.dg_enumerate_stream(g, 0, numel, torch.empty(2 * 2560, dtype=torch.uint8, device="cuda"), 4,
+                              lambda first, o, i, c, s: got.append((first, int(o[-1]))))
+    assert e.value.name == "DG_E_BUFFER"
+    assert got == [(0, int(want_off[1]))]
