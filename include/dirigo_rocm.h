@@ -251,29 +251,32 @@ dg_status dg_enumerate_range(const dg_graph* g, int64_t first, int64_t n, int64_
 /* dg_enumerate_stream: the rows of the flat locations [first, first + n)
  * streamed in chunks through two halves of one caller-owned device buffer,
  * so that a whole output whose CSR does not fit in memory (the full
- * verification of Sec. 5, RQ4) is produced with bounded memory.  Chunks
- * alternate between the halves and between stream_a and stream_b; while
- * the consumer's work on one chunk runs on its stream, the next chunk is
- * enumerated on the other.
- *   d_buf, buf_bytes  device buffer; each half holds the offsets and the
- *                     workspace for max_chunk locations and as many
- *                     (id, count) entries as the rest of the half allows
- *   max_chunk         most locations per chunk (> 0); a chunk whose rows do
- *                     not fit its half is cut to the longest prefix of
- *                     locations that does, and later chunks start from
- *                     that size
+ * verification of Sec. 5, RQ4) is produced with bounded memory.  A first
+ * pass computes the row sizes and offsets of the whole range (kept at the
+ * start of the buffer); chunks are then cut exactly where the rows stop
+ * fitting a half, and filled alternately into the two halves on stream_a
+ * and stream_b without waiting for each other: while the consumer's work
+ * on one chunk runs on its stream, the next chunk is written on the other.
+ *   d_buf, buf_bytes  device buffer: the range's offsets (8 * (n + 1) bytes)
+ *                     and the workspace of n locations, then two halves,
+ *                     each with the offsets and workspace of max_chunk
+ *                     locations and as many (id, count) entries as the rest
+ *                     of the half allows
+ *   max_chunk         most locations per chunk (> 0)
  *   fn(user, first, n, d_offsets, d_ids, d_counts, total, stream)
  *                     called on the calling thread once per chunk, in
- *                     location order, after the chunk is complete: rows of
- *                     locations first .. first + n - 1 in CSR form (device
- *                     pointers into the buffer, offsets start at 0, total
- *                     entries).  The consumer may enqueue work on `stream`
- *                     and return at once: the half is not reused until
- *                     that stream has finished.  A nonzero return stops
- *                     the stream (DG_E_STOPPED).
- * Returns after all consumer work has finished.  DG_E_RANGE if the range
- * leaves the output; DG_E_BUFFER if one location's row alone does not fit
- * a half; DG_E_OVERFLOW as for dg_enumerate_sizes. */
+ *                     location order, right after the chunk's work has been
+ *                     enqueued on `stream`: rows of locations first ..
+ *                     first + n - 1 in CSR form (device pointers into the
+ *                     buffer, offsets start at 0, `total` entries).  Work
+ *                     the consumer enqueues on `stream` sees the finished
+ *                     chunk; the half is not reused until that stream has
+ *                     finished.  A nonzero return stops the stream
+ *                     (DG_E_STOPPED).
+ * Returns after all chunk and consumer work has finished.  DG_E_RANGE if
+ * the range leaves the output; DG_E_BUFFER if the buffer cannot hold the
+ * offsets and two chunks, or one location's row alone does not fit a half;
+ * DG_E_OVERFLOW as for dg_enumerate_sizes. */
 typedef int32_t (*dg_chunk_fn)(void* user, int64_t first, int64_t n, const int64_t* d_offsets, const uint32_t* d_ids,
                                const uint32_t* d_counts, int64_t total, void* stream);
 dg_status dg_enumerate_stream(const dg_graph* g, int64_t first, int64_t n, void* d_buf, size_t buf_bytes,

@@ -312,10 +312,12 @@ def device_view(ptr: int, n: int, dtype: torch.dtype) -> torch.Tensor:
 
 def dg_enumerate_stream(g: Graph, first: int, n: int, d_buf: torch.Tensor, max_chunk: int, consume,
                         streams=None) -> None:
-    """Streams rows of locations first .. first + n - 1 through the two halves
-    of d_buf.  consume(first, offsets, ids, counts, stream) gets each chunk
-    as device tensors (views into d_buf, valid until it returns and the
-    work it enqueued on `stream` has finished); a truthy return stops."""
+    """Streams rows of locations first .. first + n - 1 through d_buf.
+    consume(first, offsets, ids, counts, stream) gets each chunk as device
+    tensors (views into d_buf) right after its work was enqueued on
+    `stream`, which is current during the call: work it enqueues there sees
+    the finished chunk, and the views stay valid until that work is done.
+    A truthy return stops."""
     if not d_buf.is_cuda or not d_buf.is_contiguous():
         raise ValueError("the buffer must be a contiguous device tensor")
     sa, sb = streams if streams is not None else (torch.cuda.Stream(), torch.cuda.Stream())

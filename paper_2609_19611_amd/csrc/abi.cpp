@@ -146,6 +146,17 @@ hipError_t launch_module(hipFunction_t f, int64_t n, int block, uint32_t lds, hi
   return hipModuleLaunchKernel(f, (unsigned)n, 1, 1, (unsigned)block, 1, 1, lds, s, args, nullptr);
 }
 
+// The fill kernel of g (specialised or precompiled): rows of the n
+// locations of src at [offsets[i] - base, offsets[i+1] - base).
+hipError_t fill_launch(const dg_graph* g, const uint8_t* blob, dgc::LocSrc src, int64_t n, const int64_t* offsets,
+                       int64_t base, uint32_t* ids, uint32_t* cnt, uint32_t* err, hipStream_t s) {
+  if (const dg::JitModule* jm = graph_jit(g)) {
+    void* args[] = {&src, &n, (void*)&offsets, &base, &ids, &cnt, &err};
+    return launch_module(jm->fill, n, g->block, g->lds, s, args);
+  }
+  return dgk::launch_fill(blob, src, n, offsets, base, ids, cnt, err, g->block, g->lds, s);
+}
+
 struct WsLayout {
   size_t err, ticket, found, pair, sums, flags, total;
 };
@@ -305,13 +316,14 @@ dg_status dg_workspace_size(const dg_graph* g, int64_t n_locs, size_t* bytes) {
   return DG_OK;
 }
 
-dg_status dg_enumerate_sizes(const dg_graph* g, const int64_t* d_locs, int64_t n, int64_t* d_offsets, void* d_ws,
-                             int64_t* h_total, void* stream) {
-  if (!g || !d_offsets || !h_total || n < 0 || (n > 0 && !d_locs)) return set_error(DG_E_INVALID_ARG, "bad argument");
+namespace {
+
+// Row sizes and offsets of the locations of `src` (synchronous).
+dg_status sizes_impl(const dg_graph* g, dgc::LocSrc src, int64_t n, int64_t* d_offsets, void* d_ws,
+                     int64_t* h_total, hipStream_t s) {
   if (!d_ws) return set_error(DG_E_WORKSPACE, "workspace is required");
   if (g->lds > (uint32_t)max_lds_per_block())
     return set_error(DG_E_CAPACITY, "one location needs " + std::to_string(g->lds) + " bytes of LDS");
-  hipStream_t s = static_cast<hipStream_t>(stream);
   const uint8_t* blob = nullptr;
   dg_status st = device_blob(g, &blob);
   if (st != DG_OK) return st;
@@ -319,7 +331,6 @@ dg_status dg_enumerate_sizes(const dg_graph* g, const int64_t* d_locs, int64_t n
   uint8_t* ws = static_cast<uint8_t*>(d_ws);
   uint32_t* err = reinterpret_cast<uint32_t*>(ws + w.err);
   DG_HIP(dgk::launch_zero(err, s), "zero");
-  dgc::LocSrc src{d_locs, 0};
   if (const dg::JitModule* jm = graph_jit(g)) {
     void* args[] = {&src, &n, &d_offsets, &err};
     DG_HIP(launch_module(jm->sizes, n, g->block, g->lds, s, args), "sizes kernel");
@@ -338,6 +349,14 @@ dg_status dg_enumerate_sizes(const dg_graph* g, const int64_t* d_locs, int64_t n
   return DG_OK;
 }
 
+}  // namespace
+
+dg_status dg_enumerate_sizes(const dg_graph* g, const int64_t* d_locs, int64_t n, int64_t* d_offsets, void* d_ws,
+                             int64_t* h_total, void* stream) {
+  if (!g || !d_offsets || !h_total || n < 0 || (n > 0 && !d_locs)) return set_error(DG_E_INVALID_ARG, "bad argument");
+  return sizes_impl(g, dgc::LocSrc{d_locs, 0}, n, d_offsets, d_ws, h_total, static_cast<hipStream_t>(stream));
+}
+
 dg_status dg_enumerate_fill(const dg_graph* g, const int64_t* d_locs, int64_t n, const int64_t* d_offsets,
                             uint32_t* d_ids, uint32_t* d_counts, void* d_ws, void* stream) {
   if (!g || n < 0 || (n > 0 && (!d_locs || !d_offsets || !d_ids || !d_counts)))
@@ -352,13 +371,7 @@ dg_status dg_enumerate_fill(const dg_graph* g, const int64_t* d_locs, int64_t n,
   if (st != DG_OK) return st;
   uint32_t* err = reinterpret_cast<uint32_t*>(static_cast<uint8_t*>(d_ws) + ws_layout(n).err);
   DG_HIP(dgk::launch_zero(err, s), "zero");
-  dgc::LocSrc src{d_locs, 0};
-  if (const dg::JitModule* jm = graph_jit(g)) {
-    void* args[] = {&src, &n, (void*)&d_offsets, &d_ids, &d_counts, &err};
-    DG_HIP(launch_module(jm->fill, n, g->block, g->lds, s, args), "fill kernel");
-  } else {
-    DG_HIP(dgk::launch_fill(blob, src, n, d_offsets, d_ids, d_counts, err, g->block, g->lds, s), "fill kernel");
-  }
+  DG_HIP(fill_launch(g, blob, dgc::LocSrc{d_locs, 0}, n, d_offsets, 0, d_ids, d_counts, err, s), "fill kernel");
   return DG_OK;
 }
 
@@ -435,56 +448,86 @@ dg_status dg_enumerate_stream(const dg_graph* g, int64_t first, int64_t n, void*
                               int64_t max_chunk, dg_chunk_fn fn, void* user, void* stream_a, void* stream_b) {
   if (!g || !d_buf || !fn || n < 0 || max_chunk <= 0) return set_error(DG_E_INVALID_ARG, "bad argument");
   if (!range_ok(g, first, n)) return set_error(DG_E_RANGE, "the location range leaves the output");
+  if (n == 0) return DG_OK;
   return guarded([&]() -> dg_status {
-    // Each half: offsets[max_chunk + 1] | workspace | ids | counts.
-    const size_t half = (buf_bytes / 2) & ~size_t(255);
-    const size_t off_bytes = (8 * (size_t)(max_chunk + 1) + 255) & ~size_t(255);
-    const size_t ws_bytes = (ws_layout(max_chunk).total + 255) & ~size_t(255);
-    if (half <= off_bytes + ws_bytes + 512) return set_error(DG_E_BUFFER, "buffer too small for one chunk");
-    const int64_t cap = (int64_t)((half - off_bytes - ws_bytes) / 8) & ~int64_t(63);
+    // Buffer: offsets of the whole range | sizes workspace | two halves of
+    // (chunk offsets from 0 | fill workspace | ids | counts).
+    auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
+    uint8_t* p = static_cast<uint8_t*>(d_buf);
+    int64_t* g_off = reinterpret_cast<int64_t*>(p);
+    size_t used_bytes = up(8 * (size_t)(n + 1));
+    void* s_ws = p + used_bytes;
+    used_bytes += up(ws_layout(n).total);
+    max_chunk = std::min(max_chunk, n);
+    const size_t rel_bytes = up(8 * (size_t)(max_chunk + 1));
+    const size_t fws_bytes = up(ws_layout(max_chunk).total);
+    if (buf_bytes < used_bytes + 2 * (rel_bytes + fws_bytes + 512))
+      return set_error(DG_E_BUFFER, "buffer too small for the range's offsets and two chunks");
+    const size_t half = ((buf_bytes - used_bytes) / 2) & ~size_t(255);
+    const int64_t cap = (int64_t)((half - rel_bytes - fws_bytes) / 8) & ~int64_t(63);
     hipStream_t st[2] = {static_cast<hipStream_t>(stream_a), static_cast<hipStream_t>(stream_b)};
+    const uint8_t* blob = nullptr;
+    dg_status rc = device_blob(g, &blob);
+    if (rc != DG_OK) return rc;
+    // 1. Row sizes and offsets of the whole range, then chunks cut exactly
+    //    where the rows stop fitting a half.
+    int64_t total = 0;
+    rc = sizes_impl(g, dgc::LocSrc{nullptr, first}, n, g_off, s_ws, &total, st[0]);
+    if (rc != DG_OK) return rc;
+    std::vector<int64_t> h_off((size_t)n + 1);
+    DG_HIP(hipMemcpy(h_off.data(), g_off, 8 * (size_t)(n + 1), hipMemcpyDeviceToHost), "copy offsets");
+    // 2. Chunks alternate halves and streams; the fills are asynchronous.
     bool used[2] = {false, false};
-    int64_t pos = first, chunk = max_chunk;
-    std::vector<int64_t> h_off;
-    int c = 0;
-    dg_status rc = DG_OK;
-    while (pos < first + n) {
+    uint32_t bits = 0;
+    auto retire = [&](int h) -> dg_status {  // the half's fill and consumer have finished
+      uint8_t* base = p + used_bytes + h * half;
+      uint32_t b = 0;
+      DG_HIP(hipStreamSynchronize(st[h]), "chunk sync");
+      DG_HIP(hipMemcpy(&b, base + rel_bytes + ws_layout(max_chunk).err, 4, hipMemcpyDeviceToHost), "copy flags");
+      bits |= b;
+      used[h] = false;
+      return DG_OK;
+    };
+    int64_t pos = 0;
+    for (int c = 0; pos < n; ++c) {
       const int h = c & 1;
-      uint8_t* base = static_cast<uint8_t*>(d_buf) + h * half;
-      int64_t* d_off = reinterpret_cast<int64_t*>(base);
-      void* ws = base + off_bytes;
-      uint32_t* ids = reinterpret_cast<uint32_t*>(base + off_bytes + ws_bytes);
-      uint32_t* cnt = ids + cap;
-      // The consumer of the chunk that last used this half has finished.
-      if (used[h]) DG_HIP(hipStreamSynchronize(st[h]), "consumer sync");
-      int64_t m = std::min(chunk, first + n - pos), total = 0;
-      dg_status e = enumerate_impl(g, dgc::LocSrc{nullptr, pos}, m, d_off, ids, cnt, cap, ws, &total, st[h]);
-      if (e == DG_E_BUFFER) {
-        // The rows of the longest prefix below `cap` are complete.
-        h_off.resize((size_t)m + 1);
-        DG_HIP(hipMemcpy(h_off.data(), d_off, 8 * (size_t)(m + 1), hipMemcpyDeviceToHost), "copy offsets");
-        const int64_t k = (int64_t)(std::upper_bound(h_off.begin(), h_off.end(), cap) - h_off.begin()) - 1;
-        if (k <= 0) {
-          rc = set_error(DG_E_BUFFER, "one location's row does not fit half of the buffer");
-          break;
-        }
-        m = k;
-        total = h_off[(size_t)k];
-        chunk = k;
-      } else if (e != DG_OK) {
-        rc = e;
+      if (used[h]) {
+        rc = retire(h);
+        if (rc != DG_OK) break;
+        if (bits) break;
+      }
+      const int64_t lim = std::min(n, pos + max_chunk);
+      const int64_t end = (int64_t)(std::upper_bound(h_off.begin() + pos, h_off.begin() + lim + 1, h_off[pos] + cap) -
+                                    h_off.begin()) - 1;
+      const int64_t m = end - pos;
+      if (m <= 0) {
+        rc = set_error(DG_E_BUFFER, "one location's row does not fit half of the buffer");
         break;
       }
+      uint8_t* base = p + used_bytes + h * half;
+      int64_t* rel = reinterpret_cast<int64_t*>(base);
+      uint8_t* fws = base + rel_bytes;
+      uint32_t* ids = reinterpret_cast<uint32_t*>(base + rel_bytes + fws_bytes);
+      uint32_t* cnt = ids + cap;
+      uint32_t* err = reinterpret_cast<uint32_t*>(fws + ws_layout(max_chunk).err);
+      DG_HIP(dgk::launch_zero(err, st[h]), "zero");
+      DG_HIP(fill_launch(g, blob, dgc::LocSrc{nullptr, first + pos}, m, g_off + pos, h_off[pos], ids, cnt, err,
+                         st[h]),
+             "fill kernel");
+      DG_HIP(dgk::launch_rebase(g_off + pos, rel, m + 1, h_off[pos], st[h]), "chunk offsets");
       used[h] = true;
-      if (fn(user, pos, m, d_off, ids, cnt, total, st[h]) != 0) {
+      if (fn(user, first + pos, m, rel, ids, cnt, h_off[end] - h_off[pos], st[h]) != 0) {
         rc = set_error(DG_E_STOPPED, "the chunk consumer stopped the stream");
         break;
       }
-      pos += m;
-      ++c;
+      pos = end;
     }
     for (int h = 0; h < 2; ++h)
-      if (used[h]) DG_HIP(hipStreamSynchronize(st[h]), "final sync");
+      if (used[h]) {
+        dg_status r2 = retire(h);
+        if (rc == DG_OK) rc = r2;
+      }
+    if (rc == DG_OK && bits) rc = device_errors(bits);
     return rc;
   });
 }

@@ -44,9 +44,9 @@ std::string jit_enum_source(const Plan& p, int block) {
     << "    int64_t* __restrict__ offsets, uint32_t* __restrict__ err) {\n"
     << "  dgk_dev::sizes_body<DG_B>(dg_plan, locs, n, offsets, err);\n}\n"
     << "extern \"C\" __global__ __launch_bounds__(DG_B) void dg_fill(dgc::LocSrc locs, int64_t n,\n"
-    << "    const int64_t* __restrict__ offsets, uint32_t* __restrict__ ids, uint32_t* __restrict__ cnt,\n"
-    << "    uint32_t* __restrict__ err) {\n"
-    << "  dgk_dev::fill_body<DG_B>(dg_plan, locs, n, offsets, ids, cnt, err);\n}\n"
+    << "    const int64_t* __restrict__ offsets, int64_t base, uint32_t* __restrict__ ids,\n"
+    << "    uint32_t* __restrict__ cnt, uint32_t* __restrict__ err) {\n"
+    << "  dgk_dev::fill_body<DG_B>(dg_plan, locs, n, offsets, base, ids, cnt, err);\n}\n"
     << "extern \"C\" __global__ __launch_bounds__(DG_B) void dg_enumerate(dgc::LocSrc locs, int64_t n,\n"
     << "    int64_t* __restrict__ offsets, uint32_t* __restrict__ ids, uint32_t* __restrict__ cnt, uint64_t capacity,\n"
     << "    uint64_t* __restrict__ status, unsigned long long* __restrict__ ticket, uint32_t* __restrict__ err) {\n"

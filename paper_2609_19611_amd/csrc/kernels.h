@@ -9,8 +9,11 @@ namespace dgk {
 
 hipError_t launch_sizes(const uint8_t* blob, dgc::LocSrc locs, int64_t n, int64_t* offsets, uint32_t* err,
                         int block, uint32_t lds, hipStream_t s);
-hipError_t launch_fill(const uint8_t* blob, dgc::LocSrc locs, int64_t n, const int64_t* offsets, uint32_t* ids,
-                       uint32_t* cnt, uint32_t* err, int block, uint32_t lds, hipStream_t s);
+// Row i is written at [offsets[i] - base, offsets[i+1] - base) of ids/cnt.
+hipError_t launch_fill(const uint8_t* blob, dgc::LocSrc locs, int64_t n, const int64_t* offsets, int64_t base,
+                       uint32_t* ids, uint32_t* cnt, uint32_t* err, int block, uint32_t lds, hipStream_t s);
+// dst[i] = src[i] - base for i < count.
+hipError_t launch_rebase(const int64_t* src, int64_t* dst, int64_t count, int64_t base, hipStream_t s);
 // pp: device copy of the pair plan; lds: pp's lds_bytes.  found: a word
 // counting mismatching locations (cleared by the caller); with limit > 0,
 // locations that start after `limit` mismatches were found are skipped.

@@ -20,10 +20,10 @@ __global__ __launch_bounds__(BLOCK) void k_sizes(const uint8_t* __restrict__ blo
 
 template <int BLOCK>
 __global__ __launch_bounds__(BLOCK) void k_fill(const uint8_t* __restrict__ blob, dgc::LocSrc locs, int64_t n,
-                                                const int64_t* __restrict__ offsets,
+                                                const int64_t* __restrict__ offsets, int64_t base,
                                                 uint32_t* __restrict__ ids, uint32_t* __restrict__ cnt,
                                                 uint32_t* __restrict__ err) {
-  dgk_dev::fill_body<BLOCK>(blob, locs, n, offsets, ids, cnt, err);
+  dgk_dev::fill_body<BLOCK>(blob, locs, n, offsets, base, ids, cnt, err);
 }
 
 template <int BLOCK>
@@ -139,6 +139,11 @@ __global__ void k_scatter_mismatch(const uint8_t* __restrict__ status, const int
 
 __global__ void k_zero_offsets(int64_t* __restrict__ v) { v[0] = 0; }
 
+__global__ void k_rebase(const int64_t* __restrict__ src, int64_t* __restrict__ dst, int64_t count, int64_t base) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < count) dst[i] = src[i] - base;
+}
+
 __global__ void k_zero_word(uint32_t* __restrict__ p) { *p = 0u; }
 
 template <class K>
@@ -167,17 +172,18 @@ hipError_t launch_sizes(const uint8_t* blob, dgc::LocSrc locs, int64_t n, int64_
   return hipGetLastError();
 }
 
-hipError_t launch_fill(const uint8_t* blob, dgc::LocSrc locs, int64_t n, const int64_t* offsets, uint32_t* ids,
-                       uint32_t* cnt, uint32_t* err, int block, uint32_t lds, hipStream_t s) {
+hipError_t launch_fill(const uint8_t* blob, dgc::LocSrc locs, int64_t n, const int64_t* offsets, int64_t base,
+                       uint32_t* ids, uint32_t* cnt, uint32_t* err, int block, uint32_t lds, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   if (block != 64 && block != 256) return hipErrorInvalidConfiguration;
   hipError_t e;
   if (block == 256) {
     if ((e = allow_lds(k_fill<256>, lds)) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_fill<256>, dim3((unsigned)n), dim3(256), lds, s, blob, locs, n, offsets, ids, cnt, err);
+    hipLaunchKernelGGL(k_fill<256>, dim3((unsigned)n), dim3(256), lds, s, blob, locs, n, offsets, base, ids, cnt,
+                       err);
   } else {
     if ((e = allow_lds(k_fill<64>, lds)) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_fill<64>, dim3((unsigned)n), dim3(64), lds, s, blob, locs, n, offsets, ids, cnt, err);
+    hipLaunchKernelGGL(k_fill<64>, dim3((unsigned)n), dim3(64), lds, s, blob, locs, n, offsets, base, ids, cnt, err);
   }
   return hipGetLastError();
 }
@@ -222,6 +228,12 @@ hipError_t launch_enumerate(const uint8_t* blob, dgc::LocSrc locs, int64_t n, in
     hipLaunchKernelGGL(k_enumerate<64>, dim3((unsigned)n), dim3(64), lds, s, blob, locs, n, offsets, ids, cnt,
                        capacity, status, t, err);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_rebase(const int64_t* src, int64_t* dst, int64_t count, int64_t base, hipStream_t s) {
+  if (count <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_rebase, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, s, src, dst, count, base);
   return hipGetLastError();
 }
 

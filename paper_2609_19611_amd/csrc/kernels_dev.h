@@ -110,17 +110,17 @@ DGC void sizes_body(const uint8_t* __restrict__ blob, dgc::LocSrc locs, int64_t 
 
 template <int BLOCK>
 DGC void fill_body(const uint8_t* __restrict__ blob, dgc::LocSrc locs, int64_t n,
-                   const int64_t* __restrict__ offsets, uint32_t* __restrict__ ids, uint32_t* __restrict__ cnt,
-                   uint32_t* __restrict__ err) {
+                   const int64_t* __restrict__ offsets, int64_t base, uint32_t* __restrict__ ids,
+                   uint32_t* __restrict__ cnt, uint32_t* __restrict__ err) {
   __shared__ uint32_t wsum[BLOCK / 64];
   const int64_t i = blockIdx.x;
   if (i >= n) return;
   DevCtx<BLOCK> c{wsum};
   uint32_t e = 0;
   uint8_t* area = reinterpret_cast<uint8_t*>(dg_smem);
-  const int64_t start = offsets[i];
-  const int64_t room = offsets[i + 1] - start;
-  // Writes stay inside [offsets[i], offsets[i+1]) whatever this row's size.
+  // Row i goes to [offsets[i] - base, offsets[i+1] - base) whatever its size.
+  const int64_t start = offsets[i] - base;
+  const int64_t room = offsets[i + 1] - offsets[i];
   const uint64_t rows = dgc::location_row<DevCtx<BLOCK>, dgc::EMIT_FILL>(
       c, blob, dgc::loc_at(locs, i), area, ids + start, cnt + start, room > 0 ? (uint64_t)room : 0ull, &e);
   if (threadIdx.x == 0 && (int64_t)rows != room) e |= DGP_ERR_SIZE;

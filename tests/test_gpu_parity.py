@@ -428,6 +428,7 @@ def test_streamed_enumeration_matches_one_pass(B):
     chunks = []
 
     def consume(first, o, i, c, stream):
+        # (.cpu() on the current stream, which is the chunk's)
         chunks.append((first, o.cpu().numpy().copy(), i.cpu().numpy().copy(), c.cpu().numpy().copy()))
 
     B.dg_enumerate_stream(g, 0, numel, buf, 8192, consume)
@@ -449,8 +450,13 @@ def test_streamed_enumeration_matches_one_pass(B):
     # halves of 64 entries: the first row (56 entries, a corner) fits, the
     # second (65) does not
     got = []
+    def up(x):
+        return (x + 255) & ~255
+
+    used = up(8 * 9) + up(B.dg_workspace_size(g, 8))
+    half = up(8 * 5) + up(B.dg_workspace_size(g, 4)) + 64 * 8  # room for 64 entries
+    small = torch.empty(used + 2 * half, dtype=torch.uint8, device="cuda")
     with pytest.raises(B.DgError) as e:
-        B.dg_enumerate_stream(g, 0, numel, torch.empty(2 * 2560, dtype=torch.uint8, device="cuda"), 4,
-                              lambda first, o, i, c, s: got.append((first, int(o[-1]))))
+        B.dg_enumerate_stream(g, 0, 8, small, 4, lambda first, o, i, c, s: got.append((first, int(o[-1]))))
     assert e.value.name == "DG_E_BUFFER"
     assert got == [(0, int(want_off[1]))]
