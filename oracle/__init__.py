@@ -58,11 +58,12 @@ def _load():
     lib.dgo_leaf_total.argtypes = [P]
     lib.dgo_leaf_total.restype = ctypes.c_uint64
     lib.dgo_tensor_info.argtypes = [P, ctypes.c_int, ctypes.c_char_p, ctypes.c_int, P, P, P, P]
-    lib.dgo_enumerate.argtypes = [P, P, i64, ctypes.c_int]
+    lib.dgo_enumerate.argtypes = [P, P, i64, ctypes.c_int, ctypes.c_int]
     lib.dgo_enumerate.restype = P
     lib.dgo_result_total.argtypes = [P]
     lib.dgo_result_total.restype = i64
     lib.dgo_result_copy.argtypes = [P, P, P, P]
+    lib.dgo_result_copy_wide.argtypes = [P, P, P, P]
     lib.dgo_result_free.argtypes = [P]
     lib.dgo_compare.argtypes = [P, P, P, i64, ctypes.c_int, P]
     lib.dgo_reads.argtypes = [P, ctypes.c_int, i64, P, P, P, i64]
@@ -132,19 +133,22 @@ class Graph:
                 return i
         raise KeyError(name)
 
-    def enumerate(self, locs, threads: int = 1):
-        """CSR of the footprints: (offsets int64[n+1], ids uint32, counts uint32)."""
+    def enumerate(self, locs, threads: int = 1, wide: bool = False):
+        """CSR of the footprints: (offsets int64[n+1], ids, counts), ids and
+        counts uint32 (wide=False) or uint64 (wide=True)."""
         lib = _load()
         locs = np.ascontiguousarray(np.asarray(locs, dtype=np.int64))
-        r = lib.dgo_enumerate(self._h, locs.ctypes.data, len(locs), threads)
+        r = lib.dgo_enumerate(self._h, locs.ctypes.data, len(locs), threads, int(wide))
         if not r:
             raise OracleError(lib.dgo_error().decode())
         try:
             total = lib.dgo_result_total(r)
             offsets = np.empty(len(locs) + 1, dtype=np.int64)
-            ids = np.empty(total, dtype=np.uint32)
-            counts = np.empty(total, dtype=np.uint32)
-            lib.dgo_result_copy(r, offsets.ctypes.data, ids.ctypes.data, counts.ctypes.data)
+            dt = np.uint64 if wide else np.uint32
+            ids = np.empty(total, dtype=dt)
+            counts = np.empty(total, dtype=dt)
+            copy = lib.dgo_result_copy_wide if wide else lib.dgo_result_copy
+            copy(r, offsets.ctypes.data, ids.ctypes.data, counts.ctypes.data)
         finally:
             lib.dgo_result_free(r)
         return offsets, ids, counts

@@ -29,7 +29,11 @@
 // element index, as (global id = leaf base + row-major flat index, count).
 // Locations are flat row-major indices into the output (Sec. 3.3 "Setup":
 // R_y maps flat indices).  Path counts are exact (uint64 with overflow
-// checks); a count that does not fit 32 bits is an error.
+// checks).  Two result widths (the paper fixes none; ids are a leaf base
+// plus a flat index, counts are path counts): the 32-bit form rejects a graph
+// with more than 2^32 - 1 leaf elements and a count that does not fit 32
+// bits, the 64-bit form holds both in 64 bits.  Graphs are limited to 2^62
+// leaf elements, so that every id and every offset is a non-negative int64.
 
 #include <algorithm>
 #include <cctype>
@@ -577,7 +581,7 @@ Graph parse_graph(const std::string& text) {
   }
   if (!header) throw Error("missing 'dgir 1' header");
   if (g.output < 0) throw Error("missing 'output' statement");
-  if (g.leaf_total > 0xFFFFFFFFull) throw Error("leaf elements exceed 32-bit ids");
+  if (g.leaf_total > (1ull << 62)) throw Error("leaf elements exceed 2^62");
   return g;
 }
 
@@ -899,7 +903,7 @@ uint64_t checked_mul(uint64_t a, uint64_t b) {
   return r;
 }
 
-typedef std::vector<std::pair<uint32_t, uint32_t>> Row;
+typedef std::vector<std::pair<uint64_t, uint64_t>> Row;
 
 // Back-projection of one output location to its leaf multiset.
 Row enumerate_one(const Graph& g, int64_t loc) {
@@ -922,17 +926,26 @@ Row enumerate_one(const Graph& g, int64_t loc) {
   Row row;
   for (int t : g.leaves) {
     const Tensor& T = g.tensors[t];
-    for (const auto& kv : F[t]) {
-      if (kv.second > 0xFFFFFFFFull) throw Error("path count exceeds 32 bits");
-      row.push_back({(uint32_t)(T.base + (uint64_t)kv.first), (uint32_t)kv.second});
-    }
+    for (const auto& kv : F[t]) row.push_back({T.base + (uint64_t)kv.first, kv.second});
   }
   return row;
 }
 
+// The 32-bit form of a row: every count must fit 32 bits (ids do when the
+// graph has at most 2^32 - 1 leaf elements, checked once per call).
+const Row& narrow(const Row& row) {
+  for (const auto& e : row)
+    if (e.second > 0xFFFFFFFFull) throw Error("path count exceeds 32 bits");
+  return row;
+}
+
+void require_narrow_ids(const Graph& g) {
+  if (g.leaf_total > 0xFFFFFFFFull) throw Error("leaf ids need 64 bits");
+}
+
 struct Result {
   std::vector<int64_t> offsets;
-  std::vector<uint32_t> ids, counts;
+  std::vector<uint64_t> ids, counts;
 };
 
 template <class F>
@@ -954,10 +967,14 @@ void parallel_blocks(int64_t n, int nthreads, F f) {
   for (auto& e : errs) if (!e.empty()) throw Error(e);
 }
 
-Result enumerate_all(const Graph& g, const int64_t* locs, int64_t n, int nthreads) {
+Result enumerate_all(const Graph& g, const int64_t* locs, int64_t n, int nthreads, bool wide) {
+  if (!wide) require_narrow_ids(g);
   std::vector<Row> rows(n);
   parallel_blocks(n, nthreads, [&](int64_t lo, int64_t hi, int) {
-    for (int64_t i = lo; i < hi; ++i) rows[i] = enumerate_one(g, locs[i]);
+    for (int64_t i = lo; i < hi; ++i) {
+      rows[i] = enumerate_one(g, locs[i]);
+      if (!wide) narrow(rows[i]);
+    }
   });
   Result r;
   r.offsets.resize(n + 1);
@@ -1038,10 +1055,11 @@ int dgo_tensor_info(const dgo_graph* g, int t, char* name, int name_len, int64_t
 
 int dgo_output_tensor(const dgo_graph* g) { return g->g.output; }
 
-dgo_result* dgo_enumerate(const dgo_graph* g, const int64_t* locs, int64_t n, int nthreads) {
+// wide = 0: 32-bit ids and counts; wide = 1: 64-bit ids and counts.
+dgo_result* dgo_enumerate(const dgo_graph* g, const int64_t* locs, int64_t n, int nthreads, int wide) {
   try {
     auto* r = new dgo_result;
-    r->r = enumerate_all(g->g, locs, n, nthreads);
+    r->r = enumerate_all(g->g, locs, n, nthreads, wide != 0);
     return r;
   } catch (const std::exception& e) {
     g_err = e.what();
@@ -1051,11 +1069,21 @@ dgo_result* dgo_enumerate(const dgo_graph* g, const int64_t* locs, int64_t n, in
 
 int64_t dgo_result_total(const dgo_result* r) { return r->r.offsets.back(); }
 
+// Copies a result made with dgo_enumerate(..., wide = 0).
 void dgo_result_copy(const dgo_result* r, int64_t* offsets, uint32_t* ids, uint32_t* counts) {
   memcpy(offsets, r->r.offsets.data(), r->r.offsets.size() * sizeof(int64_t));
+  for (size_t i = 0; i < r->r.ids.size(); ++i) {
+    ids[i] = (uint32_t)r->r.ids[i];
+    counts[i] = (uint32_t)r->r.counts[i];
+  }
+}
+
+// Copies a result made with dgo_enumerate(..., wide = 1).
+void dgo_result_copy_wide(const dgo_result* r, int64_t* offsets, uint64_t* ids, uint64_t* counts) {
+  memcpy(offsets, r->r.offsets.data(), r->r.offsets.size() * sizeof(int64_t));
   if (!r->r.ids.empty()) {
-    memcpy(ids, r->r.ids.data(), r->r.ids.size() * sizeof(uint32_t));
-    memcpy(counts, r->r.counts.data(), r->r.counts.size() * sizeof(uint32_t));
+    memcpy(ids, r->r.ids.data(), r->r.ids.size() * sizeof(uint64_t));
+    memcpy(counts, r->r.counts.data(), r->r.counts.size() * sizeof(uint64_t));
   }
 }
 
@@ -1065,9 +1093,10 @@ int dgo_compare(const dgo_graph* a, const dgo_graph* b, const int64_t* locs, int
                 uint8_t* status) {
   try {
     check_signature(a->g, b->g);
+    require_narrow_ids(a->g);
     parallel_blocks(n, nthreads, [&](int64_t lo, int64_t hi, int) {
       for (int64_t i = lo; i < hi; ++i)
-        status[i] = compare_rows(enumerate_one(a->g, locs[i]), enumerate_one(b->g, locs[i]));
+        status[i] = compare_rows(narrow(enumerate_one(a->g, locs[i])), narrow(enumerate_one(b->g, locs[i])));
     });
     return 0;
   } catch (const std::exception& e) {

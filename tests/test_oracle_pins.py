@@ -319,15 +319,47 @@ def test_location_out_of_range_and_overflow():
         g.enumerate([8])
     with pytest.raises(oracle.OracleError):
         g.enumerate([-1])
-    # Nested group norms over 4096 elements: counts pass 2**32.
-    txt = tiny_graphs._g([("x", [1, 4096])],
-                         [("a", "layer_norm", ["x"], dict(ndims=1)), ("b", "layer_norm", ["a"], dict(ndims=1)),
-                          ("y", "layer_norm", ["b"], dict(ndims=1))], "y", [1, 4096])
+    # Nested layer norms over 4096 elements: counts pass 2**32.
     with pytest.raises(oracle.OracleError) as e:
-        oracle.Graph(txt).enumerate([0])
+        oracle.Graph(tiny_graphs.nested_layer_norms(4096)).enumerate([0])
     assert "32 bits" in str(e.value)
 
 
+@pytest.mark.parametrize("n,loc", [(5, 3), (4096, 0), (4096, 4095)])
+def test_wide_counts_closed_form(n, loc):
+    """64-bit path counts past 2^32 (n = 4096 gives about 1.2e18)."""
+    off, ids, cnt = oracle.Graph(tiny_graphs.nested_layer_norms(n)).enumerate([loc], wide=True)
+    assert ids.dtype == np.uint64 and cnt.dtype == np.uint64
+    assert off.tolist() == [0, n]
+    assert ids.tolist() == list(range(n))
+    assert cnt.tolist() == tiny_graphs.nested_layer_norm_counts(n, loc)
+    if n == 4096:
+        assert int(cnt.min()) > 2 ** 32
+
+
+def test_wide_equals_narrow_where_both_fit():
+    for name in ("c1", "c2", "c3"):
+        g = oracle.Graph(W.CONFIGS[name]["text"]())
+        locs = W.config_locations(name)[:64]
+        o32, i32, c32 = g.enumerate(locs)
+        o64, i64, c64 = g.enumerate(locs, wide=True)
+        assert (o32 == o64).all()
+        assert (i32.astype(np.uint64) == i64).all() and (c32.astype(np.uint64) == c64).all()
+
+
 def test_leaf_total_limit():
-    with pytest.raises(oracle.OracleError):
-        oracle.Graph("dgir 1\nleaf x 65536,65536\noutput x 65536,65536\n")
+    """Graphs up to 2^62 leaf elements parse; 32-bit ids refuse more than
+    2^32 - 1 of them; 64-bit ids name a leaf past 2^32 as its base plus its
+    flat index (leaves in declaration order)."""
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.Graph("dgir 1\nleaf x 1073741824,1073741824,8\noutput x 1073741824,1073741824,8\n")
+    assert "2^62" in str(e.value)
+    g = oracle.Graph("dgir 1\nleaf a 65536,65536\nleaf x 8\nop y relu x\noutput y 8\n")
+    assert g.leaf_total == 2 ** 32 + 8
+    with pytest.raises(oracle.OracleError) as e:
+        g.enumerate([0])
+    assert "64 bits" in str(e.value)
+    off, ids, cnt = g.enumerate([0, 5, 7], wide=True)
+    assert off.tolist() == [0, 1, 2, 3]
+    assert ids.tolist() == [2 ** 32, 2 ** 32 + 5, 2 ** 32 + 7]
+    assert cnt.tolist() == [1, 1, 1]

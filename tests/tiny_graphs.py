@@ -159,3 +159,22 @@ def catalogue():
     G["paper_ref_small"] = (paper_reference_text(N=2, C=3, H=4, W=2), True)
     G["paper_kernel_small"] = (paper_kernel_text(N=2, C=3, H=4, W=2, h_limit=2), True)
     return G
+
+
+def nested_layer_norms(n):
+    """Three layer norms in a row over n elements: path counts near
+    n^5 (past 2^32 from n = 1024 on)."""
+    return _g([("x", [1, n])],
+               [("a", "layer_norm", ["x"], dict(ndims=1)), ("b", "layer_norm", ["a"], dict(ndims=1)),
+                ("y", "layer_norm", ["b"], dict(ndims=1))], "y", [1, n])
+
+
+def nested_layer_norm_counts(n, loc):
+    """Closed form of three nested layer norms (no affine) over n elements.
+    One norm reaches x[s] n + 2 times through its statistics and x[l] once
+    more, so its path-count matrix is M = a J + I with a = n + 2 and J the
+    all-ones matrix; path counts compose as matrix products and J^2 = n J
+    gives M^3 = c J + I with c = (a^2 n + 2a)(a n + 1) + a."""
+    a = n + 2
+    c = (a * a * n + 2 * a) * (a * n + 1) + a
+    return [c + (1 if s == loc else 0) for s in range(n)]
