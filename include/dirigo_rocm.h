@@ -69,8 +69,10 @@ typedef int32_t dg_status;
 #define DG_E_SHAPE (-3)          /* inconsistent shapes or attributes */
 #define DG_E_UNSUPPORTED_OP (-4) /* op kind, or a form of it, not handled */
 #define DG_E_RANGE (-5)          /* a location outside [0, output numel) */
-#define DG_E_OVERFLOW (-6)       /* leaf elements >= 2^32, or a path count
-                                    that does not fit 32 bits */
+#define DG_E_OVERFLOW (-6)       /* leaf elements beyond 2^62 or a static
+                                    path-count bound beyond 2^63; in the
+                                    32-bit calls, ids or a path count that
+                                    do not fit 32 bits */
 #define DG_E_SIGNATURE (-7)      /* compare: leaves or output shape differ */
 #define DG_E_WORKSPACE (-8)      /* workspace missing or too small */
 #define DG_E_HIP (-9)            /* HIP runtime error (message attached) */
@@ -124,7 +126,7 @@ typedef struct dg_graph dg_graph;
  *     "(expr)/s"; "(expr)//s" floors).  Expressions are sums of c*o<k>,
  *     c*w<k> and integers.
  * Returns DG_E_PARSE, DG_E_SHAPE, DG_E_UNSUPPORTED_OP or DG_E_OVERFLOW
- * (leaf elements >= 2^32, or a static path-count bound beyond 64 bits) on
+ * (leaf elements beyond 2^62, or a static path-count bound beyond 2^63) on
  * failure; *out is set only on success and is owned by the caller, who
  * releases it with dg_graph_destroy.
  */
@@ -169,6 +171,7 @@ typedef struct {
   double count_bound;         /* static upper bound on one path count */
   int32_t n_instructions;     /* per-location plan length */
   int32_t lds_bytes;          /* local data share one location needs */
+  int32_t lds_wide_bytes;     /* the same with 64-bit ids and counts */
   int32_t block_threads;      /* threads working on one location */
   int32_t max_leaf_terms;     /* separable terms of the busiest leaf */
   int32_t specialized;        /* kernels specialised for this graph on the
@@ -238,6 +241,18 @@ dg_status dg_enumerate_fill(const dg_graph* g, const int64_t* d_locs, int64_t n,
  * (the same graph and locations as an earlier call) needs this one call. */
 dg_status dg_enumerate(const dg_graph* g, const int64_t* d_locs, int64_t n, int64_t* d_offsets, uint32_t* d_ids,
                        uint32_t* d_counts, int64_t capacity, void* d_ws, int64_t* h_total, void* stream);
+
+/* dg_enumerate_wide: dg_enumerate with 64-bit ids and path counts, for
+ * graphs whose leaves hold 2^32 elements or more (global ids up to 2^62)
+ * or whose path counts reach 2^32 (the static bound is below 2^63, so
+ * 64-bit counts never overflow).  d_ids and d_counts hold `capacity`
+ * uint64 entries each.  The 32-bit calls (dg_enumerate_fill, dg_enumerate,
+ * dg_enumerate_range, dg_enumerate_stream) return DG_E_OVERFLOW for a graph
+ * whose ids need 64 bits, and for a path count of 2^32 or more.
+ * Otherwise as dg_enumerate. */
+dg_status dg_enumerate_wide(const dg_graph* g, const int64_t* d_locs, int64_t n, int64_t* d_offsets,
+                            uint64_t* d_ids, uint64_t* d_counts, int64_t capacity, void* d_ws, int64_t* h_total,
+                            void* stream);
 
 /* dg_enumerate_range: dg_enumerate over the contiguous flat locations
  * first, first + 1, ..., first + n - 1 (row i belongs to location

@@ -48,6 +48,7 @@ class GraphInfo(ctypes.Structure):
         ("count_bound", ctypes.c_double),
         ("n_instructions", ctypes.c_int32),
         ("lds_bytes", ctypes.c_int32),
+        ("lds_wide_bytes", ctypes.c_int32),
         ("block_threads", ctypes.c_int32),
         ("max_leaf_terms", ctypes.c_int32),
         ("specialized", ctypes.c_int32),
@@ -98,6 +99,7 @@ def _load():
         "dg_enumerate_range": ([P, i64, i64, P, P, P, i64, P, ctypes.POINTER(i64), P], i32),
         "dg_compare_range": ([P, P, i64, i64, i64, P, P, ctypes.POINTER(i64), P, P], i32),
         "dg_enumerate_stream": ([P, i64, i64, P, sz, i64, CHUNK_FN, P, P, P], i32),
+        "dg_enumerate_wide": ([P, P, i64, P, P, P, i64, P, ctypes.POINTER(i64), P], i32),
         "dg_last_error": ([], ctypes.c_char_p),
     }
     for name, (args, res) in sig.items():
@@ -185,6 +187,7 @@ def dg_graph_info(g: Graph) -> dict:
         "count_bound": info.count_bound,
         "n_instructions": info.n_instructions,
         "lds_bytes": info.lds_bytes,
+        "lds_wide_bytes": info.lds_wide_bytes,
         "block_threads": info.block_threads,
         "max_leaf_terms": info.max_leaf_terms,
         "specialized": info.specialized,
@@ -262,6 +265,27 @@ def dg_compare(a: Graph, b: Graph, d_locs: torch.Tensor, d_status: torch.Tensor,
     _check(_lib.dg_compare(a.handle, b.handle, _ptr(d_locs), n, _ptr(d_status), _ptr(d_mismatch),
                            ctypes.byref(nm), _ptr(d_ws), _stream(stream)))
     return nm.value
+
+
+def dg_enumerate_wide(g: Graph, d_locs: torch.Tensor, d_offsets: torch.Tensor, d_ids: torch.Tensor,
+                      d_counts: torch.Tensor, d_ws: torch.Tensor, stream=None) -> int:
+    """dg_enumerate with 64-bit ids and counts (int64 or uint64 device
+    tensors; int64 ones hold the uint64 values' bits).  Returns the total;
+    raises DgError(DG_E_BUFFER) if the rows do not fit (the offsets are then
+    valid)."""
+    n = d_locs.numel()
+    _dev_i64(d_locs, "locations")
+    _dev_i64(d_offsets, "offsets")
+    if d_offsets.numel() < n + 1:
+        raise ValueError("offsets needs n + 1 entries")
+    for t, what in ((d_ids, "ids"), (d_counts, "counts")):
+        if not t.is_cuda or t.dtype not in (torch.int64, torch.uint64) or not t.is_contiguous():
+            raise ValueError(f"{what} must be a contiguous 64-bit device tensor")
+    cap = min(d_ids.numel(), d_counts.numel())
+    total = ctypes.c_int64()
+    _check(_lib.dg_enumerate_wide(g.handle, _ptr(d_locs), n, _ptr(d_offsets), _ptr(d_ids), _ptr(d_counts), cap,
+                                  _ptr(d_ws), ctypes.byref(total), _stream(stream)))
+    return total.value
 
 
 def dg_enumerate_range(g: Graph, first: int, n: int, d_offsets: torch.Tensor, d_ids: torch.Tensor,

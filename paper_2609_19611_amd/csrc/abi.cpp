@@ -34,6 +34,8 @@ struct dg_graph {
   std::mutex mu;
   std::map<int, uint8_t*> dev_blob;  // compiled plan per device
   std::map<int, DevKernels> jit;     // specialised kernels per device
+  std::map<int, DevKernels> jit_wide;  // specialised 64-bit enumeration per device
+  uint32_t lds_wide = 0;             // LDS per location with 64-bit ids and counts
   uint64_t serial = 0;               // unique per graph in the process
   // Specialised comparison kernels with another graph: (device, other's
   // serial, block) -> kernels.
@@ -81,6 +83,7 @@ dg_status finalize(dg_graph* g) {
     if (b == 64 || b == 128 || b == 256 || b == 512 || b == 1024) g->block = b;
   }
   g->lds = dg::plan_lds_bytes(g->plan, g->block);
+  g->lds_wide = dg::plan_lds_bytes(g->plan, g->block, 8);
   return DG_OK;
 }
 
@@ -140,6 +143,24 @@ const dg::JitModule* pair_jit(const dg_graph* ca, const dg_graph* b, const dgc::
   }
   return k.ok ? &k.jm : nullptr;
 }
+
+// Specialised 64-bit enumeration kernel of g on the current device, or null.
+const dg::JitModule* graph_jit_wide(const dg_graph* cg) {
+  if (!dg::jit_enabled()) return nullptr;
+  dg_graph* g = const_cast<dg_graph*>(cg);
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return nullptr;
+  std::lock_guard<std::mutex> lock(g->mu);
+  DevKernels& k = g->jit_wide[dev];
+  if (!k.tried) {
+    k.tried = true;
+    k.ok = dg::jit_load(dg::jit_wide_source(g->plan, g->block), &k.jm, &k.log) && k.jm.enumerate_wide;
+  }
+  return k.ok ? &k.jm : nullptr;
+}
+
+// Leaf ids of g fit 32 bits.
+bool narrow_ids(const dg_graph* g) { return g->ir.leaf_total <= 0xFFFFFFFFull; }
 
 hipError_t launch_module(hipFunction_t f, int64_t n, int block, uint32_t lds, hipStream_t s, void** args) {
   if (n <= 0) return hipSuccess;
@@ -280,6 +301,7 @@ dg_status dg_graph_info(const dg_graph* g, dg_graph_info_t* out) {
   out->count_bound = g->plan.count_bound;
   out->n_instructions = g->plan.header().ninstr;
   out->lds_bytes = (int32_t)g->lds;
+  out->lds_wide_bytes = (int32_t)g->lds_wide;
   out->block_threads = g->block;
   out->max_leaf_terms = g->plan.max_leaf_terms;
   out->specialized = -1;
@@ -362,6 +384,7 @@ dg_status dg_enumerate_fill(const dg_graph* g, const int64_t* d_locs, int64_t n,
   if (!g || n < 0 || (n > 0 && (!d_locs || !d_offsets || !d_ids || !d_counts)))
     return set_error(DG_E_INVALID_ARG, "bad argument");
   if (!d_ws) return set_error(DG_E_WORKSPACE, "workspace is required");
+  if (!narrow_ids(g)) return set_error(DG_E_OVERFLOW, "leaf ids need 64 bits: use dg_enumerate_wide");
   if (n == 0) return DG_OK;
   if (g->lds > (uint32_t)max_lds_per_block())
     return set_error(DG_E_CAPACITY, "one location needs " + std::to_string(g->lds) + " bytes of LDS");
@@ -377,12 +400,18 @@ dg_status dg_enumerate_fill(const dg_graph* g, const int64_t* d_locs, int64_t n,
 
 namespace {
 
-// Single pass over the locations of `src` (a list or a flat range).
-dg_status enumerate_impl(const dg_graph* g, dgc::LocSrc src, int64_t n, int64_t* d_offsets, uint32_t* d_ids,
-                         uint32_t* d_counts, int64_t capacity, void* d_ws, int64_t* h_total, void* stream) {
+// Single pass over the locations of `src` (a list or a flat range), with
+// 32-bit (Word = uint32_t) or 64-bit ids and counts.
+extern "C++" template <class Word>
+dg_status enumerate_impl(const dg_graph* g, dgc::LocSrc src, int64_t n, int64_t* d_offsets, Word* d_ids,
+                         Word* d_counts, int64_t capacity, void* d_ws, int64_t* h_total, void* stream) {
+  constexpr bool wide = sizeof(Word) == 8;
   if (!d_ws) return set_error(DG_E_WORKSPACE, "workspace is required");
-  if (g->lds > (uint32_t)max_lds_per_block())
-    return set_error(DG_E_CAPACITY, "one location needs " + std::to_string(g->lds) + " bytes of LDS");
+  if (!wide && !narrow_ids(g))
+    return set_error(DG_E_OVERFLOW, "leaf ids need 64 bits: use dg_enumerate_wide");
+  const uint32_t lds = wide ? g->lds_wide : g->lds;
+  if (lds > (uint32_t)max_lds_per_block())
+    return set_error(DG_E_CAPACITY, "one location needs " + std::to_string(lds) + " bytes of LDS");
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (n == 0) {
     DG_HIP(dgk::launch_scan(d_offsets, 0, nullptr, s), "offsets");
@@ -400,14 +429,19 @@ dg_status enumerate_impl(const dg_graph* g, dgc::LocSrc src, int64_t n, int64_t*
   uint64_t* status = reinterpret_cast<uint64_t*>(ws + w.flags);
   uint64_t* ticket = reinterpret_cast<uint64_t*>(ws + w.ticket);
   uint64_t cap = (uint64_t)capacity;
-  if (const dg::JitModule* jm = graph_jit(g)) {
+  const dg::JitModule* jm = wide ? graph_jit_wide(g) : graph_jit(g);
+  if (jm) {
     DG_HIP(dgk::launch_zero_u64(status, n, s), "zero status");
     DG_HIP(dgk::launch_zero_u64(ticket, 1, s), "zero ticket");
     void* args[] = {&src, &n, &d_offsets, &d_ids, &d_counts, &cap, &status, &ticket, &err};
-    DG_HIP(launch_module(jm->enumerate, n, g->block, g->lds, s, args), "enumerate kernel");
+    DG_HIP(launch_module(wide ? jm->enumerate_wide : jm->enumerate, n, g->block, lds, s, args), "enumerate kernel");
+  } else if constexpr (wide) {
+    DG_HIP(dgk::launch_enumerate_wide(blob, src, n, d_offsets, d_ids, d_counts, cap, status, ticket, err, g->block,
+                                      lds, s),
+           "enumerate kernel");
   } else {
-    DG_HIP(dgk::launch_enumerate(blob, src, n, d_offsets, d_ids, d_counts, cap, status, ticket, err, g->block,
-                                 g->lds, s),
+    DG_HIP(dgk::launch_enumerate(blob, src, n, d_offsets, d_ids, d_counts, cap, status, ticket, err, g->block, lds,
+                                 s),
            "enumerate kernel");
   }
   int64_t total = 0;
@@ -435,6 +469,15 @@ dg_status dg_enumerate(const dg_graph* g, const int64_t* d_locs, int64_t n, int6
   return enumerate_impl(g, dgc::LocSrc{d_locs, 0}, n, d_offsets, d_ids, d_counts, capacity, d_ws, h_total, stream);
 }
 
+dg_status dg_enumerate_wide(const dg_graph* g, const int64_t* d_locs, int64_t n, int64_t* d_offsets,
+                            uint64_t* d_ids, uint64_t* d_counts, int64_t capacity, void* d_ws, int64_t* h_total,
+                            void* stream) {
+  if (!g || !d_offsets || !h_total || n < 0 || capacity < 0 || (n > 0 && !d_locs) ||
+      (capacity > 0 && (!d_ids || !d_counts)))
+    return set_error(DG_E_INVALID_ARG, "bad argument");
+  return enumerate_impl(g, dgc::LocSrc{d_locs, 0}, n, d_offsets, d_ids, d_counts, capacity, d_ws, h_total, stream);
+}
+
 dg_status dg_enumerate_range(const dg_graph* g, int64_t first, int64_t n, int64_t* d_offsets, uint32_t* d_ids,
                              uint32_t* d_counts, int64_t capacity, void* d_ws, int64_t* h_total, void* stream) {
   if (!g || !d_offsets || !h_total || n < 0 || capacity < 0 || (capacity > 0 && (!d_ids || !d_counts)))
@@ -448,6 +491,7 @@ dg_status dg_enumerate_stream(const dg_graph* g, int64_t first, int64_t n, void*
                               int64_t max_chunk, dg_chunk_fn fn, void* user, void* stream_a, void* stream_b) {
   if (!g || !d_buf || !fn || n < 0 || max_chunk <= 0) return set_error(DG_E_INVALID_ARG, "bad argument");
   if (!range_ok(g, first, n)) return set_error(DG_E_RANGE, "the location range leaves the output");
+  if (!narrow_ids(g)) return set_error(DG_E_OVERFLOW, "leaf ids need 64 bits: use dg_enumerate_wide");
   if (n == 0) return DG_OK;
   return guarded([&]() -> dg_status {
     // Buffer: offsets of the whole range | sizes workspace | two halves of

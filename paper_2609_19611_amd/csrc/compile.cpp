@@ -430,6 +430,36 @@ class Compiler {
     return r;
   }
 
+  // How many points of a component sum can land on one target value: all of
+  // them, except that a variable occurring in exactly one target term is
+  // pinned by the others.  With the others fixed, one target value leaves K
+  // inner values (1 without an outer division or with an exact one, s with
+  // a floor division by s), so at most ceil(K / |coef|) values of that
+  // term's quotient, each taken by at most vdiv values of the variable
+  // (2 vdiv - 1 where it can be negative: the division truncates).
+  double collisions(const IndexFn& target, const std::vector<int>& vars, const std::vector<int64_t>& width, int R,
+                    const ReadGroup& G) {
+    double points = 1;
+    for (int64_t w : width) points *= (double)w;
+    const int64_t K = target.mode == 2 ? target.s : 1;
+    double best = points;
+    for (size_t q = 0; q < vars.size(); ++q) {
+      const IndexFn::Term* only = nullptr;
+      int uses = 0;
+      for (const auto& tm : target.terms)
+        if (tm.var == vars[q]) {
+          only = &tm;
+          ++uses;
+        }
+      if (uses != 1 || only->coef == 0 || width[q] <= 0) continue;
+      const bool negative = vars[q] >= R && G.wlo[vars[q] - R] < 0;
+      const int64_t per = only->vdiv == 1 ? 1 : (negative ? 2 * only->vdiv - 1 : only->vdiv);
+      const int64_t pin = std::min<int64_t>(width[q], ceil_div(K, std::llabs(only->coef)) * per);
+      best = std::min(best, points / (double)width[q] * (double)pin);
+    }
+    return best;
+  }
+
   // Sum over one component.  Returns a factor slot (target != nullptr) or a
   // scalar slot; a component of window variables without predicates and
   // without a target folds into `folded` and returns -1.
@@ -515,7 +545,7 @@ class Compiler {
       int64_t count = (target->mode ? ceil_div(span, target->s) : span) + 1;
       FactorPos tp = target_pos(*target, t, vars, R, G);
       if (tp.known) count = std::min(count, floor_frac(tp.hi - tp.lo) + 1);
-      slot = new_factor(std::min(count, tsize), tsize, points * weight);
+      slot = new_factor(std::min(count, tsize), tsize, collisions(*target, vars, width, R, G) * weight);
       pos_[slot] = tp;
       if (preds.empty() && vars.size() == 1 && vars[0] >= R && target->mode == 0 && target->terms.size() == 1 &&
           target->terms[0].vdiv == 1 && (target->terms[0].coef == 1 || target->terms[0].coef == -1)) {
@@ -665,11 +695,11 @@ Plan Compiler::run() {
     L.rank = (int32_t)T.shape.size();
     L.nterm = (int32_t)ts.size();
     L.term0 = (int32_t)dterms.size();
-    L.base = (uint32_t)T.base;
+    L.base = T.base;
     uint64_t stride = 1;
     for (int d = L.rank - 1; d >= 0; --d) {
       L.shape[d] = (int32_t)T.shape[d];
-      L.stride[d] = (uint32_t)stride;
+      L.stride[d] = stride;
       stride *= (uint64_t)T.shape[d];
     }
     double lb = 0;
@@ -857,10 +887,10 @@ Plan Compiler::run() {
 
 Plan compile_plan(const GraphIR& g) { return Compiler(g).run(); }
 
-uint32_t plan_lds_bytes(const Plan& p, int nthreads) {
+uint32_t plan_lds_bytes(const Plan& p, int nthreads, uint32_t word_bytes) {
   const DgpHeader& h = p.header();
   dgc::PlanLayout PL = dgc::plan_layout(&h, dgc::vars_bytes(h.serial_vars, nthreads));
-  dgc::EmitLayout E = dgc::emit_layout(PL.end, h.max_leaf_terms, h.union_entries, h.emit_entries);
+  dgc::EmitLayout E = dgc::emit_layout(PL.end, h.max_leaf_terms, h.union_entries, h.emit_entries, word_bytes);
   return (E.end + 15u) & ~15u;
 }
 

@@ -43,8 +43,8 @@ struct Plan {
 Plan compile_plan(const GraphIR& g);
 
 // Local data share bytes one location of this plan needs with a block of
-// `nthreads` threads.
-uint32_t plan_lds_bytes(const Plan& p, int nthreads);
+// `nthreads` threads (word_bytes 4: 32-bit ids and counts, 8: 64-bit).
+uint32_t plan_lds_bytes(const Plan& p, int nthreads, uint32_t word_bytes = 4);
 
 // Combined per-leaf emission shapes and LDS layout for comparing two plans
 // location by location (same leaves in the same order).

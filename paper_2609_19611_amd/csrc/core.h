@@ -109,12 +109,15 @@ DGC PlanLayout plan_layout(const DgpHeader* h, uint32_t base) {
   return L;
 }
 
-DGC EmitLayout emit_layout(uint32_t base, int32_t max_terms, int32_t union_entries, int32_t emit_entries) {
+// word_bytes: 4 for 32-bit ids and counts, 8 for 64-bit ones (the tables'
+// words have that width).
+DGC EmitLayout emit_layout(uint32_t base, int32_t max_terms, int32_t union_entries, int32_t emit_entries,
+                           uint32_t word_bytes = 4) {
   EmitLayout E;
   E.terms = align8(base);
   E.ulist = E.terms + (uint32_t)sizeof(TermRef) * (uint32_t)(max_terms > 0 ? max_terms : 1);
-  E.tables = align8(E.ulist + 4u * (uint32_t)union_entries);
-  E.hdr = align8(E.tables + 4u * (uint32_t)emit_entries);
+  E.tables = (E.ulist + 4u * (uint32_t)union_entries + 15u) & ~15u;
+  E.hdr = align8(E.tables + word_bytes * (uint32_t)emit_entries);
   E.tmax = E.hdr + (uint32_t)sizeof(LeafHdr);
   E.end = E.tmax + 16u * (uint32_t)(max_terms > 0 ? max_terms : 1);
   return E;
@@ -683,16 +686,23 @@ enum { EMIT_COUNT = 0, EMIT_FILL = 1, EMIT_COMPARE = 2 };
 
 struct LeafGeom {
   int32_t rank;
-  uint32_t base;
-  uint32_t stride[DGP_MAX_RANK];
+  uint64_t base;
+  uint64_t stride[DGP_MAX_RANK];
 };
+
+// Width of the emitted ids and counts (and of the emission tables' words):
+// uint32_t, or uint64_t for outputs whose ids or counts need 64 bits.
+template <class Word>
+DGC Word to_word(uint64_t v) {
+  return sizeof(Word) == 4 ? (Word)(v > 0xFFFFFFFFull ? 0xFFFFFFFFull : v) : (Word)v;
+}
 
 // Builds one table: entries r < n over dims [d0, d1); entry = (id part,
 // count part of every term).  With `tmax`, records each term's largest
 // value there (per-thread maxima, combined once per wave and term).
-template <class C>
+template <class C, class Word>
 DGC void build_table(C& c, const LeafGeom& G, const TermRef* terms, int nterm, const int32_t* ulist,
-                     const LeafHdr* H, int d0, int d1, bool with_base, uint32_t n, uint32_t* tab, uint64_t* tmax,
+                     const LeafHdr* H, int d0, int d1, bool with_base, uint32_t n, Word* tab, uint64_t* tmax,
                      const uint64_t* a64) {
   const int W = 1 + nterm;
   int32_t u[DGP_MAX_RANK];
@@ -717,16 +727,16 @@ DGC void build_table(C& c, const LeafGeom& G, const TermRef* terms, int nterm, c
     for (uint32_t r = (uint32_t)c.tid(); r < n; r += (uint32_t)c.nthreads()) {
       int32_t x[DGP_MAX_RANK];
       coords(r, x);
-      uint32_t pos = with_base ? G.base : 0u;
+      uint64_t pos = with_base ? G.base : 0u;
       uint64_t v = with_base ? terms[0].coef : 1ull;
       DG_UNROLL
       for (int d = 0; d < DGP_MAX_RANK; ++d)
         if (d >= d0 && d < d1) {
-          pos += (uint32_t)x[d] * G.stride[d];
+          pos += (uint64_t)x[d] * G.stride[d];
           if (v) v = mul_sat(v, term_val(terms[0], d, x[d], a64));
         }
-      tab[2 * (uint64_t)r] = pos;
-      tab[2 * (uint64_t)r + 1] = v > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)v;
+      tab[2 * (uint64_t)r] = (Word)pos;
+      tab[2 * (uint64_t)r + 1] = to_word<Word>(v);
       m = v > m ? v : m;
     }
     if (tmax) c.reduce_max(&tmax[0], m);
@@ -735,11 +745,11 @@ DGC void build_table(C& c, const LeafGeom& G, const TermRef* terms, int nterm, c
   for (uint32_t r = (uint32_t)c.tid(); r < n; r += (uint32_t)c.nthreads()) {
     int32_t x[DGP_MAX_RANK];
     coords(r, x);
-    uint32_t pos = with_base ? G.base : 0u;
+    uint64_t pos = with_base ? G.base : 0u;
     DG_UNROLL
     for (int d = 0; d < DGP_MAX_RANK; ++d)
-      if (d >= d0 && d < d1) pos += (uint32_t)x[d] * G.stride[d];
-    tab[(uint64_t)r * W] = pos;
+      if (d >= d0 && d < d1) pos += (uint64_t)x[d] * G.stride[d];
+    tab[(uint64_t)r * W] = (Word)pos;
   }
   DG_PLAN_UNROLL
   for (int t = 0; t < nterm; ++t) {
@@ -751,7 +761,7 @@ DGC void build_table(C& c, const LeafGeom& G, const TermRef* terms, int nterm, c
       DG_UNROLL
       for (int d = 0; d < DGP_MAX_RANK; ++d)
         if (d >= d0 && d < d1 && v) v = mul_sat(v, term_val(terms[t], d, x[d], a64));
-      tab[(uint64_t)r * W + 1 + t] = v > 0xFFFFFFFFull ? 0xFFFFFFFFu : (uint32_t)v;
+      tab[(uint64_t)r * W + 1 + t] = to_word<Word>(v);
       m = v > m ? v : m;
     }
     if (tmax) c.reduce_max(&tmax[t], m);
@@ -767,7 +777,7 @@ DGC bool prod_overflows(uint64_t a, uint64_t b) {
 // terms' nonzero coordinates and, with a split, the outer and inner tables,
 // and publishes in the leaf header: ok (0 when the leaf has no entry), the
 // union lengths, and the table lengths O and In.
-template <class W, int MODE>
+template <class W, int MODE, class Word = uint32_t>
 DGC void leaf_prepare(W& w, const LeafGeom& G, int split, const int32_t* ucap, const TermRef* terms, int na, int nb,
                       uint8_t* area, const EmitLayout& E, const FStat* st, bool checks, uint32_t* err) {
   const int tid = w.tid(), nt = w.nthreads();
@@ -834,8 +844,8 @@ DGC void leaf_prepare(W& w, const LeafGeom& G, int split, const int32_t* ucap, c
       else if (d < rank) In *= (uint32_t)u[d];
     }
     const int Wd = 1 + nterm;
-    uint32_t* otab = (uint32_t*)(area + E.tables);
-    uint32_t* itab = otab + (uint64_t)O * Wd;
+    Word* otab = (Word*)(area + E.tables);
+    Word* itab = otab + (uint64_t)O * Wd;
     uint64_t* tmax = checks ? (uint64_t*)(area + E.tmax) : nullptr;
     if (checks) {
       for (int i = tid; i < 2 * nterm; i += nt) tmax[i] = 0;
@@ -858,15 +868,31 @@ DGC void leaf_prepare(W& w, const LeafGeom& G, int split, const int32_t* ucap, c
   }
 }
 
+// Entry r of a single-term table: (id part, count part), one aligned
+// 8-byte (narrow) or 16-byte (wide) pair.
+DGC void pair_at(const uint32_t* tab, uint32_t r, uint32_t* id, uint32_t* cnt) {
+  const uint64_t v = ((const uint64_t*)tab)[r];
+  *id = (uint32_t)v;
+  *cnt = (uint32_t)(v >> 32);
+}
+DGC void pair_at(const uint64_t* tab, uint32_t r, uint64_t* id, uint64_t* cnt) {
+  struct alignas(16) P2 {
+    uint64_t a, b;
+  };
+  const P2 v = ((const P2*)tab)[r];
+  *id = v.a;
+  *cnt = v.b;
+}
+
 // Emits one prepared leaf (block `c`).
 //   EMIT_COUNT:   returns the number of nonzero entries.
 //   EMIT_FILL:    writes them at ids/cnt and returns their number.
 //   EMIT_COMPARE: returns 0 equal, 1 nonzero sets differ, 2 counts differ.
 //   `room` bounds the entries EMIT_FILL may write at ids/cnt; a leaf that
 //   would need more raises DGP_ERR_SIZE and writes nothing past it.
-template <class C, int MODE>
+template <class C, int MODE, class Word = uint32_t>
 DGC uint64_t leaf_emit(C& c, const LeafGeom& G, int split, const TermRef* terms, int na, int nb, uint8_t* area,
-                       const EmitLayout& E, uint32_t* ids, uint32_t* cnt, uint64_t room, uint32_t* err) {
+                       const EmitLayout& E, Word* ids, Word* cnt, uint64_t room, uint32_t* err) {
   const int tid = c.tid(), nt = c.nthreads();
   const int nterm = na + nb;
   const int rank = G.rank;
@@ -881,8 +907,8 @@ DGC uint64_t leaf_emit(C& c, const LeafGeom& G, int split, const TermRef* terms,
   if (!H->notab) {
     const int W = 1 + nterm;
     const uint32_t O = H->O, In = H->In;
-    const uint32_t* otab = (const uint32_t*)(area + E.tables);
-    const uint32_t* itab = otab + (uint64_t)O * W;
+    const Word* otab = (const Word*)(area + E.tables);
+    const Word* itab = otab + (uint64_t)O * W;
     const uint64_t total = (uint64_t)O * In;
     if (MODE == EMIT_FILL && nterm == 1) {
       // Dense single-term grid: every cell is an entry, in order.  Lanes are
@@ -895,25 +921,27 @@ DGC uint64_t leaf_emit(C& c, const LeafGeom& G, int split, const TermRef* terms,
       const int64_t head = nt >= 64 ? (int64_t)((((uintptr_t)ids) >> 2) & 63u) : 0;
       const int64_t step = nt;
       int64_t p = (int64_t)tid - head;
-      // (Single-term entries are 8-byte aligned (id part, count part)
-      // pairs: one 64-bit LDS read each, which keeps a wave's reads free of
-      // bank conflicts.)
-      const uint64_t* otab2 = (const uint64_t*)otab;
-      const uint64_t* itab2 = (const uint64_t*)itab;
+      // (Single-term entries are aligned (id part, count part) pairs, read
+      // as one 64- or 128-bit LDS access each, which keeps a wave's reads
+      // free of bank conflicts.)
       if (p >= 0 && p < tot) {
         const uint32_t r = (uint32_t)(p / In), j = (uint32_t)(p % In);
-        const uint64_t o = otab2[r], q = itab2[j];
-        c.store(&ids[p], (uint32_t)o + (uint32_t)q);
-        c.store(&cnt[p], (uint32_t)(o >> 32) * (uint32_t)(q >> 32));
+        Word oi, oc, qi, qc;
+        pair_at(otab, r, &oi, &oc);
+        pair_at(itab, j, &qi, &qc);
+        c.store(&ids[p], (Word)(oi + qi));
+        c.store(&cnt[p], (Word)(oc * qc));
       }
       p += step;
       if (p < tot) {
         uint32_t r = (uint32_t)(p / In), j = (uint32_t)(p % In);
         const uint32_t dr = (uint32_t)(step / In), dj = (uint32_t)(step % In);
         for (; p < tot; p += step) {
-          const uint64_t o = otab2[r], q = itab2[j];
-          c.store(&ids[p], (uint32_t)o + (uint32_t)q);
-          c.store(&cnt[p], (uint32_t)(o >> 32) * (uint32_t)(q >> 32));
+          Word oi, oc, qi, qc;
+          pair_at(otab, r, &oi, &oc);
+          pair_at(itab, j, &qi, &qc);
+          c.store(&ids[p], (Word)(oi + qi));
+          c.store(&cnt[p], (Word)(oc * qc));
           j += dj;
           r += dr;
           if (j >= In) {
@@ -930,12 +958,12 @@ DGC uint64_t leaf_emit(C& c, const LeafGeom& G, int split, const TermRef* terms,
     for (uint64_t chunk = 0; chunk < total; chunk += (uint64_t)nt) {
       const uint64_t p = chunk + (uint64_t)tid;
       uint64_t ca = 0, cb = 0;
-      uint32_t pos = 0;
+      Word pos = 0;
       if (p < total) {
-        // (A leaf has fewer than 2^32 elements, so cell indices fit 32 bits.)
+        // (Tables hold fewer than 2^32 cells, so cell indices fit 32 bits.)
         const uint32_t r = (uint32_t)p / In, j = (uint32_t)p - r * In;
-        const uint32_t* o = otab + (uint64_t)r * W;
-        const uint32_t* q = itab + (uint64_t)j * W;
+        const Word* o = otab + (uint64_t)r * W;
+        const Word* q = itab + (uint64_t)j * W;
         pos = o[0] + q[0];
         DG_PLAN_UNROLL
         for (int t = 0; t < na; ++t) ca += (uint64_t)o[1 + t] * q[1 + t];
@@ -947,14 +975,14 @@ DGC uint64_t leaf_emit(C& c, const LeafGeom& G, int split, const TermRef* terms,
         else if (ca != cb) flags |= 2u;
         if (c.any((flags & 1u) != 0)) return 1;
       } else {
-        if (ca > 0xFFFFFFFFull) *err |= DGP_ERR_OVERFLOW;
+        if (sizeof(Word) == 4 && ca > 0xFFFFFFFFull) *err |= DGP_ERR_OVERFLOW;
         const bool nz = ca != 0;
         uint32_t tot;
         const uint32_t pre = c.prefix(nz, &tot);
         if (MODE == EMIT_FILL && nz) {
           if (written + pre < room) {
             c.store(&ids[written + pre], pos);
-            c.store(&cnt[written + pre], (uint32_t)ca);
+            c.store(&cnt[written + pre], (Word)ca);
           } else {
             *err |= DGP_ERR_SIZE;
           }
@@ -975,7 +1003,7 @@ DGC uint64_t leaf_emit(C& c, const LeafGeom& G, int split, const TermRef* terms,
   for (uint64_t chunk = 0; chunk < total; chunk += (uint64_t)nt) {
     const uint64_t p = chunk + (uint64_t)tid;
     uint64_t ca = 0, cb = 0;
-    uint32_t pos = G.base;
+    uint64_t pos = G.base;
     if (p < total) {
       int32_t x[DGP_MAX_RANK];
       uint32_t rem = (uint32_t)p;  // (fewer than 2^32 cells)
@@ -986,7 +1014,7 @@ DGC uint64_t leaf_emit(C& c, const LeafGeom& G, int split, const TermRef* terms,
           const uint32_t i = rem % (uint32_t)u[d];
           rem /= (uint32_t)u[d];
           x[d] = ucoord(H, ulist, d, (int32_t)i);
-          pos += (uint32_t)x[d] * G.stride[d];
+          pos += (uint64_t)x[d] * G.stride[d];
         }
       }
       DG_PLAN_UNROLL
@@ -1004,14 +1032,14 @@ DGC uint64_t leaf_emit(C& c, const LeafGeom& G, int split, const TermRef* terms,
       else if (ca != cb) flags |= 2u;
       if (c.any((flags & 1u) != 0)) return 1;
     } else {
-      if (ca > 0xFFFFFFFFull) *err |= DGP_ERR_OVERFLOW;
+      if (sizeof(Word) == 4 && ca > 0xFFFFFFFFull) *err |= DGP_ERR_OVERFLOW;
       const bool nz = ca != 0;
       uint32_t tot;
       const uint32_t pre = c.prefix(nz, &tot);
       if (MODE == EMIT_FILL && nz) {
         if (written + pre < room) {
-          c.store(&ids[written + pre], pos);
-          c.store(&cnt[written + pre], (uint32_t)ca);
+          c.store(&ids[written + pre], (Word)pos);
+          c.store(&cnt[written + pre], (Word)ca);
         } else {
           *err |= DGP_ERR_SIZE;
         }
@@ -1073,12 +1101,14 @@ struct PlaceAt {
 // Leaf passes over a plan already in LDS (the block has synchronised since
 // the plan): the row size (EMIT_COUNT) or the row itself (EMIT_FILL, at most
 // `room` entries written at ids/cnt + place()).
-template <class C, int MODE, class Place>
-DGC uint64_t location_leaves(C& c, const uint8_t* blob, uint8_t* area, uint32_t* ids, uint32_t* cnt, uint64_t room,
+template <class C, int MODE, class Place, class Word = uint32_t>
+DGC uint64_t location_leaves(C& c, const uint8_t* blob, uint8_t* area, Word* ids, Word* cnt, uint64_t room,
                              uint32_t* err, Place& place) {
   const DgpHeader* h = (const DgpHeader*)blob;
   const PlanLayout PL = plan_layout(h, vars_bytes(h->serial_vars, c.nthreads()));
-  const EmitLayout E = emit_layout(PL.end, h->max_leaf_terms, h->union_entries, h->emit_entries);
+  const EmitLayout E = emit_layout(PL.end, h->max_leaf_terms, h->union_entries, h->emit_entries, sizeof(Word));
+  // 64-bit counts cannot overflow: the static bound is below 2^63.
+  const bool checks = sizeof(Word) == 4 && !h->no_overflow;
   const DgpLeaf* leaves = (const DgpLeaf*)(blob + h->leaf_off);
   const DgpTerm* T0 = (const DgpTerm*)(blob + h->term_off);
   const uint64_t* scal = (const uint64_t*)(area + PL.scal);
@@ -1101,24 +1131,24 @@ DGC uint64_t location_leaves(C& c, const uint8_t* blob, uint8_t* area, uint32_t*
       DG_PLAN_UNROLL
       for (int d = 0; d < L.rank; ++d) {
         n *= st[T.factor[d]].nnz;
-        if (!h->no_overflow) mx = mul_sat(mx, st[T.factor[d]].vmax);
+        if (checks) mx = mul_sat(mx, st[T.factor[d]].vmax);
       }
-      if (!h->no_overflow && n && mx > 0xFFFFFFFFull) *err |= DGP_ERR_OVERFLOW;
+      if (checks && n && mx > 0xFFFFFFFFull) *err |= DGP_ERR_OVERFLOW;
       off += n;
       continue;
     }
     const LeafGeom G = leaf_geom(L);
     leaf_terms(c, blob, l, area, PL, terms);
     c.sync();
-    leaf_prepare<C, MODE>(c, G, L.split, L.ucap, terms, L.nterm, 0, area, E, st, !h->no_overflow, err);
+    leaf_prepare<C, MODE, Word>(c, G, L.split, L.ucap, terms, L.nterm, 0, area, E, st, checks, err);
     c.sync();
     if (!placed) {
       base = place(c, &go);
       placed = true;
       if (!go) break;
     }
-    off += leaf_emit<C, MODE>(c, G, L.split, terms, L.nterm, 0, area, E, ids ? ids + base + off : nullptr,
-                              cnt ? cnt + base + off : nullptr, off < room ? room - off : 0, err);
+    off += leaf_emit<C, MODE, Word>(c, G, L.split, terms, L.nterm, 0, area, E, ids ? ids + base + off : nullptr,
+                                    cnt ? cnt + base + off : nullptr, off < room ? room - off : 0, err);
     c.sync();
   }
   if (!placed) place(c, &go);
@@ -1185,8 +1215,8 @@ DGC uint32_t location_compare(C& c, const uint8_t* blob_a, const uint8_t* blob_b
     leaf_prepare<C, EMIT_COMPARE>(c, G, PP->leaf[l].split, PP->leaf[l].ucap, terms, na, nb, area, E, nullptr,
                                   checks, err);
     c.sync();
-    const uint32_t s = (uint32_t)leaf_emit<C, EMIT_COMPARE>(c, G, PP->leaf[l].split, terms, na, nb, area, E,
-                                                            nullptr, nullptr, 0, err);
+    const uint32_t s = (uint32_t)leaf_emit<C, EMIT_COMPARE, uint32_t>(c, G, PP->leaf[l].split, terms, na, nb, area,
+                                                                      E, nullptr, nullptr, 0, err);
     c.sync();
     if (s == 1) return 1;
     if (s == 2) status = 2;

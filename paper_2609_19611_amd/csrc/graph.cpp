@@ -719,7 +719,7 @@ void add_leaf(GraphIR& g, const std::string& name, const Dims& shape) {
   t.leaf = (int)g.leaves.size();
   t.base = g.leaf_total;
   g.leaf_total += (uint64_t)numel(shape);
-  if (g.leaf_total > 0xFFFFFFFFull) fail(DG_E_OVERFLOW, "leaf elements exceed 32-bit global ids");
+  if (g.leaf_total > (1ull << 62)) fail(DG_E_OVERFLOW, "leaf elements exceed 2^62");
   g.leaves.push_back((int)g.tensors.size());
   g.tensors.push_back(t);
 }

@@ -28,6 +28,7 @@ struct HostCtx {
     if (v > *p) *p = v;
   }
   void store(uint32_t* p, uint32_t v) const { *p = v; }
+  void store(uint64_t* p, uint64_t v) const { *p = v; }
   void reduce_add(uint64_t* p, uint64_t v) const { *p += v; }
   void reduce_max(uint64_t* p, uint64_t v) const {
     if (v > *p) *p = v;

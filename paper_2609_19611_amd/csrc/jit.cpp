@@ -113,6 +113,7 @@ bool jit_load(const std::string& source, JitModule* out, std::string* log) {
   get("dg_fill", &out->fill);
   get("dg_enumerate", &out->enumerate);
   get("dg_compare", &out->compare);
+  get("dg_enumerate_wide", &out->enumerate_wide);
   return true;
 }
 

@@ -19,6 +19,8 @@ namespace dg {
 // Source of the specialised enumeration kernels (dg_sizes, dg_fill,
 // dg_enumerate) of one plan for blocks of `block` threads.
 std::string jit_enum_source(const Plan& p, int block);
+// Source of the specialised 64-bit enumeration kernel (dg_enumerate_wide).
+std::string jit_wide_source(const Plan& p, int block);
 // Source of the specialised comparison kernel (dg_compare) of a pair.
 std::string jit_compare_source(const Plan& a, const Plan& b, const dgc::PairPlan& pp, int block);
 
@@ -36,7 +38,7 @@ namespace dg {
 // Returns true and the module; on failure a message in *log.
 struct JitModule {
   hipModule_t mod = nullptr;
-  hipFunction_t sizes = nullptr, fill = nullptr, enumerate = nullptr, compare = nullptr;
+  hipFunction_t sizes = nullptr, fill = nullptr, enumerate = nullptr, compare = nullptr, enumerate_wide = nullptr;
 };
 bool jit_load(const std::string& source, JitModule* out, std::string* log);
 

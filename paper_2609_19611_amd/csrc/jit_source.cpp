@@ -54,6 +54,20 @@ std::string jit_enum_source(const Plan& p, int block) {
   return o.str();
 }
 
+std::string jit_wide_source(const Plan& p, int block) {
+  std::ostringstream o;
+  o << kPrelude;
+  emit_bytes(o, "dg_plan", p.blob);
+  o << "#define DG_B " << block << "\n"
+    << "extern \"C\" __global__ __launch_bounds__(DG_B) void dg_enumerate_wide(dgc::LocSrc locs, int64_t n,\n"
+    << "    int64_t* __restrict__ offsets, uint64_t* __restrict__ ids, uint64_t* __restrict__ cnt,\n"
+    << "    uint64_t capacity, uint64_t* __restrict__ status, unsigned long long* __restrict__ ticket,\n"
+    << "    uint32_t* __restrict__ err) {\n"
+    << "  dgk_dev::enumerate_body<DG_B, uint64_t>(dg_plan, locs, n, offsets, ids, cnt, capacity, status, ticket,"
+       " err);\n}\n";
+  return o.str();
+}
+
 std::string jit_compare_source(const Plan& a, const Plan& b, const dgc::PairPlan& pp, int block) {
   std::ostringstream o;
   o << kPrelude;

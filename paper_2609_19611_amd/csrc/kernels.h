@@ -28,6 +28,10 @@ int64_t scan_temp_entries(int64_t n);
 hipError_t launch_enumerate(const uint8_t* blob, dgc::LocSrc locs, int64_t n, int64_t* offsets, uint32_t* ids,
                             uint32_t* cnt, uint64_t capacity, uint64_t* status, uint64_t* ticket, uint32_t* err,
                             int block, uint32_t lds, hipStream_t s);
+// The same with 64-bit ids and counts.
+hipError_t launch_enumerate_wide(const uint8_t* blob, dgc::LocSrc locs, int64_t n, int64_t* offsets,
+                                 uint64_t* ids, uint64_t* cnt, uint64_t capacity, uint64_t* status, uint64_t* ticket,
+                                 uint32_t* err, int block, uint32_t lds, hipStream_t s);
 // Clears count 64-bit words.
 hipError_t launch_zero_u64(uint64_t* p, int64_t count, hipStream_t s);
 // Clears one error word (a kernel, so it may be recorded in a captured graph).

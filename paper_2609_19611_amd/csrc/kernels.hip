@@ -46,6 +46,16 @@ __global__ __launch_bounds__(BLOCK) void k_enumerate(const uint8_t* __restrict__
   dgk_dev::enumerate_body<BLOCK>(blob, locs, n, offsets, ids, cnt, capacity, status, ticket, err);
 }
 
+template <int BLOCK>
+__global__ __launch_bounds__(BLOCK) void k_enumerate_wide(const uint8_t* __restrict__ blob, dgc::LocSrc locs,
+                                                          int64_t n, int64_t* __restrict__ offsets,
+                                                          uint64_t* __restrict__ ids, uint64_t* __restrict__ cnt,
+                                                          uint64_t capacity, uint64_t* __restrict__ status,
+                                                          unsigned long long* __restrict__ ticket,
+                                                          uint32_t* __restrict__ err) {
+  dgk_dev::enumerate_body<BLOCK, uint64_t>(blob, locs, n, offsets, ids, cnt, capacity, status, ticket, err);
+}
+
 __global__ void k_zero_u64(uint64_t* __restrict__ p, int64_t count) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < count) p[i] = 0ull;
@@ -234,6 +244,27 @@ hipError_t launch_enumerate(const uint8_t* blob, dgc::LocSrc locs, int64_t n, in
 hipError_t launch_rebase(const int64_t* src, int64_t* dst, int64_t count, int64_t base, hipStream_t s) {
   if (count <= 0) return hipSuccess;
   hipLaunchKernelGGL(k_rebase, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, s, src, dst, count, base);
+  return hipGetLastError();
+}
+
+hipError_t launch_enumerate_wide(const uint8_t* blob, dgc::LocSrc locs, int64_t n, int64_t* offsets,
+                                 uint64_t* ids, uint64_t* cnt, uint64_t capacity, uint64_t* status, uint64_t* ticket,
+                                 uint32_t* err, int block, uint32_t lds, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  if (block != 64 && block != 256) return hipErrorInvalidConfiguration;
+  hipLaunchKernelGGL(k_zero_u64, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, status, n);
+  hipLaunchKernelGGL(k_zero_u64, dim3(1), dim3(1), 0, s, ticket, (int64_t)1);
+  hipError_t e;
+  unsigned long long* t = reinterpret_cast<unsigned long long*>(ticket);
+  if (block == 256) {
+    if ((e = allow_lds(k_enumerate_wide<256>, lds)) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_enumerate_wide<256>, dim3((unsigned)n), dim3(256), lds, s, blob, locs, n, offsets, ids, cnt,
+                       capacity, status, t, err);
+  } else {
+    if ((e = allow_lds(k_enumerate_wide<64>, lds)) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_enumerate_wide<64>, dim3((unsigned)n), dim3(64), lds, s, blob, locs, n, offsets, ids, cnt,
+                       capacity, status, t, err);
+  }
   return hipGetLastError();
 }
 

@@ -25,6 +25,7 @@ struct DevCtx {
     atomicMax(reinterpret_cast<unsigned long long*>(p), (unsigned long long)v);
   }
   DGC void store(uint32_t* p, uint32_t v) const { __builtin_nontemporal_store(v, p); }
+  DGC void store(uint64_t* p, uint64_t v) const { __builtin_nontemporal_store(v, p); }
   // Adds (or takes the maximum of) every thread's v into *p with at most
   // four LDS atomics per wave instead of one per thread: DPP lane permutes
   // (xor 1, xor 2, mirror within 8, mirror within 16) leave every row of 16
@@ -247,10 +248,10 @@ struct LookBack {
   }
 };
 
-template <int BLOCK>
+template <int BLOCK, class Word = uint32_t>
 DGC void enumerate_body(const uint8_t* __restrict__ blob, dgc::LocSrc locs, int64_t n,
-                                                     int64_t* __restrict__ offsets, uint32_t* __restrict__ ids,
-                                                     uint32_t* __restrict__ cnt, uint64_t capacity,
+                                                     int64_t* __restrict__ offsets, Word* __restrict__ ids,
+                                                     Word* __restrict__ cnt, uint64_t capacity,
                                                      uint64_t* __restrict__ status,
                                                      unsigned long long* __restrict__ ticket,
                                                      uint32_t* __restrict__ err) {
@@ -270,8 +271,9 @@ DGC void enumerate_body(const uint8_t* __restrict__ blob, dgc::LocSrc locs, int6
   if (ok) dgc::location_plan(c, blob, loc, area, &e);
   __syncthreads();
   dgc::PlaceAt none{0};
-  const uint64_t size =
-      ok ? dgc::location_leaves<DevCtx<BLOCK>, dgc::EMIT_COUNT>(c, blob, area, nullptr, nullptr, 0, &e, none) : 0ull;
+  const uint64_t size = ok ? dgc::location_leaves<DevCtx<BLOCK>, dgc::EMIT_COUNT, dgc::PlaceAt, Word>(
+                                 c, blob, area, nullptr, nullptr, 0, &e, none)
+                           : 0ull;
   if (threadIdx.x == 0) {
     __hip_atomic_store(&status[i], (i == 0 ? ST_PREFIX : ST_SIZE) | size, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   }
@@ -279,8 +281,8 @@ DGC void enumerate_body(const uint8_t* __restrict__ blob, dgc::LocSrc locs, int6
   // once when it has nothing to write).
   LookBack<BLOCK> place{status, i, n, size, capacity, offsets, &sh_off, &e};
   if (ok && size > 0) {
-    const uint64_t rows =
-        dgc::location_leaves<DevCtx<BLOCK>, dgc::EMIT_FILL>(c, blob, area, ids, cnt, size, &e, place);
+    const uint64_t rows = dgc::location_leaves<DevCtx<BLOCK>, dgc::EMIT_FILL, LookBack<BLOCK>, Word>(
+        c, blob, area, ids, cnt, size, &e, place);
     if (threadIdx.x == 0 && place.fits && rows != size) e |= DGP_ERR_SIZE;
   } else {
     bool go;

@@ -90,12 +90,11 @@ struct DgpLeaf {
   int32_t nterm;
   int32_t term0;      // first term in the term array
   int32_t split;      // dims [0, split) form the outer table, [split, rank) the inner
-  uint32_t base;      // global id of element 0
+  uint64_t base;      // global id of element 0
   int32_t outer_cap;  // table capacities (entries)
   int32_t inner_cap;
-  int32_t pad;
   int32_t shape[DGP_MAX_RANK];
-  uint32_t stride[DGP_MAX_RANK];
+  uint64_t stride[DGP_MAX_RANK];
   int32_t ucap[DGP_MAX_RANK];  // capacity of the per-dim union of nonzero coordinates
 };
 

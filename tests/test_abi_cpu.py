@@ -17,7 +17,7 @@ CAT = tiny_graphs.catalogue()
 
 def test_library_exports_every_header_symbol():
     names = B.header_symbols()
-    assert len(names) == 14
+    assert len(names) == 15
     lib = ctypes.CDLL(B.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -63,7 +63,7 @@ def test_build_matches_parse():
     ("dgir 1\nleaf x 2\nop y relu q\noutput y 2\n", "DG_E_PARSE"),
     ("dgir 1\nleaf x 2\nop y relu x\noutput y 3\n", "DG_E_SHAPE"),
     ("dgir 1\nleaf x 2\nop y relu x\n", "DG_E_PARSE"),
-    ("dgir 1\nleaf x 65536,65536\noutput x 65536,65536\n", "DG_E_OVERFLOW"),
+    ("dgir 1\nleaf x 1073741824,1073741824,8\noutput x 1073741824,1073741824,8\n", "DG_E_OVERFLOW"),
     ("dgir 1\nleaf x 2,3\nop y affine_gather x ; shape=2 idx0=o0+,o1\noutput y 2\n", "DG_E_PARSE"),
     ("dgir 1\nleaf x 2,3\nop y affine_gather x ; shape=2 idx0=o0\noutput y 2\n", "DG_E_SHAPE"),
     ("dgir 1\nleaf x 2,3\nop y conv x x\noutput y 2\n", "DG_E_SHAPE"),
@@ -119,3 +119,41 @@ def test_ranges_outside_the_output_are_rejected_before_any_work():
         assert B.STATUS_NAMES[rc] == "DG_E_RANGE", (first, n)
     rc = B._lib.dg_compare_range(g.handle, g.handle, 0, 4, -1, fake, fake, ctypes.byref(total), fake, None)
     assert B.STATUS_NAMES[rc] == "DG_E_INVALID_ARG"
+
+
+def test_graphs_with_64_bit_ids_parse_and_32_bit_calls_refuse_them():
+    """2^32 leaf elements: the graph builds; the 32-bit enumeration calls
+    report DG_E_OVERFLOW before any device work, the 64-bit call exists."""
+    g = B.dg_graph_parse("dgir 1\nleaf x 65536,65536\nop y relu x\noutput y 65536,65536\n")
+    assert B.dg_graph_info(g)["leaf_total"] == 1 << 32
+    fake = ctypes.c_void_p(0x1000)  # never dereferenced
+    total = ctypes.c_int64()
+    rc = B._lib.dg_enumerate(g.handle, fake, 1, fake, fake, fake, 16, fake, ctypes.byref(total), None)
+    assert B.STATUS_NAMES[rc] == "DG_E_OVERFLOW"
+    rc = B._lib.dg_enumerate_range(g.handle, 0, 1, fake, fake, fake, 16, fake, ctypes.byref(total), None)
+    assert B.STATUS_NAMES[rc] == "DG_E_OVERFLOW"
+    assert "64 bits" in B.dg_last_error()
+
+
+@pytest.mark.parametrize("name", sorted(tiny_graphs.catalogue()))
+def test_static_bounds_hold_everywhere(name):
+    """count_bound and max_row_size bound the oracle's rows at every output
+    location of the small graphs (the 32-bit kernels skip their run-time
+    overflow checks when count_bound fits 32 bits, so it must be sound)."""
+    text = tiny_graphs.catalogue()[name][0]
+    try:
+        info = B.dg_graph_info(B.dg_graph_parse(text))
+    except B.DgError as e:
+        pytest.skip(f"not handled by the library: {e}")
+    og = oracle.Graph(text)
+    off, ids, cnt = og.enumerate(range(og.output_numel), threads=4, wide=True)
+    assert info["max_row_size"] >= int(np.diff(off).max())
+    assert info["count_bound"] >= int(cnt.max())
+
+
+def test_static_bound_of_nested_norms_is_tight():
+    """Three nested layer norms over 4096 elements: the exact largest count
+    is about 1.15e18; the bound stays below 2^63, so the graph is accepted."""
+    info = B.dg_graph_info(B.dg_graph_parse(tiny_graphs.nested_layer_norms(4096)))
+    exact = max(tiny_graphs.nested_layer_norm_counts(4096, 0))
+    assert exact <= info["count_bound"] <= 1.01 * exact

@@ -203,12 +203,14 @@ def test_edge_cases(B):
     with pytest.raises(B.DgError) as e:
         B.enumerate_locations(g, [-1])
     assert e.value.name == "DG_E_RANGE"
-    txt = tiny_graphs._g([("x", [1, 4096])],
-                         [("a", "layer_norm", ["x"], dict(ndims=1)), ("b", "layer_norm", ["a"], dict(ndims=1)),
-                          ("y", "layer_norm", ["b"], dict(ndims=1))], "y", [1, 4096])
+    # Path counts past 32 bits (the 64-bit call handles them).
     with pytest.raises(B.DgError) as e:
-        B.enumerate_locations(B.dg_graph_parse(txt), [0])
+        B.enumerate_locations(B.dg_graph_parse(tiny_graphs.nested_layer_norms(2048)), [0])
     assert e.value.name == "DG_E_OVERFLOW"
+    # More LDS than one block can have.
+    with pytest.raises(B.DgError) as e:
+        B.enumerate_locations(B.dg_graph_parse(tiny_graphs.nested_layer_norms(4096)), [0])
+    assert e.value.name == "DG_E_CAPACITY"
     with pytest.raises(B.DgError) as e:
         B.compare_locations(g, B.dg_graph_parse(W.c1_text()), [0])
     assert e.value.name == "DG_E_SIGNATURE"
@@ -460,3 +462,108 @@ def test_streamed_enumeration_matches_one_pass(B):
         B.dg_enumerate_stream(g, 0, 8, small, 4, lambda first, o, i, c, s: got.append((first, int(o[-1]))))
     assert e.value.name == "DG_E_BUFFER"
     assert got == [(0, int(want_off[1]))]
+
+
+def _wide(B, g, locs):
+    """dg_enumerate_wide in two calls: the first, with no room for rows,
+    gives the offsets (DG_E_BUFFER unless every row is empty)."""
+    d_locs = torch.as_tensor(locs, dtype=torch.int64, device="cuda")
+    n = d_locs.numel()
+    ws = B.workspace(g, n)
+    off = torch.full((n + 1,), -7, dtype=torch.int64, device="cuda")
+    none = torch.empty(0, dtype=torch.int64, device="cuda")
+    try:
+        total = B.dg_enumerate_wide(g, d_locs, off, none, none, ws)
+    except B.DgError as e:
+        assert e.name == "DG_E_BUFFER"
+        total = int(off[-1])
+    ids = torch.full((max(total, 1),), -1, dtype=torch.int64, device="cuda")
+    cnt = torch.full((max(total, 1),), -1, dtype=torch.int64, device="cuda")
+    off2 = torch.full((n + 1,), -7, dtype=torch.int64, device="cuda")
+    assert B.dg_enumerate_wide(g, d_locs, off2, ids, cnt, ws) == total
+    assert torch.equal(off, off2)
+    return off2, ids[:total], cnt[:total]
+
+
+def _u64(t):
+    return t.cpu().numpy().view(np.uint64)
+
+
+@pytest.mark.parametrize("name", ["c5_small_var", "conv3d_groups", "gather_floor_flat", "diamond", "paper_kernel_small"])
+@pytest.mark.parametrize("kernels", ["specialized", "interpreted"])
+def test_wide_catalogue(B, name, kernels, monkeypatch):
+    monkeypatch.setenv("DIRIGO_JIT", "1" if kernels == "specialized" else "0")
+    text = CAT[name][0]
+    og = oracle.Graph(text)
+    locs = list(range(og.output_numel))[::-1]
+    off, ids, cnt = _wide(B, B.dg_graph_parse(text), locs)
+    ro, io, co = og.enumerate(locs, wide=True)
+    assert np.array_equal(off.cpu().numpy(), ro)
+    assert np.array_equal(_u64(ids), io) and np.array_equal(_u64(cnt), co)
+
+
+@pytest.mark.parametrize("name,step", [("c1", 1), ("c2", 1), ("c3", 5), ("c4", 97)])
+def test_wide_equals_narrow_on_workloads(B, name, step):
+    g = B.dg_graph_parse(W.CONFIGS[name]["text"]())
+    locs = W.config_locations(name)[::step]
+    a = _fused(B, g, locs)
+    b = _wide(B, g, locs)
+    assert torch.equal(a[0], b[0])
+    for x, y in zip(a[1:], b[1:]):
+        assert torch.equal(x.to(torch.int64) & 0xFFFFFFFF, y)
+
+
+@pytest.mark.parametrize("kernels", ["specialized", "interpreted"])
+def test_wide_counts_past_32_bits(B, kernels, monkeypatch):
+    """Three nested layer norms over 2048 elements: counts near 3.6e16.
+    The 32-bit call reports DG_E_OVERFLOW; the 64-bit one matches the
+    closed form and the oracle."""
+    monkeypatch.setenv("DIRIGO_JIT", "1" if kernels == "specialized" else "0")
+    n = 2048
+    text = tiny_graphs.nested_layer_norms(n)
+    g = B.dg_graph_parse(text)
+    locs = [0, 1, 1000, n - 1]
+    d_locs = torch.as_tensor(locs, dtype=torch.int64, device="cuda")
+    ws = B.workspace(g, len(locs))
+    off = torch.empty(len(locs) + 1, dtype=torch.int64, device="cuda")
+    ids = torch.empty(len(locs) * n, dtype=torch.int32, device="cuda")
+    cnt = torch.empty(len(locs) * n, dtype=torch.int32, device="cuda")
+    with pytest.raises(B.DgError) as e:
+        B.dg_enumerate(g, d_locs, off, ids, cnt, ws)
+    assert e.value.name == "DG_E_OVERFLOW"
+    off, ids, cnt = _wide(B, g, locs)
+    assert off.cpu().tolist() == [i * n for i in range(len(locs) + 1)]
+    ids_h, cnt_h = _u64(ids), _u64(cnt)
+    for i, l in enumerate(locs):
+        assert ids_h[i * n:(i + 1) * n].tolist() == list(range(n))
+        assert cnt_h[i * n:(i + 1) * n].tolist() == tiny_graphs.nested_layer_norm_counts(n, l)
+    ro, io, co = oracle.Graph(text).enumerate(locs, threads=4, wide=True)
+    assert np.array_equal(ids_h, io) and np.array_equal(cnt_h, co)
+
+
+def test_wide_ids_past_2_32(B):
+    """Leaves holding more than 2^32 elements: ids past 2^32, 32-bit calls
+    refuse the graph before any device work."""
+    # Row sums of a 2^20 x 4096 leaf declared after a 4096-element one: the
+    # last rows' ids cross 2^32.
+    R, K = 1 << 20, 4096
+    text = f"dgir 1\nleaf p {K}\nleaf a {R},{K}\nop y sum a ; dims=1 keepdim=0\noutput y {R}\n"
+    g = B.dg_graph_parse(text)
+    assert B.dg_graph_info(g)["leaf_total"] == K + 2 ** 32
+    locs = [0, 12345, R - 2, R - 1]
+    d_locs = torch.as_tensor(locs, dtype=torch.int64, device="cuda")
+    ws = B.workspace(g, len(locs))
+    off = torch.empty(len(locs) + 1, dtype=torch.int64, device="cuda")
+    buf = torch.empty(len(locs) * K, dtype=torch.int32, device="cuda")
+    with pytest.raises(B.DgError) as e:
+        B.dg_enumerate(g, d_locs, off, buf, buf, ws)
+    assert e.value.name == "DG_E_OVERFLOW"
+    off, ids, cnt = _wide(B, g, locs)
+    ids_h = _u64(ids)
+    for i, l in enumerate(locs):
+        want = K + l * K + np.arange(K, dtype=np.uint64)
+        assert np.array_equal(ids_h[i * K:(i + 1) * K], want)
+    assert bool((cnt == 1).all())
+    assert int(ids_h.max()) > 2 ** 32
+    ro, io, co = oracle.Graph(text).enumerate(locs, threads=4, wide=True)
+    assert np.array_equal(off.cpu().numpy(), ro) and np.array_equal(ids_h, io) and np.array_equal(_u64(cnt), co)
