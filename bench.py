@@ -40,6 +40,8 @@ def parse_args():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--two-pass", action="store_true",
                    help="time dg_enumerate_sizes + dg_enumerate_fill instead of the single-pass dg_enumerate")
+    p.add_argument("--wide", action="store_true",
+                   help="time dg_enumerate_wide (64-bit ids and counts) instead of dg_enumerate")
     p.add_argument("--full-output", action="store_true",
                    help="every output location: c5 compares all 33,554,432 (dg_compare_range; the faulty variants "
                         "stop at their first mismatch); c1-c4 stream the whole output's rows through a bounded "
@@ -198,6 +200,10 @@ def main():
               "rate is N times the one-GPU rate measured here.", file=sys.stderr)
         sys.exit(2)
 
+    if args.wide and (args.two_pass or args.full_output or args.workload == "c5"):
+        print("--wide times the single-pass enumeration of c1-c4 only", file=sys.stderr)
+        sys.exit(2)
+
     if args.copy_gib > 0:
         copy_calibration(args.copy_gib, args.steps, args.warmup)
         return
@@ -257,6 +263,7 @@ def main():
         if args.full_output:
             fault_ms = []
             for v in variants[1:]:
+                B.dg_compare_range(g, v, 0, 1, status, mism, ws)  # loads the pair's kernel (untimed)
                 torch.cuda.synchronize()
                 t1 = time.perf_counter()
                 B.dg_compare_range(g, v, 0, n, status, mism, ws, max_mismatch=1)
@@ -289,8 +296,9 @@ def main():
     # Size the output buffers once (untimed); every timed step then computes
     # the offsets and rows from scratch.
     total = B.dg_enumerate_sizes(g, d_locs, offsets, ws)
-    ids = torch.empty(max(total, 1), dtype=torch.int32, device=dev)
-    cnt = torch.empty(max(total, 1), dtype=torch.int32, device=dev)
+    word = torch.int64 if args.wide else torch.int32
+    ids = torch.empty(max(total, 1), dtype=word, device=dev)
+    cnt = torch.empty(max(total, 1), dtype=word, device=dev)
     kern_ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
                for _ in range(args.steps)]
 
@@ -306,12 +314,13 @@ def main():
                 kern_ev[i][1].record(stream)
             return t
     else:
-        kernel = "k_enumerate"
+        kernel = "k_enumerate_wide" if args.wide else "k_enumerate"
+        enumerate_call = B.dg_enumerate_wide if args.wide else B.dg_enumerate
 
         def step(i=None):
             if i is not None:
                 kern_ev[i][0].record(stream)
-            t = B.dg_enumerate(g, d_locs, offsets, ids, cnt, ws)
+            t = enumerate_call(g, d_locs, offsets, ids, cnt, ws)
             if i is not None:
                 kern_ev[i][1].record(stream)
             return t
@@ -333,18 +342,19 @@ def main():
     kern_ms = float(np.mean([a.elapsed_time(b) for a, b in kern_ev]))
     ms = elapsed * 1000 / args.steps
     # Algorithmic bytes per location: 8 (location) + 8 (offset) + 8 per entry
-    # (uint32 id + uint32 count).
-    alg_bytes = 16 * n + 8 * total
+    # (uint32 id + uint32 count; 16 with 64-bit ids and counts).
+    alg_bytes = 16 * n + (16 if args.wide else 8) * total
     achieved = alg_bytes / (kern_ms * 1e-3) / 1e9
     line = {
         "metric": "footprint entries/sec enumerated (with output locations/sec and % of HBM peak)",
         "value": total / (elapsed / args.steps), "unit": "entries/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": ms, "higher_is_better": True, "scaling": "weak",
-        "vs_baseline": None, "dtype": "u32",
+        "vs_baseline": None, "dtype": "u64" if args.wide else "u32",
         "data": "synthetic (shapes only; footprints are data independent)",
         "config": {"workload": f"{args.workload}: " + cfg["desc"], "locations": n, "entries_per_step": total,
                    "locations_per_s": n / (elapsed / args.steps), "block_threads": info["block_threads"],
-                   "lds_bytes": info["lds_bytes"], "path": "two-pass" if args.two_pass else "single-pass",
+                   "lds_bytes": info["lds_wide_bytes" if args.wide else "lds_bytes"],
+                   "path": "two-pass" if args.two_pass else ("single-pass, 64-bit" if args.wide else "single-pass"),
                    "kernels": "specialized" if specialized else "interpreted"},
         "roofline": {"bound": "hbm", "kernel": kernel, "achieved": achieved, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBS,

@@ -912,13 +912,14 @@ DGC uint64_t leaf_emit(C& c, const LeafGeom& G, int split, const TermRef* terms,
     const uint64_t total = (uint64_t)O * In;
     if (MODE == EMIT_FILL && nterm == 1) {
       // Dense single-term grid: every cell is an entry, in order.  Lanes are
-      // shifted so that each wave's stores cover whole aligned 256-byte
-      // blocks of the id array.
+      // shifted so that each wave's stores cover whole aligned blocks of 64
+      // words of the id array (256 bytes, or 512 with 64-bit words): rows
+      // start anywhere, and unaligned wave stores halve the write rate.
       if (total > room) *err |= DGP_ERR_SIZE;
       const int64_t tot = (int64_t)(total < room ? total : room);
-      // (Shift by the entries that precede ids in its 256-byte block; the
+      // (Shift by the entries that precede ids in its 64-word block; the
       // shift stays below the block width, so p + step >= 0 below.)
-      const int64_t head = nt >= 64 ? (int64_t)((((uintptr_t)ids) >> 2) & 63u) : 0;
+      const int64_t head = nt >= 64 ? (int64_t)((((uintptr_t)ids) / sizeof(Word)) & 63u) : 0;
       const int64_t step = nt;
       int64_t p = (int64_t)tid - head;
       // (Single-term entries are aligned (id part, count part) pairs, read

@@ -140,6 +140,19 @@ int dgh_jit_source(const char* text, int64_t len, int block, char* out, int64_t 
   }
 }
 
+// Source of the specialised 64-bit enumeration kernel of a graph.
+int dgh_jit_wide_source(const char* text, int64_t len, int block, char* out, int64_t cap) {
+  try {
+    dg::GraphIR ir = dg::parse_dgir(std::string(text, (size_t)len));
+    dg::Plan plan = dg::compile_plan(ir);
+    std::string s = dg::jit_wide_source(plan, block);
+    snprintf(out, (size_t)cap, "%s", s.c_str());
+    return (int)s.size();
+  } catch (const dg::Failure& e) {
+    return fail_with(e);
+  }
+}
+
 // Source of the specialised comparison kernel of a pair of graphs.
 int dgh_jit_compare_source(const char* ta, int64_t la, const char* tb, int64_t lb, int block, char* out,
                            int64_t cap) {

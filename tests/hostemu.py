@@ -30,6 +30,7 @@ def lib():
         _lib.dgh_fill.argtypes = [ctypes.c_char_p, i64, P, i64, P, P, P]
         _lib.dgh_compare.argtypes = [ctypes.c_char_p, i64, ctypes.c_char_p, i64, P, i64, P]
         _lib.dgh_jit_source.argtypes = [ctypes.c_char_p, i64, ctypes.c_int, ctypes.c_char_p, i64]
+        _lib.dgh_jit_wide_source.argtypes = [ctypes.c_char_p, i64, ctypes.c_int, ctypes.c_char_p, i64]
         _lib.dgh_jit_compare_source.argtypes = [ctypes.c_char_p, i64, ctypes.c_char_p, i64, ctypes.c_int,
                                                 ctypes.c_char_p, i64]
         _lib.dgh_jit_options.argtypes = [ctypes.c_char_p, i64]

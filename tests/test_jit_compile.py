@@ -89,6 +89,15 @@ def test_enumeration_kernels_compile(name, block):
         assert all(p == 0 for _, p in notes), notes
 
 
+@pytest.mark.parametrize("name,block", [("c1", 64), ("c4", 256)])
+def test_wide_enumeration_kernel_compiles(name, block):
+    t = W.CONFIGS[name]["text"]().encode()
+    src = _source(hostemu.lib().dgh_jit_wide_source, t, len(t), block)
+    notes = _kernel_notes(_compile(src))
+    assert [n for n, _ in notes] == ["dg_enumerate_wide"]
+    assert all(p == 0 for _, p in notes), notes
+
+
 def test_comparison_kernel_compiles():
     a = W.c5_reference_text(n=2, c=4, hw=6, co=3).encode()
     b = W.c5_variant_text(fault=W.c5_faults()[0], n=2, c=4, hw=6, co=3).encode()
