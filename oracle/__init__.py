@@ -66,6 +66,13 @@ def _load():
     lib.dgo_result_copy_wide.argtypes = [P, P, P, P]
     lib.dgo_result_free.argtypes = [P]
     lib.dgo_compare.argtypes = [P, P, P, i64, ctypes.c_int, P]
+    lib.dgo_tensor_gid.argtypes = [P, ctypes.c_int]
+    lib.dgo_tensor_gid.restype = ctypes.c_uint64
+    lib.dgo_dag_build.argtypes = [P, P, i64, ctypes.c_int]
+    lib.dgo_dag_build.restype = P
+    lib.dgo_dag_totals.argtypes = [P, P, P]
+    lib.dgo_dag_copy.argtypes = [P, P, P, P, P, P, P]
+    lib.dgo_dag_free.argtypes = [P]
     lib.dgo_reads.argtypes = [P, ctypes.c_int, i64, P, P, P, i64]
     lib.dgo_reads.restype = i64
     _lib = lib
@@ -157,6 +164,35 @@ class Graph:
         """{global id: path count} of one location."""
         off, ids, cnt = self.enumerate([loc])
         return dict(zip(ids.tolist(), cnt.tolist()))
+
+    def gid(self, tensor: int) -> int:
+        """Global id of element 0 of a tensor: its leaf base, or for an op
+        output leaf_total plus the element counts of the earlier ops."""
+        return _load().dgo_tensor_gid(self._h, tensor)
+
+    def dag(self, locs, threads: int = 1):
+        """Expression DAGs of res(y[l]) per location, as a dict of arrays:
+        node_offsets, edge_offsets (int64[n+1]); nodes, node_edge, edges,
+        mults (uint64).  Nodes are the non-leaf cone elements (ops in reverse
+        SSA order, elements ascending); node_edge is each node's first edge
+        relative to its location's first edge; edges are child global ids
+        in equation order with their multiplicities."""
+        lib = _load()
+        locs = np.ascontiguousarray(np.asarray(locs, dtype=np.int64))
+        h = lib.dgo_dag_build(self._h, locs.ctypes.data, len(locs), threads)
+        if not h:
+            raise OracleError(lib.dgo_error().decode())
+        try:
+            nn, ne = ctypes.c_int64(), ctypes.c_int64()
+            lib.dgo_dag_totals(h, ctypes.byref(nn), ctypes.byref(ne))
+            r = {"node_offsets": np.empty(len(locs) + 1, np.int64), "edge_offsets": np.empty(len(locs) + 1, np.int64),
+                 "nodes": np.empty(nn.value, np.uint64), "node_edge": np.empty(nn.value, np.uint64),
+                 "edges": np.empty(ne.value, np.uint64), "mults": np.empty(ne.value, np.uint64)}
+            lib.dgo_dag_copy(h, *(r[k].ctypes.data for k in ("node_offsets", "edge_offsets", "nodes", "node_edge",
+                                                             "edges", "mults")))
+        finally:
+            lib.dgo_dag_free(h)
+        return r
 
     def reads(self, tensor: int, loc: int):
         """R_k(l) of the op writing ``tensor``: list of (tensor, flat index, multiplicity)."""

@@ -683,8 +683,9 @@ void op_reads(const Graph& g, const Op& op, int64_t loc, const Emit& emit) {
     // Scatter form: input x[n, ci, i..] with W[ci, co_l, t..] lands on
     // out[n, co, i*s - p + t*d ..].  The reads of out[l] are every (ci, i, t)
     // of co's group with i*s - p + t*d == o in every dim and i inside x;
-    // plus b[co].  The condition is tested per dim by looping over all
-    // input positions and taps of that dim.
+    // plus b[co].  The condition is tested per dim by looping over all taps
+    // and input positions of that dim.  Order: ci, then taps ascending in
+    // row-major order (the canonical order of the summation, as in conv).
     const Shape &x = S(0), &w = S(1);
     size_t nsp = x.size() - 2;
     auto st = get_attr_or(op, "stride", std::vector<int64_t>(nsp, 1));
@@ -695,8 +696,8 @@ void op_reads(const Graph& g, const Op& op, int64_t loc, const Emit& emit) {
     int64_t n = o[0], co = o[1], grp = co / cout_g, col = co % cout_g;
     std::vector<std::vector<std::pair<int64_t, int64_t>>> pairs(nsp);  // (i, t) per dim
     for (size_t d = 0; d < nsp; ++d)
-      for (int64_t i = 0; i < x[2 + d]; ++i)
-        for (int64_t t = 0; t < w[2 + d]; ++t)
+      for (int64_t t = 0; t < w[2 + d]; ++t)
+        for (int64_t i = 0; i < x[2 + d]; ++i)
           if (i * st[d] - pd[d] + t * dl[d] == o[2 + d]) pairs[d].push_back({i, t});
     Shape pext(nsp);
     for (size_t d = 0; d < nsp; ++d) pext[d] = (int64_t)pairs[d].size();
@@ -948,6 +949,64 @@ struct Result {
   std::vector<uint64_t> ids, counts;
 };
 
+// ---------------------------------------------------------------------------
+// Expression DAG of res(y[l]) (Sec. 3.4, "Back-projection"): every tensor
+// element in the cone of y[l] is one node, shared wherever it occurs; a leaf
+// element is a variable, any other node is its op applied to the element
+// references of its per-element equation, in the equation's order.
+//
+// Global element ids: a leaf element keeps its id (leaf base + flat index);
+// the output of op k (SSA order) follows all leaves, at
+// leaf_total + sum of the element counts of ops 0..k-1, plus its flat index.
+// Nodes: the non-leaf cone elements, ops in reverse SSA order (y[l] first),
+// elements ascending within an op.  Edges of a node: R_k(e) in the order the
+// read enumeration lists it (operands in equation order; sums over windows
+// in row-major window order), as (child id, multiplicity).
+// ---------------------------------------------------------------------------
+struct Dag {
+  std::vector<uint64_t> nodes, node_edge;  // node_edge: first edge, relative to the location's first
+  std::vector<uint64_t> edges, mults;
+};
+
+std::vector<uint64_t> op_bases(const Graph& g) {
+  std::vector<uint64_t> base(g.ops.size());
+  uint64_t b = g.leaf_total;
+  for (size_t k = 0; k < g.ops.size(); ++k) {
+    base[k] = b;
+    b += (uint64_t)numel_of(g.tensors[g.ops[k].out].shape);
+  }
+  return base;
+}
+
+Dag dag_one(const Graph& g, const std::vector<uint64_t>& obase, int64_t loc) {
+  int64_t onumel = numel_of(g.tensors[g.output].shape);
+  if (loc < 0 || loc >= onumel) throw Error("location out of range");
+  std::vector<int> producer(g.tensors.size(), -1);
+  for (size_t k = 0; k < g.ops.size(); ++k) producer[g.ops[k].out] = (int)k;
+  std::vector<std::set<int64_t>> F(g.tensors.size());
+  F[g.output].insert(loc);
+  Dag d;
+  for (int k = (int)g.ops.size() - 1; k >= 0; --k) {
+    const Op& op = g.ops[k];
+    for (int64_t e : F[op.out]) {
+      d.nodes.push_back(obase[k] + (uint64_t)e);
+      d.node_edge.push_back(d.edges.size());
+      op_reads(g, op, e, [&](int t, int64_t idx, uint64_t m) {
+        const Tensor& T = g.tensors[t];
+        d.edges.push_back(producer[t] < 0 ? T.base + (uint64_t)idx : obase[producer[t]] + (uint64_t)idx);
+        d.mults.push_back(m);
+        if (producer[t] >= 0) F[t].insert(idx);
+      });
+    }
+  }
+  return d;
+}
+
+struct DagResult {
+  std::vector<int64_t> node_offsets, edge_offsets;
+  std::vector<uint64_t> nodes, node_edge, edges, mults;
+};
+
 template <class F>
 void parallel_blocks(int64_t n, int nthreads, F f) {
   if (nthreads <= 1 || n < 2) {
@@ -1004,6 +1063,28 @@ uint8_t compare_rows(const Row& a, const Row& b) {
   for (size_t i = 0; i < a.size(); ++i) if (a[i].first != b[i].first) return 1;
   for (size_t i = 0; i < a.size(); ++i) if (a[i].second != b[i].second) return 2;
   return 0;
+}
+
+DagResult dag_all(const Graph& g, const int64_t* locs, int64_t n, int nthreads) {
+  const std::vector<uint64_t> obase = op_bases(g);
+  std::vector<Dag> dags(n);
+  parallel_blocks(n, nthreads, [&](int64_t lo, int64_t hi, int) {
+    for (int64_t i = lo; i < hi; ++i) dags[i] = dag_one(g, obase, locs[i]);
+  });
+  DagResult r;
+  r.node_offsets.assign(n + 1, 0);
+  r.edge_offsets.assign(n + 1, 0);
+  for (int64_t i = 0; i < n; ++i) {
+    r.node_offsets[i + 1] = r.node_offsets[i] + (int64_t)dags[i].nodes.size();
+    r.edge_offsets[i + 1] = r.edge_offsets[i] + (int64_t)dags[i].edges.size();
+  }
+  for (auto& d : dags) {
+    r.nodes.insert(r.nodes.end(), d.nodes.begin(), d.nodes.end());
+    r.node_edge.insert(r.node_edge.end(), d.node_edge.begin(), d.node_edge.end());
+    r.edges.insert(r.edges.end(), d.edges.begin(), d.edges.end());
+    r.mults.insert(r.mults.end(), d.mults.begin(), d.mults.end());
+  }
+  return r;
 }
 
 thread_local std::string g_err;
@@ -1088,6 +1169,50 @@ void dgo_result_copy_wide(const dgo_result* r, int64_t* offsets, uint64_t* ids, 
 }
 
 void dgo_result_free(dgo_result* r) { delete r; }
+
+struct dgo_dag { DagResult r; };
+
+// Global id of element 0 of tensor t (leaf base, or the op output's base).
+uint64_t dgo_tensor_gid(const dgo_graph* g, int t) {
+  const Graph& G = g->g;
+  if (G.tensors[t].leaf_index >= 0) return G.tensors[t].base;
+  std::vector<uint64_t> obase = op_bases(G);
+  for (size_t k = 0; k < G.ops.size(); ++k) if (G.ops[k].out == t) return obase[k];
+  return 0;
+}
+
+dgo_dag* dgo_dag_build(const dgo_graph* g, const int64_t* locs, int64_t n, int nthreads) {
+  try {
+    auto* r = new dgo_dag;
+    r->r = dag_all(g->g, locs, n, nthreads);
+    return r;
+  } catch (const std::exception& e) {
+    g_err = e.what();
+    return nullptr;
+  }
+}
+
+void dgo_dag_totals(const dgo_dag* d, int64_t* nodes, int64_t* edges) {
+  *nodes = d->r.node_offsets.back();
+  *edges = d->r.edge_offsets.back();
+}
+
+void dgo_dag_copy(const dgo_dag* d, int64_t* node_offsets, int64_t* edge_offsets, uint64_t* nodes,
+                  uint64_t* node_edge, uint64_t* edges, uint64_t* mults) {
+  const DagResult& r = d->r;
+  memcpy(node_offsets, r.node_offsets.data(), r.node_offsets.size() * sizeof(int64_t));
+  memcpy(edge_offsets, r.edge_offsets.data(), r.edge_offsets.size() * sizeof(int64_t));
+  if (!r.nodes.empty()) {
+    memcpy(nodes, r.nodes.data(), r.nodes.size() * sizeof(uint64_t));
+    memcpy(node_edge, r.node_edge.data(), r.node_edge.size() * sizeof(uint64_t));
+  }
+  if (!r.edges.empty()) {
+    memcpy(edges, r.edges.data(), r.edges.size() * sizeof(uint64_t));
+    memcpy(mults, r.mults.data(), r.mults.size() * sizeof(uint64_t));
+  }
+}
+
+void dgo_dag_free(dgo_dag* d) { delete d; }
 
 int dgo_compare(const dgo_graph* a, const dgo_graph* b, const int64_t* locs, int64_t n, int nthreads,
                 uint8_t* status) {

@@ -209,7 +209,7 @@ def _norm_sets(kind, attrs, x):
     return sum_s, aff
 
 
-def _run(text: str, leaves: dict, linear: bool):
+def _run(text: str, leaves: dict, linear: bool, every: bool = False):
     _, ops, output = parse(text)
     env = dict(leaves)
     for name, kind, operands, attrs in ops:
@@ -330,11 +330,16 @@ def _run(text: str, leaves: dict, linear: bool):
         else:
             raise NotImplementedError(kind)
         env[name] = y
-    return env[output]
+    return env if every else env[output]
 
 
 def evaluate(text: str, leaves: dict) -> torch.Tensor:
     return _run(text, leaves, linear=False)
+
+
+def evaluate_all(text: str, leaves: dict) -> dict:
+    """Every tensor of the program (leaves and op outputs) by name."""
+    return _run(text, leaves, linear=False, every=True)
 
 
 def linearised(text: str, leaves: dict) -> torch.Tensor:
