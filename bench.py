@@ -42,6 +42,9 @@ def parse_args():
                    help="time dg_enumerate_sizes + dg_enumerate_fill instead of the single-pass dg_enumerate")
     p.add_argument("--wide", action="store_true",
                    help="time dg_enumerate_wide (64-bit ids and counts) instead of dg_enumerate")
+    p.add_argument("--dag", action="store_true",
+                   help="time expression-DAG emission (dg_dag_sizes + dg_dag_fill) instead of the rows; c3 takes "
+                        "every 8th of its locations, c5 the reference graph")
     p.add_argument("--full-output", action="store_true",
                    help="every output location: c5 compares all 33,554,432 (dg_compare_range; the faulty variants "
                         "stop at their first mismatch); c1-c4 stream the whole output's rows through a bounded "
@@ -192,6 +195,70 @@ def stream_full_output(args, B, g, cfg, info, text):
     print(json.dumps(line), flush=True)
 
 
+def dag_bench(args, B, g, cfg, locs, text):
+    """Expression DAGs of res(y[l]) for every listed location: sizes pass,
+    scans and fill per step, buffers sized once beforehand."""
+    import torch
+    dev = torch.device("cuda", 0)
+    d_locs = torch.as_tensor(locs, dtype=torch.int64, device=dev)
+    n = len(locs)
+    ws = torch.empty(max(B.dg_workspace_size(g, n), 1), dtype=torch.uint8, device=dev)
+    noff = torch.empty(n + 1, dtype=torch.int64, device=dev)
+    eoff = torch.empty(n + 1, dtype=torch.int64, device=dev)
+    nn, ne = B.dg_dag_sizes(g, d_locs, noff, eoff, ws)
+    nodes = torch.empty(max(nn, 1), dtype=torch.int32, device=dev)
+    node_edge = torch.empty(max(nn, 1), dtype=torch.int32, device=dev)
+    edges = torch.empty(max(ne, 1), dtype=torch.int32, device=dev)
+    mults = torch.empty(max(ne, 1), dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+
+    def step(i=None):
+        B.dg_dag_sizes(g, d_locs, noff, eoff, ws)
+        if i is not None:
+            ev[i][0].record(stream)
+        B.dg_dag_fill(g, d_locs, noff, eoff, nodes, node_edge, edges, mults, ws)
+        if i is not None:
+            ev[i][1].record(stream)
+
+    for _ in range(max(1, args.warmup)):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(i)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    fill_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    # Algorithmic bytes of the fill: 8 (location) + 16 (two offsets) per
+    # location, 8 per node (id + first edge), 8 per edge (child + multiplicity).
+    alg = 24 * n + 8 * nn + 8 * ne
+    achieved = alg / (fill_ms * 1e-3) / 1e9
+    line = {
+        "metric": "expression-DAG edges/sec emitted (sizes + fill; nodes and locations/sec in config)",
+        "value": ne / (elapsed / args.steps), "unit": "edges/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": elapsed * 1000 / args.steps, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "u32",
+        "data": "synthetic (shapes only; footprints are data independent)",
+        "config": {"workload": f"{args.workload}: " + cfg["desc"] + " (expression DAGs)", "locations": n,
+                   "nodes_per_step": nn, "edges_per_step": ne, "locations_per_s": n / (elapsed / args.steps),
+                   "dag_lds_bytes": None},
+        "roofline": {"bound": "hbm", "kernel": "k_dag_fill", "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None, "kernel_ms": fill_ms,
+                     "algorithmic_bytes": alg},
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        m = max(1, min(n, 64))
+        t1 = time.perf_counter()
+        oracle.Graph(text).dag(locs[:m], threads=os.cpu_count() or 1)
+        dt = time.perf_counter() - t1
+        line["cpu_baseline"] = {"value": m / dt, "unit": "locations/s", "cores": os.cpu_count() or 1,
+                                "kind": "oracle", "sample": f"first {m} of {n} locations"}
+    line["git"] = git_sha()
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse_args()
     if args.gpus != 1:
@@ -200,6 +267,9 @@ def main():
               "rate is N times the one-GPU rate measured here.", file=sys.stderr)
         sys.exit(2)
 
+    if args.dag and (args.wide or args.two_pass or args.full_output):
+        print("--dag takes no other mode", file=sys.stderr)
+        sys.exit(2)
     if args.wide and (args.two_pass or args.full_output or args.workload == "c5"):
         print("--wide times the single-pass enumeration of c1-c4 only", file=sys.stderr)
         sys.exit(2)
@@ -222,6 +292,10 @@ def main():
     n = len(locs)
     g = B.dg_graph_parse(text)
     info = B.dg_graph_info(g)
+
+    if args.dag:
+        dag_bench(args, B, g, cfg, locs if args.workload != "c3" else locs[::8], text)
+        return
 
     if args.workload == "c5":
         variants = [B.dg_graph_parse(W.c5_variant_text())] + [B.dg_graph_parse(W.c5_variant_text(fault=f))

@@ -174,6 +174,7 @@ typedef struct {
   int32_t lds_wide_bytes;     /* the same with 64-bit ids and counts */
   int32_t block_threads;      /* threads working on one location */
   int32_t max_leaf_terms;     /* separable terms of the busiest leaf */
+  int32_t n_tensors;          /* leaves and op outputs (dg_graph_tensor) */
   int32_t specialized;        /* kernels specialised for this graph on the
                                  current device: 1 loaded, 0 off or failed
                                  (the precompiled kernels run the plan),
@@ -192,6 +193,23 @@ typedef struct {
 
 /* Leaf i in declaration order, 0 <= i < n_leaves. */
 dg_status dg_graph_leaf(const dg_graph* g, int32_t i, dg_leaf_info_t* out);
+
+typedef struct {
+  char name[DG_NAME_LEN];
+  int32_t rank;
+  int64_t shape[DG_MAX_RANK];
+  int64_t numel;
+  uint64_t gid;       /* element id of element 0 in expression DAGs: a
+                         leaf's base, or for an op output the total leaf
+                         elements plus the elements of all earlier ops'
+                         outputs (SSA order) */
+  int32_t leaf;       /* leaf index, or -1 for an op output */
+  int32_t producer;   /* index of the op writing it (SSA order), or -1 */
+  char kind[32];      /* that op's kind ("" for a leaf) */
+} dg_tensor_info_t;
+
+/* Tensor i in declaration order (leaves and op outputs), 0 <= i < n_tensors. */
+dg_status dg_graph_tensor(const dg_graph* g, int32_t i, dg_tensor_info_t* out);
 
 /* ------------------------------------------------------------------------
  * Enumeration.
@@ -253,6 +271,50 @@ dg_status dg_enumerate(const dg_graph* g, const int64_t* d_locs, int64_t n, int6
 dg_status dg_enumerate_wide(const dg_graph* g, const int64_t* d_locs, int64_t n, int64_t* d_offsets,
                             uint64_t* d_ids, uint64_t* d_counts, int64_t capacity, void* d_ws, int64_t* h_total,
                             void* stream);
+
+/* ------------------------------------------------------------------------
+ * Expression DAGs of res(y[l]) (Sec. 3.4, "Back-projection": substituting
+ * the per-element equations backwards from y[l]).  Every element of the
+ * cone of y[l] is one node, shared wherever it occurs.  A leaf element is a
+ * variable; every other node is its op (dg_tensor_info_t.kind) applied to
+ * the element references of its per-element equation, in the equation's
+ * order: read groups in order, window points in row-major order, a group's
+ * operands in order at each point (a point with any operand index outside
+ * its tensor, or not exactly divisible, reads nothing).  So a conv node's
+ * references are x, W pairs over (input channel, taps...) followed by its
+ * bias; a matmul node's are A, B pairs over k; a norm node's are its
+ * statistics set (multiplicity |S| + 2 each), its own element, then gamma
+ * and beta.  Elements are named by global ids (dg_tensor_info_t.gid plus
+ * the row-major flat index), which must fit 32 bits (DG_E_OVERFLOW).
+ *
+ * Per location i, CSR over CSR:
+ *   nodes      [d_node_offsets[i], d_node_offsets[i+1]): the non-leaf cone
+ *              elements, ops in reverse SSA order (y[l] first), elements
+ *              ascending within an op;
+ *   node_edge  per node, its first edge relative to d_edge_offsets[i]; its
+ *              edges end where the next node's begin (the last node's at
+ *              d_edge_offsets[i+1]);
+ *   edges, mults [d_edge_offsets[i], d_edge_offsets[i+1]): child id and
+ *              multiplicity of each reference.
+ * Leaf elements appear only as children (ids below leaf_total).  The
+ * per-location frontiers live in LDS; a graph whose static frontier bound
+ * does not fit returns DG_E_CAPACITY.
+ * ------------------------------------------------------------------------ */
+
+/* dg_dag_sizes: node and edge counts of every location as running totals
+ * (d_node_offsets[n+1], d_edge_offsets[n+1], device int64, written; [0] = 0)
+ * and the totals on the host.  Synchronous.  DG_E_RANGE for a location
+ * outside the output; the workspace is dg_workspace_size(g, n). */
+dg_status dg_dag_sizes(const dg_graph* g, const int64_t* d_locs, int64_t n, int64_t* d_node_offsets,
+                       int64_t* d_edge_offsets, void* d_ws, int64_t* h_nodes, int64_t* h_edges, void* stream);
+
+/* dg_dag_fill: writes the DAGs with offsets from dg_dag_sizes on the same
+ * graph and locations: d_nodes and d_node_edge hold d_node_offsets[n]
+ * uint32 entries, d_edges and d_mults d_edge_offsets[n].  Synchronous;
+ * DG_E_INVALID_ARG if the offsets do not match. */
+dg_status dg_dag_fill(const dg_graph* g, const int64_t* d_locs, int64_t n, const int64_t* d_node_offsets,
+                      const int64_t* d_edge_offsets, uint32_t* d_nodes, uint32_t* d_node_edge, uint32_t* d_edges,
+                      uint32_t* d_mults, void* d_ws, void* stream);
 
 /* dg_enumerate_range: dg_enumerate over the contiguous flat locations
  * first, first + 1, ..., first + n - 1 (row i belongs to location

@@ -51,6 +51,7 @@ class GraphInfo(ctypes.Structure):
         ("lds_wide_bytes", ctypes.c_int32),
         ("block_threads", ctypes.c_int32),
         ("max_leaf_terms", ctypes.c_int32),
+        ("n_tensors", ctypes.c_int32),
         ("specialized", ctypes.c_int32),
     ]
 
@@ -62,6 +63,19 @@ class LeafInfo(ctypes.Structure):
         ("shape", ctypes.c_int64 * MAX_RANK),
         ("base", ctypes.c_uint64),
         ("numel", ctypes.c_int64),
+    ]
+
+
+class TensorInfo(ctypes.Structure):
+    _fields_ = [
+        ("name", ctypes.c_char * 64),
+        ("rank", ctypes.c_int32),
+        ("shape", ctypes.c_int64 * MAX_RANK),
+        ("numel", ctypes.c_int64),
+        ("gid", ctypes.c_uint64),
+        ("leaf", ctypes.c_int32),
+        ("producer", ctypes.c_int32),
+        ("kind", ctypes.c_char * 32),
     ]
 
 
@@ -100,6 +114,9 @@ def _load():
         "dg_compare_range": ([P, P, i64, i64, i64, P, P, ctypes.POINTER(i64), P, P], i32),
         "dg_enumerate_stream": ([P, i64, i64, P, sz, i64, CHUNK_FN, P, P, P], i32),
         "dg_enumerate_wide": ([P, P, i64, P, P, P, i64, P, ctypes.POINTER(i64), P], i32),
+        "dg_graph_tensor": ([P, i32, P], i32),
+        "dg_dag_sizes": ([P, P, i64, P, P, P, ctypes.POINTER(i64), ctypes.POINTER(i64), P], i32),
+        "dg_dag_fill": ([P, P, i64, P, P, P, P, P, P, P, P], i32),
         "dg_last_error": ([], ctypes.c_char_p),
     }
     for name, (args, res) in sig.items():
@@ -141,7 +158,8 @@ class Graph:
 
     def __del__(self):
         h = getattr(self, "_h", None)
-        if h:
+        # (At interpreter exit the module's globals may already be gone.)
+        if h and _lib is not None:
             _lib.dg_graph_destroy(h)
             self._h = None
 
@@ -190,6 +208,7 @@ def dg_graph_info(g: Graph) -> dict:
         "lds_wide_bytes": info.lds_wide_bytes,
         "block_threads": info.block_threads,
         "max_leaf_terms": info.max_leaf_terms,
+        "n_tensors": info.n_tensors,
         "specialized": info.specialized,
     }
 
@@ -198,6 +217,13 @@ def dg_graph_leaf(g: Graph, i: int) -> dict:
     li = LeafInfo()
     _check(_lib.dg_graph_leaf(g.handle, i, ctypes.byref(li)))
     return {"name": li.name.decode(), "shape": tuple(li.shape[: li.rank]), "base": li.base, "numel": li.numel}
+
+
+def dg_graph_tensor(g: Graph, i: int) -> dict:
+    ti = TensorInfo()
+    _check(_lib.dg_graph_tensor(g.handle, i, ctypes.byref(ti)))
+    return {"name": ti.name.decode(), "shape": tuple(ti.shape[: ti.rank]), "numel": ti.numel, "gid": ti.gid,
+            "leaf": ti.leaf, "producer": ti.producer, "kind": ti.kind.decode()}
 
 
 def dg_workspace_size(g: Graph, n_locs: int) -> int:
@@ -390,6 +416,60 @@ def enumerate_locations(g: Graph, locs, stream=None):
     cnt = torch.empty(max(1, total), dtype=torch.int32, device=d_locs.device)
     dg_enumerate_fill(g, d_locs, offsets, ids, cnt, ws, stream)
     return offsets, ids[:total], cnt[:total]
+
+
+def _dev_u32(t: torch.Tensor, what: str) -> None:
+    if not t.is_cuda or t.dtype not in (torch.int32, torch.uint32) or not t.is_contiguous():
+        raise ValueError(f"{what} must be a contiguous 32-bit device tensor")
+
+
+def dg_dag_sizes(g: Graph, d_locs: torch.Tensor, d_node_offsets: torch.Tensor, d_edge_offsets: torch.Tensor,
+                 d_ws: torch.Tensor, stream=None):
+    """Expression DAG sizes: fills both offset arrays (n + 1 entries);
+    returns (total nodes, total edges)."""
+    n = d_locs.numel()
+    _dev_i64(d_locs, "locations")
+    for t, what in ((d_node_offsets, "node offsets"), (d_edge_offsets, "edge offsets")):
+        _dev_i64(t, what)
+        if t.numel() < n + 1:
+            raise ValueError(f"{what} needs n + 1 entries")
+    nn, ne = ctypes.c_int64(), ctypes.c_int64()
+    _check(_lib.dg_dag_sizes(g.handle, _ptr(d_locs), n, _ptr(d_node_offsets), _ptr(d_edge_offsets), _ptr(d_ws),
+                             ctypes.byref(nn), ctypes.byref(ne), _stream(stream)))
+    return nn.value, ne.value
+
+
+def dg_dag_fill(g: Graph, d_locs: torch.Tensor, d_node_offsets: torch.Tensor, d_edge_offsets: torch.Tensor,
+                d_nodes: torch.Tensor, d_node_edge: torch.Tensor, d_edges: torch.Tensor, d_mults: torch.Tensor,
+                d_ws: torch.Tensor, stream=None) -> None:
+    n = d_locs.numel()
+    _dev_i64(d_locs, "locations")
+    _dev_i64(d_node_offsets, "node offsets")
+    _dev_i64(d_edge_offsets, "edge offsets")
+    for t, what in ((d_nodes, "nodes"), (d_node_edge, "node edges"), (d_edges, "edges"), (d_mults, "mults")):
+        _dev_u32(t, what)
+    _check(_lib.dg_dag_fill(g.handle, _ptr(d_locs), n, _ptr(d_node_offsets), _ptr(d_edge_offsets), _ptr(d_nodes),
+                            _ptr(d_node_edge), _ptr(d_edges), _ptr(d_mults), _ptr(d_ws), _stream(stream)))
+
+
+def dag_locations(g: Graph, locs, stream=None) -> dict:
+    """Expression DAGs of res(y[l]) for the given locations, on the device:
+    node_offsets, edge_offsets (int64[n+1]); nodes, node_edge, edges, mults
+    (uint32 values in int32 storage)."""
+    d_locs = locs if isinstance(locs, torch.Tensor) else torch.as_tensor(locs, dtype=torch.int64)
+    d_locs = d_locs.to(device="cuda", dtype=torch.int64).contiguous()
+    n = d_locs.numel()
+    ws = workspace(g, n, d_locs.device)
+    noff = torch.empty(n + 1, dtype=torch.int64, device=d_locs.device)
+    eoff = torch.empty(n + 1, dtype=torch.int64, device=d_locs.device)
+    nn, ne = dg_dag_sizes(g, d_locs, noff, eoff, ws, stream)
+    out = {"node_offsets": noff, "edge_offsets": eoff}
+    for k, m in (("nodes", nn), ("node_edge", nn), ("edges", ne), ("mults", ne)):
+        out[k] = torch.empty(max(1, m), dtype=torch.int32, device=d_locs.device)
+    dg_dag_fill(g, d_locs, noff, eoff, out["nodes"], out["node_edge"], out["edges"], out["mults"], ws, stream)
+    for k, m in (("nodes", nn), ("node_edge", nn), ("edges", ne), ("mults", ne)):
+        out[k] = out[k][:m]
+    return out
 
 
 def compare_locations(a: Graph, b: Graph, locs, stream=None):

@@ -40,6 +40,14 @@ struct dg_graph {
   // Specialised comparison kernels with another graph: (device, other's
   // serial, block) -> kernels.
   std::map<std::tuple<int, uint64_t, int>, DevKernels> pair_jit;
+  // Expression-DAG program, compiled on first use (dag_status: DG_OK or
+  // the failure, with its message).
+  bool dag_tried = false;
+  dg_status dag_status = DG_OK;
+  std::string dag_error;
+  dg::DagProgram dag;
+  int dag_block = 256;
+  std::map<int, uint8_t*> dev_dag;  // DAG program per device
 };
 
 namespace {
@@ -106,6 +114,45 @@ dg_status device_blob(const dg_graph* cg, const uint8_t** out) {
     return hip_error(e, "hipMemcpy(plan)");
   }
   g->dev_blob[dev] = static_cast<uint8_t*>(p);
+  *out = static_cast<uint8_t*>(p);
+  return DG_OK;
+}
+
+// The graph's expression-DAG program (compiled on first use) and its device
+// copy on the current device.
+dg_status dag_program(const dg_graph* cg, const uint8_t** out) {
+  dg_graph* g = const_cast<dg_graph*>(cg);
+  std::lock_guard<std::mutex> lock(g->mu);
+  if (!g->dag_tried) {
+    g->dag_tried = true;
+    try {
+      // Small DAGs (a few thousand references per location) run on one wave.
+      dg::DagProgram probe = dg::compile_dag(g->ir, 64);
+      g->dag_block = probe.max_edges >= 4096 ? 256 : 64;
+      g->dag = g->dag_block == 64 ? std::move(probe) : dg::compile_dag(g->ir, g->dag_block);
+    } catch (const dg::Failure& f) {
+      g->dag_status = (dg_status)f.code;
+      g->dag_error = f.what();
+    }
+  }
+  if (g->dag_status != DG_OK) return set_error(g->dag_status, g->dag_error);
+  if (!out) return DG_OK;
+  int dev = 0;
+  DG_HIP(hipGetDevice(&dev), "hipGetDevice");
+  auto it = g->dev_dag.find(dev);
+  if (it != g->dev_dag.end()) {
+    *out = it->second;
+    return DG_OK;
+  }
+  void* p = nullptr;
+  const size_t bytes = g->dag.blob.size();
+  DG_HIP(hipMalloc(&p, bytes), "hipMalloc(DAG program)");
+  hipError_t e = hipMemcpy(p, g->dag.blob.data(), bytes, hipMemcpyHostToDevice);
+  if (e != hipSuccess) {
+    (void)hipFree(p);
+    return hip_error(e, "hipMemcpy(DAG program)");
+  }
+  g->dev_dag[dev] = static_cast<uint8_t*>(p);
   *out = static_cast<uint8_t*>(p);
   return DG_OK;
 }
@@ -284,6 +331,9 @@ void dg_graph_destroy(dg_graph* g) {
   for (auto& kv : g->dev_blob) {
     if (hipSetDevice(kv.first) == hipSuccess) (void)hipFree(kv.second);
   }
+  for (auto& kv : g->dev_dag) {
+    if (hipSetDevice(kv.first) == hipSuccess) (void)hipFree(kv.second);
+  }
   if (have) (void)hipSetDevice(cur);
   delete g;
 }
@@ -304,6 +354,7 @@ dg_status dg_graph_info(const dg_graph* g, dg_graph_info_t* out) {
   out->lds_wide_bytes = (int32_t)g->lds_wide;
   out->block_threads = g->block;
   out->max_leaf_terms = g->plan.max_leaf_terms;
+  out->n_tensors = (int32_t)g->ir.tensors.size();
   out->specialized = -1;
   if (!dg::jit_enabled()) {
     out->specialized = 0;
@@ -329,6 +380,30 @@ dg_status dg_graph_leaf(const dg_graph* g, int32_t i, dg_leaf_info_t* out) {
   for (size_t d = 0; d < t.shape.size(); ++d) out->shape[d] = t.shape[d];
   out->base = t.base;
   out->numel = dg::numel(t.shape);
+  return DG_OK;
+}
+
+dg_status dg_graph_tensor(const dg_graph* g, int32_t i, dg_tensor_info_t* out) {
+  if (!g || !out) return set_error(DG_E_INVALID_ARG, "null argument");
+  if (i < 0 || i >= (int32_t)g->ir.tensors.size()) return set_error(DG_E_INVALID_ARG, "tensor index out of range");
+  std::memset(out, 0, sizeof(*out));
+  const dg::Tensor& t = g->ir.tensors[i];
+  std::snprintf(out->name, DG_NAME_LEN, "%s", t.name.c_str());
+  out->rank = (int32_t)t.shape.size();
+  for (size_t d = 0; d < t.shape.size(); ++d) out->shape[d] = t.shape[d];
+  out->numel = dg::numel(t.shape);
+  out->leaf = t.leaf;
+  out->producer = t.producer;
+  if (t.producer >= 0) std::snprintf(out->kind, sizeof(out->kind), "%s", g->ir.ops[t.producer].kind.c_str());
+  // Global id of element 0: leaves keep theirs, op outputs follow all leaves
+  // in SSA order.
+  uint64_t gid = g->ir.leaf_total;
+  if (t.leaf >= 0) {
+    gid = t.base;
+  } else {
+    for (int k = 0; k < t.producer; ++k) gid += (uint64_t)dg::numel(g->ir.tensors[g->ir.ops[k].out].shape);
+  }
+  out->gid = gid;
   return DG_OK;
 }
 
@@ -643,6 +718,70 @@ dg_status compare_impl(const dg_graph* a, const dg_graph* b, dgc::LocSrc src, in
 }
 
 }  // namespace
+
+dg_status dg_dag_sizes(const dg_graph* g, const int64_t* d_locs, int64_t n, int64_t* d_node_offsets,
+                       int64_t* d_edge_offsets, void* d_ws, int64_t* h_nodes, int64_t* h_edges, void* stream) {
+  if (!g || !d_node_offsets || !d_edge_offsets || !h_nodes || !h_edges || n < 0 || (n > 0 && !d_locs))
+    return set_error(DG_E_INVALID_ARG, "bad argument");
+  if (!d_ws) return set_error(DG_E_WORKSPACE, "workspace is required");
+  return guarded([&]() -> dg_status {
+    const uint8_t* dblob = nullptr;
+    dg_status st = dag_program(g, &dblob);
+    if (st != DG_OK) return st;
+    if (g->dag.lds_bytes > (uint32_t)max_lds_per_block())
+      return set_error(DG_E_CAPACITY, "one location's DAG frontiers need " + std::to_string(g->dag.lds_bytes) +
+                                          " bytes of LDS");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    WsLayout w = ws_layout(n);
+    uint8_t* ws = static_cast<uint8_t*>(d_ws);
+    uint32_t* err = reinterpret_cast<uint32_t*>(ws + w.err);
+    DG_HIP(dgk::launch_zero(err, s), "zero");
+    DG_HIP(dgk::launch_dag_sizes(dblob, dgc::LocSrc{d_locs, 0}, n, d_node_offsets, d_edge_offsets, err, g->dag_block,
+                                 g->dag.lds_bytes, s),
+           "DAG sizes kernel");
+    int64_t* sums = reinterpret_cast<int64_t*>(ws + w.sums);
+    DG_HIP(dgk::launch_scan(d_node_offsets, n, sums, s), "scan");
+    DG_HIP(dgk::launch_scan(d_edge_offsets, n, sums, s), "scan");
+    int64_t tn = 0, te = 0;
+    uint32_t bits = 0;
+    DG_HIP(hipMemcpyAsync(&tn, d_node_offsets + n, sizeof(int64_t), hipMemcpyDeviceToHost, s), "copy total");
+    DG_HIP(hipMemcpyAsync(&te, d_edge_offsets + n, sizeof(int64_t), hipMemcpyDeviceToHost, s), "copy total");
+    DG_HIP(hipMemcpyAsync(&bits, err, sizeof(uint32_t), hipMemcpyDeviceToHost, s), "copy flags");
+    DG_HIP(hipStreamSynchronize(s), "DAG sizes sync");
+    st = device_errors(bits);
+    if (st != DG_OK) return st;
+    *h_nodes = tn;
+    *h_edges = te;
+    return DG_OK;
+  });
+}
+
+dg_status dg_dag_fill(const dg_graph* g, const int64_t* d_locs, int64_t n, const int64_t* d_node_offsets,
+                      const int64_t* d_edge_offsets, uint32_t* d_nodes, uint32_t* d_node_edge, uint32_t* d_edges,
+                      uint32_t* d_mults, void* d_ws, void* stream) {
+  if (!g || n < 0 || (n > 0 && (!d_locs || !d_node_offsets || !d_edge_offsets || !d_nodes || !d_node_edge ||
+                                !d_edges || !d_mults)))
+    return set_error(DG_E_INVALID_ARG, "bad argument");
+  if (!d_ws) return set_error(DG_E_WORKSPACE, "workspace is required");
+  return guarded([&]() -> dg_status {
+    const uint8_t* dblob = nullptr;
+    dg_status st = dag_program(g, &dblob);
+    if (st != DG_OK) return st;
+    if (g->dag.lds_bytes > (uint32_t)max_lds_per_block())
+      return set_error(DG_E_CAPACITY, "one location's DAG frontiers need " + std::to_string(g->dag.lds_bytes) +
+                                          " bytes of LDS");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    uint32_t* err = reinterpret_cast<uint32_t*>(static_cast<uint8_t*>(d_ws) + ws_layout(n).err);
+    DG_HIP(dgk::launch_zero(err, s), "zero");
+    DG_HIP(dgk::launch_dag_fill(dblob, dgc::LocSrc{d_locs, 0}, n, d_node_offsets, d_edge_offsets, d_nodes,
+                                d_node_edge, d_edges, d_mults, err, g->dag_block, g->dag.lds_bytes, s),
+           "DAG fill kernel");
+    uint32_t bits = 0;
+    DG_HIP(hipMemcpyAsync(&bits, err, sizeof(uint32_t), hipMemcpyDeviceToHost, s), "copy flags");
+    DG_HIP(hipStreamSynchronize(s), "DAG fill sync");
+    return device_errors(bits);
+  });
+}
 
 dg_status dg_compare(const dg_graph* a, const dg_graph* b, const int64_t* d_locs, int64_t n, uint8_t* d_status,
                      int64_t* d_mismatch, int64_t* h_n_mismatch, void* d_ws, void* stream) {

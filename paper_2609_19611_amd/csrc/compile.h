@@ -50,6 +50,21 @@ uint32_t plan_lds_bytes(const Plan& p, int nthreads, uint32_t word_bytes = 4);
 // location by location (same leaves in the same order).
 void pair_plan(const Plan& a, const Plan& b, int nthreads, dgc::PairPlan* out);
 
+// Expression-DAG program of a graph (DgdHeader and its arrays) for blocks of
+// `nthreads` threads.  Throws Failure(DG_E_OVERFLOW) when the element ids of
+// all tensors need more than 32 bits and Failure(DG_E_CAPACITY) when a
+// frontier bound is unreasonably large.
+struct DagProgram {
+  std::vector<uint8_t> blob;
+  uint32_t lds_bytes = 0;      // LDS area of one location
+  uint32_t vars_off = 0;
+  int max_vars = 0;
+  int64_t max_nodes = 0;       // static bounds for one location
+  int64_t max_edges = 0;
+  std::vector<uint64_t> gid;   // global id of element 0 per tensor
+};
+DagProgram compile_dag(const GraphIR& g, int nthreads);
+
 // Text listing of a plan's instructions and leaf terms.
 std::string plan_listing(const Plan& p);
 

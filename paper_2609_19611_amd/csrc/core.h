@@ -1225,4 +1225,214 @@ DGC uint32_t location_compare(C& c, const uint8_t* blob_a, const uint8_t* blob_b
   return status;
 }
 
+// ---------------------------------------------------------------------------
+// Expression DAG of res(y[l]) for one location (program.h, DgdHeader).
+//
+// Frontiers of the non-leaf tensors live in the LDS area: a consumer node
+// appends every non-leaf element it references to the operand's candidate
+// list; when the ops are walked back to that tensor's producer (reverse SSA
+// order, so every consumer has been walked), the list is sorted and made
+// unique, giving the tensor's nodes in ascending order.  A node's edges are
+// its (group, window point, operand) references in order; a point whose
+// operand indices are not all valid is skipped.  Work is spread over the
+// block as (node, reference) pairs, and a block-wide prefix count of the
+// valid ones gives each edge its position.
+// ---------------------------------------------------------------------------
+enum : int { DAG_COUNT = 0, DAG_FILL = 1 };
+
+struct DagOut {
+  uint32_t* nodes;      // node ids (global element ids)
+  uint32_t* node_edge;  // first edge of each node, relative to the location's first edge
+  uint32_t* edges;      // child ids
+  uint32_t* mults;      // multiplicities
+  uint64_t room_nodes, room_edges;
+};
+
+// Sorts the first n entries of f (capacity cap, a power of two) and keeps
+// one of each value; returns the number kept.  All threads call it.
+template <class C>
+DGC uint32_t sort_unique(C& c, uint32_t* f, uint32_t n, uint32_t cap) {
+  const int tid = c.tid(), nt = c.nthreads();
+  uint32_t p2 = 1;
+  while (p2 < n) p2 <<= 1;
+  if (p2 > cap) p2 = cap;
+  for (uint32_t i = n + (uint32_t)tid; i < p2; i += (uint32_t)nt) f[i] = 0xFFFFFFFFu;
+  c.sync();
+  for (uint32_t k = 2; k <= p2; k <<= 1) {
+    for (uint32_t j = k >> 1; j > 0; j >>= 1) {
+      for (uint32_t i = (uint32_t)tid; i < p2; i += (uint32_t)nt) {
+        const uint32_t l = i ^ j;
+        if (l > i) {
+          const uint32_t a = f[i], b = f[l];
+          const bool up = (i & k) == 0;
+          if ((a > b) == up) {
+            f[i] = b;
+            f[l] = a;
+          }
+        }
+      }
+      c.sync();
+    }
+  }
+  uint32_t kept = 0;
+  for (uint32_t b0 = 0; b0 < n; b0 += (uint32_t)nt) {
+    const uint32_t i = b0 + (uint32_t)tid;
+    uint32_t v = 0;
+    bool keep = false;
+    if (i < n) {
+      v = f[i];
+      keep = i == 0 || f[i - 1] != v;
+    }
+    uint32_t tot;
+    const uint32_t pre = c.prefix(keep, &tot);
+    if (keep) f[kept + pre] = v;
+    kept += tot;
+    c.sync();
+  }
+  return kept;
+}
+
+// Index function over the variable table vt (stride nt): the value, and
+// whether it is valid (divisible where exact, inside the dimension).
+DGC bool dag_index(const DgpIFn& f, const int32_t* vt, int nt, int32_t* out) { return ifn_eval(f, vt, nt, out); }
+
+template <class C, int MODE>
+DGC void location_dag(C& c, const uint8_t* dblob, int64_t loc, uint8_t* area, const DagOut& o, uint64_t* n_nodes,
+                      uint64_t* n_edges, uint32_t* err) {
+  const DgdHeader* h = (const DgdHeader*)dblob;
+  const DgdTensor* T = (const DgdTensor*)(dblob + h->tensor_off);
+  const DgdOp* O = (const DgdOp*)(dblob + h->op_off);
+  const DgdGroup* Gs = (const DgdGroup*)(dblob + h->group_off);
+  const DgdOperand* Ps = (const DgdOperand*)(dblob + h->operand_off);
+  const int tid = c.tid(), nt = c.nthreads();
+  uint32_t* cnt = (uint32_t*)(area + h->count_off);
+  int32_t* vt = (int32_t*)(area + h->vars_off) + tid;  // this thread's variables, stride nt
+  *n_nodes = 0;
+  *n_edges = 0;
+  if (loc < 0 || loc >= h->out_numel) {
+    *err |= DGP_ERR_RANGE;
+    return;
+  }
+  for (int t = tid; t < h->ntensor; t += nt) cnt[t] = 0;
+  c.sync();
+  const DgdTensor& Ty = T[h->output];
+  if (!Ty.leaf) {
+    if (tid == 0) {
+      ((uint32_t*)(area + Ty.lds))[0] = (uint32_t)loc;
+      cnt[h->output] = 1;
+    }
+  }
+  c.sync();
+  uint64_t nb = 0, eb = 0;
+  for (int k = h->nop - 1; k >= 0; --k) {
+    const DgdOp& op = O[k];
+    const DgdTensor& X = T[op.out];
+    const uint32_t got = cnt[op.out];
+    if (got == 0) continue;
+    c.sync();  // every thread has read the counter
+    if (got > (uint32_t)X.cap) {
+      *err |= DGP_ERR_CAPACITY;
+      return;
+    }
+    uint32_t* F = (uint32_t*)(area + X.lds);
+    const uint32_t n = sort_unique(c, F, got, (uint32_t)X.cap);
+    if (MODE == DAG_FILL) {
+      for (uint32_t i = (uint32_t)tid; i < n; i += (uint32_t)nt)
+        if (nb + i < o.room_nodes) c.store(&o.nodes[nb + i], X.gid + F[i]);
+    }
+    const int R = X.rank;
+    const uint64_t E = (uint64_t)op.refs;
+    if (E == 0) {
+      if (MODE == DAG_FILL)
+        for (uint32_t i = (uint32_t)tid; i < n; i += (uint32_t)nt)
+          if (nb + i < o.room_nodes) c.store(&o.node_edge[nb + i], (uint32_t)eb);
+      nb += n;
+      continue;
+    }
+    const uint64_t total = (uint64_t)n * E;
+    uint64_t run = 0;
+    for (uint64_t b0 = 0; b0 < total; b0 += (uint64_t)nt) {
+      const uint64_t pidx = b0 + (uint64_t)tid;
+      bool valid = false;
+      bool first = false;
+      uint32_t node = 0, child = 0, mult = 0;
+      int ctensor = -1;
+      int32_t cflat = 0;
+      if (pidx < total) {
+        node = (uint32_t)(pidx / E);
+        uint64_t r = pidx - (uint64_t)node * E;
+        first = r == 0;
+        // Group, window point and operand of reference r.
+        int gi = op.g0;
+        for (int q = 0; q < op.ng; ++q) {
+          const DgdGroup& G = Gs[op.g0 + q];
+          const uint64_t span = (uint64_t)G.points * (uint64_t)G.nop;
+          if (r < span) {
+            gi = op.g0 + q;
+            break;
+          }
+          r -= span;
+        }
+        const DgdGroup& G = Gs[gi];
+        const uint64_t point = r / (uint64_t)G.nop;
+        const int j = (int)(r - point * (uint64_t)G.nop);
+        // Output coordinates of the node, then the window point.
+        uint32_t e = F[node];
+        for (int d = R - 1; d >= 0; --d) {
+          const uint32_t s = (uint32_t)X.shape[d];
+          vt[d * nt] = (int32_t)(e % s);
+          e /= s;
+        }
+        uint64_t w = point;
+        for (int q = G.nwin - 1; q >= 0; --q) {
+          const uint64_t s = (uint64_t)(G.whi[q] - G.wlo[q]);
+          vt[(R + q) * nt] = G.wlo[q] + (int32_t)(w % s);
+          w /= s;
+        }
+        valid = true;
+        for (int a = 0; a < G.nop && valid; ++a) {
+          const DgdOperand& P = Ps[G.op0 + a];
+          const DgdTensor& Ta = T[P.tensor];
+          int64_t flat = 0;
+          for (int d = 0; d < Ta.rank; ++d) {
+            int32_t v;
+            if (!dag_index(P.idx[d], vt, nt, &v)) {
+              valid = false;
+              break;
+            }
+            flat = flat * Ta.shape[d] + v;
+          }
+          if (valid && a == j) {
+            ctensor = P.tensor;
+            cflat = (int32_t)flat;
+            child = Ta.gid + (uint32_t)flat;
+            mult = P.mult;
+          }
+        }
+      }
+      uint32_t tot;
+      const uint32_t pre = c.prefix(valid, &tot);
+      if (MODE == DAG_FILL) {
+        if (first && nb + node < o.room_nodes) c.store(&o.node_edge[nb + node], (uint32_t)(eb + run + pre));
+        if (valid && eb + run + pre < o.room_edges) {
+          c.store(&o.edges[eb + run + pre], child);
+          c.store(&o.mults[eb + run + pre], mult);
+        }
+      }
+      if (valid && !T[ctensor].leaf) {
+        const DgdTensor& Tc = T[ctensor];
+        const uint32_t slot = c.atomic_inc(&cnt[ctensor]);
+        if (slot < (uint32_t)Tc.cap) ((uint32_t*)(area + Tc.lds))[slot] = (uint32_t)cflat;
+        else *err |= DGP_ERR_CAPACITY;
+      }
+      run += tot;
+    }
+    c.sync();
+    nb += n;
+    eb += run;
+  }
+  *n_nodes = nb;
+  *n_edges = eb;
+}
+
 }  // namespace dgc

@@ -1,0 +1,192 @@
+// Host compiler of the expression-DAG program (program.h, DgdHeader): the
+// ops of a graph as read groups with device index functions, element ids of
+// every tensor, and static frontier capacities for one location.
+#include <algorithm>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/dirigo_rocm.h"
+#include "compile.h"
+
+namespace dg {
+
+namespace {
+
+[[noreturn]] void fail(int code, const std::string& m) { throw Failure(code, m); }
+
+int32_t i32(int64_t v, const char* what) {
+  if (v < INT32_MIN || v > INT32_MAX) fail(DG_E_UNSUPPORTED_OP, std::string(what) + " exceeds 32 bits");
+  return (int32_t)v;
+}
+
+DgpIFn device_fn(const IndexFn& f, int64_t size) {
+  DgpIFn d;
+  std::memset(&d, 0, sizeof(d));
+  if (f.terms.size() > DGP_MAX_FTERMS) fail(DG_E_UNSUPPORTED_OP, "index function with more than 4 terms");
+  d.nterm = (int32_t)f.terms.size();
+  for (size_t q = 0; q < f.terms.size(); ++q) {
+    d.var[q] = f.terms[q].var;
+    d.coef[q] = i32(f.terms[q].coef, "index coefficient");
+    d.vdiv[q] = i32(f.terms[q].vdiv, "index divisor");
+  }
+  d.c = i32(f.c, "index constant");
+  d.mode = f.mode;
+  d.s = i32(f.s, "index divisor");
+  d.size = i32(size, "tensor dimension");
+  return d;
+}
+
+uint64_t pow2_at_least(uint64_t v) {
+  uint64_t p = 1;
+  while (p < v) p <<= 1;
+  return p;
+}
+
+}  // namespace
+
+DagProgram compile_dag(const GraphIR& g, int nthreads) {
+  const int nt = (int)g.tensors.size(), nop = (int)g.ops.size();
+  // Element ids: leaves keep theirs, op outputs follow in SSA order.
+  std::vector<uint64_t> gid(nt, 0);
+  uint64_t next = g.leaf_total;
+  for (int t = 0; t < nt; ++t)
+    if (g.tensors[t].leaf >= 0) gid[t] = g.tensors[t].base;
+  for (const OpNode& op : g.ops) {
+    gid[op.out] = next;
+    next += (uint64_t)numel(g.tensors[op.out].shape);
+  }
+  if (next > 0xFFFFFFFFull) fail(DG_E_OVERFLOW, "DAG element ids need more than 32 bits");
+
+  // Static frontier bounds for one location, in reverse SSA order: a
+  // tensor's candidate list receives, from every node of a consumer, one
+  // entry per window point of every group operand that reads it.
+  std::vector<uint64_t> appends(nt, 0), nodes(nt, 0);
+  if (g.tensors[g.output].leaf < 0) appends[g.output] = 1;
+  DagProgram p;
+  int max_vars = 1;
+  for (int k = nop - 1; k >= 0; --k) {
+    const OpNode& op = g.ops[k];
+    const uint64_t n = std::min<uint64_t>(appends[op.out], (uint64_t)numel(g.tensors[op.out].shape));
+    nodes[op.out] = n;
+    p.max_nodes += (int64_t)n;
+    const int R = (int)g.tensors[op.out].shape.size();
+    for (const ReadGroup& G : op.groups) {
+      uint64_t pts = 1;
+      for (size_t q = 0; q < G.wlo.size(); ++q) pts *= (uint64_t)std::max<int64_t>(0, G.whi[q] - G.wlo[q]);
+      max_vars = std::max(max_vars, R + (int)G.wlo.size());
+      p.max_edges += (int64_t)(n * pts * G.ops.size());
+      for (const Operand& o : G.ops)
+        if (g.tensors[o.tensor].leaf < 0) appends[o.tensor] += n * pts;
+    }
+  }
+
+  // Layout of one location's LDS area: frontiers (u32 entries, capacity a
+  // power of two for the in-place sort), then one counter per tensor, then
+  // the per-thread variable tables.
+  std::vector<DgdTensor> T(nt);
+  uint64_t lds = 0;
+  for (int t = 0; t < nt; ++t) {
+    DgdTensor& d = T[t];
+    std::memset(&d, 0, sizeof(d));
+    const Tensor& x = g.tensors[t];
+    d.rank = (int32_t)x.shape.size();
+    d.leaf = x.leaf >= 0 ? 1 : 0;
+    d.gid = (uint32_t)gid[t];
+    d.numel = i32(numel(x.shape), "tensor size");
+    for (size_t q = 0; q < x.shape.size(); ++q) d.shape[q] = (int32_t)x.shape[q];
+    d.lds = -1;
+    if (!d.leaf && appends[t] > 0) {
+      const uint64_t cap = pow2_at_least(appends[t]);
+      if (cap > (1u << 20)) fail(DG_E_CAPACITY, "DAG frontier of '" + x.name + "' exceeds 2^20 elements");
+      d.cap = (int32_t)cap;
+      d.lds = (int32_t)lds;
+      lds += 4 * cap;
+    }
+  }
+  const uint64_t count_off = lds;
+  lds += 4 * (uint64_t)nt;
+  lds = (lds + 7) & ~7ull;
+  p.vars_off = (uint32_t)lds;
+  p.max_vars = max_vars;
+  lds += 4ull * (uint64_t)max_vars * (uint64_t)nthreads;
+  if (lds > (1u << 30)) fail(DG_E_CAPACITY, "DAG frontiers too large");
+
+  std::vector<DgdOp> O(nop);
+  std::vector<DgdGroup> Gs;
+  std::vector<DgdOperand> Ps;
+  for (int k = 0; k < nop; ++k) {
+    const OpNode& op = g.ops[k];
+    DgdOp& d = O[k];
+    std::memset(&d, 0, sizeof(d));
+    d.out = op.out;
+    d.g0 = (int32_t)Gs.size();
+    d.ng = (int32_t)op.groups.size();
+    for (const ReadGroup& G : op.groups) {
+      DgdGroup e;
+      std::memset(&e, 0, sizeof(e));
+      if (G.wlo.size() > DGD_MAX_WIN) fail(DG_E_UNSUPPORTED_OP, op.kind + ": window with more than 8 dims");
+      if (G.ops.size() > DGD_MAX_OPERANDS) fail(DG_E_UNSUPPORTED_OP, op.kind + ": more than 8 operands in a group");
+      e.nwin = (int32_t)G.wlo.size();
+      e.nop = (int32_t)G.ops.size();
+      e.op0 = (int32_t)Ps.size();
+      int64_t pts = 1;
+      for (size_t q = 0; q < G.wlo.size(); ++q) {
+        e.wlo[q] = i32(G.wlo[q], "window bound");
+        e.whi[q] = i32(G.whi[q], "window bound");
+        pts *= std::max<int64_t>(0, G.whi[q] - G.wlo[q]);
+      }
+      e.points = pts;
+      d.refs += pts * (int64_t)G.ops.size();
+      for (const Operand& o : G.ops) {
+        DgdOperand P;
+        std::memset(&P, 0, sizeof(P));
+        P.tensor = o.tensor;
+        if (o.mult > 0xFFFFFFFFull) fail(DG_E_OVERFLOW, op.kind + ": multiplicity exceeds 32 bits");
+        P.mult = (uint32_t)o.mult;
+        const Dims& s = g.tensors[o.tensor].shape;
+        for (size_t q = 0; q < s.size(); ++q) P.idx[q] = device_fn(o.idx[q], s[q]);
+        Ps.push_back(P);
+      }
+      Gs.push_back(e);
+    }
+  }
+
+  DgdHeader h;
+  std::memset(&h, 0, sizeof(h));
+  h.magic = DGD_MAGIC;
+  h.ntensor = nt;
+  h.nop = nop;
+  h.ngroup = (int32_t)Gs.size();
+  h.noperand = (int32_t)Ps.size();
+  size_t off = (sizeof(DgdHeader) + 15) & ~(size_t)15;
+  h.tensor_off = (int32_t)off;
+  off += sizeof(DgdTensor) * T.size();
+  off = (off + 15) & ~(size_t)15;
+  h.op_off = (int32_t)off;
+  off += sizeof(DgdOp) * O.size();
+  off = (off + 15) & ~(size_t)15;
+  h.group_off = (int32_t)off;
+  off += sizeof(DgdGroup) * Gs.size();
+  off = (off + 15) & ~(size_t)15;
+  h.operand_off = (int32_t)off;
+  off += sizeof(DgdOperand) * Ps.size();
+  h.blob_bytes = (int32_t)off;
+  h.output = g.output;
+  h.count_off = (int32_t)count_off;
+  h.lds_bytes = (int32_t)lds;
+  h.vars_off = (int32_t)p.vars_off;
+  h.max_vars = max_vars;
+  h.out_numel = numel(g.tensors[g.output].shape);
+  p.blob.assign(off, 0);
+  std::memcpy(p.blob.data(), &h, sizeof(h));
+  if (!T.empty()) std::memcpy(p.blob.data() + h.tensor_off, T.data(), sizeof(DgdTensor) * T.size());
+  if (!O.empty()) std::memcpy(p.blob.data() + h.op_off, O.data(), sizeof(DgdOp) * O.size());
+  if (!Gs.empty()) std::memcpy(p.blob.data() + h.group_off, Gs.data(), sizeof(DgdGroup) * Gs.size());
+  if (!Ps.empty()) std::memcpy(p.blob.data() + h.operand_off, Ps.data(), sizeof(DgdOperand) * Ps.size());
+  p.lds_bytes = (uint32_t)lds;
+  p.gid = gid;
+  return p;
+}
+
+}  // namespace dg

@@ -27,6 +27,7 @@ struct HostCtx {
   void atomic_max(uint64_t* p, uint64_t v) const {
     if (v > *p) *p = v;
   }
+  uint32_t atomic_inc(uint32_t* p) const { return (*p)++; }
   void store(uint32_t* p, uint32_t v) const { *p = v; }
   void store(uint64_t* p, uint64_t v) const { *p = v; }
   void reduce_add(uint64_t* p, uint64_t v) const { *p += v; }
@@ -135,6 +136,56 @@ int dgh_jit_source(const char* text, int64_t len, int block, char* out, int64_t 
     std::string s = dg::jit_enum_source(plan, block);
     snprintf(out, (size_t)cap, "%s", s.c_str());
     return (int)s.size();
+  } catch (const dg::Failure& e) {
+    return fail_with(e);
+  }
+}
+
+// Expression DAGs: node and edge counts as running totals (n + 1 entries
+// each), then the DAGs themselves (as the device's dg_dag_sizes / dg_dag_fill).
+int dgh_dag_sizes(const char* text, int64_t len, const int64_t* locs, int64_t n, int64_t* node_off,
+                  int64_t* edge_off) {
+  try {
+    dg::GraphIR ir = dg::parse_dgir(std::string(text, (size_t)len));
+    dg::DagProgram p = dg::compile_dag(ir, 1);
+    std::vector<uint64_t> area(p.lds_bytes / 8 + 1);
+    HostCtx c;
+    uint32_t err = 0;
+    node_off[0] = edge_off[0] = 0;
+    dgc::DagOut o{nullptr, nullptr, nullptr, nullptr, 0, 0};
+    for (int64_t i = 0; i < n; ++i) {
+      std::memset(area.data(), 0xA5, area.size() * 8);
+      uint64_t nn = 0, ne = 0;
+      dgc::location_dag<HostCtx, dgc::DAG_COUNT>(c, p.blob.data(), locs[i], reinterpret_cast<uint8_t*>(area.data()),
+                                                 o, &nn, &ne, &err);
+      node_off[i + 1] = node_off[i] + (int64_t)nn;
+      edge_off[i + 1] = edge_off[i] + (int64_t)ne;
+    }
+    return bits_status(err);
+  } catch (const dg::Failure& e) {
+    return fail_with(e);
+  }
+}
+
+int dgh_dag_fill(const char* text, int64_t len, const int64_t* locs, int64_t n, const int64_t* node_off,
+                 const int64_t* edge_off, uint32_t* nodes, uint32_t* node_edge, uint32_t* edges, uint32_t* mults) {
+  try {
+    dg::GraphIR ir = dg::parse_dgir(std::string(text, (size_t)len));
+    dg::DagProgram p = dg::compile_dag(ir, 1);
+    std::vector<uint64_t> area(p.lds_bytes / 8 + 1);
+    HostCtx c;
+    uint32_t err = 0;
+    for (int64_t i = 0; i < n; ++i) {
+      std::memset(area.data(), 0x5A, area.size() * 8);
+      dgc::DagOut o{nodes + node_off[i], node_edge + node_off[i], edges + edge_off[i], mults + edge_off[i],
+                    (uint64_t)(node_off[i + 1] - node_off[i]), (uint64_t)(edge_off[i + 1] - edge_off[i])};
+      uint64_t nn = 0, ne = 0;
+      dgc::location_dag<HostCtx, dgc::DAG_FILL>(c, p.blob.data(), locs[i], reinterpret_cast<uint8_t*>(area.data()),
+                                                o, &nn, &ne, &err);
+      if ((int64_t)nn != node_off[i + 1] - node_off[i] || (int64_t)ne != edge_off[i + 1] - edge_off[i])
+        err |= DGP_ERR_SIZE;
+    }
+    return bits_status(err);
   } catch (const dg::Failure& e) {
     return fail_with(e);
   }

@@ -24,6 +24,7 @@ struct DevCtx {
   DGC void atomic_max(uint64_t* p, uint64_t v) const {
     atomicMax(reinterpret_cast<unsigned long long*>(p), (unsigned long long)v);
   }
+  DGC uint32_t atomic_inc(uint32_t* p) const { return atomicAdd(p, 1u); }
   DGC void store(uint32_t* p, uint32_t v) const { __builtin_nontemporal_store(v, p); }
   DGC void store(uint64_t* p, uint64_t v) const { __builtin_nontemporal_store(v, p); }
   // Adds (or takes the maximum of) every thread's v into *p with at most
@@ -288,6 +289,50 @@ DGC void enumerate_body(const uint8_t* __restrict__ blob, dgc::LocSrc locs, int6
     bool go;
     place(c, &go);
   }
+  if (e) atomicOr(err, e);
+}
+
+// Expression DAGs: the sizes pass writes the node and edge counts of
+// location i to nodes_n[i + 1] and edges_n[i + 1] (scanned afterwards into
+// offsets); the fill pass writes location i's nodes at node_off[i] and its
+// edges at edge_off[i].
+template <int BLOCK>
+DGC void dag_sizes_body(const uint8_t* __restrict__ dblob, dgc::LocSrc locs, int64_t n, int64_t* __restrict__ nodes_n,
+                        int64_t* __restrict__ edges_n, uint32_t* __restrict__ err) {
+  __shared__ uint32_t wsum[BLOCK / 64];
+  const int64_t i = blockIdx.x;
+  if (i >= n) return;
+  DevCtx<BLOCK> c{wsum};
+  uint32_t e = 0;
+  uint8_t* area = reinterpret_cast<uint8_t*>(dg_smem);
+  dgc::DagOut o{nullptr, nullptr, nullptr, nullptr, 0, 0};
+  uint64_t nn = 0, ne = 0;
+  dgc::location_dag<DevCtx<BLOCK>, dgc::DAG_COUNT>(c, dblob, dgc::loc_at(locs, i), area, o, &nn, &ne, &e);
+  if (threadIdx.x == 0) {
+    nodes_n[i + 1] = (int64_t)nn;
+    edges_n[i + 1] = (int64_t)ne;
+  }
+  if (e) atomicOr(err, e);
+}
+
+template <int BLOCK>
+DGC void dag_fill_body(const uint8_t* __restrict__ dblob, dgc::LocSrc locs, int64_t n,
+                       const int64_t* __restrict__ node_off, const int64_t* __restrict__ edge_off,
+                       uint32_t* __restrict__ nodes, uint32_t* __restrict__ node_edge, uint32_t* __restrict__ edges,
+                       uint32_t* __restrict__ mults, uint32_t* __restrict__ err) {
+  __shared__ uint32_t wsum[BLOCK / 64];
+  const int64_t i = blockIdx.x;
+  if (i >= n) return;
+  DevCtx<BLOCK> c{wsum};
+  uint32_t e = 0;
+  uint8_t* area = reinterpret_cast<uint8_t*>(dg_smem);
+  const int64_t n0 = node_off[i], e0 = edge_off[i];
+  const int64_t rn = node_off[i + 1] - n0, re = edge_off[i + 1] - e0;
+  dgc::DagOut o{nodes + n0, node_edge + n0, edges + e0, mults + e0, rn > 0 ? (uint64_t)rn : 0ull,
+                re > 0 ? (uint64_t)re : 0ull};
+  uint64_t nn = 0, ne = 0;
+  dgc::location_dag<DevCtx<BLOCK>, dgc::DAG_FILL>(c, dblob, dgc::loc_at(locs, i), area, o, &nn, &ne, &e);
+  if (threadIdx.x == 0 && ((int64_t)nn != rn || (int64_t)ne != re)) e |= DGP_ERR_SIZE;
   if (e) atomicOr(err, e);
 }
 

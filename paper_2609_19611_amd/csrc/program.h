@@ -135,3 +135,65 @@ struct DgpHeader {
 #define DGP_ERR_SIZE 8u       // fill found a row size different from the sizes pass
 #define DGP_ERR_BUFFER 16u    // single pass: the rows do not fit the output buffers
 #define DGP_ERR_TIMEOUT 32u   // single pass: a predecessor's row size never arrived
+
+// ---------------------------------------------------------------------------
+// Expression-DAG program: the ops of a graph as read groups, for emitting
+// the DAG of res(y[l]) (Sec. 3.4, "Back-projection") one location at a time.
+// Every non-leaf element of the cone of y[l] is a node; its edges are the
+// element references of its per-element equation in the equation's order:
+// groups in order, window points in row-major order, a group's operands in
+// order at each point (a point whose operand indices are not all valid reads
+// nothing).  Element ids: leaves keep their global ids, op outputs follow in
+// SSA order (gid of element 0 below).
+// ---------------------------------------------------------------------------
+#define DGD_MAX_WIN 8       // window variables of one group
+#define DGD_MAX_OPERANDS 8  // operands of one group
+
+struct DgdTensor {
+  int32_t rank;
+  int32_t leaf;    // 1: a leaf (a variable; never expanded)
+  int32_t cap;     // frontier capacity in entries (a power of two; 0 when never reached)
+  int32_t lds;     // byte offset of the frontier in the location's LDS area
+  uint32_t gid;    // global id of element 0
+  int32_t numel;
+  int32_t shape[DGP_MAX_RANK];
+};
+
+struct DgdOperand {
+  int32_t tensor;
+  uint32_t mult;
+  DgpIFn idx[DGP_MAX_RANK];  // variables: output coordinates, then window coordinates
+};
+
+struct DgdGroup {
+  int32_t nwin;
+  int32_t nop;
+  int32_t op0;     // first operand in the operand array
+  int32_t pad;
+  int32_t wlo[DGD_MAX_WIN];
+  int32_t whi[DGD_MAX_WIN];
+  int64_t points;  // window points (1 without a window, 0 for an empty window)
+};
+
+struct DgdOp {
+  int32_t out;     // tensor written
+  int32_t g0, ng;  // read groups
+  int32_t pad;
+  int64_t refs;    // element references of one node when every point is valid
+};
+
+struct DgdHeader {
+  uint32_t magic;
+  int32_t ntensor, nop, ngroup, noperand;
+  int32_t tensor_off, op_off, group_off, operand_off;  // byte offsets in the blob
+  int32_t blob_bytes;
+  int32_t output;     // output tensor
+  int32_t count_off;  // byte offset of the per-tensor frontier counters in the LDS area
+  int32_t vars_off;   // byte offset of the per-thread variable tables (max_vars words per thread)
+  int32_t max_vars;   // output plus window variables of the largest group
+  int32_t lds_bytes;  // LDS area of one location
+  int64_t out_numel;
+};
+
+#define DGD_MAGIC 0x44474431u  // "DGD1"
+

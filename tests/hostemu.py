@@ -34,6 +34,8 @@ def lib():
         _lib.dgh_jit_compare_source.argtypes = [ctypes.c_char_p, i64, ctypes.c_char_p, i64, ctypes.c_int,
                                                 ctypes.c_char_p, i64]
         _lib.dgh_jit_options.argtypes = [ctypes.c_char_p, i64]
+        _lib.dgh_dag_sizes.argtypes = [ctypes.c_char_p, i64, P, i64, P, P]
+        _lib.dgh_dag_fill.argtypes = [ctypes.c_char_p, i64, P, i64, P, P, P, P, P, P]
     return _lib
 
 
@@ -51,6 +53,30 @@ def enumerate(text, locs):
     if rc:
         raise HostEmuError(rc, L.dgh_error().decode())
     return off, ids[: off[-1]], cnt[: off[-1]]
+
+
+def dag(text, locs):
+    """Expression DAGs from the library's block code on one host thread, in
+    the layout of oracle.Graph.dag (ids as uint64 for comparison)."""
+    L = lib()
+    t = text.encode()
+    locs = np.ascontiguousarray(np.asarray(locs, dtype=np.int64))
+    noff = np.zeros(len(locs) + 1, dtype=np.int64)
+    eoff = np.zeros(len(locs) + 1, dtype=np.int64)
+    rc = L.dgh_dag_sizes(t, len(t), locs.ctypes.data, len(locs), noff.ctypes.data, eoff.ctypes.data)
+    if rc:
+        raise HostEmuError(rc, L.dgh_error().decode())
+    nodes = np.zeros(max(1, noff[-1]), dtype=np.uint32)
+    node_edge = np.zeros(max(1, noff[-1]), dtype=np.uint32)
+    edges = np.zeros(max(1, eoff[-1]), dtype=np.uint32)
+    mults = np.zeros(max(1, eoff[-1]), dtype=np.uint32)
+    rc = L.dgh_dag_fill(t, len(t), locs.ctypes.data, len(locs), noff.ctypes.data, eoff.ctypes.data,
+                        nodes.ctypes.data, node_edge.ctypes.data, edges.ctypes.data, mults.ctypes.data)
+    if rc:
+        raise HostEmuError(rc, L.dgh_error().decode())
+    return {"node_offsets": noff, "edge_offsets": eoff, "nodes": nodes[: noff[-1]].astype(np.uint64),
+            "node_edge": node_edge[: noff[-1]].astype(np.uint64), "edges": edges[: eoff[-1]].astype(np.uint64),
+            "mults": mults[: eoff[-1]].astype(np.uint64)}
 
 
 def compare(text_a, text_b, locs):

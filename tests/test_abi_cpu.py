@@ -17,7 +17,7 @@ CAT = tiny_graphs.catalogue()
 
 def test_library_exports_every_header_symbol():
     names = B.header_symbols()
-    assert len(names) == 15
+    assert len(names) == 18
     lib = ctypes.CDLL(B.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -157,3 +157,19 @@ def test_static_bound_of_nested_norms_is_tight():
     info = B.dg_graph_info(B.dg_graph_parse(tiny_graphs.nested_layer_norms(4096)))
     exact = max(tiny_graphs.nested_layer_norm_counts(4096, 0))
     assert exact <= info["count_bound"] <= 1.01 * exact
+
+
+@pytest.mark.parametrize("name", ["c1", "c3", "c4", "c5"])
+def test_tensor_ids_match_the_oracle(name):
+    """Element ids of every tensor (leaves keep their base; op outputs follow
+    in SSA order), as the expression DAGs name them."""
+    text = W.CONFIGS[name]["text"]()
+    g = B.dg_graph_parse(text)
+    og = oracle.Graph(text)
+    info = B.dg_graph_info(g)
+    assert info["n_tensors"] == len(og.tensors)
+    for t in range(info["n_tensors"]):
+        ti = B.dg_graph_tensor(g, t)
+        assert ti["name"] == og.tensors[t].name and ti["shape"] == og.tensors[t].shape
+        assert ti["gid"] == og.gid(t)
+        assert (ti["leaf"] >= 0) == (og.tensors[t].leaf_index >= 0)

@@ -1,0 +1,74 @@
+"""GPU parity of the expression DAGs of res(y[l]) (dg_dag_sizes,
+dg_dag_fill) against the oracle's DAGs, element by element, through the C
+ABI: every location of the small catalogue graphs, samples of the five
+workloads (c5's variant and faulty variants too), error paths."""
+
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import tiny_graphs
+from paper_2609_19611_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+CAT = tiny_graphs.catalogue()
+SEPARABLE = sorted(set(CAT) - tiny_graphs.NONSEPARABLE)
+KEYS = ("node_offsets", "edge_offsets", "nodes", "node_edge", "edges", "mults")
+
+
+@pytest.fixture(scope="module")
+def B():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_19611_amd import binding
+    return binding
+
+
+def _host(d):
+    out = {}
+    for k in KEYS:
+        a = d[k].cpu().numpy()
+        out[k] = a if a.dtype == np.int64 else a.view(np.uint32).astype(np.uint64)
+    return out
+
+
+def _check(B, text, locs, threads=8):
+    got = _host(B.dag_locations(B.dg_graph_parse(text), locs))
+    want = oracle.Graph(text).dag(locs, threads=threads)
+    for k in KEYS:
+        assert np.array_equal(got[k], want[k]), k
+    return got
+
+
+@pytest.mark.parametrize("name", SEPARABLE)
+def test_dag_catalogue_all_locations(B, name):
+    text = CAT[name][0]
+    n = oracle.Graph(text).output_numel
+    _check(B, text, list(range(n))[::-1])
+
+
+@pytest.mark.parametrize("name,step", [("c1", 1), ("c2", 1), ("c3", 4096), ("c4", 8191), ("c5", 65536)])
+def test_dag_workloads(B, name, step):
+    locs = W.config_locations(name)[::step]
+    _check(B, W.CONFIGS[name]["text"](), locs)
+
+
+def test_dag_c5_variants(B):
+    locs = W.config_locations("c5")[::32768]
+    for text in [W.c5_variant_text()] + [W.c5_variant_text(fault=f) for f in W.c5_faults()]:
+        _check(B, text, locs)
+
+
+def test_dag_edge_cases(B):
+    g = B.dg_graph_parse(W.c2_text())
+    d = B.dag_locations(g, torch.empty(0, dtype=torch.int64))
+    assert d["node_offsets"].cpu().tolist() == [0] and d["edges"].numel() == 0
+    _check(B, W.c2_text(), [65535, 3, 3, 0])
+    with pytest.raises(B.DgError) as e:
+        B.dag_locations(g, [0, 65536])
+    assert e.value.name == "DG_E_RANGE"
+    # Output that is a leaf: no nodes, no edges.
+    d = B.dag_locations(B.dg_graph_parse("dgir 1\nleaf x 4\noutput x 4\n"), [0, 3])
+    assert d["node_offsets"].cpu().tolist() == [0, 0, 0] and d["edge_offsets"].cpu().tolist() == [0, 0, 0]

@@ -87,3 +87,36 @@ def test_range_and_overflow_errors():
     with pytest.raises(hostemu.HostEmuError) as e:
         hostemu.enumerate(txt, [0])
     assert e.value.code == -6
+
+
+# ---- expression DAGs (the library's DAG block code on one host thread) ----
+_CAT = tiny_graphs.catalogue()
+_SEP = sorted(set(_CAT) - tiny_graphs.NONSEPARABLE)
+
+
+def _dag_equal(a, b):
+    for k in ("node_offsets", "edge_offsets", "nodes", "node_edge", "edges", "mults"):
+        assert np.array_equal(np.asarray(a[k]), np.asarray(b[k])), k
+
+
+@pytest.mark.parametrize("name", _SEP)
+def test_dag_catalogue(name):
+    text = _CAT[name][0]
+    g = oracle.Graph(text)
+    n = g.output_numel
+    locs = list(range(n)) if n <= 256 else sorted(set(np.linspace(0, n - 1, 96).astype(int).tolist()))
+    _dag_equal(hostemu.dag(text, locs), g.dag(locs))
+
+
+@pytest.mark.parametrize("name,count", [("c1", 8), ("c2", 64), ("c3", 2), ("c4", 3), ("c5", 8)])
+def test_dag_workloads(name, count):
+    text = W.CONFIGS[name]["text"]()
+    locs = W.config_locations(name)
+    locs = [locs[i] for i in np.linspace(0, len(locs) - 1, count).astype(int)]
+    _dag_equal(hostemu.dag(text, locs), oracle.Graph(text).dag(locs, threads=4))
+
+
+def test_dag_c5_variants():
+    locs = W.config_locations("c5")[::262144]
+    for text in [W.c5_variant_text()] + [W.c5_variant_text(fault=f) for f in W.c5_faults()[:4]]:
+        _dag_equal(hostemu.dag(text, locs), oracle.Graph(text).dag(locs))
