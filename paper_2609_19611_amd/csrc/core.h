@@ -1234,9 +1234,14 @@ DGC uint32_t location_compare(C& c, const uint8_t* blob_a, const uint8_t* blob_b
 // order, so every consumer has been walked), the list is sorted and made
 // unique, giving the tensor's nodes in ascending order.  A node's edges are
 // its (group, window point, operand) references in order; a point whose
-// operand indices are not all valid is skipped.  Work is spread over the
-// block as (node, reference) pairs, and a block-wide prefix count of the
-// valid ones gives each edge its position.
+// operand indices are not all valid is skipped.
+//
+// Per op, every node's edge count is taken first and an exclusive scan over
+// the nodes gives each node its first edge; the edges are then written at
+// known positions.  Pointwise ops give one thread a node; the others give
+// one wave a node and take each group per variable (the product of per-
+// variable valid sets, no per-point test) or point by point (wave-level
+// compaction), as the compiler decided.
 // ---------------------------------------------------------------------------
 enum : int { DAG_COUNT = 0, DAG_FILL = 1 };
 
@@ -1292,21 +1297,622 @@ DGC uint32_t sort_unique(C& c, uint32_t* f, uint32_t n, uint32_t cap) {
   return kept;
 }
 
-// Index function over the variable table vt (stride nt): the value, and
-// whether it is valid (divisible where exact, inside the dimension).
-DGC bool dag_index(const DgpIFn& f, const int32_t* vt, int nt, int32_t* out) { return ifn_eval(f, vt, nt, out); }
+// Replaces a[0..n) by its exclusive running sums and returns the total.
+// All threads call it; ends past a barrier.
+template <class C>
+DGC uint64_t block_scan(C& c, uint32_t* a, uint32_t n) {
+  const uint32_t nt = (uint32_t)c.nthreads(), tid = (uint32_t)c.tid();
+  const uint32_t per = (n + nt - 1) / nt;
+  const uint32_t b = tid * per < n ? tid * per : n;
+  const uint32_t e = b + per < n ? b + per : n;
+  uint64_t s = 0;
+  for (uint32_t j = b; j < e; ++j) s += a[j];
+  uint64_t tot;
+  uint64_t run = c.scan_add(s, &tot);
+  for (uint32_t j = b; j < e; ++j) {
+    const uint32_t v = a[j];
+    a[j] = (uint32_t)run;
+    run += v;
+  }
+  c.sync();
+  return tot;
+}
 
+// Quotient of a 32-bit n by a tensor dim from its magic number m (0: the
+// dim is 1): the high 64 bits of n * m, from two 32 x 32-bit products.
+DGC uint32_t magic_div(uint32_t n, uint64_t m) {
+  if (!m) return n;
+  const uint64_t lo = (uint64_t)n * (uint32_t)m;
+  const uint64_t hi = (uint64_t)n * (uint32_t)(m >> 32);
+  return (uint32_t)((hi + (lo >> 32)) >> 32);
+}
+
+// n / d and n % d for n < 2^16 (digits of a lane index or the wave width).
+DGC uint32_t small_divmod(uint32_t n, uint32_t d, uint32_t* r) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  uint32_t q = (uint32_t)((float)n * __builtin_amdgcn_rcpf((float)d));
+  int32_t rr = (int32_t)n - (int32_t)(q * d);
+  if (rr < 0) {
+    --q;
+    rr += (int32_t)d;
+  } else if (rr >= (int32_t)d) {
+    ++q;
+    rr -= (int32_t)d;
+  }
+  *r = (uint32_t)rr;
+  return q;
+#else
+  *r = n % d;
+  return n / d;
+#endif
+}
+
+// Floor and ceiling of a / b for b > 0.
+DGC int32_t floor_div(int32_t a, int32_t b) { return fdiv(a, b); }
+DGC int32_t ceil_div(int32_t a, int32_t b) { return -fdiv(-a, b); }
+
+// Coordinates of element e of X into the calling thread's variables 0..R-1.
+DGC void node_coords(const DgdTensor& X, uint32_t e, int32_t* vt, int nt) {
+  for (int d = DGP_MAX_RANK - 1; d >= 0; --d) {
+    if (d < X.rank) {
+      const uint32_t q = magic_div(e, X.magic[d]);
+      vt[d * nt] = (int32_t)(e - q * (uint32_t)X.shape[d]);
+      e = q;
+    }
+  }
+}
+
+// Element index of operand P at the calling thread's variables; false if an
+// index is invalid.
+DGC bool operand_flat(const DgdOperand& P, const DgdTensor& Ta, const int32_t* vt, int nt, uint32_t* flat) {
+  uint32_t f = 0;
+  bool ok = true;
+  for (int d = 0; d < DGP_MAX_RANK; ++d) {
+    if (d < Ta.rank) {
+      int32_t v = 0;
+      ok = ifn_eval(P.idx[d], vt, nt, &v) && ok;
+      f += Ta.stride[d] * (uint32_t)v;
+    }
+  }
+  *flat = f;
+  return ok;
+}
+
+// An interval variable's index function at the node as c0 + k * w (w the
+// variable with index `wv`).
+DGC void ifn_linear(const DgpIFn& f, int wv, const int32_t* vt, int nt, int32_t* c0, int32_t* k) {
+  int32_t c = f.c, kk = 0;
+  for (int t = 0; t < DGP_MAX_FTERMS; ++t) {
+    if (t < f.nterm) {
+      if (f.var[t] == wv) {
+        kk = f.coef[t];
+      } else {
+        int32_t vv = vt[f.var[t] * nt];
+        if (f.vdiv[t] != 1) vv /= f.vdiv[t];
+        c += f.coef[t] * vv;
+      }
+    }
+  }
+  *c0 = c;
+  *k = kk;
+}
+
+// Appends element `flat` of non-leaf tensor t to its frontier.
+template <class C>
+DGC void dag_append(C& c, const DgdTensor& Tc, int t, uint32_t flat, uint8_t* area, uint32_t* cnt, uint32_t* err) {
+  const uint32_t slot = c.atomic_inc(&cnt[t]);
+  if (slot < (uint32_t)Tc.cap) ((uint32_t*)(area + Tc.lds))[slot] = flat;
+  else *err |= DGP_ERR_CAPACITY;
+}
+
+struct DagCtx {
+  const DgdHeader* h;
+  const DgdTensor* T;
+  const DgdGroup* Gs;
+  const DgdOperand* Ps;
+  uint8_t* area;
+  uint32_t* cnt;
+  int32_t* vt;
+  int nt;
+  uint32_t* err;
+};
+
+// One thread, one node of a pointwise op: the node's edges (written from
+// `pos` when `emit`), non-leaf children appended when `append`; returns the
+// number of edges.  The node's coordinates are in the thread's variables.
+template <class C>
+DGC uint32_t pointwise_node(C& c, const DagCtx& x, const DgdOp& op, uint64_t pos, const DagOut& o, bool emit,
+                            bool append) {
+  uint32_t k = 0;
+  for (int q = 0; q < op.ng; ++q) {
+    const DgdGroup& G = x.Gs[op.g0 + q];
+    if (G.points == 0) continue;
+    bool ok = true;
+    for (int a = 0; a < G.nop; ++a) {
+      const DgdOperand& P = x.Ps[G.op0 + a];
+      uint32_t f;
+      ok = operand_flat(P, x.T[P.tensor], x.vt, x.nt, &f) && ok;
+    }
+    if (!ok) continue;
+    for (int a = 0; a < G.nop; ++a) {
+      const DgdOperand& P = x.Ps[G.op0 + a];
+      const DgdTensor& Ta = x.T[P.tensor];
+      uint32_t f = 0;
+      operand_flat(P, Ta, x.vt, x.nt, &f);
+      if (emit && pos + k < o.room_edges) {
+        c.store(&o.edges[pos + k], Ta.gid + f);
+        c.store(&o.mults[pos + k], P.mult);
+      }
+      if (append && !Ta.leaf) dag_append(c, Ta, P.tensor, f, x.area, x.cnt, x.err);
+      ++k;
+    }
+  }
+  return k;
+}
+
+// Digits of v in the mixed radix len[0..Q) (last digit fastest, the first
+// one unbounded), for v < 2^16.
+DGC void radix_digits(uint32_t v, const uint32_t* len, int Q, uint32_t* dg) {
+  DG_UNROLL
+  for (int q = DGD_MAX_WIN - 1; q >= 1; --q) {
+    if (q < Q) {
+      uint32_t r;
+      v = small_divmod(v, len[q], &r);
+      dg[q] = r;
+    } else {
+      dg[q] = 0;
+    }
+  }
+  dg[0] = v;
+}
+
+// Adds the digits inc to dg (each digit below its radix, the first one
+// unbounded).
+DGC void radix_add(uint32_t* dg, const uint32_t* inc, const uint32_t* len, int Q) {
+  uint32_t carry = 0;
+  DG_UNROLL
+  for (int q = DGD_MAX_WIN - 1; q >= 1; --q) {
+    if (q < Q) {
+      const uint32_t t = dg[q] + inc[q] + carry;
+      carry = t >= len[q] ? 1u : 0u;
+      dg[q] = carry ? t - len[q] : t;
+    }
+  }
+  dg[0] += inc[0] + carry;
+}
+
+// Group G of the wave's node point by point over the whole window box: the
+// valid points are compacted within the wave; writes from `pos` when
+// `emit`, appends non-leaf children when `append`; returns the edge count.
+template <class C>
+DGC uint64_t box_group(C& c, const DagCtx& x, const DgdGroup& G, int R, uint64_t pos, const DagOut& o, bool emit,
+                       bool append) {
+  const int lane = c.lane(), L = c.lanes();
+  const int Q = G.nwin, nop = G.nop;
+  const uint64_t P = (uint64_t)G.points;
+  uint32_t len[DGD_MAX_WIN], dg[DGD_MAX_WIN], inc[DGD_MAX_WIN];
+  DG_UNROLL
+  for (int q = 0; q < DGD_MAX_WIN; ++q) len[q] = q < Q ? (uint32_t)(G.whi[q] - G.wlo[q]) : 1u;
+  radix_digits((uint32_t)lane, len, Q, dg);
+  radix_digits((uint32_t)L, len, Q, inc);
+  uint64_t run = 0;
+  for (uint64_t p0 = 0; p0 < P; p0 += (uint64_t)L) {
+    bool ok = p0 + (uint64_t)lane < P;
+    if (ok) {
+      DG_UNROLL
+      for (int q = 0; q < DGD_MAX_WIN; ++q)
+        if (q < Q) x.vt[(R + q) * x.nt] = G.wlo[q] + (int32_t)dg[q];
+      for (int a = 0; a < G.nop; ++a) {
+        const DgdOperand& Pa = x.Ps[G.op0 + a];
+        uint32_t f;
+        ok = operand_flat(Pa, x.T[Pa.tensor], x.vt, x.nt, &f) && ok;
+      }
+    }
+    uint32_t tot;
+    const uint32_t pre = c.wave_prefix(ok, &tot);
+    if (ok && (emit || append)) {
+      for (int a = 0; a < G.nop; ++a) {
+        const DgdOperand& Pa = x.Ps[G.op0 + a];
+        const DgdTensor& Ta = x.T[Pa.tensor];
+        uint32_t f = 0;
+        operand_flat(Pa, Ta, x.vt, x.nt, &f);
+        const uint64_t at = pos + (run + pre) * (uint64_t)nop + (uint64_t)a;
+        if (emit && at < o.room_edges) {
+          c.store(&o.edges[at], Ta.gid + f);
+          c.store(&o.mults[at], Pa.mult);
+        }
+        if (append && !Ta.leaf) dag_append(c, Ta, Pa.tensor, f, x.area, x.cnt, x.err);
+      }
+    }
+    run += tot;
+    radix_add(dg, inc, len, Q);
+  }
+  return run * (uint64_t)nop;
+}
+
+// Per-thread node slots (DgdHeader.slot_off, stride = block threads): per
+// window variable its first valid value, progression length and 64-bit
+// quotient magic; per operand its element index at the first valid point;
+// the node's point count and its 64-bit first edge of the group.
+struct Slots {
+  uint32_t* s;  // this wave's lane 0 column; lane j's column is s + j
+  int nt, MQ, MA;
+  DGC uint32_t& first(int j, int q) const { return s[(size_t)q * nt + j]; }
+  DGC uint32_t& len(int j, int q) const { return s[(size_t)(MQ + q) * nt + j]; }
+  DGC uint32_t& mlo(int j, int q) const { return s[(size_t)(2 * MQ + 2 * q) * nt + j]; }
+  DGC uint32_t& mhi(int j, int q) const { return s[(size_t)(2 * MQ + 2 * q + 1) * nt + j]; }
+  DGC uint32_t& base(int j, int a) const { return s[(size_t)(4 * MQ + a) * nt + j]; }
+  DGC uint32_t& glo(int j) const { return s[(size_t)(4 * MQ + MA + 1) * nt + j]; }
+  DGC uint32_t& ghi(int j) const { return s[(size_t)(4 * MQ + MA + 2) * nt + j]; }
+};
+
+DGC int32_t pmod(int32_t a, int32_t m) {
+  const int32_t r = a % m;
+  return r < 0 ? r + m : r;
+}
+
+// Progressions of group G at the calling thread's node (coordinates in its
+// variables): every window variable's first valid value and length, every
+// operand's element index at the first point, and the quotient magics, in
+// the thread's slot column j.  Returns the number of valid points.
+DGC uint64_t ap_setup(const DagCtx& x, const DgdGroup& G, int R, const Slots& S, int j) {
+  const int Q = G.nwin;
+  for (int q = 0; q < Q; ++q) {
+    S.first(j, q) = (uint32_t)G.wlo[q];
+    S.len(j, q) = (uint32_t)(G.whi[q] - 1);  // inclusive upper bound while constraining
+    S.mlo(j, q) = 0u;                        // residue of the exact division
+  }
+  bool bad = false;
+  for (int pi = 0; pi < G.npair; ++pi) {
+    const DgdPair pr = G.pair[pi];
+    const DgdOperand& P = x.Ps[G.op0 + pr.a];
+    const DgpIFn& f = P.idx[pr.d];
+    if (pr.q < 0) {
+      int32_t v;
+      if (!ifn_eval(f, x.vt, x.nt, &v)) bad = true;
+      continue;
+    }
+    const int q = pr.q;
+    int32_t c0, k;
+    ifn_linear(f, R + q, x.vt, x.nt, &c0, &k);
+    const int32_t top = f.mode == 1 ? f.s * (f.size - 1) : f.size - 1;
+    int32_t l2, h2;
+    if (k > 0) {
+      l2 = ceil_div(-c0, k);
+      h2 = floor_div(top - c0, k);
+    } else {
+      l2 = ceil_div(c0 - top, -k);
+      h2 = floor_div(c0, -k);
+    }
+    if (l2 > (int32_t)S.first(j, q)) S.first(j, q) = (uint32_t)l2;
+    if (h2 < (int32_t)S.len(j, q)) S.len(j, q) = (uint32_t)h2;
+    if (pi == G.mpair[q]) {
+      // c0 + k w = 0 (mod s): g = s / step must divide c0, then
+      // w = (-c0 / g) * inverse(k / g) (mod step).
+      const int32_t m = G.step[q], g = f.s / m;
+      if (c0 % g != 0) bad = true;
+      else S.mlo(j, q) = (uint32_t)((int32_t)(((int64_t)pmod(-(c0 / g), m) * G.minv[q]) % m));
+    }
+  }
+  if (bad) return 0;
+  uint64_t P = 1;
+  for (int q = 0; q < Q; ++q) {
+    const int32_t lo = (int32_t)S.first(j, q), hi = (int32_t)S.len(j, q), m = G.step[q];
+    const int32_t first = m == 1 ? lo : lo + pmod((int32_t)S.mlo(j, q) - lo, m);
+    const uint32_t len = first <= hi ? (uint32_t)((hi - first) / m + 1) : 0u;
+    const uint64_t mg = len > 1 ? ~0ull / len + 1 : 0ull;
+    S.first(j, q) = (uint32_t)first;
+    S.len(j, q) = len;
+    S.mlo(j, q) = (uint32_t)mg;
+    S.mhi(j, q) = (uint32_t)(mg >> 32);
+    P *= len;
+  }
+  if (P == 0) return 0;
+  for (int a = 0; a < G.nop; ++a) S.base(j, a) = x.T[x.Ps[G.op0 + a].tensor].gid;
+  for (int pi = 0; pi < G.npair; ++pi) {
+    const DgdPair pr = G.pair[pi];
+    const DgdOperand& P = x.Ps[G.op0 + pr.a];
+    const DgdTensor& Ta = x.T[P.tensor];
+    const DgpIFn& f = P.idx[pr.d];
+    int32_t v = 0;
+    if (pr.q < 0) {
+      ifn_eval(f, x.vt, x.nt, &v);
+    } else {
+      int32_t c0, k;
+      ifn_linear(f, R + pr.q, x.vt, x.nt, &c0, &k);
+      v = c0 + k * (int32_t)S.first(j, pr.q);
+      if (f.mode == 1) v /= f.s;
+    }
+    S.base(j, pr.a) += Ta.stride[pr.d] * (uint32_t)v;
+  }
+  return P;
+}
+
+// Writes group G's edges for the wave's batch of nodes: lane j's node has
+// Pj points (0 for none), set up in slot column j with its first edge.  The
+// points of the batch are taken flattened across the lanes: point t belongs
+// to the node whose prefix brackets it, and its operands go to that node's
+// first edge + p * nop + a.
+template <class C>
+DGC void flat_emit(C& c, const DagCtx& x, const DgdGroup& G, const Slots& S, uint32_t* WP, uint32_t Pj,
+                   const DagOut& o, bool emit, bool append) {
+  const int lane = c.lane(), L = c.lanes();
+  const int Q = G.nwin, nop = G.nop;
+  uint32_t T;
+  WP[lane] = c.wave_scan(Pj, &T);
+  c.wave_sync();
+  for (uint64_t t0 = 0; t0 < (uint64_t)T; t0 += (uint64_t)L) {
+    const uint64_t tt = t0 + (uint64_t)lane;
+    if (tt < (uint64_t)T) {
+      const uint32_t t = (uint32_t)tt;
+      int j = 0;
+      for (int st = L >> 1; st >= 1; st >>= 1)
+        if (WP[j + st] <= t) j += st;
+      const uint32_t p0 = t - WP[j];
+      uint32_t p = p0, idx[DGD_MAX_WIN];
+      DG_UNROLL
+      for (int q = DGD_MAX_WIN - 1; q >= 1; --q) {
+        idx[q] = 0;
+        if (q < Q) {
+          const uint32_t len = S.len(j, q);
+          const uint64_t mg = ((uint64_t)S.mhi(j, q) << 32) | S.mlo(j, q);
+          const uint32_t quo = magic_div(p, mg);
+          idx[q] = p - quo * len;
+          p = quo;
+        }
+      }
+      idx[0] = p;
+      const uint64_t at0 = (((uint64_t)S.ghi(j) << 32) | S.glo(j)) + (uint64_t)p0 * (uint64_t)nop;
+      for (int a = 0; a < nop; ++a) {
+        const DgdOperand& Pa = x.Ps[G.op0 + a];
+        uint32_t child = S.base(j, a);
+        DG_UNROLL
+        for (int q = 0; q < DGD_MAX_WIN; ++q)
+          if (q < Q) child += G.astep[a][q] * idx[q];
+        const uint64_t at = at0 + (uint64_t)a;
+        if (emit && at < o.room_edges) {
+          c.store(&o.edges[at], child);
+          c.store(&o.mults[at], Pa.mult);
+        }
+        if (append) {
+          const DgdTensor& Ta = x.T[Pa.tensor];
+          if (!Ta.leaf) dag_append(c, Ta, Pa.tensor, child - Ta.gid, x.area, x.cnt, x.err);
+        }
+      }
+    }
+  }
+  c.wave_sync();
+}
+
+// Writes group G's edges of the batch node in lane column j (a node with
+// at least half a wave of points): the wave covers the node's points with
+// its lanes, the digits of each lane's point advancing by the wave width
+// with carries.  NOP operands and Q window variables are compile-time
+// constants, so the steps stay in registers.
+template <class C, int NOP, int Q>
+DGC void node_emit(C& c, const DagCtx& x, const DgdGroup& G, const Slots& S, int j, const DagOut& o, bool emit,
+                   bool append) {
+  const int lane = c.lane(), L = c.lanes();
+  uint32_t len[DGD_MAX_WIN], dg[DGD_MAX_WIN], inc[DGD_MAX_WIN];
+  uint64_t P = 1;
+  DG_UNROLL
+  for (int q = 0; q < DGD_MAX_WIN; ++q) {
+    len[q] = q < Q ? S.len(j, q) : 1u;
+    P *= len[q];
+  }
+  uint32_t base[NOP], mult[NOP], as[NOP][Q > 0 ? Q : 1];
+  bool leaf[NOP];
+  DG_UNROLL
+  for (int a = 0; a < NOP; ++a) {
+    const DgdOperand& Pa = x.Ps[G.op0 + a];
+    base[a] = S.base(j, a);
+    mult[a] = Pa.mult;
+    leaf[a] = x.T[Pa.tensor].leaf != 0;
+    DG_UNROLL
+    for (int q = 0; q < Q; ++q) as[a][q] = G.astep[a][q];
+  }
+  const uint64_t at0 = ((uint64_t)S.ghi(j) << 32) | S.glo(j);
+  radix_digits((uint32_t)lane, len, Q, dg);
+  radix_digits((uint32_t)L, len, Q, inc);
+  for (uint64_t p0 = 0; p0 < P; p0 += (uint64_t)L) {
+    const uint64_t p = p0 + (uint64_t)lane;
+    if (p < P) {
+      const uint64_t at = at0 + p * (uint64_t)NOP;
+      DG_UNROLL
+      for (int a = 0; a < NOP; ++a) {
+        uint32_t child = base[a];
+        DG_UNROLL
+        for (int q = 0; q < Q; ++q) child += as[a][q] * dg[q];
+        if (emit && at + a < o.room_edges) {
+          c.store(&o.edges[at + a], child);
+          c.store(&o.mults[at + a], mult[a]);
+        }
+        if (append && !leaf[a]) {
+          const DgdOperand& Pa = x.Ps[G.op0 + a];
+          const DgdTensor& Ta = x.T[Pa.tensor];
+          dag_append(c, Ta, Pa.tensor, child - Ta.gid, x.area, x.cnt, x.err);
+        }
+      }
+    }
+    radix_add(dg, inc, len, Q);
+  }
+}
+
+// Node-major emission of the batch nodes in `mask` (lane columns) when the
+// group's shape has a compiled emitter; false when it has none.
+template <class C>
+DGC bool emit_nodes(C& c, const DagCtx& x, const DgdGroup& G, const Slots& S, uint64_t mask, const DagOut& o,
+                    bool emit, bool append) {
+  const int key = G.nop * 16 + G.nwin;
+  switch (key) {
+    case 0x11: case 0x12: case 0x13: case 0x14:
+    case 0x21: case 0x22: case 0x23: case 0x24:
+    case 0x31: case 0x32: case 0x33: case 0x34:
+      break;
+    default:
+      return false;
+  }
+  while (mask) {
+    const int j = (int)__builtin_ctzll(mask);
+    mask &= mask - 1;
+    switch (key) {
+      case 0x11: node_emit<C, 1, 1>(c, x, G, S, j, o, emit, append); break;
+      case 0x12: node_emit<C, 1, 2>(c, x, G, S, j, o, emit, append); break;
+      case 0x13: node_emit<C, 1, 3>(c, x, G, S, j, o, emit, append); break;
+      case 0x14: node_emit<C, 1, 4>(c, x, G, S, j, o, emit, append); break;
+      case 0x21: node_emit<C, 2, 1>(c, x, G, S, j, o, emit, append); break;
+      case 0x22: node_emit<C, 2, 2>(c, x, G, S, j, o, emit, append); break;
+      case 0x23: node_emit<C, 2, 3>(c, x, G, S, j, o, emit, append); break;
+      case 0x24: node_emit<C, 2, 4>(c, x, G, S, j, o, emit, append); break;
+      case 0x31: node_emit<C, 3, 1>(c, x, G, S, j, o, emit, append); break;
+      case 0x32: node_emit<C, 3, 2>(c, x, G, S, j, o, emit, append); break;
+      case 0x33: node_emit<C, 3, 3>(c, x, G, S, j, o, emit, append); break;
+      default:   node_emit<C, 3, 4>(c, x, G, S, j, o, emit, append); break;
+    }
+  }
+  return true;
+}
+
+// One op of the walk (ops in reverse SSA order): the op's nodes from its
+// frontier, each node's edge count, the scan, then the edges and the
+// non-leaf children.  *nb and *eb are the location's node and edge counts
+// so far.  Returns false when the location stops with an error.  Called by
+// every thread of the block.
+template <class C, int MODE>
+DGC bool dag_op(C& c, const DagCtx& x, const DgdOp& op, uint32_t* NC, const Slots& S, uint32_t* WP, const DagOut& o,
+                uint64_t* nb_, uint64_t* eb_) {
+  const int tid = c.tid(), nt = c.nthreads();
+  const int lane = c.lane(), wv = c.wave(), W = c.nwaves(), L = c.lanes();
+  const DgdTensor& X = x.T[op.out];
+  const uint32_t got = x.cnt[op.out];
+  if (got == 0) return true;
+  const uint64_t nb = *nb_, eb = *eb_;
+  c.sync();  // every thread has read the counter
+  if (got > (uint32_t)X.cap) {
+    *x.err |= DGP_ERR_CAPACITY;
+    return false;
+  }
+  uint32_t* F = (uint32_t*)(x.area + X.lds);
+  const uint32_t n = sort_unique(c, F, got, (uint32_t)X.cap);
+  if (MODE == DAG_FILL) {
+    for (uint32_t i = (uint32_t)tid; i < n; i += (uint32_t)nt)
+      if (nb + i < o.room_nodes) c.store(&o.nodes[nb + i], X.gid + F[i]);
+  }
+  const int R = X.rank;
+  bool any_box = false;
+  for (int q = 0; q < op.ng; ++q) any_box = any_box || (!x.Gs[op.g0 + q].fast && x.Gs[op.g0 + q].points > 0);
+  // Edge count of every node.
+  if (op.pointwise) {
+    for (uint32_t i = (uint32_t)tid; i < n; i += (uint32_t)nt) {
+      node_coords(X, F[i], x.vt, nt);
+      NC[i] = pointwise_node(c, x, op, 0, o, false, false);
+    }
+  } else {
+    for (uint32_t b0 = (uint32_t)(wv * L); b0 < n; b0 += (uint32_t)(W * L)) {
+      const uint32_t i = b0 + (uint32_t)lane;
+      const bool has = i < n;
+      uint64_t m = 0;
+      if (any_box) {
+        for (uint32_t j = 0; j < (uint32_t)L && b0 + j < n; ++j) {
+          node_coords(X, F[b0 + j], x.vt, nt);
+          uint64_t mj = 0;
+          for (int q = 0; q < op.ng; ++q) {
+            const DgdGroup& G = x.Gs[op.g0 + q];
+            if (!G.fast && G.points > 0) mj += box_group(c, x, G, R, 0, o, false, false);
+          }
+          if ((uint32_t)lane == j) m += mj;
+        }
+      }
+      if (has) {
+        node_coords(X, F[i], x.vt, nt);
+        for (int q = 0; q < op.ng; ++q) {
+          const DgdGroup& G = x.Gs[op.g0 + q];
+          if (G.fast && G.points > 0) m += ap_setup(x, G, R, S, lane) * (uint64_t)G.nop;
+        }
+        if (m > 0xFFFFFFFFull) *x.err |= DGP_ERR_OVERFLOW;
+        NC[i] = (uint32_t)m;
+      }
+    }
+  }
+  c.sync();
+  const uint64_t total = block_scan(c, NC, n);
+  if (eb + total > 0xFFFFFFFFull) {
+    *x.err |= DGP_ERR_OVERFLOW;
+    return false;
+  }
+  if (MODE == DAG_FILL) {
+    for (uint32_t i = (uint32_t)tid; i < n; i += (uint32_t)nt)
+      if (nb + i < o.room_nodes) c.store(&o.node_edge[nb + i], (uint32_t)(eb + NC[i]));
+  }
+  // The edges, and the non-leaf children.
+  const bool emit = MODE == DAG_FILL, append = op.nonleaf != 0;
+  if (emit || append) {
+    if (op.pointwise) {
+      for (uint32_t i = (uint32_t)tid; i < n; i += (uint32_t)nt) {
+        node_coords(X, F[i], x.vt, nt);
+        pointwise_node(c, x, op, eb + NC[i], o, emit, append);
+      }
+    } else {
+      for (uint32_t b0 = (uint32_t)(wv * L); b0 < n; b0 += (uint32_t)(W * L)) {
+        const uint32_t i = b0 + (uint32_t)lane;
+        const bool has = i < n;
+        uint64_t gpos = has ? eb + NC[i] : 0ull;
+        for (int q = 0; q < op.ng; ++q) {
+          const DgdGroup& G = x.Gs[op.g0 + q];
+          if (G.points == 0) continue;
+          if (G.fast) {
+            uint32_t Pj = 0;
+            if (has) {
+              node_coords(X, F[i], x.vt, nt);
+              Pj = (uint32_t)ap_setup(x, G, R, S, lane);
+              S.glo(lane) = (uint32_t)gpos;
+              S.ghi(lane) = (uint32_t)(gpos >> 32);
+            }
+            // Nodes with at least half a wave of points node by node, the
+            // others flattened across the lanes.
+            const bool big = Pj >= (uint32_t)((L + 1) / 2);
+            const uint64_t mask = c.ballot(big);
+            c.wave_sync();
+            const bool done = mask != 0 && emit_nodes(c, x, G, S, mask, o, emit, append);
+            flat_emit(c, x, G, S, WP, done && big ? 0u : Pj, o, emit, append);
+            gpos += (uint64_t)Pj * (uint64_t)G.nop;
+          } else {
+            S.glo(lane) = (uint32_t)gpos;
+            S.ghi(lane) = (uint32_t)(gpos >> 32);
+            c.wave_sync();
+            for (uint32_t j = 0; j < (uint32_t)L && b0 + j < n; ++j) {
+              node_coords(X, F[b0 + j], x.vt, nt);
+              const uint64_t gj = ((uint64_t)S.ghi((int)j) << 32) | S.glo((int)j);
+              const uint64_t mj = box_group(c, x, G, R, gj, o, emit, append);
+              if ((uint32_t)lane == j) gpos += mj;
+            }
+            c.wave_sync();
+          }
+        }
+      }
+    }
+  }
+  c.sync();
+  *nb_ = nb + n;
+  *eb_ = eb + total;
+  return true;
+}
+
+// Expression DAG of res(y[loc]).
 template <class C, int MODE>
 DGC void location_dag(C& c, const uint8_t* dblob, int64_t loc, uint8_t* area, const DagOut& o, uint64_t* n_nodes,
                       uint64_t* n_edges, uint32_t* err) {
   const DgdHeader* h = (const DgdHeader*)dblob;
   const DgdTensor* T = (const DgdTensor*)(dblob + h->tensor_off);
   const DgdOp* O = (const DgdOp*)(dblob + h->op_off);
-  const DgdGroup* Gs = (const DgdGroup*)(dblob + h->group_off);
-  const DgdOperand* Ps = (const DgdOperand*)(dblob + h->operand_off);
   const int tid = c.tid(), nt = c.nthreads();
   uint32_t* cnt = (uint32_t*)(area + h->count_off);
-  int32_t* vt = (int32_t*)(area + h->vars_off) + tid;  // this thread's variables, stride nt
+  uint32_t* NC = (uint32_t*)(area + h->ncount_off);
+  const int wbase = c.wave() * c.lanes();
+  const Slots S{(uint32_t*)(area + h->slot_off) + wbase, nt, h->max_win, h->max_opnd};
+  uint32_t* WP = (uint32_t*)(area + h->wave_off) + wbase;
+  DagCtx x{h, T, (const DgdGroup*)(dblob + h->group_off), (const DgdOperand*)(dblob + h->operand_off), area, cnt,
+           (int32_t*)(area + h->vars_off) + tid, nt, err};
   *n_nodes = 0;
   *n_edges = 0;
   if (loc < 0 || loc >= h->out_numel) {
@@ -1324,113 +1930,8 @@ DGC void location_dag(C& c, const uint8_t* dblob, int64_t loc, uint8_t* area, co
   }
   c.sync();
   uint64_t nb = 0, eb = 0;
-  for (int k = h->nop - 1; k >= 0; --k) {
-    const DgdOp& op = O[k];
-    const DgdTensor& X = T[op.out];
-    const uint32_t got = cnt[op.out];
-    if (got == 0) continue;
-    c.sync();  // every thread has read the counter
-    if (got > (uint32_t)X.cap) {
-      *err |= DGP_ERR_CAPACITY;
-      return;
-    }
-    uint32_t* F = (uint32_t*)(area + X.lds);
-    const uint32_t n = sort_unique(c, F, got, (uint32_t)X.cap);
-    if (MODE == DAG_FILL) {
-      for (uint32_t i = (uint32_t)tid; i < n; i += (uint32_t)nt)
-        if (nb + i < o.room_nodes) c.store(&o.nodes[nb + i], X.gid + F[i]);
-    }
-    const int R = X.rank;
-    const uint64_t E = (uint64_t)op.refs;
-    if (E == 0) {
-      if (MODE == DAG_FILL)
-        for (uint32_t i = (uint32_t)tid; i < n; i += (uint32_t)nt)
-          if (nb + i < o.room_nodes) c.store(&o.node_edge[nb + i], (uint32_t)eb);
-      nb += n;
-      continue;
-    }
-    const uint64_t total = (uint64_t)n * E;
-    uint64_t run = 0;
-    for (uint64_t b0 = 0; b0 < total; b0 += (uint64_t)nt) {
-      const uint64_t pidx = b0 + (uint64_t)tid;
-      bool valid = false;
-      bool first = false;
-      uint32_t node = 0, child = 0, mult = 0;
-      int ctensor = -1;
-      int32_t cflat = 0;
-      if (pidx < total) {
-        node = (uint32_t)(pidx / E);
-        uint64_t r = pidx - (uint64_t)node * E;
-        first = r == 0;
-        // Group, window point and operand of reference r.
-        int gi = op.g0;
-        for (int q = 0; q < op.ng; ++q) {
-          const DgdGroup& G = Gs[op.g0 + q];
-          const uint64_t span = (uint64_t)G.points * (uint64_t)G.nop;
-          if (r < span) {
-            gi = op.g0 + q;
-            break;
-          }
-          r -= span;
-        }
-        const DgdGroup& G = Gs[gi];
-        const uint64_t point = r / (uint64_t)G.nop;
-        const int j = (int)(r - point * (uint64_t)G.nop);
-        // Output coordinates of the node, then the window point.
-        uint32_t e = F[node];
-        for (int d = R - 1; d >= 0; --d) {
-          const uint32_t s = (uint32_t)X.shape[d];
-          vt[d * nt] = (int32_t)(e % s);
-          e /= s;
-        }
-        uint64_t w = point;
-        for (int q = G.nwin - 1; q >= 0; --q) {
-          const uint64_t s = (uint64_t)(G.whi[q] - G.wlo[q]);
-          vt[(R + q) * nt] = G.wlo[q] + (int32_t)(w % s);
-          w /= s;
-        }
-        valid = true;
-        for (int a = 0; a < G.nop && valid; ++a) {
-          const DgdOperand& P = Ps[G.op0 + a];
-          const DgdTensor& Ta = T[P.tensor];
-          int64_t flat = 0;
-          for (int d = 0; d < Ta.rank; ++d) {
-            int32_t v;
-            if (!dag_index(P.idx[d], vt, nt, &v)) {
-              valid = false;
-              break;
-            }
-            flat = flat * Ta.shape[d] + v;
-          }
-          if (valid && a == j) {
-            ctensor = P.tensor;
-            cflat = (int32_t)flat;
-            child = Ta.gid + (uint32_t)flat;
-            mult = P.mult;
-          }
-        }
-      }
-      uint32_t tot;
-      const uint32_t pre = c.prefix(valid, &tot);
-      if (MODE == DAG_FILL) {
-        if (first && nb + node < o.room_nodes) c.store(&o.node_edge[nb + node], (uint32_t)(eb + run + pre));
-        if (valid && eb + run + pre < o.room_edges) {
-          c.store(&o.edges[eb + run + pre], child);
-          c.store(&o.mults[eb + run + pre], mult);
-        }
-      }
-      if (valid && !T[ctensor].leaf) {
-        const DgdTensor& Tc = T[ctensor];
-        const uint32_t slot = c.atomic_inc(&cnt[ctensor]);
-        if (slot < (uint32_t)Tc.cap) ((uint32_t*)(area + Tc.lds))[slot] = (uint32_t)cflat;
-        else *err |= DGP_ERR_CAPACITY;
-      }
-      run += tot;
-    }
-    c.sync();
-    nb += n;
-    eb += run;
-  }
+  for (int k = h->nop - 1; k >= 0; --k)
+    if (!dag_op<C, MODE>(c, x, O[k], NC, S, WP, o, &nb, &eb)) return;
   *n_nodes = nb;
   *n_edges = eb;
 }

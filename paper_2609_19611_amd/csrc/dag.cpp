@@ -37,6 +37,60 @@ DgpIFn device_fn(const IndexFn& f, int64_t size) {
   return d;
 }
 
+// floor(2^64 / d) + 1 = ceil(2^64 / d) for d >= 2: the quotient of any
+// 32-bit n by d is then the high 64 bits of n * magic (Lemire, Kaser and
+// Kurz, "Faster remainder by direct computation", 2019).  0 for d = 1.
+uint64_t quotient_magic(int64_t d) { return d <= 1 ? 0 : ~0ull / (uint64_t)d + 1; }
+
+// The one window variable (index into the window) of an index function of a
+// group with R output variables; -1 for none, -2 for two or more.
+int window_var(const IndexFn& f, int R) {
+  int w = -1;
+  for (const IndexFn::Term& t : f.terms)
+    if (t.var >= R) {
+      if (w >= 0 && w != t.var - R) return -2;
+      w = t.var - R;
+    }
+  return w;
+}
+
+// Coefficient of window variable q in f when f is c0 + k * w (mode 0) or
+// (c0 + k * w) / s exactly (mode 1) with a single unit-divisor term in w;
+// 0 otherwise.
+int64_t progression_coef(const IndexFn& f, int R, int q) {
+  if (f.mode != 0 && f.mode != 1) return 0;
+  int n = 0;
+  int64_t k = 0;
+  for (const IndexFn::Term& t : f.terms)
+    if (t.var == R + q) {
+      if (t.vdiv != 1) return 0;
+      k = t.coef;
+      ++n;
+    }
+  return n == 1 ? k : 0;
+}
+
+int64_t gcd64(int64_t a, int64_t b) {
+  a = a < 0 ? -a : a;
+  b = b < 0 ? -b : b;
+  while (b) {
+    int64_t t = a % b;
+    a = b;
+    b = t;
+  }
+  return a;
+}
+
+// Inverse of a modulo m (gcd(a, m) = 1, m >= 1); 0 for m = 1.
+int64_t mod_inverse(int64_t a, int64_t m) {
+  if (m == 1) return 0;
+  a %= m;
+  if (a < 0) a += m;
+  for (int64_t x = 1; x < m; ++x)
+    if ((a * x) % m == 1) return x;
+  fail(DG_E_UNSUPPORTED_OP, "no modular inverse");
+}
+
 uint64_t pow2_at_least(uint64_t v) {
   uint64_t p = 1;
   while (p < v) p <<= 1;
@@ -46,6 +100,9 @@ uint64_t pow2_at_least(uint64_t v) {
 }  // namespace
 
 DagProgram compile_dag(const GraphIR& g, int nthreads) {
+  // Waves of 64 lanes on the device; the host emulation runs one thread.
+  const int lanes = nthreads >= 64 ? 64 : 1;
+  const int nwaves = nthreads / lanes;
   const int nt = (int)g.tensors.size(), nop = (int)g.ops.size();
   // Element ids: leaves keep theirs, op outputs follow in SSA order.
   std::vector<uint64_t> gid(nt, 0);
@@ -94,7 +151,13 @@ DagProgram compile_dag(const GraphIR& g, int nthreads) {
     d.leaf = x.leaf >= 0 ? 1 : 0;
     d.gid = (uint32_t)gid[t];
     d.numel = i32(numel(x.shape), "tensor size");
-    for (size_t q = 0; q < x.shape.size(); ++q) d.shape[q] = (int32_t)x.shape[q];
+    int64_t st = 1;
+    for (int q = (int)x.shape.size() - 1; q >= 0; --q) {
+      d.shape[q] = (int32_t)x.shape[q];
+      d.stride[q] = (uint32_t)st;
+      d.magic[q] = quotient_magic(x.shape[q]);
+      st *= x.shape[q];
+    }
     d.lds = -1;
     if (!d.leaf && appends[t] > 0) {
       const uint64_t cap = pow2_at_least(appends[t]);
@@ -104,16 +167,20 @@ DagProgram compile_dag(const GraphIR& g, int nthreads) {
       lds += 4 * cap;
     }
   }
+  int64_t ncount_cap = 0;
+  for (int t = 0; t < nt; ++t) ncount_cap = std::max<int64_t>(ncount_cap, T[t].cap);
   const uint64_t count_off = lds;
   lds += 4 * (uint64_t)nt;
   lds = (lds + 7) & ~7ull;
   p.vars_off = (uint32_t)lds;
   p.max_vars = max_vars;
   lds += 4ull * (uint64_t)max_vars * (uint64_t)nthreads;
-  if (lds > (1u << 30)) fail(DG_E_CAPACITY, "DAG frontiers too large");
+  const uint64_t ncount_off = lds;
+  lds += 4ull * (uint64_t)ncount_cap;
 
   std::vector<DgdOp> O(nop);
   std::vector<DgdGroup> Gs;
+  int max_win = 1, max_opnd = 1;
   std::vector<DgdOperand> Ps;
   for (int k = 0; k < nop; ++k) {
     const OpNode& op = g.ops[k];
@@ -130,6 +197,61 @@ DagProgram compile_dag(const GraphIR& g, int nthreads) {
       e.nwin = (int32_t)G.wlo.size();
       e.nop = (int32_t)G.ops.size();
       e.op0 = (int32_t)Ps.size();
+      const int R = (int)g.tensors[op.out].shape.size();
+      // Progressions: every index function uses at most one window
+      // variable, in a single unit-divisor term, with no floor division;
+      // at most one exact division per variable.
+      bool fast = true;
+      int npair = 0;
+      for (int q = 0; q < (int)G.wlo.size(); ++q) {
+        e.step[q] = 1;
+        e.mpair[q] = -1;
+      }
+      for (size_t a = 0; a < G.ops.size(); ++a)
+        for (size_t d = 0; d < G.ops[a].idx.size(); ++d) {
+          const IndexFn& f = G.ops[a].idx[d];
+          const int q = window_var(f, R);
+          if (q == -2) {
+            fast = false;
+            continue;
+          }
+          if (npair < DGD_MAX_PAIRS) e.pair[npair] = DgdPair{(int16_t)a, (int16_t)d, (int16_t)q, 0};
+          if (q >= 0) {
+            const int64_t k = progression_coef(f, R, q);
+            if (k == 0) {
+              fast = false;
+            } else if (f.mode == 1) {
+              if (e.mpair[q] >= 0) fast = false;
+              const int64_t gk = gcd64(k, f.s);
+              e.mpair[q] = npair;
+              e.step[q] = (int32_t)(f.s / gk);
+              e.minv[q] = (int32_t)mod_inverse(k / gk, f.s / gk);
+            }
+          }
+          ++npair;
+        }
+      if (npair > DGD_MAX_PAIRS) fast = false;
+      e.fast = fast ? 1 : 0;
+      e.npair = fast ? npair : 0;
+      if (fast) {
+        // Element-index steps per progression step.
+        for (size_t a = 0; a < G.ops.size(); ++a) {
+          const Dims& sh = g.tensors[G.ops[a].tensor].shape;
+          int64_t st = 1;
+          for (int d = (int)sh.size() - 1; d >= 0; --d) {
+            const IndexFn& f = G.ops[a].idx[d];
+            const int q = window_var(f, R);
+            if (q >= 0) {
+              const int64_t k = progression_coef(f, R, q);
+              const int64_t per = f.mode == 1 ? k * e.step[q] / f.s : k * e.step[q];
+              e.astep[a][q] += (uint32_t)(st * per);
+            }
+            st *= sh[d];
+          }
+        }
+        max_win = std::max(max_win, (int)G.wlo.size());
+        max_opnd = std::max(max_opnd, (int)G.ops.size());
+      }
       int64_t pts = 1;
       for (size_t q = 0; q < G.wlo.size(); ++q) {
         e.wlo[q] = i32(G.wlo[q], "window bound");
@@ -142,6 +264,7 @@ DagProgram compile_dag(const GraphIR& g, int nthreads) {
         DgdOperand P;
         std::memset(&P, 0, sizeof(P));
         P.tensor = o.tensor;
+        if (g.tensors[o.tensor].leaf < 0) d.nonleaf = 1;
         if (o.mult > 0xFFFFFFFFull) fail(DG_E_OVERFLOW, op.kind + ": multiplicity exceeds 32 bits");
         P.mult = (uint32_t)o.mult;
         const Dims& s = g.tensors[o.tensor].shape;
@@ -150,7 +273,20 @@ DagProgram compile_dag(const GraphIR& g, int nthreads) {
       }
       Gs.push_back(e);
     }
+    d.pointwise = 1;
+    for (const ReadGroup& G : op.groups)
+      if (!G.wlo.empty()) d.pointwise = 0;
   }
+  // Per-thread node slots (per window variable: first value, count and a
+  // 64-bit quotient magic; per operand: element index at the first point;
+  // then the point count and the 64-bit first edge), then one prefix word
+  // per lane of every wave.
+  const int slot_words = 4 * max_win + max_opnd + 3;
+  const uint64_t slot_off = lds;
+  lds += 4ull * (uint64_t)slot_words * (uint64_t)nthreads;
+  const uint64_t wave_off = lds;
+  lds += 4ull * (uint64_t)lanes * (uint64_t)nwaves;
+  if (lds > (1u << 30)) fail(DG_E_CAPACITY, "DAG frontiers too large");
 
   DgdHeader h;
   std::memset(&h, 0, sizeof(h));
@@ -178,6 +314,13 @@ DagProgram compile_dag(const GraphIR& g, int nthreads) {
   h.vars_off = (int32_t)p.vars_off;
   h.max_vars = max_vars;
   h.out_numel = numel(g.tensors[g.output].shape);
+  h.ncount_off = (int32_t)ncount_off;
+  h.ncount_cap = (int32_t)ncount_cap;
+  h.slot_off = (int32_t)slot_off;
+  h.slot_words = slot_words;
+  h.wave_off = (int32_t)wave_off;
+  h.max_win = max_win;
+  h.max_opnd = max_opnd;
   p.blob.assign(off, 0);
   std::memcpy(p.blob.data(), &h, sizeof(h));
   if (!T.empty()) std::memcpy(p.blob.data() + h.tensor_off, T.data(), sizeof(DgdTensor) * T.size());

@@ -22,6 +22,24 @@ namespace {
 struct HostCtx {
   int tid() const { return 0; }
   int nthreads() const { return 1; }
+  int lane() const { return 0; }
+  int lanes() const { return 1; }
+  int wave() const { return 0; }
+  int nwaves() const { return 1; }
+  void wave_sync() const {}
+  uint32_t wave_prefix(bool f, uint32_t* total) const {
+    *total = f ? 1u : 0u;
+    return 0u;
+  }
+  uint64_t scan_add(uint64_t v, uint64_t* total) const {
+    *total = v;
+    return 0u;
+  }
+  uint64_t ballot(bool f) const { return f ? 1u : 0u; }
+  uint32_t wave_scan(uint32_t v, uint32_t* total) const {
+    *total = v;
+    return 0u;
+  }
   void sync() const {}
   void atomic_add(uint64_t* p, uint64_t v) const { *p += v; }
   void atomic_max(uint64_t* p, uint64_t v) const {
@@ -186,6 +204,35 @@ int dgh_dag_fill(const char* text, int64_t len, const int64_t* locs, int64_t n, 
         err |= DGP_ERR_SIZE;
     }
     return bits_status(err);
+  } catch (const dg::Failure& e) {
+    return fail_with(e);
+  }
+}
+
+// How the DAG program takes each read group: per group, four int32 values
+// (op index, 1 if the op is pointwise, 1 if the group is taken per variable,
+// the number of list variables).  Returns the group count (at most cap are
+// written) or a negative status.
+int dgh_dag_groups(const char* text, int64_t len, int32_t* out, int64_t cap) {
+  try {
+    dg::GraphIR ir = dg::parse_dgir(std::string(text, (size_t)len));
+    dg::DagProgram p = dg::compile_dag(ir, 64);
+    const DgdHeader* h = reinterpret_cast<const DgdHeader*>(p.blob.data());
+    const DgdOp* O = reinterpret_cast<const DgdOp*>(p.blob.data() + h->op_off);
+    const DgdGroup* G = reinterpret_cast<const DgdGroup*>(p.blob.data() + h->group_off);
+    int64_t k = 0;
+    for (int o = 0; o < h->nop; ++o)
+      for (int q = 0; q < O[o].ng; ++q, ++k) {
+        if (k >= cap) continue;
+        const DgdGroup& g = G[O[o].g0 + q];
+        int lists = 0;  // variables with an exact division (progression step > 1)
+        for (int v = 0; v < g.nwin; ++v) lists += g.fast && g.mpair[v] >= 0 ? 1 : 0;
+        out[4 * k] = o;
+        out[4 * k + 1] = O[o].pointwise;
+        out[4 * k + 2] = g.fast;
+        out[4 * k + 3] = lists;
+      }
+    return (int)k;
   } catch (const dg::Failure& e) {
     return fail_with(e);
   }

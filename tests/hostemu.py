@@ -36,6 +36,7 @@ def lib():
         _lib.dgh_jit_options.argtypes = [ctypes.c_char_p, i64]
         _lib.dgh_dag_sizes.argtypes = [ctypes.c_char_p, i64, P, i64, P, P]
         _lib.dgh_dag_fill.argtypes = [ctypes.c_char_p, i64, P, i64, P, P, P, P, P, P]
+        _lib.dgh_dag_groups.argtypes = [ctypes.c_char_p, i64, P, i64]
     return _lib
 
 
@@ -77,6 +78,18 @@ def dag(text, locs):
     return {"node_offsets": noff, "edge_offsets": eoff, "nodes": nodes[: noff[-1]].astype(np.uint64),
             "node_edge": node_edge[: noff[-1]].astype(np.uint64), "edges": edges[: eoff[-1]].astype(np.uint64),
             "mults": mults[: eoff[-1]].astype(np.uint64)}
+
+
+def dag_groups(text):
+    """How the DAG program takes each read group, as (op index, pointwise op,
+    per-variable group, list variables) rows."""
+    L = lib()
+    t = text.encode()
+    out = np.zeros((256, 4), dtype=np.int32)
+    k = L.dgh_dag_groups(t, len(t), out.ctypes.data, 256)
+    if k < 0:
+        raise HostEmuError(k, L.dgh_error().decode())
+    return [tuple(int(v) for v in r) for r in out[:k]]
 
 
 def compare(text_a, text_b, locs):

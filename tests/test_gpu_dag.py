@@ -49,6 +49,16 @@ def test_dag_catalogue_all_locations(B, name):
     _check(B, text, list(range(n))[::-1])
 
 
+DAGCAT = tiny_graphs.dag_catalogue()
+
+
+@pytest.mark.parametrize("name", sorted(DAGCAT))
+def test_dag_extra_catalogue(B, name):
+    text = DAGCAT[name]
+    n = oracle.Graph(text).output_numel
+    _check(B, text, list(range(n))[::-1])
+
+
 @pytest.mark.parametrize("name,step", [("c1", 1), ("c2", 1), ("c3", 4096), ("c4", 8191), ("c5", 65536)])
 def test_dag_workloads(B, name, step):
     locs = W.config_locations(name)[::step]

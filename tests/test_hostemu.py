@@ -116,6 +116,35 @@ def test_dag_workloads(name, count):
     _dag_equal(hostemu.dag(text, locs), oracle.Graph(text).dag(locs, threads=4))
 
 
+_DAGCAT = tiny_graphs.dag_catalogue()
+
+
+@pytest.mark.parametrize("name", sorted(_DAGCAT))
+def test_dag_extra_catalogue(name):
+    """Coupled window indices (point by point), an oversized list table,
+    grouped conv-transpose, boundary reads, coupled reads of a non-leaf."""
+    text = _DAGCAT[name]
+    g = oracle.Graph(text)
+    locs = list(range(g.output_numel))[::-1]
+    _dag_equal(hostemu.dag(text, locs), g.dag(locs))
+
+
+def test_dag_paths_taken():
+    """Each way of taking a group is exercised: by progressions (with and
+    without an exact division), point by point (two window variables in one
+    index, floor division of a window variable), pointwise."""
+    rows = {name: hostemu.dag_groups(text) for name, text in _DAGCAT.items()}
+    assert any(r[1] == 0 and r[2] == 0 for r in rows["gather_coupled"])
+    assert any(r[1] == 0 and r[2] == 0 for r in rows["gather_coupled_nonleaf"])
+    assert any(r[1] == 0 and r[2] == 1 and r[3] == 1 for r in rows["gather_big_list"])
+    assert any(r[1] == 1 for r in rows["gather_shift"])
+    floor = hostemu.dag_groups(_CAT["gather_floor_flat"][0])
+    assert any(r[1] == 0 and r[2] == 0 for r in floor)
+    c3 = hostemu.dag_groups(W.c3_text())
+    assert c3[0][2] == 1 and c3[0][3] == 3  # conv-transpose taps: exact divisions
+    assert all(r[2] == 1 for r in hostemu.dag_groups(W.c4_text()))
+
+
 def test_dag_c5_variants():
     locs = W.config_locations("c5")[::262144]
     for text in [W.c5_variant_text()] + [W.c5_variant_text(fault=f) for f in W.c5_faults()[:4]]:

@@ -161,6 +161,35 @@ def catalogue():
     return G
 
 
+def dag_catalogue():
+    """Graphs for the expression-DAG path beyond the catalogue: index
+    functions coupling two window variables (taken point by point), a list
+    variable whose table is too large for the per-variable path, reads that
+    leave the operand at the boundary, and coupled reads of a non-leaf
+    tensor."""
+    G = {}
+    G["gather_coupled"] = _g([("x", [6, 10])],
+                             [("y", "affine_gather", ["x"],
+                               dict(shape=[6, 5], window=[3, 4], idx0=["o0", "o1+w0+w1-2"], mult=[1]))],
+                             "y", [6, 5])
+    G["gather_coupled_nonleaf"] = _g([("x", [4, 9]), ("v", [3])],
+                                     [("r", "relu", ["x"], {}),
+                                      ("y", "affine_gather", ["r", "v"],
+                                       dict(shape=[4, 4], window=[3, 2, 2], idx0=["(o0+w1)/2", "2*o1+w0-w2"],
+                                            idx1=["w0"], mult=[1, 2]))],
+                                     "y", [4, 4])
+    G["gather_big_list"] = _g([("x", [600]), ("w", [1100])],
+                              [("y", "affine_gather", ["x", "w"],
+                                dict(shape=[5], window=[1100], idx0=["(o0+w0)/2"], idx1=["w0"], mult=[1, 3]))],
+                              "y", [5])
+    G["gather_shift"] = _g([("x", [2, 5]), ("z", [2, 5])],
+                           [("t", "exp", ["x"], {}),
+                            ("y", "affine_gather", ["t", "z"],
+                             dict(shape=[2, 5], window=[1], idx0=["o0", "o1-1"], idx1=["o0", "o1+1+w0"], mult=[1, 1]))],
+                           "y", [2, 5])
+    return G
+
+
 def nested_layer_norms(n):
     """Three layer norms in a row over n elements: path counts near
     n^5 (past 2^32 from n = 1024 on)."""
