@@ -1253,24 +1253,22 @@ struct DagOut {
   uint64_t room_nodes, room_edges;
 };
 
-// Sorts the first n entries of f (capacity cap, a power of two) and keeps
-// one of each value; returns the number kept.  All threads call it.
+// Sorts the first n entries of f and keeps one of each value; returns the
+// number kept.  Bitonic network whose comparators all put the smaller value
+// at the lower index (each merge starts by comparing mirrored positions), so
+// positions at or past n act as +infinity and their comparators are
+// skipped: any n, sorted in place.  All threads call it.
 template <class C>
-DGC uint32_t sort_unique(C& c, uint32_t* f, uint32_t n, uint32_t cap) {
+DGC uint32_t sort_unique(C& c, uint32_t* f, uint32_t n) {
   const int tid = c.tid(), nt = c.nthreads();
-  uint32_t p2 = 1;
-  while (p2 < n) p2 <<= 1;
-  if (p2 > cap) p2 = cap;
-  for (uint32_t i = n + (uint32_t)tid; i < p2; i += (uint32_t)nt) f[i] = 0xFFFFFFFFu;
-  c.sync();
-  for (uint32_t k = 2; k <= p2; k <<= 1) {
+  for (uint32_t k = 2; (k >> 1) < n; k <<= 1) {
     for (uint32_t j = k >> 1; j > 0; j >>= 1) {
-      for (uint32_t i = (uint32_t)tid; i < p2; i += (uint32_t)nt) {
-        const uint32_t l = i ^ j;
-        if (l > i) {
+      const uint32_t mask = j == (k >> 1) ? k - 1 : j;  // mirror within the block first
+      for (uint32_t i = (uint32_t)tid; i < n; i += (uint32_t)nt) {
+        const uint32_t l = i ^ mask;
+        if (l > i && l < n) {
           const uint32_t a = f[i], b = f[l];
-          const bool up = (i & k) == 0;
-          if ((a > b) == up) {
+          if (a > b) {
             f[i] = b;
             f[l] = a;
           }
@@ -1279,6 +1277,7 @@ DGC uint32_t sort_unique(C& c, uint32_t* f, uint32_t n, uint32_t cap) {
       c.sync();
     }
   }
+  c.sync();
   uint32_t kept = 0;
   for (uint32_t b0 = 0; b0 < n; b0 += (uint32_t)nt) {
     const uint32_t i = b0 + (uint32_t)tid;
@@ -1531,19 +1530,17 @@ DGC uint64_t box_group(C& c, const DagCtx& x, const DgdGroup& G, int R, uint64_t
 }
 
 // Per-thread node slots (DgdHeader.slot_off, stride = block threads): per
-// window variable its first valid value, progression length and 64-bit
-// quotient magic; per operand its element index at the first valid point;
-// the node's point count and its 64-bit first edge of the group.
+// window variable its first valid value and progression length (while
+// setting up: its bounds), per operand its element index at the first valid
+// point, and the node's 64-bit first edge of the group.
 struct Slots {
   uint32_t* s;  // this wave's lane 0 column; lane j's column is s + j
   int nt, MQ, MA;
   DGC uint32_t& first(int j, int q) const { return s[(size_t)q * nt + j]; }
   DGC uint32_t& len(int j, int q) const { return s[(size_t)(MQ + q) * nt + j]; }
-  DGC uint32_t& mlo(int j, int q) const { return s[(size_t)(2 * MQ + 2 * q) * nt + j]; }
-  DGC uint32_t& mhi(int j, int q) const { return s[(size_t)(2 * MQ + 2 * q + 1) * nt + j]; }
-  DGC uint32_t& base(int j, int a) const { return s[(size_t)(4 * MQ + a) * nt + j]; }
-  DGC uint32_t& glo(int j) const { return s[(size_t)(4 * MQ + MA + 1) * nt + j]; }
-  DGC uint32_t& ghi(int j) const { return s[(size_t)(4 * MQ + MA + 2) * nt + j]; }
+  DGC uint32_t& base(int j, int a) const { return s[(size_t)(2 * MQ + a) * nt + j]; }
+  DGC uint32_t& glo(int j) const { return s[(size_t)(2 * MQ + MA) * nt + j]; }
+  DGC uint32_t& ghi(int j) const { return s[(size_t)(2 * MQ + MA + 1) * nt + j]; }
 };
 
 DGC int32_t pmod(int32_t a, int32_t m) {
@@ -1552,15 +1549,14 @@ DGC int32_t pmod(int32_t a, int32_t m) {
 }
 
 // Progressions of group G at the calling thread's node (coordinates in its
-// variables): every window variable's first valid value and length, every
-// operand's element index at the first point, and the quotient magics, in
-// the thread's slot column j.  Returns the number of valid points.
-DGC uint64_t ap_setup(const DagCtx& x, const DgdGroup& G, int R, const Slots& S, int j) {
+// variables): every window variable's first valid value and length and,
+// with `bases`, every operand's element index at the first point, in the
+// thread's slot column j.  Returns the number of valid points.
+DGC uint64_t ap_setup(const DagCtx& x, const DgdGroup& G, int R, const Slots& S, int j, bool bases) {
   const int Q = G.nwin;
   for (int q = 0; q < Q; ++q) {
     S.first(j, q) = (uint32_t)G.wlo[q];
     S.len(j, q) = (uint32_t)(G.whi[q] - 1);  // inclusive upper bound while constraining
-    S.mlo(j, q) = 0u;                        // residue of the exact division
   }
   bool bad = false;
   for (int pi = 0; pi < G.npair; ++pi) {
@@ -1586,28 +1582,30 @@ DGC uint64_t ap_setup(const DagCtx& x, const DgdGroup& G, int R, const Slots& S,
     }
     if (l2 > (int32_t)S.first(j, q)) S.first(j, q) = (uint32_t)l2;
     if (h2 < (int32_t)S.len(j, q)) S.len(j, q) = (uint32_t)h2;
-    if (pi == G.mpair[q]) {
-      // c0 + k w = 0 (mod s): g = s / step must divide c0, then
-      // w = (-c0 / g) * inverse(k / g) (mod step).
-      const int32_t m = G.step[q], g = f.s / m;
-      if (c0 % g != 0) bad = true;
-      else S.mlo(j, q) = (uint32_t)((int32_t)(((int64_t)pmod(-(c0 / g), m) * G.minv[q]) % m));
-    }
   }
   if (bad) return 0;
   uint64_t P = 1;
   for (int q = 0; q < Q; ++q) {
     const int32_t lo = (int32_t)S.first(j, q), hi = (int32_t)S.len(j, q), m = G.step[q];
-    const int32_t first = m == 1 ? lo : lo + pmod((int32_t)S.mlo(j, q) - lo, m);
+    int32_t first = lo;
+    if (m > 1) {
+      // The exact division c0 + k w = 0 (mod s): g = s / step must divide
+      // c0, then w = (-c0 / g) * inverse(k / g) (mod step).
+      const DgdPair pr = G.pair[G.mpair[q]];
+      const DgpIFn& f = x.Ps[G.op0 + pr.a].idx[pr.d];
+      int32_t c0, k;
+      ifn_linear(f, R + q, x.vt, x.nt, &c0, &k);
+      const int32_t g = f.s / m;
+      if (c0 % g != 0) return 0;
+      const int32_t r = (int32_t)(((int64_t)pmod(-(c0 / g), m) * G.minv[q]) % m);
+      first = lo + pmod(r - lo, m);
+    }
     const uint32_t len = first <= hi ? (uint32_t)((hi - first) / m + 1) : 0u;
-    const uint64_t mg = len > 1 ? ~0ull / len + 1 : 0ull;
     S.first(j, q) = (uint32_t)first;
     S.len(j, q) = len;
-    S.mlo(j, q) = (uint32_t)mg;
-    S.mhi(j, q) = (uint32_t)(mg >> 32);
     P *= len;
   }
-  if (P == 0) return 0;
+  if (P == 0 || !bases) return P;
   for (int a = 0; a < G.nop; ++a) S.base(j, a) = x.T[x.Ps[G.op0 + a].tensor].gid;
   for (int pi = 0; pi < G.npair; ++pi) {
     const DgdPair pr = G.pair[pi];
@@ -1655,9 +1653,14 @@ DGC void flat_emit(C& c, const DagCtx& x, const DgdGroup& G, const Slots& S, uin
         idx[q] = 0;
         if (q < Q) {
           const uint32_t len = S.len(j, q);
-          const uint64_t mg = ((uint64_t)S.mhi(j, q) << 32) | S.mlo(j, q);
-          const uint32_t quo = magic_div(p, mg);
-          idx[q] = p - quo * len;
+          uint32_t r, quo;
+          if (p < 65536u) {
+            quo = small_divmod(p, len, &r);
+          } else {
+            quo = p / len;
+            r = p - quo * len;
+          }
+          idx[q] = r;
           p = quo;
         }
       }
@@ -1685,7 +1688,7 @@ DGC void flat_emit(C& c, const DagCtx& x, const DgdGroup& G, const Slots& S, uin
 }
 
 // Writes group G's edges of the batch node in lane column j (a node with
-// at least half a wave of points): the wave covers the node's points with
+// at least four waves of points): the wave covers the node's points with
 // its lanes, the digits of each lane's point advancing by the wave width
 // with carries.  NOP operands and Q window variables are compile-time
 // constants, so the steps stay in registers.
@@ -1773,6 +1776,39 @@ DGC bool emit_nodes(C& c, const DagCtx& x, const DgdGroup& G, const Slots& S, ui
   return true;
 }
 
+// Edge count of the calling lane's node in the wave's batch starting at
+// node b0 (0 past the end): the box groups node by node across the wave,
+// the progression groups one node per lane.  Called by all lanes of the
+// wave; leaves every lane's variables at its own node.
+template <class C>
+DGC uint64_t batch_node_count(C& c, const DagCtx& x, const DgdOp& op, const DgdTensor& X, const uint32_t* F,
+                              uint32_t n, uint32_t b0, int R, const Slots& S) {
+  const int lane = c.lane(), L = c.lanes();
+  uint64_t m = 0;
+  bool any_box = false;
+  for (int q = 0; q < op.ng; ++q) any_box = any_box || (!x.Gs[op.g0 + q].fast && x.Gs[op.g0 + q].points > 0);
+  if (any_box) {
+    for (uint32_t j = 0; j < (uint32_t)L && b0 + j < n; ++j) {
+      node_coords(X, F[b0 + j], x.vt, x.nt);
+      uint64_t mj = 0;
+      for (int q = 0; q < op.ng; ++q) {
+        const DgdGroup& G = x.Gs[op.g0 + q];
+        if (!G.fast && G.points > 0) mj += box_group(c, x, G, R, 0, DagOut{}, false, false);
+      }
+      if ((uint32_t)lane == j) m += mj;
+    }
+  }
+  const uint32_t i = b0 + (uint32_t)lane;
+  if (i < n) {
+    node_coords(X, F[i], x.vt, x.nt);
+    for (int q = 0; q < op.ng; ++q) {
+      const DgdGroup& G = x.Gs[op.g0 + q];
+      if (G.fast && G.points > 0) m += ap_setup(x, G, R, S, lane, false) * (uint64_t)G.nop;
+    }
+  }
+  return m;
+}
+
 // One op of the walk (ops in reverse SSA order): the op's nodes from its
 // frontier, each node's edge count, the scan, then the edges and the
 // non-leaf children.  *nb and *eb are the location's node and edge counts
@@ -1793,15 +1829,15 @@ DGC bool dag_op(C& c, const DagCtx& x, const DgdOp& op, uint32_t* NC, const Slot
     return false;
   }
   uint32_t* F = (uint32_t*)(x.area + X.lds);
-  const uint32_t n = sort_unique(c, F, got, (uint32_t)X.cap);
+  const uint32_t n = sort_unique(c, F, got);
   if (MODE == DAG_FILL) {
     for (uint32_t i = (uint32_t)tid; i < n; i += (uint32_t)nt)
       if (nb + i < o.room_nodes) c.store(&o.nodes[nb + i], X.gid + F[i]);
   }
   const int R = X.rank;
-  bool any_box = false;
-  for (int q = 0; q < op.ng; ++q) any_box = any_box || (!x.Gs[op.g0 + q].fast && x.Gs[op.g0 + q].points > 0);
-  // Edge count of every node.
+  // Edge counts: per node for pointwise ops, per batch of L nodes (one wave's
+  // lanes) otherwise; a node's first edge is then its batch's offset plus a
+  // wave scan of the batch's node counts.
   if (op.pointwise) {
     for (uint32_t i = (uint32_t)tid; i < n; i += (uint32_t)nt) {
       node_coords(X, F[i], x.vt, nt);
@@ -1809,85 +1845,67 @@ DGC bool dag_op(C& c, const DagCtx& x, const DgdOp& op, uint32_t* NC, const Slot
     }
   } else {
     for (uint32_t b0 = (uint32_t)(wv * L); b0 < n; b0 += (uint32_t)(W * L)) {
-      const uint32_t i = b0 + (uint32_t)lane;
-      const bool has = i < n;
-      uint64_t m = 0;
-      if (any_box) {
-        for (uint32_t j = 0; j < (uint32_t)L && b0 + j < n; ++j) {
-          node_coords(X, F[b0 + j], x.vt, nt);
-          uint64_t mj = 0;
-          for (int q = 0; q < op.ng; ++q) {
-            const DgdGroup& G = x.Gs[op.g0 + q];
-            if (!G.fast && G.points > 0) mj += box_group(c, x, G, R, 0, o, false, false);
-          }
-          if ((uint32_t)lane == j) m += mj;
-        }
-      }
-      if (has) {
-        node_coords(X, F[i], x.vt, nt);
-        for (int q = 0; q < op.ng; ++q) {
-          const DgdGroup& G = x.Gs[op.g0 + q];
-          if (G.fast && G.points > 0) m += ap_setup(x, G, R, S, lane) * (uint64_t)G.nop;
-        }
-        if (m > 0xFFFFFFFFull) *x.err |= DGP_ERR_OVERFLOW;
-        NC[i] = (uint32_t)m;
-      }
+      const uint64_t m = batch_node_count(c, x, op, X, F, n, b0, R, S);
+      const uint64_t tot = c.wave_sum64(m);
+      if (tot > 0xFFFFFFFFull) *x.err |= DGP_ERR_OVERFLOW;
+      if (lane == 0) NC[b0 / (uint32_t)L] = (uint32_t)tot;
     }
   }
   c.sync();
-  const uint64_t total = block_scan(c, NC, n);
+  const uint32_t ncount = op.pointwise ? n : (n + (uint32_t)L - 1) / (uint32_t)L;
+  const uint64_t total = block_scan(c, NC, ncount);
   if (eb + total > 0xFFFFFFFFull) {
     *x.err |= DGP_ERR_OVERFLOW;
     return false;
   }
-  if (MODE == DAG_FILL) {
-    for (uint32_t i = (uint32_t)tid; i < n; i += (uint32_t)nt)
-      if (nb + i < o.room_nodes) c.store(&o.node_edge[nb + i], (uint32_t)(eb + NC[i]));
-  }
   // The edges, and the non-leaf children.
   const bool emit = MODE == DAG_FILL, append = op.nonleaf != 0;
-  if (emit || append) {
-    if (op.pointwise) {
-      for (uint32_t i = (uint32_t)tid; i < n; i += (uint32_t)nt) {
+  if (op.pointwise) {
+    for (uint32_t i = (uint32_t)tid; i < n; i += (uint32_t)nt) {
+      if (MODE == DAG_FILL && nb + i < o.room_nodes) c.store(&o.node_edge[nb + i], (uint32_t)(eb + NC[i]));
+      if (emit || append) {
         node_coords(X, F[i], x.vt, nt);
         pointwise_node(c, x, op, eb + NC[i], o, emit, append);
       }
-    } else {
-      for (uint32_t b0 = (uint32_t)(wv * L); b0 < n; b0 += (uint32_t)(W * L)) {
-        const uint32_t i = b0 + (uint32_t)lane;
-        const bool has = i < n;
-        uint64_t gpos = has ? eb + NC[i] : 0ull;
-        for (int q = 0; q < op.ng; ++q) {
-          const DgdGroup& G = x.Gs[op.g0 + q];
-          if (G.points == 0) continue;
-          if (G.fast) {
-            uint32_t Pj = 0;
-            if (has) {
-              node_coords(X, F[i], x.vt, nt);
-              Pj = (uint32_t)ap_setup(x, G, R, S, lane);
-              S.glo(lane) = (uint32_t)gpos;
-              S.ghi(lane) = (uint32_t)(gpos >> 32);
-            }
-            // Nodes with at least half a wave of points node by node, the
-            // others flattened across the lanes.
-            const bool big = Pj >= (uint32_t)((L + 1) / 2);
-            const uint64_t mask = c.ballot(big);
-            c.wave_sync();
-            const bool done = mask != 0 && emit_nodes(c, x, G, S, mask, o, emit, append);
-            flat_emit(c, x, G, S, WP, done && big ? 0u : Pj, o, emit, append);
-            gpos += (uint64_t)Pj * (uint64_t)G.nop;
-          } else {
+    }
+  } else if (emit || append) {
+    for (uint32_t b0 = (uint32_t)(wv * L); b0 < n; b0 += (uint32_t)(W * L)) {
+      const uint32_t i = b0 + (uint32_t)lane;
+      const bool has = i < n;
+      const uint64_t m = batch_node_count(c, x, op, X, F, n, b0, R, S);
+      uint32_t tot;
+      uint64_t gpos = eb + NC[b0 / (uint32_t)L] + c.wave_scan((uint32_t)m, &tot);
+      if (MODE == DAG_FILL && has && nb + i < o.room_nodes) c.store(&o.node_edge[nb + i], (uint32_t)gpos);
+      for (int q = 0; q < op.ng; ++q) {
+        const DgdGroup& G = x.Gs[op.g0 + q];
+        if (G.points == 0) continue;
+        if (G.fast) {
+          uint32_t Pj = 0;
+          if (has) {
+            node_coords(X, F[i], x.vt, nt);
+            Pj = (uint32_t)ap_setup(x, G, R, S, lane, true);
             S.glo(lane) = (uint32_t)gpos;
             S.ghi(lane) = (uint32_t)(gpos >> 32);
-            c.wave_sync();
-            for (uint32_t j = 0; j < (uint32_t)L && b0 + j < n; ++j) {
-              node_coords(X, F[b0 + j], x.vt, nt);
-              const uint64_t gj = ((uint64_t)S.ghi((int)j) << 32) | S.glo((int)j);
-              const uint64_t mj = box_group(c, x, G, R, gj, o, emit, append);
-              if ((uint32_t)lane == j) gpos += mj;
-            }
-            c.wave_sync();
           }
+          // Nodes with at least four waves of points node by node, the
+          // others flattened across the lanes.
+          const bool big = Pj >= 4u * (uint32_t)L;
+          const uint64_t mask = c.ballot(big);
+          c.wave_sync();
+          const bool done = mask != 0 && emit_nodes(c, x, G, S, mask, o, emit, append);
+          flat_emit(c, x, G, S, WP, done && big ? 0u : Pj, o, emit, append);
+          gpos += (uint64_t)Pj * (uint64_t)G.nop;
+        } else {
+          S.glo(lane) = (uint32_t)gpos;
+          S.ghi(lane) = (uint32_t)(gpos >> 32);
+          c.wave_sync();
+          for (uint32_t j = 0; j < (uint32_t)L && b0 + j < n; ++j) {
+            node_coords(X, F[b0 + j], x.vt, nt);
+            const uint64_t gj = ((uint64_t)S.ghi((int)j) << 32) | S.glo((int)j);
+            const uint64_t mj = box_group(c, x, G, R, gj, o, emit, append);
+            if ((uint32_t)lane == j) gpos += mj;
+          }
+          c.wave_sync();
         }
       }
     }

@@ -91,12 +91,6 @@ int64_t mod_inverse(int64_t a, int64_t m) {
   fail(DG_E_UNSUPPORTED_OP, "no modular inverse");
 }
 
-uint64_t pow2_at_least(uint64_t v) {
-  uint64_t p = 1;
-  while (p < v) p <<= 1;
-  return p;
-}
-
 }  // namespace
 
 DagProgram compile_dag(const GraphIR& g, int nthreads) {
@@ -138,9 +132,10 @@ DagProgram compile_dag(const GraphIR& g, int nthreads) {
     }
   }
 
-  // Layout of one location's LDS area: frontiers (u32 entries, capacity a
-  // power of two for the in-place sort), then one counter per tensor, then
-  // the per-thread variable tables.
+  // Layout of one location's LDS area: frontiers (u32 entries, sorted in
+  // place), then one counter per tensor, the per-thread variable tables, the
+  // per-node edge counts, the per-thread node slots and the per-wave prefix
+  // arrays.
   std::vector<DgdTensor> T(nt);
   uint64_t lds = 0;
   for (int t = 0; t < nt; ++t) {
@@ -160,15 +155,23 @@ DagProgram compile_dag(const GraphIR& g, int nthreads) {
     }
     d.lds = -1;
     if (!d.leaf && appends[t] > 0) {
-      const uint64_t cap = pow2_at_least(appends[t]);
+      const uint64_t cap = appends[t];
       if (cap > (1u << 20)) fail(DG_E_CAPACITY, "DAG frontier of '" + x.name + "' exceeds 2^20 elements");
       d.cap = (int32_t)cap;
       d.lds = (int32_t)lds;
       lds += 4 * cap;
     }
   }
-  int64_t ncount_cap = 0;
-  for (int t = 0; t < nt; ++t) ncount_cap = std::max<int64_t>(ncount_cap, T[t].cap);
+  // Edge counts: one per node of a pointwise op, one per batch of `lanes`
+  // nodes otherwise.
+  int64_t ncount_cap = 1;
+  for (const OpNode& op : g.ops) {
+    bool pointwise = true;
+    for (const ReadGroup& G : op.groups)
+      if (!G.wlo.empty()) pointwise = false;
+    const int64_t cap = T[op.out].cap;
+    ncount_cap = std::max<int64_t>(ncount_cap, pointwise ? cap : (cap + lanes - 1) / lanes);
+  }
   const uint64_t count_off = lds;
   lds += 4 * (uint64_t)nt;
   lds = (lds + 7) & ~7ull;
@@ -277,11 +280,10 @@ DagProgram compile_dag(const GraphIR& g, int nthreads) {
     for (const ReadGroup& G : op.groups)
       if (!G.wlo.empty()) d.pointwise = 0;
   }
-  // Per-thread node slots (per window variable: first value, count and a
-  // 64-bit quotient magic; per operand: element index at the first point;
-  // then the point count and the 64-bit first edge), then one prefix word
-  // per lane of every wave.
-  const int slot_words = 4 * max_win + max_opnd + 3;
+  // Per-thread node slots (per window variable: first value and count; per
+  // operand: element index at the first point; the 64-bit first edge), then
+  // one prefix word per lane of every wave.
+  const int slot_words = 2 * max_win + max_opnd + 2;
   const uint64_t slot_off = lds;
   lds += 4ull * (uint64_t)slot_words * (uint64_t)nthreads;
   const uint64_t wave_off = lds;

@@ -36,6 +36,7 @@ struct HostCtx {
     return 0u;
   }
   uint64_t ballot(bool f) const { return f ? 1u : 0u; }
+  uint64_t wave_sum64(uint64_t v) const { return v; }
   uint32_t wave_scan(uint32_t v, uint32_t* total) const {
     *total = v;
     return 0u;

@@ -64,6 +64,12 @@ struct DevCtx {
     return before + x - v;
   }
   DGC uint64_t ballot(bool f) const { return __ballot(f); }
+  // Sum of v over the wave, in every lane (no barrier).
+  DGC uint64_t wave_sum64(uint64_t v) const {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+    return v;
+  }
   // Exclusive sum of v over lower lanes of the wave, and the wave total
   // (no barrier).
   DGC uint32_t wave_scan(uint32_t v, uint32_t* total) const {

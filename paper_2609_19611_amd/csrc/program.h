@@ -171,7 +171,7 @@ struct DgpHeader {
 struct DgdTensor {
   int32_t rank;
   int32_t leaf;    // 1: a leaf (a variable; never expanded)
-  int32_t cap;     // frontier capacity in entries (a power of two; 0 when never reached)
+  int32_t cap;     // frontier capacity in entries (0 when never reached)
   int32_t lds;     // byte offset of the frontier in the location's LDS area
   uint32_t gid;    // global id of element 0
   int32_t numel;
@@ -235,10 +235,10 @@ struct DgdHeader {
   int32_t vars_off;   // byte offset of the per-thread variable tables (max_vars words per thread)
   int32_t max_vars;   // output plus window variables of the largest group
   int32_t lds_bytes;  // LDS area of one location
-  int32_t ncount_off; // byte offset of the per-node edge counts (ncount_cap words)
-  int32_t ncount_cap; // largest frontier capacity
+  int32_t ncount_off; // byte offset of the edge counts (ncount_cap words)
+  int32_t ncount_cap; // per node of a pointwise op, per wave-wide batch of nodes otherwise
   int32_t slot_off;   // byte offset of the per-thread node slots (slot_words words per thread)
-  int32_t slot_words; // 3 per window variable, 1 per operand, 3 more (see core.h)
+  int32_t slot_words; // 2 per window variable, 1 per operand, 2 more (see core.h)
   int32_t wave_off;   // byte offset of the per-wave prefix arrays (one word per lane)
   int32_t max_win;    // window variables and operands of the largest fast group
   int32_t max_opnd;
