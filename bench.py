@@ -84,21 +84,24 @@ def copy_calibration(gib, steps, warmup):
 
 KERNEL_SOURCES = ["program.h", "core.h", "kernels_dev.h", "jit_source.cpp", "jit.cpp", "compile.cpp", "graph.cpp"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "dg_enumerate_hbm_traffic.txt")
+DAG_SOURCES = ["program.h", "core.h", "kernels_dev.h", "dag_program.h", "dag_core.h", "dag.cpp", "kernels.hip",
+               "graph.cpp"]
+DAG_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "dg_dag_fill_hbm_traffic.txt")
 
 
-def measured_traffic(workload):
-    """HBM bytes per dg_enumerate launch from the committed rocprofv3 counter
-    summary (FETCH_SIZE and WRITE_SIZE scaled by a copy of known size), or
-    None when the kernel sources have changed since it was taken."""
+def measured_traffic(workload, path=TRAFFIC_FILE, sources=KERNEL_SOURCES):
+    """HBM bytes per launch of the dominant kernel from a committed rocprofv3
+    counter summary (FETCH_SIZE and WRITE_SIZE scaled by a copy of known
+    size), or None when the kernel sources have changed since it was taken."""
     import hashlib
-    if not os.path.exists(TRAFFIC_FILE):
+    if not os.path.exists(path):
         return None
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in sources:
         with open(os.path.join(ROOT, "paper_2609_19611_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     stored, traffic = None, None
-    for line in open(TRAFFIC_FILE):
+    for line in open(path):
         parts = line.split()
         if len(parts) == 2 and parts[0] == "kernel_sources_sha256":
             stored = parts[1]
@@ -241,11 +244,12 @@ def dag_bench(args, B, g, cfg, locs, text):
         "scaling": "weak", "vs_baseline": None, "dtype": "u32",
         "data": "synthetic (shapes only; footprints are data independent)",
         "config": {"workload": f"{args.workload}: " + cfg["desc"] + " (expression DAGs)", "locations": n,
-                   "nodes_per_step": nn, "edges_per_step": ne, "locations_per_s": n / (elapsed / args.steps),
-                   "dag_lds_bytes": None},
+                   "nodes_per_step": nn, "edges_per_step": ne, "locations_per_s": n / (elapsed / args.steps)},
         "roofline": {"bound": "hbm", "kernel": "k_dag_fill", "achieved": achieved, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None, "kernel_ms": fill_ms,
-                     "algorithmic_bytes": alg},
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": measured_traffic(args.workload, DAG_TRAFFIC_FILE, DAG_SOURCES),
+                     "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE x2 + WRITE_SIZE x1)",
+                     "kernel_ms": fill_ms, "algorithmic_bytes": alg},
     }
     if not args.no_cpu_baseline:
         import oracle

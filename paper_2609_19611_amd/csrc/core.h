@@ -1225,733 +1225,4 @@ DGC uint32_t location_compare(C& c, const uint8_t* blob_a, const uint8_t* blob_b
   return status;
 }
 
-// ---------------------------------------------------------------------------
-// Expression DAG of res(y[l]) for one location (program.h, DgdHeader).
-//
-// Frontiers of the non-leaf tensors live in the LDS area: a consumer node
-// appends every non-leaf element it references to the operand's candidate
-// list; when the ops are walked back to that tensor's producer (reverse SSA
-// order, so every consumer has been walked), the list is sorted and made
-// unique, giving the tensor's nodes in ascending order.  A node's edges are
-// its (group, window point, operand) references in order; a point whose
-// operand indices are not all valid is skipped.
-//
-// Per op, every node's edge count is taken first and an exclusive scan over
-// the nodes gives each node its first edge; the edges are then written at
-// known positions.  Pointwise ops give one thread a node; the others give
-// one wave a node and take each group per variable (the product of per-
-// variable valid sets, no per-point test) or point by point (wave-level
-// compaction), as the compiler decided.
-// ---------------------------------------------------------------------------
-enum : int { DAG_COUNT = 0, DAG_FILL = 1 };
-
-struct DagOut {
-  uint32_t* nodes;      // node ids (global element ids)
-  uint32_t* node_edge;  // first edge of each node, relative to the location's first edge
-  uint32_t* edges;      // child ids
-  uint32_t* mults;      // multiplicities
-  uint64_t room_nodes, room_edges;
-};
-
-// Sorts the first n entries of f and keeps one of each value; returns the
-// number kept.  Bitonic network whose comparators all put the smaller value
-// at the lower index (each merge starts by comparing mirrored positions), so
-// positions at or past n act as +infinity and their comparators are
-// skipped: any n, sorted in place.  All threads call it.
-template <class C>
-DGC uint32_t sort_unique(C& c, uint32_t* f, uint32_t n) {
-  const int tid = c.tid(), nt = c.nthreads();
-  for (uint32_t k = 2; (k >> 1) < n; k <<= 1) {
-    for (uint32_t j = k >> 1; j > 0; j >>= 1) {
-      const uint32_t mask = j == (k >> 1) ? k - 1 : j;  // mirror within the block first
-      for (uint32_t i = (uint32_t)tid; i < n; i += (uint32_t)nt) {
-        const uint32_t l = i ^ mask;
-        if (l > i && l < n) {
-          const uint32_t a = f[i], b = f[l];
-          if (a > b) {
-            f[i] = b;
-            f[l] = a;
-          }
-        }
-      }
-      c.sync();
-    }
-  }
-  c.sync();
-  uint32_t kept = 0;
-  for (uint32_t b0 = 0; b0 < n; b0 += (uint32_t)nt) {
-    const uint32_t i = b0 + (uint32_t)tid;
-    uint32_t v = 0;
-    bool keep = false;
-    if (i < n) {
-      v = f[i];
-      keep = i == 0 || f[i - 1] != v;
-    }
-    uint32_t tot;
-    const uint32_t pre = c.prefix(keep, &tot);
-    if (keep) f[kept + pre] = v;
-    kept += tot;
-    c.sync();
-  }
-  return kept;
-}
-
-// Replaces a[0..n) by its exclusive running sums and returns the total.
-// All threads call it; ends past a barrier.
-template <class C>
-DGC uint64_t block_scan(C& c, uint32_t* a, uint32_t n) {
-  const uint32_t nt = (uint32_t)c.nthreads(), tid = (uint32_t)c.tid();
-  const uint32_t per = (n + nt - 1) / nt;
-  const uint32_t b = tid * per < n ? tid * per : n;
-  const uint32_t e = b + per < n ? b + per : n;
-  uint64_t s = 0;
-  for (uint32_t j = b; j < e; ++j) s += a[j];
-  uint64_t tot;
-  uint64_t run = c.scan_add(s, &tot);
-  for (uint32_t j = b; j < e; ++j) {
-    const uint32_t v = a[j];
-    a[j] = (uint32_t)run;
-    run += v;
-  }
-  c.sync();
-  return tot;
-}
-
-// Quotient of a 32-bit n by a tensor dim from its magic number m (0: the
-// dim is 1): the high 64 bits of n * m, from two 32 x 32-bit products.
-DGC uint32_t magic_div(uint32_t n, uint64_t m) {
-  if (!m) return n;
-  const uint64_t lo = (uint64_t)n * (uint32_t)m;
-  const uint64_t hi = (uint64_t)n * (uint32_t)(m >> 32);
-  return (uint32_t)((hi + (lo >> 32)) >> 32);
-}
-
-// n / d and n % d for n < 2^16 (digits of a lane index or the wave width).
-DGC uint32_t small_divmod(uint32_t n, uint32_t d, uint32_t* r) {
-#if defined(__HIP_DEVICE_COMPILE__)
-  uint32_t q = (uint32_t)((float)n * __builtin_amdgcn_rcpf((float)d));
-  int32_t rr = (int32_t)n - (int32_t)(q * d);
-  if (rr < 0) {
-    --q;
-    rr += (int32_t)d;
-  } else if (rr >= (int32_t)d) {
-    ++q;
-    rr -= (int32_t)d;
-  }
-  *r = (uint32_t)rr;
-  return q;
-#else
-  *r = n % d;
-  return n / d;
-#endif
-}
-
-// Floor and ceiling of a / b for b > 0.
-DGC int32_t floor_div(int32_t a, int32_t b) { return fdiv(a, b); }
-DGC int32_t ceil_div(int32_t a, int32_t b) { return -fdiv(-a, b); }
-
-// Coordinates of element e of X into the calling thread's variables 0..R-1.
-DGC void node_coords(const DgdTensor& X, uint32_t e, int32_t* vt, int nt) {
-  for (int d = DGP_MAX_RANK - 1; d >= 0; --d) {
-    if (d < X.rank) {
-      const uint32_t q = magic_div(e, X.magic[d]);
-      vt[d * nt] = (int32_t)(e - q * (uint32_t)X.shape[d]);
-      e = q;
-    }
-  }
-}
-
-// Element index of operand P at the calling thread's variables; false if an
-// index is invalid.
-DGC bool operand_flat(const DgdOperand& P, const DgdTensor& Ta, const int32_t* vt, int nt, uint32_t* flat) {
-  uint32_t f = 0;
-  bool ok = true;
-  for (int d = 0; d < DGP_MAX_RANK; ++d) {
-    if (d < Ta.rank) {
-      int32_t v = 0;
-      ok = ifn_eval(P.idx[d], vt, nt, &v) && ok;
-      f += Ta.stride[d] * (uint32_t)v;
-    }
-  }
-  *flat = f;
-  return ok;
-}
-
-// An interval variable's index function at the node as c0 + k * w (w the
-// variable with index `wv`).
-DGC void ifn_linear(const DgpIFn& f, int wv, const int32_t* vt, int nt, int32_t* c0, int32_t* k) {
-  int32_t c = f.c, kk = 0;
-  for (int t = 0; t < DGP_MAX_FTERMS; ++t) {
-    if (t < f.nterm) {
-      if (f.var[t] == wv) {
-        kk = f.coef[t];
-      } else {
-        int32_t vv = vt[f.var[t] * nt];
-        if (f.vdiv[t] != 1) vv /= f.vdiv[t];
-        c += f.coef[t] * vv;
-      }
-    }
-  }
-  *c0 = c;
-  *k = kk;
-}
-
-// Appends element `flat` of non-leaf tensor t to its frontier.
-template <class C>
-DGC void dag_append(C& c, const DgdTensor& Tc, int t, uint32_t flat, uint8_t* area, uint32_t* cnt, uint32_t* err) {
-  const uint32_t slot = c.atomic_inc(&cnt[t]);
-  if (slot < (uint32_t)Tc.cap) ((uint32_t*)(area + Tc.lds))[slot] = flat;
-  else *err |= DGP_ERR_CAPACITY;
-}
-
-struct DagCtx {
-  const DgdHeader* h;
-  const DgdTensor* T;
-  const DgdGroup* Gs;
-  const DgdOperand* Ps;
-  uint8_t* area;
-  uint32_t* cnt;
-  int32_t* vt;
-  int nt;
-  uint32_t* err;
-};
-
-// One thread, one node of a pointwise op: the node's edges (written from
-// `pos` when `emit`), non-leaf children appended when `append`; returns the
-// number of edges.  The node's coordinates are in the thread's variables.
-template <class C>
-DGC uint32_t pointwise_node(C& c, const DagCtx& x, const DgdOp& op, uint64_t pos, const DagOut& o, bool emit,
-                            bool append) {
-  uint32_t k = 0;
-  for (int q = 0; q < op.ng; ++q) {
-    const DgdGroup& G = x.Gs[op.g0 + q];
-    if (G.points == 0) continue;
-    bool ok = true;
-    for (int a = 0; a < G.nop; ++a) {
-      const DgdOperand& P = x.Ps[G.op0 + a];
-      uint32_t f;
-      ok = operand_flat(P, x.T[P.tensor], x.vt, x.nt, &f) && ok;
-    }
-    if (!ok) continue;
-    for (int a = 0; a < G.nop; ++a) {
-      const DgdOperand& P = x.Ps[G.op0 + a];
-      const DgdTensor& Ta = x.T[P.tensor];
-      uint32_t f = 0;
-      operand_flat(P, Ta, x.vt, x.nt, &f);
-      if (emit && pos + k < o.room_edges) {
-        c.store(&o.edges[pos + k], Ta.gid + f);
-        c.store(&o.mults[pos + k], P.mult);
-      }
-      if (append && !Ta.leaf) dag_append(c, Ta, P.tensor, f, x.area, x.cnt, x.err);
-      ++k;
-    }
-  }
-  return k;
-}
-
-// Digits of v in the mixed radix len[0..Q) (last digit fastest, the first
-// one unbounded), for v < 2^16.
-DGC void radix_digits(uint32_t v, const uint32_t* len, int Q, uint32_t* dg) {
-  DG_UNROLL
-  for (int q = DGD_MAX_WIN - 1; q >= 1; --q) {
-    if (q < Q) {
-      uint32_t r;
-      v = small_divmod(v, len[q], &r);
-      dg[q] = r;
-    } else {
-      dg[q] = 0;
-    }
-  }
-  dg[0] = v;
-}
-
-// Adds the digits inc to dg (each digit below its radix, the first one
-// unbounded).
-DGC void radix_add(uint32_t* dg, const uint32_t* inc, const uint32_t* len, int Q) {
-  uint32_t carry = 0;
-  DG_UNROLL
-  for (int q = DGD_MAX_WIN - 1; q >= 1; --q) {
-    if (q < Q) {
-      const uint32_t t = dg[q] + inc[q] + carry;
-      carry = t >= len[q] ? 1u : 0u;
-      dg[q] = carry ? t - len[q] : t;
-    }
-  }
-  dg[0] += inc[0] + carry;
-}
-
-// Group G of the wave's node point by point over the whole window box: the
-// valid points are compacted within the wave; writes from `pos` when
-// `emit`, appends non-leaf children when `append`; returns the edge count.
-template <class C>
-DGC uint64_t box_group(C& c, const DagCtx& x, const DgdGroup& G, int R, uint64_t pos, const DagOut& o, bool emit,
-                       bool append) {
-  const int lane = c.lane(), L = c.lanes();
-  const int Q = G.nwin, nop = G.nop;
-  const uint64_t P = (uint64_t)G.points;
-  uint32_t len[DGD_MAX_WIN], dg[DGD_MAX_WIN], inc[DGD_MAX_WIN];
-  DG_UNROLL
-  for (int q = 0; q < DGD_MAX_WIN; ++q) len[q] = q < Q ? (uint32_t)(G.whi[q] - G.wlo[q]) : 1u;
-  radix_digits((uint32_t)lane, len, Q, dg);
-  radix_digits((uint32_t)L, len, Q, inc);
-  uint64_t run = 0;
-  for (uint64_t p0 = 0; p0 < P; p0 += (uint64_t)L) {
-    bool ok = p0 + (uint64_t)lane < P;
-    if (ok) {
-      DG_UNROLL
-      for (int q = 0; q < DGD_MAX_WIN; ++q)
-        if (q < Q) x.vt[(R + q) * x.nt] = G.wlo[q] + (int32_t)dg[q];
-      for (int a = 0; a < G.nop; ++a) {
-        const DgdOperand& Pa = x.Ps[G.op0 + a];
-        uint32_t f;
-        ok = operand_flat(Pa, x.T[Pa.tensor], x.vt, x.nt, &f) && ok;
-      }
-    }
-    uint32_t tot;
-    const uint32_t pre = c.wave_prefix(ok, &tot);
-    if (ok && (emit || append)) {
-      for (int a = 0; a < G.nop; ++a) {
-        const DgdOperand& Pa = x.Ps[G.op0 + a];
-        const DgdTensor& Ta = x.T[Pa.tensor];
-        uint32_t f = 0;
-        operand_flat(Pa, Ta, x.vt, x.nt, &f);
-        const uint64_t at = pos + (run + pre) * (uint64_t)nop + (uint64_t)a;
-        if (emit && at < o.room_edges) {
-          c.store(&o.edges[at], Ta.gid + f);
-          c.store(&o.mults[at], Pa.mult);
-        }
-        if (append && !Ta.leaf) dag_append(c, Ta, Pa.tensor, f, x.area, x.cnt, x.err);
-      }
-    }
-    run += tot;
-    radix_add(dg, inc, len, Q);
-  }
-  return run * (uint64_t)nop;
-}
-
-// Per-thread node slots (DgdHeader.slot_off, stride = block threads): per
-// window variable its first valid value and progression length (while
-// setting up: its bounds), per operand its element index at the first valid
-// point, and the node's 64-bit first edge of the group.
-struct Slots {
-  uint32_t* s;  // this wave's lane 0 column; lane j's column is s + j
-  int nt, MQ, MA;
-  DGC uint32_t& first(int j, int q) const { return s[(size_t)q * nt + j]; }
-  DGC uint32_t& len(int j, int q) const { return s[(size_t)(MQ + q) * nt + j]; }
-  DGC uint32_t& base(int j, int a) const { return s[(size_t)(2 * MQ + a) * nt + j]; }
-  DGC uint32_t& glo(int j) const { return s[(size_t)(2 * MQ + MA) * nt + j]; }
-  DGC uint32_t& ghi(int j) const { return s[(size_t)(2 * MQ + MA + 1) * nt + j]; }
-};
-
-DGC int32_t pmod(int32_t a, int32_t m) {
-  const int32_t r = a % m;
-  return r < 0 ? r + m : r;
-}
-
-// Progressions of group G at the calling thread's node (coordinates in its
-// variables): every window variable's first valid value and length and,
-// with `bases`, every operand's element index at the first point, in the
-// thread's slot column j.  Returns the number of valid points.
-DGC uint64_t ap_setup(const DagCtx& x, const DgdGroup& G, int R, const Slots& S, int j, bool bases) {
-  const int Q = G.nwin;
-  for (int q = 0; q < Q; ++q) {
-    S.first(j, q) = (uint32_t)G.wlo[q];
-    S.len(j, q) = (uint32_t)(G.whi[q] - 1);  // inclusive upper bound while constraining
-  }
-  bool bad = false;
-  for (int pi = 0; pi < G.npair; ++pi) {
-    const DgdPair pr = G.pair[pi];
-    const DgdOperand& P = x.Ps[G.op0 + pr.a];
-    const DgpIFn& f = P.idx[pr.d];
-    if (pr.q < 0) {
-      int32_t v;
-      if (!ifn_eval(f, x.vt, x.nt, &v)) bad = true;
-      continue;
-    }
-    const int q = pr.q;
-    int32_t c0, k;
-    ifn_linear(f, R + q, x.vt, x.nt, &c0, &k);
-    const int32_t top = f.mode == 1 ? f.s * (f.size - 1) : f.size - 1;
-    int32_t l2, h2;
-    if (k > 0) {
-      l2 = ceil_div(-c0, k);
-      h2 = floor_div(top - c0, k);
-    } else {
-      l2 = ceil_div(c0 - top, -k);
-      h2 = floor_div(c0, -k);
-    }
-    if (l2 > (int32_t)S.first(j, q)) S.first(j, q) = (uint32_t)l2;
-    if (h2 < (int32_t)S.len(j, q)) S.len(j, q) = (uint32_t)h2;
-  }
-  if (bad) return 0;
-  uint64_t P = 1;
-  for (int q = 0; q < Q; ++q) {
-    const int32_t lo = (int32_t)S.first(j, q), hi = (int32_t)S.len(j, q), m = G.step[q];
-    int32_t first = lo;
-    if (m > 1) {
-      // The exact division c0 + k w = 0 (mod s): g = s / step must divide
-      // c0, then w = (-c0 / g) * inverse(k / g) (mod step).
-      const DgdPair pr = G.pair[G.mpair[q]];
-      const DgpIFn& f = x.Ps[G.op0 + pr.a].idx[pr.d];
-      int32_t c0, k;
-      ifn_linear(f, R + q, x.vt, x.nt, &c0, &k);
-      const int32_t g = f.s / m;
-      if (c0 % g != 0) return 0;
-      const int32_t r = (int32_t)(((int64_t)pmod(-(c0 / g), m) * G.minv[q]) % m);
-      first = lo + pmod(r - lo, m);
-    }
-    const uint32_t len = first <= hi ? (uint32_t)((hi - first) / m + 1) : 0u;
-    S.first(j, q) = (uint32_t)first;
-    S.len(j, q) = len;
-    P *= len;
-  }
-  if (P == 0 || !bases) return P;
-  for (int a = 0; a < G.nop; ++a) S.base(j, a) = x.T[x.Ps[G.op0 + a].tensor].gid;
-  for (int pi = 0; pi < G.npair; ++pi) {
-    const DgdPair pr = G.pair[pi];
-    const DgdOperand& P = x.Ps[G.op0 + pr.a];
-    const DgdTensor& Ta = x.T[P.tensor];
-    const DgpIFn& f = P.idx[pr.d];
-    int32_t v = 0;
-    if (pr.q < 0) {
-      ifn_eval(f, x.vt, x.nt, &v);
-    } else {
-      int32_t c0, k;
-      ifn_linear(f, R + pr.q, x.vt, x.nt, &c0, &k);
-      v = c0 + k * (int32_t)S.first(j, pr.q);
-      if (f.mode == 1) v /= f.s;
-    }
-    S.base(j, pr.a) += Ta.stride[pr.d] * (uint32_t)v;
-  }
-  return P;
-}
-
-// Writes group G's edges for the wave's batch of nodes: lane j's node has
-// Pj points (0 for none), set up in slot column j with its first edge.  The
-// points of the batch are taken flattened across the lanes: point t belongs
-// to the node whose prefix brackets it, and its operands go to that node's
-// first edge + p * nop + a.
-template <class C>
-DGC void flat_emit(C& c, const DagCtx& x, const DgdGroup& G, const Slots& S, uint32_t* WP, uint32_t Pj,
-                   const DagOut& o, bool emit, bool append) {
-  const int lane = c.lane(), L = c.lanes();
-  const int Q = G.nwin, nop = G.nop;
-  uint32_t T;
-  WP[lane] = c.wave_scan(Pj, &T);
-  c.wave_sync();
-  for (uint64_t t0 = 0; t0 < (uint64_t)T; t0 += (uint64_t)L) {
-    const uint64_t tt = t0 + (uint64_t)lane;
-    if (tt < (uint64_t)T) {
-      const uint32_t t = (uint32_t)tt;
-      int j = 0;
-      for (int st = L >> 1; st >= 1; st >>= 1)
-        if (WP[j + st] <= t) j += st;
-      const uint32_t p0 = t - WP[j];
-      uint32_t p = p0, idx[DGD_MAX_WIN];
-      DG_UNROLL
-      for (int q = DGD_MAX_WIN - 1; q >= 1; --q) {
-        idx[q] = 0;
-        if (q < Q) {
-          const uint32_t len = S.len(j, q);
-          uint32_t r, quo;
-          if (p < 65536u) {
-            quo = small_divmod(p, len, &r);
-          } else {
-            quo = p / len;
-            r = p - quo * len;
-          }
-          idx[q] = r;
-          p = quo;
-        }
-      }
-      idx[0] = p;
-      const uint64_t at0 = (((uint64_t)S.ghi(j) << 32) | S.glo(j)) + (uint64_t)p0 * (uint64_t)nop;
-      for (int a = 0; a < nop; ++a) {
-        const DgdOperand& Pa = x.Ps[G.op0 + a];
-        uint32_t child = S.base(j, a);
-        DG_UNROLL
-        for (int q = 0; q < DGD_MAX_WIN; ++q)
-          if (q < Q) child += G.astep[a][q] * idx[q];
-        const uint64_t at = at0 + (uint64_t)a;
-        if (emit && at < o.room_edges) {
-          c.store(&o.edges[at], child);
-          c.store(&o.mults[at], Pa.mult);
-        }
-        if (append) {
-          const DgdTensor& Ta = x.T[Pa.tensor];
-          if (!Ta.leaf) dag_append(c, Ta, Pa.tensor, child - Ta.gid, x.area, x.cnt, x.err);
-        }
-      }
-    }
-  }
-  c.wave_sync();
-}
-
-// Writes group G's edges of the batch node in lane column j (a node with
-// at least four waves of points): the wave covers the node's points with
-// its lanes, the digits of each lane's point advancing by the wave width
-// with carries.  NOP operands and Q window variables are compile-time
-// constants, so the steps stay in registers.
-template <class C, int NOP, int Q>
-DGC void node_emit(C& c, const DagCtx& x, const DgdGroup& G, const Slots& S, int j, const DagOut& o, bool emit,
-                   bool append) {
-  const int lane = c.lane(), L = c.lanes();
-  uint32_t len[DGD_MAX_WIN], dg[DGD_MAX_WIN], inc[DGD_MAX_WIN];
-  uint64_t P = 1;
-  DG_UNROLL
-  for (int q = 0; q < DGD_MAX_WIN; ++q) {
-    len[q] = q < Q ? S.len(j, q) : 1u;
-    P *= len[q];
-  }
-  uint32_t base[NOP], mult[NOP], as[NOP][Q > 0 ? Q : 1];
-  bool leaf[NOP];
-  DG_UNROLL
-  for (int a = 0; a < NOP; ++a) {
-    const DgdOperand& Pa = x.Ps[G.op0 + a];
-    base[a] = S.base(j, a);
-    mult[a] = Pa.mult;
-    leaf[a] = x.T[Pa.tensor].leaf != 0;
-    DG_UNROLL
-    for (int q = 0; q < Q; ++q) as[a][q] = G.astep[a][q];
-  }
-  const uint64_t at0 = ((uint64_t)S.ghi(j) << 32) | S.glo(j);
-  radix_digits((uint32_t)lane, len, Q, dg);
-  radix_digits((uint32_t)L, len, Q, inc);
-  for (uint64_t p0 = 0; p0 < P; p0 += (uint64_t)L) {
-    const uint64_t p = p0 + (uint64_t)lane;
-    if (p < P) {
-      const uint64_t at = at0 + p * (uint64_t)NOP;
-      DG_UNROLL
-      for (int a = 0; a < NOP; ++a) {
-        uint32_t child = base[a];
-        DG_UNROLL
-        for (int q = 0; q < Q; ++q) child += as[a][q] * dg[q];
-        if (emit && at + a < o.room_edges) {
-          c.store(&o.edges[at + a], child);
-          c.store(&o.mults[at + a], mult[a]);
-        }
-        if (append && !leaf[a]) {
-          const DgdOperand& Pa = x.Ps[G.op0 + a];
-          const DgdTensor& Ta = x.T[Pa.tensor];
-          dag_append(c, Ta, Pa.tensor, child - Ta.gid, x.area, x.cnt, x.err);
-        }
-      }
-    }
-    radix_add(dg, inc, len, Q);
-  }
-}
-
-// Node-major emission of the batch nodes in `mask` (lane columns) when the
-// group's shape has a compiled emitter; false when it has none.
-template <class C>
-DGC bool emit_nodes(C& c, const DagCtx& x, const DgdGroup& G, const Slots& S, uint64_t mask, const DagOut& o,
-                    bool emit, bool append) {
-  const int key = G.nop * 16 + G.nwin;
-  switch (key) {
-    case 0x11: case 0x12: case 0x13: case 0x14:
-    case 0x21: case 0x22: case 0x23: case 0x24:
-    case 0x31: case 0x32: case 0x33: case 0x34:
-      break;
-    default:
-      return false;
-  }
-  while (mask) {
-    const int j = (int)__builtin_ctzll(mask);
-    mask &= mask - 1;
-    switch (key) {
-      case 0x11: node_emit<C, 1, 1>(c, x, G, S, j, o, emit, append); break;
-      case 0x12: node_emit<C, 1, 2>(c, x, G, S, j, o, emit, append); break;
-      case 0x13: node_emit<C, 1, 3>(c, x, G, S, j, o, emit, append); break;
-      case 0x14: node_emit<C, 1, 4>(c, x, G, S, j, o, emit, append); break;
-      case 0x21: node_emit<C, 2, 1>(c, x, G, S, j, o, emit, append); break;
-      case 0x22: node_emit<C, 2, 2>(c, x, G, S, j, o, emit, append); break;
-      case 0x23: node_emit<C, 2, 3>(c, x, G, S, j, o, emit, append); break;
-      case 0x24: node_emit<C, 2, 4>(c, x, G, S, j, o, emit, append); break;
-      case 0x31: node_emit<C, 3, 1>(c, x, G, S, j, o, emit, append); break;
-      case 0x32: node_emit<C, 3, 2>(c, x, G, S, j, o, emit, append); break;
-      case 0x33: node_emit<C, 3, 3>(c, x, G, S, j, o, emit, append); break;
-      default:   node_emit<C, 3, 4>(c, x, G, S, j, o, emit, append); break;
-    }
-  }
-  return true;
-}
-
-// Edge count of the calling lane's node in the wave's batch starting at
-// node b0 (0 past the end): the box groups node by node across the wave,
-// the progression groups one node per lane.  Called by all lanes of the
-// wave; leaves every lane's variables at its own node.
-template <class C>
-DGC uint64_t batch_node_count(C& c, const DagCtx& x, const DgdOp& op, const DgdTensor& X, const uint32_t* F,
-                              uint32_t n, uint32_t b0, int R, const Slots& S) {
-  const int lane = c.lane(), L = c.lanes();
-  uint64_t m = 0;
-  bool any_box = false;
-  for (int q = 0; q < op.ng; ++q) any_box = any_box || (!x.Gs[op.g0 + q].fast && x.Gs[op.g0 + q].points > 0);
-  if (any_box) {
-    for (uint32_t j = 0; j < (uint32_t)L && b0 + j < n; ++j) {
-      node_coords(X, F[b0 + j], x.vt, x.nt);
-      uint64_t mj = 0;
-      for (int q = 0; q < op.ng; ++q) {
-        const DgdGroup& G = x.Gs[op.g0 + q];
-        if (!G.fast && G.points > 0) mj += box_group(c, x, G, R, 0, DagOut{}, false, false);
-      }
-      if ((uint32_t)lane == j) m += mj;
-    }
-  }
-  const uint32_t i = b0 + (uint32_t)lane;
-  if (i < n) {
-    node_coords(X, F[i], x.vt, x.nt);
-    for (int q = 0; q < op.ng; ++q) {
-      const DgdGroup& G = x.Gs[op.g0 + q];
-      if (G.fast && G.points > 0) m += ap_setup(x, G, R, S, lane, false) * (uint64_t)G.nop;
-    }
-  }
-  return m;
-}
-
-// One op of the walk (ops in reverse SSA order): the op's nodes from its
-// frontier, each node's edge count, the scan, then the edges and the
-// non-leaf children.  *nb and *eb are the location's node and edge counts
-// so far.  Returns false when the location stops with an error.  Called by
-// every thread of the block.
-template <class C, int MODE>
-DGC bool dag_op(C& c, const DagCtx& x, const DgdOp& op, uint32_t* NC, const Slots& S, uint32_t* WP, const DagOut& o,
-                uint64_t* nb_, uint64_t* eb_) {
-  const int tid = c.tid(), nt = c.nthreads();
-  const int lane = c.lane(), wv = c.wave(), W = c.nwaves(), L = c.lanes();
-  const DgdTensor& X = x.T[op.out];
-  const uint32_t got = x.cnt[op.out];
-  if (got == 0) return true;
-  const uint64_t nb = *nb_, eb = *eb_;
-  c.sync();  // every thread has read the counter
-  if (got > (uint32_t)X.cap) {
-    *x.err |= DGP_ERR_CAPACITY;
-    return false;
-  }
-  uint32_t* F = (uint32_t*)(x.area + X.lds);
-  const uint32_t n = sort_unique(c, F, got);
-  if (MODE == DAG_FILL) {
-    for (uint32_t i = (uint32_t)tid; i < n; i += (uint32_t)nt)
-      if (nb + i < o.room_nodes) c.store(&o.nodes[nb + i], X.gid + F[i]);
-  }
-  const int R = X.rank;
-  // Edge counts: per node for pointwise ops, per batch of L nodes (one wave's
-  // lanes) otherwise; a node's first edge is then its batch's offset plus a
-  // wave scan of the batch's node counts.
-  if (op.pointwise) {
-    for (uint32_t i = (uint32_t)tid; i < n; i += (uint32_t)nt) {
-      node_coords(X, F[i], x.vt, nt);
-      NC[i] = pointwise_node(c, x, op, 0, o, false, false);
-    }
-  } else {
-    for (uint32_t b0 = (uint32_t)(wv * L); b0 < n; b0 += (uint32_t)(W * L)) {
-      const uint64_t m = batch_node_count(c, x, op, X, F, n, b0, R, S);
-      const uint64_t tot = c.wave_sum64(m);
-      if (tot > 0xFFFFFFFFull) *x.err |= DGP_ERR_OVERFLOW;
-      if (lane == 0) NC[b0 / (uint32_t)L] = (uint32_t)tot;
-    }
-  }
-  c.sync();
-  const uint32_t ncount = op.pointwise ? n : (n + (uint32_t)L - 1) / (uint32_t)L;
-  const uint64_t total = block_scan(c, NC, ncount);
-  if (eb + total > 0xFFFFFFFFull) {
-    *x.err |= DGP_ERR_OVERFLOW;
-    return false;
-  }
-  // The edges, and the non-leaf children.
-  const bool emit = MODE == DAG_FILL, append = op.nonleaf != 0;
-  if (op.pointwise) {
-    for (uint32_t i = (uint32_t)tid; i < n; i += (uint32_t)nt) {
-      if (MODE == DAG_FILL && nb + i < o.room_nodes) c.store(&o.node_edge[nb + i], (uint32_t)(eb + NC[i]));
-      if (emit || append) {
-        node_coords(X, F[i], x.vt, nt);
-        pointwise_node(c, x, op, eb + NC[i], o, emit, append);
-      }
-    }
-  } else if (emit || append) {
-    for (uint32_t b0 = (uint32_t)(wv * L); b0 < n; b0 += (uint32_t)(W * L)) {
-      const uint32_t i = b0 + (uint32_t)lane;
-      const bool has = i < n;
-      const uint64_t m = batch_node_count(c, x, op, X, F, n, b0, R, S);
-      uint32_t tot;
-      uint64_t gpos = eb + NC[b0 / (uint32_t)L] + c.wave_scan((uint32_t)m, &tot);
-      if (MODE == DAG_FILL && has && nb + i < o.room_nodes) c.store(&o.node_edge[nb + i], (uint32_t)gpos);
-      for (int q = 0; q < op.ng; ++q) {
-        const DgdGroup& G = x.Gs[op.g0 + q];
-        if (G.points == 0) continue;
-        if (G.fast) {
-          uint32_t Pj = 0;
-          if (has) {
-            node_coords(X, F[i], x.vt, nt);
-            Pj = (uint32_t)ap_setup(x, G, R, S, lane, true);
-            S.glo(lane) = (uint32_t)gpos;
-            S.ghi(lane) = (uint32_t)(gpos >> 32);
-          }
-          // Nodes with at least four waves of points node by node, the
-          // others flattened across the lanes.
-          const bool big = Pj >= 4u * (uint32_t)L;
-          const uint64_t mask = c.ballot(big);
-          c.wave_sync();
-          const bool done = mask != 0 && emit_nodes(c, x, G, S, mask, o, emit, append);
-          flat_emit(c, x, G, S, WP, done && big ? 0u : Pj, o, emit, append);
-          gpos += (uint64_t)Pj * (uint64_t)G.nop;
-        } else {
-          S.glo(lane) = (uint32_t)gpos;
-          S.ghi(lane) = (uint32_t)(gpos >> 32);
-          c.wave_sync();
-          for (uint32_t j = 0; j < (uint32_t)L && b0 + j < n; ++j) {
-            node_coords(X, F[b0 + j], x.vt, nt);
-            const uint64_t gj = ((uint64_t)S.ghi((int)j) << 32) | S.glo((int)j);
-            const uint64_t mj = box_group(c, x, G, R, gj, o, emit, append);
-            if ((uint32_t)lane == j) gpos += mj;
-          }
-          c.wave_sync();
-        }
-      }
-    }
-  }
-  c.sync();
-  *nb_ = nb + n;
-  *eb_ = eb + total;
-  return true;
-}
-
-// Expression DAG of res(y[loc]).
-template <class C, int MODE>
-DGC void location_dag(C& c, const uint8_t* dblob, int64_t loc, uint8_t* area, const DagOut& o, uint64_t* n_nodes,
-                      uint64_t* n_edges, uint32_t* err) {
-  const DgdHeader* h = (const DgdHeader*)dblob;
-  const DgdTensor* T = (const DgdTensor*)(dblob + h->tensor_off);
-  const DgdOp* O = (const DgdOp*)(dblob + h->op_off);
-  const int tid = c.tid(), nt = c.nthreads();
-  uint32_t* cnt = (uint32_t*)(area + h->count_off);
-  uint32_t* NC = (uint32_t*)(area + h->ncount_off);
-  const int wbase = c.wave() * c.lanes();
-  const Slots S{(uint32_t*)(area + h->slot_off) + wbase, nt, h->max_win, h->max_opnd};
-  uint32_t* WP = (uint32_t*)(area + h->wave_off) + wbase;
-  DagCtx x{h, T, (const DgdGroup*)(dblob + h->group_off), (const DgdOperand*)(dblob + h->operand_off), area, cnt,
-           (int32_t*)(area + h->vars_off) + tid, nt, err};
-  *n_nodes = 0;
-  *n_edges = 0;
-  if (loc < 0 || loc >= h->out_numel) {
-    *err |= DGP_ERR_RANGE;
-    return;
-  }
-  for (int t = tid; t < h->ntensor; t += nt) cnt[t] = 0;
-  c.sync();
-  const DgdTensor& Ty = T[h->output];
-  if (!Ty.leaf) {
-    if (tid == 0) {
-      ((uint32_t*)(area + Ty.lds))[0] = (uint32_t)loc;
-      cnt[h->output] = 1;
-    }
-  }
-  c.sync();
-  uint64_t nb = 0, eb = 0;
-  for (int k = h->nop - 1; k >= 0; --k)
-    if (!dag_op<C, MODE>(c, x, O[k], NC, S, WP, o, &nb, &eb)) return;
-  *n_nodes = nb;
-  *n_edges = eb;
-}
-
 }  // namespace dgc

@@ -1,4 +1,4 @@
-// Host compiler of the expression-DAG program (program.h, DgdHeader): the
+// Host compiler of the expression-DAG program (dag_program.h, DgdHeader): the
 // ops of a graph as read groups with device index functions, element ids of
 // every tensor, and static frontier capacities for one location.
 #include <algorithm>
@@ -8,6 +8,7 @@
 
 #include "../../include/dirigo_rocm.h"
 #include "compile.h"
+#include "dag_program.h"
 
 namespace dg {
 

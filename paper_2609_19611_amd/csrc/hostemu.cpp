@@ -14,6 +14,7 @@
 #include "../../include/dirigo_rocm.h"
 #include "compile.h"
 #include "core.h"
+#include "dag_core.h"
 #include "graph.h"
 #include "jit.h"
 
@@ -48,6 +49,7 @@ struct HostCtx {
   }
   uint32_t atomic_inc(uint32_t* p) const { return (*p)++; }
   void store(uint32_t* p, uint32_t v) const { *p = v; }
+  void store_cached(uint32_t* p, uint32_t v) const { *p = v; }
   void store(uint64_t* p, uint64_t v) const { *p = v; }
   void reduce_add(uint64_t* p, uint64_t v) const { *p += v; }
   void reduce_max(uint64_t* p, uint64_t v) const {

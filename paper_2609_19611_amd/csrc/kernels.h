@@ -32,7 +32,7 @@ hipError_t launch_enumerate(const uint8_t* blob, dgc::LocSrc locs, int64_t n, in
 hipError_t launch_enumerate_wide(const uint8_t* blob, dgc::LocSrc locs, int64_t n, int64_t* offsets,
                                  uint64_t* ids, uint64_t* cnt, uint64_t capacity, uint64_t* status, uint64_t* ticket,
                                  uint32_t* err, int block, uint32_t lds, hipStream_t s);
-// Expression DAGs (program.h, DgdHeader; lds: the program's lds_bytes):
+// Expression DAGs (dag_program.h, DgdHeader; lds: the program's lds_bytes):
 // node and edge counts of location i into nodes_n[i + 1], edges_n[i + 1];
 // then nodes and edges at node_off[i], edge_off[i].
 hipError_t launch_dag_sizes(const uint8_t* dblob, dgc::LocSrc locs, int64_t n, int64_t* nodes_n, int64_t* edges_n,
