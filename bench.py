@@ -27,6 +27,7 @@ import numpy as np
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
+ALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12  # int32 VALU operations, no packing
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
 
 
@@ -42,6 +43,10 @@ def parse_args():
                    help="time dg_enumerate_sizes + dg_enumerate_fill instead of the single-pass dg_enumerate")
     p.add_argument("--wide", action="store_true",
                    help="time dg_enumerate_wide (64-bit ids and counts) instead of dg_enumerate")
+    p.add_argument("--order", action="store_true",
+                   help="time the location order (keyed permutation of every output location of the c5 split-K "
+                        "variant, corner and boundary prefix left out) and count the locations checked before "
+                        "each fault's first mismatch under three orders")
     p.add_argument("--dag", action="store_true",
                    help="time expression-DAG emission (dg_dag_sizes + dg_dag_fill) instead of the rows; c3 takes "
                         "every 8th of its locations, c5 the reference graph")
@@ -263,6 +268,103 @@ def dag_bench(args, B, g, cfg, locs, text):
     print(json.dumps(line), flush=True)
 
 
+def order_bench(args, B):
+    """The location order of the c5 split-K variant (33,554,432 output
+    locations): a step is dg_order_permute over every permutation position
+    with the prefix's locations left out (device-resident, synchronous).
+    Then, per seeded fault, the rank of the first mismatching location under
+    the heuristic order, the plain permutation and the sequential order."""
+    import torch
+    from paper_2609_19611_amd import workloads as W
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    ref = B.dg_graph_parse(W.c5_reference_text())
+    var = B.dg_graph_parse(W.c5_variant_text())
+    n = B.dg_graph_info(var)["output_numel"]
+    seed = 5
+    prefix = B.dg_order_prefix(var)
+    out = torch.empty(n, dtype=torch.int64, device=dev)
+    ws = torch.empty(max(1, B.dg_order_workspace_size(len(prefix))), dtype=torch.uint8, device=dev)
+    stream = torch.cuda.current_stream()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(args.steps)]
+
+    def step(i=None):
+        if i is not None:
+            ev[i][0].record(stream)
+        w = B.dg_order_permute(n, seed, prefix, 0, n, out, ws)
+        if i is not None:
+            ev[i][1].record(stream)
+        return w
+
+    for _ in range(max(1, args.warmup)):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        w = step(i)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    call_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    assert w + len(prefix) == n
+
+    # Rank of the first mismatch: compare the reference with each faulty
+    # variant over growing prefixes of an order until one mismatches.
+    heur = torch.cat([torch.tensor(prefix, dtype=torch.int64, device=dev), out[:w]])
+    perm = torch.empty(n, dtype=torch.int64, device=dev)
+    B.dg_order_permute(n, seed, [], 0, n, perm, ws)
+    seq = torch.arange(n, dtype=torch.int64, device=dev)
+    cws = torch.empty(max(B.dg_workspace_size(ref, n), 1), dtype=torch.uint8, device=dev)
+    status = torch.empty(n, dtype=torch.uint8, device=dev)
+    mism = torch.empty(n, dtype=torch.int64, device=dev)
+
+    def first_mismatch(v, order):
+        lo, k = 0, 64
+        while lo < n:
+            hi = min(n, lo + k)
+            m = B.dg_compare(ref, v, order[lo:hi], status, mism, cws)
+            if m:
+                return lo + int(mism[0].item())
+            lo, k = hi, k * 4
+        return None
+
+    ranks = []
+    for f in W.c5_faults():
+        v = B.dg_graph_parse(W.c5_variant_text(fault=f))
+        ranks.append({"fault": "/".join(str(x) for x in f), "heuristic": first_mismatch(v, heur),
+                      "permutation": first_mismatch(v, perm), "sequential": first_mismatch(v, seq)})
+    # ALU roofline: 24 32-bit operations per Feistel round (two 64-bit
+    # multiplies, three 64-bit shifts, five 64-bit xors and ands), four rounds
+    # per encryption, on average D / n encryptions per position (cycle walking
+    # on the domain D = 4^h), against 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz.
+    h = 0
+    while (1 << (2 * h)) < n:
+        h += 1
+    ops = 24 * 4 * ((1 << (2 * h)) / n) * n
+    achieved = ops / (call_ms * 1e-3) / 1e12
+    line = {
+        "metric": "output locations/sec ordered (keyed permutation of every output location, prefix left out)",
+        "value": n / (elapsed / args.steps), "unit": "locations/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": elapsed * 1000 / args.steps, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "int64",
+        "data": "synthetic (shapes only; the order depends on shapes and the seed)",
+        "config": {"workload": "c5 split-K variant output [64,128,64,64]: location order", "locations": n,
+                   "seed": seed, "prefix": len(prefix), "first_mismatch_rank": ranks},
+        "roofline": {"bound": "alu", "kernel": "k_order_write", "achieved": achieved, "peak": ALU_PEAK_TOPS,
+                     "unit": "Tops/s (int32)", "frac": achieved / ALU_PEAK_TOPS, "traffic": None,
+                     "call_ms": call_ms, "algorithmic_ops": ops, "hbm_bytes_written": 8 * w},
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        m = 2_000_000
+        t1 = time.perf_counter()
+        oracle.permutation(n, seed, 0, m)
+        dt = time.perf_counter() - t1
+        line["cpu_baseline"] = {"value": m / dt, "unit": "locations/s", "cores": 1, "kind": "oracle",
+                                "sample": f"first {m} of {n} permutation positions"}
+    line["git"] = git_sha()
+    print(json.dumps(line), flush=True)
+
+
 def main():
     args = parse_args()
     if args.gpus != 1:
@@ -280,6 +382,10 @@ def main():
 
     if args.copy_gib > 0:
         copy_calibration(args.copy_gib, args.steps, args.warmup)
+        return
+    if args.order:
+        from paper_2609_19611_amd import binding as B
+        order_bench(args, B)
         return
 
     import torch

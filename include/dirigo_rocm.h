@@ -392,6 +392,64 @@ dg_status dg_compare_range(const dg_graph* a, const dg_graph* b, int64_t first, 
                            void* stream);
 
 /* Message of the calling thread's last failed call ("" if none). */
+/*
+ * Location order (Sec. 4, "Search Heuristic": candidate locations ranked in
+ * tiers, then a random permutation of the unchecked ones).  The tier that
+ * needs an SMT solver (path-condition coverage) is not part of this path;
+ * the other two are:
+ *
+ *   corners -- every op is taken as one kernel launch writing its output in
+ *     row-major order, one element per thread, block_threads threads per
+ *     block.  Its corner threads are the first and last thread of the first
+ *     and last block and lanes warp-1 and warp of block 0.  A corner
+ *     thread's element is mapped to an output location through reads that
+ *     only permute dims (each consumer element reads exactly that element
+ *     and every other operand of the read is in range everywhere); the
+ *     smallest location over such paths is taken, and corners with no such
+ *     path give none.  Ops rank in reverse SSA order (later launches
+ *     first); per op: (thread 0, block 0), (last thread, block 0),
+ *     (thread 0, last block), (last thread, last block), lane warp-1,
+ *     lane warp.
+ *   boundaries -- the first and the last output location.
+ *
+ * Each location appears once, at its first rank.  The rest of [0, numel)
+ * follows in the order of a keyed permutation pi of [0, numel): a balanced
+ * four-round Feistel network on 2h bits, h the smallest with 4^h >= numel,
+ * round keys the first four outputs of SplitMix64 (Steele, Lea and Flood,
+ * 2014) seeded with `seed`, round function the SplitMix64 output mix of
+ * (right half XOR key) masked to h bits, new halves (R, L XOR F(R)); values
+ * at or past numel are encrypted again until below numel (cycle walking,
+ * Black and Rogaway, 2002).  The full order is the prefix followed by
+ * pi(0), pi(1), ... with the prefix's locations left out.
+ */
+
+/* dg_order_prefix: the ranked prefix (corners, then boundaries) of g's
+ * output for the given launch shape (block_threads >= 1, warp >= 1).  Host
+ * only, no device work.  Writes min(count, cap) locations to h_prefix
+ * (host memory; may be NULL when cap is 0) and the full count to
+ * *h_count. */
+dg_status dg_order_prefix(const dg_graph* g, int32_t block_threads, int32_t warp, int64_t* h_prefix, int64_t cap,
+                          int64_t* h_count);
+
+/* dg_order_workspace_size: bytes of device workspace dg_order_permute needs
+ * for up to n_exclude excluded values. */
+dg_status dg_order_workspace_size(int64_t n_exclude, size_t* bytes);
+
+/* dg_order_permute: pi(first), ..., pi(first + count - 1) of the keyed
+ * permutation of [0, n_out) (n_out <= 2^62), leaving out the values listed
+ * in h_exclude, written in position order to d_out (device; room for count
+ * values less those excluded values whose positions fall in the range, at
+ * most count).  h_exclude: n_exclude host int64 values in [0, n_out) (any order,
+ * repeats allowed; a value outside gives DG_E_INVALID_ARG).  The library
+ * finds each excluded value's position by the inverse permutation, so the
+ * device pass computes pi once per position.  Synchronous: *h_written
+ * receives the number of values written.  Concatenating the calls over
+ * consecutive position ranges gives the permutation part of the order; with
+ * h_exclude = the prefix it completes the order. */
+dg_status dg_order_permute(int64_t n_out, uint64_t seed, const int64_t* h_exclude, int64_t n_exclude, int64_t first,
+                           int64_t count, int64_t* d_out, int64_t* h_written, void* d_ws, size_t ws_bytes,
+                           void* stream);
+
 const char* dg_last_error(void);
 
 #ifdef __cplusplus

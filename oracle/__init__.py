@@ -75,6 +75,11 @@ def _load():
     lib.dgo_dag_free.argtypes = [P]
     lib.dgo_reads.argtypes = [P, ctypes.c_int, i64, P, P, P, i64]
     lib.dgo_reads.restype = i64
+    lib.dgo_order_prefix.argtypes = [P, i64, i64, P, i64]
+    lib.dgo_order_prefix.restype = i64
+    lib.dgo_permutation.argtypes = [i64, ctypes.c_uint64, i64, i64, P]
+    lib.dgo_feistel.argtypes = [i64, ctypes.c_uint64, ctypes.c_int, P, i64, P]
+    lib.dgo_splitmix.argtypes = [ctypes.c_uint64, i64, P]
     _lib = lib
     return lib
 
@@ -218,3 +223,47 @@ def compare(a: Graph, b: Graph, locs, threads: int = 1) -> np.ndarray:
     if lib.dgo_compare(a._h, b._h, locs.ctypes.data, len(locs), threads, status.ctypes.data) != 0:
         raise OracleError(lib.dgo_error().decode())
     return status
+
+
+# ---- location order (Sec. 4, "Search Heuristic") ------------------------------
+def order_prefix(g: Graph, threads: int = 256, warp: int = 32) -> list[int]:
+    """Corner locations of every op (later ops first), then the first and
+    last output location, each once (see dg_oracle.cpp)."""
+    lib = _load()
+    n = lib.dgo_order_prefix(g._h, threads, warp, None, 0)
+    if n < 0:
+        raise OracleError(lib.dgo_error().decode())
+    out = np.empty(max(1, n), dtype=np.int64)
+    lib.dgo_order_prefix(g._h, threads, warp, out.ctypes.data, n)
+    return out[:n].tolist()
+
+
+def permutation(n: int, seed: int, first: int = 0, count: int | None = None) -> np.ndarray:
+    """Positions [first, first + count) of the keyed permutation of [0, n)."""
+    count = n - first if count is None else count
+    out = np.empty(max(1, count), dtype=np.int64)
+    _load().dgo_permutation(n, seed & ((1 << 64) - 1), first, count, out.ctypes.data)
+    return out[:count]
+
+
+def feistel(n: int, seed: int, x, inverse: bool = False) -> np.ndarray:
+    """The Feistel network of the permutation of [0, n) without cycle walking."""
+    x = np.ascontiguousarray(np.asarray(x, dtype=np.uint64))
+    out = np.empty(max(1, len(x)), dtype=np.uint64)
+    _load().dgo_feistel(n, seed & ((1 << 64) - 1), 1 if inverse else 0, x.ctypes.data, len(x), out.ctypes.data)
+    return out[:len(x)]
+
+
+def splitmix64(seed: int, count: int) -> list[int]:
+    out = np.empty(count, dtype=np.uint64)
+    _load().dgo_splitmix(seed & ((1 << 64) - 1), count, out.ctypes.data)
+    return [int(v) for v in out]
+
+
+def location_order(g: Graph, seed: int, threads: int = 256, warp: int = 32) -> np.ndarray:
+    """The full order: the prefix, then the permutation without its locations."""
+    prefix = order_prefix(g, threads, warp)
+    rest = permutation(g.output_numel, seed)
+    if prefix:
+        rest = rest[~np.isin(rest, np.asarray(prefix, dtype=np.int64))]
+    return np.concatenate([np.asarray(prefix, dtype=np.int64), rest])

@@ -1091,6 +1091,153 @@ thread_local std::string g_err;
 
 }  // namespace
 
+namespace {
+
+// ---- location order (Sec. 4, "Search Heuristic") ---------------------------
+// Candidate locations are ranked before the rest: corner locations of every
+// kernel launch (later launches first), then the first and last element of
+// the output; the remaining locations follow in a random permutation.
+// Readings (the paper's launches are CUDA kernels; here every op is one
+// launch writing its output row-major, one element per thread):
+//  - corner threads: first and last thread of the first and last block,
+//    lanes warp-1 and warp of block 0;
+//  - a corner element becomes an output location through reads that are one
+//    to one (at every output element of the reading op, its reads of the
+//    tensor name exactly one element, and distinct output elements name
+//    distinct elements); the smallest location over such paths is taken;
+//  - a location is listed once, at its first rank.
+
+// Whether `op` reads tensor t one to one; back[o] = the element read at o.
+bool reads_one_to_one(const Graph& g, const Op& op, int t, std::vector<int64_t>* back) {
+  const int64_t m = numel_of(g.tensors[op.out].shape);
+  if (numel_of(g.tensors[t].shape) != m) return false;
+  back->assign((size_t)m, -1);
+  std::vector<char> hit((size_t)m, 0);
+  for (int64_t o = 0; o < m; ++o) {
+    int64_t e = -1;
+    bool one = true;
+    op_reads(g, op, o, [&](int tt, int64_t ii, uint64_t) {
+      if (tt != t) return;
+      if (e < 0) e = ii;
+      else if (e != ii) one = false;
+    });
+    if (!one || e < 0 || hit[(size_t)e]) return false;
+    hit[(size_t)e] = 1;
+    (*back)[(size_t)o] = e;
+  }
+  return true;
+}
+
+std::vector<int64_t> order_prefix(const Graph& g, int64_t threads, int64_t warp) {
+  if (threads < 1 || warp < 1) throw Error("threads and warp must be positive");
+  const int64_t n = numel_of(g.tensors[g.output].shape);
+  // loc[t][e]: smallest output location whose chain of one-to-one reads
+  // back from the output reaches element e of tensor t (-1: none).  Ops in
+  // reverse SSA order: every consumer of an op's output comes first.
+  std::map<int, std::vector<int64_t>> loc;
+  std::vector<int64_t>& ly = loc[g.output];
+  ly.resize((size_t)n);
+  for (int64_t l = 0; l < n; ++l) ly[(size_t)l] = l;
+  for (int k = (int)g.ops.size() - 1; k >= 0; --k) {
+    const Op& op = g.ops[k];
+    if (!loc.count(op.out)) continue;
+    std::set<int> operands(op.in.begin(), op.in.end());
+    for (int t : operands) {
+      std::vector<int64_t> back;
+      if (!reads_one_to_one(g, op, t, &back)) continue;
+      std::vector<int64_t>& lt = loc[t];
+      if (lt.empty()) lt.assign((size_t)numel_of(g.tensors[t].shape), -1);
+      const std::vector<int64_t>& lo = loc[op.out];
+      for (size_t o = 0; o < back.size(); ++o) {
+        const int64_t l = lo[o];
+        int64_t& dst = lt[(size_t)back[o]];
+        if (l >= 0 && (dst < 0 || l < dst)) dst = l;
+      }
+    }
+  }
+  std::vector<int64_t> out;
+  std::set<int64_t> seen;
+  auto add = [&](int64_t l) {
+    if (l >= 0 && seen.insert(l).second) out.push_back(l);
+  };
+  for (int k = (int)g.ops.size() - 1; k >= 0; --k) {
+    const int t = g.ops[k].out;
+    const int64_t m = numel_of(g.tensors[t].shape);
+    if (m == 0) continue;
+    const int64_t blocks = (m + threads - 1) / threads, last = (blocks - 1) * threads;
+    // (thread 0, block 0), (last thread, block 0), (thread 0, last block),
+    // (last thread, last block), then lanes warp-1 and warp of block 0.
+    std::vector<int64_t> corner = {0, threads - 1, last, last + threads - 1};
+    if (warp - 1 < threads) corner.push_back(warp - 1);
+    if (warp < threads) corner.push_back(warp);
+    for (int64_t e : corner) {
+      if (e >= m) continue;
+      auto it = loc.find(t);
+      add(it == loc.end() ? -1 : it->second[(size_t)e]);
+    }
+  }
+  if (n > 0) {
+    add(0);
+    add(n - 1);
+  }
+  return out;
+}
+
+// SplitMix64 (Steele, Lea and Flood, "Fast splittable pseudorandom number
+// generators", 2014): state += golden gamma, then the output mix.
+uint64_t splitmix_mix(uint64_t z) {
+  z = (z ^ (z >> 30)) * 0xBF58476D1CE4E5B9ull;
+  z = (z ^ (z >> 27)) * 0x94D049BB133111EBull;
+  return z ^ (z >> 31);
+}
+
+// Keyed permutation of [0, n): a balanced Feistel network (Luby and
+// Rackoff, 1988) of four rounds on 2h bits, h the smallest with 4^h >= n;
+// round r maps halves (L, R) to (R, L xor F_r(R)) with F_r(R) the SplitMix64
+// output mix of (R xor key_r) cut to h bits and key_r the r-th SplitMix64
+// output for `seed`.  Values at or past n are encrypted again until they
+// fall below n (cycle walking: Black and Rogaway, "Ciphers with arbitrary
+// finite domains", 2002).
+struct Permutation {
+  int h = 0;
+  uint64_t mask = 0, key[4] = {0, 0, 0, 0};
+  int64_t n = 0;
+  Permutation(int64_t n_, uint64_t seed) : n(n_) {
+    while (h < 31 && (1ull << (2 * h)) < (uint64_t)n) ++h;
+    mask = (1ull << h) - 1;
+    uint64_t state = seed;
+    for (int r = 0; r < 4; ++r) {
+      state += 0x9E3779B97F4A7C15ull;
+      key[r] = splitmix_mix(state);
+    }
+  }
+  uint64_t encrypt(uint64_t x) const {
+    uint64_t L = x >> h, R = x & mask;
+    for (int r = 0; r < 4; ++r) {
+      uint64_t next = L ^ (splitmix_mix(R ^ key[r]) & mask);
+      L = R;
+      R = next;
+    }
+    return (L << h) | R;
+  }
+  uint64_t decrypt(uint64_t x) const {
+    uint64_t L = x >> h, R = x & mask;
+    for (int r = 3; r >= 0; --r) {
+      uint64_t prev = R ^ (splitmix_mix(L ^ key[r]) & mask);
+      R = L;
+      L = prev;
+    }
+    return (L << h) | R;
+  }
+  int64_t at(int64_t i) const {
+    uint64_t v = encrypt((uint64_t)i);
+    while (v >= (uint64_t)n) v = encrypt(v);
+    return (int64_t)v;
+  }
+};
+
+}  // namespace
+
 // ---------------------------------------------------------------------------
 // C interface used by the Python test harness (ctypes).
 // Returns 0 on success, -1 on error (message via dgo_error()).
@@ -1227,6 +1374,41 @@ int dgo_compare(const dgo_graph* a, const dgo_graph* b, const int64_t* locs, int
   } catch (const std::exception& e) {
     g_err = e.what();
     return -1;
+  }
+}
+
+// Ranked prefix of the location order: up to cap locations into out;
+// returns the full count, or -1 on error.
+int64_t dgo_order_prefix(const dgo_graph* g, int64_t threads, int64_t warp, int64_t* out, int64_t cap) {
+  try {
+    std::vector<int64_t> p = order_prefix(g->g, threads, warp);
+    for (size_t i = 0; i < p.size() && (int64_t)i < cap; ++i) out[i] = p[i];
+    return (int64_t)p.size();
+  } catch (const std::exception& e) {
+    g_err = e.what();
+    return -1;
+  }
+}
+
+// Positions first .. first + count - 1 of the keyed permutation of [0, n).
+void dgo_permutation(int64_t n, uint64_t seed, int64_t first, int64_t count, int64_t* out) {
+  Permutation p(n, seed);
+  for (int64_t i = 0; i < count; ++i) out[i] = p.at(first + i);
+}
+
+// The Feistel network alone (no cycle walking) on the 2h-bit domain of n:
+// forward (dir = 0) or inverse (dir = 1) images of x[0..count).
+void dgo_feistel(int64_t n, uint64_t seed, int dir, const uint64_t* x, int64_t count, uint64_t* out) {
+  Permutation p(n, seed);
+  for (int64_t i = 0; i < count; ++i) out[i] = dir ? p.decrypt(x[i]) : p.encrypt(x[i]);
+}
+
+// First `count` outputs of SplitMix64 for `seed`.
+void dgo_splitmix(uint64_t seed, int64_t count, uint64_t* out) {
+  uint64_t state = seed;
+  for (int64_t i = 0; i < count; ++i) {
+    state += 0x9E3779B97F4A7C15ull;
+    out[i] = splitmix_mix(state);
   }
 }
 

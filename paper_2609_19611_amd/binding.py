@@ -117,6 +117,9 @@ def _load():
         "dg_graph_tensor": ([P, i32, P], i32),
         "dg_dag_sizes": ([P, P, i64, P, P, P, ctypes.POINTER(i64), ctypes.POINTER(i64), P], i32),
         "dg_dag_fill": ([P, P, i64, P, P, P, P, P, P, P, P], i32),
+        "dg_order_prefix": ([P, i32, i32, P, i64, ctypes.POINTER(i64)], i32),
+        "dg_order_workspace_size": ([i64, ctypes.POINTER(sz)], i32),
+        "dg_order_permute": ([i64, ctypes.c_uint64, P, i64, i64, i64, P, ctypes.POINTER(i64), P, sz, P], i32),
         "dg_last_error": ([], ctypes.c_char_p),
     }
     for name, (args, res) in sig.items():
@@ -470,6 +473,55 @@ def dag_locations(g: Graph, locs, stream=None) -> dict:
     for k, m in (("nodes", nn), ("node_edge", nn), ("edges", ne), ("mults", ne)):
         out[k] = out[k][:m]
     return out
+
+
+def dg_order_prefix(g: Graph, block_threads: int = 256, warp: int = 32) -> list[int]:
+    """The ranked prefix of the location order (corners, then the first and
+    last output location); host only."""
+    n = ctypes.c_int64()
+    _check(_lib.dg_order_prefix(g.handle, block_threads, warp, None, 0, ctypes.byref(n)))
+    buf = (ctypes.c_int64 * max(1, n.value))()
+    _check(_lib.dg_order_prefix(g.handle, block_threads, warp, buf, n.value, ctypes.byref(n)))
+    return list(buf[: n.value])
+
+
+def dg_order_workspace_size(n_exclude: int) -> int:
+    b = ctypes.c_size_t()
+    _check(_lib.dg_order_workspace_size(n_exclude, ctypes.byref(b)))
+    return b.value
+
+
+def dg_order_permute(n_out: int, seed: int, exclude, first: int, count: int, d_out: torch.Tensor,
+                     d_ws: torch.Tensor, stream=None) -> int:
+    """Positions [first, first + count) of the keyed permutation of
+    [0, n_out) without the values in `exclude` (host ints), into d_out;
+    returns the number written."""
+    _dev_i64(d_out, "out")
+    ex = list(exclude or [])
+    if d_out.numel() < count - len(set(ex)):
+        raise ValueError("out needs room for count values less the excluded ones")
+    buf = (ctypes.c_int64 * max(1, len(ex)))(*ex)
+    w = ctypes.c_int64()
+    _check(_lib.dg_order_permute(n_out, seed & ((1 << 64) - 1), buf, len(ex), first, count, _ptr(d_out),
+                                 ctypes.byref(w), _ptr(d_ws), d_ws.numel() * d_ws.element_size(), _stream(stream)))
+    return w.value
+
+
+def order_locations(g: Graph, seed: int, block_threads: int = 256, warp: int = 32, device=None) -> torch.Tensor:
+    """The full location order of g's output on the device: the prefix, then
+    the permutation without the prefix's locations."""
+    device = device or torch.device("cuda", torch.cuda.current_device())
+    n = dg_graph_info(g)["output_numel"]
+    prefix = dg_order_prefix(g, block_threads, warp)
+    k = len(prefix)
+    out = torch.empty(max(1, n), dtype=torch.int64, device=device)
+    if k:
+        out[:k] = torch.tensor(prefix, dtype=torch.int64)
+    ws = torch.empty(max(1, dg_order_workspace_size(k)), dtype=torch.uint8, device=device)
+    w = dg_order_permute(n, seed, prefix, 0, n, out[k:], ws) if n > k else 0
+    if k + w != n:
+        raise RuntimeError(f"order has {k + w} of {n} locations")
+    return out[:n]
 
 
 def compare_locations(a: Graph, b: Graph, locs, stream=None):

@@ -17,6 +17,7 @@
 #include "graph.h"
 #include "jit.h"
 #include "kernels.h"
+#include "order.h"
 
 // Specialised kernels of a graph on one device.
 struct DevKernels {
@@ -780,6 +781,54 @@ dg_status dg_dag_fill(const dg_graph* g, const int64_t* d_locs, int64_t n, const
     DG_HIP(hipMemcpyAsync(&bits, err, sizeof(uint32_t), hipMemcpyDeviceToHost, s), "copy flags");
     DG_HIP(hipStreamSynchronize(s), "DAG fill sync");
     return device_errors(bits);
+  });
+}
+
+dg_status dg_order_prefix(const dg_graph* g, int32_t block_threads, int32_t warp, int64_t* h_prefix, int64_t cap,
+                          int64_t* h_count) {
+  if (!g || !h_count || cap < 0 || (cap > 0 && !h_prefix)) return set_error(DG_E_INVALID_ARG, "bad argument");
+  return guarded([&]() -> dg_status {
+    const std::vector<int64_t> p = dg::order_prefix(g->ir, block_threads, warp);
+    *h_count = (int64_t)p.size();
+    for (int64_t i = 0; i < (int64_t)p.size() && i < cap; ++i) h_prefix[i] = p[(size_t)i];
+    return DG_OK;
+  });
+}
+
+dg_status dg_order_workspace_size(int64_t n_exclude, size_t* bytes) {
+  if (!bytes || n_exclude < 0) return set_error(DG_E_INVALID_ARG, "bad argument");
+  *bytes = 8 * (size_t)std::max<int64_t>(1, n_exclude);
+  return DG_OK;
+}
+
+dg_status dg_order_permute(int64_t n_out, uint64_t seed, const int64_t* h_exclude, int64_t n_exclude, int64_t first,
+                           int64_t count, int64_t* d_out, int64_t* h_written, void* d_ws, size_t ws_bytes,
+                           void* stream) {
+  if (!h_written || n_out < 0 || n_out > ((int64_t)1 << 62) || n_exclude < 0 || first < 0 || count < 0 ||
+      first > n_out || count > n_out - first || (n_exclude > 0 && !h_exclude) || (count > 0 && !d_out))
+    return set_error(DG_E_INVALID_ARG, "bad argument");
+  return guarded([&]() -> dg_status {
+    const DgPermKey K = dg_perm_key(n_out, seed);
+    // Positions of the excluded values inside the range, sorted.
+    std::vector<int64_t> pos;
+    for (int64_t j = 0; j < n_exclude; ++j) {
+      const int64_t v = h_exclude[j];
+      if (v < 0 || v >= n_out) return set_error(DG_E_INVALID_ARG, "an excluded value is outside [0, n_out)");
+      const int64_t p = dg_perm_position((uint64_t)v, K);
+      if (p >= first && p - first < count) pos.push_back(p);
+    }
+    std::sort(pos.begin(), pos.end());
+    pos.erase(std::unique(pos.begin(), pos.end()), pos.end());
+    if (!pos.empty() && (!d_ws || ws_bytes < 8 * pos.size()))
+      return set_error(DG_E_WORKSPACE, "workspace smaller than dg_order_workspace_size");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    int64_t* d_pos = static_cast<int64_t*>(d_ws);
+    if (!pos.empty())
+      DG_HIP(hipMemcpyAsync(d_pos, pos.data(), 8 * pos.size(), hipMemcpyHostToDevice, s), "copy positions");
+    DG_HIP(dgk::launch_order(K, d_pos, (int64_t)pos.size(), first, count, d_out, s), "order kernel");
+    DG_HIP(hipStreamSynchronize(s), "order sync");
+    *h_written = count - (int64_t)pos.size();
+    return DG_OK;
   });
 }
 

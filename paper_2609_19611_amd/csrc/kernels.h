@@ -4,6 +4,7 @@
 #include <stdint.h>
 
 #include "core.h"
+#include "order.h"
 
 namespace dgk {
 
@@ -40,6 +41,11 @@ hipError_t launch_dag_sizes(const uint8_t* dblob, dgc::LocSrc locs, int64_t n, i
 hipError_t launch_dag_fill(const uint8_t* dblob, dgc::LocSrc locs, int64_t n, const int64_t* node_off,
                            const int64_t* edge_off, uint32_t* nodes, uint32_t* node_edge, uint32_t* edges,
                            uint32_t* mults, uint32_t* err, int block, uint32_t lds, hipStream_t s);
+// Location order: positions [first, first + count) of the keyed
+// permutation K (order.h) into out, leaving out the sorted excluded
+// positions pos[0..m) (all inside the range) and closing the gaps.
+hipError_t launch_order(const DgPermKey& K, const int64_t* pos, int64_t m, int64_t first, int64_t count,
+                        int64_t* out, hipStream_t s);
 // Clears count 64-bit words.
 hipError_t launch_zero_u64(uint64_t* p, int64_t count, hipStream_t s);
 // Clears one error word (a kernel, so it may be recorded in a captured graph).

@@ -4,10 +4,13 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
+
 #define DGC __device__ __forceinline__
 #include "kernels_dev.h"
 #include "dag_core.h"
 #include "kernels.h"
+#include "order.h"
 
 namespace dgk_dev {
 
@@ -291,6 +294,26 @@ __global__ void k_scatter_mismatch(const uint8_t* __restrict__ status, const int
   if (i < n && (status[i] == 1 || status[i] == 2)) out[pos[i]] = i;
 }
 
+// ---- location order: keyed permutation with excluded positions ------------
+// Position i of [first, first + count) writes pi(i) at i - first minus the
+// number of excluded positions below i; an excluded position writes nothing.
+// pos: the sorted excluded positions inside the range.
+__global__ __launch_bounds__(256) void k_order_write(DgPermKey K, const int64_t* __restrict__ pos, int64_t m,
+                                                     int64_t first, int64_t count, int64_t* __restrict__ out) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; t < count; t += stride) {
+    const int64_t i = first + t;
+    int64_t lo = 0, hi = m;  // excluded positions below i
+    while (lo < hi) {
+      const int64_t mid = (lo + hi) >> 1;
+      if (pos[mid] < i) lo = mid + 1;
+      else hi = mid;
+    }
+    if (lo < m && pos[lo] == i) continue;
+    __builtin_nontemporal_store(dg_perm_at((uint64_t)i, K), &out[t - lo]);
+  }
+}
+
 __global__ void k_zero_offsets(int64_t* __restrict__ v) { v[0] = 0; }
 
 __global__ void k_rebase(const int64_t* __restrict__ src, int64_t* __restrict__ dst, int64_t count, int64_t base) {
@@ -467,6 +490,14 @@ hipError_t launch_scan(int64_t* v, int64_t n, int64_t* sums, hipStream_t s) {
   hipLaunchKernelGGL(k_scan_reduce, dim3((unsigned)tiles), dim3(SCAN_THREADS), 0, s, v, n, sums);
   hipLaunchKernelGGL(k_scan_sums, dim3(1), dim3(SCAN_THREADS), 0, s, sums, tiles);
   hipLaunchKernelGGL(k_scan_apply, dim3((unsigned)tiles), dim3(SCAN_THREADS), 0, s, v, n, sums);
+  return hipGetLastError();
+}
+
+hipError_t launch_order(const DgPermKey& K, const int64_t* pos, int64_t m, int64_t first, int64_t count,
+                        int64_t* out, hipStream_t s) {
+  if (count <= 0) return hipSuccess;
+  const int64_t blocks = std::min<int64_t>((count + 255) / 256, 1 << 20);
+  hipLaunchKernelGGL(k_order_write, dim3((unsigned)blocks), dim3(256), 0, s, K, pos, m, first, count, out);
   return hipGetLastError();
 }
 

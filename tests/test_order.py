@@ -1,0 +1,235 @@
+"""Location order (Sec. 4, "Search Heuristic"): the oracle pinned by the
+published SplitMix64 outputs, the invertibility of its Feistel network,
+bijectivity of the permutation, corner locations derived by hand; then the
+library's host-built prefix against the oracle, and the ABI's argument
+checks (no device work)."""
+
+import ctypes
+
+import numpy as np
+import pytest
+
+import oracle
+import tiny_graphs
+from paper_2609_19611_amd import workloads as W
+from paper_2609_19611_amd.workloads import GraphText
+
+
+# ---- oracle pins --------------------------------------------------------------
+def test_splitmix64_reference_outputs():
+    # First outputs of the reference SplitMix64 generator for seed 0
+    # (Steele, Lea and Flood 2014; the values every port reproduces).
+    assert oracle.splitmix64(0, 4) == [0xE220A8397B1DCDAF, 0x6E789E6AA1B965F4, 0x06C45D188009454F,
+                                       0xF88BB8A8724C81EC]
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 5, 16, 17, 1000, 4097])
+def test_feistel_is_invertible_on_its_domain(n):
+    h = 0
+    while (1 << (2 * h)) < n:
+        h += 1
+    x = np.arange(1 << (2 * h), dtype=np.uint64)
+    y = oracle.feistel(n, 7, x)
+    assert sorted(y.tolist()) == x.tolist()  # a bijection of the 2h-bit domain
+    assert np.array_equal(oracle.feistel(n, 7, y, inverse=True), x)
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 4, 5, 31, 64, 1000, 4097, 65537])
+def test_permutation_is_a_bijection(n):
+    p = oracle.permutation(n, 12345)
+    assert p.dtype == np.int64 and len(p) == n
+    assert np.array_equal(np.sort(p), np.arange(n))
+
+
+def test_permutation_is_cycle_walking_of_the_network():
+    # pi(i) is the first value below n on the orbit i -> E(i) -> E(E(i)) ...
+    n = 1000  # domain 1024
+    e = oracle.feistel(n, 3, np.arange(1024, dtype=np.uint64)).astype(np.int64)
+    p = oracle.permutation(n, 3)
+    for i in range(n):
+        v = e[i]
+        while v >= n:
+            v = e[v]
+        assert p[i] == v
+
+
+def test_permutation_ranges_and_seeds():
+    n = 5000
+    full = oracle.permutation(n, 99)
+    assert np.array_equal(oracle.permutation(n, 99, 1234, 777), full[1234:2011])
+    assert not np.array_equal(oracle.permutation(n, 100), full)
+    assert not np.array_equal(full, np.arange(n))
+
+
+def _c5_nhwc_to_nchw(e, n, c, hw):
+    """Output location of element e of an NHWC [n, hw, hw, c] tensor read
+    through the final permute back to NCHW."""
+    # NHWC flat: ((n_i * hw + h) * hw + w) * c + c_i
+    ci = e % c
+    rest = e // c
+    w = rest % hw
+    h = (rest // hw) % hw
+    ni = rest // (hw * hw)
+    return ((ni * c + ci) * hw + h) * hw + w
+
+
+@pytest.mark.parametrize("threads,warp", [(256, 32), (16, 4), (7, 3)])
+def test_prefix_c5_variant_by_hand(threads, warp):
+    """Every NHWC tensor of the split-K variant reaches the output through
+    dim permutations only (adds with broadcast operands, relu, the final
+    permute), the gathered tensors xc, Wc do not (they are read through
+    windows)."""
+    n, c, hw, co = 2, 4, 6, 3
+    text = W.c5_variant_text(n=n, c=c, hw=hw, co=co)
+    m = n * co * hw * hw
+    blocks = (m + threads - 1) // threads
+    last = (blocks - 1) * threads
+    corner = [0, threads - 1, last, last + threads - 1] + [x for x in (warp - 1, warp) if x < threads]
+    corner = [e for e in corner if e < m]
+    want, seen = [], set()
+    for e in corner:  # the output itself (NCHW) comes first
+        if e not in seen:
+            seen.add(e)
+            want.append(e)
+    # then r, sh, sc, cb, s_k, p_k (NHWC, 11 tensors in reverse SSA order)
+    for _ in range(11):
+        for e in corner:
+            loc = _c5_nhwc_to_nchw(e, n, co, hw)
+            if loc not in seen:
+                seen.add(loc)
+                want.append(loc)
+    for loc in (0, m - 1):
+        if loc not in seen:
+            seen.add(loc)
+            want.append(loc)
+    assert oracle.order_prefix(oracle.Graph(text), threads, warp) == want
+
+
+def test_prefix_reductions_give_no_corners():
+    # y = sum(exp(x + b)): only y's own corners and the boundaries.
+    g = GraphText()
+    g.leaf("x", [3, 5])
+    g.leaf("b", [5])
+    g.op("r", "add", "x", "b")
+    g.op("e", "exp", "r")
+    g.op("y", "sum", "e", dims=1, keepdim=0)
+    g.output("y", [3])
+    assert oracle.order_prefix(oracle.Graph(g.text()), 4, 2) == [0, 1, 2]
+
+
+def test_prefix_smallest_over_two_paths():
+    # t[a, b, c] reaches y twice: through p1 at y[b, a, c] and through p2 at
+    # y[c, b, a].  Blocks of 2 threads over 8 elements: corners 0, 1, 6, 7.
+    g = GraphText()
+    g.leaf("x", [2, 2, 2])
+    g.op("t", "relu", "x")
+    g.op("p1", "permute", "t", dims=[1, 0, 2])
+    g.op("p2", "permute", "t", dims=[2, 1, 0])
+    g.op("y", "add", "p1", "p2")
+    g.output("y", [2, 2, 2])
+    # y, p2, p1 map their corners to themselves; t's element 6 = (1, 1, 0)
+    # reaches y[1, 1, 0] = 6 through p1 and y[0, 1, 1] = 3 through p2: 3.
+    assert oracle.order_prefix(oracle.Graph(g.text()), 2, 1) == [0, 1, 6, 7, 3]
+
+
+def test_prefix_permuted_output_by_hand():
+    # y = permute(t) with t [4, 5]: blocks of 4 over 20 elements, lanes 1, 2.
+    g = GraphText()
+    g.leaf("x", [4, 5])
+    g.op("t", "relu", "x")
+    g.op("y", "permute", "t", dims=[1, 0])
+    g.output("y", [5, 4])
+    # y's corners 0, 3, 16, 19, 1, 2; t's element (a, b) is y[b, a] = 4b + a.
+    assert oracle.order_prefix(oracle.Graph(g.text()), 4, 2) == [0, 3, 16, 19, 1, 2, 12, 7, 4, 8]
+
+
+def test_location_order_is_a_permutation_led_by_the_prefix():
+    text = W.c5_variant_text(n=1, c=4, hw=5, co=3)
+    g = oracle.Graph(text)
+    order = oracle.location_order(g, 5, 16, 4)
+    prefix = oracle.order_prefix(g, 16, 4)
+    assert order[: len(prefix)].tolist() == prefix
+    assert np.array_equal(np.sort(order), np.arange(g.output_numel))
+
+
+# ---- library (host side) against the oracle -----------------------------------
+@pytest.fixture(scope="module")
+def B():
+    from paper_2609_19611_amd import binding
+    return binding
+
+
+CAT = tiny_graphs.catalogue()
+SEPARABLE = sorted(set(CAT) - tiny_graphs.NONSEPARABLE)
+
+
+@pytest.mark.parametrize("name", SEPARABLE)
+def test_library_prefix_matches_oracle_catalogue(B, name):
+    text = CAT[name][0]
+    for threads, warp in [(256, 32), (4, 2), (7, 3), (1, 1)]:
+        assert B.dg_order_prefix(B.dg_graph_parse(text), threads, warp) == \
+            oracle.order_prefix(oracle.Graph(text), threads, warp), (threads, warp)
+
+
+@pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4"])
+def test_library_prefix_matches_oracle_workloads(B, name):
+    text = W.CONFIGS[name]["text"]()
+    assert B.dg_order_prefix(B.dg_graph_parse(text)) == oracle.order_prefix(oracle.Graph(text))
+
+
+def test_library_prefix_c5_variant_full_size(B):
+    # The full-size variant against the hand-derived map (the oracle's
+    # brute force over 33.5M elements per tensor is too slow for a unit test).
+    n, c, hw, co = 64, 64, 64, 128
+    got = B.dg_order_prefix(B.dg_graph_parse(W.c5_variant_text()))
+    m = n * co * hw * hw
+    corner = [0, 255, m - 256, m - 1, 31, 32]
+    want = list(corner)
+    for e in corner:
+        loc = _c5_nhwc_to_nchw(e, n, co, hw)
+        if loc not in want:
+            want.append(loc)
+    assert got == want
+    small = W.c5_variant_text(n=2, c=4, hw=6, co=3)
+    for threads, warp in [(256, 32), (16, 4)]:
+        assert B.dg_order_prefix(B.dg_graph_parse(small), threads, warp) == \
+            oracle.order_prefix(oracle.Graph(small), threads, warp)
+    for f in W.c5_faults()[:4]:
+        t = W.c5_variant_text(fault=f, n=2, c=4, hw=6, co=3)
+        assert B.dg_order_prefix(B.dg_graph_parse(t), 16, 4) == oracle.order_prefix(oracle.Graph(t), 16, 4)
+
+
+def test_library_prefix_unit_dims_and_paths(B):
+    g = GraphText()
+    g.leaf("x", [3, 1, 5])
+    g.op("r", "relu", "x")
+    g.op("s", "reshape", "r", shape=[3, 5])
+    g.op("y", "permute", "s", dims=[1, 0])
+    g.output("y", [5, 3])
+    text = g.text()
+    assert B.dg_order_prefix(B.dg_graph_parse(text), 4, 2) == oracle.order_prefix(oracle.Graph(text), 4, 2)
+    for extra in tiny_graphs.dag_catalogue().values():
+        assert B.dg_order_prefix(B.dg_graph_parse(extra), 4, 2) == oracle.order_prefix(oracle.Graph(extra), 4, 2)
+
+
+def test_order_argument_errors(B):
+    # Status codes: 0 ok, -1 DG_E_INVALID_ARG, -8 DG_E_WORKSPACE.
+    lib = B._lib
+    w = ctypes.c_int64()
+    g = B.dg_graph_parse(W.c1_text())
+    assert lib.dg_order_prefix(g.handle, 0, 32, None, 0, ctypes.byref(w)) == -1
+    assert lib.dg_order_prefix(g.handle, 4, 0, None, 0, ctypes.byref(w)) == -1
+    assert lib.dg_order_prefix(g.handle, 4, 2, None, 1, ctypes.byref(w)) == -1
+    assert lib.dg_order_prefix(g.handle, 4, 2, None, 0, ctypes.byref(w)) == 0 and w.value == 6  # 0, 3, 4, 7, 1, 2
+    bad = [(-1, 0, 0), (10, 0, 11), (10, 11, 0), (10, -1, 1), (10, 0, -1)]
+    for n_out, first, count in bad:
+        assert lib.dg_order_permute(n_out, 1, None, 0, first, count, None, ctypes.byref(w), None, 0,
+                                    None) == -1, (n_out, first, count)
+    assert lib.dg_order_permute(10, 1, None, 1, 0, 0, None, ctypes.byref(w), None, 0, None) == -1
+    # An excluded value outside [0, n_out), and a missing workspace, are
+    # reported before any device work.
+    ex = (ctypes.c_int64 * 2)(3, 10)
+    assert lib.dg_order_permute(10, 1, ex, 2, 0, 10, ctypes.c_void_p(16), ctypes.byref(w), None, 0, None) == -1
+    ex = (ctypes.c_int64 * 1)(3)
+    assert lib.dg_order_permute(10, 1, ex, 1, 0, 10, ctypes.c_void_p(16), ctypes.byref(w), None, 0, None) == -8
+    assert B.dg_order_workspace_size(0) >= 8
