@@ -43,6 +43,10 @@ def parse_args():
                    help="time dg_enumerate_sizes + dg_enumerate_fill instead of the single-pass dg_enumerate")
     p.add_argument("--wide", action="store_true",
                    help="time dg_enumerate_wide (64-bit ids and counts) instead of dg_enumerate")
+    p.add_argument("--merge", action="store_true",
+                   help="time the comparison of the paper's two whole programs (shared convolution, reference "
+                        "ops vs fused kernel) at every output location, after MERGE with and without trimming "
+                        "the common prefix")
     p.add_argument("--order", action="store_true",
                    help="time the location order (keyed permutation of every output location of the c5 split-K "
                         "variant, corner and boundary prefix left out) and count the locations checked before "
@@ -268,6 +272,69 @@ def dag_bench(args, B, g, cfg, locs, text):
     print(json.dumps(line), flush=True)
 
 
+def merge_bench(args, B):
+    """The running example as whole programs (both start with the same
+    convolution): a step is dg_compare of the merged pair, common prefix
+    trimmed, over all 131,072 output locations.  The same comparison of the
+    untrimmed obligation (inputs matched only) and the merge itself are
+    timed beside it."""
+    import torch
+    from paper_2609_19611_amd import workloads as W
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    a = B.dg_graph_parse(W.paper_program_text(False))
+    b = B.dg_graph_parse(W.paper_program_text(True))
+    t0 = time.perf_counter()
+    ta, tb, k = B.dg_graph_merge(a, b, True)
+    merge_ms = (time.perf_counter() - t0) * 1e3
+    ua, ub, _ = B.dg_graph_merge(a, b, False)
+    n = B.dg_graph_info(ta)["output_numel"]
+    locs = torch.arange(n, dtype=torch.int64, device=dev)
+    ws = torch.empty(max(B.dg_workspace_size(ta, n), B.dg_workspace_size(ua, n), 1), dtype=torch.uint8,
+                     device=dev)
+    status = torch.empty(n, dtype=torch.uint8, device=dev)
+    mism = torch.empty(n, dtype=torch.int64, device=dev)
+
+    def timed(x, y, steps, warmup):
+        for _ in range(max(1, warmup)):
+            m = B.dg_compare(x, y, locs, status, mism, ws)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        for _ in range(steps):
+            m = B.dg_compare(x, y, locs, status, mism, ws)
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t1) / steps, m
+
+    dt, mism_trim = timed(ta, tb, args.steps, args.warmup)
+    du, mism_full = timed(ua, ub, max(1, args.steps // 5), 1)
+    line = {
+        "metric": "output locations/sec compared after MERGE (common prefix trimmed)",
+        "value": n / dt, "unit": "locations/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": dt * 1e3, "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "u32",
+        "data": "synthetic (shapes only; footprints are data independent)",
+        "config": {"workload": "paper running example as whole programs: x[128,3,64,64] -> conv(16, k3 p1) -> "
+                               "min(C) -> sum(H) -> gelu -> +b vs the fused min/sum kernel (h < 32)",
+                   "locations": n, "trimmed_ops": k, "merge_host_ms": merge_ms,
+                   "mismatching_locations_trimmed": int(mism_trim),
+                   "mismatching_locations_untrimmed": int(mism_full),
+                   "untrimmed_locations_per_s": n / du, "untrimmed_ms_per_compare": du * 1e3,
+                   "speedup_from_trimming": du / dt},
+        "roofline": {"bound": "alu", "achieved": None, "peak": None, "unit": None, "frac": None, "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        oa, ob, _ = oracle.merge(oracle.Graph(W.paper_program_text(False)), oracle.Graph(W.paper_program_text(True)))
+        ga, gb = oracle.Graph(oa), oracle.Graph(ob)
+        m = 4096
+        t1 = time.perf_counter()
+        oracle.compare(ga, gb, list(range(m)), threads=os.cpu_count() or 1)
+        d = time.perf_counter() - t1
+        line["cpu_baseline"] = {"value": m / d, "unit": "locations/s", "cores": os.cpu_count() or 1,
+                                "kind": "oracle", "sample": f"first {m} of {n} locations, trimmed pair"}
+    line["git"] = git_sha()
+    print(json.dumps(line), flush=True)
+
+
 def order_bench(args, B):
     """The location order of the c5 split-K variant (33,554,432 output
     locations): a step is dg_order_permute over every permutation position
@@ -383,9 +450,9 @@ def main():
     if args.copy_gib > 0:
         copy_calibration(args.copy_gib, args.steps, args.warmup)
         return
-    if args.order:
+    if args.order or args.merge:
         from paper_2609_19611_amd import binding as B
-        order_bench(args, B)
+        (order_bench if args.order else merge_bench)(args, B)
         return
 
     import torch

@@ -392,6 +392,31 @@ dg_status dg_compare_range(const dg_graph* a, const dg_graph* b, int64_t first, 
                            void* stream);
 
 /* Message of the calling thread's last failed call ("" if none). */
+/* dg_graph_text: the graph as dgir v1 text (leaves, ops in SSA order,
+ * output); writes at most cap - 1 characters and a terminating NUL to buf
+ * (host; may be NULL when cap is 0) and the full length to *len. */
+dg_status dg_graph_text(const dg_graph* g, char* buf, size_t cap, size_t* len);
+
+/* dg_graph_merge: MERGE of two programs (Sec. 3.2) into one obligation.
+ *  - Inputs are matched: a leaf of b pairs with the leaf of a of the same
+ *    name and shape, the rest pair in declaration order among leaves of the
+ *    same shape; an input without a partner, or different output shapes,
+ *    give DG_E_SIGNATURE.
+ *  - With trim_prefix nonzero, the longest common prefix of ops is
+ *    trimmed: op i of a and op i of b
+ *    match when kind, attributes and (matched) operands agree.  The prefix
+ *    results that later ops of either graph read, or that are an output,
+ *    become leaves, appended after a's leaves in prefix order.  A common
+ *    suffix is never trimmed.
+ * *a_out and *b_out receive two new graphs (owned by the caller, free with
+ * dg_graph_destroy) over the same leaves in the same order under a's names,
+ * ready for dg_compare; *n_trimmed (may be NULL) the number of prefix ops.
+ * The trimming keeps equivalence when the prefix is surjective; in any case
+ * a location that compares equal after trimming compares equal before
+ * (rows compose through the shared prefix). */
+dg_status dg_graph_merge(const dg_graph* a, const dg_graph* b, int32_t trim_prefix, dg_graph** a_out,
+                         dg_graph** b_out, int32_t* n_trimmed);
+
 /*
  * Location order (Sec. 4, "Search Heuristic": candidate locations ranked in
  * tiers, then a random permutation of the unchecked ones).  The tier that

@@ -80,6 +80,8 @@ def _load():
     lib.dgo_permutation.argtypes = [i64, ctypes.c_uint64, i64, i64, P]
     lib.dgo_feistel.argtypes = [i64, ctypes.c_uint64, ctypes.c_int, P, i64, P]
     lib.dgo_splitmix.argtypes = [ctypes.c_uint64, i64, P]
+    lib.dgo_merge.argtypes = [P, P, ctypes.c_int, ctypes.c_char_p, i64, P]
+    lib.dgo_merge.restype = i64
     _lib = lib
     return lib
 
@@ -267,3 +269,18 @@ def location_order(g: Graph, seed: int, threads: int = 256, warp: int = 32) -> n
     if prefix:
         rest = rest[~np.isin(rest, np.asarray(prefix, dtype=np.int64))]
     return np.concatenate([np.asarray(prefix, dtype=np.int64), rest])
+
+
+# ---- MERGE (Sec. 3.2) -------------------------------------------------------------
+def merge(a: Graph, b: Graph, trim: bool = True) -> tuple[str, str, int]:
+    """Matched inputs and (with trim) the common op prefix trimmed: (text of
+    a, text of b, number of prefix ops)."""
+    lib = _load()
+    k = ctypes.c_int()
+    n = lib.dgo_merge(a._h, b._h, 1 if trim else 0, None, 0, ctypes.byref(k))
+    if n < 0:
+        raise OracleError(lib.dgo_error().decode())
+    buf = ctypes.create_string_buffer(n)
+    lib.dgo_merge(a._h, b._h, 1 if trim else 0, buf, n, ctypes.byref(k))
+    ta, tb = buf.raw[:n].split(b"\0")
+    return ta.decode(), tb.decode(), k.value

@@ -182,6 +182,7 @@ struct Op {
   int out = -1;
   std::map<std::string, std::vector<int64_t>> attr;
   std::vector<std::vector<Expr>> idx;  // affine_gather
+  std::map<std::string, std::string> raw;  // attribute text as written (key -> value)
 };
 
 struct Graph {
@@ -546,6 +547,7 @@ Graph parse_graph(const std::string& text) {
             raw[toks[i].substr(0, eq)] = toks[i].substr(eq + 1);
           }
         }
+        op.raw = raw;
         if (op.kind == "affine_gather") {
           op.idx.resize(op.in.size());
           for (size_t j = 0; j < op.in.size(); ++j) {
@@ -1242,6 +1244,138 @@ struct Permutation {
 // C interface used by the Python test harness (ctypes).
 // Returns 0 on success, -1 on error (message via dgo_error()).
 // ---------------------------------------------------------------------------
+namespace {
+
+// ---- MERGE (Sec. 3.2): matched inputs, trimmed common prefix ----------------
+// The two programs must take the same inputs: a leaf of b pairs with the leaf
+// of a of the same name and shape, the others pair in declaration order among
+// leaves of one shape.  Then the longest common prefix of ops (same kind,
+// same attributes, paired operands) is trimmed; its results that a remaining
+// op or an output still uses become inputs shared by both, after a's leaves
+// in prefix order.  No suffix is trimmed.
+struct Merged {
+  std::string a, b;
+  int trimmed = 0;
+};
+
+std::string shape_text(const Shape& s) {
+  std::string o;
+  for (size_t i = 0; i < s.size(); ++i) o += (i ? "," : "") + std::to_string(s[i]);
+  return o;
+}
+
+std::string op_line(const Graph& g, const Op& op, const std::vector<std::string>& name) {
+  std::string o = "op " + name[op.out] + " " + op.kind;
+  for (int t : op.in) o += " " + name[t];
+  if (!op.raw.empty()) {
+    o += " ;";
+    for (const auto& kv : op.raw) o += " " + kv.first + "=" + kv.second;
+  }
+  return o + "\n";
+}
+
+bool same_attrs(const Op& x, const Op& y) {
+  if (x.kind != y.kind || x.in.size() != y.in.size() || x.attr != y.attr) return false;
+  for (const auto& kv : x.raw)
+    if (kv.first.compare(0, 3, "idx") == 0) {
+      auto it = y.raw.find(kv.first);
+      if (it == y.raw.end() || it->second != kv.second) return false;
+    }
+  return true;
+}
+
+Merged merge_programs(const Graph& a, const Graph& b, bool trim) {
+  const size_t na = a.leaves.size(), nb = b.leaves.size();
+  std::vector<int> pa(na, -1), pb(nb, -1);  // partner leaf positions
+  for (size_t j = 0; j < nb; ++j)
+    for (size_t i = 0; i < na; ++i) {
+      const Tensor &x = a.tensors[a.leaves[i]], &y = b.tensors[b.leaves[j]];
+      if (pa[i] < 0 && x.name == y.name && x.shape == y.shape) {
+        pa[i] = (int)j;
+        pb[j] = (int)i;
+        break;
+      }
+    }
+  for (size_t j = 0; j < nb; ++j) {
+    if (pb[j] >= 0) continue;
+    for (size_t i = 0; i < na; ++i)
+      if (pa[i] < 0 && a.tensors[a.leaves[i]].shape == b.tensors[b.leaves[j]].shape) {
+        pa[i] = (int)j;
+        pb[j] = (int)i;
+        break;
+      }
+    if (pb[j] < 0) throw Error("merge: an input of the second program has no partner");
+  }
+  for (size_t i = 0; i < na; ++i)
+    if (pa[i] < 0) throw Error("merge: an input of the first program has no partner");
+  if (a.tensors[a.output].shape != b.tensors[b.output].shape) throw Error("merge: output shapes differ");
+
+  std::vector<int> same(b.tensors.size(), -1);  // tensor of a each tensor of b equals
+  for (size_t j = 0; j < nb; ++j) same[b.leaves[j]] = a.leaves[pb[j]];
+  size_t k = 0;
+  for (; trim && k < a.ops.size() && k < b.ops.size(); ++k) {
+    const Op &x = a.ops[k], &y = b.ops[k];
+    if (!same_attrs(x, y)) break;
+    bool operands = true;
+    for (size_t q = 0; q < x.in.size(); ++q) operands = operands && same[y.in[q]] == x.in[q];
+    if (!operands) break;
+    same[y.out] = x.out;
+  }
+  // Prefix results still used (tensors of a).
+  std::vector<int> prefix_op_a(a.tensors.size(), -1), prefix_op_b(b.tensors.size(), -1);
+  for (size_t i = 0; i < k; ++i) {
+    prefix_op_a[a.ops[i].out] = (int)i;
+    prefix_op_b[b.ops[i].out] = (int)i;
+  }
+  std::set<int> used;
+  for (size_t i = k; i < a.ops.size(); ++i)
+    for (int t : a.ops[i].in)
+      if (prefix_op_a[t] >= 0) used.insert(t);
+  for (size_t i = k; i < b.ops.size(); ++i)
+    for (int t : b.ops[i].in)
+      if (prefix_op_b[t] >= 0) used.insert(same[t]);
+  if (prefix_op_a[a.output] >= 0) used.insert(a.output);
+  if (prefix_op_b[b.output] >= 0) used.insert(same[b.output]);
+
+  std::string leaves;
+  std::set<std::string> taken;
+  for (int t : a.leaves) {
+    leaves += "leaf " + a.tensors[t].name + " " + shape_text(a.tensors[t].shape) + "\n";
+    taken.insert(a.tensors[t].name);
+  }
+  for (size_t i = 0; i < k; ++i)
+    if (used.count(a.ops[i].out)) {
+      const Tensor& t = a.tensors[a.ops[i].out];
+      leaves += "leaf " + t.name + " " + shape_text(t.shape) + "\n";
+      taken.insert(t.name);
+    }
+  Merged m;
+  m.trimmed = (int)k;
+  std::vector<std::string> an(a.tensors.size());
+  for (size_t t = 0; t < a.tensors.size(); ++t) an[t] = a.tensors[t].name;
+  m.a = "dgir 1\n" + leaves;
+  for (size_t i = k; i < a.ops.size(); ++i) m.a += op_line(a, a.ops[i], an);
+  m.a += "output " + an[a.output] + " " + shape_text(a.tensors[a.output].shape) + "\n";
+  std::vector<std::string> bn(b.tensors.size());
+  std::set<std::string> names = taken;
+  for (size_t t = 0; t < b.tensors.size(); ++t) {
+    if (same[t] >= 0) {
+      bn[t] = a.tensors[same[t]].name;
+      continue;
+    }
+    std::string nm = b.tensors[t].name;
+    for (int s = 1; names.count(nm); ++s) nm = b.tensors[t].name + "_" + std::to_string(s);
+    names.insert(nm);
+    bn[t] = nm;
+  }
+  m.b = "dgir 1\n" + leaves;
+  for (size_t i = k; i < b.ops.size(); ++i) m.b += op_line(b, b.ops[i], bn);
+  m.b += "output " + bn[b.output] + " " + shape_text(b.tensors[b.output].shape) + "\n";
+  return m;
+}
+
+}  // namespace
+
 extern "C" {
 
 struct dgo_graph { Graph g; };
@@ -1371,6 +1505,23 @@ int dgo_compare(const dgo_graph* a, const dgo_graph* b, const int64_t* locs, int
         status[i] = compare_rows(narrow(enumerate_one(a->g, locs[i])), narrow(enumerate_one(b->g, locs[i])));
     });
     return 0;
+  } catch (const std::exception& e) {
+    g_err = e.what();
+    return -1;
+  }
+}
+
+// MERGE of two programs (trim = 0: inputs matched, no op trimmed): the two
+// dgir texts, NUL-separated, into
+// out (up to cap bytes); returns the bytes needed, or -1 on error.  *trimmed
+// receives the number of prefix ops.
+int64_t dgo_merge(const dgo_graph* a, const dgo_graph* b, int trim, char* out, int64_t cap, int* trimmed) {
+  try {
+    Merged m = merge_programs(a->g, b->g, trim != 0);
+    std::string s = m.a + std::string(1, '\0') + m.b;
+    if ((int64_t)s.size() <= cap) memcpy(out, s.data(), s.size());
+    *trimmed = m.trimmed;
+    return (int64_t)s.size();
   } catch (const std::exception& e) {
     g_err = e.what();
     return -1;

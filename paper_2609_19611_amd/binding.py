@@ -118,6 +118,8 @@ def _load():
         "dg_dag_sizes": ([P, P, i64, P, P, P, ctypes.POINTER(i64), ctypes.POINTER(i64), P], i32),
         "dg_dag_fill": ([P, P, i64, P, P, P, P, P, P, P, P], i32),
         "dg_order_prefix": ([P, i32, i32, P, i64, ctypes.POINTER(i64)], i32),
+        "dg_graph_text": ([P, ctypes.c_char_p, sz, ctypes.POINTER(sz)], i32),
+        "dg_graph_merge": ([P, P, i32, ctypes.POINTER(P), ctypes.POINTER(P), ctypes.POINTER(i32)], i32),
         "dg_order_workspace_size": ([i64, ctypes.POINTER(sz)], i32),
         "dg_order_permute": ([i64, ctypes.c_uint64, P, i64, i64, i64, P, ctypes.POINTER(i64), P, sz, P], i32),
         "dg_last_error": ([], ctypes.c_char_p),
@@ -473,6 +475,24 @@ def dag_locations(g: Graph, locs, stream=None) -> dict:
     for k, m in (("nodes", nn), ("node_edge", nn), ("edges", ne), ("mults", ne)):
         out[k] = out[k][:m]
     return out
+
+
+def dg_graph_text(g: Graph) -> str:
+    """The graph as dgir v1 text."""
+    n = ctypes.c_size_t()
+    _check(_lib.dg_graph_text(g.handle, None, 0, ctypes.byref(n)))
+    buf = ctypes.create_string_buffer(n.value + 1)
+    _check(_lib.dg_graph_text(g.handle, buf, n.value + 1, ctypes.byref(n)))
+    return buf.value.decode()
+
+
+def dg_graph_merge(a: Graph, b: Graph, trim_prefix: bool = True) -> tuple[Graph, Graph, int]:
+    """MERGE: the two graphs with matched inputs and (by default) the common
+    prefix trimmed, and the number of trimmed ops."""
+    ha, hb, k = ctypes.c_void_p(), ctypes.c_void_p(), ctypes.c_int32()
+    _check(_lib.dg_graph_merge(a.handle, b.handle, 1 if trim_prefix else 0, ctypes.byref(ha), ctypes.byref(hb),
+                               ctypes.byref(k)))
+    return Graph(ha.value), Graph(hb.value), k.value
 
 
 def dg_order_prefix(g: Graph, block_threads: int = 256, warp: int = 32) -> list[int]:

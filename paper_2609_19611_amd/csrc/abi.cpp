@@ -18,6 +18,7 @@
 #include "jit.h"
 #include "kernels.h"
 #include "order.h"
+#include "merge.h"
 
 // Specialised kernels of a graph on one device.
 struct DevKernels {
@@ -782,6 +783,41 @@ dg_status dg_dag_fill(const dg_graph* g, const int64_t* d_locs, int64_t n, const
     DG_HIP(hipStreamSynchronize(s), "DAG fill sync");
     return device_errors(bits);
   });
+}
+
+dg_status dg_graph_text(const dg_graph* g, char* buf, size_t cap, size_t* len) {
+  if (!g || !len || (cap > 0 && !buf)) return set_error(DG_E_INVALID_ARG, "bad argument");
+  return guarded([&]() -> dg_status {
+    const std::string t = dg::graph_text(g->ir);
+    *len = t.size();
+    if (cap > 0) {
+      const size_t n = std::min(cap - 1, t.size());
+      std::memcpy(buf, t.data(), n);
+      buf[n] = '\0';
+    }
+    return DG_OK;
+  });
+}
+
+dg_status dg_graph_merge(const dg_graph* a, const dg_graph* b, int32_t trim_prefix, dg_graph** a_out,
+                         dg_graph** b_out, int32_t* n_trimmed) {
+  if (!a || !b || !a_out || !b_out) return set_error(DG_E_INVALID_ARG, "bad argument");
+  *a_out = *b_out = nullptr;
+  dg_status st = guarded([&]() -> dg_status {
+    const dg::Merged m = dg::merge_graphs(a->ir, b->ir, trim_prefix != 0);
+    dg_status s = dg_graph_parse(m.a_text.c_str(), m.a_text.size(), a_out);
+    if (s != DG_OK) return s;
+    s = dg_graph_parse(m.b_text.c_str(), m.b_text.size(), b_out);
+    if (s != DG_OK) return s;
+    if (n_trimmed) *n_trimmed = m.trimmed;
+    return DG_OK;
+  });
+  if (st != DG_OK) {
+    if (*a_out) dg_graph_destroy(*a_out);
+    if (*b_out) dg_graph_destroy(*b_out);
+    *a_out = *b_out = nullptr;
+  }
+  return st;
 }
 
 dg_status dg_order_prefix(const dg_graph* g, int32_t block_threads, int32_t warp, int64_t* h_prefix, int64_t cap,

@@ -355,6 +355,39 @@ def paper_kernel_text(N=128, C=16, H=64, W=64, h_limit=32) -> str:
     return g.text()
 
 
+def paper_program_text(kernel: bool, N=128, Cin=3, C=16, H=64, W=64, h_limit=32) -> str:
+    """The running example as the two whole programs that MERGE receives
+    (Sec. 3.2, the trace-merge illustration): both start with the same
+    convolution, whose result M is then reduced by the reference ops or by
+    the fused kernel (``paper_reference_text`` / ``paper_kernel_text`` from M
+    on).  The kernel program names and orders its inputs differently, so
+    that its inputs are matched by shape."""
+    g = GraphText()
+    conv = dict(stride=[1, 1], pad=[1, 1], dilation=[1, 1], groups=1)
+    if not kernel:
+        g.leaf("x", [N, Cin, H, W])
+        g.leaf("Wt", [C, Cin, 3, 3])
+        g.leaf("conv_b", [C])
+        g.leaf("b", [C, 1])
+        g.op("M", "conv", "x", "Wt", "conv_b", **conv)
+        g.op("R", "amin", "M", dims=1, keepdim=0)
+        g.op("S", "sum", "R", dims=1, keepdim=1)
+        g.op("G", "gelu", "S")
+        g.op("Y", "add", "G", "b")
+    else:
+        g.leaf("wgt", [C, Cin, 3, 3])
+        g.leaf("inp", [N, Cin, H, W])
+        g.leaf("bias", [C, 1])
+        g.leaf("cb", [C])
+        g.op("conv_out", "conv", "inp", "wgt", "cb", **conv)
+        g.op("S", "affine_gather", "conv_out", shape=[N, 1, W], window=[C, h_limit],
+             idx0=["o0", "w0", "w1", "o2"], mult=[1])
+        g.op("G", "gelu", "S")
+        g.op("Y", "add", "G", "bias")
+    g.output("Y", [N, C, W])
+    return g.text()
+
+
 CONFIGS = {
     "c1": dict(text=c1_text, numel=8, n_locs=8, seed=None,
                desc="matmul A[8x16]@B[16x8] -> relu -> row-sum"),
