@@ -130,7 +130,10 @@ dg_status dag_program(const dg_graph* cg, const uint8_t** out) {
     try {
       // Small DAGs (a few thousand references per location) run on one wave.
       dg::DagProgram probe = dg::compile_dag(g->ir, 64);
-      g->dag_block = probe.max_edges >= 4096 ? 256 : 64;
+      // Four waves when some op has more than four waves' worth of nodes
+      // (the batches of nodes then run side by side) and the DAG is large;
+      // one wave otherwise (its barriers are nearly free).
+      g->dag_block = probe.max_edges >= 4096 && probe.max_frontier > 256 ? 256 : 64;
       g->dag = g->dag_block == 64 ? std::move(probe) : dg::compile_dag(g->ir, g->dag_block);
     } catch (const dg::Failure& f) {
       g->dag_status = (dg_status)f.code;

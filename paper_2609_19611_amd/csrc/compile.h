@@ -61,6 +61,7 @@ struct DagProgram {
   int max_vars = 0;
   int64_t max_nodes = 0;       // static bounds for one location
   int64_t max_edges = 0;
+  int64_t max_frontier = 0;    // largest frontier capacity (nodes of one op, bound)
   std::vector<uint64_t> gid;   // global id of element 0 per tensor
 };
 DagProgram compile_dag(const GraphIR& g, int nthreads);

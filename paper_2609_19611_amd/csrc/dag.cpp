@@ -165,6 +165,7 @@ DagProgram compile_dag(const GraphIR& g, int nthreads) {
   }
   // Edge counts: one per node of a pointwise op, one per batch of `lanes`
   // nodes otherwise.
+  for (int t = 0; t < nt; ++t) p.max_frontier = std::max<int64_t>(p.max_frontier, T[t].cap);
   int64_t ncount_cap = 1;
   for (const OpNode& op : g.ops) {
     bool pointwise = true;

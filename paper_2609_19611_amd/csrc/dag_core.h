@@ -474,7 +474,7 @@ DGC void flat_emit(C& c, const DagCtx& x, const DgdGroup& G, const Slots& S, uin
 }
 
 // Writes group G's edges of the batch node in lane column j (a node with
-// at least four waves of points): the wave covers the node's points with
+// at least half a wave of points): the wave covers the node's points with
 // its lanes, the digits of each lane's point advancing by the wave width
 // with carries.  NOP operands and Q window variables are compile-time
 // constants, so the steps stay in registers.
@@ -673,9 +673,9 @@ DGC bool dag_op(C& c, const DagCtx& x, const DgdOp& op, uint32_t* NC, const Slot
             S.glo(lane) = (uint32_t)gpos;
             S.ghi(lane) = (uint32_t)(gpos >> 32);
           }
-          // Nodes with at least four waves of points node by node, the
+          // Nodes with at least half a wave of points node by node, the
           // others flattened across the lanes.
-          const bool big = Pj >= 4u * (uint32_t)L;
+          const bool big = Pj >= (uint32_t)((L + 1) / 2);
           const uint64_t mask = c.ballot(big);
           c.wave_sync();
           const bool done = mask != 0 && emit_nodes(c, x, G, S, mask, o, emit, append);
