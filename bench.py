@@ -28,6 +28,9 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 ALU_PEAK_TOPS = 256 * 4 * 16 * 2.4e9 / 1e12  # int32 VALU operations, no packing
+# A comparison's per-entry work: the entry's id (one add of two table
+# parts), its count (one product) and its share of the equality test.
+COMPARE_OPS_PER_ENTRY = 3
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
 
 
@@ -511,6 +514,29 @@ def main():
         compares = len(variants_timed)
         value = n * compares / (elapsed / args.steps)
         extra = {}
+        roofline = {"bound": "alu", "achieved": None, "peak": None, "unit": None, "frac": None, "traffic": None}
+        if not args.full_output:
+            # The clean variant alone, whose every location compares whole
+            # rows: entries compared are both graphs' row entries (their
+            # sizes, untimed), priced at COMPARE_OPS_PER_ENTRY int32 ops.
+            offs = torch.empty(n + 1, dtype=torch.int64, device=dev)
+            entries = B.dg_enumerate_sizes(g, d_locs, offs, ws) + B.dg_enumerate_sizes(variants[0], d_locs, offs, ws)
+            ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+                  for _ in range(args.steps)]
+            for i in range(args.steps):
+                ev[i][0].record(stream)
+                B.dg_compare(g, variants[0], d_locs, status, mism, ws)
+                ev[i][1].record(stream)
+            torch.cuda.synchronize()
+            clean_ms = float(np.mean([x.elapsed_time(y) for x, y in ev]))
+            achieved = COMPARE_OPS_PER_ENTRY * entries / (clean_ms * 1e-3) / 1e12
+            extra = {"clean_ms_per_compare": clean_ms, "clean_entries_compared": entries,
+                     "clean_entries_compared_per_s": entries / (clean_ms * 1e-3),
+                     "clean_locations_per_s": n / (clean_ms * 1e-3)}
+            roofline = {"bound": "alu", "kernel": "dg_compare (clean variant, whole call)", "achieved": achieved,
+                        "peak": ALU_PEAK_TOPS, "unit": "Tops/s (int32)", "frac": achieved / ALU_PEAK_TOPS,
+                        "traffic": None, "kernel_ms": clean_ms,
+                        "model": f"{COMPARE_OPS_PER_ENTRY} int32 ops per row entry of either graph"}
         if args.full_output:
             fault_ms = []
             for v in variants[1:]:
@@ -529,8 +555,7 @@ def main():
             "config": {"workload": "c5: " + cfg["desc"] + (" (full output)" if args.full_output else ""),
                        "locations": n, "compares_per_step": compares,
                        "mismatching_locations_last_step": int(mismatches), **extra},
-            "roofline": {"bound": "alu", "achieved": None, "peak": None, "unit": None, "frac": None,
-                         "traffic": None},
+            "roofline": roofline,
         }
         if not args.no_cpu_baseline:
             line["cpu_baseline"] = cpu_baseline("c5", text, W.c5_variant_text(), locs, args.cpu_seconds)

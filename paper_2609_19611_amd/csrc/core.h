@@ -697,6 +697,29 @@ DGC Word to_word(uint64_t v) {
   return sizeof(Word) == 4 ? (Word)(v > 0xFFFFFFFFull ? 0xFFFFFFFFull : v) : (Word)v;
 }
 
+// q = n / d and *rem = n % d for n < 2^20, d >= 1.  On the device a float
+// reciprocal gives a quotient within one of the exact one (relative error
+// below 2^-21, so an absolute error below 1/2 for these n), which one
+// correction step fixes; the host divides.
+DGC uint32_t table_divmod(uint32_t n, uint32_t d, uint32_t* rem) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  uint32_t q = (uint32_t)((float)n * __builtin_amdgcn_rcpf((float)d));
+  int32_t r = (int32_t)n - (int32_t)(q * d);
+  if (r < 0) {
+    --q;
+    r += (int32_t)d;
+  } else if (r >= (int32_t)d) {
+    ++q;
+    r -= (int32_t)d;
+  }
+  *rem = (uint32_t)r;
+  return q;
+#else
+  *rem = n % d;
+  return n / d;
+#endif
+}
+
 // Builds one table: entries r < n over dims [d0, d1); entry = (id part,
 // count part of every term).  With `tmax`, records each term's largest
 // value there (per-thread maxima, combined once per wave and term).
@@ -708,15 +731,16 @@ DGC void build_table(C& c, const LeafGeom& G, const TermRef* terms, int nterm, c
   int32_t u[DGP_MAX_RANK];
   DG_UNROLL
   for (int d = 0; d < DGP_MAX_RANK; ++d) u[d] = H->u[d];
-  // Coordinates of entry r (row-major over the union lists of [d0, d1)).
+  // Coordinates of entry r (row-major over the union lists of [d0, d1);
+  // tables hold at most 8192 entries).
   auto coords = [&](uint32_t r, int32_t* x) {
     uint32_t rem = r;
     DG_UNROLL
     for (int d = DGP_MAX_RANK - 1; d >= 0; --d) {
       x[d] = 0;
       if (d >= d0 && d < d1) {
-        const uint32_t i = rem % (uint32_t)u[d];
-        rem /= (uint32_t)u[d];
+        uint32_t i;
+        rem = table_divmod(rem, (uint32_t)u[d], &i);
         x[d] = ucoord(H, ulist, d, (int32_t)i);
       }
     }
@@ -740,6 +764,28 @@ DGC void build_table(C& c, const LeafGeom& G, const TermRef* terms, int nterm, c
       m = v > m ? v : m;
     }
     if (tmax) c.reduce_max(&tmax[0], m);
+    return;
+  }
+  if (!tmax) {
+    // Several terms and no maxima to record: one pass, each entry's
+    // coordinates decoded once for all terms.
+    for (uint32_t r = (uint32_t)c.tid(); r < n; r += (uint32_t)c.nthreads()) {
+      int32_t x[DGP_MAX_RANK];
+      coords(r, x);
+      uint64_t pos = with_base ? G.base : 0u;
+      DG_UNROLL
+      for (int d = 0; d < DGP_MAX_RANK; ++d)
+        if (d >= d0 && d < d1) pos += (uint64_t)x[d] * G.stride[d];
+      tab[(uint64_t)r * W] = (Word)pos;
+      DG_PLAN_UNROLL
+      for (int t = 0; t < nterm; ++t) {
+        uint64_t v = with_base ? terms[t].coef : 1ull;
+        DG_UNROLL
+        for (int d = 0; d < DGP_MAX_RANK; ++d)
+          if (d >= d0 && d < d1 && v) v = mul_sat(v, term_val(terms[t], d, x[d], a64));
+        tab[(uint64_t)r * W + 1 + t] = to_word<Word>(v);
+      }
+    }
     return;
   }
   for (uint32_t r = (uint32_t)c.tid(); r < n; r += (uint32_t)c.nthreads()) {
@@ -954,15 +1000,18 @@ DGC uint64_t leaf_emit(C& c, const LeafGeom& G, int split, const TermRef* terms,
       return total;
     }
     // Several terms: evaluate each cell, keep the nonzero ones in order.
+    // Cell p is (outer r, inner j) = (p / In, p % In); (r, j) advances by
+    // the block's width each chunk.  (Tables hold fewer than 2^32 cells, so
+    // cell indices fit 32 bits.)
     uint64_t written = 0;
     uint32_t flags = 0;
+    uint32_t r = (uint32_t)tid / In, j = (uint32_t)tid % In;
+    const uint32_t dr = (uint32_t)nt / In, dj = (uint32_t)nt % In;
     for (uint64_t chunk = 0; chunk < total; chunk += (uint64_t)nt) {
       const uint64_t p = chunk + (uint64_t)tid;
       uint64_t ca = 0, cb = 0;
       Word pos = 0;
       if (p < total) {
-        // (Tables hold fewer than 2^32 cells, so cell indices fit 32 bits.)
-        const uint32_t r = (uint32_t)p / In, j = (uint32_t)p - r * In;
         const Word* o = otab + (uint64_t)r * W;
         const Word* q = itab + (uint64_t)j * W;
         pos = o[0] + q[0];
@@ -970,6 +1019,12 @@ DGC uint64_t leaf_emit(C& c, const LeafGeom& G, int split, const TermRef* terms,
         for (int t = 0; t < na; ++t) ca += (uint64_t)o[1 + t] * q[1 + t];
         DG_PLAN_UNROLL
         for (int t = na; t < nterm; ++t) cb += (uint64_t)o[1 + t] * q[1 + t];
+      }
+      j += dj;
+      r += dr;
+      if (j >= In) {
+        j -= In;
+        ++r;
       }
       if (MODE == EMIT_COMPARE) {
         if ((ca == 0) != (cb == 0)) flags |= 1u;

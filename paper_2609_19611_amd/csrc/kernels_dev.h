@@ -90,7 +90,12 @@ struct DevCtx {
     *total = tot;
     return before + pre;
   }
-  DGC bool any(bool f) const { return __syncthreads_or(f) != 0; }
+  // Whether f holds on any thread of the block.  A one-wave block takes
+  // the wave's ballot instead of the block-wide reduction.
+  DGC bool any(bool f) const {
+    if (BLOCK == 64) return __ballot(f) != 0;
+    return __syncthreads_or(f) != 0;
+  }
 };
 
 extern __shared__ uint64_t dg_smem[];
