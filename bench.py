@@ -136,7 +136,7 @@ def cpu_baseline(workload, text_a, text_b, locs, target_s):
     threads = min(16, os.cpu_count() or 1)
     if workload == "c5":
         ga, gb = oracle.Graph(text_a), oracle.Graph(text_b)
-        m = 256
+        m = min(256, len(locs))
         while True:
             t0 = time.perf_counter()
             oracle.compare(ga, gb, locs[:m], threads=threads)
@@ -148,7 +148,7 @@ def cpu_baseline(workload, text_a, text_b, locs, target_s):
                 "sample": f"first {m} of {len(locs)} locations, one compare (clean variant)",
                 "seconds": round(dt, 3)}
     g = oracle.Graph(text_a)
-    m = 16
+    m = min(16, len(locs))
     while True:
         t0 = time.perf_counter()
         off, _, _ = g.enumerate(locs[:m], threads=threads)
@@ -156,9 +156,17 @@ def cpu_baseline(workload, text_a, text_b, locs, target_s):
         if dt > 0.5 * target_s or m >= len(locs):
             break
         m = min(len(locs), int(m * min(64.0, max(2.0, 0.8 * target_s / max(dt, 1e-3)))))
-    return {"value": float(off[-1]) / dt, "unit": "entries/s", "cores": threads, "kind": "oracle",
-            "sample": f"first {m} of {len(locs)} locations", "locations_per_s": m / dt,
-            "seconds": round(dt, 3)}
+    reps = 1
+    if dt < 1.0:
+        # The whole list takes under a second: repeat it for about a second.
+        reps = int(min(1000, max(2, 1.0 / max(dt, 1e-4))))
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            off, _, _ = g.enumerate(locs[:m], threads=threads)
+        dt = time.perf_counter() - t0
+    sample = f"first {m} of {len(locs)} locations" + (f", {reps} passes" if reps > 1 else "")
+    return {"value": float(off[-1]) * reps / dt, "unit": "entries/s", "cores": threads, "kind": "oracle",
+            "sample": sample, "locations_per_s": m * reps / dt, "seconds": round(dt, 3)}
 
 
 def stream_full_output(args, B, g, cfg, info, text):
