@@ -823,12 +823,25 @@ Plan Compiler::run() {
   level_start.push_back((int32_t)sorted.size());
   ins_.swap(sorted);
 
-  // Factor value offsets.
+  // Factor value offsets: the factors leaf terms read first, then those of
+  // intermediate tensors only.
+  std::vector<char> live(fac_.size(), 0);
+  for (const DgpLeaf& L : leaves)
+    for (int t = 0; t < L.nterm; ++t)
+      for (int d = 0; d < L.rank; ++d) {
+        const int f = dterms[(size_t)(L.term0 + t)].factor[d];
+        if (f >= 0 && f < (int)fac_.size()) live[(size_t)f] = 1;
+      }
   int64_t fval = 0;
-  for (auto& f : fac_) {
-    f.off = (int32_t)fval;
-    fval += f.cap;
-  }
+  for (int pass = 1; pass >= 0; --pass)
+    for (size_t i = 0; i < fac_.size(); ++i)
+      if (live[i] == pass) {
+        fac_[i].off = (int32_t)fval;
+        fval += fac_[i].cap;
+      }
+  int64_t fval_live = 0;
+  for (size_t i = 0; i < fac_.size(); ++i)
+    if (live[i]) fval_live += fac_[i].cap;
   DgpHeader h;
   std::memset(&h, 0, sizeof(h));
   h.magic = DGP_MAGIC;
@@ -846,6 +859,7 @@ Plan Compiler::run() {
   h.nleaf = (int32_t)leaves.size();
   h.nterm = (int32_t)dterms.size();
   h.fval_entries = (int32_t)fval;
+  h.fval_live = (int32_t)fval_live;
   h.max_leaf_terms = plan.max_leaf_terms;
   h.emit_entries = (int32_t)emit_entries;
   h.union_entries = (int32_t)union_entries;
@@ -958,8 +972,10 @@ void pair_plan(const Plan& a, const Plan& b, int nthreads, dgc::PairPlan* pp) {
   dgc::PlanLayout PA = dgc::plan_layout(&ha, pp->vars);
   pp->plan_b = dgc::align8(PA.end);
   dgc::PlanLayout PB = dgc::plan_layout(&hb, pp->plan_b);
-  dgc::EmitLayout E = dgc::emit_layout(PB.end, pp->max_terms, pp->union_entries, pp->emit_entries);
-  pp->lds_bytes = (E.end + 15u) & ~15u;
+  dgc::EmitLayout E =
+      dgc::emit_layout(dgc::compare_emit_base(&hb, PB), pp->max_terms, pp->union_entries, pp->emit_entries);
+  // (B's plan writes up to PB.end before the emission area takes over.)
+  pp->lds_bytes = (std::max(E.end, PB.end) + 15u) & ~15u;
 }
 
 }  // namespace dg

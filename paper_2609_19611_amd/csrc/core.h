@@ -123,6 +123,14 @@ DGC EmitLayout emit_layout(uint32_t base, int32_t max_terms, int32_t union_entri
   return E;
 }
 
+// A comparison's emission area starts right after graph B's live factor
+// values: the values of intermediate tensors and the factor statistics
+// (which a comparison never reads) are dead once both plans have run, so
+// the emission area may overlay them.
+DGC uint32_t compare_emit_base(const DgpHeader* hb, const PlanLayout& PB) {
+  return align8(PB.fval + 8u * (uint32_t)hb->fval_live);
+}
+
 // Per-leaf emission shape (the compiled one, or the combined one for a
 // two-graph comparison).
 struct LeafShape {
@@ -1252,9 +1260,10 @@ DGC uint32_t location_compare(C& c, const uint8_t* blob_a, const uint8_t* blob_b
   }
   const PlanLayout PA = plan_layout(ha, PP->vars);
   const PlanLayout PB = plan_layout(hb, PP->plan_b);
-  const EmitLayout E = emit_layout(PB.end, PP->max_terms, PP->union_entries, PP->emit_entries);
+  const EmitLayout E = emit_layout(compare_emit_base(hb, PB), PP->max_terms, PP->union_entries, PP->emit_entries);
   plan_exec(c, blob_a, loc, area, PA, err);
   plan_exec(c, blob_b, loc, area, PB, err);
+  c.sync();  // (the emission area overlays B's dead values)
   const bool checks = !(ha->no_overflow && hb->no_overflow);
   const DgpLeaf* la = (const DgpLeaf*)(blob_a + ha->leaf_off);
   const DgpLeaf* lb = (const DgpLeaf*)(blob_b + hb->leaf_off);

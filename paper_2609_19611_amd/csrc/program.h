@@ -124,6 +124,10 @@ struct DgpHeader {
   // 1 when the static bound on every path count is below 2^32: the
   // run-time overflow checks (factor and table maxima) are then skipped.
   int32_t no_overflow;
+  // Factor values that leaf terms read come first in the value area:
+  // fval_live entries.  The rest belong to intermediate tensors only and are
+  // dead once the plan has run.
+  int32_t fval_live;
 };
 
 #define DGP_MAGIC 0x44475031u  // "DGP1"

@@ -214,6 +214,17 @@ def test_edge_cases(B):
     with pytest.raises(B.DgError) as e:
         B.compare_locations(g, B.dg_graph_parse(W.c1_text()), [0])
     assert e.value.name == "DG_E_SIGNATURE"
+    # Comparisons: no locations; an output that is a leaf against an op of
+    # it (same footprint) and against x + x (same footprint, counts 2).
+    st, mm = B.compare_locations(g, g, torch.empty(0, dtype=torch.int64))
+    assert st.numel() == 0 and mm.numel() == 0
+    leaf = B.dg_graph_parse("dgir 1\nleaf x 4\noutput x 4\n")
+    relu = B.dg_graph_parse("dgir 1\nleaf x 4\nop y relu x\noutput y 4\n")
+    twice = B.dg_graph_parse("dgir 1\nleaf x 4\nop y add x x\noutput y 4\n")
+    st, mm = B.compare_locations(leaf, relu, [0, 1, 2, 3])
+    assert st.cpu().tolist() == [0] * 4 and mm.numel() == 0
+    st, mm = B.compare_locations(relu, twice, [3, 0])
+    assert st.cpu().tolist() == [2, 2] and mm.cpu().tolist() == [0, 1]
 
 
 def test_repeatable(B):
