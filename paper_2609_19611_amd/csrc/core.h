@@ -734,7 +734,7 @@ DGC uint32_t table_divmod(uint32_t n, uint32_t d, uint32_t* rem) {
 template <class C, class Word>
 DGC void build_table(C& c, const LeafGeom& G, const TermRef* terms, int nterm, const int32_t* ulist,
                      const LeafHdr* H, int d0, int d1, bool with_base, uint32_t n, Word* tab, uint64_t* tmax,
-                     const uint64_t* a64) {
+                     const uint64_t* a64, bool narrow = false) {
   const int W = 1 + nterm;
   int32_t u[DGP_MAX_RANK];
   DG_UNROLL
@@ -787,6 +787,18 @@ DGC void build_table(C& c, const LeafGeom& G, const TermRef* terms, int nterm, c
       tab[(uint64_t)r * W] = (Word)pos;
       DG_PLAN_UNROLL
       for (int t = 0; t < nterm; ++t) {
+        if (narrow) {
+          // Every path count is below 2^32 (static bound).  A part of a
+          // term that is nonzero somewhere is at most a real count, so 32
+          // bits hold it; a part that is never nonzero multiplies only
+          // zeros, whatever its bits.
+          uint32_t v = with_base ? (uint32_t)terms[t].coef : 1u;
+          DG_UNROLL
+          for (int d = 0; d < DGP_MAX_RANK; ++d)
+            if (d >= d0 && d < d1) v *= (uint32_t)term_val(terms[t], d, x[d], a64);
+          tab[(uint64_t)r * W + 1 + t] = (Word)v;
+          continue;
+        }
         uint64_t v = with_base ? terms[t].coef : 1ull;
         DG_UNROLL
         for (int d = 0; d < DGP_MAX_RANK; ++d)
@@ -833,7 +845,8 @@ DGC bool prod_overflows(uint64_t a, uint64_t b) {
 // union lengths, and the table lengths O and In.
 template <class W, int MODE, class Word = uint32_t>
 DGC void leaf_prepare(W& w, const LeafGeom& G, int split, const int32_t* ucap, const TermRef* terms, int na, int nb,
-                      uint8_t* area, const EmitLayout& E, const FStat* st, bool checks, uint32_t* err) {
+                      uint8_t* area, const EmitLayout& E, const FStat* st, bool checks, uint32_t* err,
+                      bool narrow = false) {
   const int tid = w.tid(), nt = w.nthreads();
   const int nterm = na + nb;
   const int rank = G.rank;
@@ -905,8 +918,9 @@ DGC void leaf_prepare(W& w, const LeafGeom& G, int split, const int32_t* ucap, c
       for (int i = tid; i < 2 * nterm; i += nt) tmax[i] = 0;
       w.sync();
     }
-    build_table(w, G, terms, nterm, ulist, H, 0, split, true, O, otab, tmax, a64);
-    build_table(w, G, terms, nterm, ulist, H, split, rank, false, In, itab, checks ? tmax + nterm : nullptr, a64);
+    build_table(w, G, terms, nterm, ulist, H, 0, split, true, O, otab, tmax, a64, narrow);
+    build_table(w, G, terms, nterm, ulist, H, split, rank, false, In, itab, checks ? tmax + nterm : nullptr, a64,
+                narrow);
     w.sync();
     // A term whose largest outer and inner parts multiply past 32 bits has a
     // real cell with that count.
@@ -946,7 +960,8 @@ DGC void pair_at(const uint64_t* tab, uint32_t r, uint64_t* id, uint64_t* cnt) {
 //   would need more raises DGP_ERR_SIZE and writes nothing past it.
 template <class C, int MODE, class Word = uint32_t>
 DGC uint64_t leaf_emit(C& c, const LeafGeom& G, int split, const TermRef* terms, int na, int nb, uint8_t* area,
-                       const EmitLayout& E, Word* ids, Word* cnt, uint64_t room, uint32_t* err) {
+                       const EmitLayout& E, Word* ids, Word* cnt, uint64_t room, uint32_t* err,
+                       bool narrow = false) {
   const int tid = c.tid(), nt = c.nthreads();
   const int nterm = na + nb;
   const int rank = G.rank;
@@ -1023,10 +1038,22 @@ DGC uint64_t leaf_emit(C& c, const LeafGeom& G, int split, const TermRef* terms,
         const Word* o = otab + (uint64_t)r * W;
         const Word* q = itab + (uint64_t)j * W;
         pos = o[0] + q[0];
-        DG_PLAN_UNROLL
-        for (int t = 0; t < na; ++t) ca += (uint64_t)o[1 + t] * q[1 + t];
-        DG_PLAN_UNROLL
-        for (int t = na; t < nterm; ++t) cb += (uint64_t)o[1 + t] * q[1 + t];
+        if (narrow) {
+          // (Counts below 2^32: each nonzero product and each sum is at
+          // most a real count.)
+          uint32_t a = 0, b = 0;
+          DG_PLAN_UNROLL
+          for (int t = 0; t < na; ++t) a += (uint32_t)o[1 + t] * (uint32_t)q[1 + t];
+          DG_PLAN_UNROLL
+          for (int t = na; t < nterm; ++t) b += (uint32_t)o[1 + t] * (uint32_t)q[1 + t];
+          ca = a;
+          cb = b;
+        } else {
+          DG_PLAN_UNROLL
+          for (int t = 0; t < na; ++t) ca += (uint64_t)o[1 + t] * q[1 + t];
+          DG_PLAN_UNROLL
+          for (int t = na; t < nterm; ++t) cb += (uint64_t)o[1 + t] * q[1 + t];
+        }
       }
       j += dj;
       r += dr;
@@ -1278,10 +1305,10 @@ DGC uint32_t location_compare(C& c, const uint8_t* blob_a, const uint8_t* blob_b
     leaf_terms(c, blob_b, l, area, PB, terms + na);
     c.sync();
     leaf_prepare<C, EMIT_COMPARE>(c, G, PP->leaf[l].split, PP->leaf[l].ucap, terms, na, nb, area, E, nullptr,
-                                  checks, err);
+                                  checks, err, !checks);
     c.sync();
     const uint32_t s = (uint32_t)leaf_emit<C, EMIT_COMPARE, uint32_t>(c, G, PP->leaf[l].split, terms, na, nb, area,
-                                                                      E, nullptr, nullptr, 0, err);
+                                                                      E, nullptr, nullptr, 0, err, !checks);
     c.sync();
     if (s == 1) return 1;
     if (s == 2) status = 2;
