@@ -67,10 +67,9 @@ def parse_args():
     return p.parse_args()
 
 
-def copy_calibration(gib, steps, warmup):
-    """Device-to-device copy and a write-only fill of a known size: measured
-    HBM bandwidth, and the reference dispatches for scaling the FETCH_SIZE /
-    WRITE_SIZE counters."""
+def write_rates(gib, steps, warmup):
+    """Device-to-device copy and a write-only fill of a known size (torch's
+    kernels): the HBM bandwidth this machine reaches, beside the spec peak."""
     import torch
     n = int(gib * (1 << 30)) // 4
     src = torch.ones(n, dtype=torch.int32, device="cuda")
@@ -90,8 +89,15 @@ def copy_calibration(gib, steps, warmup):
 
     ms_copy = timed(lambda: dst.copy_(src))
     ms_fill = timed(lambda: dst.fill_(7))
-    print(json.dumps({"bytes": n * 4, "copy_ms": ms_copy, "copy_GBps_read_plus_write": 2 * n * 4 / (ms_copy * 1e-3) / 1e9,
-                      "fill_ms": ms_fill, "fill_GBps_write": n * 4 / (ms_fill * 1e-3) / 1e9}), flush=True)
+    return {"bytes": n * 4, "copy_ms": ms_copy, "copy_GBps_read_plus_write": 2 * n * 4 / (ms_copy * 1e-3) / 1e9,
+            "fill_ms": ms_fill, "fill_GBps_write": n * 4 / (ms_fill * 1e-3) / 1e9}
+
+
+def copy_calibration(gib, steps, warmup):
+    """The copy and fill of write_rates as a line of their own; their
+    dispatches are the reference for scaling the FETCH_SIZE / WRITE_SIZE
+    counters."""
+    print(json.dumps(write_rates(gib, steps, warmup)), flush=True)
 
 
 KERNEL_SOURCES = ["program.h", "core.h", "kernels_dev.h", "jit_source.cpp", "jit.cpp", "compile.cpp", "graph.cpp"]
@@ -646,6 +652,13 @@ def main():
                      "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE x2 + WRITE_SIZE x1)",
                      "kernel_ms": kern_ms, "algorithmic_bytes": alg_bytes},
     }
+    # The bandwidth plain torch kernels reach on this machine (after the timed
+    # region), beside the spec peak.
+    del ids, cnt
+    rates = write_rates(2.0, 5, 2)
+    line["roofline"]["measured_fill_GBps"] = rates["fill_GBps_write"]
+    line["roofline"]["measured_copy_GBps"] = rates["copy_GBps_read_plus_write"]
+    line["roofline"]["frac_of_measured_fill"] = achieved / rates["fill_GBps_write"]
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(args.workload, text, None, locs, args.cpu_seconds)
     line["git"] = git_sha()
