@@ -227,6 +227,21 @@ def test_edge_cases(B):
     assert st.cpu().tolist() == [2, 2] and mm.cpu().tolist() == [0, 1]
 
 
+@pytest.mark.parametrize("shape", [[1, 6, 12], [2, 6, 12]])
+def test_compare_counts_near_2_32(B, shape):
+    """32-bit comparison arithmetic under static bounds just below 2^32
+    (counts up to 2,101,864,255), at every location, against the oracle."""
+    a = tiny_graphs.large_count_norms(shape)
+    ga = B.dg_graph_parse(a)
+    n = B.dg_graph_info(ga)["output_numel"]
+    assert B.dg_graph_info(ga)["count_bound"] < 2 ** 32
+    for v in ("permuted", "mid_1d"):
+        b = tiny_graphs.large_count_norms(shape, v)
+        st, _ = B.compare_locations(ga, B.dg_graph_parse(b), list(range(n)))
+        want = oracle.compare(oracle.Graph(a), oracle.Graph(b), range(n))
+        assert np.array_equal(st.cpu().numpy(), want)
+
+
 def test_repeatable(B):
     g = B.dg_graph_parse(W.c3_text())
     locs = W.config_locations("c3")[:2048]

@@ -72,6 +72,19 @@ def test_compare_status_two():
     assert list(hostemu.compare(a, a, range(6))) == [0] * 6
 
 
+@pytest.mark.parametrize("shape", [[1, 6, 12], [2, 6, 12]])
+def test_compare_counts_near_2_32(shape):
+    """Both static bounds below 2^32, so the comparison's tables and sums
+    are 32-bit; counts reach 2,101,864,255."""
+    a = tiny_graphs.large_count_norms(shape)
+    n = oracle.Graph(a).output_numel
+    for v in ("permuted", "mid_1d"):
+        b = tiny_graphs.large_count_norms(shape, v)
+        want = oracle.compare(oracle.Graph(a), oracle.Graph(b), range(n))
+        assert np.array_equal(hostemu.compare(a, b, list(range(n))), want)
+        assert set(want.tolist()) == ({0} if v == "permuted" else {2})
+
+
 def test_paper_example():
     st = hostemu.compare(W.paper_kernel_text(), W.paper_reference_text(), [11596, 0, 131071])
     assert list(st) == [1, 1, 1]

@@ -198,6 +198,22 @@ def nested_layer_norms(n):
                 ("y", "layer_norm", ["b"], dict(ndims=1))], "y", [1, n])
 
 
+def large_count_norms(shape, variant=None):
+    """Three layer norms over the last two dims of x: the static count bound
+    of [1, 6, 12] is 2,101,864,255, just below 2^32 and reached.  variant
+    "permuted": x goes through two transposes that undo each other (same
+    rows, other plan); "mid_1d": the middle norm is over the last dim only
+    (same footprint, other counts)."""
+    ops, src = [], "x"
+    if variant == "permuted":
+        ops += [("p", "permute", ["x"], dict(dims=[0, 2, 1])), ("q", "permute", ["p"], dict(dims=[0, 2, 1]))]
+        src = "q"
+    mid = 1 if variant == "mid_1d" else 2
+    ops += [("a", "layer_norm", [src], dict(ndims=2)), ("b", "layer_norm", ["a"], dict(ndims=mid)),
+            ("y", "layer_norm", ["b"], dict(ndims=2))]
+    return _g([("x", list(shape))], ops, "y", list(shape))
+
+
 def nested_layer_norm_counts(n, loc):
     """Closed form of three nested layer norms (no affine) over n elements.
     One norm reaches x[s] n + 2 times through its statistics and x[l] once
