@@ -473,57 +473,65 @@ DGC void flat_emit(C& c, const DagCtx& x, const DgdGroup& G, const Slots& S, uin
   c.wave_sync();
 }
 
-// Writes group G's edges of the batch node in lane column j (a node with
-// at least half a wave of points): the wave covers the node's points with
-// its lanes, the digits of each lane's point advancing by the wave width
-// with carries.  NOP operands and Q window variables are compile-time
-// constants, so the steps stay in registers.
+// Writes group G's edges of the batch nodes in `mask` (lane columns of
+// nodes with at least half a wave of points), one node after another: the
+// wave covers a node's points with its lanes, the digits of each lane's
+// point advancing by the wave width with carries.  NOP operands and Q
+// window variables are compile-time constants, so the steps stay in
+// registers; the group's operand fields are read once for all the nodes.
 template <class C, int NOP, int Q>
-DGC void node_emit(C& c, const DagCtx& x, const DgdGroup& G, const Slots& S, int j, const DagOut& o, bool emit,
-                   bool append) {
+DGC void node_emit(C& c, const DagCtx& x, const DgdGroup& G, const Slots& S, uint64_t mask, const DagOut& o,
+                   bool emit, bool append) {
   const int lane = c.lane(), L = c.lanes();
-  uint32_t len[DGD_MAX_WIN], dg[DGD_MAX_WIN], inc[DGD_MAX_WIN];
-  uint64_t P = 1;
-  DG_UNROLL
-  for (int q = 0; q < DGD_MAX_WIN; ++q) {
-    len[q] = q < Q ? S.len(j, q) : 1u;
-    P *= len[q];
-  }
-  uint32_t base[NOP], mult[NOP], as[NOP][Q > 0 ? Q : 1];
+  // The group's operands: the same for every node.
+  uint32_t mult[NOP], as[NOP][Q > 0 ? Q : 1];
   bool leaf[NOP];
   DG_UNROLL
   for (int a = 0; a < NOP; ++a) {
     const DgdOperand& Pa = x.Ps[G.op0 + a];
-    base[a] = S.base(j, a);
     mult[a] = Pa.mult;
     leaf[a] = x.T[Pa.tensor].leaf != 0;
     DG_UNROLL
     for (int q = 0; q < Q; ++q) as[a][q] = G.astep[a][q];
   }
-  const uint64_t at0 = ((uint64_t)S.ghi(j) << 32) | S.glo(j);
-  radix_digits((uint32_t)lane, len, Q, dg);
-  radix_digits((uint32_t)L, len, Q, inc);
-  for (uint64_t p0 = 0; p0 < P; p0 += (uint64_t)L) {
-    const uint64_t p = p0 + (uint64_t)lane;
-    if (p < P) {
-      const uint64_t at = at0 + p * (uint64_t)NOP;
-      DG_UNROLL
-      for (int a = 0; a < NOP; ++a) {
-        uint32_t child = base[a];
+  while (mask) {
+    const int j = (int)__builtin_ctzll(mask);
+    mask &= mask - 1;
+    uint32_t len[DGD_MAX_WIN], dg[DGD_MAX_WIN], inc[DGD_MAX_WIN];
+    uint64_t P = 1;
+    DG_UNROLL
+    for (int q = 0; q < DGD_MAX_WIN; ++q) {
+      len[q] = q < Q ? S.len(j, q) : 1u;
+      P *= len[q];
+    }
+    uint32_t base[NOP];
+    DG_UNROLL
+    for (int a = 0; a < NOP; ++a) base[a] = S.base(j, a);
+    const uint64_t at0 = ((uint64_t)S.ghi(j) << 32) | S.glo(j);
+    radix_digits((uint32_t)lane, len, Q, dg);
+    radix_digits((uint32_t)L, len, Q, inc);
+    for (uint64_t p0 = 0; p0 < P; p0 += (uint64_t)L) {
+      const uint64_t p = p0 + (uint64_t)lane;
+      if (p < P) {
+        const uint64_t at = at0 + p * (uint64_t)NOP;
         DG_UNROLL
-        for (int q = 0; q < Q; ++q) child += as[a][q] * dg[q];
-        if (emit && at + a < o.room_edges) {
-          c.store_cached(&o.edges[at + a], child);
-          c.store_cached(&o.mults[at + a], mult[a]);
-        }
-        if (append && !leaf[a]) {
-          const DgdOperand& Pa = x.Ps[G.op0 + a];
-          const DgdTensor& Ta = x.T[Pa.tensor];
-          dag_append(c, Ta, Pa.tensor, child - Ta.gid, x.area, x.cnt, x.err);
+        for (int a = 0; a < NOP; ++a) {
+          uint32_t child = base[a];
+          DG_UNROLL
+          for (int q = 0; q < Q; ++q) child += as[a][q] * dg[q];
+          if (emit && at + a < o.room_edges) {
+            c.store_cached(&o.edges[at + a], child);
+            c.store_cached(&o.mults[at + a], mult[a]);
+          }
+          if (append && !leaf[a]) {
+            const DgdOperand& Pa = x.Ps[G.op0 + a];
+            const DgdTensor& Ta = x.T[Pa.tensor];
+            dag_append(c, Ta, Pa.tensor, child - Ta.gid, x.area, x.cnt, x.err);
+          }
         }
       }
+      radix_add(dg, inc, len, Q);
     }
-    radix_add(dg, inc, len, Q);
   }
 }
 
@@ -532,34 +540,21 @@ DGC void node_emit(C& c, const DagCtx& x, const DgdGroup& G, const Slots& S, int
 template <class C>
 DGC bool emit_nodes(C& c, const DagCtx& x, const DgdGroup& G, const Slots& S, uint64_t mask, const DagOut& o,
                     bool emit, bool append) {
-  const int key = G.nop * 16 + G.nwin;
-  switch (key) {
-    case 0x11: case 0x12: case 0x13: case 0x14:
-    case 0x21: case 0x22: case 0x23: case 0x24:
-    case 0x31: case 0x32: case 0x33: case 0x34:
-      break;
-    default:
-      return false;
+  switch (G.nop * 16 + G.nwin) {
+    case 0x11: node_emit<C, 1, 1>(c, x, G, S, mask, o, emit, append); return true;
+    case 0x12: node_emit<C, 1, 2>(c, x, G, S, mask, o, emit, append); return true;
+    case 0x13: node_emit<C, 1, 3>(c, x, G, S, mask, o, emit, append); return true;
+    case 0x14: node_emit<C, 1, 4>(c, x, G, S, mask, o, emit, append); return true;
+    case 0x21: node_emit<C, 2, 1>(c, x, G, S, mask, o, emit, append); return true;
+    case 0x22: node_emit<C, 2, 2>(c, x, G, S, mask, o, emit, append); return true;
+    case 0x23: node_emit<C, 2, 3>(c, x, G, S, mask, o, emit, append); return true;
+    case 0x24: node_emit<C, 2, 4>(c, x, G, S, mask, o, emit, append); return true;
+    case 0x31: node_emit<C, 3, 1>(c, x, G, S, mask, o, emit, append); return true;
+    case 0x32: node_emit<C, 3, 2>(c, x, G, S, mask, o, emit, append); return true;
+    case 0x33: node_emit<C, 3, 3>(c, x, G, S, mask, o, emit, append); return true;
+    case 0x34: node_emit<C, 3, 4>(c, x, G, S, mask, o, emit, append); return true;
+    default: return false;
   }
-  while (mask) {
-    const int j = (int)__builtin_ctzll(mask);
-    mask &= mask - 1;
-    switch (key) {
-      case 0x11: node_emit<C, 1, 1>(c, x, G, S, j, o, emit, append); break;
-      case 0x12: node_emit<C, 1, 2>(c, x, G, S, j, o, emit, append); break;
-      case 0x13: node_emit<C, 1, 3>(c, x, G, S, j, o, emit, append); break;
-      case 0x14: node_emit<C, 1, 4>(c, x, G, S, j, o, emit, append); break;
-      case 0x21: node_emit<C, 2, 1>(c, x, G, S, j, o, emit, append); break;
-      case 0x22: node_emit<C, 2, 2>(c, x, G, S, j, o, emit, append); break;
-      case 0x23: node_emit<C, 2, 3>(c, x, G, S, j, o, emit, append); break;
-      case 0x24: node_emit<C, 2, 4>(c, x, G, S, j, o, emit, append); break;
-      case 0x31: node_emit<C, 3, 1>(c, x, G, S, j, o, emit, append); break;
-      case 0x32: node_emit<C, 3, 2>(c, x, G, S, j, o, emit, append); break;
-      case 0x33: node_emit<C, 3, 3>(c, x, G, S, j, o, emit, append); break;
-      default:   node_emit<C, 3, 4>(c, x, G, S, j, o, emit, append); break;
-    }
-  }
-  return true;
 }
 
 // Edge count of the calling lane's node in the wave's batch starting at
