@@ -863,26 +863,29 @@ DGC void leaf_prepare(W& w, const LeafGeom& G, int split, const int32_t* ucap, c
     // hull grid of all terms (cells outside every support are zero on both
     // sides), as long as each hull fits the union's capacity.
     bool fits = true, empty = false;
-    DG_PLAN_UNROLL
-    for (int d = 0; d < rank; ++d) {
-      int32_t hlo, hhi;
-      term_hull(terms, nterm, d, &hlo, &hhi);
-      if (hhi <= hlo) empty = true;
-      else if (hhi - hlo > ucap[d]) fits = false;
+    int32_t hlo[DGP_MAX_RANK], hhi[DGP_MAX_RANK];
+    DG_UNROLL
+    for (int d = 0; d < DGP_MAX_RANK; ++d) {
+      hlo[d] = 0;
+      hhi[d] = 1;
+      if (d < rank) {
+        term_hull(terms, nterm, d, &hlo[d], &hhi[d]);
+        if (hhi[d] <= hlo[d]) empty = true;
+        else if (hhi[d] - hlo[d] > ucap[d]) fits = false;
+      }
     }
     if (empty) {
       ok = false;
       hull = true;
     } else if (fits) {
       if (tid == 0) {
-        DG_PLAN_UNROLL
-        for (int d = 0; d < rank; ++d) {
-          int32_t hlo, hhi;
-          term_hull(terms, nterm, d, &hlo, &hhi);
-          H->u[d] = hhi - hlo;
-          H->hlo[d] = hlo;
-          H->dense[d] = 1;
-        }
+        DG_UNROLL
+        for (int d = 0; d < DGP_MAX_RANK; ++d)
+          if (d < rank) {
+            H->u[d] = hhi[d] - hlo[d];
+            H->hlo[d] = hlo[d];
+            H->dense[d] = 1;
+          }
       }
       w.sync();
       hull = true;
