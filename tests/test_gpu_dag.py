@@ -71,6 +71,17 @@ def test_dag_c5_variants(B):
         _check(B, text, locs)
 
 
+def test_dag_c5_boundaries(B):
+    """DAGs at the output's padding edges of c5's reference, its split-K
+    variant and every fault, against the oracle."""
+    N, C, H, Wd = 64, 128, 64, 64
+    locs = [((n * C + c) * H + h) * Wd + w for n in (0, N - 1) for c in (0, C - 1)
+            for h in (0, 1, H - 2, H - 1) for w in (0, 1, Wd - 2, Wd - 1)]
+    texts = [W.c5_reference_text(), W.c5_variant_text()] + [W.c5_variant_text(fault=f) for f in W.c5_faults()]
+    for text in texts:
+        _check(B, text, locs)
+
+
 def test_dag_edge_cases(B):
     g = B.dg_graph_parse(W.c2_text())
     d = B.dag_locations(g, torch.empty(0, dtype=torch.int64))

@@ -163,6 +163,26 @@ def test_c5_clean_and_faults(B):
         assert st.any(), f
 
 
+def test_c5_faults_at_boundaries(B):
+    """Every fault of the split-K variant against the oracle at the output's
+    padding edges (first and last two rows and columns, corner images and
+    channels) and at 1,024 more locations drawn over the whole output."""
+    ref_text = W.c5_reference_text()
+    ref = B.dg_graph_parse(ref_text)
+    N, C, H, Wd = 64, 128, 64, 64
+    edge = [((n * C + c) * H + h) * Wd + w for n in (0, N - 1) for c in (0, C - 1)
+            for h in (0, 1, H - 2, H - 1) for w in (0, 1, Wd - 2, Wd - 1)]
+    rng = np.random.default_rng(55)
+    locs = edge + sorted(rng.choice(N * C * H * Wd, 1024, replace=False).tolist())
+    og_ref = oracle.Graph(ref_text)
+    for f in W.c5_faults():
+        vt = W.c5_variant_text(fault=f)
+        st, mism = B.compare_locations(ref, B.dg_graph_parse(vt), locs)
+        want = oracle.compare(og_ref, oracle.Graph(vt), locs, threads=8)
+        assert np.array_equal(st.cpu().numpy(), want), f
+        assert np.array_equal(mism.cpu().numpy(), np.nonzero(want)[0]), f
+
+
 def test_paper_example(B):
     a = B.dg_graph_parse(W.paper_kernel_text())
     b = B.dg_graph_parse(W.paper_reference_text())
