@@ -193,7 +193,9 @@ def test_paper_example(B):
     assert int(off_a[1]) == 513 and int(off_b[1]) == 1025
 
 
-def test_compare_small_graphs_against_oracle(B):
+@pytest.mark.parametrize("kernels", ["specialized", "interpreted"])
+def test_compare_small_graphs_against_oracle(B, kernels, monkeypatch):
+    monkeypatch.setenv("DIRIGO_JIT", "1" if kernels == "specialized" else "0")
     ref = W.c5_reference_text(n=2, c=4, hw=6, co=3)
     locs = list(range(2 * 3 * 6 * 6))
     g_ref, o_ref = B.dg_graph_parse(ref), oracle.Graph(ref)
@@ -248,9 +250,12 @@ def test_edge_cases(B):
 
 
 @pytest.mark.parametrize("shape", [[1, 6, 12], [2, 6, 12]])
-def test_compare_counts_near_2_32(B, shape):
+@pytest.mark.parametrize("kernels", ["specialized", "interpreted"])
+def test_compare_counts_near_2_32(B, shape, kernels, monkeypatch):
     """32-bit comparison arithmetic under static bounds just below 2^32
-    (counts up to 2,101,864,255), at every location, against the oracle."""
+    (counts up to 2,101,864,255), at every location, against the oracle,
+    with the specialised and the precompiled comparison kernels."""
+    monkeypatch.setenv("DIRIGO_JIT", "1" if kernels == "specialized" else "0")
     a = tiny_graphs.large_count_norms(shape)
     ga = B.dg_graph_parse(a)
     n = B.dg_graph_info(ga)["output_numel"]
