@@ -58,9 +58,13 @@ struct Error : std::runtime_error {
   explicit Error(const std::string& m) : std::runtime_error(m) {}
 };
 
+// Element count of a shape; a tensor may hold at most 2^62 elements.
 int64_t numel_of(const Shape& s) {
   int64_t n = 1;
-  for (int64_t d : s) n *= d;
+  for (int64_t d : s) {
+    if (d < 0 || __builtin_mul_overflow(n, d, &n) || n > (int64_t(1) << 62))
+      throw Error("tensor element count exceeds 2^62");
+  }
   return n;
 }
 
@@ -525,6 +529,7 @@ Graph parse_graph(const std::string& text) {
         t.leaf_index = (int)g.leaves.size();
         t.base = g.leaf_total;
         g.leaf_total += (uint64_t)numel_of(t.shape);
+        if (g.leaf_total > (1ull << 62)) throw Error("leaf elements exceed 2^62");
         g.by_name[t.name] = (int)g.tensors.size();
         g.leaves.push_back((int)g.tensors.size());
         g.tensors.push_back(t);
@@ -562,6 +567,7 @@ Graph parse_graph(const std::string& text) {
         t.name = toks[1];
         op.out = (int)g.tensors.size();
         t.shape = infer_shape(g, op);
+        numel_of(t.shape);  // at most 2^62 elements
         g.by_name[t.name] = (int)g.tensors.size();
         g.tensors.push_back(t);
         g.ops.push_back(op);

@@ -16,9 +16,15 @@
 
 namespace dg {
 
+// Element count of a shape.  Every tensor of a graph, leaf or op result,
+// holds at most 2^62 elements, so a larger product (or one that would
+// overflow 64 bits) is an error rather than a wrapped count.
 int64_t numel(const Dims& d) {
   int64_t n = 1;
-  for (int64_t x : d) n *= x;
+  for (int64_t x : d) {
+    if (x < 0 || __builtin_mul_overflow(n, x, &n) || n > (int64_t(1) << 62))
+      throw Failure(DG_E_OVERFLOW, "tensor element count exceeds 2^62");
+  }
   return n;
 }
 
@@ -759,6 +765,7 @@ void add_op(GraphIR& g, const std::string& name, const std::string& kind, const 
   if (shape.size() > DG_MAX_RANK) fail(DG_E_SHAPE, kind + ": result rank above 8");
   for (int64_t d : shape)
     if (d >= (int64_t(1) << 31)) fail(DG_E_SHAPE, kind + ": result dim too large");
+  numel(shape);  // a result of more than 2^62 elements is DG_E_OVERFLOW
   Tensor t;
   t.name = name;
   t.shape = shape;

@@ -173,3 +173,12 @@ def test_tensor_ids_match_the_oracle(name):
         assert ti["name"] == og.tensors[t].name and ti["shape"] == og.tensors[t].shape
         assert ti["gid"] == og.gid(t)
         assert (ti["leaf"] >= 0) == (og.tensors[t].leaf_index >= 0)
+
+
+@pytest.mark.parametrize("text", tiny_graphs.OVERFLOWING_SHAPES)
+def test_element_counts_past_2_62_are_rejected(text):
+    """A leaf or an op result with more than 2^62 elements (including
+    products that wrap 64 bits) is DG_E_OVERFLOW, not a wrapped count."""
+    with pytest.raises(B.DgError) as e:
+        B.dg_graph_parse(text)
+    assert e.value.name == "DG_E_OVERFLOW"

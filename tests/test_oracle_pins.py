@@ -363,3 +363,11 @@ def test_leaf_total_limit():
     assert off.tolist() == [0, 1, 2, 3]
     assert ids.tolist() == [2 ** 32, 2 ** 32 + 5, 2 ** 32 + 7]
     assert cnt.tolist() == [1, 1, 1]
+
+
+
+@pytest.mark.parametrize("text", tiny_graphs.OVERFLOWING_SHAPES)
+def test_element_counts_past_2_62_are_rejected(text):
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.Graph(text)
+    assert "2^62" in str(e.value)

@@ -223,3 +223,13 @@ def nested_layer_norm_counts(n, loc):
     a = n + 2
     c = (a * a * n + 2 * a) * (a * n + 1) + a
     return [c + (1 if s == loc else 0) for s in range(n)]
+
+
+# Shapes whose element counts wrap 64-bit arithmetic or pass 2^62: a leaf
+# (3 x 1431655766^3 is about 8.8e27) and a broadcast result of two leaves
+# that each fit ((2^31 - 1)^3 elements).
+OVERFLOWING_SHAPES = [
+    "dgir 1\nleaf x 3,1431655766,1431655766,1431655766\nleaf y 4\nop z relu y\noutput z 4\n",
+    "dgir 1\nleaf a 2147483647,1,1\nleaf b 1,2147483647,2147483647\nop y add a b\n"
+    "output y 2147483647,2147483647,2147483647\n",
+]
