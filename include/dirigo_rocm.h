@@ -32,11 +32,21 @@
  *
  * Memory and streams: every device pointer argument is caller-owned device
  * memory (for example a torch tensor's data pointer); `stream` is a
- * hipStream_t passed as void* (NULL = the default stream).  The library
- * allocates no device memory in these calls except the compiled graph
- * itself (a few KB), which each graph handle uploads once per device on its
- * first use and frees in dg_graph_destroy.  Scratch space is the caller's
- * workspace, sized by dg_workspace_size.
+ * hipStream_t passed as void* (NULL = the default stream).  Scratch space is
+ * the caller's workspace, sized by dg_workspace_size.  The calls allocate
+ * no other device memory, with two exceptions, both made once per graph and
+ * device on the graph's first device call there and both released by
+ * dg_graph_destroy:
+ *  - the graph's compiled plan (a few KB; its expression-DAG program too,
+ *    on the first DAG call), copied to the device with hipMalloc;
+ *  - with specialisation on, the code object of the graph's kernels
+ *    (hipModuleLoadData), shared by graphs whose plans are identical; a
+ *    comparison loads one for the pair, released when either graph of the
+ *    pair is destroyed.
+ *
+ * Sizes: a call takes at most 2^31 locations (DG_E_INVALID_ARG beyond);
+ * the library splits its launches so that no grid exceeds the device's
+ * limit.
  *
  * Errors: every call returns a dg_status; 0 is success, negative values are
  * errors and dg_last_error() returns a message for the calling thread.  No
@@ -168,7 +178,8 @@ typedef struct {
   int64_t output_numel;
   uint64_t leaf_total;        /* total leaf elements (global id space) */
   int64_t max_row_size;       /* static upper bound on one row's entries */
-  double count_bound;         /* static upper bound on one path count */
+  uint64_t count_bound;       /* static upper bound on one path count
+                                 (exact integer arithmetic; below 2^63) */
   int32_t n_instructions;     /* per-location plan length */
   int32_t lds_bytes;          /* local data share one location needs */
   int32_t lds_wide_bytes;     /* the same with 64-bit ids and counts */
@@ -368,7 +379,11 @@ dg_status dg_enumerate_stream(const dg_graph* g, int64_t first, int64_t n, void*
  *   d_mismatch[n]    device, written: the positions i (into d_locs) with
  *                    d_status[i] != 0, ascending
  *   h_n_mismatch     host, written: how many positions were written
- * Synchronous.  DG_E_RANGE / DG_E_OVERFLOW as for dg_enumerate_sizes. */
+ * Synchronous.  DG_E_RANGE / DG_E_OVERFLOW as for dg_enumerate_sizes.
+ * The two graphs may have at most 16 leaves (DG_E_UNSUPPORTED_OP beyond:
+ * the comparison keeps one emission shape per leaf in a fixed table), and
+ * both plans plus the comparison's tables must fit the device's LDS
+ * (DG_E_CAPACITY). */
 dg_status dg_compare(const dg_graph* a, const dg_graph* b, const int64_t* d_locs, int64_t n, uint8_t* d_status,
                      int64_t* d_mismatch, int64_t* h_n_mismatch, void* d_ws, void* stream);
 
@@ -391,7 +406,6 @@ dg_status dg_compare_range(const dg_graph* a, const dg_graph* b, int64_t first, 
                            uint8_t* d_status, int64_t* d_mismatch, int64_t* h_n_mismatch, void* d_ws,
                            void* stream);
 
-/* Message of the calling thread's last failed call ("" if none). */
 /* dg_graph_text: the graph as dgir v1 text (leaves, ops in SSA order,
  * output); writes at most cap - 1 characters and a terminating NUL to buf
  * (host; may be NULL when cap is 0) and the full length to *len. */
@@ -475,6 +489,7 @@ dg_status dg_order_permute(int64_t n_out, uint64_t seed, const int64_t* h_exclud
                            int64_t count, int64_t* d_out, int64_t* h_written, void* d_ws, size_t ws_bytes,
                            void* stream);
 
+/* Message of the calling thread's last failed call ("" if none). */
 const char* dg_last_error(void);
 
 #ifdef __cplusplus

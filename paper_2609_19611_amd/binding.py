@@ -45,7 +45,7 @@ class GraphInfo(ctypes.Structure):
         ("output_numel", ctypes.c_int64),
         ("leaf_total", ctypes.c_uint64),
         ("max_row_size", ctypes.c_int64),
-        ("count_bound", ctypes.c_double),
+        ("count_bound", ctypes.c_uint64),
         ("n_instructions", ctypes.c_int32),
         ("lds_bytes", ctypes.c_int32),
         ("lds_wide_bytes", ctypes.c_int32),

@@ -39,9 +39,6 @@ struct dg_graph {
   std::map<int, DevKernels> jit_wide;  // specialised 64-bit enumeration per device
   uint32_t lds_wide = 0;             // LDS per location with 64-bit ids and counts
   uint64_t serial = 0;               // unique per graph in the process
-  // Specialised comparison kernels with another graph: (device, other's
-  // serial, block) -> kernels.
-  std::map<std::tuple<int, uint64_t, int>, DevKernels> pair_jit;
   // Expression-DAG program, compiled on first use (dag_status: DG_OK or
   // the failure, with its message).
   bool dag_tried = false;
@@ -55,6 +52,15 @@ struct dg_graph {
 namespace {
 
 thread_local std::string g_last_error;
+
+// Specialised comparison kernels of graph pairs: (serial of a, serial of b,
+// device, block) -> kernels.  Released when either graph is destroyed.
+std::mutex g_pair_mu;
+std::map<std::tuple<uint64_t, uint64_t, int, int>, DevKernels> g_pair_jit;
+
+// Most locations one call takes (the helper kernels run flat grids of one
+// thread per location).
+constexpr int64_t kMaxLocations = int64_t(1) << 31;
 
 dg_status set_error(dg_status code, const std::string& msg) {
   g_last_error = msg;
@@ -184,14 +190,13 @@ const dg::JitModule* graph_jit(const dg_graph* cg) {
 // nullptr when specialisation is off or failed.
 const dg::JitModule* pair_jit(const dg_graph* ca, const dg_graph* b, const dgc::PairPlan& pp, int block) {
   if (!dg::jit_enabled()) return nullptr;
-  dg_graph* a = const_cast<dg_graph*>(ca);
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return nullptr;
-  std::lock_guard<std::mutex> lock(a->mu);
-  DevKernels& k = a->pair_jit[std::make_tuple(dev, b->serial, block)];
+  std::lock_guard<std::mutex> lock(g_pair_mu);
+  DevKernels& k = g_pair_jit[std::make_tuple(ca->serial, b->serial, dev, block)];
   if (!k.tried) {
     k.tried = true;
-    k.ok = dg::jit_load(dg::jit_compare_source(a->plan, b->plan, pp, block), &k.jm, &k.log) && k.jm.compare;
+    k.ok = dg::jit_load(dg::jit_compare_source(ca->plan, b->plan, pp, block), &k.jm, &k.log) && k.jm.compare;
   }
   return k.ok ? &k.jm : nullptr;
 }
@@ -214,8 +219,29 @@ const dg::JitModule* graph_jit_wide(const dg_graph* cg) {
 // Leaf ids of g fit 32 bits.
 bool narrow_ids(const dg_graph* g) { return g->ir.leaf_total <= 0xFFFFFFFFull; }
 
+// One block per location, in launches of at most kGridLimit / block blocks
+// (a grid holds fewer than 2^32 work-items per dimension).  launch(first,
+// m) launches blocks for locations first .. first + m - 1.
+constexpr int64_t kGridLimit = (int64_t(1) << 32) - 1;
+
+template <class F>
+hipError_t per_location(int64_t n, int block, F launch) {
+  const int64_t step = kGridLimit / block;
+  for (int64_t first = 0; first < n; first += step) {
+    hipError_t e = launch(first, std::min(step, n - first));
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
+}
+
+// The locations of src from position `first` on.
+dgc::LocSrc shifted(dgc::LocSrc src, int64_t first) {
+  return src.locs ? dgc::LocSrc{src.locs + first, 0} : dgc::LocSrc{nullptr, src.first + first};
+}
+
 hipError_t launch_module(hipFunction_t f, int64_t n, int block, uint32_t lds, hipStream_t s, void** args) {
   if (n <= 0) return hipSuccess;
+  if (n > kGridLimit / block) return hipErrorInvalidConfiguration;
   return hipModuleLaunchKernel(f, (unsigned)n, 1, 1, (unsigned)block, 1, 1, lds, s, args, nullptr);
 }
 
@@ -223,11 +249,16 @@ hipError_t launch_module(hipFunction_t f, int64_t n, int block, uint32_t lds, hi
 // locations of src at [offsets[i] - base, offsets[i+1] - base).
 hipError_t fill_launch(const dg_graph* g, const uint8_t* blob, dgc::LocSrc src, int64_t n, const int64_t* offsets,
                        int64_t base, uint32_t* ids, uint32_t* cnt, uint32_t* err, hipStream_t s) {
-  if (const dg::JitModule* jm = graph_jit(g)) {
-    void* args[] = {&src, &n, (void*)&offsets, &base, &ids, &cnt, &err};
-    return launch_module(jm->fill, n, g->block, g->lds, s, args);
-  }
-  return dgk::launch_fill(blob, src, n, offsets, base, ids, cnt, err, g->block, g->lds, s);
+  const dg::JitModule* jm = graph_jit(g);
+  return per_location(n, g->block, [&](int64_t first, int64_t m) {
+    dgc::LocSrc part = shifted(src, first);
+    const int64_t* off = offsets + first;
+    if (jm) {
+      void* args[] = {&part, &m, (void*)&off, &base, &ids, &cnt, &err};
+      return launch_module(jm->fill, m, g->block, g->lds, s, args);
+    }
+    return dgk::launch_fill(blob, part, m, off, base, ids, cnt, err, g->block, g->lds, s);
+  });
 }
 
 struct WsLayout {
@@ -331,6 +362,19 @@ dg_status dg_graph_build(const dg_tensor_desc* tensors, int32_t nt, const dg_op_
 
 void dg_graph_destroy(dg_graph* g) {
   if (!g) return;
+  for (auto& kv : g->jit) dg::jit_release(&kv.second.jm);
+  for (auto& kv : g->jit_wide) dg::jit_release(&kv.second.jm);
+  {
+    std::lock_guard<std::mutex> lock(g_pair_mu);
+    for (auto it = g_pair_jit.begin(); it != g_pair_jit.end();) {
+      if (std::get<0>(it->first) == g->serial || std::get<1>(it->first) == g->serial) {
+        dg::jit_release(&it->second.jm);
+        it = g_pair_jit.erase(it);
+      } else {
+        ++it;
+      }
+    }
+  }
   int cur = 0;
   bool have = hipGetDevice(&cur) == hipSuccess;
   for (auto& kv : g->dev_blob) {
@@ -433,12 +477,18 @@ dg_status sizes_impl(const dg_graph* g, dgc::LocSrc src, int64_t n, int64_t* d_o
   uint8_t* ws = static_cast<uint8_t*>(d_ws);
   uint32_t* err = reinterpret_cast<uint32_t*>(ws + w.err);
   DG_HIP(dgk::launch_zero(err, s), "zero");
-  if (const dg::JitModule* jm = graph_jit(g)) {
-    void* args[] = {&src, &n, &d_offsets, &err};
-    DG_HIP(launch_module(jm->sizes, n, g->block, g->lds, s, args), "sizes kernel");
-  } else {
-    DG_HIP(dgk::launch_sizes(blob, src, n, d_offsets, err, g->block, g->lds, s), "sizes kernel");
-  }
+  const dg::JitModule* jm = graph_jit(g);
+  DG_HIP(per_location(n, g->block,
+                      [&](int64_t first, int64_t m) {
+                        dgc::LocSrc part = shifted(src, first);
+                        int64_t* off = d_offsets + first;
+                        if (jm) {
+                          void* args[] = {&part, &m, &off, &err};
+                          return launch_module(jm->sizes, m, g->block, g->lds, s, args);
+                        }
+                        return dgk::launch_sizes(blob, part, m, off, err, g->block, g->lds, s);
+                      }),
+         "sizes kernel");
   DG_HIP(dgk::launch_scan(d_offsets, n, reinterpret_cast<int64_t*>(ws + w.sums), s), "scan");
   int64_t total = 0;
   uint32_t bits = 0;
@@ -455,13 +505,13 @@ dg_status sizes_impl(const dg_graph* g, dgc::LocSrc src, int64_t n, int64_t* d_o
 
 dg_status dg_enumerate_sizes(const dg_graph* g, const int64_t* d_locs, int64_t n, int64_t* d_offsets, void* d_ws,
                              int64_t* h_total, void* stream) {
-  if (!g || !d_offsets || !h_total || n < 0 || (n > 0 && !d_locs)) return set_error(DG_E_INVALID_ARG, "bad argument");
+  if (!g || !d_offsets || !h_total || n < 0 || n > kMaxLocations || (n > 0 && !d_locs)) return set_error(DG_E_INVALID_ARG, "bad argument");
   return sizes_impl(g, dgc::LocSrc{d_locs, 0}, n, d_offsets, d_ws, h_total, static_cast<hipStream_t>(stream));
 }
 
 dg_status dg_enumerate_fill(const dg_graph* g, const int64_t* d_locs, int64_t n, const int64_t* d_offsets,
                             uint32_t* d_ids, uint32_t* d_counts, void* d_ws, void* stream) {
-  if (!g || n < 0 || (n > 0 && (!d_locs || !d_offsets || !d_ids || !d_counts)))
+  if (!g || n < 0 || n > kMaxLocations || (n > 0 && (!d_locs || !d_offsets || !d_ids || !d_counts)))
     return set_error(DG_E_INVALID_ARG, "bad argument");
   if (!d_ws) return set_error(DG_E_WORKSPACE, "workspace is required");
   if (!narrow_ids(g)) return set_error(DG_E_OVERFLOW, "leaf ids need 64 bits: use dg_enumerate_wide");
@@ -510,20 +560,26 @@ dg_status enumerate_impl(const dg_graph* g, dgc::LocSrc src, int64_t n, int64_t*
   uint64_t* ticket = reinterpret_cast<uint64_t*>(ws + w.ticket);
   uint64_t cap = (uint64_t)capacity;
   const dg::JitModule* jm = wide ? graph_jit_wide(g) : graph_jit(g);
-  if (jm) {
-    DG_HIP(dgk::launch_zero_u64(status, n, s), "zero status");
-    DG_HIP(dgk::launch_zero_u64(ticket, 1, s), "zero ticket");
-    void* args[] = {&src, &n, &d_offsets, &d_ids, &d_counts, &cap, &status, &ticket, &err};
-    DG_HIP(launch_module(wide ? jm->enumerate_wide : jm->enumerate, n, g->block, lds, s, args), "enumerate kernel");
-  } else if constexpr (wide) {
-    DG_HIP(dgk::launch_enumerate_wide(blob, src, n, d_offsets, d_ids, d_counts, cap, status, ticket, err, g->block,
-                                      lds, s),
-           "enumerate kernel");
-  } else {
-    DG_HIP(dgk::launch_enumerate(blob, src, n, d_offsets, d_ids, d_counts, cap, status, ticket, err, g->block, lds,
-                                 s),
-           "enumerate kernel");
-  }
+  // Blocks take their locations from a ticket counter, so a list longer
+  // than one grid runs as several launches of the same kernel on the
+  // stream: the blocks of a later launch take the next tickets and look
+  // back over words the earlier launches have finished.
+  DG_HIP(dgk::launch_zero_u64(status, n, s), "zero status");
+  DG_HIP(dgk::launch_zero_u64(ticket, 1, s), "zero ticket");
+  DG_HIP(per_location(n, g->block,
+                      [&](int64_t, int64_t m) {
+                        if (jm) {
+                          void* args[] = {&src, &n, &d_offsets, &d_ids, &d_counts, &cap, &status, &ticket, &err};
+                          return launch_module(wide ? jm->enumerate_wide : jm->enumerate, m, g->block, lds, s, args);
+                        }
+                        if constexpr (wide)
+                          return dgk::launch_enumerate_wide(blob, src, n, m, d_offsets, d_ids, d_counts, cap, status,
+                                                            ticket, err, g->block, lds, s);
+                        else
+                          return dgk::launch_enumerate(blob, src, n, m, d_offsets, d_ids, d_counts, cap, status,
+                                                       ticket, err, g->block, lds, s);
+                      }),
+         "enumerate kernel");
   int64_t total = 0;
   uint32_t bits = 0;
   DG_HIP(hipMemcpyAsync(&total, d_offsets + n, sizeof(int64_t), hipMemcpyDeviceToHost, s), "copy total");
@@ -543,7 +599,7 @@ bool range_ok(const dg_graph* g, int64_t first, int64_t n) {
 
 dg_status dg_enumerate(const dg_graph* g, const int64_t* d_locs, int64_t n, int64_t* d_offsets, uint32_t* d_ids,
                        uint32_t* d_counts, int64_t capacity, void* d_ws, int64_t* h_total, void* stream) {
-  if (!g || !d_offsets || !h_total || n < 0 || capacity < 0 || (n > 0 && !d_locs) ||
+  if (!g || !d_offsets || !h_total || n < 0 || n > kMaxLocations || capacity < 0 || (n > 0 && !d_locs) ||
       (capacity > 0 && (!d_ids || !d_counts)))
     return set_error(DG_E_INVALID_ARG, "bad argument");
   return enumerate_impl(g, dgc::LocSrc{d_locs, 0}, n, d_offsets, d_ids, d_counts, capacity, d_ws, h_total, stream);
@@ -552,7 +608,7 @@ dg_status dg_enumerate(const dg_graph* g, const int64_t* d_locs, int64_t n, int6
 dg_status dg_enumerate_wide(const dg_graph* g, const int64_t* d_locs, int64_t n, int64_t* d_offsets,
                             uint64_t* d_ids, uint64_t* d_counts, int64_t capacity, void* d_ws, int64_t* h_total,
                             void* stream) {
-  if (!g || !d_offsets || !h_total || n < 0 || capacity < 0 || (n > 0 && !d_locs) ||
+  if (!g || !d_offsets || !h_total || n < 0 || n > kMaxLocations || capacity < 0 || (n > 0 && !d_locs) ||
       (capacity > 0 && (!d_ids || !d_counts)))
     return set_error(DG_E_INVALID_ARG, "bad argument");
   return enumerate_impl(g, dgc::LocSrc{d_locs, 0}, n, d_offsets, d_ids, d_counts, capacity, d_ws, h_total, stream);
@@ -560,7 +616,7 @@ dg_status dg_enumerate_wide(const dg_graph* g, const int64_t* d_locs, int64_t n,
 
 dg_status dg_enumerate_range(const dg_graph* g, int64_t first, int64_t n, int64_t* d_offsets, uint32_t* d_ids,
                              uint32_t* d_counts, int64_t capacity, void* d_ws, int64_t* h_total, void* stream) {
-  if (!g || !d_offsets || !h_total || n < 0 || capacity < 0 || (capacity > 0 && (!d_ids || !d_counts)))
+  if (!g || !d_offsets || !h_total || n < 0 || n > kMaxLocations || capacity < 0 || (capacity > 0 && (!d_ids || !d_counts)))
     return set_error(DG_E_INVALID_ARG, "bad argument");
   if (!range_ok(g, first, n)) return set_error(DG_E_RANGE, "the location range leaves the output");
   return enumerate_impl(g, dgc::LocSrc{nullptr, first}, n, d_offsets, d_ids, d_counts, capacity, d_ws, h_total,
@@ -569,7 +625,7 @@ dg_status dg_enumerate_range(const dg_graph* g, int64_t first, int64_t n, int64_
 
 dg_status dg_enumerate_stream(const dg_graph* g, int64_t first, int64_t n, void* d_buf, size_t buf_bytes,
                               int64_t max_chunk, dg_chunk_fn fn, void* user, void* stream_a, void* stream_b) {
-  if (!g || !d_buf || !fn || n < 0 || max_chunk <= 0) return set_error(DG_E_INVALID_ARG, "bad argument");
+  if (!g || !d_buf || !fn || n < 0 || n > kMaxLocations || max_chunk <= 0) return set_error(DG_E_INVALID_ARG, "bad argument");
   if (!range_ok(g, first, n)) return set_error(DG_E_RANGE, "the location range leaves the output");
   if (!narrow_ids(g)) return set_error(DG_E_OVERFLOW, "leaf ids need 64 bits: use dg_enumerate_wide");
   if (n == 0) return DG_OK;
@@ -697,17 +753,26 @@ dg_status compare_impl(const dg_graph* a, const dg_graph* b, dgc::LocSrc src, in
     DG_HIP(dgk::launch_zero(err, s), "zero");
     uint64_t* found = reinterpret_cast<uint64_t*>(ws + w.found);
     DG_HIP(dgk::launch_zero_u64(found, 1, s), "zero count");
-    if (const dg::JitModule* jm = pair_jit(a, b, pp, block)) {
-      void* args[] = {&src, &n, &d_status, &flags, &found, &limit, &err};
-      DG_HIP(launch_module(jm->compare, n, block, pp.lds_bytes, s, args), "compare kernel");
-    } else {
+    const dg::JitModule* jm = pair_jit(a, b, pp, block);
+    dgc::PairPlan* d_pp = reinterpret_cast<dgc::PairPlan*>(ws + w.pair);
+    if (!jm) {
       if (block != 64 && block != 256) return set_error(DG_E_INVALID_ARG, "block size needs specialised kernels");
-      dgc::PairPlan* d_pp = reinterpret_cast<dgc::PairPlan*>(ws + w.pair);
       // Pageable source: the copy has completed when the call returns.
       DG_HIP(hipMemcpyAsync(d_pp, &pp, sizeof(pp), hipMemcpyHostToDevice, s), "copy pair plan");
-      DG_HIP(dgk::launch_compare(ba, bb, d_pp, pp.lds_bytes, src, n, d_status, flags, found, limit, err, block, s),
-             "compare kernel");
     }
+    DG_HIP(per_location(n, block,
+                        [&](int64_t first, int64_t m) {
+                          dgc::LocSrc part = shifted(src, first);
+                          uint8_t* st_part = d_status + first;
+                          int64_t* fl_part = flags + first;
+                          if (jm) {
+                            void* args[] = {&part, &m, &st_part, &fl_part, &found, &limit, &err};
+                            return launch_module(jm->compare, m, block, pp.lds_bytes, s, args);
+                          }
+                          return dgk::launch_compare(ba, bb, d_pp, pp.lds_bytes, part, m, st_part, fl_part, found,
+                                                     limit, err, block, s);
+                        }),
+           "compare kernel");
     DG_HIP(dgk::launch_scan(flags, n, reinterpret_cast<int64_t*>(ws + w.sums), s), "scan");
     DG_HIP(dgk::launch_scatter_mismatch(d_status, flags, n, d_mismatch, s), "scatter");
     int64_t total = 0;
@@ -726,7 +791,7 @@ dg_status compare_impl(const dg_graph* a, const dg_graph* b, dgc::LocSrc src, in
 
 dg_status dg_dag_sizes(const dg_graph* g, const int64_t* d_locs, int64_t n, int64_t* d_node_offsets,
                        int64_t* d_edge_offsets, void* d_ws, int64_t* h_nodes, int64_t* h_edges, void* stream) {
-  if (!g || !d_node_offsets || !d_edge_offsets || !h_nodes || !h_edges || n < 0 || (n > 0 && !d_locs))
+  if (!g || !d_node_offsets || !d_edge_offsets || !h_nodes || !h_edges || n < 0 || n > kMaxLocations || (n > 0 && !d_locs))
     return set_error(DG_E_INVALID_ARG, "bad argument");
   if (!d_ws) return set_error(DG_E_WORKSPACE, "workspace is required");
   return guarded([&]() -> dg_status {
@@ -741,8 +806,12 @@ dg_status dg_dag_sizes(const dg_graph* g, const int64_t* d_locs, int64_t n, int6
     uint8_t* ws = static_cast<uint8_t*>(d_ws);
     uint32_t* err = reinterpret_cast<uint32_t*>(ws + w.err);
     DG_HIP(dgk::launch_zero(err, s), "zero");
-    DG_HIP(dgk::launch_dag_sizes(dblob, dgc::LocSrc{d_locs, 0}, n, d_node_offsets, d_edge_offsets, err, g->dag_block,
-                                 g->dag.lds_bytes, s),
+    DG_HIP(per_location(n, g->dag_block,
+                        [&](int64_t first, int64_t m) {
+                          return dgk::launch_dag_sizes(dblob, dgc::LocSrc{d_locs + first, 0}, m,
+                                                       d_node_offsets + first, d_edge_offsets + first, err,
+                                                       g->dag_block, g->dag.lds_bytes, s);
+                        }),
            "DAG sizes kernel");
     int64_t* sums = reinterpret_cast<int64_t*>(ws + w.sums);
     DG_HIP(dgk::launch_scan(d_node_offsets, n, sums, s), "scan");
@@ -764,7 +833,7 @@ dg_status dg_dag_sizes(const dg_graph* g, const int64_t* d_locs, int64_t n, int6
 dg_status dg_dag_fill(const dg_graph* g, const int64_t* d_locs, int64_t n, const int64_t* d_node_offsets,
                       const int64_t* d_edge_offsets, uint32_t* d_nodes, uint32_t* d_node_edge, uint32_t* d_edges,
                       uint32_t* d_mults, void* d_ws, void* stream) {
-  if (!g || n < 0 || (n > 0 && (!d_locs || !d_node_offsets || !d_edge_offsets || !d_nodes || !d_node_edge ||
+  if (!g || n < 0 || n > kMaxLocations || (n > 0 && (!d_locs || !d_node_offsets || !d_edge_offsets || !d_nodes || !d_node_edge ||
                                 !d_edges || !d_mults)))
     return set_error(DG_E_INVALID_ARG, "bad argument");
   if (!d_ws) return set_error(DG_E_WORKSPACE, "workspace is required");
@@ -778,8 +847,13 @@ dg_status dg_dag_fill(const dg_graph* g, const int64_t* d_locs, int64_t n, const
     hipStream_t s = static_cast<hipStream_t>(stream);
     uint32_t* err = reinterpret_cast<uint32_t*>(static_cast<uint8_t*>(d_ws) + ws_layout(n).err);
     DG_HIP(dgk::launch_zero(err, s), "zero");
-    DG_HIP(dgk::launch_dag_fill(dblob, dgc::LocSrc{d_locs, 0}, n, d_node_offsets, d_edge_offsets, d_nodes,
-                                d_node_edge, d_edges, d_mults, err, g->dag_block, g->dag.lds_bytes, s),
+    DG_HIP(per_location(n, g->dag_block,
+                        [&](int64_t first, int64_t m) {
+                          return dgk::launch_dag_fill(dblob, dgc::LocSrc{d_locs + first, 0}, m,
+                                                      d_node_offsets + first, d_edge_offsets + first, d_nodes,
+                                                      d_node_edge, d_edges, d_mults, err, g->dag_block,
+                                                      g->dag.lds_bytes, s);
+                        }),
            "DAG fill kernel");
     uint32_t bits = 0;
     DG_HIP(hipMemcpyAsync(&bits, err, sizeof(uint32_t), hipMemcpyDeviceToHost, s), "copy flags");
@@ -873,7 +947,7 @@ dg_status dg_order_permute(int64_t n_out, uint64_t seed, const int64_t* h_exclud
 
 dg_status dg_compare(const dg_graph* a, const dg_graph* b, const int64_t* d_locs, int64_t n, uint8_t* d_status,
                      int64_t* d_mismatch, int64_t* h_n_mismatch, void* d_ws, void* stream) {
-  if (!a || !b || !h_n_mismatch || n < 0 || (n > 0 && (!d_locs || !d_status || !d_mismatch)))
+  if (!a || !b || !h_n_mismatch || n < 0 || n > kMaxLocations || (n > 0 && (!d_locs || !d_status || !d_mismatch)))
     return set_error(DG_E_INVALID_ARG, "bad argument");
   return compare_impl(a, b, dgc::LocSrc{d_locs, 0}, n, 0, d_status, d_mismatch, h_n_mismatch, d_ws, stream);
 }
@@ -881,7 +955,7 @@ dg_status dg_compare(const dg_graph* a, const dg_graph* b, const int64_t* d_locs
 dg_status dg_compare_range(const dg_graph* a, const dg_graph* b, int64_t first, int64_t n, int64_t max_mismatch,
                            uint8_t* d_status, int64_t* d_mismatch, int64_t* h_n_mismatch, void* d_ws,
                            void* stream) {
-  if (!a || !b || !h_n_mismatch || n < 0 || max_mismatch < 0 || (n > 0 && (!d_status || !d_mismatch)))
+  if (!a || !b || !h_n_mismatch || n < 0 || n > kMaxLocations || max_mismatch < 0 || (n > 0 && (!d_status || !d_mismatch)))
     return set_error(DG_E_INVALID_ARG, "bad argument");
   if (!range_ok(a, first, n)) return set_error(DG_E_RANGE, "the location range leaves the output");
   return compare_impl(a, b, dgc::LocSrc{nullptr, first}, n, (uint64_t)max_mismatch, d_status, d_mismatch,

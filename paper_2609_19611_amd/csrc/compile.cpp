@@ -94,7 +94,17 @@ bool fn_uses(const IndexFn& f, int v) {
   return false;
 }
 
-double sat(double x) { return std::isfinite(x) ? x : 1e300; }
+// Static bounds are unsigned 64-bit integers that saturate at kBoundMax
+// (a bound that large means "2^64 - 1 or more").
+const uint64_t kBoundMax = ~uint64_t(0);
+uint64_t bmul(uint64_t a, uint64_t b) {
+  uint64_t r;
+  return __builtin_mul_overflow(a, b, &r) ? kBoundMax : r;
+}
+uint64_t badd(uint64_t a, uint64_t b) {
+  uint64_t r;
+  return __builtin_add_overflow(a, b, &r) ? kBoundMax : r;
+}
 
 // ------------------------------------------------- anchored coordinate ranges
 // Static capacities of factors and of a leaf's per-dim unions.  A factor's
@@ -174,23 +184,23 @@ class Compiler {
   // the range does not depend on the location (a single point: ROOT,
   // CONST; a window mapped one-to-one: length of its clamped image), else 0.
   std::vector<int64_t> unit_len_;
-  std::vector<double> fbound_;
-  std::vector<double> sbound_;
+  std::vector<uint64_t> fbound_;
+  std::vector<uint64_t> sbound_;
   std::map<std::string, int> memo_;
   std::vector<std::vector<SymTerm>> terms_;
 
-  int new_factor(int64_t cap, int64_t size, double bound) {
+  int new_factor(int64_t cap, int64_t size, uint64_t bound) {
     DgpFactor f{};
     f.cap = (int32_t)std::max<int64_t>(1, cap);
     f.size = (int32_t)size;
     fac_.push_back(f);
     pos_.push_back(FactorPos{});
     unit_len_.push_back(0);
-    fbound_.push_back(sat(bound));
+    fbound_.push_back(bound);
     return (int)fac_.size() - 1;
   }
-  int new_scalar(double bound) {
-    sbound_.push_back(sat(bound));
+  int new_scalar(uint64_t bound) {
+    sbound_.push_back(bound);
     return (int)sbound_.size() - 1;
   }
   DgpInstr blank(int opcode) {
@@ -205,7 +215,7 @@ class Compiler {
     std::string key = "ROOT " + std::to_string(a);
     auto it = memo_.find(key);
     if (it != memo_.end()) return it->second;
-    int f = new_factor(1, g_.tensors[g_.output].shape[a], 1.0);
+    int f = new_factor(1, g_.tensors[g_.output].shape[a], 1);
     unit_len_[f] = 1;
     pos_[f].known = true;
     pos_[f].a = {{a, Frac{1, 1}}};
@@ -220,7 +230,7 @@ class Compiler {
     std::string key = "CONST " + std::to_string(v) + " " + std::to_string(size);
     auto it = memo_.find(key);
     if (it != memo_.end()) return it->second;
-    int f = new_factor(1, size, 1.0);
+    int f = new_factor(1, size, 1);
     unit_len_[f] = 1;
     pos_[f].known = true;
     pos_[f].lo = pos_[f].hi = frac(v);
@@ -231,10 +241,10 @@ class Compiler {
     return memo_[key] = f;
   }
 
-  double coef_bound(const Coef& c) {
-    double b = (double)c.k;
-    for (int s : c.slots) b *= sbound_[s];
-    return sat(b);
+  uint64_t coef_bound(const Coef& c) {
+    uint64_t b = c.k;
+    for (int s : c.slots) b = bmul(b, sbound_[s]);
+    return b;
   }
 
   // Materialises the product of a coefficient's scalar slots: (slot or -1, constant).
@@ -252,8 +262,8 @@ class Compiler {
       slot = it->second;
     } else {
       if (s.size() > 8) fail(DG_E_UNSUPPORTED_OP, "coefficient with more than 8 scalar factors");
-      double b = 1;
-      for (int x : s) b *= sbound_[x];
+      uint64_t b = 1;
+      for (int x : s) b = bmul(b, sbound_[x]);
       slot = new_scalar(b);
       DgpInstr i = blank(DGP_SMUL);
       i.dst = slot;
@@ -280,7 +290,7 @@ class Compiler {
     if (it != memo_.end()) {
       slot = it->second;
     } else {
-      slot = new_scalar(coef_bound(a) + coef_bound(b));
+      slot = new_scalar(badd(coef_bound(a), coef_bound(b)));
       DgpInstr i = blank(DGP_SADD);
       i.dst = slot;
       i.dst_is_scalar = 1;
@@ -310,7 +320,7 @@ class Compiler {
       if (pos_[f2].lo < hp.lo) hp.lo = pos_[f2].lo;
       if (hp.hi < pos_[f2].hi) hp.hi = pos_[f2].hi;
     }
-    int f = new_factor(cap, size, fbound_[f1] * coef_bound(c1) + fbound_[f2] * coef_bound(c2));
+    int f = new_factor(cap, size, badd(bmul(fbound_[f1], coef_bound(c1)), bmul(fbound_[f2], coef_bound(c2))));
     pos_[f] = hp;
     DgpInstr i = blank(DGP_LINCOMB);
     i.dst = f;
@@ -437,12 +447,12 @@ class Compiler {
   // a floor division by s), so at most ceil(K / |coef|) values of that
   // term's quotient, each taken by at most vdiv values of the variable
   // (2 vdiv - 1 where it can be negative: the division truncates).
-  double collisions(const IndexFn& target, const std::vector<int>& vars, const std::vector<int64_t>& width, int R,
-                    const ReadGroup& G) {
-    double points = 1;
-    for (int64_t w : width) points *= (double)w;
+  uint64_t collisions(const IndexFn& target, const std::vector<int>& vars, const std::vector<int64_t>& width, int R,
+                      const ReadGroup& G) {
+    uint64_t points = 1;
+    for (int64_t w : width) points = bmul(points, (uint64_t)std::max<int64_t>(w, 0));
     const int64_t K = target.mode == 2 ? target.s : 1;
-    double best = points;
+    uint64_t best = points;
     for (size_t q = 0; q < vars.size(); ++q) {
       const IndexFn::Term* only = nullptr;
       int uses = 0;
@@ -455,7 +465,10 @@ class Compiler {
       const bool negative = vars[q] >= R && G.wlo[vars[q] - R] < 0;
       const int64_t per = only->vdiv == 1 ? 1 : (negative ? 2 * only->vdiv - 1 : only->vdiv);
       const int64_t pin = std::min<int64_t>(width[q], ceil_div(K, std::llabs(only->coef)) * per);
-      best = std::min(best, points / (double)width[q] * (double)pin);
+      uint64_t others = 1;  // the other variables' widths
+      for (size_t r = 0; r < vars.size(); ++r)
+        if (r != q) others = bmul(others, (uint64_t)std::max<int64_t>(width[r], 0));
+      best = std::min(best, bmul(others, (uint64_t)pin));
     }
     return best;
   }
@@ -493,21 +506,21 @@ class Compiler {
     for (size_t q = 0; q < vars.size(); ++q) local[vars[q]] = (int)q;
     std::ostringstream key;
     key << "COMP";
-    double points = 1, weight = 1;
+    uint64_t points = 1, weight = 1;
     std::vector<int64_t> width(vars.size());
     for (size_t q = 0; q < vars.size(); ++q) {
       int v = vars[q];
       if (v < R) {
         key << " o" << t.f[v];
         width[q] = fac_[t.f[v]].cap;
-        weight *= fbound_[t.f[v]];
+        weight = bmul(weight, fbound_[t.f[v]]);
       } else {
         key << " w" << G.wlo[v - R] << ":" << G.whi[v - R];
         width[q] = G.whi[v - R] - G.wlo[v - R];
       }
-      points *= (double)width[q];
+      points = bmul(points, (uint64_t)std::max<int64_t>(width[q], 0));
     }
-    if (points > 2147483647.0) fail(DG_E_UNSUPPORTED_OP, "component sum over more than 2^31 points");
+    if (points > 2147483647u) fail(DG_E_UNSUPPORTED_OP, "component sum over more than 2^31 points");
     key << " P";
     for (size_t p = 0; p < preds.size(); ++p) key_fn(key, *preds[p], local, psize[p]);
     if (target) {
@@ -545,7 +558,7 @@ class Compiler {
       int64_t count = (target->mode ? ceil_div(span, target->s) : span) + 1;
       FactorPos tp = target_pos(*target, t, vars, R, G);
       if (tp.known) count = std::min(count, floor_frac(tp.hi - tp.lo) + 1);
-      slot = new_factor(std::min(count, tsize), tsize, collisions(*target, vars, width, R, G) * weight);
+      slot = new_factor(std::min(count, tsize), tsize, bmul(collisions(*target, vars, width, R, G), weight));
       pos_[slot] = tp;
       if (preds.empty() && vars.size() == 1 && vars[0] >= R && target->mode == 0 && target->terms.size() == 1 &&
           target->terms[0].vdiv == 1 && (target->terms[0].coef == 1 || target->terms[0].coef == -1)) {
@@ -558,7 +571,7 @@ class Compiler {
       i.target = to_dev(*target, local, tsize);
       i.dst_is_scalar = 0;
     } else {
-      slot = new_scalar(points * weight);
+      slot = new_scalar(bmul(points, weight));
       i.dst_is_scalar = 1;
     }
     i.dst = slot;
@@ -683,7 +696,7 @@ Plan Compiler::run() {
   std::vector<DgpTerm> dterms;
   Plan plan;
   int64_t max_row = 0, emit_entries = 0, union_entries = 0;
-  double cbound = 0;
+  uint64_t cbound = 0;
   for (int li = 0; li < (int)g.leaves.size(); ++li) {
     const Tensor& T = g.tensors[g.leaves[li]];
     std::vector<SymTerm>& ts = terms_[g.leaves[li]];
@@ -702,7 +715,7 @@ Plan Compiler::run() {
       L.stride[d] = stride;
       stride *= (uint64_t)T.shape[d];
     }
-    double lb = 0;
+    uint64_t lb = 0;
     if (ts.size() == 1)
       for (int d = 0; d < L.rank; ++d) fac_[ts[0].f[d]].stat = 1;
     for (const SymTerm& t : ts) {
@@ -711,12 +724,12 @@ Plan Compiler::run() {
       auto cs = coef_slot(t.coef);
       dt.coef_slot = cs.first;
       dt.coef_const = cs.second;
-      double b = coef_bound(t.coef);
+      uint64_t b = coef_bound(t.coef);
       for (int d = 0; d < L.rank; ++d) {
         dt.factor[d] = t.f[d];
-        b *= fbound_[t.f[d]];
+        b = bmul(b, fbound_[t.f[d]]);
       }
-      lb += b;
+      lb = badd(lb, b);
       dterms.push_back(dt);
     }
     cbound = std::max(cbound, lb);
@@ -764,11 +777,12 @@ Plan Compiler::run() {
     leaves.push_back(L);
     plan.max_leaf_terms = std::max(plan.max_leaf_terms, (int)ts.size());
   }
-  if (cbound > 9.2e18) fail(DG_E_OVERFLOW, "static path-count bound exceeds 2^63");
-  for (double b : fbound_)
-    if (b > 9.2e18) fail(DG_E_OVERFLOW, "static path-count bound exceeds 2^63");
-  for (double b : sbound_)
-    if (b > 9.2e18) fail(DG_E_OVERFLOW, "static path-count bound exceeds 2^63");
+  const uint64_t k2_63 = uint64_t(1) << 63;
+  if (cbound >= k2_63) fail(DG_E_OVERFLOW, "static path-count bound reaches 2^63");
+  for (uint64_t b : fbound_)
+    if (b >= k2_63) fail(DG_E_OVERFLOW, "static path-count bound reaches 2^63");
+  for (uint64_t b : sbound_)
+    if (b >= k2_63) fail(DG_E_OVERFLOW, "static path-count bound reaches 2^63");
 
   // Levels: an instruction runs one level after the latest instruction it
   // reads; within a level the order is free.  Component sums over more than
@@ -865,9 +879,7 @@ Plan Compiler::run() {
   h.union_entries = (int32_t)union_entries;
   h.nlevel = (int32_t)level_start.size() - 1;
   h.serial_vars = serial_vars;
-  // (Bounds are products and sums of integers; below 2^53 doubles hold
-  // them exactly.)
-  h.no_overflow = cbound <= 4294967295.0 ? 1 : 0;
+  h.no_overflow = cbound <= 4294967295u ? 1 : 0;
   size_t off = (sizeof(DgpHeader) + 15) & ~size_t(15);
   h.instr_off = (int32_t)off;
   off += ins_.size() * sizeof(DgpInstr);

@@ -29,7 +29,7 @@ struct FactorPos {
 struct Plan {
   std::vector<uint8_t> blob;  // DgpHeader followed by the instruction, factor, leaf and term arrays
   int64_t max_row_size = 0;   // static bound on entries per row
-  double count_bound = 0;     // static bound on one path count
+  uint64_t count_bound = 0;   // static bound on one path count
   int max_leaf_terms = 0;
   std::vector<FactorPos> fpos;  // per factor (host side only)
 

@@ -19,8 +19,33 @@ extern const char* const kJitKernelsDevH;
 namespace {
 
 std::mutex g_mu;
-std::map<std::string, std::vector<char>> g_code;                    // source -> code object
-std::map<std::pair<int, std::string>, hipModule_t> g_modules;       // (device, source) -> module
+// Loaded modules: (device, source) -> module and the number of holders.
+struct Loaded {
+  hipModule_t mod = nullptr;
+  int refs = 0;
+};
+std::map<std::pair<int, std::string>, Loaded> g_modules;
+// Compiled code objects by source, with a use stamp; at most kCodeCache are
+// kept (least recently used dropped first).
+struct Code {
+  std::vector<char> bytes;
+  uint64_t stamp = 0;
+};
+const size_t kCodeCache = 32;
+std::map<std::string, Code> g_code;
+uint64_t g_clock = 0;
+
+void remember_code(const std::string& source, const std::vector<char>& code) {  // g_mu held
+  Code& c = g_code[source];
+  c.bytes = code;
+  c.stamp = ++g_clock;
+  while (g_code.size() > kCodeCache) {
+    auto oldest = g_code.begin();
+    for (auto it = g_code.begin(); it != g_code.end(); ++it)
+      if (it->second.stamp < oldest->second.stamp) oldest = it;
+    g_code.erase(oldest);
+  }
+}
 
 bool compile(const std::string& src, std::vector<char>* code, std::string* log) {
   hiprtcProgram prog;
@@ -67,21 +92,26 @@ bool jit_load(const std::string& source, JitModule* out, std::string* log) {
     return false;
   }
   std::vector<char> code;
+  out->mod = nullptr;
   {
     std::lock_guard<std::mutex> lock(g_mu);
     auto mit = g_modules.find({dev, source});
     if (mit != g_modules.end()) {
-      out->mod = mit->second;
+      ++mit->second.refs;
+      out->mod = mit->second.mod;
     } else {
       auto it = g_code.find(source);
-      if (it != g_code.end()) code = it->second;
+      if (it != g_code.end()) {
+        code = it->second.bytes;
+        it->second.stamp = ++g_clock;
+      }
     }
   }
   if (!out->mod) {
     if (code.empty()) {
       if (!compile(source, &code, log)) return false;
       std::lock_guard<std::mutex> lock(g_mu);
-      g_code[source] = code;
+      remember_code(source, code);
     }
     hipModule_t m = nullptr;
     hipError_t e = hipModuleLoadData(&m, code.data());
@@ -90,15 +120,17 @@ bool jit_load(const std::string& source, JitModule* out, std::string* log) {
       return false;
     }
     std::lock_guard<std::mutex> lock(g_mu);
-    auto mit = g_modules.find({dev, source});
-    if (mit != g_modules.end()) {
-      (void)hipModuleUnload(m);
-      out->mod = mit->second;
+    Loaded& L = g_modules[{dev, source}];
+    if (L.mod) {
+      (void)hipModuleUnload(m);  // another thread loaded it meanwhile
     } else {
-      g_modules[{dev, source}] = m;
-      out->mod = m;
+      L.mod = m;
     }
+    ++L.refs;
+    out->mod = L.mod;
   }
+  out->dev = dev;
+  out->source = source;
   // A module holds either the enumeration kernels or the comparison kernel;
   // a name it lacks leaves a null function.  The failed lookup also sets
   // the thread's last HIP error, which is cleared here so that it is not
@@ -115,6 +147,20 @@ bool jit_load(const std::string& source, JitModule* out, std::string* log) {
   get("dg_compare", &out->compare);
   get("dg_enumerate_wide", &out->enumerate_wide);
   return true;
+}
+
+void jit_release(JitModule* m) {
+  if (!m || !m->mod) return;
+  std::lock_guard<std::mutex> lock(g_mu);
+  auto it = g_modules.find({m->dev, m->source});
+  if (it != g_modules.end() && --it->second.refs == 0) {
+    int cur = -1;
+    const bool have = hipGetDevice(&cur) == hipSuccess;
+    if (hipSetDevice(m->dev) == hipSuccess) (void)hipModuleUnload(it->second.mod);
+    if (have) (void)hipSetDevice(cur);
+    g_modules.erase(it);
+  }
+  *m = JitModule{};
 }
 
 }  // namespace dg

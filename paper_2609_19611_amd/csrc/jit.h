@@ -35,12 +35,20 @@ const char* const* jit_compile_options();
 namespace dg {
 
 // Compiles (or takes from the cache) and loads on the current device.
-// Returns true and the module; on failure a message in *log.
+// Returns true and the module; on failure a message in *log.  Modules are
+// shared by every caller that loads the same source on the same device and
+// counted: each successful jit_load is matched by one jit_release, and the
+// last release unloads the module.  Compiled code objects stay in a small
+// host-side cache (the most recently used few) so that a graph built again
+// from the same text is not compiled again.
 struct JitModule {
   hipModule_t mod = nullptr;
   hipFunction_t sizes = nullptr, fill = nullptr, enumerate = nullptr, compare = nullptr, enumerate_wide = nullptr;
+  int dev = -1;        // device the module is loaded on
+  std::string source;  // its source (the key of the shared module)
 };
 bool jit_load(const std::string& source, JitModule* out, std::string* log);
+void jit_release(JitModule* m);
 
 // Whether run-time specialisation is enabled (environment DIRIGO_JIT=0
 // turns it off; the precompiled kernels then run every graph).

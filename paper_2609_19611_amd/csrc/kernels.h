@@ -25,14 +25,17 @@ hipError_t launch_compare(const uint8_t* blob_a, const uint8_t* blob_b, const dg
 hipError_t launch_scan(int64_t* v, int64_t n, int64_t* sums, hipStream_t s);
 int64_t scan_temp_entries(int64_t n);
 // Single pass over n locations: offsets[0..n] and the rows (written only
-// where they fit `capacity` entries).  status: n words, ticket: one word.
-hipError_t launch_enumerate(const uint8_t* blob, dgc::LocSrc locs, int64_t n, int64_t* offsets, uint32_t* ids,
-                            uint32_t* cnt, uint64_t capacity, uint64_t* status, uint64_t* ticket, uint32_t* err,
-                            int block, uint32_t lds, hipStream_t s);
+// where they fit `capacity` entries).  status: n words, ticket: one word,
+// both cleared by the caller before the first launch.  One launch runs
+// `blocks` blocks, each taking the next location from the ticket; launches
+// whose blocks add up to n cover every location.
+hipError_t launch_enumerate(const uint8_t* blob, dgc::LocSrc locs, int64_t n, int64_t blocks, int64_t* offsets,
+                            uint32_t* ids, uint32_t* cnt, uint64_t capacity, uint64_t* status, uint64_t* ticket,
+                            uint32_t* err, int block, uint32_t lds, hipStream_t s);
 // The same with 64-bit ids and counts.
-hipError_t launch_enumerate_wide(const uint8_t* blob, dgc::LocSrc locs, int64_t n, int64_t* offsets,
-                                 uint64_t* ids, uint64_t* cnt, uint64_t capacity, uint64_t* status, uint64_t* ticket,
-                                 uint32_t* err, int block, uint32_t lds, hipStream_t s);
+hipError_t launch_enumerate_wide(const uint8_t* blob, dgc::LocSrc locs, int64_t n, int64_t blocks,
+                                 int64_t* offsets, uint64_t* ids, uint64_t* cnt, uint64_t capacity, uint64_t* status,
+                                 uint64_t* ticket, uint32_t* err, int block, uint32_t lds, hipStream_t s);
 // Expression DAGs (dag_program.h, DgdHeader; lds: the program's lds_bytes):
 // node and edge counts of location i into nodes_n[i + 1], edges_n[i + 1];
 // then nodes and edges at node_off[i], edge_off[i].

@@ -420,24 +420,20 @@ hipError_t launch_compare(const uint8_t* blob_a, const uint8_t* blob_b, const dg
 
 int64_t scan_temp_entries(int64_t n) { return (n + SCAN_TILE - 1) / SCAN_TILE + 1; }
 
-hipError_t launch_enumerate(const uint8_t* blob, dgc::LocSrc locs, int64_t n, int64_t* offsets, uint32_t* ids,
-                            uint32_t* cnt, uint64_t capacity, uint64_t* status, uint64_t* ticket, uint32_t* err,
-                            int block, uint32_t lds, hipStream_t s) {
-  if (n <= 0) return hipSuccess;
+hipError_t launch_enumerate(const uint8_t* blob, dgc::LocSrc locs, int64_t n, int64_t blocks, int64_t* offsets,
+                            uint32_t* ids, uint32_t* cnt, uint64_t capacity, uint64_t* status, uint64_t* ticket,
+                            uint32_t* err, int block, uint32_t lds, hipStream_t s) {
+  if (blocks <= 0) return hipSuccess;
   if (block != 64 && block != 256) return hipErrorInvalidConfiguration;
-  // Clear the look-back status words and the ticket (status holds n words,
-  // the ticket one more).
-  hipLaunchKernelGGL(k_zero_u64, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, status, n);
-  hipLaunchKernelGGL(k_zero_u64, dim3(1), dim3(1), 0, s, ticket, (int64_t)1);
   hipError_t e;
   unsigned long long* t = reinterpret_cast<unsigned long long*>(ticket);
   if (block == 256) {
     if ((e = allow_lds(k_enumerate<256>, lds)) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_enumerate<256>, dim3((unsigned)n), dim3(256), lds, s, blob, locs, n, offsets, ids, cnt,
+    hipLaunchKernelGGL(k_enumerate<256>, dim3((unsigned)blocks), dim3(256), lds, s, blob, locs, n, offsets, ids, cnt,
                        capacity, status, t, err);
   } else {
     if ((e = allow_lds(k_enumerate<64>, lds)) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_enumerate<64>, dim3((unsigned)n), dim3(64), lds, s, blob, locs, n, offsets, ids, cnt,
+    hipLaunchKernelGGL(k_enumerate<64>, dim3((unsigned)blocks), dim3(64), lds, s, blob, locs, n, offsets, ids, cnt,
                        capacity, status, t, err);
   }
   return hipGetLastError();
@@ -449,23 +445,21 @@ hipError_t launch_rebase(const int64_t* src, int64_t* dst, int64_t count, int64_
   return hipGetLastError();
 }
 
-hipError_t launch_enumerate_wide(const uint8_t* blob, dgc::LocSrc locs, int64_t n, int64_t* offsets,
-                                 uint64_t* ids, uint64_t* cnt, uint64_t capacity, uint64_t* status, uint64_t* ticket,
-                                 uint32_t* err, int block, uint32_t lds, hipStream_t s) {
-  if (n <= 0) return hipSuccess;
+hipError_t launch_enumerate_wide(const uint8_t* blob, dgc::LocSrc locs, int64_t n, int64_t blocks,
+                                 int64_t* offsets, uint64_t* ids, uint64_t* cnt, uint64_t capacity, uint64_t* status,
+                                 uint64_t* ticket, uint32_t* err, int block, uint32_t lds, hipStream_t s) {
+  if (blocks <= 0) return hipSuccess;
   if (block != 64 && block != 256) return hipErrorInvalidConfiguration;
-  hipLaunchKernelGGL(k_zero_u64, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, status, n);
-  hipLaunchKernelGGL(k_zero_u64, dim3(1), dim3(1), 0, s, ticket, (int64_t)1);
   hipError_t e;
   unsigned long long* t = reinterpret_cast<unsigned long long*>(ticket);
   if (block == 256) {
     if ((e = allow_lds(k_enumerate_wide<256>, lds)) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_enumerate_wide<256>, dim3((unsigned)n), dim3(256), lds, s, blob, locs, n, offsets, ids, cnt,
-                       capacity, status, t, err);
+    hipLaunchKernelGGL(k_enumerate_wide<256>, dim3((unsigned)blocks), dim3(256), lds, s, blob, locs, n, offsets, ids,
+                       cnt, capacity, status, t, err);
   } else {
     if ((e = allow_lds(k_enumerate_wide<64>, lds)) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_enumerate_wide<64>, dim3((unsigned)n), dim3(64), lds, s, blob, locs, n, offsets, ids, cnt,
-                       capacity, status, t, err);
+    hipLaunchKernelGGL(k_enumerate_wide<64>, dim3((unsigned)blocks), dim3(64), lds, s, blob, locs, n, offsets, ids,
+                       cnt, capacity, status, t, err);
   }
   return hipGetLastError();
 }

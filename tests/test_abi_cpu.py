@@ -182,3 +182,33 @@ def test_element_counts_past_2_62_are_rejected(text):
     with pytest.raises(B.DgError) as e:
         B.dg_graph_parse(text)
     assert e.value.name == "DG_E_OVERFLOW"
+
+
+def test_calls_over_2_31_locations_are_rejected_before_any_work():
+    """A call takes at most 2^31 locations; more is DG_E_INVALID_ARG, checked
+    before any device work (no device is needed here)."""
+    g = B.dg_graph_parse("dgir 1\nleaf x 65536,65536\nop y relu x\noutput y 65536,65536\n")  # 2^32 outputs
+    fake = ctypes.c_void_p(0x1000)  # never dereferenced
+    total = ctypes.c_int64()
+    n = (1 << 31) + 1
+    calls = [
+        lambda: B._lib.dg_enumerate_sizes(g.handle, fake, n, fake, fake, ctypes.byref(total), None),
+        lambda: B._lib.dg_enumerate_fill(g.handle, fake, n, fake, fake, fake, fake, None),
+        lambda: B._lib.dg_enumerate(g.handle, fake, n, fake, fake, fake, 16, fake, ctypes.byref(total), None),
+        lambda: B._lib.dg_enumerate_range(g.handle, 0, n, fake, fake, fake, 16, fake, ctypes.byref(total), None),
+        lambda: B._lib.dg_compare(g.handle, g.handle, fake, n, fake, fake, ctypes.byref(total), fake, None),
+        lambda: B._lib.dg_compare_range(g.handle, g.handle, 0, n, 0, fake, fake, ctypes.byref(total), fake, None),
+    ]
+    for call in calls:
+        assert B.STATUS_NAMES[call()] == "DG_E_INVALID_ARG"
+
+
+def test_count_bound_is_an_exact_integer():
+    """The static path-count bound is reported as an integer: above 2^53,
+    where a double would round, it is still a sound bound of the exact
+    counts (three nested layer norms over 4,096 elements)."""
+    text = tiny_graphs.nested_layer_norms(4096)
+    info = B.dg_graph_info(B.dg_graph_parse(text))
+    assert isinstance(info["count_bound"], int) and info["count_bound"] > 2 ** 53
+    exact = max(tiny_graphs.nested_layer_norm_counts(4096, 0))
+    assert exact <= info["count_bound"] < 2 ** 63
