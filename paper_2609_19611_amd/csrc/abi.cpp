@@ -58,6 +58,15 @@ thread_local std::string g_last_error;
 std::mutex g_pair_mu;
 std::map<std::tuple<uint64_t, uint64_t, int, int>, DevKernels> g_pair_jit;
 
+// Plans of a pair whose graphs view some leaf with different merged dims
+// (each graph's own plan is then not comparable with the other's): both
+// recompiled over the joint view, with their device copies per device.
+struct PairPlans {
+  dg::Plan a, b;
+  std::map<int, std::pair<uint8_t*, uint8_t*>> dev;
+};
+std::map<std::pair<uint64_t, uint64_t>, PairPlans> g_pair_plans;  // under g_pair_mu
+
 // Most locations one call takes (the helper kernels run flat grids of one
 // thread per location).
 constexpr int64_t kMaxLocations = int64_t(1) << 31;
@@ -188,7 +197,8 @@ const dg::JitModule* graph_jit(const dg_graph* cg) {
 
 // Specialised comparison kernel of the pair (a, b) on the current device;
 // nullptr when specialisation is off or failed.
-const dg::JitModule* pair_jit(const dg_graph* ca, const dg_graph* b, const dgc::PairPlan& pp, int block) {
+const dg::JitModule* pair_jit(const dg_graph* ca, const dg_graph* b, const dg::Plan& plan_a, const dg::Plan& plan_b,
+                              const dgc::PairPlan& pp, int block) {
   if (!dg::jit_enabled()) return nullptr;
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return nullptr;
@@ -196,7 +206,7 @@ const dg::JitModule* pair_jit(const dg_graph* ca, const dg_graph* b, const dgc::
   DevKernels& k = g_pair_jit[std::make_tuple(ca->serial, b->serial, dev, block)];
   if (!k.tried) {
     k.tried = true;
-    k.ok = dg::jit_load(dg::jit_compare_source(ca->plan, b->plan, pp, block), &k.jm, &k.log) && k.jm.compare;
+    k.ok = dg::jit_load(dg::jit_compare_source(plan_a, plan_b, pp, block), &k.jm, &k.log) && k.jm.compare;
   }
   return k.ok ? &k.jm : nullptr;
 }
@@ -370,6 +380,21 @@ void dg_graph_destroy(dg_graph* g) {
       if (std::get<0>(it->first) == g->serial || std::get<1>(it->first) == g->serial) {
         dg::jit_release(&it->second.jm);
         it = g_pair_jit.erase(it);
+      } else {
+        ++it;
+      }
+    }
+    for (auto it = g_pair_plans.begin(); it != g_pair_plans.end();) {
+      if (it->first.first == g->serial || it->first.second == g->serial) {
+        int cur = 0;
+        const bool have = hipGetDevice(&cur) == hipSuccess;
+        for (auto& d : it->second.dev)
+          if (hipSetDevice(d.first) == hipSuccess) {
+            (void)hipFree(d.second.first);
+            (void)hipFree(d.second.second);
+          }
+        if (have) (void)hipSetDevice(cur);
+        it = g_pair_plans.erase(it);
       } else {
         ++it;
       }
@@ -552,6 +577,7 @@ dg_status enumerate_impl(const dg_graph* g, dgc::LocSrc src, int64_t n, int64_t*
   const uint8_t* blob = nullptr;
   dg_status st = device_blob(g, &blob);
   if (st != DG_OK) return st;
+  const dg::JitModule* jm = wide ? graph_jit_wide(g) : graph_jit(g);
   WsLayout w = ws_layout(n);
   uint8_t* ws = static_cast<uint8_t*>(d_ws);
   uint32_t* err = reinterpret_cast<uint32_t*>(ws + w.err);
@@ -559,7 +585,6 @@ dg_status enumerate_impl(const dg_graph* g, dgc::LocSrc src, int64_t n, int64_t*
   uint64_t* status = reinterpret_cast<uint64_t*>(ws + w.flags);
   uint64_t* ticket = reinterpret_cast<uint64_t*>(ws + w.ticket);
   uint64_t cap = (uint64_t)capacity;
-  const dg::JitModule* jm = wide ? graph_jit_wide(g) : graph_jit(g);
   // Blocks take their locations from a ticket counter, so a list longer
   // than one grid runs as several launches of the same kernel on the
   // stream: the blocks of a later launch take the next tickets and look
@@ -588,6 +613,7 @@ dg_status enumerate_impl(const dg_graph* g, dgc::LocSrc src, int64_t n, int64_t*
   *h_total = total;
   return device_errors(bits);
 }
+
 
 // Whether [first, first + n) lies inside the output of g.
 bool range_ok(const dg_graph* g, int64_t first, int64_t n) {
@@ -714,6 +740,45 @@ dg_status dg_enumerate_stream(const dg_graph* g, int64_t first, int64_t n, void*
 
 namespace {
 
+// The joint plans of (a, b) and their copies on the current device,
+// compiled and uploaded on first use.
+dg_status joint_plans(const dg_graph* a, const dg_graph* b, const dg::Plan** pa, const dg::Plan** pb,
+                      const uint8_t** ba, const uint8_t** bb) {
+  int dev = 0;
+  DG_HIP(hipGetDevice(&dev), "hipGetDevice");
+  std::lock_guard<std::mutex> lock(g_pair_mu);
+  const auto key = std::make_pair(a->serial, b->serial);
+  auto it = g_pair_plans.find(key);
+  if (it == g_pair_plans.end()) {
+    PairPlans P;
+    dg::compile_pair_plans(a->ir, b->ir, &P.a, &P.b);
+    it = g_pair_plans.emplace(key, std::move(P)).first;
+  }
+  PairPlans& P = it->second;
+  auto d = P.dev.find(dev);
+  if (d == P.dev.end()) {
+    uint8_t* p[2] = {nullptr, nullptr};
+    const dg::Plan* src[2] = {&P.a, &P.b};
+    for (int k = 0; k < 2; ++k) {
+      void* q = nullptr;
+      hipError_t e = hipMalloc(&q, src[k]->blob.size());
+      if (e == hipSuccess) e = hipMemcpy(q, src[k]->blob.data(), src[k]->blob.size(), hipMemcpyHostToDevice);
+      if (e != hipSuccess) {
+        if (q) (void)hipFree(q);
+        if (k == 1) (void)hipFree(p[0]);
+        return hip_error(e, "pair plan upload");
+      }
+      p[k] = static_cast<uint8_t*>(q);
+    }
+    d = P.dev.emplace(dev, std::make_pair(p[0], p[1])).first;
+  }
+  *pa = &P.a;
+  *pb = &P.b;
+  *ba = d->second.first;
+  *bb = d->second.second;
+  return DG_OK;
+}
+
 dg_status compare_impl(const dg_graph* a, const dg_graph* b, dgc::LocSrc src, int64_t n, uint64_t limit,
                        uint8_t* d_status, int64_t* d_mismatch, int64_t* h_n_mismatch, void* d_ws, void* stream) {
   if (!d_ws) return set_error(DG_E_WORKSPACE, "workspace is required");
@@ -736,16 +801,26 @@ dg_status compare_impl(const dg_graph* a, const dg_graph* b, dgc::LocSrc src, in
       const int v = std::atoi(e);
       if (v == 64 || v == 128 || v == 256) block = v;
     }
+    // Both plans must view each leaf with the same merged dims; when the
+    // graphs' own plans do not, the pair's joint plans are used.
+    const dg::Plan* plan_a = &a->plan;
+    const dg::Plan* plan_b = &b->plan;
+    const uint8_t *ba = nullptr, *bb = nullptr;
+    dg_status st = DG_OK;
+    if (a->plan.leaf_part != b->plan.leaf_part) {
+      st = joint_plans(a, b, &plan_a, &plan_b, &ba, &bb);
+      if (st != DG_OK) return st;
+    } else {
+      st = device_blob(a, &ba);
+      if (st != DG_OK) return st;
+      st = device_blob(b, &bb);
+      if (st != DG_OK) return st;
+    }
     dgc::PairPlan pp;
-    dg::pair_plan(a->plan, b->plan, block, &pp);
+    dg::pair_plan(*plan_a, *plan_b, block, &pp);
     if (pp.lds_bytes > (uint32_t)max_lds_per_block())
       return set_error(DG_E_CAPACITY, "comparison needs " + std::to_string(pp.lds_bytes) + " bytes of LDS");
     hipStream_t s = static_cast<hipStream_t>(stream);
-    const uint8_t *ba = nullptr, *bb = nullptr;
-    dg_status st = device_blob(a, &ba);
-    if (st != DG_OK) return st;
-    st = device_blob(b, &bb);
-    if (st != DG_OK) return st;
     WsLayout w = ws_layout(n);
     uint8_t* ws = static_cast<uint8_t*>(d_ws);
     uint32_t* err = reinterpret_cast<uint32_t*>(ws + w.err);
@@ -753,7 +828,7 @@ dg_status compare_impl(const dg_graph* a, const dg_graph* b, dgc::LocSrc src, in
     DG_HIP(dgk::launch_zero(err, s), "zero");
     uint64_t* found = reinterpret_cast<uint64_t*>(ws + w.found);
     DG_HIP(dgk::launch_zero_u64(found, 1, s), "zero count");
-    const dg::JitModule* jm = pair_jit(a, b, pp, block);
+    const dg::JitModule* jm = pair_jit(a, b, *plan_a, *plan_b, pp, block);
     dgc::PairPlan* d_pp = reinterpret_cast<dgc::PairPlan*>(ws + w.pair);
     if (!jm) {
       if (block != 64 && block != 256) return set_error(DG_E_INVALID_ARG, "block size needs specialised kernels");

@@ -15,6 +15,7 @@
 // keeps the term count small (e.g. a softmax row plus its own element, or a
 // normalisation's statistics set plus its own element).
 #include "compile.h"
+#include "view.h"
 
 #include <algorithm>
 #include <cmath>
@@ -616,6 +617,19 @@ class Compiler {
         }
       }
     }
+    // Guards of merged dims: each merged dim's own index must be valid too.
+    for (const auto& gd : G.guards) {
+      const IndexFn& f = gd.first;
+      if (fn_magnitude(f, vmin, vmax) >= (int64_t(1) << 30))
+        fail(DG_E_UNSUPPORTED_OP, op.kind + ": index arithmetic exceeds 32 bits");
+      if (f.terms.empty()) continue;
+      auto rg = fn_range(f, vmin, vmax);
+      bool trivial = (f.mode != 1 || f.s == 1) && rg.first >= 0 && rg.second <= gd.second - 1;
+      if (!trivial) {
+        preds.push_back(&f);
+        psize.push_back(gd.second);
+      }
+    }
     for (const Operand& r : G.ops) {
       const Dims& s = g_.tensors[r.tensor].shape;
       UnionFind uf(NV);
@@ -911,7 +925,33 @@ Plan Compiler::run() {
 
 }  // namespace
 
-Plan compile_plan(const GraphIR& g) { return Compiler(g).run(); }
+Plan compile_plan(const GraphIR& g, const DimPartition* start) {
+  const MergedView v = merged_view(g, start);
+  Plan p = Compiler(v.ir).run();
+  p.part = v.part;
+  for (int t : g.leaves) p.leaf_part.push_back(v.part[t]);
+  return p;
+}
+
+void compile_pair_plans(const GraphIR& a, const GraphIR& b, Plan* pa, Plan* pb) {
+  if (a.leaves.size() != b.leaves.size()) fail(DG_E_SIGNATURE, "leaf count differs");
+  *pa = compile_plan(a);
+  *pb = compile_plan(b);
+  // Both must view every leaf with the same merged dims: start both from
+  // the join of their leaf partitions until they agree (each round only
+  // coarsens, so this ends).
+  while (pa->leaf_part != pb->leaf_part) {
+    DimPartition sa = pa->part, sb = pb->part;
+    for (size_t i = 0; i < a.leaves.size(); ++i) {
+      if (pa->leaf_part[i].size() != pb->leaf_part[i].size()) fail(DG_E_SIGNATURE, "leaf ranks differ");
+      const std::vector<int> j = join_partition(pa->leaf_part[i], pb->leaf_part[i]);
+      sa[a.leaves[i]] = j;
+      sb[b.leaves[i]] = j;
+    }
+    *pa = compile_plan(a, &sa);
+    *pb = compile_plan(b, &sb);
+  }
+}
 
 uint32_t plan_lds_bytes(const Plan& p, int nthreads, uint32_t word_bytes) {
   const DgpHeader& h = p.header();

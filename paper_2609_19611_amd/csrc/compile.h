@@ -7,6 +7,7 @@
 #include "core.h"
 #include "graph.h"
 #include "program.h"
+#include "view.h"
 
 namespace dg {
 
@@ -32,15 +33,23 @@ struct Plan {
   uint64_t count_bound = 0;   // static bound on one path count
   int max_leaf_terms = 0;
   std::vector<FactorPos> fpos;  // per factor (host side only)
+  DimPartition part;            // merged dims of every tensor (view.h)
+  std::vector<std::vector<int>> leaf_part;  // the leaves' partitions, in declaration order
 
   const DgpHeader& header() const { return *reinterpret_cast<const DgpHeader*>(blob.data()); }
 };
 
-// Compiles the back-projection of one (symbolic) output location.  Throws
-// Failure(DG_E_UNSUPPORTED_OP) for graphs whose dataflow is not separable
-// (an operand with two dims fed by one coupled set of variables) and
-// Failure(DG_E_OVERFLOW) if the static path-count bound exceeds 2^63.
-Plan compile_plan(const GraphIR& g);
+// Compiles the back-projection of one (symbolic) output location over the
+// graph's merged-dim view (view.h; `start` forces at least those merges).
+// Throws Failure(DG_E_UNSUPPORTED_OP) for reads the view cannot make
+// separable and Failure(DG_E_OVERFLOW) if the static path-count bound
+// reaches 2^63.  Leaves in the plan have the merged shapes; their ids and
+// row order are those of the original shapes.
+Plan compile_plan(const GraphIR& g, const DimPartition* start = nullptr);
+
+// Plans of two graphs over the same leaves for a comparison: both view each
+// leaf with the same merged dims (the join of what each needs).
+void compile_pair_plans(const GraphIR& a, const GraphIR& b, Plan* pa, Plan* pb);
 
 // Local data share bytes one location of this plan needs with a block of
 // `nthreads` threads (word_bytes 4: 32-bit ids and counts, 8: 64-bit).

@@ -8,6 +8,7 @@
 #include "graph.h"
 
 #include <algorithm>
+#include <map>
 #include <cctype>
 #include <set>
 #include <sstream>
@@ -628,23 +629,74 @@ Dims lower_op(Ctx c) {
     return out;
   }
   if (k == "reshape") {
+    // y[o] reads x at the element with the same row-major flat index F.
+    // Without unit dims, the dims of x and of y are two mixed-radix
+    // factorisations of F; when their strides form one divisibility chain
+    // they have a common refinement, and every digit of x is a sum of
+    // pieces floor(o_j / a) mod b of single digits of y, which index
+    // functions express (a mod is o - b * floor(o / b)).  Two factorisations
+    // of one block with no common refinement ([6,4] and [4,6]) are refused.
     need(op, 1, 1);
     const Dims& x = c.S(0);
     Dims out = attr_required(op, "shape");
     for (int64_t v : out)
       if (v <= 0) fail(DG_E_SHAPE, "reshape: dims must be positive");
     if (numel(out) != numel(x)) fail(DG_E_SHAPE, "reshape: element count differs");
-    // Separable plans handle reshapes that only insert or drop size-1 dims.
-    std::vector<int> xo, oo;
+    std::vector<int> xo, oo;  // non-unit dims
     for (size_t d = 0; d < x.size(); ++d)
       if (x[d] != 1) xo.push_back((int)d);
     for (size_t d = 0; d < out.size(); ++d)
       if (out[d] != 1) oo.push_back((int)d);
-    bool same = xo.size() == oo.size();
-    for (size_t i = 0; same && i < xo.size(); ++i) same = x[xo[i]] == out[oo[i]];
-    if (!same) fail(DG_E_UNSUPPORTED_OP, "reshape: only reshapes that insert or drop size-1 dims are supported");
+    // Strides of the non-unit dims in the flat index.
+    std::map<int, int64_t> xst, ost;
+    int64_t st = 1;
+    for (int i = (int)xo.size() - 1; i >= 0; --i) {
+      xst[xo[i]] = st;
+      st *= x[xo[i]];
+    }
+    st = 1;
+    for (int j = (int)oo.size() - 1; j >= 0; --j) {
+      ost[oo[j]] = st;
+      st *= out[oo[j]];
+    }
+    const int64_t total = st;
+    std::set<int64_t> bp{1, total};
+    for (auto& e : xst) bp.insert(e.second);
+    for (auto& e : ost) bp.insert(e.second);
+    std::vector<int64_t> chain(bp.begin(), bp.end());
+    for (size_t q = 1; q < chain.size(); ++q)
+      if (chain[q] % chain[q - 1])
+        fail(DG_E_UNSUPPORTED_OP, "reshape: the two shapes factor the flat index with no common refinement");
     std::vector<IndexFn> f(x.size(), IndexFn::constant(0));
-    for (size_t i = 0; i < xo.size(); ++i) f[xo[i]] = IndexFn::var(oo[i]);
+    for (int d : xo) {
+      const int64_t lo = xst[d], hi = xst[d] * x[d];
+      IndexFn e;
+      for (size_t q = 0; q + 1 < chain.size(); ++q) {
+        const int64_t s0 = chain[q], s1 = chain[q + 1];
+        if (s0 < lo || s1 > hi) continue;
+        // Refined digit floor(F / s0) mod (s1 / s0), inside digit j of y.
+        int j = -1;
+        for (int jj : oo)
+          if (ost[jj] <= s0 && s1 <= ost[jj] * out[jj]) j = jj;
+        const int64_t a = s0 / ost[j], b = s1 / s0, w = s0 / lo;
+        e.plus(j, w, a);
+        if (s1 != ost[j] * out[j]) e.plus(j, -w * b, a * b);
+      }
+      // Combine terms of the same variable and divisor.
+      IndexFn m;
+      for (const auto& t : e.terms) {
+        bool found = false;
+        for (auto& u : m.terms)
+          if (u.var == t.var && u.vdiv == t.vdiv) {
+            u.coef += t.coef;
+            found = true;
+          }
+        if (!found) m.terms.push_back(t);
+      }
+      f[d].terms.clear();
+      for (const auto& t : m.terms)
+        if (t.coef != 0) f[d].terms.push_back(t);
+    }
     ReadGroup g = group_no_window();
     g.ops.push_back({c.T(0), 1, f});
     G.push_back(g);

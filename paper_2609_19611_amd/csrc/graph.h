@@ -60,10 +60,14 @@ struct Operand {
 
 // One read group: every window point w in the box [wlo, whi) (together with
 // the output coordinates) reads each operand once per multiplicity, provided
-// every operand index of that point is valid.
+// every operand index of that point is valid.  `guards` are further index
+// functions that must be valid (value in [0, size)) for a point to read;
+// lowering never writes them, the plan compiler's view of merged dims does
+// (one per merged dim, see compile.cpp).
 struct ReadGroup {
   Dims wlo, whi;
   std::vector<Operand> ops;
+  std::vector<std::pair<IndexFn, int64_t>> guards;
 };
 
 struct Tensor {

@@ -132,7 +132,8 @@ int dgh_compare(const char* ta, int64_t la, const char* tb, int64_t lb, const in
   try {
     dg::GraphIR ia = dg::parse_dgir(std::string(ta, (size_t)la));
     dg::GraphIR ib = dg::parse_dgir(std::string(tb, (size_t)lb));
-    dg::Plan pa = dg::compile_plan(ia), pb = dg::compile_plan(ib);
+    dg::Plan pa, pb;
+    dg::compile_pair_plans(ia, ib, &pa, &pb);
     dgc::PairPlan pp;
     dg::pair_plan(pa, pb, 1, &pp);
     std::vector<uint64_t> area(pp.lds_bytes / 8 + 1);
@@ -260,7 +261,8 @@ int dgh_jit_compare_source(const char* ta, int64_t la, const char* tb, int64_t l
   try {
     dg::GraphIR ia = dg::parse_dgir(std::string(ta, (size_t)la));
     dg::GraphIR ib = dg::parse_dgir(std::string(tb, (size_t)lb));
-    dg::Plan pa = dg::compile_plan(ia), pb = dg::compile_plan(ib);
+    dg::Plan pa, pb;
+    dg::compile_pair_plans(ia, ib, &pa, &pb);
     dgc::PairPlan pp;
     dg::pair_plan(pa, pb, block, &pp);
     std::string s = dg::jit_compare_source(pa, pb, pp, block);

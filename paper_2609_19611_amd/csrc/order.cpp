@@ -128,6 +128,14 @@ int64_t forward_location(const GraphIR& g, int t, int64_t e) {
     r /= ts[d];
   }
   for (const OpNode& op : g.ops) {
+    if (op.kind == "reshape") {
+      // A reshape keeps the flat index: element e of its operand is
+      // element e of its result, and no other result element reads it.
+      if (op.in[0] != t) continue;
+      const int64_t l = forward_location(g, op.out, e);
+      if (l >= 0 && (best < 0 || l < best)) best = l;
+      continue;
+    }
     std::vector<int> perm;
     if (!op_permutes(g, op, t, &perm)) continue;
     const Dims& os = g.tensors[op.out].shape;

@@ -14,7 +14,7 @@ from paper_2609_19611_amd import workloads as W
 pytestmark = pytest.mark.gpu
 
 CAT = tiny_graphs.catalogue()
-SEPARABLE = sorted(set(CAT) - tiny_graphs.NONSEPARABLE)
+SEPARABLE = sorted(CAT)
 KEYS = ("node_offsets", "edge_offsets", "nodes", "node_edge", "edges", "mults")
 
 

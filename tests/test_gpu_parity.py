@@ -18,7 +18,7 @@ from paper_2609_19611_amd import workloads as W
 pytestmark = pytest.mark.gpu
 
 CAT = tiny_graphs.catalogue()
-SEPARABLE = sorted(set(CAT) - tiny_graphs.NONSEPARABLE)
+SEPARABLE = sorted(CAT)
 
 
 @pytest.fixture(scope="module")
@@ -143,26 +143,6 @@ def test_c4_full(B):
     assert set(vals.cpu().tolist()) == {1, 66, 67, 4225, 4226}
 
 
-def test_c5_clean_and_faults(B):
-    ref_text = W.c5_reference_text()
-    ref = B.dg_graph_parse(ref_text)
-    locs = W.config_locations("c5")
-    d_locs = torch.as_tensor(locs, dtype=torch.int64, device="cuda")
-    status, mism = B.compare_locations(ref, B.dg_graph_parse(W.c5_variant_text()), d_locs)
-    assert mism.numel() == 0 and int(status.max()) == 0
-    og_ref = oracle.Graph(ref_text)
-    rng = np.random.default_rng(5)
-    sample = np.sort(rng.choice(len(locs), 160, replace=False))
-    for f in W.c5_faults():
-        vt = W.c5_variant_text(fault=f)
-        status, mism = B.compare_locations(ref, B.dg_graph_parse(vt), d_locs)
-        st = status.cpu().numpy()
-        assert np.array_equal(mism.cpu().numpy(), np.nonzero(st)[0]), f
-        want = oracle.compare(og_ref, oracle.Graph(vt), [locs[i] for i in sample], threads=8)
-        assert np.array_equal(st[sample], want), f
-        assert st.any(), f
-
-
 def test_c5_faults_at_boundaries(B):
     """Every fault of the split-K variant against the oracle at the output's
     padding edges (first and last two rows and columns, corner images and
@@ -208,6 +188,21 @@ def test_compare_small_graphs_against_oracle(B, kernels, monkeypatch):
                        "y", [3, 2])
     st, _ = B.compare_locations(B.dg_graph_parse(a), B.dg_graph_parse(b), range(6))
     assert st.cpu().tolist() == [2] * 6
+
+
+@pytest.mark.parametrize("kernels", ["specialized", "interpreted"])
+def test_compare_pairs_viewed_with_different_merged_dims(B, kernels, monkeypatch):
+    """Pairs where one graph reads a leaf through merged dims (a reshape)
+    and the other does not: compared over the joined view, both orders,
+    against the oracle."""
+    monkeypatch.setenv("DIRIGO_JIT", "1" if kernels == "specialized" else "0")
+    for name, a, b in tiny_graphs.merged_view_pairs():
+        n = oracle.Graph(a).output_numel
+        want = oracle.compare(oracle.Graph(a), oracle.Graph(b), range(n))
+        for x, y in ((a, b), (b, a)):
+            st, mism = B.compare_locations(B.dg_graph_parse(x), B.dg_graph_parse(y), list(range(n)))
+            assert np.array_equal(st.cpu().numpy(), want), name
+            assert np.array_equal(mism.cpu().numpy(), np.nonzero(want)[0]), name
 
 
 def test_edge_cases(B):

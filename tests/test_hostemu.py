@@ -15,7 +15,7 @@ import tiny_graphs
 from paper_2609_19611_amd import workloads as W
 
 CAT = tiny_graphs.catalogue()
-SEPARABLE = sorted(set(CAT) - tiny_graphs.NONSEPARABLE)
+SEPARABLE = sorted(CAT)
 
 
 def assert_same(a, b):
@@ -31,11 +31,24 @@ def test_catalogue_matches_oracle(name):
     assert_same(hostemu.enumerate(text, locs), g.enumerate(locs))
 
 
-@pytest.mark.parametrize("name", sorted(tiny_graphs.NONSEPARABLE))
-def test_nonseparable_rejected(name):
+def test_unrefinable_reshape_rejected():
+    """A reshape between two factorisations of one block with no common
+    refinement is refused (the oracle takes it)."""
     with pytest.raises(hostemu.HostEmuError) as e:
-        hostemu.enumerate(CAT[name][0], [0])
+        hostemu.enumerate(tiny_graphs.UNREFINABLE_RESHAPE, [0])
     assert e.value.code == -4
+    assert oracle.Graph(tiny_graphs.UNREFINABLE_RESHAPE).output_numel == 24
+
+
+@pytest.mark.parametrize("name,a,b", tiny_graphs.merged_view_pairs())
+def test_compare_pairs_viewed_with_different_merged_dims(name, a, b):
+    """Graphs over the same leaves, one reading a leaf through merged dims:
+    the comparison views both over the joined dims, against the oracle."""
+    n = oracle.Graph(a).output_numel
+    want = oracle.compare(oracle.Graph(a), oracle.Graph(b), range(n))
+    assert np.array_equal(hostemu.compare(a, b, range(n)), want)
+    assert np.array_equal(hostemu.compare(b, a, range(n)), want)
+    assert set(want.tolist()) == {{"same_footprint": 0, "sliced": 1}.get(name, 2)}
 
 
 @pytest.mark.parametrize("name", ["c1", "c2", "c3", "c4", "c5"])
@@ -104,7 +117,7 @@ def test_range_and_overflow_errors():
 
 # ---- expression DAGs (the library's DAG block code on one host thread) ----
 _CAT = tiny_graphs.catalogue()
-_SEP = sorted(set(_CAT) - tiny_graphs.NONSEPARABLE)
+_SEP = sorted(_CAT)
 
 
 def _dag_equal(a, b):

@@ -153,7 +153,7 @@ def _pairs():
              ("c5", W.c5_reference_text(n=1, c=4, hw=5, co=3), W.c5_variant_text(n=1, c=4, hw=5, co=3)),
              ("same_c4", W.c4_text(), W.c4_text()), ("same_c2", W.c2_text(), W.c2_text())]
     cat = tiny_graphs.catalogue()
-    for name in sorted(set(cat) - tiny_graphs.NONSEPARABLE)[:10]:
+    for name in sorted(cat)[:10]:
         pairs.append(("cat_" + name, cat[name][0], cat[name][0]))
     return pairs
 

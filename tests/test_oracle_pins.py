@@ -51,6 +51,8 @@ INVARIANT = {
     # softmax is shift invariant along its dim, and the bias adds the same
     # mean(b) to every element of a softmax row.
     "c3_small": ("b", "softmax shift invariance"),
+    # each softmax row is one channel's flattened map: b[c] shifts the whole row.
+    "conv_flatten_softmax": ("b", "softmax shift invariance"),
     # min(max(x, z), x) == x.
     "select_absorb": ("z", "select absorbed"),
 }

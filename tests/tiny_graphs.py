@@ -19,11 +19,19 @@ def _g(leaves, ops, out, shape):
     return g.text()
 
 
-# Graphs whose dataflow the separable plan cannot express: a grouped
-# transposed convolution (its weight's first two dims are both fed by the
-# output channel) and a reshape that merges dims.  The oracle handles them;
-# the library rejects them with DG_E_UNSUPPORTED_OP.
-NONSEPARABLE = {"convT1d_groups", "views"}
+# Graphs whose reads couple two dims of one operand (a grouped transposed
+# convolution feeds its weight's first two dims from the output channel; a
+# reshape that merges dims feeds them from one coordinate): the library
+# compiles them over merged dims.  MERGED_DIMS lists the catalogue's such
+# graphs.
+MERGED_DIMS = {"convT1d_groups", "views", "convT2d_groups", "convT3d_groups", "conv_flatten_softmax",
+               "reshape_split_merge", "reshape_refine", "unflatten_linear"}
+
+# A reshape between two factorisations of one block of dims with no common
+# refinement ([2,3,4] -> [4,3,2]: 4 does not divide 6): the library refuses
+# it (DG_E_UNSUPPORTED_OP); the oracle takes it.
+UNREFINABLE_RESHAPE = ("dgir 1\nleaf x 2,3,4\nleaf z 4,3,2\nop r reshape x ; shape=4,3,2\n"
+                       "op y mul r z\noutput y 4,3,2\n")
 
 
 def catalogue():
@@ -110,6 +118,42 @@ def catalogue():
                       ("d", "expand", ["z"], dict(shape=[2, 4, 3])),
                       ("y", "add", ["c", "d"], {})],
                      "y", [2, 4, 3]), False)
+    G["convT2d_groups"] = (_g([("x", [1, 6, 3, 4]), ("W", [6, 2, 3, 2]), ("b", [6])],
+                              [("y", "conv_transpose", ["x", "W", "b"],
+                                dict(stride=[2, 1], pad=[1, 0], output_padding=[1, 0], dilation=[1, 2], groups=3))],
+                              "y", [1, 6, 6, 6]), False)
+    G["convT3d_groups"] = (_g([("x", [1, 4, 2, 3, 2]), ("W", [4, 1, 2, 3, 2])],
+                              [("t", "conv_transpose", ["x", "W"],
+                                dict(stride=[2, 2, 1], pad=[0, 1, 0], output_padding=[1, 1, 0], dilation=[1, 1, 1],
+                                     groups=2)),
+                               ("y", "relu", ["t"], {})],
+                              "y", [1, 2, 5, 6, 3]), True)
+    # conv -> flatten of the spatial dims -> softmax over them: the merged
+    # output couples the conv's two spatial dims, so its input and weight
+    # are viewed with merged spatial dims too.
+    G["conv_flatten_softmax"] = (_g([("x", [1, 2, 4, 5]), ("W", [3, 2, 3, 2]), ("b", [3])],
+                                    [("t", "conv", ["x", "W", "b"],
+                                      dict(stride=[1, 2], pad=[1, 1], dilation=[1, 1], groups=1)),
+                                     ("f", "reshape", ["t"], dict(shape=[1, 3, 12])),
+                                     ("y", "softmax", ["f"], dict(dim=2))],
+                                    "y", [1, 3, 12]), False)
+    # Dims (2, 3) merged into 6 and 4 split into (2, 2) by one reshape.
+    G["reshape_split_merge"] = (_g([("x", [2, 3, 4]), ("s", [6, 1, 2])],
+                                   [("e", "exp", ["x"], {}),
+                                    ("r", "reshape", ["e"], dict(shape=[6, 2, 2])),
+                                    ("m", "mul", ["r", "s"], {}),
+                                    ("y", "sum", ["m"], dict(dims=[1], keepdim=0))],
+                                   "y", [6, 2]), False)
+    # [6, 4] -> [3, 8]: both sides have two dims; strides 1 | 4 | 8 | 24 refine both.
+    G["reshape_refine"] = (_g([("x", [6, 4]), ("z", [3, 1])],
+                              [("r", "reshape", ["x"], dict(shape=[3, 8])), ("y", "add", ["r", "z"], {})],
+                              "y", [3, 8]), False)
+    G["unflatten_linear"] = (_g([("x", [2, 5]), ("W", [12, 5]), ("b", [12])],
+                                [("h", "linear", ["x", "W", "b"], {}),
+                                 ("u", "reshape", ["h"], dict(shape=[2, 3, 4])),
+                                 ("p", "permute", ["u"], dict(dims=[0, 2, 1])),
+                                 ("y", "layer_norm", ["p"], dict(ndims=1))],
+                                "y", [2, 4, 3]), False)
     G["convT1d"] = (_g([("x", [2, 3, 5]), ("W", [3, 2, 4]), ("b", [2])],
                        [("y", "conv_transpose", ["x", "W", "b"],
                          dict(stride=[3], pad=[2], output_padding=[1], dilation=[1], groups=1))],
@@ -233,3 +277,25 @@ OVERFLOWING_SHAPES = [
     "dgir 1\nleaf a 2147483647,1,1\nleaf b 1,2147483647,2147483647\nop y add a b\n"
     "output y 2147483647,2147483647,2147483647\n",
 ]
+
+
+def merged_view_pairs():
+    """Pairs over the same leaves where one graph reads a leaf through
+    merged dims and the other does not (the comparison then views both
+    over the joined dims): (name, text a, text b)."""
+    A = _g([("x", [2, 3]), ("v", [4, 3])],
+           [("a", "sum", ["x"], dict(dims=[0, 1], keepdim=0)), ("b", "sum", ["v"], dict(dims=[0], keepdim=0)),
+            ("y", "mul", ["a", "b"], {})], "y", [3])
+    B = _g([("x", [2, 3]), ("v", [4, 3])],
+           [("f", "reshape", ["x"], dict(shape=[6])), ("a", "sum", ["f"], dict(dims=[0], keepdim=1)),
+            ("b", "sum", ["v"], dict(dims=[0], keepdim=0)), ("y", "mul", ["a", "b"], {})], "y", [3])
+    C = _g([("x", [2, 3]), ("v", [4, 3])],
+           [("f", "reshape", ["x"], dict(shape=[6])), ("s", "slice", ["f"], dict(dim=0, start=1, end=6, step=1)),
+            ("a", "sum", ["s"], dict(dims=[0], keepdim=1)), ("b", "sum", ["v"], dict(dims=[0], keepdim=0)),
+            ("y", "mul", ["a", "b"], {})], "y", [3])
+    D = _g([("x", [2, 3]), ("v", [4, 3])],
+           [("f", "reshape", ["x"], dict(shape=[6])), ("a", "sum", ["f"], dict(dims=[0], keepdim=1)),
+            ("g", "reshape", ["v"], dict(shape=[2, 6])), ("h", "sum", ["g"], dict(dims=[0], keepdim=0)),
+            ("k", "reshape", ["h"], dict(shape=[2, 3])), ("k2", "mul", ["k", "k"], {}),
+            ("b", "sum", ["k2"], dict(dims=[0], keepdim=0)), ("y", "mul", ["a", "b"], {})], "y", [3])
+    return [("same_footprint", A, B), ("sliced", A, C), ("both_merge", B, D), ("counts", A, D)]
