@@ -271,6 +271,27 @@ dg_status dg_enumerate_fill(const dg_graph* g, const int64_t* d_locs, int64_t n,
 dg_status dg_enumerate(const dg_graph* g, const int64_t* d_locs, int64_t n, int64_t* d_offsets, uint32_t* d_ids,
                        uint32_t* d_counts, int64_t capacity, void* d_ws, int64_t* h_total, void* stream);
 
+/* dg_enumerate_noalloc: dg_enumerate for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Takes no workspace and allocates and
+ * loads nothing: its workspace is a library-owned device array of about
+ * 16 MiB, one per GPU the library runs on, held until the process ends.
+ *  - n <= DG_NOALLOC_MAX_LOCATIONS, else DG_E_WORKSPACE.
+ *  - The graph must already be resident on the current device: its plan
+ *    copied there and, with specialisation on, its kernels loaded, which
+ *    any earlier enumeration call with the graph on that device does (for
+ *    example dg_enumerate with n = 0 or a few locations); else
+ *    DG_E_INVALID_ARG.
+ *  - Every call on one GPU shares that GPU's array: calls that overlap in
+ *    time on one GPU (from several host threads or streams) race and must
+ *    not be made.  Each call clears what it needs first, so one call's
+ *    leftovers never affect the next.
+ * Arguments, results and errors otherwise as dg_enumerate; synchronous. */
+#define DG_NOALLOC_MAX_LOCATIONS 2097152
+dg_status dg_enumerate_noalloc(const dg_graph* g, const int64_t* d_locs, int64_t n, int64_t* d_offsets,
+                               uint32_t* d_ids, uint32_t* d_counts, int64_t capacity, int64_t* h_total,
+                               void* stream);
+
 /* dg_enumerate_wide: dg_enumerate with 64-bit ids and path counts, for
  * graphs whose leaves hold 2^32 elements or more (global ids up to 2^62)
  * or whose path counts reach 2^32 (the static bound is below 2^63, so

@@ -114,6 +114,7 @@ def _load():
         "dg_compare_range": ([P, P, i64, i64, i64, P, P, ctypes.POINTER(i64), P, P], i32),
         "dg_enumerate_stream": ([P, i64, i64, P, sz, i64, CHUNK_FN, P, P, P], i32),
         "dg_enumerate_wide": ([P, P, i64, P, P, P, i64, P, ctypes.POINTER(i64), P], i32),
+        "dg_enumerate_noalloc": ([P, P, i64, P, P, P, i64, ctypes.POINTER(i64), P], i32),
         "dg_graph_tensor": ([P, i32, P], i32),
         "dg_dag_sizes": ([P, P, i64, P, P, P, ctypes.POINTER(i64), ctypes.POINTER(i64), P], i32),
         "dg_dag_fill": ([P, P, i64, P, P, P, P, P, P, P, P], i32),
@@ -282,6 +283,29 @@ def dg_enumerate(g: Graph, d_locs: torch.Tensor, d_offsets: torch.Tensor, d_ids:
     total = ctypes.c_int64()
     _check(_lib.dg_enumerate(g.handle, _ptr(d_locs), n, _ptr(d_offsets), _ptr(d_ids), _ptr(d_counts), cap,
                              _ptr(d_ws), ctypes.byref(total), _stream(stream)))
+    return total.value
+
+
+NOALLOC_MAX_LOCATIONS = 2097152
+
+
+def dg_enumerate_noalloc(g: Graph, d_locs: torch.Tensor, d_offsets: torch.Tensor, d_ids: torch.Tensor,
+                         d_counts: torch.Tensor, stream=None) -> int:
+    """dg_enumerate with the library's own device scratch instead of a
+    workspace (no allocation; the graph must be resident on the device from
+    an earlier enumeration call).  Returns the total."""
+    n = d_locs.numel()
+    _dev_i64(d_locs, "locations")
+    _dev_i64(d_offsets, "offsets")
+    if d_offsets.numel() < n + 1:
+        raise ValueError("offsets needs n + 1 entries")
+    cap = min(d_ids.numel(), d_counts.numel())
+    for t, what in ((d_ids, "ids"), (d_counts, "counts")):
+        if not t.is_cuda or t.dtype not in (torch.int32, torch.uint32) or not t.is_contiguous():
+            raise ValueError(f"{what} must be a contiguous 32-bit device tensor")
+    total = ctypes.c_int64()
+    _check(_lib.dg_enumerate_noalloc(g.handle, _ptr(d_locs), n, _ptr(d_offsets), _ptr(d_ids), _ptr(d_counts), cap,
+                                     ctypes.byref(total), _stream(stream)))
     return total.value
 
 

@@ -229,6 +229,32 @@ const dg::JitModule* graph_jit_wide(const dg_graph* cg) {
 // Leaf ids of g fit 32 bits.
 bool narrow_ids(const dg_graph* g) { return g->ir.leaf_total <= 0xFFFFFFFFull; }
 
+// What an allocation-free call may use on the current device: the plan's
+// device copy and the specialised kernels, only if an earlier call put them
+// there (DG_E_INVALID_ARG otherwise).  *jm is null when specialisation is
+// off or failed (the precompiled kernels then run the plan).
+dg_status resident(const dg_graph* cg, bool wide, const uint8_t** blob, const dg::JitModule** jm) {
+  dg_graph* g = const_cast<dg_graph*>(cg);
+  int dev = 0;
+  DG_HIP(hipGetDevice(&dev), "hipGetDevice");
+  std::lock_guard<std::mutex> lock(g->mu);
+  auto b = g->dev_blob.find(dev);
+  if (b == g->dev_blob.end())
+    return set_error(DG_E_INVALID_ARG, "the graph is not resident on this device: make one ordinary enumeration "
+                                       "call with it on this device first");
+  *blob = b->second;
+  *jm = nullptr;
+  if (dg::jit_enabled()) {
+    auto& tab = wide ? g->jit_wide : g->jit;
+    auto k = tab.find(dev);
+    if (k == tab.end() || !k->second.tried)
+      return set_error(DG_E_INVALID_ARG, "the graph's kernels are not loaded on this device: make one ordinary "
+                                         "enumeration call with it on this device first");
+    if (k->second.ok) *jm = &k->second.jm;
+  }
+  return DG_OK;
+}
+
 // One block per location, in launches of at most kGridLimit / block blocks
 // (a grid holds fewer than 2^32 work-items per dimension).  launch(first,
 // m) launches blocks for locations first .. first + m - 1.
@@ -557,9 +583,12 @@ namespace {
 
 // Single pass over the locations of `src` (a list or a flat range), with
 // 32-bit (Word = uint32_t) or 64-bit ids and counts.
+// With `no_alloc`, only what resident() allows is used: the call allocates
+// nothing and loads nothing.
 extern "C++" template <class Word>
 dg_status enumerate_impl(const dg_graph* g, dgc::LocSrc src, int64_t n, int64_t* d_offsets, Word* d_ids,
-                         Word* d_counts, int64_t capacity, void* d_ws, int64_t* h_total, void* stream) {
+                         Word* d_counts, int64_t capacity, void* d_ws, int64_t* h_total, void* stream,
+                         bool no_alloc = false) {
   constexpr bool wide = sizeof(Word) == 8;
   if (!d_ws) return set_error(DG_E_WORKSPACE, "workspace is required");
   if (!wide && !narrow_ids(g))
@@ -575,9 +604,15 @@ dg_status enumerate_impl(const dg_graph* g, dgc::LocSrc src, int64_t n, int64_t*
     return DG_OK;
   }
   const uint8_t* blob = nullptr;
-  dg_status st = device_blob(g, &blob);
-  if (st != DG_OK) return st;
-  const dg::JitModule* jm = wide ? graph_jit_wide(g) : graph_jit(g);
+  const dg::JitModule* jm = nullptr;
+  if (no_alloc) {
+    dg_status st = resident(g, wide, &blob, &jm);
+    if (st != DG_OK) return st;
+  } else {
+    dg_status st = device_blob(g, &blob);
+    if (st != DG_OK) return st;
+    jm = wide ? graph_jit_wide(g) : graph_jit(g);
+  }
   WsLayout w = ws_layout(n);
   uint8_t* ws = static_cast<uint8_t*>(d_ws);
   uint32_t* err = reinterpret_cast<uint32_t*>(ws + w.err);
@@ -614,6 +649,26 @@ dg_status enumerate_impl(const dg_graph* g, dgc::LocSrc src, int64_t n, int64_t*
   return device_errors(bits);
 }
 
+}  // namespace
+
+extern "C++" {
+namespace dg_internal {
+
+dg_status fail(dg_status code, const std::string& msg) { return set_error(code, msg); }
+
+size_t workspace_bytes(int64_t n) { return ws_layout(n).total; }
+
+dg_status enumerate_resident(const dg_graph* g, const int64_t* d_locs, int64_t n, int64_t* d_offsets,
+                             uint32_t* d_ids, uint32_t* d_counts, int64_t capacity, void* d_ws, int64_t* h_total,
+                             void* stream) {
+  return enumerate_impl(g, dgc::LocSrc{d_locs, 0}, n, d_offsets, d_ids, d_counts, capacity, d_ws, h_total, stream,
+                        true);
+}
+
+}  // namespace dg_internal
+}  // extern "C++"
+
+namespace {
 
 // Whether [first, first + n) lies inside the output of g.
 bool range_ok(const dg_graph* g, int64_t first, int64_t n) {

@@ -17,7 +17,7 @@ CAT = tiny_graphs.catalogue()
 
 def test_library_exports_every_header_symbol():
     names = B.header_symbols()
-    assert len(names) == 23
+    assert len(names) == 24
     lib = ctypes.CDLL(B.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
