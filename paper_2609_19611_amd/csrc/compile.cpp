@@ -622,7 +622,13 @@ class Compiler {
       const IndexFn& f = gd.first;
       if (fn_magnitude(f, vmin, vmax) >= (int64_t(1) << 30))
         fail(DG_E_UNSUPPORTED_OP, op.kind + ": index arithmetic exceeds 32 bits");
-      if (f.terms.empty()) continue;
+      if (f.terms.empty()) {
+        int64_t v = f.c;
+        if (f.mode == 1 && floor_div(v, f.s) * f.s != v) return;
+        if (f.mode) v = floor_div(v, f.s);
+        if (v < 0 || v >= gd.second) return;  // a merged dim's constant index out of range: nothing is read
+        continue;
+      }
       auto rg = fn_range(f, vmin, vmax);
       bool trivial = (f.mode != 1 || f.s == 1) && rg.first >= 0 && rg.second <= gd.second - 1;
       if (!trivial) {

@@ -374,17 +374,20 @@ DGC uint64_t ap_setup(const DagCtx& x, const DgdGroup& G, int R, const Slots& S,
   for (int q = 0; q < Q; ++q) {
     const int32_t lo = (int32_t)S.first(j, q), hi = (int32_t)S.len(j, q), m = G.step[q];
     int32_t first = lo;
-    if (m > 1) {
+    if (G.mpair[q] >= 0) {
       // The exact division c0 + k w = 0 (mod s): g = s / step must divide
-      // c0, then w = (-c0 / g) * inverse(k / g) (mod step).
+      // c0 (also when the step is 1, i.e. s divides k: then no w helps an
+      // indivisible c0), then w = (-c0 / g) * inverse(k / g) (mod step).
       const DgdPair pr = G.pair[G.mpair[q]];
       const DgpIFn& f = x.Ps[G.op0 + pr.a].idx[pr.d];
       int32_t c0, k;
       ifn_linear(f, R + q, x.vt, x.nt, &c0, &k);
       const int32_t g = f.s / m;
       if (c0 % g != 0) return 0;
-      const int32_t r = (int32_t)(((int64_t)pmod(-(c0 / g), m) * G.minv[q]) % m);
-      first = lo + pmod(r - lo, m);
+      if (m > 1) {
+        const int32_t r = (int32_t)(((int64_t)pmod(-(c0 / g), m) * G.minv[q]) % m);
+        first = lo + pmod(r - lo, m);
+      }
     }
     const uint32_t len = first <= hi ? (uint32_t)((hi - first) / m + 1) : 0u;
     S.first(j, q) = (uint32_t)first;

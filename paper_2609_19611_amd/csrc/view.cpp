@@ -89,6 +89,23 @@ std::pair<int64_t, int64_t> fn_range(const IndexFn& f, const std::vector<int64_t
   return {lo, hi};
 }
 
+// Range of a division-free index function over the merged output
+// coordinates [0, size) and the group's window boxes.
+std::pair<int64_t, int64_t> var_range(const IndexFn& f, const std::vector<int64_t>& oc_size, const ReadGroup& G) {
+  const int Rc = (int)oc_size.size();
+  std::vector<int64_t> vmin, vmax;
+  for (int64_t n : oc_size) {
+    vmin.push_back(0);
+    vmax.push_back(n - 1);
+  }
+  for (size_t b = 0; b < G.wlo.size(); ++b) {
+    vmin.push_back(G.wlo[b]);
+    vmax.push_back(G.whi[b] - 1);
+  }
+  (void)Rc;
+  return fn_range(f, vmin, vmax);
+}
+
 // The graph over partition P.
 GraphIR build(const GraphIR& g, const DimPartition& P) {
   GraphIR c = g;
@@ -134,6 +151,10 @@ GraphIR build(const GraphIR& g, const DimPartition& P) {
           if (a != ga) r.terms.push_back({m, -t.coef * sa, st * sa});
         } else if (a == ga) {
           r.terms.push_back({m, t.coef, st * t.vdiv});
+        } else if (sa % t.vdiv == 0) {
+          // floor((floor(m / st) mod sa) / q) = floor(m / (st q)) mod (sa / q)
+          r.terms.push_back({m, t.coef, st * t.vdiv});
+          r.terms.push_back({m, -t.coef * (sa / t.vdiv), st * sa});
         } else {
           fail(op.kind + ": a merged output coordinate is divided inside its group");
         }
@@ -141,12 +162,19 @@ GraphIR build(const GraphIR& g, const DimPartition& P) {
       return combined(r);
     };
     OpNode& cop = c.ops[k];
+    std::vector<int64_t> oc_size;  // extent of each merged output coordinate
+    for (auto& gr : og) {
+      int64_t n = 1;
+      for (int d = gr.first; d < gr.second; ++d) n *= oshape[d];
+      oc_size.push_back(n);
+    }
     for (size_t gi = 0; gi < op.groups.size(); ++gi) {
       const ReadGroup& G = op.groups[gi];
       ReadGroup& CG = cop.groups[gi];
       CG.guards.clear();
       auto add_guard = [&](const IndexFn& f, int64_t size) {
-        if (f.terms.empty()) return;
+        // (A constant guard is kept too: out of range, it makes the group
+        // read nothing.)
         for (const auto& e : CG.guards)
           if (e.second == size && same_fn(e.first, f)) return;
         CG.guards.push_back({f, size});
@@ -167,8 +195,30 @@ GraphIR build(const GraphIR& g, const DimPartition& P) {
           IndexFn m;
           int64_t w = 1;
           for (int d = gr.second - 1; d >= gr.first; --d) {
-            const IndexFn& f = sf[d];
-            if (f.mode != 0) fail(op.kind + ": dims of an operand read through a division must stay separate");
+            IndexFn f = sf[d];
+            if (f.mode != 0 && !f.terms.empty()) {
+              // An index (e)/s or (e)//s inside a merged dim: its quotient
+              // becomes a window variable q of the group, pinned by the
+              // guard e - s q in [0, 1) (exact) or [0, s) (floor).
+              IndexFn inner = f;
+              inner.mode = 0;
+              inner.s = 1;
+              auto rg = var_range(inner, oc_size, CG);
+              const int q = Rc + (int)CG.wlo.size();
+              CG.wlo.push_back(floor_div(rg.first, f.s));
+              CG.whi.push_back(floor_div(rg.second, f.s) + 1);
+              inner.terms.push_back({q, -f.s, 1});
+              add_guard(inner, f.mode == 1 ? 1 : f.s);
+              f = IndexFn::var(q);
+            } else if (f.mode != 0) {
+              // A constant: evaluate the division here.
+              const int64_t v = f.c;
+              if (f.mode == 1 && floor_div(v, f.s) * f.s != v) {
+                f = IndexFn::constant(-1);  // not divisible: reads nothing
+              } else {
+                f = IndexFn::constant(floor_div(v, f.s));
+              }
+            }
             for (const auto& t : f.terms) m.terms.push_back({t.var, t.coef * w, t.vdiv});
             m.c += f.c * w;
             add_guard(f, us[d]);

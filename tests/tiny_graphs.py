@@ -226,6 +226,13 @@ def dag_catalogue():
                               [("y", "affine_gather", ["x", "w"],
                                 dict(shape=[5], window=[1100], idx0=["(o0+w0)/2"], idx1=["w0"], mult=[1, 3]))],
                               "y", [5])
+    # Stride and dilation both 2: the tap coefficient shares the divisor, so
+    # every tap or none reaches an output element (the exact division's
+    # progression has step 1 and a divisibility condition of its own).
+    G["convT_stride_dilation"] = _g([("x", [1, 2, 4]), ("W", [2, 2, 3])],
+                                    [("y", "conv_transpose", ["x", "W"],
+                                      dict(stride=[2], pad=[1], output_padding=[0], dilation=[2], groups=1))],
+                                    "y", [1, 2, 9])
     G["gather_shift"] = _g([("x", [2, 5]), ("z", [2, 5])],
                            [("t", "exp", ["x"], {}),
                             ("y", "affine_gather", ["t", "z"],
