@@ -42,6 +42,8 @@ def parse_args():
     p.add_argument("--workload", default="c4", choices=["c1", "c2", "c3", "c4", "c5"])
     p.add_argument("--cpu-seconds", type=float, default=15.0, help="target length of the oracle sample")
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--no-secondary", action="store_true",
+                   help="skip the c3 enumeration and c5 comparison figures added to the default c4 line")
     p.add_argument("--two-pass", action="store_true",
                    help="time dg_enumerate_sizes + dg_enumerate_fill instead of the single-pass dg_enumerate")
     p.add_argument("--wide", action="store_true",
@@ -126,6 +128,76 @@ def measured_traffic(workload, path=TRAFFIC_FILE, sources=KERNEL_SOURCES):
         if len(parts) == 3 and parts[0] == "traffic_bytes_per_launch" and parts[1] == workload:
             traffic = int(parts[2])
     return traffic if stored == h.hexdigest() else None
+
+
+def _median_ms(fn, steps, warmup, stream):
+    """Median of `steps` timed calls of fn (HIP events on `stream`)."""
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    for a, b in ev:
+        a.record(stream)
+        fn()
+        b.record(stream)
+    torch.cuda.synchronize()
+    return float(np.median([a.elapsed_time(b) for a, b in ev]))
+
+
+def secondary_enumeration(B, W, name, fill_gbps, steps=10, warmup=3):
+    """Single-pass enumeration of another workload: median call time of
+    `steps` calls, rates and the HBM fraction (algorithmic bytes)."""
+    import torch
+    stream = torch.cuda.current_stream()
+    g = B.dg_graph_parse(W.CONFIGS[name]["text"]())
+    locs = W.config_locations(name)
+    d_locs = torch.as_tensor(locs, dtype=torch.int64, device="cuda")
+    n = len(locs)
+    ws = B.workspace(g, n)
+    off = torch.empty(n + 1, dtype=torch.int64, device="cuda")
+    total = B.dg_enumerate_sizes(g, d_locs, off, ws)
+    ids = torch.empty(total, dtype=torch.int32, device="cuda")
+    cnt = torch.empty(total, dtype=torch.int32, device="cuda")
+    ms = _median_ms(lambda: B.dg_enumerate(g, d_locs, off, ids, cnt, ws), steps, warmup, stream)
+    alg = 16 * n + 8 * total
+    gbps = alg / (ms * 1e-3) / 1e9
+    del ids, cnt
+    torch.cuda.empty_cache()
+    return {"workload": f"{name}: " + W.CONFIGS[name]["desc"], "locations": n, "entries": total,
+            "ms_per_call": ms, "statistic": f"median of {steps} calls (dg_enumerate, whole call)",
+            "entries_per_s": total / (ms * 1e-3), "locations_per_s": n / (ms * 1e-3),
+            "achieved_GBps": gbps, "frac_of_hbm_peak": gbps / HBM_PEAK_GBS, "frac_of_measured_fill": gbps / fill_gbps}
+
+
+def secondary_compare(B, W, steps=5, warmup=2):
+    """The pair check: the clean split-K variant alone (median of 10 calls)
+    and the step of 17 comparisons (clean + 16 faults; median of `steps`)."""
+    import concurrent.futures as cf
+    import torch
+    stream = torch.cuda.current_stream()
+    ref = B.dg_graph_parse(W.c5_reference_text())
+    variants = [B.dg_graph_parse(W.c5_variant_text())] + [B.dg_graph_parse(W.c5_variant_text(fault=f))
+                                                          for f in W.c5_faults()]
+    locs = W.config_locations("c5")
+    d_locs = torch.as_tensor(locs, dtype=torch.int64, device="cuda")
+    n = len(locs)
+
+    def load(v):  # compiles the pair's specialised kernel (one location, own buffers)
+        B.compare_locations(ref, v, locs[:1])
+    with cf.ThreadPoolExecutor(8) as ex:
+        list(ex.map(load, variants))
+    torch.cuda.synchronize()
+    ws = B.workspace(ref, n)
+    status = torch.empty(n, dtype=torch.uint8, device="cuda")
+    mism = torch.empty(n, dtype=torch.int64, device="cuda")
+    clean = _median_ms(lambda: B.dg_compare(ref, variants[0], d_locs, status, mism, ws), 10, 2, stream)
+    step = _median_ms(lambda: [B.dg_compare(ref, v, d_locs, status, mism, ws) for v in variants], steps, warmup,
+                      stream)
+    return {"workload": "c5: " + W.CONFIGS["c5"]["desc"], "locations": n,
+            "clean_ms_per_compare": clean, "clean_locations_per_s": n / (clean * 1e-3),
+            "step_ms_17_compares": step, "locations_per_s_17_compares": 17 * n / (step * 1e-3),
+            "statistic": "median of 10 calls (clean) and of %d steps (17 compares)" % steps}
 
 
 def git_sha():
@@ -629,7 +701,8 @@ def main():
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     assert t == total
-    kern_ms = float(np.mean([a.elapsed_time(b) for a, b in kern_ev]))
+    kern_times = [a.elapsed_time(b) for a, b in kern_ev]
+    kern_ms = float(np.median(kern_times))
     ms = elapsed * 1000 / args.steps
     # Algorithmic bytes per location: 8 (location) + 8 (offset) + 8 per entry
     # (uint32 id + uint32 count; 16 with 64-bit ids and counts).
@@ -650,7 +723,8 @@ def main():
                      "frac": achieved / HBM_PEAK_GBS,
                      "traffic": measured_traffic(args.workload) if kernel == "dg_enumerate" else None,
                      "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE x2 + WRITE_SIZE x1)",
-                     "kernel_ms": kern_ms, "algorithmic_bytes": alg_bytes},
+                     "kernel_ms": kern_ms, "kernel_ms_mean": float(np.mean(kern_times)),
+                     "kernel_ms_statistic": f"median of {args.steps} launches", "algorithmic_bytes": alg_bytes},
     }
     # The bandwidth plain torch kernels reach on this machine (after the timed
     # region), beside the spec peak.
@@ -659,6 +733,11 @@ def main():
     line["roofline"]["measured_fill_GBps"] = rates["fill_GBps_write"]
     line["roofline"]["measured_copy_GBps"] = rates["copy_GBps_read_plus_write"]
     line["roofline"]["frac_of_measured_fill"] = achieved / rates["fill_GBps_write"]
+    if args.workload == "c4" and not (args.two_pass or args.wide) and not args.no_secondary:
+        # The other two headline figures, timed after the main one: the
+        # conv-transpose + softmax enumeration and the pair check.
+        line["secondary"] = {"c3": secondary_enumeration(B, W, "c3", rates["fill_GBps_write"]),
+                             "c5": secondary_compare(B, W)}
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(args.workload, text, None, locs, args.cpu_seconds)
     line["git"] = git_sha()

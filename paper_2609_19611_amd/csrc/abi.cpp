@@ -7,6 +7,7 @@
 #include <vector>
 #include <cstring>
 #include <map>
+#include <memory>
 #include <cstdlib>
 #include <mutex>
 #include <new>
@@ -55,8 +56,13 @@ thread_local std::string g_last_error;
 
 // Specialised comparison kernels of graph pairs: (serial of a, serial of b,
 // device, block) -> kernels.  Released when either graph is destroyed.
+// Each entry has its own lock, so that different pairs compile at once.
+struct PairKernels {
+  std::mutex mu;
+  DevKernels k;
+};
 std::mutex g_pair_mu;
-std::map<std::tuple<uint64_t, uint64_t, int, int>, DevKernels> g_pair_jit;
+std::map<std::tuple<uint64_t, uint64_t, int, int>, std::shared_ptr<PairKernels>> g_pair_jit;
 
 // Plans of a pair whose graphs view some leaf with different merged dims
 // (each graph's own plan is then not comparable with the other's): both
@@ -202,8 +208,15 @@ const dg::JitModule* pair_jit(const dg_graph* ca, const dg_graph* b, const dg::P
   if (!dg::jit_enabled()) return nullptr;
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return nullptr;
-  std::lock_guard<std::mutex> lock(g_pair_mu);
-  DevKernels& k = g_pair_jit[std::make_tuple(ca->serial, b->serial, dev, block)];
+  std::shared_ptr<PairKernels> e;
+  {
+    std::lock_guard<std::mutex> lock(g_pair_mu);
+    auto& slot = g_pair_jit[std::make_tuple(ca->serial, b->serial, dev, block)];
+    if (!slot) slot = std::make_shared<PairKernels>();
+    e = slot;
+  }
+  std::lock_guard<std::mutex> lock(e->mu);
+  DevKernels& k = e->k;
   if (!k.tried) {
     k.tried = true;
     k.ok = dg::jit_load(dg::jit_compare_source(plan_a, plan_b, pp, block), &k.jm, &k.log) && k.jm.compare;
@@ -404,7 +417,11 @@ void dg_graph_destroy(dg_graph* g) {
     std::lock_guard<std::mutex> lock(g_pair_mu);
     for (auto it = g_pair_jit.begin(); it != g_pair_jit.end();) {
       if (std::get<0>(it->first) == g->serial || std::get<1>(it->first) == g->serial) {
-        dg::jit_release(&it->second.jm);
+        std::shared_ptr<PairKernels> e = it->second;  // outlives the erase below
+        {
+          std::lock_guard<std::mutex> el(e->mu);
+          dg::jit_release(&e->k.jm);
+        }
         it = g_pair_jit.erase(it);
       } else {
         ++it;

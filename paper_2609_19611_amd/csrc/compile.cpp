@@ -171,6 +171,103 @@ int64_t hull_bound(const std::vector<const FactorPos*>& ps) {
   return floor_frac(hi - lo) + 1;
 }
 
+// Canonical forms of factors that are the same at every location whenever
+// their forms are equal (two such factors then share one slot, and terms
+// that differ only in such factors merge).  Two kinds:
+//  - kind 0, a pattern placed at the location: value(x) = coef[x - anchor]
+//    for x in [0, size), anchor = the location's coordinate `dim` (or 0 for
+//    dim = -1: location independent);
+//  - kind 1, fixed positions whose values depend on one coordinate r of the
+//    location (dim, extent `span`): value(x) = step[x](r), each a step
+//    function over [0, span) kept as (interval start, value) with adjacent
+//    values different; positions whose function is zero are dropped.
+// A kind 1 form with only constant functions is written as kind 0 with
+// dim = -1, so that equal factors always get equal forms.  `unclipped`
+// (kind 0): no offset ever leaves [0, size) wherever the anchor is, so the
+// pattern can be shifted again.
+struct CanonForm {
+  bool known = false;
+  int kind = 0;
+  int dim = -1;
+  int64_t size = 0;
+  int64_t span = 0;
+  std::map<int64_t, uint64_t> coef;
+  std::map<int64_t, std::vector<std::pair<int64_t, uint64_t>>> step;
+  bool unclipped = false;
+};
+
+std::string canon_key(const CanonForm& f) {
+  std::ostringstream k;
+  k << "CF" << f.kind << " " << f.dim << " " << f.size << " " << f.span << " " << (f.unclipped ? 1 : 0);
+  for (const auto& e : f.coef) k << " " << e.first << ":" << e.second;
+  for (const auto& e : f.step) {
+    k << " @" << e.first;
+    for (const auto& iv : e.second) k << "," << iv.first << "=" << iv.second;
+  }
+  return k.str();
+}
+
+// Step functions from per-position difference arrays (position -> (r ->
+// change of value at r)) over [0, span); fails (false) on overflow.
+bool steps_from_deltas(const std::map<int64_t, std::map<int64_t, int64_t>>& d, int64_t span,
+                       std::map<int64_t, std::vector<std::pair<int64_t, uint64_t>>>* out) {
+  out->clear();
+  for (const auto& e : d) {
+    std::vector<std::pair<int64_t, uint64_t>> fn;
+    int64_t v = 0;
+    bool nonzero = false;
+    for (const auto& c : e.second) {
+      if (c.first >= span) break;
+      if (__builtin_add_overflow(v, c.second, &v) || v < 0) return false;
+      if (c.second == 0) continue;
+      if (!fn.empty() && fn.back().first == c.first) fn.back().second = (uint64_t)v;
+      else fn.push_back({c.first, (uint64_t)v});
+    }
+    // Intervals start at 0 and adjacent values differ.
+    if (fn.empty() || fn.front().first != 0) fn.insert(fn.begin(), {0, 0});
+    std::vector<std::pair<int64_t, uint64_t>> m;
+    for (const auto& iv : fn)
+      if (m.empty() || m.back().second != iv.second) m.push_back(iv);
+    for (const auto& iv : m) nonzero = nonzero || iv.second != 0;
+    if (nonzero) (*out)[e.first] = m;
+  }
+  return true;
+}
+
+// Kind 1 forms with constant functions become kind 0 at dim -1.
+void normalise(CanonForm* f) {
+  if (!f->known || f->kind != 1) return;
+  for (const auto& e : f->step)
+    if (e.second.size() != 1) return;
+  CanonForm r;
+  r.known = true;
+  r.kind = 0;
+  r.dim = -1;
+  r.size = f->size;
+  r.unclipped = true;
+  for (const auto& e : f->step) r.coef[e.first] = e.second[0].second;
+  *f = r;
+}
+
+// A form as difference arrays over the anchor coordinate (kind 1, or a
+// location-independent kind 0 form on the given anchor).
+bool as_deltas(const CanonForm& f, std::map<int64_t, std::map<int64_t, int64_t>>* d) {
+  d->clear();
+  if (f.kind == 0) {
+    if (f.dim >= 0) return false;
+    for (const auto& e : f.coef) (*d)[e.first][0] += (int64_t)e.second;
+    return true;
+  }
+  for (const auto& e : f.step) {
+    uint64_t prev = 0;
+    for (const auto& iv : e.second) {
+      (*d)[e.first][iv.first] += (int64_t)iv.second - (int64_t)prev;
+      prev = iv.second;
+    }
+  }
+  return true;
+}
+
 class Compiler {
  public:
   explicit Compiler(const GraphIR& g) : g_(g) {}
@@ -188,6 +285,7 @@ class Compiler {
   std::vector<uint64_t> fbound_;
   std::vector<uint64_t> sbound_;
   std::map<std::string, int> memo_;
+  std::vector<CanonForm> cf_;  // per factor
   std::vector<std::vector<SymTerm>> terms_;
 
   int new_factor(int64_t cap, int64_t size, uint64_t bound) {
@@ -195,6 +293,7 @@ class Compiler {
     f.cap = (int32_t)std::max<int64_t>(1, cap);
     f.size = (int32_t)size;
     fac_.push_back(f);
+    cf_.push_back(CanonForm{});
     pos_.push_back(FactorPos{});
     unit_len_.push_back(0);
     fbound_.push_back(bound);
@@ -217,6 +316,12 @@ class Compiler {
     auto it = memo_.find(key);
     if (it != memo_.end()) return it->second;
     int f = new_factor(1, g_.tensors[g_.output].shape[a], 1);
+    cf_[f].known = true;
+    cf_[f].dim = a;
+    cf_[f].size = g_.tensors[g_.output].shape[a];
+    cf_[f].coef[0] = 1;
+    cf_[f].unclipped = true;
+    memo_[canon_key(cf_[f])] = f;
     unit_len_[f] = 1;
     pos_[f].known = true;
     pos_[f].a = {{a, Frac{1, 1}}};
@@ -232,6 +337,13 @@ class Compiler {
     auto it = memo_.find(key);
     if (it != memo_.end()) return it->second;
     int f = new_factor(1, size, 1);
+    if (v >= 0 && v < size) {
+      cf_[f].known = true;
+      cf_[f].size = size;
+      cf_[f].coef[v] = 1;
+      cf_[f].unclipped = true;
+      memo_[canon_key(cf_[f])] = f;
+    }
     unit_len_[f] = 1;
     pos_[f].known = true;
     pos_[f].lo = pos_[f].hi = frac(v);
@@ -305,6 +417,54 @@ class Compiler {
     return Coef{1, {slot}};
   }
 
+  // Canonical form of k1 f1 + k2 f2 with constant k1, k2, when both have one.
+  CanonForm lincomb_form(int f1, std::pair<int, uint64_t> s1, int f2, std::pair<int, uint64_t> s2, int64_t size) {
+    CanonForm none;
+    const CanonForm &a = cf_[f1], &b = cf_[f2];
+    if (s1.first >= 0 || s2.first >= 0 || !a.known || !b.known || a.size != size || b.size != size) return none;
+    CanonForm r;
+    r.known = true;
+    r.size = size;
+    if (a.kind == 0 && b.kind == 0 && a.dim == b.dim) {
+      r.dim = a.dim;
+      r.unclipped = a.unclipped && b.unclipped;
+      for (int q = 0; q < 2; ++q)
+        for (const auto& e : (q ? b : a).coef) {
+          uint64_t v;
+          if (__builtin_mul_overflow(e.second, q ? s2.second : s1.second, &v) ||
+              __builtin_add_overflow(r.coef[e.first], v, &r.coef[e.first]))
+            return none;
+        }
+      for (auto it = r.coef.begin(); it != r.coef.end();) it = it->second == 0 ? r.coef.erase(it) : std::next(it);
+      return r;
+    }
+    // Fixed positions over one anchor coordinate.
+    const CanonForm& anchored = a.kind == 1 ? a : b;
+    if (anchored.kind != 1) return none;
+    for (const CanonForm* f : {&a, &b})
+      if (f->kind == 1 && (f->dim != anchored.dim || f->span != anchored.span)) return none;
+    std::map<int64_t, std::map<int64_t, int64_t>> da, db, sum;
+    if (!as_deltas(a, &da) || !as_deltas(b, &db)) return none;
+    for (int q = 0; q < 2; ++q) {
+      const uint64_t k = q ? s2.second : s1.second;
+      if (k > (uint64_t)INT64_MAX) return none;
+      for (const auto& e : (q ? db : da))
+        for (const auto& c : e.second) {
+          int64_t v;
+          if (__builtin_mul_overflow(c.second, (int64_t)k, &v) ||
+              __builtin_add_overflow(sum[e.first][c.first], v, &sum[e.first][c.first]))
+            return none;
+        }
+    }
+    da.swap(sum);
+    r.kind = 1;
+    r.dim = anchored.dim;
+    r.span = anchored.span;
+    if (!steps_from_deltas(da, r.span, &r.step)) return none;
+    normalise(&r);
+    return r;
+  }
+
   int lincomb(int f1, const Coef& c1, int f2, const Coef& c2, int64_t size) {
     auto s1 = coef_slot(c1), s2 = coef_slot(c2);
     std::ostringstream key;
@@ -312,6 +472,11 @@ class Compiler {
         << " " << size;
     auto it = memo_.find(key.str());
     if (it != memo_.end()) return it->second;
+    const CanonForm cf = lincomb_form(f1, s1, f2, s2, size);
+    if (cf.known) {
+      auto hit = memo_.find(canon_key(cf));
+      if (hit != memo_.end()) return memo_[key.str()] = hit->second;
+    }
     int64_t cap = size <= kLincombFullDim ? size : std::min<int64_t>(size, (int64_t)fac_[f1].cap + fac_[f2].cap);
     const int64_t hb = hull_bound({&pos_[f1], &pos_[f2]});
     if (hb > 0) cap = std::min(cap, hb);
@@ -323,6 +488,10 @@ class Compiler {
     }
     int f = new_factor(cap, size, badd(bmul(fbound_[f1], coef_bound(c1)), bmul(fbound_[f2], coef_bound(c2))));
     pos_[f] = hp;
+    if (cf.known) {
+      cf_[f] = cf;
+      memo_[canon_key(cf)] = f;
+    }
     DgpInstr i = blank(DGP_LINCOMB);
     i.dst = f;
     i.f1 = f1;
@@ -474,6 +643,130 @@ class Compiler {
     return best;
   }
 
+  // Canonical form of a component sum into a factor, when it has one.  At
+  // most one factor variable, whose factor has an unclipped kind 0 form;
+  // every index function linear with undivided terms.  Either the target
+  // takes the factor variable with coefficient 1 and there is no predicate
+  // but the target's own validity (kind 0: the pattern shifted by every
+  // window point), or the target takes window variables only (kind 1:
+  // fixed positions, each valid for an interval of the anchor coordinate).
+  CanonForm component_form(const SymTerm& t, const std::vector<int>& vars, const std::vector<const IndexFn*>& preds,
+                           const std::vector<int64_t>& psize, const IndexFn& target, int64_t tsize, int R,
+                           const ReadGroup& G) {
+    CanonForm none;
+    auto linear = [](const IndexFn& f) {
+      if (f.mode != 0) return false;
+      for (const auto& tm : f.terms)
+        if (tm.vdiv != 1) return false;
+      return true;
+    };
+    if (!linear(target)) return none;
+    for (const IndexFn* p : preds)
+      if (!linear(*p)) return none;
+    int fvar = -1;
+    std::vector<int> wvars;
+    for (int v : vars) {
+      if (v < R) {
+        if (fvar >= 0) return none;
+        fvar = v;
+      } else {
+        wvars.push_back(v);
+      }
+    }
+    auto coef_of = [](const IndexFn& f, int v) {
+      int64_t a = 0;
+      for (const auto& tm : f.terms) a += tm.var == v ? tm.coef : 0;
+      return a;
+    };
+    for (const auto& tm : target.terms)
+      if (tm.var < R && tm.var != fvar) return none;
+    CanonForm src;
+    if (fvar >= 0) {
+      src = cf_[t.f[fvar]];
+      if (!src.known || src.kind != 0 || !src.unclipped) return none;
+    } else {
+      src.known = true;
+      src.dim = -1;
+      src.coef[0] = 1;
+    }
+    int64_t box = 1;
+    for (int v : wvars) box *= G.whi[v - R] - G.wlo[v - R];
+    if (box <= 0 || box * (int64_t)src.coef.size() > 4096) return none;
+    // Every window point, as values of wvars.
+    std::vector<std::vector<int64_t>> points{{}};
+    for (int v : wvars) {
+      std::vector<std::vector<int64_t>> next;
+      for (const auto& p0 : points)
+        for (int64_t w = G.wlo[v - R]; w < G.whi[v - R]; ++w) {
+          next.push_back(p0);
+          next.back().push_back(w);
+        }
+      points.swap(next);
+    }
+    auto window_part = [&](const IndexFn& f, const std::vector<int64_t>& pt) {
+      int64_t x = f.c;
+      for (size_t q = 0; q < wvars.size(); ++q) x += coef_of(f, wvars[q]) * pt[q];
+      return x;
+    };
+    const int64_t tf = fvar >= 0 ? coef_of(target, fvar) : 0;
+    if (fvar < 0 || tf != 0) {
+      // Kind 0 (a location-independent pattern without a factor variable).
+      if (fvar >= 0 && tf != 1) return none;
+      for (size_t p = 0; p < preds.size(); ++p)
+        if (preds[p] != &target || psize[p] != tsize) return none;
+      CanonForm r;
+      r.known = true;
+      r.dim = src.dim;
+      r.size = tsize;
+      r.unclipped = src.dim < 0;  // a location-independent pattern is clipped here
+      for (const auto& e : src.coef)
+        for (const auto& pt : points) {
+          const int64_t off = e.first + window_part(target, pt);
+          if (src.dim < 0 && (off < 0 || off >= tsize)) continue;
+          if (__builtin_add_overflow(r.coef[off], e.second, &r.coef[off])) return none;
+        }
+      for (auto it = r.coef.begin(); it != r.coef.end();) it = it->second == 0 ? r.coef.erase(it) : std::next(it);
+      return r;
+    }
+    // Kind 1: the target is fixed by the window point; each predicate
+    // bounds the anchor coordinate r (the factor variable is r + offset).
+    if (fvar < 0 || src.dim < 0) return none;
+    const int64_t span = g_.tensors[g_.output].shape[src.dim];
+    std::map<int64_t, std::map<int64_t, int64_t>> delta;
+    for (const auto& e : src.coef)
+      for (const auto& pt : points) {
+        const int64_t pos = window_part(target, pt);
+        if (pos < 0 || pos >= tsize) continue;
+        int64_t lo = 0, hi = span;  // r in [lo, hi)
+        for (size_t p = 0; p < preds.size(); ++p) {
+          const int64_t a = coef_of(*preds[p], fvar);
+          const int64_t c = window_part(*preds[p], pt) + a * e.first;  // value = a r + c
+          if (a == 0) {
+            if (c < 0 || c >= psize[p]) lo = hi;
+          } else if (a > 0) {
+            lo = std::max(lo, ceil_div(-c, a));
+            hi = std::min(hi, floor_div(psize[p] - 1 - c, a) + 1);
+          } else {
+            lo = std::max(lo, ceil_div(psize[p] - 1 - c, a));
+            hi = std::min(hi, floor_div(-c, a) + 1);
+          }
+        }
+        if (lo >= hi) continue;
+        if (__builtin_add_overflow(delta[pos][lo], (int64_t)e.second, &delta[pos][lo]) ||
+            __builtin_sub_overflow(delta[pos][hi], (int64_t)e.second, &delta[pos][hi]))
+          return none;
+      }
+    CanonForm r;
+    r.known = true;
+    r.kind = 1;
+    r.dim = src.dim;
+    r.size = tsize;
+    r.span = span;
+    if (!steps_from_deltas(delta, span, &r.step)) return none;
+    normalise(&r);
+    return r;
+  }
+
   // Sum over one component.  Returns a factor slot (target != nullptr) or a
   // scalar slot; a component of window variables without predicates and
   // without a target folds into `folded` and returns -1.
@@ -532,6 +825,11 @@ class Compiler {
     }
     auto it = memo_.find(key.str());
     if (it != memo_.end()) return it->second;
+    const CanonForm cf = target ? component_form(t, vars, preds, psize, *target, tsize, R, G) : CanonForm{};
+    if (cf.known) {
+      auto hit = memo_.find(canon_key(cf));
+      if (hit != memo_.end()) return memo_[key.str()] = hit->second;
+    }
 
     DgpInstr i = blank(DGP_COMP);
     i.nvar = (int32_t)vars.size();
@@ -571,6 +869,10 @@ class Compiler {
       }
       i.target = to_dev(*target, local, tsize);
       i.dst_is_scalar = 0;
+      if (cf.known) {
+        cf_[slot] = cf;
+        memo_[canon_key(cf)] = slot;
+      }
     } else {
       slot = new_scalar(bmul(points, weight));
       i.dst_is_scalar = 1;

@@ -1278,6 +1278,76 @@ struct PairPlan {
   LeafShape leaf[16];
 };
 
+// Compares two single-term leaves without expanding their cells.  A term is
+// coef * prod_d f_d(x_d).  When both have entries (nonzero coefficient and
+// a nonzero coordinate in every dim), their nonzero cells agree iff every
+// dim's two factors have the same nonzero coordinates; then their counts
+// agree iff every dim's two factors are proportional there and one cell
+// (the first nonzero coordinate of every dim) has the same count.  Factor
+// values and that cell's count are real counts below 2^32 (the caller
+// checks the static bounds), so the cross products fit 64 bits.
+// w: LDS scratch of 2 * DGP_MAX_RANK + 2 words.
+// Returns 0 equal, 1 nonzero sets differ, 2 counts differ.
+template <class C>
+DGC uint32_t compare_single_terms(C& c, const TermRef& A, const TermRef& B, int rank, uint8_t* area, uint64_t* w) {
+  const uint64_t* a64 = (const uint64_t*)area;
+  const int tid = c.tid(), nt = c.nthreads();
+  const uint64_t BIG = 1ull << 40;  // first nonzero coordinate x kept as the maximum of BIG - x
+  for (int i = tid; i < 2 * DGP_MAX_RANK + 2; i += nt) w[i] = 0;
+  c.sync();
+  uint64_t differ = 0;
+  DG_PLAN_UNROLL
+  for (int d = 0; d < rank; ++d) {
+    int32_t lo, hi;
+    term_hull(&A, 1, d, &lo, &hi);
+    int32_t lo2, hi2;
+    term_hull(&B, 1, d, &lo2, &hi2);
+    if (hi2 > lo2) {
+      if (hi <= lo) {
+        lo = lo2;
+        hi = hi2;
+      } else {
+        lo = lo2 < lo ? lo2 : lo;
+        hi = hi2 > hi ? hi2 : hi;
+      }
+    }
+    uint64_t fa = 0, fb = 0;
+    for (int32_t x = lo + tid; x < hi; x += nt) {  // ascending per thread: the first hit is its least
+      const uint64_t a = term_val(A, d, x, a64), b = term_val(B, d, x, a64);
+      if (a != 0 && fa == 0) fa = BIG - (uint64_t)x;
+      if (b != 0 && fb == 0) fb = BIG - (uint64_t)x;
+      differ |= (a != 0) != (b != 0) ? 1u : 0u;
+    }
+    c.reduce_max(&w[d], fa);
+    c.reduce_max(&w[DGP_MAX_RANK + d], fb);
+  }
+  c.reduce_add(&w[2 * DGP_MAX_RANK], differ);
+  c.sync();
+  bool empty_a = A.coef == 0, empty_b = B.coef == 0;
+  DG_PLAN_UNROLL
+  for (int d = 0; d < rank; ++d) {
+    empty_a = empty_a || w[d] == 0;
+    empty_b = empty_b || w[DGP_MAX_RANK + d] == 0;
+  }
+  if (empty_a || empty_b) return empty_a == empty_b ? 0u : 1u;
+  if (w[2 * DGP_MAX_RANK] != 0) return 1u;
+  uint64_t unequal = 0, ca = A.coef, cb = B.coef;
+  DG_PLAN_UNROLL
+  for (int d = 0; d < rank; ++d) {
+    const int32_t x0 = (int32_t)(BIG - w[d]);
+    const uint64_t a0 = term_val(A, d, x0, a64), b0 = term_val(B, d, x0, a64);
+    ca *= a0;
+    cb *= b0;
+    // (Same nonzero coordinates in both: A's range covers them all.)
+    for (int32_t x = A.lo[d] + tid; x < A.lo[d] + A.len[d]; x += nt) {
+      const uint64_t a = term_val(A, d, x, a64), b = term_val(B, d, x, a64);
+      unequal |= a * b0 != b * a0 ? 1u : 0u;
+    }
+  }
+  const bool any = c.any(unequal != 0);
+  return (any || ca != cb) ? 2u : 0u;
+}
+
 // PP lives in global memory (the kernels read it from the workspace).
 template <class C>
 DGC uint32_t location_compare(C& c, const uint8_t* blob_a, const uint8_t* blob_b, const PairPlan* PP, int64_t loc,
@@ -1303,6 +1373,17 @@ DGC uint32_t location_compare(C& c, const uint8_t* blob_a, const uint8_t* blob_b
   for (int l = 0; l < nleaf; ++l) {
     const int na = la[l].nterm, nb = lb[l].nterm;
     if (na + nb == 0) continue;
+    if (na == 1 && nb == 1 && !checks) {
+      // Two single-term leaves: compared factor by factor.
+      leaf_terms(c, blob_a, l, area, PA, terms);
+      leaf_terms(c, blob_b, l, area, PB, terms + 1);
+      c.sync();
+      const uint32_t s = compare_single_terms(c, terms[0], terms[1], la[l].rank, area, (uint64_t*)(area + E.hdr));
+      c.sync();
+      if (s == 1) return 1;
+      if (s == 2) status = 2;
+      continue;
+    }
     const LeafGeom G = leaf_geom(la[l]);
     leaf_terms(c, blob_a, l, area, PA, terms);
     leaf_terms(c, blob_b, l, area, PB, terms + na);

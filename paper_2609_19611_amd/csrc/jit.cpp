@@ -31,7 +31,7 @@ struct Code {
   std::vector<char> bytes;
   uint64_t stamp = 0;
 };
-const size_t kCodeCache = 32;
+const size_t kCodeCache = 128;
 std::map<std::string, Code> g_code;
 uint64_t g_clock = 0;
 

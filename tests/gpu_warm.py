@@ -1,0 +1,26 @@
+"""Compiles graphs' specialised kernels ahead of the GPU tests, many at
+once: each graph (or pair) compiles on first use, and doing that for dozens
+of graphs one after another would dominate the tests' run time.  The
+returned handles keep the loaded kernels alive for the caller's scope."""
+
+import concurrent.futures as cf
+
+
+def warm_graphs(B, texts, threads=8):
+    """Parses each text and runs one location through it (which compiles
+    and loads its specialised kernels); returns the graph handles."""
+    def one(text):
+        g = B.dg_graph_parse(text)
+        B.enumerate_locations(g, [0])
+        return g
+    with cf.ThreadPoolExecutor(threads) as ex:
+        return list(ex.map(one, texts))
+
+
+def warm_pairs(B, pairs, threads=8):
+    """The same for comparisons: (graph a, graph b) handles, one location each."""
+    def one(p):
+        B.compare_locations(p[0], p[1], [0])
+        return p
+    with cf.ThreadPoolExecutor(threads) as ex:
+        return list(ex.map(one, pairs))

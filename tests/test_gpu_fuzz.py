@@ -9,6 +9,7 @@ import pytest
 import torch
 
 import fuzz_graphs
+import gpu_warm
 import oracle
 from fuzz_graphs import REFUSALS, squared_variant
 
@@ -73,5 +74,13 @@ def test_fuzz_precompiled_kernels(B, chunk, monkeypatch):
 
 def test_fuzz_specialized_kernels(B, monkeypatch):
     monkeypatch.setenv("DIRIGO_JIT", "1")
+    texts = []
+    for seed in range(1000, 1016):
+        try:
+            B.dg_graph_parse(fuzz_graphs.random_graph(seed))
+            texts.append(fuzz_graphs.random_graph(seed))
+        except B.DgError:
+            pass
+    warm = gpu_warm.warm_graphs(B, texts)  # noqa: F841  (compiled several at once, kept loaded)
     done = sum(check_graph(B, seed, dags=False) for seed in range(1000, 1016))
     assert done >= 15

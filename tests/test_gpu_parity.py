@@ -11,6 +11,7 @@ import numpy as np
 import pytest
 import torch
 
+import gpu_warm
 import oracle
 import tiny_graphs
 from paper_2609_19611_amd import workloads as W
@@ -26,6 +27,15 @@ def B():
     if not torch.cuda.is_available():
         pytest.skip("no GPU")
     from paper_2609_19611_amd import binding
+    # Compile the specialised kernels of every catalogue graph and of the
+    # comparison pairs below ahead, several at once (the handles keep them
+    # loaded for the module).
+    global _WARM
+    ref = binding.dg_graph_parse(W.c5_reference_text())
+    small = binding.dg_graph_parse(W.c5_reference_text(n=2, c=4, hw=6, co=3))
+    pairs = [(ref, binding.dg_graph_parse(W.c5_variant_text(fault=f))) for f in W.c5_faults()]
+    pairs += [(small, binding.dg_graph_parse(W.c5_variant_text(fault=f, n=2, c=4, hw=6, co=3))) for f in W.c5_faults()]
+    _WARM = (gpu_warm.warm_graphs(binding, [CAT[n][0] for n in SEPARABLE]), gpu_warm.warm_pairs(binding, pairs))
     return binding
 
 
@@ -197,6 +207,18 @@ def test_compare_pairs_viewed_with_different_merged_dims(B, kernels, monkeypatch
     against the oracle."""
     monkeypatch.setenv("DIRIGO_JIT", "1" if kernels == "specialized" else "0")
     for name, a, b in tiny_graphs.merged_view_pairs():
+        n = oracle.Graph(a).output_numel
+        want = oracle.compare(oracle.Graph(a), oracle.Graph(b), range(n))
+        for x, y in ((a, b), (b, a)):
+            st, mism = B.compare_locations(B.dg_graph_parse(x), B.dg_graph_parse(y), list(range(n)))
+            assert np.array_equal(st.cpu().numpy(), want), name
+            assert np.array_equal(mism.cpu().numpy(), np.nonzero(want)[0]), name
+
+
+@pytest.mark.parametrize("kernels", ["specialized", "interpreted"])
+def test_factored_comparison_of_single_term_leaves(B, kernels, monkeypatch):
+    monkeypatch.setenv("DIRIGO_JIT", "1" if kernels == "specialized" else "0")
+    for name, a, b, _ in tiny_graphs.factored_compare_pairs():
         n = oracle.Graph(a).output_numel
         want = oracle.compare(oracle.Graph(a), oracle.Graph(b), range(n))
         for x, y in ((a, b), (b, a)):

@@ -175,3 +175,27 @@ def test_dag_c5_variants():
     locs = W.config_locations("c5")[::262144]
     for text in [W.c5_variant_text()] + [W.c5_variant_text(fault=f) for f in W.c5_faults()[:4]]:
         _dag_equal(hostemu.dag(text, locs), oracle.Graph(text).dag(locs))
+
+
+@pytest.mark.parametrize("name,a,b,interior", tiny_graphs.factored_compare_pairs())
+def test_factored_comparison_of_single_term_leaves(name, a, b, interior):
+    """Single-term leaves compared factor by factor: support changes in one
+    dim, a tap count changed in one dim, counts scaled, another leaf's
+    counts changed; every location against the oracle."""
+    from paper_2609_19611_amd import binding
+    for t in (a, b):
+        assert binding.dg_graph_info(binding.dg_graph_parse(t))["max_leaf_terms"] == 1
+    n = oracle.Graph(a).output_numel
+    want = oracle.compare(oracle.Graph(a), oracle.Graph(b), range(n))
+    assert want[n // 2] == interior
+    assert np.array_equal(hostemu.compare(a, b, range(n)), want)
+    assert np.array_equal(hostemu.compare(b, a, range(n)), want)
+
+
+def test_split_k_variant_has_single_term_leaves():
+    """The canonical forms of factors make every leaf of the split-K NHWC
+    variant one term (equal factors share a slot, so its K-split pieces
+    merge), at the workload's full size and at a small one."""
+    from paper_2609_19611_amd import binding
+    for text in (W.c5_variant_text(), W.c5_variant_text(n=2, c=4, hw=6, co=3)):
+        assert binding.dg_graph_info(binding.dg_graph_parse(text))["max_leaf_terms"] == 1

@@ -306,3 +306,22 @@ def merged_view_pairs():
             ("k", "reshape", ["h"], dict(shape=[2, 3])), ("k2", "mul", ["k", "k"], {}),
             ("b", "sum", ["k2"], dict(dims=[0], keepdim=0)), ("y", "mul", ["a", "b"], {})], "y", [3])
     return [("same_footprint", A, B), ("sliced", A, C), ("both_merge", B, D), ("counts", A, D)]
+
+
+def factored_compare_pairs():
+    """Pairs of graphs over the same leaves whose leaves are single terms
+    (the comparison then checks factor by factor): (name, a, b, status at
+    interior locations)."""
+    def g(ops, out_shape):
+        return _g([("x", [4, 7]), ("v", [7])], ops, "y", out_shape)
+    win3 = ("a", "affine_gather", ["x"], dict(shape=[4, 7], window=[3], idx0=["o0", "o1+w0-1"], mult=[1]))
+    win2 = ("a", "affine_gather", ["x"], dict(shape=[4, 7], window=[2], idx0=["o0", "o1+w0-1"], mult=[1]))
+    mid = ("c", "affine_gather", ["x"], dict(shape=[4, 7], window=[1], idx0=["o0", "o1"], mult=[1]))
+    scale_v = ("y", "mul", ["b", "v"], {})
+    A = g([win3, ("b", "relu", ["a"], {}), scale_v], [4, 7])                        # x taps 1,1,1
+    B = g([win3, mid, ("b", "add", ["a", "c"], {}), scale_v], [4, 7])               # x taps 1,2,1
+    C = g([win2, ("b", "relu", ["a"], {}), scale_v], [4, 7])                        # x taps 1,1
+    D = g([win3, ("b", "add", ["a", "a"], {}), scale_v], [4, 7])                    # x taps 2,2,2
+    E = g([win3, ("b", "relu", ["a"], {}), ("v2", "mul", ["v", "v"], {}), ("y", "mul", ["b", "v2"], {})], [4, 7])
+    return [("same", A, A, 0), ("middle_tap_doubled", A, B, 2), ("one_tap_fewer", A, C, 1),
+            ("all_doubled", A, D, 2), ("other_leaf_doubled", A, E, 2)]
