@@ -18,6 +18,8 @@
 #include "view.h"
 
 #include <algorithm>
+#include <array>
+#include <climits>
 #include <cmath>
 #include <cstring>
 #include <map>
@@ -415,6 +417,52 @@ class Compiler {
       memo_[key.str()] = slot;
     }
     return Coef{1, {slot}};
+  }
+
+  // The PATTERN instruction writing factor `dst` of canonical form cf, if
+  // the pattern fits one instruction (at most DGP_MAX_PAT runs or entries,
+  // values below 2^32, coordinates in int32).
+  bool pattern_instr(const CanonForm& cf, int dst, DgpInstr* out) {
+    DgpInstr P = blank(DGP_PATTERN);
+    P.dst = dst;
+    P.a = cf.dim;
+    P.pkind = cf.kind;
+    std::vector<std::array<int64_t, 4>> e;
+    if (cf.kind == 0) {
+      // Maximal runs of one value over consecutive offsets.
+      for (const auto& c : cf.coef) {
+        if (!e.empty() && e.back()[1] == c.first && (uint64_t)e.back()[3] == c.second) {
+          e.back()[1] = c.first + 1;
+        } else {
+          e.push_back({c.first, c.first + 1, 0, (int64_t)c.second});
+        }
+      }
+    } else {
+      for (const auto& c : cf.step)
+        for (size_t i = 0; i < c.second.size(); ++i) {
+          if (c.second[i].second == 0) continue;
+          const int64_t hi = i + 1 < c.second.size() ? c.second[i + 1].first : cf.span;
+          e.push_back({c.first, c.second[i].first, hi, (int64_t)c.second[i].second});
+        }
+    }
+    if (e.empty() || e.size() > DGP_MAX_PAT) return false;
+    int64_t pmin = INT64_MAX, pmax = INT64_MIN;
+    for (const auto& x : e) {
+      if (x[3] <= 0 || x[3] > (int64_t)UINT32_MAX) return false;
+      for (int q = 0; q < 3; ++q)
+        if (x[q] < INT32_MIN / 2 || x[q] > INT32_MAX / 2) return false;
+      pmin = std::min(pmin, x[0]);
+      pmax = std::max(pmax, cf.kind == 0 ? x[1] : x[0] + 1);
+    }
+    P.npat = (int32_t)e.size();
+    P.pmin = (int32_t)pmin;
+    P.pmax = (int32_t)pmax;
+    for (size_t i = 0; i < e.size(); ++i)
+      for (int q = 0; q < 4; ++q) P.pat[i][q] = (int32_t)(uint32_t)e[i][q];
+    const int64_t span = std::min<int64_t>(pmax - pmin, fac_[(size_t)dst].size);
+    fac_[(size_t)dst].cap = (int32_t)std::max<int64_t>(1, std::min<int64_t>(fac_[(size_t)dst].cap, span));
+    *out = P;
+    return true;
   }
 
   // Canonical form of k1 f1 + k2 f2 with constant k1, k2, when both have one.
@@ -1106,6 +1154,58 @@ Plan Compiler::run() {
   for (uint64_t b : sbound_)
     if (b >= k2_63) fail(DG_E_OVERFLOW, "static path-count bound reaches 2^63");
 
+  // Factors with canonical forms are written directly from their pattern
+  // (one PATTERN instruction, no sources); then every instruction whose
+  // result no leaf term reads, directly or through others, is dropped, and
+  // its factor keeps no values.
+  for (DgpInstr& I : ins_) {
+    const bool to_factor = (I.opcode == DGP_COMP && !I.dst_is_scalar) || I.opcode == DGP_LINCOMB;
+    if (to_factor && cf_[I.dst].known) {
+      DgpInstr P;
+      if (pattern_instr(cf_[I.dst], I.dst, &P)) I = P;
+    }
+  }
+  {
+    std::vector<char> flive(fac_.size(), 0), slive(sbound_.size(), 0);
+    for (const DgpLeaf& L : leaves)
+      for (int t = 0; t < L.nterm; ++t) {
+        const DgpTerm& T = dterms[(size_t)(L.term0 + t)];
+        if (T.coef_slot >= 0) slive[(size_t)T.coef_slot] = 1;
+        for (int d = 0; d < L.rank; ++d) flive[(size_t)T.factor[d]] = 1;
+      }
+    std::vector<char> keep(ins_.size(), 0);
+    for (int k = (int)ins_.size() - 1; k >= 0; --k) {
+      const DgpInstr& I = ins_[k];
+      if (!(I.dst_is_scalar ? slive[(size_t)I.dst] : flive[(size_t)I.dst])) continue;
+      keep[(size_t)k] = 1;
+      auto f = [&](int x) {
+        if (x >= 0) flive[(size_t)x] = 1;
+      };
+      auto sc = [&](int x) {
+        if (x >= 0) slive[(size_t)x] = 1;
+      };
+      if (I.opcode == DGP_COMP) {
+        for (int q = 0; q < I.nvar; ++q) f(I.var_src[q]);
+      } else if (I.opcode == DGP_LINCOMB) {
+        f(I.f1);
+        f(I.f2);
+        sc(I.k1);
+        sc(I.k2);
+      } else if (I.opcode == DGP_SMUL) {
+        for (int q = 0; q < I.ns; ++q) sc(I.s[q]);
+      } else if (I.opcode == DGP_SADD) {
+        sc(I.f1);
+        sc(I.f2);
+      }
+    }
+    std::vector<DgpInstr> kept;
+    for (size_t k = 0; k < ins_.size(); ++k)
+      if (keep[k]) kept.push_back(ins_[k]);
+    ins_.swap(kept);
+    for (size_t f = 0; f < fac_.size(); ++f)
+      if (!flive[f]) fac_[f].cap = 0;
+  }
+
   // Levels: an instruction runs one level after the latest instruction it
   // reads; within a level the order is free.  Component sums over more than
   // two variables get a level of their own.
@@ -1393,6 +1493,11 @@ std::string plan_listing(const Plan& p) {
         break;
       case DGP_SMUL: o << dst << " = SMUL " << I.cst; for (int q = 0; q < I.ns; ++q) o << " *s" << I.s[q]; break;
       case DGP_SADD: o << dst << " = SADD s" << I.f1 << "*" << I.c1 << " + s" << I.f2 << "*" << I.c2; break;
+      case DGP_PATTERN:
+        o << dst << " = PATTERN kind " << I.pkind << " at " << (I.a >= 0 ? "dim " + std::to_string(I.a) : "0");
+        for (int e = 0; e < I.npat; ++e)
+          o << " {" << I.pat[e][0] << "," << I.pat[e][1] << "," << I.pat[e][2] << ":" << I.pat[e][3] << "}";
+        break;
     }
     o << "\n";
   }

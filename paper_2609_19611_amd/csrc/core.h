@@ -382,6 +382,33 @@ DGC void plan_exec(C& c, const uint8_t* blob, int64_t loc, uint8_t* area, const 
             scal[I.dst] = 0;
           }
         }
+      } else if (op == DGP_PATTERN) {
+        const int32_t r = I.a >= 0 ? (int32_t)((loc / h->out_stride[I.a]) % h->out_shape[I.a]) : 0;
+        const DgpFactor F = fac[I.dst];
+        int32_t lo = I.pkind == 0 ? r + I.pmin : I.pmin, hi = I.pkind == 0 ? r + I.pmax : I.pmax;
+        if (lo < 0) lo = 0;
+        if (hi > F.size) hi = F.size;
+        int32_t len = hi > lo ? hi - lo : 0;
+        if (len > F.cap) {
+          *err |= DGP_ERR_CAPACITY;
+          len = F.cap;
+        }
+        if (tid == 0) {
+          meta[2 * I.dst] = lo;
+          meta[2 * I.dst + 1] = len;
+        }
+        uint64_t* dv = fval + F.off;
+        for (int i = tid; i < len; i += nt) {
+          const int32_t x = lo + i;
+          uint64_t v = 0;
+          DG_PLAN_UNROLL
+          for (int e = 0; e < I.npat; ++e) {
+            const int32_t* P = I.pat[e];
+            const bool on = I.pkind == 0 ? (x >= r + P[0] && x < r + P[1]) : (x == P[0] && r >= P[1] && r < P[2]);
+            if (on) v += (uint32_t)P[3];
+          }
+          dv[i] = v;
+        }
       } else if (op == DGP_ROOT || op == DGP_CONST) {
         if (tid == 0) {
           int32_t x;
@@ -1278,74 +1305,109 @@ struct PairPlan {
   LeafShape leaf[16];
 };
 
-// Compares two single-term leaves without expanding their cells.  A term is
-// coef * prod_d f_d(x_d).  When both have entries (nonzero coefficient and
-// a nonzero coordinate in every dim), their nonzero cells agree iff every
-// dim's two factors have the same nonzero coordinates; then their counts
-// agree iff every dim's two factors are proportional there and one cell
-// (the first nonzero coordinate of every dim) has the same count.  Factor
-// values and that cell's count are real counts below 2^32 (the caller
-// checks the static bounds), so the cross products fit 64 bits.
-// w: LDS scratch of 2 * DGP_MAX_RANK + 2 words.
-// Returns 0 equal, 1 nonzero sets differ, 2 counts differ.
+// One factor of a single-term leaf, as the comparison reads it: values
+// vals[0 .. len) at coordinates lo .. lo + len - 1 (LDS).
+struct FacView {
+  int32_t lo, len;
+  const uint64_t* vals;
+  DGC uint32_t at(int32_t x) const {  // (values below 2^32 here)
+    const int32_t i = x - lo;
+    return (i >= 0 && i < len) ? (uint32_t)vals[i] : 0u;
+  }
+};
+
+DGC FacView fac_view(const uint8_t* blob, const uint8_t* area, const PlanLayout& PL, int f) {
+  const DgpHeader* h = (const DgpHeader*)blob;
+  const DgpFactor* fac = (const DgpFactor*)(blob + h->factor_off);
+  const int32_t* meta = (const int32_t*)(area + PL.fmeta);
+  FacView v;
+  v.lo = meta[2 * f];
+  v.len = meta[2 * f + 1];
+  v.vals = (const uint64_t*)(area + PL.fval) + fac[f].off;
+  return v;
+}
+
+DGC uint64_t term_coef(const uint8_t* blob, const uint8_t* area, const PlanLayout& PL, const DgpTerm& T) {
+  const uint64_t* scal = (const uint64_t*)(area + PL.scal);
+  return (T.coef_slot < 0 ? 1ull : scal[T.coef_slot]) * T.coef_const;
+}
+
+// Compares leaf `leaf` of two plans whose leaf is one term each, without
+// expanding cells.  A term is coef * prod_d f_d(x_d).  When both have
+// entries (nonzero coefficient and a nonzero coordinate in every dim),
+// their nonzero cells agree iff every dim's two factors have the same
+// nonzero coordinates; then their counts agree iff every dim's two factors
+// are proportional there and one cell (the first nonzero coordinate of
+// every dim) has the same count.  Factor values and that cell's count are
+// real counts below 2^32 (the caller checks the static bounds), so the
+// cross products fit 64 bits.  Block-uniform results come from ballots;
+// nothing is written.  Returns 0 equal, 1 nonzero sets differ, 2 counts
+// differ.
 template <class C>
-DGC uint32_t compare_single_terms(C& c, const TermRef& A, const TermRef& B, int rank, uint8_t* area, uint64_t* w) {
-  const uint64_t* a64 = (const uint64_t*)area;
-  const int tid = c.tid(), nt = c.nthreads();
-  const uint64_t BIG = 1ull << 40;  // first nonzero coordinate x kept as the maximum of BIG - x
-  for (int i = tid; i < 2 * DGP_MAX_RANK + 2; i += nt) w[i] = 0;
-  c.sync();
-  uint64_t differ = 0;
+DGC uint32_t compare_single_terms(C& c, const uint8_t* blob_a, const uint8_t* blob_b, int leaf, const uint8_t* area,
+                                  const PlanLayout& PA, const PlanLayout& PB) {
+  const DgpHeader* ha = (const DgpHeader*)blob_a;
+  const DgpHeader* hb = (const DgpHeader*)blob_b;
+  const DgpLeaf& La = ((const DgpLeaf*)(blob_a + ha->leaf_off))[leaf];
+  const DgpLeaf& Lb = ((const DgpLeaf*)(blob_b + hb->leaf_off))[leaf];
+  const DgpTerm& Ta = ((const DgpTerm*)(blob_a + ha->term_off))[La.term0];
+  const DgpTerm& Tb = ((const DgpTerm*)(blob_b + hb->term_off))[Lb.term0];
+  const int tid = c.tid(), nt = c.nthreads(), rank = La.rank;
+  uint64_t ca = term_coef(blob_a, area, PA, Ta), cb = term_coef(blob_b, area, PB, Tb);
+  bool empty_a = ca == 0, empty_b = cb == 0, differ = false;
+  int32_t x0[DGP_MAX_RANK];
+  // Pass 1: first nonzero coordinate of each factor, and whether the
+  // nonzero coordinates agree.
   DG_PLAN_UNROLL
   for (int d = 0; d < rank; ++d) {
-    int32_t lo, hi;
-    term_hull(&A, 1, d, &lo, &hi);
-    int32_t lo2, hi2;
-    term_hull(&B, 1, d, &lo2, &hi2);
-    if (hi2 > lo2) {
-      if (hi <= lo) {
-        lo = lo2;
-        hi = hi2;
+    const FacView A = fac_view(blob_a, area, PA, Ta.factor[d]);
+    const FacView B = fac_view(blob_b, area, PB, Tb.factor[d]);
+    int32_t lo = A.lo, hi = A.lo + A.len;
+    if (B.len > 0) {
+      if (A.len <= 0) {
+        lo = B.lo;
+        hi = B.lo + B.len;
       } else {
-        lo = lo2 < lo ? lo2 : lo;
-        hi = hi2 > hi ? hi2 : hi;
+        lo = B.lo < lo ? B.lo : lo;
+        hi = B.lo + B.len > hi ? B.lo + B.len : hi;
       }
     }
-    uint64_t fa = 0, fb = 0;
-    for (int32_t x = lo + tid; x < hi; x += nt) {  // ascending per thread: the first hit is its least
-      const uint64_t a = term_val(A, d, x, a64), b = term_val(B, d, x, a64);
-      if (a != 0 && fa == 0) fa = BIG - (uint64_t)x;
-      if (b != 0 && fb == 0) fb = BIG - (uint64_t)x;
-      differ |= (a != 0) != (b != 0) ? 1u : 0u;
+    int32_t fa = -1, fb = -1;
+    bool diff = false;
+    for (int32_t base = lo; base < hi; base += nt) {
+      const int32_t x = base + tid;
+      const bool nza = x < hi && A.at(x) != 0u, nzb = x < hi && B.at(x) != 0u;
+      if (fa < 0) {
+        const int k = c.first(nza);
+        if (k >= 0) fa = base + k;
+      }
+      if (fb < 0) {
+        const int k = c.first(nzb);
+        if (k >= 0) fb = base + k;
+      }
+      diff = diff || nza != nzb;
     }
-    c.reduce_max(&w[d], fa);
-    c.reduce_max(&w[DGP_MAX_RANK + d], fb);
-  }
-  c.reduce_add(&w[2 * DGP_MAX_RANK], differ);
-  c.sync();
-  bool empty_a = A.coef == 0, empty_b = B.coef == 0;
-  DG_PLAN_UNROLL
-  for (int d = 0; d < rank; ++d) {
-    empty_a = empty_a || w[d] == 0;
-    empty_b = empty_b || w[DGP_MAX_RANK + d] == 0;
+    empty_a = empty_a || fa < 0;
+    empty_b = empty_b || fb < 0;
+    differ = differ || c.any(diff);
+    x0[d] = fa;
   }
   if (empty_a || empty_b) return empty_a == empty_b ? 0u : 1u;
-  if (w[2 * DGP_MAX_RANK] != 0) return 1u;
-  uint64_t unequal = 0, ca = A.coef, cb = B.coef;
+  if (differ) return 1u;
+  // Pass 2: proportional values against the first nonzero coordinate.
+  bool unequal = false;
   DG_PLAN_UNROLL
   for (int d = 0; d < rank; ++d) {
-    const int32_t x0 = (int32_t)(BIG - w[d]);
-    const uint64_t a0 = term_val(A, d, x0, a64), b0 = term_val(B, d, x0, a64);
+    const FacView A = fac_view(blob_a, area, PA, Ta.factor[d]);
+    const FacView B = fac_view(blob_b, area, PB, Tb.factor[d]);
+    const uint32_t a0 = A.at(x0[d]), b0 = B.at(x0[d]);
     ca *= a0;
     cb *= b0;
-    // (Same nonzero coordinates in both: A's range covers them all.)
-    for (int32_t x = A.lo[d] + tid; x < A.lo[d] + A.len[d]; x += nt) {
-      const uint64_t a = term_val(A, d, x, a64), b = term_val(B, d, x, a64);
-      unequal |= a * b0 != b * a0 ? 1u : 0u;
-    }
+    // (Both have the same nonzero coordinates: A's range covers them.)
+    for (int32_t x = A.lo + tid; x < A.lo + A.len; x += nt)
+      unequal = unequal || (uint64_t)A.at(x) * b0 != (uint64_t)B.at(x) * a0;
   }
-  const bool any = c.any(unequal != 0);
-  return (any || ca != cb) ? 2u : 0u;
+  return (c.any(unequal) || ca != cb) ? 2u : 0u;
 }
 
 // PP lives in global memory (the kernels read it from the workspace).
@@ -1375,11 +1437,7 @@ DGC uint32_t location_compare(C& c, const uint8_t* blob_a, const uint8_t* blob_b
     if (na + nb == 0) continue;
     if (na == 1 && nb == 1 && !checks) {
       // Two single-term leaves: compared factor by factor.
-      leaf_terms(c, blob_a, l, area, PA, terms);
-      leaf_terms(c, blob_b, l, area, PB, terms + 1);
-      c.sync();
-      const uint32_t s = compare_single_terms(c, terms[0], terms[1], la[l].rank, area, (uint64_t*)(area + E.hdr));
-      c.sync();
+      const uint32_t s = compare_single_terms(c, blob_a, blob_b, l, area, PA, PB);
       if (s == 1) return 1;
       if (s == 2) status = 2;
       continue;

@@ -60,6 +60,7 @@ struct HostCtx {
     return 0u;
   }
   bool any(bool f) const { return f; }
+  int first(bool f) const { return f ? 0 : -1; }
 };
 
 thread_local std::string g_err;

@@ -100,6 +100,23 @@ struct DevCtx {
     if (BLOCK == 64) return __ballot(f) != 0;
     return __syncthreads_or(f) != 0;
   }
+  // Lowest thread index of the block with f set, or -1 (the same on every
+  // thread).  A one-wave block takes the wave's ballot.
+  DGC int first(bool f) const {
+    const uint64_t m = __ballot(f);
+    if (BLOCK == 64) return m ? (int)__builtin_ctzll(m) : -1;
+    const uint32_t wave = threadIdx.x >> 6;
+    __syncthreads();
+    if ((threadIdx.x & 63u) == 0) wsum[wave] = m ? (uint32_t)__builtin_ctzll(m) : 64u;
+    __syncthreads();
+    int r = -1;
+#pragma unroll
+    for (int w = BLOCK / 64 - 1; w >= 0; --w) {
+      const uint32_t x = wsum[w];
+      if (x < 64u) r = w * 64 + (int)x;
+    }
+    return r;
+  }
 };
 
 extern __shared__ uint64_t dg_smem[];

@@ -45,7 +45,10 @@ enum DgpOpcode : int32_t {
   DGP_LINCOMB = 4,  // factor = k1 * f1 + k2 * f2
   DGP_SMUL = 5,     // scalar = cst * prod s[i]
   DGP_SADD = 6,     // scalar = k1 * s1 + k2 * s2
+  DGP_PATTERN = 7,  // factor = a fixed pattern placed at the location (see DgpInstr.pat)
 };
+
+#define DGP_MAX_PAT 16  // entries of one pattern
 
 struct DgpInstr {
   int32_t opcode;
@@ -68,6 +71,15 @@ struct DgpInstr {
   int32_t ns;
   int32_t s[8];
   uint64_t cst;
+  // PATTERN: r is the location's coordinate `a` (0 when a < 0); entry e is
+  // pat[e] = {p, q, u, value} (value below 2^32):
+  //   kind 0: coordinates [r + p, r + q) hold value (entries disjoint);
+  //   kind 1: coordinate p holds value when q <= r < u (entries of one
+  //           coordinate never hold at the same r).
+  // Coordinates outside [0, size) are dropped.  The factor's range is
+  // [r + pmin, r + pmax) (kind 0) or [pmin, pmax) (kind 1), clipped.
+  int32_t pkind, npat, pmin, pmax;
+  int32_t pat[DGP_MAX_PAT][4];
 };
 
 struct DgpFactor {
