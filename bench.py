@@ -66,6 +66,9 @@ def parse_args():
     p.add_argument("--stream-gib", type=float, default=16.0, help="buffer of the streamed full output (two halves)")
     p.add_argument("--copy-gib", type=float, default=0.0,
                    help="instead of the workload, time a plain device copy of this many GiB (HBM calibration)")
+    p.add_argument("--write-sweep", action="store_true",
+                   help="instead of the workload, time torch's fill (int32) over buffers of 0.5 to 32 GiB: the "
+                        "plain write rate against the size written")
     return p.parse_args()
 
 
@@ -100,6 +103,23 @@ def copy_calibration(gib, steps, warmup):
     dispatches are the reference for scaling the FETCH_SIZE / WRITE_SIZE
     counters."""
     print(json.dumps(write_rates(gib, steps, warmup)), flush=True)
+
+
+def write_sweep(steps, warmup):
+    """Plain write rate against buffer size: torch's int32 fill over one
+    buffer of each size (median of `steps` fills), one JSON line."""
+    import torch
+    stream = torch.cuda.current_stream()
+    rows = []
+    for gib in (0.5, 1, 2, 4, 8, 16, 32):
+        n = int(gib * (1 << 30)) // 4
+        buf = torch.empty(n, dtype=torch.int32, device="cuda")
+        ms = _median_ms(lambda: buf.fill_(7), steps, warmup, stream)
+        rows.append({"gib": gib, "bytes": n * 4, "ms": ms, "GBps": n * 4 / (ms * 1e-3) / 1e9})
+        print(f"fill {gib} GiB: {ms:.3f} ms, {rows[-1]['GBps']:.1f} GB/s", file=sys.stderr, flush=True)
+        del buf
+        torch.cuda.empty_cache()
+    print(json.dumps({"write_sweep": rows, "statistic": f"median of {steps} fills", "git": git_sha()}), flush=True)
 
 
 KERNEL_SOURCES = ["program.h", "core.h", "kernels_dev.h", "jit_source.cpp", "jit.cpp", "compile.cpp", "graph.cpp"]
@@ -145,6 +165,16 @@ def _median_ms(fn, steps, warmup, stream):
     return float(np.median([a.elapsed_time(b) for a, b in ev]))
 
 
+def same_buffer_fill(ids, cnt, stream, steps=5, warmup=2):
+    """Write rate of torch's fill over the enumeration's own output arrays
+    (the same bytes at the same addresses).  Plain write rates fall with the
+    size written (about 6.5 TB/s over 2 GiB, 5.7-6.0 TB/s over 35 GB on the
+    same boxes), so this, not a 2 GiB fill, is the ceiling a writer of
+    these rows is held to."""
+    ms = _median_ms(lambda: (ids.fill_(7), cnt.fill_(7)), steps, warmup, stream)
+    return (ids.numel() * ids.element_size() + cnt.numel() * cnt.element_size()) / (ms * 1e-3) / 1e9
+
+
 def secondary_enumeration(B, W, name, fill_gbps, steps=10, warmup=3):
     """Single-pass enumeration of another workload: median call time of
     `steps` calls, rates and the HBM fraction (algorithmic bytes)."""
@@ -162,12 +192,14 @@ def secondary_enumeration(B, W, name, fill_gbps, steps=10, warmup=3):
     ms = _median_ms(lambda: B.dg_enumerate(g, d_locs, off, ids, cnt, ws), steps, warmup, stream)
     alg = 16 * n + 8 * total
     gbps = alg / (ms * 1e-3) / 1e9
+    same = same_buffer_fill(ids, cnt, stream)
     del ids, cnt
     torch.cuda.empty_cache()
     return {"workload": f"{name}: " + W.CONFIGS[name]["desc"], "locations": n, "entries": total,
             "ms_per_call": ms, "statistic": f"median of {steps} calls (dg_enumerate, whole call)",
             "entries_per_s": total / (ms * 1e-3), "locations_per_s": n / (ms * 1e-3),
-            "achieved_GBps": gbps, "frac_of_hbm_peak": gbps / HBM_PEAK_GBS, "frac_of_measured_fill": gbps / fill_gbps}
+            "achieved_GBps": gbps, "frac_of_hbm_peak": gbps / HBM_PEAK_GBS, "frac_of_measured_fill": gbps / fill_gbps,
+            "same_buffer_fill_GBps": same, "frac_of_same_buffer_fill": gbps / same}
 
 
 def secondary_compare(B, W, steps=5, warmup=2):
@@ -536,6 +568,9 @@ def main():
         print("--wide times the single-pass enumeration of c1-c4 only", file=sys.stderr)
         sys.exit(2)
 
+    if args.write_sweep:
+        write_sweep(args.steps, args.warmup)
+        return
     if args.copy_gib > 0:
         copy_calibration(args.copy_gib, args.steps, args.warmup)
         return
@@ -727,10 +762,15 @@ def main():
                      "kernel_ms_statistic": f"median of {args.steps} launches", "algorithmic_bytes": alg_bytes},
     }
     # The bandwidth plain torch kernels reach on this machine (after the timed
-    # region), beside the spec peak.
+    # region), beside the spec peak: a fill of the same output arrays, and
+    # a 2 GiB fill and copy.
+    same = same_buffer_fill(ids, cnt, stream)
     del ids, cnt
     rates = write_rates(2.0, 5, 2)
+    line["roofline"]["same_buffer_fill_GBps"] = same
+    line["roofline"]["frac_of_same_buffer_fill"] = achieved / same
     line["roofline"]["measured_fill_GBps"] = rates["fill_GBps_write"]
+    line["roofline"]["measured_fill_bytes"] = rates["bytes"]
     line["roofline"]["measured_copy_GBps"] = rates["copy_GBps_read_plus_write"]
     line["roofline"]["frac_of_measured_fill"] = achieved / rates["fill_GBps_write"]
     if args.workload == "c4" and not (args.two_pass or args.wide) and not args.no_secondary:

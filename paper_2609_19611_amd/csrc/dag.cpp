@@ -92,6 +92,42 @@ int64_t mod_inverse(int64_t a, int64_t m) {
   fail(DG_E_UNSUPPORTED_OP, "no modular inverse");
 }
 
+// Whether index function f of a group can leave its valid range at some
+// node and window point (or, with an exact division and no window
+// variable, fail to divide): interval bounds over every output coordinate
+// of an op with output shape `out` and every point of the window [wlo,
+// whi).  A function that cannot only enters the element indices.
+bool can_bind(const IndexFn& f, const Dims& out, const ReadGroup& G, int64_t size, bool window) {
+  const int R = (int)out.size();
+  int64_t lo = f.c, hi = f.c;
+  for (const IndexFn::Term& t : f.terms) {
+    int64_t vlo, vhi;
+    if (t.var < R) {
+      vlo = 0;
+      vhi = out[t.var] - 1;
+    } else {
+      const int q = t.var - R;
+      if (q >= (int)G.wlo.size()) return true;
+      vlo = G.wlo[q];
+      vhi = G.whi[q] - 1;
+    }
+    if (vhi < vlo) return true;
+    if (t.vdiv != 1) {
+      // (The device truncates; variables are non-negative.)
+      if (vlo < 0 || t.vdiv <= 0) return true;
+      vlo /= t.vdiv;
+      vhi /= t.vdiv;
+    }
+    const int64_t a = t.coef * vlo, b = t.coef * vhi;
+    lo += std::min(a, b);
+    hi += std::max(a, b);
+  }
+  if (f.mode == 0) return !(lo >= 0 && hi <= size - 1);
+  if (f.mode == 1 && window) return !(lo >= 0 && hi <= f.s * (size - 1));  // divisibility: the progression's
+  if (f.mode == 1) return f.s != 1 || !(lo >= 0 && hi <= size - 1);
+  return true;
+}
+
 }  // namespace
 
 DagProgram compile_dag(const GraphIR& g, int nthreads) {
@@ -220,7 +256,21 @@ DagProgram compile_dag(const GraphIR& g, int nthreads) {
             fast = false;
             continue;
           }
-          if (npair < DGD_MAX_PAIRS) e.pair[npair] = DgdPair{(int16_t)a, (int16_t)d, (int16_t)q, 0};
+          if (npair < DGD_MAX_PAIRS) {
+            const int64_t size = g.tensors[G.ops[a].tensor].shape[d];
+            const bool bind = can_bind(f, g.tensors[op.out].shape, G, size, q >= 0);
+            DgdPair pr;
+            std::memset(&pr, 0, sizeof(pr));
+            pr.a = (int32_t)a;
+            pr.d = (int32_t)d;
+            pr.q = (int32_t)q;
+            pr.bind = bind ? 1 : 0;
+            int64_t st = 1;
+            for (size_t d2 = d + 1; d2 < g.tensors[G.ops[a].tensor].shape.size(); ++d2)
+              st *= g.tensors[G.ops[a].tensor].shape[d2];
+            pr.stride = (uint32_t)st;
+            e.pair[npair] = pr;
+          }
           if (q >= 0) {
             const int64_t k = progression_coef(f, R, q);
             if (k == 0) {
@@ -239,6 +289,26 @@ DagProgram compile_dag(const GraphIR& g, int nthreads) {
       e.fast = fast ? 1 : 0;
       e.npair = fast ? npair : 0;
       if (fast) {
+        // The pairs that can bind first (in their order), the others after;
+        // the exact-division pairs renumbered to match.
+        std::vector<int> order;
+        for (int pi = 0; pi < npair; ++pi)
+          if (e.pair[pi].bind) order.push_back(pi);
+        e.nbind = (int32_t)order.size();
+        for (int pi = 0; pi < npair; ++pi)
+          if (!e.pair[pi].bind) order.push_back(pi);
+        std::vector<int> where(npair);
+        DgdPair sorted[DGD_MAX_PAIRS];
+        std::memset(sorted, 0, sizeof(sorted));
+        for (int k2 = 0; k2 < npair; ++k2) {
+          sorted[k2] = e.pair[order[k2]];
+          where[order[k2]] = k2;
+        }
+        std::memcpy(e.pair, sorted, sizeof(sorted));
+        for (size_t q = 0; q < G.wlo.size(); ++q)
+          if (e.mpair[q] >= 0) e.mpair[q] = where[e.mpair[q]];
+      }
+      if (fast) {
         // Element-index steps per progression step.
         for (size_t a = 0; a < G.ops.size(); ++a) {
           const Dims& sh = g.tensors[G.ops[a].tensor].shape;
@@ -254,6 +324,12 @@ DagProgram compile_dag(const GraphIR& g, int nthreads) {
             st *= sh[d];
           }
         }
+        e.steps24 = 1;
+        for (size_t a = 0; a < G.ops.size(); ++a)
+          for (size_t q = 0; q < G.wlo.size(); ++q) {
+            const int32_t v = (int32_t)e.astep[a][q];
+            if (v < -(1 << 23) || v >= (1 << 23)) e.steps24 = 0;
+          }
         max_win = std::max(max_win, (int)G.wlo.size());
         max_opnd = std::max(max_opnd, (int)G.ops.size());
       }

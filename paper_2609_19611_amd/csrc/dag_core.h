@@ -136,6 +136,152 @@ DGC uint32_t small_divmod(uint32_t n, uint32_t d, uint32_t* r) {
 DGC int32_t floor_div(int32_t a, int32_t b) { return fdiv(a, b); }
 DGC int32_t ceil_div(int32_t a, int32_t b) { return -fdiv(-a, b); }
 
+DGC int32_t pmod(int32_t a, int32_t m) {
+  if ((m & (m - 1)) == 0) return a & (m - 1);  // (a power of two: two's complement)
+  const int32_t r = a % m;
+  return r < 0 ? r + m : r;
+}
+
+// a / m for a >= 0 and m >= 1 (shift for a power of two).
+DGC int32_t qpos(int32_t a, int32_t m) {
+  if ((m & (m - 1)) == 0) return a >> __builtin_ctz((unsigned)m);
+  return a / m;
+}
+
+// a / m for a multiple a of m >= 1 of either sign.
+DGC int32_t qexact(int32_t a, int32_t m) {
+  if ((m & (m - 1)) == 0) return a >> __builtin_ctz((unsigned)m);
+  return a / m;
+}
+
+// Coordinates of element e of X in registers (row-major, last fastest).
+DGC void elem_coords(const DgdTensor& X, uint32_t e, uint32_t* x) {
+  DG_UNROLL
+  for (int d = DGP_MAX_RANK - 1; d >= 0; --d) {
+    x[d] = 0;
+    if (d < X.rank) {
+      const uint32_t q = magic_div(e, X.magic[d]);
+      x[d] = e - q * (uint32_t)X.shape[d];
+      e = q;
+    }
+  }
+}
+
+// The frontier F[0..n) of tensor X made sorted and unique through a bitmap
+// over the bounding box of its candidates' coordinates: the box's cells in
+// row-major order are in ascending element order, so the set cells, read
+// word by word with a scan of the words' counts, are the sorted unique
+// elements.  Applies when the box's bitmap and counts fit `ws` (LDS words
+// free for the call); returns the number kept, or ~0u with F untouched.
+// Called by all threads; ends past a barrier.
+template <class C>
+DGC uint32_t box_unique(C& c, const DgdTensor& X, uint32_t* F, uint32_t n, uint32_t* ws, uint32_t ws_words) {
+  const int tid = c.tid(), nt = c.nthreads();
+  const int R = X.rank;
+  uint32_t* mn = ws;
+  uint32_t* mx = ws + DGP_MAX_RANK;
+  if (n < 2 || R < 1 || ws_words < 2 * DGP_MAX_RANK + 2) return ~0u;
+  for (int d = tid; d < DGP_MAX_RANK; d += nt) {
+    mn[d] = 0xFFFFFFFFu;
+    mx[d] = 0;
+  }
+  c.sync();
+  uint32_t lmn[DGP_MAX_RANK], lmx[DGP_MAX_RANK];
+  DG_UNROLL
+  for (int d = 0; d < DGP_MAX_RANK; ++d) {
+    lmn[d] = 0xFFFFFFFFu;
+    lmx[d] = 0;
+  }
+  for (uint32_t i = (uint32_t)tid; i < n; i += (uint32_t)nt) {
+    uint32_t x[DGP_MAX_RANK];
+    elem_coords(X, F[i], x);
+    DG_UNROLL
+    for (int d = 0; d < DGP_MAX_RANK; ++d) {
+      lmn[d] = x[d] < lmn[d] ? x[d] : lmn[d];
+      lmx[d] = x[d] > lmx[d] ? x[d] : lmx[d];
+    }
+  }
+  DG_UNROLL
+  for (int d = 0; d < DGP_MAX_RANK; ++d)
+    if (d < R) {
+      c.reduce_min32(&mn[d], lmn[d]);
+      c.reduce_max32(&mx[d], lmx[d]);
+    }
+  c.sync();
+  uint32_t lo[DGP_MAX_RANK], e[DGP_MAX_RANK];
+  uint64_t V = 1;
+  DG_UNROLL
+  for (int d = 0; d < DGP_MAX_RANK; ++d) {
+    lo[d] = d < R ? mn[d] : 0u;
+    e[d] = d < R ? mx[d] - mn[d] + 1u : 1u;
+    V *= e[d];
+  }
+  const uint64_t W = (V + 31) / 32;
+  if (V > (1ull << 26) || 2 * DGP_MAX_RANK + 2 * W > (uint64_t)ws_words) {
+    c.sync();  // (every thread has read mn and mx)
+    return ~0u;
+  }
+  uint32_t* bm = ws + 2 * DGP_MAX_RANK;
+  uint32_t* pre = bm + W;
+  for (uint32_t w = (uint32_t)tid; w < (uint32_t)W; w += (uint32_t)nt) bm[w] = 0;
+  c.sync();
+  // Box strides, row-major over the extents.
+  uint32_t bs[DGP_MAX_RANK];
+  {
+    uint32_t st = 1;
+    DG_UNROLL
+    for (int d = DGP_MAX_RANK - 1; d >= 0; --d) {
+      bs[d] = st;
+      st *= e[d];
+    }
+  }
+  for (uint32_t i = (uint32_t)tid; i < n; i += (uint32_t)nt) {
+    uint32_t x[DGP_MAX_RANK];
+    elem_coords(X, F[i], x);
+    uint32_t b = 0;
+    DG_UNROLL
+    for (int d = 0; d < DGP_MAX_RANK; ++d) b += (x[d] - lo[d]) * bs[d];
+    c.atomic_or32(&bm[b >> 5], 1u << (b & 31u));
+  }
+  c.sync();
+  for (uint32_t w = (uint32_t)tid; w < (uint32_t)W; w += (uint32_t)nt) pre[w] = (uint32_t)__builtin_popcount(bm[w]);
+  c.sync();
+  const uint64_t total = block_scan(c, pre, (uint32_t)W);
+  // Each thread expands whole words: the coordinates of the word's first
+  // cell, then one cell at a time (last coordinate fastest).
+  for (uint32_t w = (uint32_t)tid; w < (uint32_t)W; w += (uint32_t)nt) {
+    uint32_t bits = bm[w];
+    if (!bits) continue;
+    uint32_t pos = pre[w];
+    uint32_t o[DGP_MAX_RANK];
+    uint32_t r = w * 32u;
+    DG_UNROLL
+    for (int d = DGP_MAX_RANK - 1; d >= 0; --d) {
+      o[d] = r % e[d];
+      r /= e[d];
+    }
+    uint32_t flat = 0;
+    DG_UNROLL
+    for (int d = 0; d < DGP_MAX_RANK; ++d)
+      if (d < R) flat += (lo[d] + o[d]) * X.stride[d];
+    for (int k = 0; k < 32 && bits; ++k) {
+      if (bits & 1u) F[pos++] = flat;
+      bits >>= 1;
+      // Next cell: add one to the last coordinate, carrying.
+      DG_UNROLL
+      for (int d = DGP_MAX_RANK - 1; d >= 0; --d) {
+        if (d >= R) continue;
+        flat += X.stride[d];
+        if (++o[d] < e[d]) break;
+        flat -= e[d] * X.stride[d];
+        o[d] = 0;
+      }
+    }
+  }
+  c.sync();
+  return (uint32_t)total;
+}
+
 // Coordinates of element e of X into the calling thread's variables 0..R-1.
 DGC void node_coords(const DgdTensor& X, uint32_t e, int32_t* vt, int nt) {
   for (int d = DGP_MAX_RANK - 1; d >= 0; --d) {
@@ -173,7 +319,7 @@ DGC void ifn_linear(const DgpIFn& f, int wv, const int32_t* vt, int nt, int32_t*
         kk = f.coef[t];
       } else {
         int32_t vv = vt[f.var[t] * nt];
-        if (f.vdiv[t] != 1) vv /= f.vdiv[t];
+        if (f.vdiv[t] != 1) vv = qpos(vv, f.vdiv[t]);  // (variables are non-negative)
         c += f.coef[t] * vv;
       }
     }
@@ -329,10 +475,6 @@ struct Slots {
   DGC uint32_t& ghi(int j) const { return s[(size_t)(2 * MQ + MA + 1) * nt + j]; }
 };
 
-DGC int32_t pmod(int32_t a, int32_t m) {
-  const int32_t r = a % m;
-  return r < 0 ? r + m : r;
-}
 
 // Progressions of group G at the calling thread's node (coordinates in its
 // variables): every window variable's first valid value and length and,
@@ -347,6 +489,7 @@ DGC uint64_t ap_setup(const DagCtx& x, const DgdGroup& G, int R, const Slots& S,
   bool bad = false;
   for (int pi = 0; pi < G.npair; ++pi) {
     const DgdPair pr = G.pair[pi];
+    if (!pr.bind) continue;
     const DgdOperand& P = x.Ps[G.op0 + pr.a];
     const DgpIFn& f = P.idx[pr.d];
     if (pr.q < 0) {
@@ -413,6 +556,132 @@ DGC uint64_t ap_setup(const DagCtx& x, const DgdGroup& G, int R, const Slots& S,
     S.base(j, pr.a) += Ta.stride[pr.d] * (uint32_t)v;
   }
   return P;
+}
+
+// ---- progressions in registers ---------------------------------------------
+// The same progressions for groups of Q window variables and NOP operands
+// known at compile time: every value stays in the calling thread's
+// registers (the window variable of a pair selects its entry by unrolled
+// comparison), the pairs that cannot bind are skipped, and the common
+// coefficients (unit k, unit steps, no division) take short paths.
+template <int Q, int NOP>
+struct NodeAP {
+  int32_t first[Q > 0 ? Q : 1];
+  uint32_t len[Q > 0 ? Q : 1];
+  uint32_t base[NOP];
+};
+
+template <int Q, int NOP>
+DGC uint64_t ap_setup_reg(const DagCtx& x, const DgdGroup& G, int R, bool bases, NodeAP<Q, NOP>& N) {
+  constexpr int QD = Q > 0 ? Q : 1;
+  int32_t lo[QD], hi[QD];
+  DG_UNROLL
+  for (int q = 0; q < Q; ++q) {
+    lo[q] = G.wlo[q];
+    hi[q] = G.whi[q] - 1;
+  }
+  const int np = G.npair, nb = G.nbind;
+  bool bad = false;
+  // Only the pairs that can bind (the first nb).
+  for (int pi = 0; pi < nb; ++pi) {
+    const DgdPair pr = G.pair[pi];
+    const DgpIFn& f = x.Ps[G.op0 + pr.a].idx[pr.d];
+    if (pr.q < 0) {
+      int32_t v;
+      if (!ifn_eval(f, x.vt, x.nt, &v)) bad = true;
+      continue;
+    }
+    int32_t c0, k;
+    ifn_linear(f, R + pr.q, x.vt, x.nt, &c0, &k);
+    const int32_t top = f.mode == 1 ? f.s * (f.size - 1) : f.size - 1;
+    int32_t l2, h2;
+    if (k == 1) {
+      l2 = -c0;
+      h2 = top - c0;
+    } else if (k == -1) {
+      l2 = c0 - top;
+      h2 = c0;
+    } else if (k > 0) {
+      l2 = ceil_div(-c0, k);
+      h2 = floor_div(top - c0, k);
+    } else {
+      l2 = ceil_div(c0 - top, -k);
+      h2 = floor_div(c0, -k);
+    }
+    DG_UNROLL
+    for (int q = 0; q < Q; ++q)
+      if (q == pr.q) {
+        lo[q] = l2 > lo[q] ? l2 : lo[q];
+        hi[q] = h2 < hi[q] ? h2 : hi[q];
+      }
+  }
+  if (bad) return 0;
+  uint64_t P = 1;
+  DG_UNROLL
+  for (int q = 0; q < Q; ++q) {
+    const int32_t m = G.step[q];
+    int32_t first = lo[q];
+    if (G.mpair[q] >= 0) {
+      // The exact division c0 + k w = 0 (mod s), as in ap_setup.
+      const DgdPair pr = G.pair[G.mpair[q]];
+      const DgpIFn& f = x.Ps[G.op0 + pr.a].idx[pr.d];
+      int32_t c0, k;
+      ifn_linear(f, R + q, x.vt, x.nt, &c0, &k);
+      const int32_t g = qexact(f.s, m);
+      if (g != 1 && pmod(c0, g) != 0) return 0;
+      if (m > 1) {
+        const int32_t cg = g != 1 ? qexact(c0, g) : c0;
+        // (m is a divisor of the stride: pmod(...) * minv stays below m^2.)
+        const int32_t r = m < 46341 ? pmod(pmod(-cg, m) * G.minv[q], m)
+                                    : (int32_t)(((int64_t)pmod(-cg, m) * G.minv[q]) % m);
+        first = lo[q] + pmod(r - lo[q], m);
+      }
+    }
+    const uint32_t len = first <= hi[q] ? (uint32_t)qpos(hi[q] - first, m) + 1u : 0u;
+    N.first[q] = first;
+    N.len[q] = len;
+    P *= len;
+  }
+  if (P == 0 || !bases) return P;
+  DG_UNROLL
+  for (int a = 0; a < NOP; ++a) N.base[a] = x.T[x.Ps[G.op0 + a].tensor].gid;
+  // Every pair's element index at the first point.
+  for (int pi = 0; pi < np; ++pi) {
+    const DgdPair pr = G.pair[pi];
+    const DgpIFn& f = x.Ps[G.op0 + pr.a].idx[pr.d];
+    int32_t v = 0;
+    if (pr.q < 0) {
+      ifn_eval(f, x.vt, x.nt, &v);
+    } else {
+      int32_t c0, k;
+      ifn_linear(f, R + pr.q, x.vt, x.nt, &c0, &k);
+      int32_t fq = 0;
+      DG_UNROLL
+      for (int q = 0; q < Q; ++q)
+        if (q == pr.q) fq = N.first[q];
+      v = c0 + k * fq;
+      if (f.mode == 1 && f.s != 1) v = qexact(v, f.s);
+    }
+    const uint32_t add = pr.stride * (uint32_t)v;
+    DG_UNROLL
+    for (int a = 0; a < NOP; ++a)
+      if (a == pr.a) N.base[a] += add;
+  }
+  return P;
+}
+
+// Valid points of fast group G at the calling thread's node (registers,
+// no element indices); groups of more than four window variables take
+// ap_setup.
+DGC uint64_t ap_count(const DagCtx& x, const DgdGroup& G, int R, const Slots& S, int j) {
+  switch (G.nwin) {
+    case 0: { NodeAP<0, 1> N; return ap_setup_reg<0, 1>(x, G, R, false, N); }
+    case 1: { NodeAP<1, 1> N; return ap_setup_reg<1, 1>(x, G, R, false, N); }
+    case 2: { NodeAP<2, 1> N; return ap_setup_reg<2, 1>(x, G, R, false, N); }
+    case 3: { NodeAP<3, 1> N; return ap_setup_reg<3, 1>(x, G, R, false, N); }
+    case 4: { NodeAP<4, 1> N; return ap_setup_reg<4, 1>(x, G, R, false, N); }
+    default: return ap_setup(x, G, R, S, j, false);
+  }
 }
 
 // Writes group G's edges for the wave's batch of nodes: lane j's node has
@@ -538,6 +807,274 @@ DGC void node_emit(C& c, const DagCtx& x, const DgdGroup& G, const Slots& S, uin
   }
 }
 
+// Digits of v in the mixed radix len[0..Q) (last digit fastest, the first
+// one unbounded), for v < 2^16.
+template <int Q>
+DGC void digits_q(uint32_t v, const uint32_t* len, uint32_t* dg) {
+  DG_UNROLL
+  for (int q = Q - 1; q >= 1; --q) {
+    uint32_t r;
+    v = small_divmod(v, len[q], &r);
+    dg[q] = r;
+  }
+  if (Q > 0) dg[0] = v;
+}
+
+// The NOP words of one point (the point's operand elements, or their
+// multiplicities) at p (4-byte aligned): one store instruction per point.
+template <class C, int NOP>
+DGC void store_point(C& c, uint32_t* p, const uint32_t* v) {
+  if constexpr (NOP == 2) {
+    c.store2(p, v[0], v[1]);
+  } else if constexpr (NOP == 3) {
+    c.store3(p, v[0], v[1], v[2]);
+  } else {
+    DG_UNROLL
+    for (int a = 0; a < NOP; ++a) c.store_cached(p + a, v[a]);
+  }
+}
+
+// a * b (mod 2^32) for a and b in [-2^23, 2^23) as signed values: one
+// full-rate 24-bit multiply on the device.
+DGC uint32_t mul24(uint32_t a, uint32_t b) {
+#if defined(__HIP_DEVICE_COMPILE__)
+  return (uint32_t)__mul24((int)a, (int)b);
+#else
+  return (uint32_t)((int64_t)(int32_t)a * (int64_t)(int32_t)b);
+#endif
+}
+
+// q = n / d and *r = n % d for n < 64 and 1 <= d <= 64 from m = ceil(2^16 / d):
+// n * m / 2^16 = n / d + n * (m * d - 2^16) / (2^16 d), and the second term
+// stays below 1 / d, so the floor is exact.
+DGC uint32_t div64(uint32_t n, uint32_t d, uint32_t m, uint32_t* r) {
+  const uint32_t q = mul24(n, m) >> 16;
+  *r = n - mul24(q, d);
+  return q;
+}
+
+// Edges of the batch nodes in `mask` (lanes whose node has at least half a
+// wave of points), one node after another, from the registers that
+// ap_setup_reg filled: each node's lengths, element indices, point count
+// and first edge are read from its lane.
+//
+// The bounded digits (all but the first) span B = len[1] * ... * len[Q-1]
+// points.  When B is at most the wave width, the node is covered with the
+// largest multiple of B lanes, W: a lane then keeps its bounded digits at
+// every step and only the first digit advances (by W / B), so each
+// operand's element index advances by a constant (no digit arithmetic per
+// point).  Each lane first derives, for its own node, B, W / B and the
+// reciprocals that split a lane index into digits; a node's lanes then
+// take its digits by multiplications.  Larger B (rare) advance all digits
+// with carries.  A node whose edges all fit the room is written without a
+// check per edge.
+template <class C, int NOP, int Q>
+DGC void node_emit_reg(C& c, const DagCtx& x, const DgdGroup& G, const NodeAP<Q, NOP>& N, uint32_t Pj, uint64_t gpos,
+                       uint64_t mask, const DagOut& o, bool emit, bool append) {
+  if constexpr (Q == 0) return;  // (a group without a window has one point per node: never emitted here)
+  constexpr int QD = Q > 0 ? Q : 1;
+  const int lane = c.lane(), L = c.lanes();
+  uint32_t mult[NOP], as[NOP][QD];
+  bool leaf[NOP], any_nonleaf = false;
+  DG_UNROLL
+  for (int a = 0; a < NOP; ++a) {
+    const DgdOperand& Pa = x.Ps[G.op0 + a];
+    mult[a] = Pa.mult;
+    leaf[a] = x.T[Pa.tensor].leaf != 0;
+    any_nonleaf = any_nonleaf || !leaf[a];
+    DG_UNROLL
+    for (int q = 0; q < Q; ++q) as[a][q] = G.astep[a][q];
+  }
+  // The lane's own node, packed for one broadcast per word: B (0 when above
+  // the wave width) and the bounded lengths (7 bits each, all at most 64
+  // when B is), and the reciprocals ceil(2^16 / d) - 1 of B and of those
+  // lengths (16 bits each).
+  uint32_t mylens = 0, mym[(QD + 1) / 2];
+  {
+    uint64_t b = 1;
+    DG_UNROLL
+    for (int q = 1; q < Q; ++q) b *= N.len[q];
+    const uint32_t B = Pj != 0 && b <= (uint64_t)L ? (uint32_t)b : 0u;
+    mylens = B;
+    uint32_t m[QD];
+    const uint32_t bd = B ? B : 1u;
+    m[0] = (65536u + bd - 1u) / bd - 1u;
+    DG_UNROLL
+    for (int q = 1; q < Q; ++q) {
+      const uint32_t d = B ? N.len[q] : 1u;
+      mylens |= (B ? d : 0u) << (7 * q);
+      m[q] = (65536u + d - 1u) / d - 1u;
+    }
+    DG_UNROLL
+    for (int k = 0; k < (QD + 1) / 2; ++k) mym[k] = m[2 * k] | (2 * k + 1 < Q ? m[2 * k + 1] << 16 : 0u);
+  }
+  while (mask) {
+    const int j = (int)__builtin_ctzll(mask);
+    mask &= mask - 1;
+    uint32_t base[NOP];
+    DG_UNROLL
+    for (int a = 0; a < NOP; ++a) base[a] = c.bcast(N.base[a], j);
+    const uint32_t P = c.bcast(Pj, j);
+    const uint64_t at0 = ((uint64_t)c.bcast((uint32_t)(gpos >> 32), j) << 32) | c.bcast((uint32_t)gpos, j);
+    const bool fits = at0 + (uint64_t)P * NOP <= o.room_edges;
+    uint32_t* eb = o.edges + at0;
+    uint32_t* mb = o.mults + at0;
+    uint32_t child[NOP];
+    const uint32_t lens = c.bcast(mylens, j);
+    const uint32_t B = lens & 127u;
+    if (B != 0) {
+      // Bounded digits of lane % B, first digit lane / B; W = (L / B) * B
+      // (L / B = L * m / 2^16 by the same bound as div64, L <= 64).
+      uint32_t m[QD];
+      DG_UNROLL
+      for (int k = 0; k < (QD + 1) / 2; ++k) {
+        const uint32_t w = c.bcast(mym[k], j);
+        m[2 * k] = (w & 0xFFFFu) + 1u;
+        if (2 * k + 1 < QD) m[2 * k + 1] = (w >> 16) + 1u;
+      }
+      const uint32_t per = ((uint32_t)L * m[0]) >> 16, W = per * B;
+      uint32_t rr;
+      const uint32_t d0 = div64((uint32_t)lane, B, m[0], &rr);
+      DG_UNROLL
+      for (int a = 0; a < NOP; ++a) child[a] = base[a] + mul24(as[a][0], d0);
+      DG_UNROLL
+      for (int q = Q - 1; q >= 1; --q) {
+        uint32_t dq;
+        rr = div64(rr, (lens >> (7 * q)) & 127u, m[q], &dq);
+        DG_UNROLL
+        for (int a = 0; a < NOP; ++a) child[a] += mul24(as[a][q], dq);
+      }
+      uint32_t step[NOP];
+      DG_UNROLL
+      for (int a = 0; a < NOP; ++a) step[a] = as[a][0] * per;
+      const bool act = (uint32_t)lane < W;
+      uint32_t off = (uint32_t)lane * NOP;
+      if (fits && emit && !(append && any_nonleaf)) {
+        for (uint32_t p0 = 0; p0 < P; p0 += W) {
+          if (act && p0 + (uint32_t)lane < P) {
+            store_point<C, NOP>(c, eb + off, child);
+            store_point<C, NOP>(c, mb + off, mult);
+          }
+          DG_UNROLL
+          for (int a = 0; a < NOP; ++a) child[a] += step[a];
+          off += W * NOP;
+        }
+      } else {
+        for (uint32_t p0 = 0; p0 < P; p0 += W) {
+          if (act && p0 + (uint32_t)lane < P) {
+            DG_UNROLL
+            for (int a = 0; a < NOP; ++a) {
+              if (emit && at0 + off + a < o.room_edges) {
+                c.store_cached(&eb[off + a], child[a]);
+                c.store_cached(&mb[off + a], mult[a]);
+              }
+              if (append && !leaf[a]) {
+                const int t = x.Ps[G.op0 + a].tensor;
+                dag_append(c, x.T[t], t, child[a] - x.T[t].gid, x.area, x.cnt, x.err);
+              }
+            }
+          }
+          DG_UNROLL
+          for (int a = 0; a < NOP; ++a) child[a] += step[a];
+          off += W * NOP;
+        }
+      }
+      continue;
+    }
+    // Every digit advances by those of the wave width, with carries: the
+    // element index by a per-node constant plus one correction per carry.
+    uint32_t len[QD];
+    DG_UNROLL
+    for (int q = 0; q < Q; ++q) len[q] = c.bcast(N.len[q], j);
+    uint32_t dg[QD], inc[QD];
+    digits_q<Q>((uint32_t)lane, len, dg);
+    digits_q<Q>((uint32_t)L, len, inc);
+    uint32_t dstep[NOP], corr[NOP][QD];
+    DG_UNROLL
+    for (int a = 0; a < NOP; ++a) {
+      child[a] = base[a];
+      dstep[a] = 0;
+      DG_UNROLL
+      for (int q = 0; q < Q; ++q) {
+        child[a] += as[a][q] * dg[q];
+        dstep[a] += as[a][q] * inc[q];
+        corr[a][q] = q > 0 ? as[a][q - 1] - as[a][q] * len[q] : 0u;
+      }
+    }
+    uint32_t off = (uint32_t)lane * NOP;
+    for (uint32_t p0 = 0; p0 < P; p0 += (uint32_t)L) {
+      if (p0 + (uint32_t)lane < P) {
+        DG_UNROLL
+        for (int a = 0; a < NOP; ++a) {
+          if (emit && (fits || at0 + off + a < o.room_edges)) {
+            c.store_cached(&eb[off + a], child[a]);
+            c.store_cached(&mb[off + a], mult[a]);
+          }
+          if (append && !leaf[a]) {
+            const int t = x.Ps[G.op0 + a].tensor;
+            dag_append(c, x.T[t], t, child[a] - x.T[t].gid, x.area, x.cnt, x.err);
+          }
+        }
+      }
+      uint32_t carry = 0;
+      DG_UNROLL
+      for (int q = Q - 1; q >= 1; --q) {
+        const uint32_t t = dg[q] + inc[q] + carry;
+        carry = t >= len[q] ? 1u : 0u;
+        dg[q] = carry ? t - len[q] : t;
+        DG_UNROLL
+        for (int a = 0; a < NOP; ++a) child[a] += carry ? corr[a][q] : 0u;
+      }
+      DG_UNROLL
+      for (int a = 0; a < NOP; ++a) child[a] += dstep[a];
+      off += (uint32_t)L * NOP;
+    }
+  }
+}
+
+// A fast group of NOP operands and Q window variables for the wave's batch
+// (lane `has` a node, its coordinates in the lane's variables, its first
+// edge of the group at gpos): progressions in registers, the nodes with at
+// least half a wave of points emitted node by node; the others get their
+// slots written and are left to flat_emit (*small: the lane's point count
+// there, 0 otherwise).  Returns the lane's point count.
+template <class C, int NOP, int Q>
+DGC uint32_t fast_group_reg(C& c, const DagCtx& x, const DgdGroup& G, int R, bool has, uint64_t gpos, const Slots& S,
+                            const DagOut& o, bool emit, bool append, uint32_t* small) {
+  const int lane = c.lane(), L = c.lanes();
+  NodeAP<Q, NOP> N{};
+  const uint32_t Pj = has ? (uint32_t)ap_setup_reg<Q, NOP>(x, G, R, true, N) : 0u;
+  const bool big = Q > 0 && Pj >= (uint32_t)((L + 1) / 2);
+  const uint64_t mask = c.ballot(big);
+  if (mask) node_emit_reg<C, NOP, Q>(c, x, G, N, Pj, gpos, mask, o, emit, append);
+  *small = big ? 0u : Pj;
+  if (*small) {
+    DG_UNROLL
+    for (int q = 0; q < Q; ++q) S.len(lane, q) = N.len[q];
+    DG_UNROLL
+    for (int a = 0; a < NOP; ++a) S.base(lane, a) = N.base[a];
+    S.glo(lane) = (uint32_t)gpos;
+    S.ghi(lane) = (uint32_t)(gpos >> 32);
+  }
+  return Pj;
+}
+
+// fast_group_reg for the group's shape; false when it has no compiled form.
+template <class C>
+DGC bool fast_group(C& c, const DagCtx& x, const DgdGroup& G, int R, bool has, uint64_t gpos, const Slots& S,
+                    const DagOut& o, bool emit, bool append, uint32_t* Pj, uint32_t* small) {
+  if (!G.steps24) return false;
+  switch (G.nop * 16 + G.nwin) {
+#define DG_FAST(NOP, Q) \
+  case NOP * 16 + Q: *Pj = fast_group_reg<C, NOP, Q>(c, x, G, R, has, gpos, S, o, emit, append, small); return true;
+    DG_FAST(1, 0) DG_FAST(1, 1) DG_FAST(1, 2) DG_FAST(1, 3) DG_FAST(1, 4)
+    DG_FAST(2, 0) DG_FAST(2, 1) DG_FAST(2, 2) DG_FAST(2, 3) DG_FAST(2, 4)
+    DG_FAST(3, 0) DG_FAST(3, 1) DG_FAST(3, 2) DG_FAST(3, 3) DG_FAST(3, 4)
+#undef DG_FAST
+    default: return false;
+  }
+}
+
 // Node-major emission of the batch nodes in `mask` (lane columns) when the
 // group's shape has a compiled emitter; false when it has none.
 template <class C>
@@ -587,7 +1124,7 @@ DGC uint64_t batch_node_count(C& c, const DagCtx& x, const DgdOp& op, const DgdT
     node_coords(X, F[i], x.vt, x.nt);
     for (int q = 0; q < op.ng; ++q) {
       const DgdGroup& G = x.Gs[op.g0 + q];
-      if (G.fast && G.points > 0) m += ap_setup(x, G, R, S, lane, false) * (uint64_t)G.nop;
+      if (G.fast && G.points > 0) m += ap_count(x, G, R, S, lane) * (uint64_t)G.nop;
     }
   }
   return m;
@@ -613,7 +1150,9 @@ DGC bool dag_op(C& c, const DagCtx& x, const DgdOp& op, uint32_t* NC, const Slot
     return false;
   }
   uint32_t* F = (uint32_t*)(x.area + X.lds);
-  const uint32_t n = sort_unique(c, F, got);
+  // (The node slots are free until the op's edge counts.)
+  uint32_t n = box_unique(c, X, F, got, (uint32_t*)(x.area + x.h->slot_off), (uint32_t)(x.h->slot_words * nt));
+  if (n == ~0u) n = sort_unique(c, F, got);
   if (MODE == DAG_FILL) {
     for (uint32_t i = (uint32_t)tid; i < n; i += (uint32_t)nt)
       if (nb + i < o.room_nodes) c.store(&o.nodes[nb + i], X.gid + F[i]);
@@ -664,20 +1203,27 @@ DGC bool dag_op(C& c, const DagCtx& x, const DgdOp& op, uint32_t* NC, const Slot
         const DgdGroup& G = x.Gs[op.g0 + q];
         if (G.points == 0) continue;
         if (G.fast) {
-          uint32_t Pj = 0;
-          if (has) {
-            node_coords(X, F[i], x.vt, nt);
-            Pj = (uint32_t)ap_setup(x, G, R, S, lane, true);
-            S.glo(lane) = (uint32_t)gpos;
-            S.ghi(lane) = (uint32_t)(gpos >> 32);
+          uint32_t Pj = 0, small = 0;
+          if (has) node_coords(X, F[i], x.vt, nt);
+          if (fast_group(c, x, G, R, has, gpos, S, o, emit, append, &Pj, &small)) {
+            if (c.ballot(small != 0)) {
+              c.wave_sync();
+              flat_emit(c, x, G, S, WP, small, o, emit, append);
+            }
+          } else {
+            if (has) {
+              Pj = (uint32_t)ap_setup(x, G, R, S, lane, true);
+              S.glo(lane) = (uint32_t)gpos;
+              S.ghi(lane) = (uint32_t)(gpos >> 32);
+            }
+            // Nodes with at least half a wave of points node by node, the
+            // others flattened across the lanes.
+            const bool big = Pj >= (uint32_t)((L + 1) / 2);
+            const uint64_t mask = c.ballot(big);
+            c.wave_sync();
+            const bool done = mask != 0 && emit_nodes(c, x, G, S, mask, o, emit, append);
+            flat_emit(c, x, G, S, WP, done && big ? 0u : Pj, o, emit, append);
           }
-          // Nodes with at least half a wave of points node by node, the
-          // others flattened across the lanes.
-          const bool big = Pj >= (uint32_t)((L + 1) / 2);
-          const uint64_t mask = c.ballot(big);
-          c.wave_sync();
-          const bool done = mask != 0 && emit_nodes(c, x, G, S, mask, o, emit, append);
-          flat_emit(c, x, G, S, WP, done && big ? 0u : Pj, o, emit, append);
           gpos += (uint64_t)Pj * (uint64_t)G.nop;
         } else {
           S.glo(lane) = (uint32_t)gpos;

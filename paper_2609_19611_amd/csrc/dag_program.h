@@ -57,9 +57,17 @@ struct DgdOperand {
 };
 
 // One index function of a fast group: operand a, dim d, its window
-// variable q (-1: none).
+// variable q (-1: none), and whether it can bind: 0 when the compiler has
+// shown that it lies in range at every node and window point of the group
+// (then it only enters the element indices, never the progressions or the
+// validity of a node).
+// (32-bit fields: the scalar unit loads dwords, and a narrower field
+// would be read by a vector load, which waits for the wave's stores.)
+// `stride` is the element stride of dim d of operand a's tensor.
 struct DgdPair {
-  int16_t a, d, q, pad;
+  int32_t a, d, q, bind;
+  uint32_t stride;
+  int32_t pad[3];
 };
 
 struct DgdGroup {
@@ -72,7 +80,7 @@ struct DgdGroup {
   int64_t points;  // window points (1 without a window, 0 for an empty window)
   // Fast groups.
   int32_t npair;
-  int32_t pad;
+  int32_t steps24;  // 1: every astep below, read as a signed value, lies in [-2^23, 2^23)
   DgdPair pair[DGD_MAX_PAIRS];
   // Per window variable: the step of its progression, and for a variable
   // with an exact division (v = (c0 + k w) / s), that pair and the inverse
@@ -80,7 +88,7 @@ struct DgdGroup {
   int32_t step[DGD_MAX_WIN];
   int32_t mpair[DGD_MAX_WIN];
   int32_t minv[DGD_MAX_WIN];
-  int32_t pad2;
+  int32_t nbind;  // the pairs that can bind come first: pair[0 .. nbind)
   // Step of each operand's element index per progression step of each
   // variable (mod 2^32).
   uint32_t astep[DGD_MAX_OPERANDS][DGD_MAX_WIN];

@@ -37,6 +37,14 @@ struct HostCtx {
     return 0u;
   }
   uint64_t ballot(bool f) const { return f ? 1u : 0u; }
+  uint32_t bcast(uint32_t v, int) const { return v; }
+  void atomic_or32(uint32_t* p, uint32_t v) const { *p |= v; }
+  void reduce_min32(uint32_t* p, uint32_t v) const {
+    if (v < *p) *p = v;
+  }
+  void reduce_max32(uint32_t* p, uint32_t v) const {
+    if (v > *p) *p = v;
+  }
   uint64_t wave_sum64(uint64_t v) const { return v; }
   uint32_t wave_scan(uint32_t v, uint32_t* total) const {
     *total = v;
@@ -50,6 +58,15 @@ struct HostCtx {
   uint32_t atomic_inc(uint32_t* p) const { return (*p)++; }
   void store(uint32_t* p, uint32_t v) const { *p = v; }
   void store_cached(uint32_t* p, uint32_t v) const { *p = v; }
+  void store2(uint32_t* p, uint32_t a, uint32_t b) const {
+    p[0] = a;
+    p[1] = b;
+  }
+  void store3(uint32_t* p, uint32_t a, uint32_t b, uint32_t c) const {
+    p[0] = a;
+    p[1] = b;
+    p[2] = c;
+  }
   void store(uint64_t* p, uint64_t v) const { *p = v; }
   void reduce_add(uint64_t* p, uint64_t v) const { *p += v; }
   void reduce_max(uint64_t* p, uint64_t v) const {
@@ -218,6 +235,27 @@ int dgh_dag_fill(const char* text, int64_t len, const int64_t* locs, int64_t n, 
 // (op index, 1 if the op is pointwise, 1 if the group is taken per variable,
 // the number of list variables).  Returns the group count (at most cap are
 // written) or a negative status.
+// The frontier dedup over a tensor of the given shape: cand[0..n) made
+// sorted and unique in place through the bounding-box bitmap with ws_words
+// words of scratch; returns the number kept, or -1 when the bitmap does not
+// apply (cand untouched).
+int64_t dgh_box_unique(int rank, const int64_t* shape, uint32_t* cand, uint32_t n, uint32_t ws_words) {
+  DgdTensor X;
+  std::memset(&X, 0, sizeof(X));
+  X.rank = rank;
+  uint64_t st = 1;
+  for (int d = rank - 1; d >= 0; --d) {
+    X.shape[d] = (int32_t)shape[d];
+    X.stride[d] = (uint32_t)st;
+    X.magic[d] = shape[d] <= 1 ? 0 : ~0ull / (uint64_t)shape[d] + 1;
+    st *= (uint64_t)shape[d];
+  }
+  std::vector<uint32_t> ws(ws_words + 1);
+  HostCtx c;
+  const uint32_t k = dgc::box_unique(c, X, cand, n, ws.data(), ws_words);
+  return k == ~0u ? -1 : (int64_t)k;
+}
+
 int dgh_dag_groups(const char* text, int64_t len, int32_t* out, int64_t cap) {
   try {
     dg::GraphIR ir = dg::parse_dgir(std::string(text, (size_t)len));

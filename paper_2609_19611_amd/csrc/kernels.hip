@@ -31,6 +31,27 @@ struct DagDevCtx : DevCtx<BLOCK> {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
   DGC uint64_t ballot(bool f) const { return __ballot(f); }
+  DGC void atomic_or32(uint32_t* p, uint32_t v) const { atomicOr(p, v); }
+  // The minimum (maximum) of v over the wave into *p, one LDS atomic per
+  // wave.
+  DGC void reduce_min32(uint32_t* p, uint32_t v) const {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const uint32_t u = (uint32_t)__shfl_xor((int)v, o, 64);
+      v = u < v ? u : v;
+    }
+    if ((threadIdx.x & 63u) == 0) atomicMin(p, v);
+  }
+  DGC void reduce_max32(uint32_t* p, uint32_t v) const {
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const uint32_t u = (uint32_t)__shfl_xor((int)v, o, 64);
+      v = u > v ? u : v;
+    }
+    if ((threadIdx.x & 63u) == 0) atomicMax(p, v);
+  }
+  // Lane j's v (j the same on every lane).
+  DGC uint32_t bcast(uint32_t v, int j) const { return (uint32_t)__builtin_amdgcn_readlane((int)v, j); }
   // Exclusive count of set flags among lower lanes of the wave, and the
   // wave's total (no barrier).
   DGC uint32_t wave_prefix(bool f, uint32_t* total) const {
@@ -89,6 +110,14 @@ struct DagDevCtx : DevCtx<BLOCK> {
   // (edges at stride `nop`, runs at any alignment), which the L2 merges
   // before writing back; non-temporal stores would send each part to HBM.
   DGC void store_cached(uint32_t* p, uint32_t v) const { *p = v; }
+  // Two or three consecutive words at a 4-byte aligned p, one store
+  // instruction (the hardware needs only dword alignment for them).
+  typedef uint32_t u32x2 __attribute__((ext_vector_type(2), aligned(4)));
+  typedef uint32_t u32x3 __attribute__((ext_vector_type(3), aligned(4)));
+  DGC void store2(uint32_t* p, uint32_t a, uint32_t b) const { *reinterpret_cast<u32x2*>(p) = u32x2{a, b}; }
+  DGC void store3(uint32_t* p, uint32_t a, uint32_t b, uint32_t c) const {
+    *reinterpret_cast<u32x3*>(p) = u32x3{a, b, c};
+  }
 };
 
 // Expression DAGs: the sizes pass writes the node and edge counts of

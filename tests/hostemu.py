@@ -37,7 +37,19 @@ def lib():
         _lib.dgh_dag_sizes.argtypes = [ctypes.c_char_p, i64, P, i64, P, P]
         _lib.dgh_dag_fill.argtypes = [ctypes.c_char_p, i64, P, i64, P, P, P, P, P, P]
         _lib.dgh_dag_groups.argtypes = [ctypes.c_char_p, i64, P, i64]
+        _lib.dgh_box_unique.argtypes = [ctypes.c_int, P, P, ctypes.c_uint32, ctypes.c_uint32]
+        _lib.dgh_box_unique.restype = i64
     return _lib
+
+
+def box_unique(shape, cand, ws_words):
+    """The DAG frontier dedup through the bounding-box bitmap: (sorted unique
+    candidates, True), or (None, False) when the bitmap does not apply."""
+    L = lib()
+    shp = np.ascontiguousarray(np.asarray(shape, dtype=np.int64))
+    c = np.ascontiguousarray(np.asarray(cand, dtype=np.uint32)).copy()
+    k = L.dgh_box_unique(len(shape), shp.ctypes.data, c.ctypes.data, len(c), ws_words)
+    return (c[:k].copy(), True) if k >= 0 else (None, False)
 
 
 def enumerate(text, locs):

@@ -199,3 +199,31 @@ def test_split_k_variant_has_single_term_leaves():
     from paper_2609_19611_amd import binding
     for text in (W.c5_variant_text(), W.c5_variant_text(n=2, c=4, hw=6, co=3)):
         assert binding.dg_graph_info(binding.dg_graph_parse(text))["max_leaf_terms"] == 1
+
+
+@pytest.mark.parametrize("seed", range(12))
+def test_frontier_box_dedup_matches_sorted_unique(seed):
+    """The frontier dedup by bounding-box bitmap gives exactly the sorted
+    set of the candidates (duplicates, one-cell boxes, boxes touching a
+    tensor's edges, rank 1 to 5), and declines when its scratch is short."""
+    rng = np.random.default_rng(seed)
+    rank = int(rng.integers(1, 6))
+    shape = [int(rng.integers(1, 9)) for _ in range(rank)]
+    lo = [int(rng.integers(0, s)) for s in shape]
+    hi = [int(rng.integers(l, s)) + 1 for l, s in zip(lo, shape)]
+    stride = np.cumprod([1] + shape[::-1])[:-1][::-1]
+    n = int(rng.integers(2, 200))
+    coords = np.stack([rng.integers(l, h, size=n) for l, h in zip(lo, hi)], axis=1)
+    cand = (coords * stride).sum(axis=1).astype(np.uint32)
+    want = np.unique(cand)
+    box = int(np.prod([h - l for l, h in zip(lo, hi)]))
+    got, ok = hostemu.box_unique(shape, cand, 16 + 2 * ((box + 31) // 32))
+    assert ok
+    assert got.tolist() == want.tolist()
+    # Scratch for one bitmap word only (16 words hold the box bounds of up
+    # to 8 dims): declined when the candidates' box spans more.
+    vol = np.prod([int(coords[:, d].max() - coords[:, d].min() + 1) for d in range(rank)])
+    got, ok = hostemu.box_unique(shape, cand, 16 + 2)
+    assert ok == (vol <= 32)
+    if ok:
+        assert got.tolist() == want.tolist()
