@@ -1,20 +1,25 @@
 // Run-time specialisation of the per-location kernels (see jit.h).
 #include "jit.h"
 
-#include <hip/hiprtc.h>
+#include <dlfcn.h>
+#include <fcntl.h>
+#include <poll.h>
+#include <pthread.h>
+#include <signal.h>
+#include <spawn.h>
+#include <sys/wait.h>
+#include <unistd.h>
 
+#include <cerrno>
 #include <cstdlib>
 #include <cstring>
 #include <map>
 #include <mutex>
 #include <sstream>
 
-namespace dg {
+extern char** environ;
 
-// Text of program.h, core.h and kernels_dev.h, embedded at build time.
-extern const char* const kJitProgramH;
-extern const char* const kJitCoreH;
-extern const char* const kJitKernelsDevH;
+namespace dg {
 
 namespace {
 
@@ -47,35 +52,121 @@ void remember_code(const std::string& source, const std::vector<char>& code) {  
   }
 }
 
+// The compile helper program beside this library (dirigo_jitc), or empty.
+std::string helper_path() {
+  Dl_info info;
+  if (!dladdr(reinterpret_cast<void*>(&helper_path), &info) || !info.dli_fname) return std::string();
+  std::string p(info.dli_fname);
+  const size_t slash = p.rfind('/');
+  p = (slash == std::string::npos ? std::string(".") : p.substr(0, slash)) + "/dirigo_jitc";
+  return access(p.c_str(), X_OK) == 0 ? p : std::string();
+}
+
+// Compiles `src` in a child process running the helper: the source goes to
+// its stdin, a status byte and the code object (or the log) come back on
+// its stdout.  The child is a separate program image that never touches
+// the GPU; the caller's process only waits for it (at most kHelperSeconds).
+// The pipes are close-on-exec, so a child started by another thread never
+// holds this call's pipe ends; a child that exits early cannot raise
+// SIGPIPE in the caller (blocked during the write, then consumed).
+const int kHelperSeconds = 900;
+
+bool compile_in_helper(const std::string& helper, const std::string& src, std::vector<char>* code,
+                       std::string* log) {
+  int in[2], out[2];
+  if (pipe2(in, O_CLOEXEC) != 0) {
+    *log = "pipe failed";
+    return false;
+  }
+  if (pipe2(out, O_CLOEXEC) != 0) {
+    close(in[0]);
+    close(in[1]);
+    *log = "pipe failed";
+    return false;
+  }
+  posix_spawn_file_actions_t fa;
+  posix_spawn_file_actions_init(&fa);
+  posix_spawn_file_actions_adddup2(&fa, in[0], 0);  // (dup2 leaves the copies inheritable)
+  posix_spawn_file_actions_adddup2(&fa, out[1], 1);
+  char* const argv[] = {const_cast<char*>(helper.c_str()), nullptr};
+  pid_t pid = -1;
+  const int rc = posix_spawn(&pid, helper.c_str(), &fa, nullptr, argv, environ);
+  posix_spawn_file_actions_destroy(&fa);
+  close(in[0]);
+  close(out[1]);
+  if (rc != 0) {
+    close(in[1]);
+    close(out[0]);
+    *log = "cannot start " + helper;
+    return false;
+  }
+  // (The helper reads its whole input before it writes anything.)
+  sigset_t pipe_set, old_set;
+  sigemptyset(&pipe_set);
+  sigaddset(&pipe_set, SIGPIPE);
+  pthread_sigmask(SIG_BLOCK, &pipe_set, &old_set);
+  size_t done = 0;
+  bool broken = false;
+  while (done < src.size()) {
+    const ssize_t w = write(in[1], src.data() + done, src.size() - done);
+    if (w < 0 && errno == EINTR) continue;
+    if (w <= 0) {
+      broken = w < 0 && errno == EPIPE;
+      break;
+    }
+    done += (size_t)w;
+  }
+  close(in[1]);
+  if (broken) {
+    const struct timespec zero = {0, 0};
+    while (sigtimedwait(&pipe_set, nullptr, &zero) < 0 && errno == EINTR) {
+    }
+  }
+  pthread_sigmask(SIG_SETMASK, &old_set, nullptr);
+  std::vector<char> buf;
+  char chunk[1 << 16];
+  bool timed_out = false;
+  for (;;) {
+    struct pollfd pf = {out[0], POLLIN, 0};
+    const int pr = poll(&pf, 1, kHelperSeconds * 1000);
+    if (pr < 0 && errno == EINTR) continue;
+    if (pr == 0) {
+      timed_out = true;
+      kill(pid, SIGKILL);
+      break;
+    }
+    const ssize_t r = read(out[0], chunk, sizeof chunk);
+    if (r < 0 && errno == EINTR) continue;
+    if (r <= 0) break;
+    buf.insert(buf.end(), chunk, chunk + r);
+  }
+  close(out[0]);
+  int status = 0;
+  while (waitpid(pid, &status, 0) < 0 && errno == EINTR) {
+  }
+  const bool ok = !timed_out && done == src.size() && WIFEXITED(status) && WEXITSTATUS(status) == 0 &&
+                  !buf.empty() && buf[0] == 0;
+  if (!ok) {
+    *log = timed_out ? std::string("compile helper timed out")
+                     : buf.size() > 1 ? std::string(buf.begin() + 1, buf.end()) : std::string("compile helper failed");
+    return false;
+  }
+  code->assign(buf.begin() + 1, buf.end());
+  return !code->empty();
+}
+
+// A process that uses PyTorch has its bundled HIP runtime loaded, and with
+// it an older runtime compiler that generates markedly slower code for these
+// kernels; the helper always compiles with the ROCm installation's.  Without
+// the helper (or with DIRIGO_JIT_INPROC=1) the kernels are compiled in
+// process.
 bool compile(const std::string& src, std::vector<char>* code, std::string* log) {
-  hiprtcProgram prog;
-  const char* headers[] = {kJitProgramH, kJitCoreH, kJitKernelsDevH};
-  const char* names[] = {"program.h", "core.h", "kernels_dev.h"};
-  if (hiprtcCreateProgram(&prog, src.c_str(), "dg_plan.hip", 3, headers, names) != HIPRTC_SUCCESS) {
-    *log = "hiprtcCreateProgram failed";
-    return false;
+  const char* e = std::getenv("DIRIGO_JIT_INPROC");
+  if (!(e && std::strcmp(e, "1") == 0)) {
+    static const std::string helper = helper_path();
+    if (!helper.empty()) return compile_in_helper(helper, src, code, log);
   }
-  const char* const* opts = jit_compile_options();
-  int nopt = 0;
-  while (opts[nopt]) ++nopt;
-  hiprtcResult r = hiprtcCompileProgram(prog, nopt, const_cast<const char**>(opts));
-  size_t n = 0;
-  hiprtcGetProgramLogSize(prog, &n);
-  if (n > 1) {
-    std::string l(n, '\0');
-    hiprtcGetProgramLog(prog, &l[0]);
-    *log = l;
-  }
-  if (r != HIPRTC_SUCCESS) {
-    hiprtcDestroyProgram(&prog);
-    return false;
-  }
-  size_t sz = 0;
-  hiprtcGetCodeSize(prog, &sz);
-  code->resize(sz);
-  hiprtcGetCode(prog, code->data());
-  hiprtcDestroyProgram(&prog);
-  return true;
+  return jit_compile_source(src, code, log);
 }
 
 }  // namespace

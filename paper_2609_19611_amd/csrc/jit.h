@@ -27,6 +27,10 @@ std::string jit_compare_source(const Plan& a, const Plan& b, const dgc::PairPlan
 // hipRTC options of the specialised kernels (null-terminated list).
 const char* const* jit_compile_options();
 
+// Compiles one specialised source with the runtime compiler linked into the
+// calling program; true and the code object, or false and the log.
+bool jit_compile_source(const std::string& src, std::vector<char>* code, std::string* log);
+
 }  // namespace dg
 
 #if defined(__HIP_PLATFORM_AMD__) || defined(__HIPCC__)

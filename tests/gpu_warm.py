@@ -4,6 +4,8 @@ of graphs one after another would dominate the tests' run time.  The
 returned handles keep the loaded kernels alive for the caller's scope."""
 
 import concurrent.futures as cf
+import sys
+import time
 
 
 def warm_graphs(B, texts, threads=8):
@@ -13,8 +15,11 @@ def warm_graphs(B, texts, threads=8):
         g = B.dg_graph_parse(text)
         B.enumerate_locations(g, [0])
         return g
+    t0 = time.time()
     with cf.ThreadPoolExecutor(threads) as ex:
-        return list(ex.map(one, texts))
+        out = list(ex.map(one, texts))
+    print(f"[warm] {len(texts)} graphs in {time.time() - t0:.1f} s", file=sys.stderr, flush=True)
+    return out
 
 
 def warm_pairs(B, pairs, threads=8):
@@ -22,5 +27,8 @@ def warm_pairs(B, pairs, threads=8):
     def one(p):
         B.compare_locations(p[0], p[1], [0])
         return p
+    t0 = time.time()
     with cf.ThreadPoolExecutor(threads) as ex:
-        return list(ex.map(one, pairs))
+        out = list(ex.map(one, pairs))
+    print(f"[warm] {len(pairs)} pairs in {time.time() - t0:.1f} s", file=sys.stderr, flush=True)
+    return out

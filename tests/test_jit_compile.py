@@ -105,3 +105,31 @@ def test_comparison_kernel_compiles():
     notes = _kernel_notes(_compile(src))
     assert [n for n, _ in notes] == ["dg_compare"]
     assert all(p == 0 for _, p in notes), notes
+
+
+HELPER = os.path.join(os.path.dirname(CSRC), "lib", "dirigo_jitc")
+
+
+@pytest.mark.skipif(not os.path.exists(HELPER), reason="compile helper not built")
+def test_compile_helper_builds_the_specialised_kernels():
+    """The compile helper the library spawns: a status byte 0 and the code
+    object of a workload's enumeration source on stdout (a kernel named
+    dg_enumerate, no scratch memory); status 1 and the compiler's log for
+    a source that does not compile; and it needs no HIP runtime."""
+    L = hostemu.lib()
+    t = W.CONFIGS["c4"]["text"]().encode()
+    buf = ctypes.create_string_buffer(1 << 24)
+    k = L.dgh_jit_source(t, len(t), 256, buf, len(buf))
+    assert k > 0
+    r = subprocess.run([HELPER], input=buf.value, capture_output=True, timeout=300)
+    assert r.returncode == 0 and r.stdout[:1] == b"\x00"
+    with tempfile.NamedTemporaryFile(suffix=".co") as f:
+        f.write(r.stdout[1:])
+        f.flush()
+        notes = subprocess.run([READELF, "--notes", f.name], capture_output=True, text=True).stdout
+    assert "dg_enumerate" in notes
+    assert all(int(v) == 0 for v in re.findall(r"\.private_segment_fixed_size:\s+(\d+)", notes))
+    bad = subprocess.run([HELPER], input=b"this is not a kernel", capture_output=True, timeout=300)
+    assert bad.returncode == 1 and bad.stdout[:1] == b"\x01" and len(bad.stdout) > 1
+    libs = subprocess.run(["ldd", HELPER], capture_output=True, text=True).stdout
+    assert "libhiprtc" in libs and "libamdhip64" not in libs
