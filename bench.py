@@ -175,6 +175,14 @@ def same_buffer_fill(ids, cnt, stream, steps=5, warmup=2):
     return (ids.numel() * ids.element_size() + cnt.numel() * cnt.element_size()) / (ms * 1e-3) / 1e9
 
 
+def same_buffer_fill_dag(arrays, stream, steps=5, warmup=2):
+    """Write rate of torch's fill over the DAG's own output arrays (nodes,
+    first edges, edges, multiplicities: the same bytes at the same
+    addresses)."""
+    ms = _median_ms(lambda: [a.fill_(7) for a in arrays], steps, warmup, stream)
+    return sum(a.numel() * a.element_size() for a in arrays) / (ms * 1e-3) / 1e9
+
+
 def secondary_enumeration(B, W, name, fill_gbps, steps=10, warmup=3):
     """Single-pass enumeration of another workload: median call time of
     `steps` calls, rates and the HBM fraction (algorithmic bytes)."""
@@ -363,6 +371,8 @@ def dag_bench(args, B, g, cfg, locs, text):
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     fill_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
+    fill_ms_median = float(np.median([a.elapsed_time(b) for a, b in ev]))
+    same = same_buffer_fill_dag((nodes, node_edge, edges, mults), stream)
     # Algorithmic bytes of the fill: 8 (location) + 16 (two offsets) per
     # location, 8 per node (id + first edge), 8 per edge (child + multiplicity).
     alg = 24 * n + 8 * nn + 8 * ne
@@ -379,7 +389,10 @@ def dag_bench(args, B, g, cfg, locs, text):
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": measured_traffic(args.workload, DAG_TRAFFIC_FILE, DAG_SOURCES),
                      "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE x2 + WRITE_SIZE x1)",
-                     "kernel_ms": fill_ms, "algorithmic_bytes": alg},
+                     "kernel_ms": fill_ms, "kernel_ms_median": fill_ms_median, "algorithmic_bytes": alg,
+                     "same_buffer_fill_GBps": same, "frac_of_same_buffer_fill": achieved / same,
+                     "kernels": {1: "specialized", 0: "precompiled", -1: "precompiled"}[
+                         B.dg_graph_info(g)["dag_specialized"]]},
     }
     if not args.no_cpu_baseline:
         import oracle

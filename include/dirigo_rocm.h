@@ -190,6 +190,15 @@ typedef struct {
                                  current device: 1 loaded, 0 off or failed
                                  (the precompiled kernels run the plan),
                                  -1 not used on this device yet */
+  int32_t dag_specialized;    /* expression-DAG kernels specialised for this
+                                 graph on the current device: 1 loaded, 0
+                                 failed or off, -1 none yet (every DAG call
+                                 so far ran the precompiled kernels: by
+                                 default only calls over at least 2^26 edges
+                                 of DAGs of at most 2^16 edges per location
+                                 take them; the environment variable
+                                 DIRIGO_DAG_JIT=1 makes every call take
+                                 them, DIRIGO_DAG_JIT=0 none) */
 } dg_graph_info_t;
 
 dg_status dg_graph_info(const dg_graph* g, dg_graph_info_t* out);

@@ -53,6 +53,7 @@ class GraphInfo(ctypes.Structure):
         ("max_leaf_terms", ctypes.c_int32),
         ("n_tensors", ctypes.c_int32),
         ("specialized", ctypes.c_int32),
+        ("dag_specialized", ctypes.c_int32),
     ]
 
 
@@ -216,6 +217,7 @@ def dg_graph_info(g: Graph) -> dict:
         "max_leaf_terms": info.max_leaf_terms,
         "n_tensors": info.n_tensors,
         "specialized": info.specialized,
+        "dag_specialized": info.dag_specialized,
     }
 
 

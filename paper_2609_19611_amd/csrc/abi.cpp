@@ -48,6 +48,7 @@ struct dg_graph {
   dg::DagProgram dag;
   int dag_block = 256;
   std::map<int, uint8_t*> dev_dag;  // DAG program per device
+  std::map<int, DevKernels> jit_dag;  // specialised DAG kernels per device
 };
 
 namespace {
@@ -239,6 +240,41 @@ const dg::JitModule* graph_jit_wide(const dg_graph* cg) {
   return k.ok ? &k.jm : nullptr;
 }
 
+// When the specialised DAG kernels run a call by default: small DAGs per
+// location (a static bound of at most kDagJitRow edges), whose time goes to
+// per-op and per-group bookkeeping that the specialised kernels fold into
+// constants, in calls of at least kDagJitEdges edges (below that the
+// compile time, seconds once per graph and device, outweighs the gain).
+// Large DAGs per location are bound by their emission loops, where the
+// unrolled kernels run no faster than the precompiled ones.
+constexpr int64_t kDagJitRow = int64_t(1) << 16;
+constexpr double kDagJitEdges = double(1 << 26);
+
+// The specialised DAG kernels of g on the current device for a call over n
+// locations, compiled on first use; nullptr when the precompiled kernels
+// run the call: specialisation off or failed, a call outside the default
+// range above, or more than 64 KiB of LDS per location.  DIRIGO_DAG_JIT=1
+// specialises every call, DIRIGO_DAG_JIT=0 none.  The DAG program must be
+// compiled.
+const dg::JitModule* dag_jit(const dg_graph* cg, int64_t n) {
+  if (!dg::jit_enabled()) return nullptr;
+  dg_graph* g = const_cast<dg_graph*>(cg);
+  const char* env = std::getenv("DIRIGO_DAG_JIT");
+  const int mode = env && env[0] == '1' ? 1 : env && env[0] == '0' ? 0 : -1;
+  if (mode == 0 || g->dag.lds_bytes > 65536u) return nullptr;
+  if (mode < 0 && (g->dag.max_edges > kDagJitRow || (double)n * (double)g->dag.max_edges < kDagJitEdges))
+    return nullptr;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return nullptr;
+  std::lock_guard<std::mutex> lock(g->mu);
+  DevKernels& k = g->jit_dag[dev];
+  if (!k.tried) {
+    k.tried = true;
+    k.ok = dg::jit_load(dg::jit_dag_source(g->dag, g->dag_block), &k.jm, &k.log) && k.jm.dag_sizes && k.jm.dag_fill;
+  }
+  return k.ok ? &k.jm : nullptr;
+}
+
 // Leaf ids of g fit 32 bits.
 bool narrow_ids(const dg_graph* g) { return g->ir.leaf_total <= 0xFFFFFFFFull; }
 
@@ -335,6 +371,7 @@ dg_status device_errors(uint32_t bits) {
   if (bits & DGP_ERR_CAPACITY)
     return set_error(DG_E_CAPACITY, "a per-location factor outgrew its compiled capacity");
   if (bits & DGP_ERR_SIZE) return set_error(DG_E_INVALID_ARG, "offsets do not match this graph and locations");
+  if (bits & DGP_ERR_SHAPE) return set_error(DG_E_HIP, "a specialised DAG kernel lacks code for one of the graph's groups");
   if (bits & DGP_ERR_TIMEOUT) return set_error(DG_E_HIP, "single pass: a predecessor's row size never arrived");
   if (bits & DGP_ERR_BUFFER) return set_error(DG_E_BUFFER, "the rows need more entries than the output buffers hold");
   return DG_OK;
@@ -413,6 +450,7 @@ void dg_graph_destroy(dg_graph* g) {
   if (!g) return;
   for (auto& kv : g->jit) dg::jit_release(&kv.second.jm);
   for (auto& kv : g->jit_wide) dg::jit_release(&kv.second.jm);
+  for (auto& kv : g->jit_dag) dg::jit_release(&kv.second.jm);
   {
     std::lock_guard<std::mutex> lock(g_pair_mu);
     for (auto it = g_pair_jit.begin(); it != g_pair_jit.end();) {
@@ -482,6 +520,16 @@ dg_status dg_graph_info(const dg_graph* g, dg_graph_info_t* out) {
       std::lock_guard<std::mutex> lock(mg->mu);
       auto it = mg->jit.find(dev);
       if (it != mg->jit.end() && it->second.tried) out->specialized = it->second.ok ? 1 : 0;
+    }
+  }
+  out->dag_specialized = dg::jit_enabled() ? -1 : 0;
+  {
+    int dev = 0;
+    if (hipGetDevice(&dev) == hipSuccess) {
+      dg_graph* mg = const_cast<dg_graph*>(g);
+      std::lock_guard<std::mutex> lock(mg->mu);
+      auto it = mg->jit_dag.find(dev);
+      if (it != mg->jit_dag.end() && it->second.tried) out->dag_specialized = it->second.ok ? 1 : 0;
     }
   }
   return DG_OK;
@@ -953,11 +1001,18 @@ dg_status dg_dag_sizes(const dg_graph* g, const int64_t* d_locs, int64_t n, int6
     uint8_t* ws = static_cast<uint8_t*>(d_ws);
     uint32_t* err = reinterpret_cast<uint32_t*>(ws + w.err);
     DG_HIP(dgk::launch_zero(err, s), "zero");
+    const dg::JitModule* jm = dag_jit(g, n);
     DG_HIP(per_location(n, g->dag_block,
                         [&](int64_t first, int64_t m) {
-                          return dgk::launch_dag_sizes(dblob, dgc::LocSrc{d_locs + first, 0}, m,
-                                                       d_node_offsets + first, d_edge_offsets + first, err,
-                                                       g->dag_block, g->dag.lds_bytes, s);
+                          dgc::LocSrc part{d_locs + first, 0};
+                          int64_t* nn = d_node_offsets + first;
+                          int64_t* en = d_edge_offsets + first;
+                          if (jm) {
+                            void* args[] = {&part, &m, &nn, &en, &err};
+                            return launch_module(jm->dag_sizes, m, g->dag_block, g->dag.lds_bytes, s, args);
+                          }
+                          return dgk::launch_dag_sizes(dblob, part, m, nn, en, err, g->dag_block, g->dag.lds_bytes,
+                                                       s);
                         }),
            "DAG sizes kernel");
     int64_t* sums = reinterpret_cast<int64_t*>(ws + w.sums);
@@ -994,12 +1049,19 @@ dg_status dg_dag_fill(const dg_graph* g, const int64_t* d_locs, int64_t n, const
     hipStream_t s = static_cast<hipStream_t>(stream);
     uint32_t* err = reinterpret_cast<uint32_t*>(static_cast<uint8_t*>(d_ws) + ws_layout(n).err);
     DG_HIP(dgk::launch_zero(err, s), "zero");
+    const dg::JitModule* jm = dag_jit(g, n);
     DG_HIP(per_location(n, g->dag_block,
                         [&](int64_t first, int64_t m) {
-                          return dgk::launch_dag_fill(dblob, dgc::LocSrc{d_locs + first, 0}, m,
-                                                      d_node_offsets + first, d_edge_offsets + first, d_nodes,
-                                                      d_node_edge, d_edges, d_mults, err, g->dag_block,
-                                                      g->dag.lds_bytes, s);
+                          dgc::LocSrc part{d_locs + first, 0};
+                          const int64_t* no = d_node_offsets + first;
+                          const int64_t* eo = d_edge_offsets + first;
+                          if (jm) {
+                            void* args[] = {&part, &m, (void*)&no, (void*)&eo, &d_nodes, &d_node_edge, &d_edges,
+                                            &d_mults, &err};
+                            return launch_module(jm->dag_fill, m, g->dag_block, g->dag.lds_bytes, s, args);
+                          }
+                          return dgk::launch_dag_fill(dblob, part, m, no, eo, d_nodes, d_node_edge, d_edges, d_mults,
+                                                      err, g->dag_block, g->dag.lds_bytes, s);
                         }),
            "DAG fill kernel");
     uint32_t bits = 0;

@@ -31,6 +31,35 @@ namespace dgc {
 // ---------------------------------------------------------------------------
 enum : int { DAG_COUNT = 0, DAG_FILL = 1 };
 
+// The ways of taking a group that a kernel carries code for.  The
+// precompiled kernels carry every way; a kernel specialised for one program
+// carries only the ways its groups use, which keeps the per-location code
+// of a large program within the instruction cache.  A group whose way a
+// kernel lacks stops the location with DGP_ERR_SHAPE (the host derives the
+// masks from the same program, so this does not happen).
+//   DG_DAG_FAST  register progressions of nop operands and nwin window
+//                variables: bit (nop - 1) * 5 + nwin (nop 1..3, nwin 0..4)
+//   DG_DAG_NODE  node-major emitters of the other progression groups: bit
+//                (nop - 1) * 4 + nwin - 1 (nop 1..3, nwin 1..4)
+//   DG_DAG_SLOW  progression groups without a register form
+//   DG_DAG_BOX   point-by-point groups
+//   DG_DAG_PW    pointwise ops
+#ifndef DG_DAG_FAST
+#define DG_DAG_FAST 0x7FFFu
+#define DG_DAG_NODE 0xFFFu
+#define DG_DAG_SLOW 1
+#define DG_DAG_BOX 1
+#define DG_DAG_PW 1
+#endif
+// A specialised kernel also defines DG_DAG_NOPS, its program's op count:
+// the walk over the ops and each op's loops over its groups are then
+// unrolled, so that every op and group field is a constant.
+#ifdef DG_DAG_NOPS
+#define DG_DAG_UNROLL _Pragma("unroll")
+#else
+#define DG_DAG_UNROLL
+#endif
+
 struct DagOut {
   uint32_t* nodes;      // node ids (global element ids)
   uint32_t* node_edge;  // first edge of each node, relative to the location's first edge
@@ -1065,8 +1094,14 @@ DGC bool fast_group(C& c, const DagCtx& x, const DgdGroup& G, int R, bool has, u
                     const DagOut& o, bool emit, bool append, uint32_t* Pj, uint32_t* small) {
   if (!G.steps24) return false;
   switch (G.nop * 16 + G.nwin) {
-#define DG_FAST(NOP, Q) \
-  case NOP * 16 + Q: *Pj = fast_group_reg<C, NOP, Q>(c, x, G, R, has, gpos, S, o, emit, append, small); return true;
+#define DG_FAST(NOP, Q)                                                                          \
+  case NOP * 16 + Q:                                                                             \
+    if constexpr (((DG_DAG_FAST) >> ((NOP - 1) * 5 + Q)) & 1u) {                                 \
+      *Pj = fast_group_reg<C, NOP, Q>(c, x, G, R, has, gpos, S, o, emit, append, small);         \
+      return true;                                                                               \
+    } else {                                                                                     \
+      return false;                                                                              \
+    }
     DG_FAST(1, 0) DG_FAST(1, 1) DG_FAST(1, 2) DG_FAST(1, 3) DG_FAST(1, 4)
     DG_FAST(2, 0) DG_FAST(2, 1) DG_FAST(2, 2) DG_FAST(2, 3) DG_FAST(2, 4)
     DG_FAST(3, 0) DG_FAST(3, 1) DG_FAST(3, 2) DG_FAST(3, 3) DG_FAST(3, 4)
@@ -1081,18 +1116,18 @@ template <class C>
 DGC bool emit_nodes(C& c, const DagCtx& x, const DgdGroup& G, const Slots& S, uint64_t mask, const DagOut& o,
                     bool emit, bool append) {
   switch (G.nop * 16 + G.nwin) {
-    case 0x11: node_emit<C, 1, 1>(c, x, G, S, mask, o, emit, append); return true;
-    case 0x12: node_emit<C, 1, 2>(c, x, G, S, mask, o, emit, append); return true;
-    case 0x13: node_emit<C, 1, 3>(c, x, G, S, mask, o, emit, append); return true;
-    case 0x14: node_emit<C, 1, 4>(c, x, G, S, mask, o, emit, append); return true;
-    case 0x21: node_emit<C, 2, 1>(c, x, G, S, mask, o, emit, append); return true;
-    case 0x22: node_emit<C, 2, 2>(c, x, G, S, mask, o, emit, append); return true;
-    case 0x23: node_emit<C, 2, 3>(c, x, G, S, mask, o, emit, append); return true;
-    case 0x24: node_emit<C, 2, 4>(c, x, G, S, mask, o, emit, append); return true;
-    case 0x31: node_emit<C, 3, 1>(c, x, G, S, mask, o, emit, append); return true;
-    case 0x32: node_emit<C, 3, 2>(c, x, G, S, mask, o, emit, append); return true;
-    case 0x33: node_emit<C, 3, 3>(c, x, G, S, mask, o, emit, append); return true;
-    case 0x34: node_emit<C, 3, 4>(c, x, G, S, mask, o, emit, append); return true;
+#define DG_NODE(NOP, Q)                                                \
+  case NOP * 16 + Q:                                                   \
+    if constexpr (((DG_DAG_NODE) >> ((NOP - 1) * 4 + Q - 1)) & 1u) {   \
+      node_emit<C, NOP, Q>(c, x, G, S, mask, o, emit, append);         \
+      return true;                                                     \
+    } else {                                                           \
+      return false;                                                    \
+    }
+    DG_NODE(1, 1) DG_NODE(1, 2) DG_NODE(1, 3) DG_NODE(1, 4)
+    DG_NODE(2, 1) DG_NODE(2, 2) DG_NODE(2, 3) DG_NODE(2, 4)
+    DG_NODE(3, 1) DG_NODE(3, 2) DG_NODE(3, 3) DG_NODE(3, 4)
+#undef DG_NODE
     default: return false;
   }
 }
@@ -1107,11 +1142,15 @@ DGC uint64_t batch_node_count(C& c, const DagCtx& x, const DgdOp& op, const DgdT
   const int lane = c.lane(), L = c.lanes();
   uint64_t m = 0;
   bool any_box = false;
+  DG_DAG_UNROLL
   for (int q = 0; q < op.ng; ++q) any_box = any_box || (!x.Gs[op.g0 + q].fast && x.Gs[op.g0 + q].points > 0);
-  if (any_box) {
+  if constexpr (!DG_DAG_BOX) {
+    if (any_box) *x.err |= DGP_ERR_SHAPE;
+  } else if (any_box) {
     for (uint32_t j = 0; j < (uint32_t)L && b0 + j < n; ++j) {
       node_coords(X, F[b0 + j], x.vt, x.nt);
       uint64_t mj = 0;
+      DG_DAG_UNROLL
       for (int q = 0; q < op.ng; ++q) {
         const DgdGroup& G = x.Gs[op.g0 + q];
         if (!G.fast && G.points > 0) mj += box_group(c, x, G, R, 0, DagOut{}, false, false);
@@ -1122,6 +1161,7 @@ DGC uint64_t batch_node_count(C& c, const DagCtx& x, const DgdOp& op, const DgdT
   const uint32_t i = b0 + (uint32_t)lane;
   if (i < n) {
     node_coords(X, F[i], x.vt, x.nt);
+    DG_DAG_UNROLL
     for (int q = 0; q < op.ng; ++q) {
       const DgdGroup& G = x.Gs[op.g0 + q];
       if (G.fast && G.points > 0) m += ap_count(x, G, R, S, lane) * (uint64_t)G.nop;
@@ -1162,9 +1202,14 @@ DGC bool dag_op(C& c, const DagCtx& x, const DgdOp& op, uint32_t* NC, const Slot
   // lanes) otherwise; a node's first edge is then its batch's offset plus a
   // wave scan of the batch's node counts.
   if (op.pointwise) {
-    for (uint32_t i = (uint32_t)tid; i < n; i += (uint32_t)nt) {
-      node_coords(X, F[i], x.vt, nt);
-      NC[i] = pointwise_node(c, x, op, 0, o, false, false);
+    if constexpr (DG_DAG_PW) {
+      for (uint32_t i = (uint32_t)tid; i < n; i += (uint32_t)nt) {
+        node_coords(X, F[i], x.vt, nt);
+        NC[i] = pointwise_node(c, x, op, 0, o, false, false);
+      }
+    } else {
+      *x.err |= DGP_ERR_SHAPE;
+      return false;
     }
   } else {
     for (uint32_t b0 = (uint32_t)(wv * L); b0 < n; b0 += (uint32_t)(W * L)) {
@@ -1184,11 +1229,13 @@ DGC bool dag_op(C& c, const DagCtx& x, const DgdOp& op, uint32_t* NC, const Slot
   // The edges, and the non-leaf children.
   const bool emit = MODE == DAG_FILL, append = op.nonleaf != 0;
   if (op.pointwise) {
-    for (uint32_t i = (uint32_t)tid; i < n; i += (uint32_t)nt) {
-      if (MODE == DAG_FILL && nb + i < o.room_nodes) c.store(&o.node_edge[nb + i], (uint32_t)(eb + NC[i]));
-      if (emit || append) {
-        node_coords(X, F[i], x.vt, nt);
-        pointwise_node(c, x, op, eb + NC[i], o, emit, append);
+    if constexpr (DG_DAG_PW) {
+      for (uint32_t i = (uint32_t)tid; i < n; i += (uint32_t)nt) {
+        if (MODE == DAG_FILL && nb + i < o.room_nodes) c.store(&o.node_edge[nb + i], (uint32_t)(eb + NC[i]));
+        if (emit || append) {
+          node_coords(X, F[i], x.vt, nt);
+          pointwise_node(c, x, op, eb + NC[i], o, emit, append);
+        }
       }
     }
   } else if (emit || append) {
@@ -1199,6 +1246,7 @@ DGC bool dag_op(C& c, const DagCtx& x, const DgdOp& op, uint32_t* NC, const Slot
       uint32_t tot;
       uint64_t gpos = eb + NC[b0 / (uint32_t)L] + c.wave_scan((uint32_t)m, &tot);
       if (MODE == DAG_FILL && has && nb + i < o.room_nodes) c.store(&o.node_edge[nb + i], (uint32_t)gpos);
+      DG_DAG_UNROLL
       for (int q = 0; q < op.ng; ++q) {
         const DgdGroup& G = x.Gs[op.g0 + q];
         if (G.points == 0) continue;
@@ -1210,7 +1258,7 @@ DGC bool dag_op(C& c, const DagCtx& x, const DgdOp& op, uint32_t* NC, const Slot
               c.wave_sync();
               flat_emit(c, x, G, S, WP, small, o, emit, append);
             }
-          } else {
+          } else if constexpr (DG_DAG_SLOW) {
             if (has) {
               Pj = (uint32_t)ap_setup(x, G, R, S, lane, true);
               S.glo(lane) = (uint32_t)gpos;
@@ -1223,8 +1271,12 @@ DGC bool dag_op(C& c, const DagCtx& x, const DgdOp& op, uint32_t* NC, const Slot
             c.wave_sync();
             const bool done = mask != 0 && emit_nodes(c, x, G, S, mask, o, emit, append);
             flat_emit(c, x, G, S, WP, done && big ? 0u : Pj, o, emit, append);
+          } else {
+            *x.err |= DGP_ERR_SHAPE;
           }
           gpos += (uint64_t)Pj * (uint64_t)G.nop;
+        } else if constexpr (!DG_DAG_BOX) {
+          *x.err |= DGP_ERR_SHAPE;
         } else {
           S.glo(lane) = (uint32_t)gpos;
           S.ghi(lane) = (uint32_t)(gpos >> 32);
@@ -1244,6 +1296,18 @@ DGC bool dag_op(C& c, const DagCtx& x, const DgdOp& op, uint32_t* NC, const Slot
   *nb_ = nb + n;
   *eb_ = eb + total;
   return true;
+}
+
+// Ops K, K-1, ..., 0 of the walk, unrolled (a specialised kernel).
+template <class C, int MODE, int K>
+DGC bool dag_walk(C& c, const DagCtx& x, const DgdOp* O, uint32_t* NC, const Slots& S, uint32_t* WP,
+                  const DagOut& o, uint64_t* nb, uint64_t* eb) {
+  if constexpr (K < 0) {
+    return true;
+  } else {
+    if (!dag_op<C, MODE>(c, x, O[K], NC, S, WP, o, nb, eb)) return false;
+    return dag_walk<C, MODE, K - 1>(c, x, O, NC, S, WP, o, nb, eb);
+  }
 }
 
 // Expression DAG of res(y[loc]).
@@ -1278,8 +1342,12 @@ DGC void location_dag(C& c, const uint8_t* dblob, int64_t loc, uint8_t* area, co
   }
   c.sync();
   uint64_t nb = 0, eb = 0;
+#ifdef DG_DAG_NOPS
+  if (!dag_walk<C, MODE, DG_DAG_NOPS - 1>(c, x, O, NC, S, WP, o, &nb, &eb)) return;
+#else
   for (int k = h->nop - 1; k >= 0; --k)
     if (!dag_op<C, MODE>(c, x, O[k], NC, S, WP, o, &nb, &eb)) return;
+#endif
   *n_nodes = nb;
   *n_edges = eb;
 }

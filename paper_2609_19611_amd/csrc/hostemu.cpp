@@ -281,6 +281,36 @@ int dgh_dag_groups(const char* text, int64_t len, int32_t* out, int64_t cap) {
   }
 }
 
+// Static bounds of a graph's DAG program for blocks of `block` threads:
+// out = {nodes, edges, largest frontier, LDS bytes} of one location.
+int dgh_dag_bounds(const char* text, int64_t len, int block, int64_t* out) {
+  try {
+    dg::GraphIR ir = dg::parse_dgir(std::string(text, (size_t)len));
+    dg::DagProgram p = dg::compile_dag(ir, block);
+    out[0] = p.max_nodes;
+    out[1] = p.max_edges;
+    out[2] = p.max_frontier;
+    out[3] = (int64_t)p.lds_bytes;
+    return 0;
+  } catch (const dg::Failure& e) {
+    return fail_with(e);
+  }
+}
+
+// Source of the specialised expression-DAG kernels of a graph (its DAG
+// program for blocks of `block` threads).
+int dgh_jit_dag_source(const char* text, int64_t len, int block, char* out, int64_t cap) {
+  try {
+    dg::GraphIR ir = dg::parse_dgir(std::string(text, (size_t)len));
+    dg::DagProgram p = dg::compile_dag(ir, block);
+    std::string s = dg::jit_dag_source(p, block);
+    snprintf(out, (size_t)cap, "%s", s.c_str());
+    return (int)s.size();
+  } catch (const dg::Failure& e) {
+    return fail_with(e);
+  }
+}
+
 // Source of the specialised 64-bit enumeration kernel of a graph.
 int dgh_jit_wide_source(const char* text, int64_t len, int block, char* out, int64_t cap) {
   try {

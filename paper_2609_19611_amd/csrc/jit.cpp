@@ -222,7 +222,8 @@ bool jit_load(const std::string& source, JitModule* out, std::string* log) {
   }
   out->dev = dev;
   out->source = source;
-  // A module holds either the enumeration kernels or the comparison kernel;
+  // A module holds the enumeration kernels, the comparison kernel or the
+  // DAG kernels;
   // a name it lacks leaves a null function.  The failed lookup also sets
   // the thread's last HIP error, which is cleared here so that it is not
   // reported by the next launch check.
@@ -237,6 +238,8 @@ bool jit_load(const std::string& source, JitModule* out, std::string* log) {
   get("dg_enumerate", &out->enumerate);
   get("dg_compare", &out->compare);
   get("dg_enumerate_wide", &out->enumerate_wide);
+  get("dg_dag_sizes", &out->dag_sizes);
+  get("dg_dag_fill", &out->dag_fill);
   return true;
 }
 

@@ -10,16 +10,19 @@
 
 namespace dg {
 
-// Text of program.h, core.h and kernels_dev.h, embedded at build time.
+// Text of the device headers, embedded at build time.
 extern const char* const kJitProgramH;
 extern const char* const kJitCoreH;
 extern const char* const kJitKernelsDevH;
+extern const char* const kJitDagProgramH;
+extern const char* const kJitDagCoreH;
+extern const char* const kJitDagDevH;
 
 bool jit_compile_source(const std::string& src, std::vector<char>* code, std::string* log) {
   hiprtcProgram prog;
-  const char* headers[] = {kJitProgramH, kJitCoreH, kJitKernelsDevH};
-  const char* names[] = {"program.h", "core.h", "kernels_dev.h"};
-  if (hiprtcCreateProgram(&prog, src.c_str(), "dg_plan.hip", 3, headers, names) != HIPRTC_SUCCESS) {
+  const char* headers[] = {kJitProgramH, kJitCoreH, kJitKernelsDevH, kJitDagProgramH, kJitDagCoreH, kJitDagDevH};
+  const char* names[] = {"program.h", "core.h", "kernels_dev.h", "dag_program.h", "dag_core.h", "dag_dev.h"};
+  if (hiprtcCreateProgram(&prog, src.c_str(), "dg_plan.hip", 6, headers, names) != HIPRTC_SUCCESS) {
     *log = "hiprtcCreateProgram failed";
     return false;
   }

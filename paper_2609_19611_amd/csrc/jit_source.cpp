@@ -3,6 +3,7 @@
 #include <cstring>
 #include <sstream>
 
+#include "dag_program.h"
 #include "jit.h"
 
 namespace dg {
@@ -82,6 +83,54 @@ std::string jit_compare_source(const Plan& a, const Plan& b, const dgc::PairPlan
     << "    uint64_t limit, uint32_t* __restrict__ err) {\n"
     << "  dgk_dev::compare_body<DG_B>(dg_plan_a, dg_plan_b, (const dgc::PairPlan*)dg_pair, locs, n, status, flags,"
        " found, limit, err);\n}\n";
+  return o.str();
+}
+
+std::string jit_dag_source(const DagProgram& p, int block) {
+  const DgdHeader* h = reinterpret_cast<const DgdHeader*>(p.blob.data());
+  const DgdOp* O = reinterpret_cast<const DgdOp*>(p.blob.data() + h->op_off);
+  const DgdGroup* G = reinterpret_cast<const DgdGroup*>(p.blob.data() + h->group_off);
+  // The ways of taking a group that the program's groups use (dag_core.h).
+  unsigned fast = 0, node = 0;
+  int slow = 0, box = 0, pw = 0;
+  for (int k = 0; k < h->nop; ++k) {
+    if (O[k].pointwise) {
+      pw = 1;
+      continue;
+    }
+    for (int q = 0; q < O[k].ng; ++q) {
+      const DgdGroup& g = G[O[k].g0 + q];
+      if (g.points == 0) continue;
+      if (!g.fast) {
+        box = 1;
+      } else if (g.steps24 && g.nop >= 1 && g.nop <= 3 && g.nwin >= 0 && g.nwin <= 4) {
+        fast |= 1u << ((g.nop - 1) * 5 + g.nwin);
+      } else {
+        slow = 1;
+        if (g.nop >= 1 && g.nop <= 3 && g.nwin >= 1 && g.nwin <= 4) node |= 1u << ((g.nop - 1) * 4 + g.nwin - 1);
+      }
+    }
+  }
+  std::ostringstream o;
+  o << "#define DG_JIT 1\n"
+    << "#define DGC __device__ __forceinline__\n"
+    << "#define DG_DAG_FAST " << fast << "u\n"
+    << "#define DG_DAG_NODE " << node << "u\n"
+    << "#define DG_DAG_SLOW " << slow << "\n"
+    << "#define DG_DAG_BOX " << box << "\n"
+    << "#define DG_DAG_PW " << pw << "\n"
+    << "#define DG_DAG_NOPS " << h->nop << "\n"
+    << "#include \"dag_dev.h\"\n";
+  emit_bytes(o, "dg_dag", p.blob);
+  o << "#define DG_B " << block << "\n"
+    << "extern \"C\" __global__ __launch_bounds__(DG_B) void dg_dag_sizes(dgc::LocSrc locs, int64_t n,\n"
+    << "    int64_t* __restrict__ nodes_n, int64_t* __restrict__ edges_n, uint32_t* __restrict__ err) {\n"
+    << "  dgk_dev::dag_sizes_body<DG_B>(dg_dag, locs, n, nodes_n, edges_n, err);\n}\n"
+    << "extern \"C\" __global__ __launch_bounds__(DG_B) void dg_dag_fill(dgc::LocSrc locs, int64_t n,\n"
+    << "    const int64_t* __restrict__ node_off, const int64_t* __restrict__ edge_off, uint32_t* __restrict__ nodes,\n"
+    << "    uint32_t* __restrict__ node_edge, uint32_t* __restrict__ edges, uint32_t* __restrict__ mults,\n"
+    << "    uint32_t* __restrict__ err) {\n"
+    << "  dgk_dev::dag_fill_body<DG_B>(dg_dag, locs, n, node_off, edge_off, nodes, node_edge, edges, mults, err);\n}\n";
   return o.str();
 }
 

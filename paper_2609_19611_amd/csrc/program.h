@@ -151,3 +151,4 @@ struct DgpHeader {
 #define DGP_ERR_SIZE 8u       // fill found a row size different from the sizes pass
 #define DGP_ERR_BUFFER 16u    // single pass: the rows do not fit the output buffers
 #define DGP_ERR_TIMEOUT 32u   // single pass: a predecessor's row size never arrived
+#define DGP_ERR_SHAPE 64u     // a specialised DAG kernel lacks the code for one of its program's groups

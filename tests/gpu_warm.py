@@ -32,3 +32,18 @@ def warm_pairs(B, pairs, threads=8):
         out = list(ex.map(one, pairs))
     print(f"[warm] {len(pairs)} pairs in {time.time() - t0:.1f} s", file=sys.stderr, flush=True)
     return out
+
+
+def warm_dags(B, texts, threads=8):
+    """The same for expression DAGs: parses each text and takes one
+    location's DAG (which compiles and loads its DAG kernels, specialised
+    when DIRIGO_DAG_JIT=1); returns the graph handles."""
+    def one(text):
+        g = B.dg_graph_parse(text)
+        B.dag_locations(g, [0])
+        return g
+    t0 = time.time()
+    with cf.ThreadPoolExecutor(threads) as ex:
+        out = list(ex.map(one, texts))
+    print(f"[warm] {len(texts)} DAG programs in {time.time() - t0:.1f} s", file=sys.stderr, flush=True)
+    return out

@@ -31,6 +31,8 @@ def lib():
         _lib.dgh_compare.argtypes = [ctypes.c_char_p, i64, ctypes.c_char_p, i64, P, i64, P]
         _lib.dgh_jit_source.argtypes = [ctypes.c_char_p, i64, ctypes.c_int, ctypes.c_char_p, i64]
         _lib.dgh_jit_wide_source.argtypes = [ctypes.c_char_p, i64, ctypes.c_int, ctypes.c_char_p, i64]
+        _lib.dgh_jit_dag_source.argtypes = [ctypes.c_char_p, i64, ctypes.c_int, ctypes.c_char_p, i64]
+        _lib.dgh_dag_bounds.argtypes = [ctypes.c_char_p, i64, ctypes.c_int, P]
         _lib.dgh_jit_compare_source.argtypes = [ctypes.c_char_p, i64, ctypes.c_char_p, i64, ctypes.c_int,
                                                 ctypes.c_char_p, i64]
         _lib.dgh_jit_options.argtypes = [ctypes.c_char_p, i64]
@@ -102,6 +104,17 @@ def dag_groups(text):
     if k < 0:
         raise HostEmuError(k, L.dgh_error().decode())
     return [tuple(int(v) for v in r) for r in out[:k]]
+
+
+def dag_bounds(text, block=64):
+    """Static bounds of one location's DAG: (nodes, edges, largest frontier,
+    LDS bytes)."""
+    out = np.zeros(4, dtype=np.int64)
+    t = text.encode()
+    rc = lib().dgh_dag_bounds(t, len(t), block, out.ctypes.data)
+    if rc:
+        raise HostEmuError(rc, lib().dgh_error().decode())
+    return tuple(int(v) for v in out)
 
 
 def compare(text_a, text_b, locs):

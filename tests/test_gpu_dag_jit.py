@@ -1,0 +1,82 @@
+"""GPU parity of the specialised expression-DAG kernels (each DAG program
+compiled at run time with its ops walked unrolled and only the ways of
+taking a group that it uses) against the oracle, element by element,
+through the C ABI: every location of the catalogue graphs, samples of the
+five workloads, c5's variant and faults.  DIRIGO_DAG_JIT=1 makes every
+call take them (by default only large calls do)."""
+
+import os
+
+import numpy as np
+import pytest
+import torch
+
+import gpu_warm
+import oracle
+import tiny_graphs
+from paper_2609_19611_amd import workloads as W
+
+pytestmark = pytest.mark.gpu
+
+KEYS = ("node_offsets", "edge_offsets", "nodes", "node_edge", "edges", "mults")
+CAT = {**{k: v[0] for k, v in tiny_graphs.catalogue().items()}, **tiny_graphs.dag_catalogue()}
+WORK = {name: W.CONFIGS[name]["text"]() for name in ("c1", "c2", "c3", "c4", "c5")}
+C5 = [W.c5_variant_text()] + [W.c5_variant_text(fault=f) for f in W.c5_faults()]
+
+
+@pytest.fixture(scope="module")
+def B():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_19611_amd import binding
+    return binding
+
+
+@pytest.fixture(scope="module")
+def graphs(B):
+    """Handles of every graph here, their specialised DAG kernels compiled
+    (several at once) and kept loaded for the module."""
+    old = os.environ.get("DIRIGO_DAG_JIT")
+    os.environ["DIRIGO_DAG_JIT"] = "1"
+    texts = list(CAT.values()) + list(WORK.values()) + C5
+    handles = gpu_warm.warm_dags(B, texts)
+    yield dict(zip(texts, handles))
+    if old is None:
+        del os.environ["DIRIGO_DAG_JIT"]
+    else:
+        os.environ["DIRIGO_DAG_JIT"] = old
+
+
+def test_specialised_dag_kernels_loaded(B, graphs):
+    assert all(B.dg_graph_info(g)["dag_specialized"] == 1 for g in graphs.values())
+
+
+def _check(B, g, text, locs):
+    d = B.dag_locations(g, locs)
+    want = oracle.Graph(text).dag(locs, threads=16)
+    for k in KEYS:
+        a = d[k].cpu().numpy()
+        a = a if a.dtype == np.int64 else a.view(np.uint32).astype(np.uint64)
+        assert np.array_equal(a, want[k]), k
+
+
+@pytest.mark.parametrize("name", sorted(CAT))
+def test_specialised_dag_catalogue(B, graphs, name):
+    text = CAT[name]
+    n = oracle.Graph(text).output_numel
+    _check(B, graphs[text], text, list(range(n))[::-1])
+
+
+@pytest.mark.parametrize("name,step", [("c1", 1), ("c2", 1), ("c3", 1024), ("c4", 64), ("c5", 256)])
+def test_specialised_dag_workloads(B, graphs, name, step):
+    text = WORK[name]
+    _check(B, graphs[text], text, W.config_locations(name)[::step])
+
+
+def test_specialised_dag_c5_variants(B, graphs):
+    locs = W.config_locations("c5")[::4096]
+    N, C, H, Wd = 64, 128, 64, 64
+    edges = [((n * C + c) * H + h) * Wd + w for n in (0, N - 1) for c in (0, C - 1)
+             for h in (0, 1, H - 2, H - 1) for w in (0, 1, Wd - 2, Wd - 1)]
+    for text in C5:
+        _check(B, graphs[text], text, locs + edges)

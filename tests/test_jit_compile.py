@@ -37,12 +37,12 @@ def _rtc():
 
 def _compile(src):
     L = _rtc()
-    names = ["program.h", "core.h", "kernels_dev.h"]
+    names = ["program.h", "core.h", "kernels_dev.h", "dag_program.h", "dag_core.h", "dag_dev.h"]
     texts = [open(os.path.join(CSRC, n), "rb").read() for n in names]
-    hdr = (ctypes.c_char_p * 3)(*texts)
-    nm = (ctypes.c_char_p * 3)(*[n.encode() for n in names])
+    hdr = (ctypes.c_char_p * len(names))(*texts)
+    nm = (ctypes.c_char_p * len(names))(*[n.encode() for n in names])
     prog = ctypes.c_void_p()
-    assert L.hiprtcCreateProgram(ctypes.byref(prog), src.encode(), b"dg_plan.hip", 3, hdr, nm) == 0
+    assert L.hiprtcCreateProgram(ctypes.byref(prog), src.encode(), b"dg_plan.hip", len(names), hdr, nm) == 0
     buf = ctypes.create_string_buffer(4096)
     hostemu.lib().dgh_jit_options(buf, 4096)
     opts = buf.value.decode().split()
@@ -107,6 +107,18 @@ def test_comparison_kernel_compiles():
     assert all(p == 0 for _, p in notes), notes
 
 
+@pytest.mark.parametrize("name,block", [("c3", 256), ("c5", 64)])
+def test_dag_kernels_compile(name, block):
+    """The specialised DAG kernels of a workload compile, carry only the
+    ways of taking a group that its program uses, and use no scratch."""
+    t = W.CONFIGS[name]["text"]().encode()
+    src = _source(hostemu.lib().dgh_jit_dag_source, t, len(t), block)
+    assert "#define DG_DAG_BOX 0" in src and "#define DG_DAG_NOPS" in src
+    notes = _kernel_notes(_compile(src))
+    assert sorted(n for n, _ in notes) == ["dg_dag_fill", "dg_dag_sizes"]
+    assert all(p == 0 for _, p in notes), notes
+
+
 HELPER = os.path.join(os.path.dirname(CSRC), "lib", "dirigo_jitc")
 
 
@@ -133,3 +145,18 @@ def test_compile_helper_builds_the_specialised_kernels():
     assert bad.returncode == 1 and bad.stdout[:1] == b"\x01" and len(bad.stdout) > 1
     libs = subprocess.run(["ldd", HELPER], capture_output=True, text=True).stdout
     assert "libhiprtc" in libs and "libamdhip64" not in libs
+
+
+def test_dag_specialisation_range():
+    """By default the specialised DAG kernels run calls over small DAGs per
+    location (a static bound of at most 2^16 edges) of at least 2^26 edges
+    in all: the conv2d pair check's 1,048,576 DAGs are in that range; the
+    large per-location DAGs of the GEMM + GroupNorm and conv-transpose +
+    softmax workloads, and the 4,096 small DAGs of the conv2d + pool
+    workload, are not."""
+    def bound(name):
+        return hostemu.dag_bounds(W.CONFIGS[name]["text"](), 64)[1]
+    n = {name: len(W.config_locations(name)) for name in ("c2", "c5")}
+    assert bound("c5") <= 1 << 16 and n["c5"] * bound("c5") >= 1 << 26
+    assert bound("c3") > 1 << 16 and bound("c4") > 1 << 16
+    assert n["c2"] * bound("c2") < 1 << 26
