@@ -272,12 +272,37 @@ def c5_faults(seed: int = 5, count: int = 16):
     return [space[i] for i in picked]
 
 
+# Sparse faults of the split-K variant: one index map of split 0 changed so
+# that only boundary locations of the output read differently (the
+# low-prevalence bugs the boundary tiers of the order target), 1/64 of the
+# output each.
+#   "last-row": x's row index o1+w0-1 becomes ((H+1)o1 + H w0 - (H-1)) // H,
+#     equal to it except at the last output row (o1 = H-1), where it is one
+#     more;
+#   "last-col": the same for the column index o2+w1-1 and the last output
+#     column (o2 = W-1).
+# (A fault confined to the last row and column together needs one index map
+# over both output coordinates, which couples the h and w dims; its merged
+# view outgrows the LDS of one location.)
+C5_SPARSE_FAULTS = ("last-row", "last-col")
+
+
+def _sparse_index(kind: str, hw: int) -> tuple[int, str]:
+    """(position in x's index maps, the faulty expression) of a sparse fault."""
+    if kind == "last-row":
+        return 1, f"({hw + 1}*o1+{hw}*w0-{hw - 1})//{hw}"
+    if kind == "last-col":
+        return 2, f"({hw + 1}*o2+{hw}*w1-{hw - 1})//{hw}"
+    raise ValueError(kind)
+
+
 def c5_variant_text(fault=None, n=64, c=64, hw=64, co=128, splits=C5_SPLITS) -> str:
     """The channels-last, split-K form of the C5 reference program: x and W
     are permuted to NHWC / (O, kh, kw, I), the K = 9*C reduction is split into
     ``splits`` contiguous flat ranges computed by separate gather kernels,
     then summed, biased, scaled and shifted in NHWC, and permuted back.
-    ``fault`` = (split, dim, kind) perturbs one index map of one split."""
+    ``fault`` = (split, dim, kind) perturbs one index map of one split; a
+    name from C5_SPARSE_FAULTS applies that sparse fault to split 0."""
     k_total = 9 * c
     if k_total % splits:
         raise ValueError("K must split evenly")
@@ -294,7 +319,11 @@ def c5_variant_text(fault=None, n=64, c=64, hw=64, co=128, splits=C5_SPLITS) -> 
     for s in range(splits):
         xc = list(_C5_XC)
         wc = list(_C5_WC)
-        if fault is not None and fault[0] == s:
+        if isinstance(fault, str):
+            if s == 0:
+                pos, expr = _sparse_index(fault, hw)
+                xc[pos] = expr
+        elif fault is not None and fault[0] == s:
             _, dim, kind = fault
             if dim == "xc-h":
                 xc[1] = _fault_expr(xc[1], kind)

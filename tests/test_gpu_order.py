@@ -85,3 +85,45 @@ def test_order_locations_c5_variant_full(B):
     perm = perm[~np.isin(perm, prefix)]
     k = len(prefix)
     assert np.array_equal(order[k: k + len(perm)].cpu().numpy(), perm)
+
+
+@pytest.mark.parametrize("kind", W.C5_SPARSE_FAULTS)
+def test_sparse_fault_found_first_by_the_order(B, kind):
+    """A sparse fault of the c5 split-K variant (split 0 reads a shifted row
+    at the last output row only, or a shifted column at the last output
+    column only): the GPU comparison over all 33,554,432 output locations
+    mismatches exactly at those locations (for the column fault, not at the
+    first row: split 0 reads only kernel row 0, which lies in the padding
+    there), the oracle agrees there and on a sample of the rest (their
+    neighbours included), and the location order reaches a mismatch within
+    its prefix, no later than the plain permutation or sequential order."""
+    dev = torch.device("cuda", 0)
+    ref_t, var_t = W.c5_reference_text(), W.c5_variant_text(fault=kind)
+    ref, var = B.dg_graph_parse(ref_t), B.dg_graph_parse(var_t)
+    N, C, H, Wd = 64, 128, 64, 64
+    n = N * C * H * Wd
+    status = torch.empty(n, dtype=torch.uint8, device=dev)
+    mism = torch.empty(n, dtype=torch.int64, device=dev)
+    ws = torch.empty(max(B.dg_workspace_size(ref, n), B.dg_workspace_size(var, n)), dtype=torch.uint8, device=dev)
+    k = B.dg_compare_range(ref, var, 0, n, status, mism, ws)
+    st = status.cpu().numpy()
+    h = (np.arange(n) // Wd) % H
+    w = np.arange(n) % Wd
+    want = (h == H - 1) if kind == "last-row" else (w == Wd - 1) & (h >= 1)
+    assert np.array_equal(st != 0, want) and k == int(want.sum())
+    rng = np.random.default_rng(7)
+    hit = np.nonzero(want)[0]
+    near = np.nonzero(((h == H - 2) | (h == 0) | (w == Wd - 2) | (w == Wd - 1)) & ~want)[0]
+    sample = np.unique(np.concatenate([rng.choice(hit, min(len(hit), 4096), replace=False),
+                                       rng.choice(near, 2048, replace=False),
+                                       rng.integers(0, n, 4096)]))
+    o = oracle.compare(oracle.Graph(ref_t), oracle.Graph(var_t), sample.tolist(), threads=16)
+    assert np.array_equal(o, st[sample])
+
+    def first(order):
+        pos = np.nonzero(want[order])[0]
+        return int(pos[0])
+    heur = B.order_locations(var, 5).cpu().numpy()
+    perm = oracle.permutation(n, 5, 0, n)
+    r_h, r_p, r_s = first(heur), first(perm), first(np.arange(n))
+    assert r_h < len(B.dg_order_prefix(var)) and r_h <= r_p and r_h <= r_s, (r_h, r_p, r_s)
