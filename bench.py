@@ -124,8 +124,8 @@ def write_sweep(steps, warmup):
 
 KERNEL_SOURCES = ["program.h", "core.h", "kernels_dev.h", "jit_source.cpp", "jit.cpp", "compile.cpp", "graph.cpp"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "dg_enumerate_hbm_traffic.txt")
-DAG_SOURCES = ["program.h", "core.h", "kernels_dev.h", "dag_program.h", "dag_core.h", "dag.cpp", "kernels.hip",
-               "graph.cpp"]
+DAG_SOURCES = ["program.h", "core.h", "kernels_dev.h", "dag_program.h", "dag_core.h", "dag_dev.h", "dag.cpp",
+               "kernels.hip", "jit_source.cpp", "jit.cpp", "graph.cpp"]
 DAG_TRAFFIC_FILE = os.path.join(ROOT, "profiles", "dg_dag_fill_hbm_traffic.txt")
 
 
@@ -373,6 +373,7 @@ def dag_bench(args, B, g, cfg, locs, text):
     fill_ms = float(np.mean([a.elapsed_time(b) for a, b in ev]))
     fill_ms_median = float(np.median([a.elapsed_time(b) for a, b in ev]))
     same = same_buffer_fill_dag((nodes, node_edge, edges, mults), stream)
+    kinds = "specialized" if B.dg_graph_info(g)["dag_specialized"] == 1 else "precompiled"
     # Algorithmic bytes of the fill: 8 (location) + 16 (two offsets) per
     # location, 8 per node (id + first edge), 8 per edge (child + multiplicity).
     alg = 24 * n + 8 * nn + 8 * ne
@@ -385,15 +386,15 @@ def dag_bench(args, B, g, cfg, locs, text):
         "data": "synthetic (shapes only; footprints are data independent)",
         "config": {"workload": f"{args.workload}: " + cfg["desc"] + " (expression DAGs)", "locations": n,
                    "nodes_per_step": nn, "edges_per_step": ne, "locations_per_s": n / (elapsed / args.steps)},
-        "roofline": {"bound": "hbm", "kernel": "k_dag_fill", "achieved": achieved, "peak": HBM_PEAK_GBS,
+        "roofline": {"bound": "hbm", "kernel": "dg_dag_fill" if kinds == "specialized" else "k_dag_fill",
+                     "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": measured_traffic(args.workload, DAG_TRAFFIC_FILE, DAG_SOURCES),
                      "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE x2 + WRITE_SIZE x1)",
                      "kernel_ms": fill_ms_median, "kernel_ms_mean": fill_ms,
                      "kernel_ms_statistic": f"median of {args.steps} launches", "algorithmic_bytes": alg,
                      "same_buffer_fill_GBps": same, "frac_of_same_buffer_fill": achieved / same,
-                     "kernels": {1: "specialized", 0: "precompiled", -1: "precompiled"}[
-                         B.dg_graph_info(g)["dag_specialized"]]},
+                     "kernels": kinds},
     }
     if not args.no_cpu_baseline:
         import oracle
