@@ -175,6 +175,30 @@ def same_buffer_fill(ids, cnt, stream, steps=5, warmup=2):
     return (ids.numel() * ids.element_size() + cnt.numel() * cnt.element_size()) / (ms * 1e-3) / 1e9
 
 
+def row_fill(ids, cnt, offsets, n, block, lds, stream, steps=5, warmup=2):
+    """Write rate of a kernel that writes the same rows with no per-location
+    work (the enumeration's grid, block size, LDS per block and lane shifts;
+    lib/libdirigo_rowfill, a measurement reference built beside the
+    library), or None when it is not built.  Plain fills run in address
+    order; a one-block-per-row writer of these rows is what this figure
+    times."""
+    import ctypes
+    path = os.path.join(ROOT, "paper_2609_19611_amd", "lib", "libdirigo_rowfill.so")
+    if not os.path.exists(path):
+        return None
+    L = ctypes.CDLL(path)
+    L.dgr_row_fill.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int64, ctypes.c_int,
+                               ctypes.c_uint32, ctypes.c_void_p]
+
+    def call():
+        rc = L.dgr_row_fill(ids.data_ptr(), cnt.data_ptr(), offsets.data_ptr(), n, block, lds,
+                            ctypes.c_void_p(stream.cuda_stream))
+        if rc:
+            raise RuntimeError(f"dgr_row_fill failed: {rc}")
+    ms = _median_ms(call, steps, warmup, stream)
+    return (ids.numel() * ids.element_size() + cnt.numel() * cnt.element_size()) / (ms * 1e-3) / 1e9
+
+
 def same_buffer_fill_dag(arrays, stream, steps=5, warmup=2):
     """Write rate of torch's fill over the DAG's own output arrays (nodes,
     first edges, edges, multiplicities: the same bytes at the same
@@ -201,13 +225,16 @@ def secondary_enumeration(B, W, name, fill_gbps, steps=10, warmup=3):
     alg = 16 * n + 8 * total
     gbps = alg / (ms * 1e-3) / 1e9
     same = same_buffer_fill(ids, cnt, stream)
+    info = B.dg_graph_info(g)
+    rows = row_fill(ids, cnt, off, n, info["block_threads"], info["lds_bytes"], stream)
     del ids, cnt
     torch.cuda.empty_cache()
     return {"workload": f"{name}: " + W.CONFIGS[name]["desc"], "locations": n, "entries": total,
             "ms_per_call": ms, "statistic": f"median of {steps} calls (dg_enumerate, whole call)",
             "entries_per_s": total / (ms * 1e-3), "locations_per_s": n / (ms * 1e-3),
             "achieved_GBps": gbps, "frac_of_hbm_peak": gbps / HBM_PEAK_GBS, "frac_of_measured_fill": gbps / fill_gbps,
-            "same_buffer_fill_GBps": same, "frac_of_same_buffer_fill": gbps / same}
+            "same_buffer_fill_GBps": same, "frac_of_same_buffer_fill": gbps / same,
+            "row_fill_GBps": rows, "frac_of_row_fill": gbps / rows if rows else None}
 
 
 def secondary_compare(B, W, steps=5, warmup=2):
@@ -784,10 +811,13 @@ def main():
     # region), beside the spec peak: a fill of the same output arrays, and
     # a 2 GiB fill and copy.
     same = same_buffer_fill(ids, cnt, stream)
+    rows = None if args.wide else row_fill(ids, cnt, offsets, n, info["block_threads"], info["lds_bytes"], stream)
     del ids, cnt
     rates = write_rates(2.0, 5, 2)
     line["roofline"]["same_buffer_fill_GBps"] = same
     line["roofline"]["frac_of_same_buffer_fill"] = achieved / same
+    line["roofline"]["row_fill_GBps"] = rows
+    line["roofline"]["frac_of_row_fill"] = achieved / rows if rows else None
     line["roofline"]["measured_fill_GBps"] = rates["fill_GBps_write"]
     line["roofline"]["measured_fill_bytes"] = rates["bytes"]
     line["roofline"]["measured_copy_GBps"] = rates["copy_GBps_read_plus_write"]
