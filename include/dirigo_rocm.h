@@ -195,7 +195,7 @@ typedef struct {
                                  failed or off, -1 none yet (every DAG call
                                  so far ran the precompiled kernels: by
                                  default only calls over at least 2^26 edges
-                                 of DAGs of at most 2^16 edges per location
+                                 of DAGs of at most 2^18 edges per location
                                  take them; the environment variable
                                  DIRIGO_DAG_JIT=1 makes every call take
                                  them, DIRIGO_DAG_JIT=0 none) */

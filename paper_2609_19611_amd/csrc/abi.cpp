@@ -240,14 +240,14 @@ const dg::JitModule* graph_jit_wide(const dg_graph* cg) {
   return k.ok ? &k.jm : nullptr;
 }
 
-// When the specialised DAG kernels run a call by default: small DAGs per
-// location (a static bound of at most kDagJitRow edges), whose time goes to
-// per-op and per-group bookkeeping that the specialised kernels fold into
+// When the specialised DAG kernels run a call by default: DAGs of at most
+// kDagJitRow edges per location (static bound), whose sizes pass and
+// per-op and per-group bookkeeping the specialised kernels fold into
 // constants, in calls of at least kDagJitEdges edges (below that the
 // compile time, seconds once per graph and device, outweighs the gain).
-// Large DAGs per location are bound by their emission loops, where the
-// unrolled kernels run no faster than the precompiled ones.
-constexpr int64_t kDagJitRow = int64_t(1) << 16;
+// DAGs of millions of edges per location spend their time in node
+// emission, where the unrolled kernels measured no faster.
+constexpr int64_t kDagJitRow = int64_t(1) << 18;
 constexpr double kDagJitEdges = double(1 << 26);
 
 // The specialised DAG kernels of g on the current device for a call over n
