@@ -199,6 +199,10 @@ typedef struct {
                                  take them; the environment variable
                                  DIRIGO_DAG_JIT=1 makes every call take
                                  them, DIRIGO_DAG_JIT=0 none) */
+  int32_t dag_block_threads;  /* threads working on one location's DAG, and */
+  int32_t dag_lds_bytes;      /* the LDS one location's DAG needs (both 0
+                                 until the graph's first DAG call compiles
+                                 its DAG program) */
 } dg_graph_info_t;
 
 dg_status dg_graph_info(const dg_graph* g, dg_graph_info_t* out);

@@ -54,6 +54,8 @@ class GraphInfo(ctypes.Structure):
         ("n_tensors", ctypes.c_int32),
         ("specialized", ctypes.c_int32),
         ("dag_specialized", ctypes.c_int32),
+        ("dag_block_threads", ctypes.c_int32),
+        ("dag_lds_bytes", ctypes.c_int32),
     ]
 
 
@@ -218,6 +220,8 @@ def dg_graph_info(g: Graph) -> dict:
         "n_tensors": info.n_tensors,
         "specialized": info.specialized,
         "dag_specialized": info.dag_specialized,
+        "dag_block_threads": info.dag_block_threads,
+        "dag_lds_bytes": info.dag_lds_bytes,
     }
 
 

@@ -532,6 +532,14 @@ dg_status dg_graph_info(const dg_graph* g, dg_graph_info_t* out) {
       if (it != mg->jit_dag.end() && it->second.tried) out->dag_specialized = it->second.ok ? 1 : 0;
     }
   }
+  {
+    dg_graph* mg = const_cast<dg_graph*>(g);
+    std::lock_guard<std::mutex> lock(mg->mu);
+    if (mg->dag_tried && mg->dag_status == DG_OK) {
+      out->dag_block_threads = mg->dag_block;
+      out->dag_lds_bytes = (int32_t)mg->dag.lds_bytes;
+    }
+  }
   return DG_OK;
 }
 

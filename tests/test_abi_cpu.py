@@ -43,6 +43,8 @@ def test_info_of_workloads(name):
     assert info["count_bound"] >= int(cnt.max())
     assert info["lds_bytes"] <= 160 * 1024
     assert info["block_threads"] in (64, 256)
+    # No DAG call yet: no DAG program, no DAG kernels.
+    assert (info["dag_block_threads"], info["dag_lds_bytes"]) == (0, 0)
 
 
 def test_build_matches_parse():
