@@ -124,6 +124,6 @@ def test_sparse_fault_found_first_by_the_order(B, kind):
         pos = np.nonzero(want[order])[0]
         return int(pos[0])
     heur = B.order_locations(var, 5).cpu().numpy()
-    perm = oracle.permutation(n, 5, 0, n)
+    perm = _permute(B, n, 5, 0, n)  # the plain permutation (its parity is tested above)
     r_h, r_p, r_s = first(heur), first(perm), first(np.arange(n))
     assert r_h < len(B.dg_order_prefix(var)) and r_h <= r_p and r_h <= r_s, (r_h, r_p, r_s)
