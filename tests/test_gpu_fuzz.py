@@ -2,7 +2,7 @@
 GPU, through the C ABI, against the oracle at every output location: the
 single-pass and two-pass enumerations, expression DAGs and comparisons with
 a variant whose counts double, with the precompiled kernels on 160 graphs
-and the specialised ones on 16 of them."""
+and the specialised ones (DAG kernels included) on 16 of them."""
 
 import numpy as np
 import pytest
@@ -73,7 +73,10 @@ def test_fuzz_precompiled_kernels(B, chunk, monkeypatch):
 
 
 def test_fuzz_specialized_kernels(B, monkeypatch):
+    """The same graphs' enumeration, comparison and DAG kernels specialised
+    (DIRIGO_DAG_JIT=1: every DAG call takes the specialised DAG kernels)."""
     monkeypatch.setenv("DIRIGO_JIT", "1")
+    monkeypatch.setenv("DIRIGO_DAG_JIT", "1")
     texts = []
     for seed in range(1000, 1016):
         try:
@@ -81,6 +84,7 @@ def test_fuzz_specialized_kernels(B, monkeypatch):
             texts.append(fuzz_graphs.random_graph(seed))
         except B.DgError:
             pass
-    warm = gpu_warm.warm_graphs(B, texts)  # noqa: F841  (compiled several at once, kept loaded)
-    done = sum(check_graph(B, seed, dags=False) for seed in range(1000, 1016))
+    # (compiled several at once, kept loaded)
+    warm = gpu_warm.warm_graphs(B, texts, threads=16) + gpu_warm.warm_dags(B, texts, threads=16)  # noqa: F841
+    done = sum(check_graph(B, seed, dags=True) for seed in range(1000, 1016))
     assert done >= 15
