@@ -42,7 +42,8 @@
  *  - with specialisation on, the code object of the graph's kernels
  *    (hipModuleLoadData), shared by graphs whose plans are identical; a
  *    comparison loads one for the pair, released when either graph of the
- *    pair is destroyed.
+ *    pair is destroyed; DAG calls that take the specialised DAG kernels
+ *    load one for the graph's DAG program.
  *
  * Sizes: a call takes at most 2^31 locations (DG_E_INVALID_ARG beyond);
  * the library splits its launches so that no grid exceeds the device's
@@ -53,9 +54,13 @@
  * C++ exception crosses this interface.
  *
  * Specialisation: on its first device call, a graph compiles kernels
- * specialised to its plan (hipRTC, a few seconds, cached per process);
- * setting the environment variable DIRIGO_JIT=0 keeps the precompiled
- * kernels, which run the same code on the plan as data.
+ * specialised to its plan (hipRTC in a helper process, lib/dirigo_jitc; a
+ * few seconds, cached per process); setting the environment variable
+ * DIRIGO_JIT=0 keeps the precompiled kernels, which run the same code on
+ * the plan as data, and DIRIGO_JIT_INPROC=1 compiles in the calling
+ * process.  Expression-DAG calls take DAG kernels specialised to the
+ * graph's DAG program by the rule given with dg_graph_info_t
+ * (dag_specialized).
  *
  * Thread safety: a dg_graph is immutable after construction and may be used
  * from several host threads and streams at once.  Calls that share one
