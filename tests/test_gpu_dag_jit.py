@@ -113,3 +113,20 @@ def test_specialised_dag_c5_variants(B, graphs):
              for h in (0, 1, H - 2, H - 1) for w in (0, 1, Wd - 2, Wd - 1)]
     for text in C5:
         _check(B, graphs[text], text, locs + edges)
+
+
+def test_specialised_dag_edge_cases(B, graphs):
+    """A graph whose output is a leaf (a DAG program with no ops), an empty
+    location list, and an out-of-range location, on the specialised DAG
+    kernels."""
+    g = B.dg_graph_parse("dgir 1\nleaf x 4\noutput x 4\n")
+    d = B.dag_locations(g, [0, 3])
+    assert d["node_offsets"].cpu().tolist() == [0, 0, 0] and d["edge_offsets"].cpu().tolist() == [0, 0, 0]
+    text = WORK["c2"]
+    g2 = graphs[text]
+    d = B.dag_locations(g2, torch.empty(0, dtype=torch.int64))
+    assert d["node_offsets"].cpu().tolist() == [0] and d["edges"].numel() == 0
+    with pytest.raises(B.DgError) as e:
+        B.dag_locations(g2, [0, 65536])
+    assert e.value.name == "DG_E_RANGE"
+    _check(B, g2, text, [65535, 3, 3, 0])
