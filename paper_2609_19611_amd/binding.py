@@ -56,6 +56,8 @@ class GraphInfo(ctypes.Structure):
         ("dag_specialized", ctypes.c_int32),
         ("dag_block_threads", ctypes.c_int32),
         ("dag_lds_bytes", ctypes.c_int32),
+        ("dag_edge_bound", ctypes.c_int64),
+        ("dag_fill_specialized", ctypes.c_int32),
     ]
 
 
@@ -222,6 +224,8 @@ def dg_graph_info(g: Graph) -> dict:
         "dag_specialized": info.dag_specialized,
         "dag_block_threads": info.dag_block_threads,
         "dag_lds_bytes": info.dag_lds_bytes,
+        "dag_edge_bound": info.dag_edge_bound,
+        "dag_fill_specialized": info.dag_fill_specialized,
     }
 
 

@@ -3,6 +3,8 @@ dg_dag_fill) against the oracle's DAGs, element by element, through the C
 ABI: every location of the small catalogue graphs, samples of the five
 workloads (c5's variant and faulty variants too), error paths."""
 
+import os
+
 import numpy as np
 import pytest
 import torch
@@ -93,3 +95,22 @@ def test_dag_edge_cases(B):
     # Output that is a leaf: no nodes, no edges.
     d = B.dag_locations(B.dg_graph_parse("dgir 1\nleaf x 4\noutput x 4\n"), [0, 3])
     assert d["node_offsets"].cpu().tolist() == [0, 0, 0] and d["edge_offsets"].cpu().tolist() == [0, 0, 0]
+
+
+def test_default_kernel_choice_for_large_dags(B):
+    """By default a call over the conv-transpose + softmax DAGs (millions of
+    edges per location) loads the specialised DAG kernels for its sizes
+    pass and keeps the precompiled fill; the result is the oracle's either
+    way."""
+    if os.environ.get("DIRIGO_DAG_JIT") or os.environ.get("DIRIGO_JIT") == "0":
+        pytest.skip("the default choice only")
+    text = W.CONFIGS["c3"]["text"]()
+    g = B.dg_graph_parse(text)
+    locs = W.config_locations("c3")[::1024]
+    got = _host(B.dag_locations(g, locs))
+    info = B.dg_graph_info(g)
+    assert info["dag_specialized"] == 1 and info["dag_fill_specialized"] == 0
+    assert info["dag_edge_bound"] > 1 << 18 and len(locs) * info["dag_edge_bound"] >= 1 << 26
+    want = oracle.Graph(text).dag(locs, threads=16)
+    for k in KEYS:
+        assert np.array_equal(got[k], want[k]), k
