@@ -401,8 +401,7 @@ def dag_bench(args, B, g, cfg, locs, text):
     fill_ms_median = float(np.median([a.elapsed_time(b) for a, b in ev]))
     same = same_buffer_fill_dag((nodes, node_edge, edges, mults), stream)
     info = B.dg_graph_info(g)
-    kinds = "specialized" if info["dag_fill_specialized"] == 1 else "precompiled"
-    sizes_kinds = "specialized" if info["dag_specialized"] == 1 else "precompiled"
+    kinds = "specialized" if info["dag_specialized"] == 1 else "precompiled"
     # The edge and multiplicity rows written by the row-writer reference with
     # the DAG kernels' grid, block size and LDS (nodes aside: 8 B per node).
     rows = row_fill(edges, mults, eoff, n, info["dag_block_threads"], info["dag_lds_bytes"], stream)
@@ -427,7 +426,7 @@ def dag_bench(args, B, g, cfg, locs, text):
                      "kernel_ms_statistic": f"median of {args.steps} launches", "algorithmic_bytes": alg,
                      "same_buffer_fill_GBps": same, "frac_of_same_buffer_fill": achieved / same,
                      "edge_row_fill_GBps": rows, "frac_of_edge_row_fill": achieved / rows if rows else None,
-                     "kernels": kinds, "sizes_kernels": sizes_kinds},
+                     "kernels": kinds},
     }
     if not args.no_cpu_baseline:
         import oracle

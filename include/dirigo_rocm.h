@@ -200,21 +200,16 @@ typedef struct {
                                  failed or off, -1 none yet (every DAG call
                                  so far ran the precompiled kernels).  By
                                  default calls over at least 2^26 edges
-                                 (static bound) load them; their sizes pass
-                                 then takes them, and their fill does for
-                                 DAGs of at most 2^18 edges per location.
-                                 The environment variable DIRIGO_DAG_JIT=1
-                                 makes every call take them for both
-                                 passes, DIRIGO_DAG_JIT=0 none */
+                                 (static bound: locations times
+                                 dag_edge_bound) take them; the environment
+                                 variable DIRIGO_DAG_JIT=1 makes every call
+                                 take them, DIRIGO_DAG_JIT=0 none */
   int32_t dag_block_threads;  /* threads working on one location's DAG, and */
   int32_t dag_lds_bytes;      /* the LDS one location's DAG needs (both 0
                                  until the graph's first DAG call compiles
                                  its DAG program) */
   int64_t dag_edge_bound;     /* static bound on one location's DAG edges
                                  (0 until then) */
-  int32_t dag_fill_specialized; /* 1 when dg_dag_fill takes the loaded
-                                 specialised kernels, under the rule above
-                                 and the current environment */
 } dg_graph_info_t;
 
 dg_status dg_graph_info(const dg_graph* g, dg_graph_info_t* out);

@@ -57,7 +57,6 @@ class GraphInfo(ctypes.Structure):
         ("dag_block_threads", ctypes.c_int32),
         ("dag_lds_bytes", ctypes.c_int32),
         ("dag_edge_bound", ctypes.c_int64),
-        ("dag_fill_specialized", ctypes.c_int32),
     ]
 
 
@@ -225,7 +224,6 @@ def dg_graph_info(g: Graph) -> dict:
         "dag_block_threads": info.dag_block_threads,
         "dag_lds_bytes": info.dag_lds_bytes,
         "dag_edge_bound": info.dag_edge_bound,
-        "dag_fill_specialized": info.dag_fill_specialized,
     }
 
 

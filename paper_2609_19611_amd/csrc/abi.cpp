@@ -240,30 +240,27 @@ const dg::JitModule* graph_jit_wide(const dg_graph* cg) {
   return k.ok ? &k.jm : nullptr;
 }
 
-// When the specialised DAG kernels run a call by default: calls of at least
-// kDagJitEdges edges (static bound; below that the compile time, seconds
-// once per graph and device, outweighs the gain).  Their sizes pass, whose
-// per-op and per-group bookkeeping folds into constants, always takes them
-// then; their fill takes them for DAGs of at most kDagJitRow edges per
-// location.  DAGs of millions of edges per location spend their fill in
-// node emission, where the unrolled kernels measured no faster.
-constexpr int64_t kDagJitRow = int64_t(1) << 18;
+// Calls whose static edge bound (locations times the per-location bound)
+// reaches this many edges take the specialised DAG kernels by default:
+// below it the compile time (seconds, once per graph and device) outweighs
+// the gain.  Both passes gain from them: the sizes pass most (its per-op
+// and per-group bookkeeping folds into constants), the fill by a few per
+// cent for DAGs of millions of edges per location (timed against the
+// precompiled fill in the same processes) up to 3.4x for small ones.
 constexpr double kDagJitEdges = double(1 << 26);
 
-// The specialised DAG kernels of g on the current device for the sizes
-// (fill false) or fill pass of a call over n locations, compiled on first
-// use; nullptr when the precompiled kernel runs it: specialisation off or
-// failed, a call outside the default range above, or more than 64 KiB of
-// LDS per location.  DIRIGO_DAG_JIT=1 specialises every call,
-// DIRIGO_DAG_JIT=0 none.  The DAG program must be compiled.
-const dg::JitModule* dag_jit(const dg_graph* cg, int64_t n, bool fill) {
+// The specialised DAG kernels of g on the current device for a call over n
+// locations, compiled on first use; nullptr when the precompiled kernels
+// run the call: specialisation off or failed, a call below kDagJitEdges,
+// or more than 64 KiB of LDS per location.  DIRIGO_DAG_JIT=1 specialises
+// every call, DIRIGO_DAG_JIT=0 none.  The DAG program must be compiled.
+const dg::JitModule* dag_jit(const dg_graph* cg, int64_t n) {
   if (!dg::jit_enabled()) return nullptr;
   dg_graph* g = const_cast<dg_graph*>(cg);
   const char* env = std::getenv("DIRIGO_DAG_JIT");
   const int mode = env && env[0] == '1' ? 1 : env && env[0] == '0' ? 0 : -1;
   if (mode == 0 || g->dag.lds_bytes > 65536u) return nullptr;
-  if (mode < 0 && ((double)n * (double)g->dag.max_edges < kDagJitEdges || (fill && g->dag.max_edges > kDagJitRow)))
-    return nullptr;
+  if (mode < 0 && (double)n * (double)g->dag.max_edges < kDagJitEdges) return nullptr;
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return nullptr;
   std::lock_guard<std::mutex> lock(g->mu);
@@ -539,10 +536,6 @@ dg_status dg_graph_info(const dg_graph* g, dg_graph_info_t* out) {
       out->dag_block_threads = mg->dag_block;
       out->dag_lds_bytes = (int32_t)mg->dag.lds_bytes;
       out->dag_edge_bound = mg->dag.max_edges;
-      const char* env = std::getenv("DIRIGO_DAG_JIT");
-      const bool forced = env && env[0] == '1';
-      out->dag_fill_specialized =
-          out->dag_specialized == 1 && (forced || mg->dag.max_edges <= kDagJitRow) ? 1 : 0;
     }
   }
   return DG_OK;
@@ -1014,7 +1007,7 @@ dg_status dg_dag_sizes(const dg_graph* g, const int64_t* d_locs, int64_t n, int6
     uint8_t* ws = static_cast<uint8_t*>(d_ws);
     uint32_t* err = reinterpret_cast<uint32_t*>(ws + w.err);
     DG_HIP(dgk::launch_zero(err, s), "zero");
-    const dg::JitModule* jm = dag_jit(g, n, false);
+    const dg::JitModule* jm = dag_jit(g, n);
     DG_HIP(per_location(n, g->dag_block,
                         [&](int64_t first, int64_t m) {
                           dgc::LocSrc part{d_locs + first, 0};
@@ -1062,7 +1055,7 @@ dg_status dg_dag_fill(const dg_graph* g, const int64_t* d_locs, int64_t n, const
     hipStream_t s = static_cast<hipStream_t>(stream);
     uint32_t* err = reinterpret_cast<uint32_t*>(static_cast<uint8_t*>(d_ws) + ws_layout(n).err);
     DG_HIP(dgk::launch_zero(err, s), "zero");
-    const dg::JitModule* jm = dag_jit(g, n, true);
+    const dg::JitModule* jm = dag_jit(g, n);
     DG_HIP(per_location(n, g->dag_block,
                         [&](int64_t first, int64_t m) {
                           dgc::LocSrc part{d_locs + first, 0};

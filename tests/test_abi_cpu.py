@@ -45,7 +45,6 @@ def test_info_of_workloads(name):
     assert info["block_threads"] in (64, 256)
     # No DAG call yet: no DAG program, no DAG kernels.
     assert (info["dag_block_threads"], info["dag_lds_bytes"], info["dag_edge_bound"]) == (0, 0, 0)
-    assert info["dag_fill_specialized"] == 0
 
 
 def test_build_matches_parse():

@@ -99,9 +99,8 @@ def test_dag_edge_cases(B):
 
 def test_default_kernel_choice_for_large_dags(B):
     """By default a call over the conv-transpose + softmax DAGs (millions of
-    edges per location) loads the specialised DAG kernels for its sizes
-    pass and keeps the precompiled fill; the result is the oracle's either
-    way."""
+    edges per location, 64 of them here) takes the specialised DAG kernels;
+    the result is the oracle's."""
     if os.environ.get("DIRIGO_DAG_JIT") or os.environ.get("DIRIGO_JIT") == "0":
         pytest.skip("the default choice only")
     text = W.CONFIGS["c3"]["text"]()
@@ -109,8 +108,8 @@ def test_default_kernel_choice_for_large_dags(B):
     locs = W.config_locations("c3")[::1024]
     got = _host(B.dag_locations(g, locs))
     info = B.dg_graph_info(g)
-    assert info["dag_specialized"] == 1 and info["dag_fill_specialized"] == 0
-    assert info["dag_edge_bound"] > 1 << 18 and len(locs) * info["dag_edge_bound"] >= 1 << 26
+    assert info["dag_specialized"] == 1
+    assert len(locs) * info["dag_edge_bound"] >= 1 << 26
     want = oracle.Graph(text).dag(locs, threads=16)
     for k in KEYS:
         assert np.array_equal(got[k], want[k]), k
