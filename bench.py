@@ -199,6 +199,26 @@ def row_fill(ids, cnt, offsets, n, block, lds, stream, steps=5, warmup=2):
     return (ids.numel() * ids.element_size() + cnt.numel() * cnt.element_size()) / (ms * 1e-3) / 1e9
 
 
+def placement_spread(B, g, d_locs, offsets, ws, total, stream, sets=3, steps=7):
+    """The enumeration and torch's fill of its output arrays in `sets` more
+    allocations of the same output arrays (untimed for the headline): a
+    writer of one row per block is sensitive to where the output's physical
+    pages fall, which the allocator decides, while an address-ordered fill
+    is not."""
+    import torch
+    # (All sets held at once, so that each is a distinct allocation.)
+    bufs = [(torch.empty(total, dtype=torch.int32, device="cuda"), torch.empty(total, dtype=torch.int32, device="cuda"))
+            for _ in range(sets)]
+    out = []
+    for ids, cnt in bufs:
+        ms = _median_ms(lambda: B.dg_enumerate(g, d_locs, offsets, ids, cnt, ws), steps, 2, stream)
+        fill = _median_ms(lambda: (ids.fill_(7), cnt.fill_(7)), steps, 2, stream)
+        out.append({"enumerate_ms": ms, "fill_ms": fill, "frac_of_fill": fill / ms})
+    del bufs
+    torch.cuda.empty_cache()
+    return out
+
+
 def same_buffer_fill_dag(arrays, stream, steps=5, warmup=2):
     """Write rate of torch's fill over the DAG's own output arrays (nodes,
     first edges, edges, multiplicities: the same bytes at the same
@@ -818,11 +838,19 @@ def main():
     same = same_buffer_fill(ids, cnt, stream)
     rows = None if args.wide else row_fill(ids, cnt, offsets, n, info["block_threads"], info["lds_bytes"], stream)
     del ids, cnt
+    spread = None
+    if args.workload == "c4" and not (args.two_pass or args.wide) and not args.no_secondary:
+        torch.cuda.empty_cache()
+        spread = placement_spread(B, g, d_locs, offsets, ws, total, stream)
     rates = write_rates(2.0, 5, 2)
     line["roofline"]["same_buffer_fill_GBps"] = same
     line["roofline"]["frac_of_same_buffer_fill"] = achieved / same
     line["roofline"]["row_fill_GBps"] = rows
     line["roofline"]["frac_of_row_fill"] = achieved / rows if rows else None
+    if spread:
+        # The same call in three more allocations of its output arrays (not
+        # part of the headline): the rate depends on the physical placement.
+        line["roofline"]["other_allocations"] = spread
     line["roofline"]["measured_fill_GBps"] = rates["fill_GBps_write"]
     line["roofline"]["measured_fill_bytes"] = rates["bytes"]
     line["roofline"]["measured_copy_GBps"] = rates["copy_GBps_read_plus_write"]
