@@ -448,6 +448,16 @@ def dag_bench(args, B, g, cfg, locs, text):
                      "edge_row_fill_GBps": rows, "frac_of_edge_row_fill": achieved / rows if rows else None,
                      "kernels": kinds},
     }
+    # The same fill in two more allocations of its output arrays (not part
+    # of the headline): its rate depends on where their physical pages fall.
+    del nodes, node_edge, edges, mults
+    torch.cuda.empty_cache()
+    others = [[torch.empty(max(m, 1), dtype=torch.int32, device=dev) for m in (nn, nn, ne, ne)] for _ in range(2)]
+    line["roofline"]["other_allocations"] = [
+        {"fill_ms": t, "frac": alg / (t * 1e-3) / 1e9 / HBM_PEAK_GBS}
+        for t in (_median_ms(lambda: B.dg_dag_fill(g, d_locs, noff, eoff, *o, ws), 5, 1, stream) for o in others)]
+    del others
+    torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         import oracle
         m = max(1, min(n, 64))
