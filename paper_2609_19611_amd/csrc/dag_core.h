@@ -713,6 +713,73 @@ DGC uint64_t ap_count(const DagCtx& x, const DgdGroup& G, int R, const Slots& S,
   }
 }
 
+// A group of one point per node (no window, leaf operands only) that
+// follows a windowed group in the op's read order: its edges sit right after
+// each node's run of the windowed group.  Written by the node loop right
+// after that run (or after the group's flat emission for the lanes whose
+// node it did not take), rather than in a pass of its own over the batch
+// once every run is out: cache lines that the runs and the point share are
+// then filled while still in the cache instead of reaching HBM in parts.
+struct PointTail {
+  bool on;        // the group after this one is written with it (same on every lane)
+  uint32_t P;     // the lane's node: 1 when its point is valid
+  int nop;
+  uint32_t v[3];  // the point's operand elements (global ids)
+  uint32_t m[3];  // their multiplicities
+};
+
+template <int NOP>
+DGC void point_tail_setup(const DagCtx& x, const DgdGroup& G1, int R, bool has, PointTail& t) {
+  NodeAP<0, NOP> N{};
+  t.P = has ? (uint32_t)ap_setup_reg<0, NOP>(x, G1, R, true, N) : 0u;
+  DG_UNROLL
+  for (int a = 0; a < NOP; ++a) {
+    t.v[a] = N.base[a];
+    t.m[a] = x.Ps[G1.op0 + a].mult;
+  }
+  t.nop = NOP;
+  t.on = true;
+}
+
+// The point tail of group q of op (off when the fill does not write, when
+// group q has no window or the next group is not such a group, or when its
+// shape has no compiled form).  The lane's node coordinates are in its
+// variables.
+DGC PointTail point_tail(const DagCtx& x, const DgdOp& op, int q, int R, bool has, bool emit) {
+  PointTail t{};
+  if (!emit || q + 1 >= op.ng) return t;
+  const DgdGroup& G = x.Gs[op.g0 + q];
+  const DgdGroup& G1 = x.Gs[op.g0 + q + 1];
+  if (G.nwin == 0 || !G1.fast || !G1.steps24 || G1.nwin != 0 || G1.points == 0) return t;
+  for (int a = 0; a < G1.nop; ++a)
+    if (!x.T[x.Ps[G1.op0 + a].tensor].leaf) return t;
+  switch (G1.nop) {
+    case 1:
+      if constexpr ((DG_DAG_FAST) & 1u) point_tail_setup<1>(x, G1, R, has, t);
+      break;
+    case 2:
+      if constexpr (((DG_DAG_FAST) >> 5) & 1u) point_tail_setup<2>(x, G1, R, has, t);
+      break;
+    case 3:
+      if constexpr (((DG_DAG_FAST) >> 10) & 1u) point_tail_setup<3>(x, G1, R, has, t);
+      break;
+    default: break;
+  }
+  return t;
+}
+
+// The lane's point of a tail at edge `at` (nothing when it has none).
+template <class C>
+DGC void point_tail_write(C& c, const PointTail& t, const DagOut& o, uint64_t at) {
+  if (!t.P) return;
+  DG_UNROLL
+  for (int a = 0; a < 3; ++a)
+    if (a < t.nop && at + (uint64_t)a < o.room_edges) {
+      c.store_cached(&o.edges[at + a], t.v[a]);
+      c.store_cached(&o.mults[at + a], t.m[a]);
+    }
+}
+
 // Writes group G's edges for the wave's batch of nodes: lane j's node has
 // Pj points (0 for none), set up in slot column j with its first edge.  The
 // points of the batch are taken flattened across the lanes: point t belongs
@@ -899,7 +966,7 @@ DGC uint32_t div64(uint32_t n, uint32_t d, uint32_t m, uint32_t* r) {
 // check per edge.
 template <class C, int NOP, int Q>
 DGC void node_emit_reg(C& c, const DagCtx& x, const DgdGroup& G, const NodeAP<Q, NOP>& N, uint32_t Pj, uint64_t gpos,
-                       uint64_t mask, const DagOut& o, bool emit, bool append) {
+                       uint64_t mask, const DagOut& o, bool emit, bool append, const PointTail& tl) {
   if constexpr (Q == 0) return;  // (a group without a window has one point per node: never emitted here)
   constexpr int QD = Q > 0 ? Q : 1;
   const int lane = c.lane(), L = c.lanes();
@@ -1008,6 +1075,7 @@ DGC void node_emit_reg(C& c, const DagCtx& x, const DgdGroup& G, const NodeAP<Q,
           off += W * NOP;
         }
       }
+      if (tl.on && lane == j) point_tail_write(c, tl, o, gpos + (uint64_t)Pj * NOP);
       continue;
     }
     // Every digit advances by those of the wave width, with carries: the
@@ -1058,6 +1126,7 @@ DGC void node_emit_reg(C& c, const DagCtx& x, const DgdGroup& G, const NodeAP<Q,
       for (int a = 0; a < NOP; ++a) child[a] += dstep[a];
       off += (uint32_t)L * NOP;
     }
+    if (tl.on && lane == j) point_tail_write(c, tl, o, gpos + (uint64_t)Pj * NOP);
   }
 }
 
@@ -1069,13 +1138,13 @@ DGC void node_emit_reg(C& c, const DagCtx& x, const DgdGroup& G, const NodeAP<Q,
 // there, 0 otherwise).  Returns the lane's point count.
 template <class C, int NOP, int Q>
 DGC uint32_t fast_group_reg(C& c, const DagCtx& x, const DgdGroup& G, int R, bool has, uint64_t gpos, const Slots& S,
-                            const DagOut& o, bool emit, bool append, uint32_t* small) {
+                            const DagOut& o, bool emit, bool append, const PointTail& tl, uint32_t* small) {
   const int lane = c.lane(), L = c.lanes();
   NodeAP<Q, NOP> N{};
   const uint32_t Pj = has ? (uint32_t)ap_setup_reg<Q, NOP>(x, G, R, true, N) : 0u;
   const bool big = Q > 0 && Pj >= (uint32_t)((L + 1) / 2);
   const uint64_t mask = c.ballot(big);
-  if (mask) node_emit_reg<C, NOP, Q>(c, x, G, N, Pj, gpos, mask, o, emit, append);
+  if (mask) node_emit_reg<C, NOP, Q>(c, x, G, N, Pj, gpos, mask, o, emit, append, tl);
   *small = big ? 0u : Pj;
   if (*small) {
     DG_UNROLL
@@ -1091,13 +1160,13 @@ DGC uint32_t fast_group_reg(C& c, const DagCtx& x, const DgdGroup& G, int R, boo
 // fast_group_reg for the group's shape; false when it has no compiled form.
 template <class C>
 DGC bool fast_group(C& c, const DagCtx& x, const DgdGroup& G, int R, bool has, uint64_t gpos, const Slots& S,
-                    const DagOut& o, bool emit, bool append, uint32_t* Pj, uint32_t* small) {
+                    const DagOut& o, bool emit, bool append, const PointTail& tl, uint32_t* Pj, uint32_t* small) {
   if (!G.steps24) return false;
   switch (G.nop * 16 + G.nwin) {
 #define DG_FAST(NOP, Q)                                                                          \
   case NOP * 16 + Q:                                                                             \
     if constexpr (((DG_DAG_FAST) >> ((NOP - 1) * 5 + Q)) & 1u) {                                 \
-      *Pj = fast_group_reg<C, NOP, Q>(c, x, G, R, has, gpos, S, o, emit, append, small);         \
+      *Pj = fast_group_reg<C, NOP, Q>(c, x, G, R, has, gpos, S, o, emit, append, tl, small);     \
       return true;                                                                               \
     } else {                                                                                     \
       return false;                                                                              \
@@ -1246,17 +1315,31 @@ DGC bool dag_op(C& c, const DagCtx& x, const DgdOp& op, uint32_t* NC, const Slot
       uint32_t tot;
       uint64_t gpos = eb + NC[b0 / (uint32_t)L] + c.wave_scan((uint32_t)m, &tot);
       if (MODE == DAG_FILL && has && nb + i < o.room_nodes) c.store(&o.node_edge[nb + i], (uint32_t)gpos);
+      bool taken = false;  // the group was written as the point tail of the one before
       DG_DAG_UNROLL
       for (int q = 0; q < op.ng; ++q) {
+        if (taken) {
+          taken = false;
+          continue;
+        }
         const DgdGroup& G = x.Gs[op.g0 + q];
         if (G.points == 0) continue;
         if (G.fast) {
           uint32_t Pj = 0, small = 0;
           if (has) node_coords(X, F[i], x.vt, nt);
-          if (fast_group(c, x, G, R, has, gpos, S, o, emit, append, &Pj, &small)) {
+          const PointTail tl = point_tail(x, op, q, R, has, emit);
+          if (fast_group(c, x, G, R, has, gpos, S, o, emit, append, tl, &Pj, &small)) {
             if (c.ballot(small != 0)) {
               c.wave_sync();
               flat_emit(c, x, G, S, WP, small, o, emit, append);
+            }
+            if (tl.on) {
+              // Nodes the node loop did not take (fewer than half a wave of
+              // points) get their point here.
+              const uint64_t at = gpos + (uint64_t)Pj * (uint64_t)G.nop;
+              if (has && Pj < (uint32_t)((L + 1) / 2)) point_tail_write(c, tl, o, at);
+              gpos += (uint64_t)tl.P * (uint64_t)tl.nop;
+              taken = true;
             }
           } else if constexpr (DG_DAG_SLOW) {
             if (has) {
