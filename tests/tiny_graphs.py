@@ -233,6 +233,16 @@ def dag_catalogue():
                                     [("y", "conv_transpose", ["x", "W"],
                                       dict(stride=[2], pad=[1], output_padding=[0], dilation=[2], groups=1))],
                                     "y", [1, 2, 9])
+    # A transposed convolution with a bias, averaged: the mean's node reads
+    # 216 conv nodes whose windows hold 16 to 128 points (1 to 8 taps of 16
+    # input channels), so a wave's batch holds nodes above and below half a
+    # wave of points, each followed by its bias edge.
+    G["convT3d_bias_mean"] = _g([("x", [1, 16, 3, 3, 3]), ("W", [16, 2, 3, 3, 3]), ("b", [2])],
+                                [("t", "conv_transpose", ["x", "W", "b"],
+                                  dict(stride=[2, 2, 2], pad=[1, 1, 1], output_padding=[1, 1, 1], dilation=[1, 1, 1],
+                                       groups=1)),
+                                 ("y", "mean", ["t"], dict(dims=[2, 3, 4], keepdim=0))],
+                                "y", [1, 2])
     G["gather_shift"] = _g([("x", [2, 5]), ("z", [2, 5])],
                            [("t", "exp", ["x"], {}),
                             ("y", "affine_gather", ["t", "z"],
