@@ -287,6 +287,37 @@ def secondary_compare(B, W, steps=5, warmup=2):
             "statistic": "median of 10 calls (clean) and of %d steps (17 compares)" % steps}
 
 
+def secondary_dag(B, W, name, every=8, steps=5, warmup=1):
+    """Expression DAGs of every `every`-th listed location of a workload:
+    the fill kernel's median over `steps` launches (sizes pass and buffers
+    beforehand, untimed), its HBM fraction (algorithmic bytes) and the row
+    writer of its edge rows on the same buffers."""
+    import torch
+    stream = torch.cuda.current_stream()
+    g = B.dg_graph_parse(W.CONFIGS[name]["text"]())
+    locs = W.config_locations(name)[::every]
+    d_locs = torch.as_tensor(locs, dtype=torch.int64, device="cuda")
+    n = len(locs)
+    ws = torch.empty(max(B.dg_workspace_size(g, n), 1), dtype=torch.uint8, device="cuda")
+    noff = torch.empty(n + 1, dtype=torch.int64, device="cuda")
+    eoff = torch.empty(n + 1, dtype=torch.int64, device="cuda")
+    nn, ne = B.dg_dag_sizes(g, d_locs, noff, eoff, ws)
+    out = [torch.empty(max(m, 1), dtype=torch.int32, device="cuda") for m in (nn, nn, ne, ne)]
+    ms = _median_ms(lambda: B.dg_dag_fill(g, d_locs, noff, eoff, *out, ws), steps, warmup, stream)
+    alg = 24 * n + 8 * nn + 8 * ne
+    gbps = alg / (ms * 1e-3) / 1e9
+    info = B.dg_graph_info(g)
+    rows = row_fill(out[2], out[3], eoff, n, info["dag_block_threads"], info["dag_lds_bytes"], stream)
+    del out
+    torch.cuda.empty_cache()
+    return {"workload": f"{name}: " + W.CONFIGS[name]["desc"] + " (expression DAGs)", "locations": n,
+            "nodes": nn, "edges": ne, "fill_ms": ms,
+            "statistic": f"median of {steps} launches (dg_dag_fill, whole call)",
+            "kernels": "specialized" if info["dag_specialized"] == 1 else "precompiled",
+            "achieved_GBps": gbps, "frac_of_hbm_peak": gbps / HBM_PEAK_GBS,
+            "edge_row_fill_GBps": rows, "frac_of_edge_row_fill": gbps / rows if rows else None}
+
+
 def git_sha():
     try:
         return subprocess.check_output(["git", "rev-parse", "--short", "HEAD"], cwd=ROOT,
@@ -866,10 +897,12 @@ def main():
     line["roofline"]["measured_copy_GBps"] = rates["copy_GBps_read_plus_write"]
     line["roofline"]["frac_of_measured_fill"] = achieved / rates["fill_GBps_write"]
     if args.workload == "c4" and not (args.two_pass or args.wide) and not args.no_secondary:
-        # The other two headline figures, timed after the main one: the
-        # conv-transpose + softmax enumeration and the pair check.
+        # The other headline figures, timed after the main one: the
+        # conv-transpose + softmax enumeration, the pair check and the
+        # conv-transpose's expression DAGs.
         line["secondary"] = {"c3": secondary_enumeration(B, W, "c3", rates["fill_GBps_write"]),
-                             "c5": secondary_compare(B, W)}
+                             "c5": secondary_compare(B, W),
+                             "c3_dag": secondary_dag(B, W, "c3")}
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(args.workload, text, None, locs, args.cpu_seconds)
     line["git"] = git_sha()
