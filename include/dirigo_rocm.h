@@ -246,9 +246,9 @@ dg_status dg_graph_tensor(const dg_graph* g, int32_t i, dg_tensor_info_t* out);
  * Enumeration.
  * ------------------------------------------------------------------------
  * dg_workspace_size: bytes of device workspace that dg_enumerate_sizes,
- * dg_enumerate_fill and dg_compare need for n_locs locations (the same
- * buffer serves all three; for dg_compare pass the larger of the two
- * graphs' sizes). */
+ * dg_enumerate_fill, dg_compare and the expression-DAG calls need for
+ * n_locs locations (the same buffer serves them all; for dg_compare pass
+ * the larger of the two graphs' sizes). */
 dg_status dg_workspace_size(const dg_graph* g, int64_t n_locs, size_t* bytes);
 
 /* dg_enumerate_sizes: row sizes and CSR offsets.
@@ -367,6 +367,32 @@ dg_status dg_dag_sizes(const dg_graph* g, const int64_t* d_locs, int64_t n, int6
 dg_status dg_dag_fill(const dg_graph* g, const int64_t* d_locs, int64_t n, const int64_t* d_node_offsets,
                       const int64_t* d_edge_offsets, uint32_t* d_nodes, uint32_t* d_node_edge, uint32_t* d_edges,
                       uint32_t* d_mults, void* d_ws, void* stream);
+
+/* dg_dag: dg_dag_sizes and dg_dag_fill in one call, with output buffers
+ * sized beforehand (Sec. 3.4, "Back-projection", as above).  A call of at
+ * most 2,048 locations whose DAG, at the program's static node and edge
+ * bounds, fits in LDS beside the walk's frontiers (64 KiB at most) walks
+ * each location once: its DAG is staged in LDS, its node and edge offsets
+ * come from decoupled look-backs over its predecessors' counts, and the
+ * stage is copied out, with no host round trip between passes.  Larger
+ * calls, where that costs more per location than the two passes, make the
+ * two passes (DIRIGO_DAG_ONEPASS=1 takes the one pass whenever the stage
+ * fits, DIRIGO_DAG_ONEPASS=0 never).
+ *   d_locs[n]            device, int64 flat output locations
+ *   d_node_offsets[n+1]  device, written as by dg_dag_sizes
+ *   d_edge_offsets[n+1]  device, written as by dg_dag_sizes
+ *   d_nodes, d_node_edge device, node_capacity uint32 entries each
+ *   d_edges, d_mults     device, edge_capacity uint32 entries each
+ *   h_nodes, h_edges     host, written: the totals
+ * Location i's DAG is written where its nodes and edges fit the capacities.
+ * Synchronous.  Returns DG_E_BUFFER when a total exceeds its capacity: the
+ * offsets and totals are then valid, the DAGs past a capacity are not
+ * written, and the call can be repeated with larger buffers.  DG_E_RANGE,
+ * DG_E_CAPACITY and DG_E_OVERFLOW as for dg_dag_sizes; the workspace is
+ * dg_workspace_size(g, n). */
+dg_status dg_dag(const dg_graph* g, const int64_t* d_locs, int64_t n, int64_t* d_node_offsets, int64_t* d_edge_offsets,
+                 uint32_t* d_nodes, uint32_t* d_node_edge, uint32_t* d_edges, uint32_t* d_mults, int64_t node_capacity,
+                 int64_t edge_capacity, void* d_ws, int64_t* h_nodes, int64_t* h_edges, void* stream);
 
 /* dg_enumerate_range: dg_enumerate over the contiguous flat locations
  * first, first + 1, ..., first + n - 1 (row i belongs to location

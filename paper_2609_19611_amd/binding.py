@@ -122,6 +122,7 @@ def _load():
         "dg_graph_tensor": ([P, i32, P], i32),
         "dg_dag_sizes": ([P, P, i64, P, P, P, ctypes.POINTER(i64), ctypes.POINTER(i64), P], i32),
         "dg_dag_fill": ([P, P, i64, P, P, P, P, P, P, P, P], i32),
+        "dg_dag": ([P, P, i64, P, P, P, P, P, P, i64, i64, P, ctypes.POINTER(i64), ctypes.POINTER(i64), P], i32),
         "dg_order_prefix": ([P, i32, i32, P, i64, ctypes.POINTER(i64)], i32),
         "dg_graph_text": ([P, ctypes.c_char_p, sz, ctypes.POINTER(sz)], i32),
         "dg_graph_merge": ([P, P, i32, ctypes.POINTER(P), ctypes.POINTER(P), ctypes.POINTER(i32)], i32),
@@ -487,6 +488,30 @@ def dg_dag_fill(g: Graph, d_locs: torch.Tensor, d_node_offsets: torch.Tensor, d_
         _dev_u32(t, what)
     _check(_lib.dg_dag_fill(g.handle, _ptr(d_locs), n, _ptr(d_node_offsets), _ptr(d_edge_offsets), _ptr(d_nodes),
                             _ptr(d_node_edge), _ptr(d_edges), _ptr(d_mults), _ptr(d_ws), _stream(stream)))
+
+
+def dg_dag(g: Graph, d_locs: torch.Tensor, d_node_offsets: torch.Tensor, d_edge_offsets: torch.Tensor,
+           d_nodes: torch.Tensor, d_node_edge: torch.Tensor, d_edges: torch.Tensor, d_mults: torch.Tensor,
+           d_ws: torch.Tensor, stream=None):
+    """Expression DAGs in one call into buffers sized beforehand (their
+    lengths are the capacities); returns (total nodes, total edges).
+    Raises DgError (DG_E_BUFFER) when a total exceeds its buffer; the
+    offsets are then written."""
+    n = d_locs.numel()
+    _dev_i64(d_locs, "locations")
+    for t, what in ((d_node_offsets, "node offsets"), (d_edge_offsets, "edge offsets")):
+        _dev_i64(t, what)
+        if t.numel() < n + 1:
+            raise ValueError(f"{what} needs n + 1 entries")
+    for t, what in ((d_nodes, "nodes"), (d_node_edge, "node edges"), (d_edges, "edges"), (d_mults, "mults")):
+        _dev_u32(t, what)
+    if d_nodes.numel() != d_node_edge.numel() or d_edges.numel() != d_mults.numel():
+        raise ValueError("nodes and node edges, and edges and mults, need equal lengths")
+    nn, ne = ctypes.c_int64(), ctypes.c_int64()
+    _check(_lib.dg_dag(g.handle, _ptr(d_locs), n, _ptr(d_node_offsets), _ptr(d_edge_offsets), _ptr(d_nodes),
+                       _ptr(d_node_edge), _ptr(d_edges), _ptr(d_mults), d_nodes.numel(), d_edges.numel(),
+                       _ptr(d_ws), ctypes.byref(nn), ctypes.byref(ne), _stream(stream)))
+    return nn.value, ne.value
 
 
 def dag_locations(g: Graph, locs, stream=None) -> dict:

@@ -362,6 +362,22 @@ WsLayout ws_layout(int64_t n) {
   return w;
 }
 
+// Workspace of the one-pass DAG call: error word | ticket | one status word
+// per location for the node counts, then one for the edge counts.
+struct DagWsLayout {
+  size_t err, ticket, st_nodes, st_edges, total;
+};
+DagWsLayout dag_ws_layout(int64_t n) {
+  const size_t words = (size_t)((n < 0 ? 0 : n) + 1);
+  DagWsLayout w;
+  w.err = 0;
+  w.ticket = 8;
+  w.st_nodes = 256;
+  w.st_edges = (w.st_nodes + 8 * words + 255) & ~size_t(255);
+  w.total = (w.st_edges + 8 * words + 255) & ~size_t(255);
+  return w;
+}
+
 dg_status device_errors(uint32_t bits) {
   if (bits & DGP_ERR_RANGE) return set_error(DG_E_RANGE, "a location lies outside the output tensor");
   if (bits & DGP_ERR_OVERFLOW) return set_error(DG_E_OVERFLOW, "a path count does not fit 32 bits");
@@ -580,7 +596,7 @@ dg_status dg_graph_tensor(const dg_graph* g, int32_t i, dg_tensor_info_t* out) {
 
 dg_status dg_workspace_size(const dg_graph* g, int64_t n_locs, size_t* bytes) {
   if (!g || !bytes || n_locs < 0) return set_error(DG_E_INVALID_ARG, "bad argument");
-  *bytes = ws_layout(n_locs).total;
+  *bytes = std::max(ws_layout(n_locs).total, dag_ws_layout(n_locs).total);
   return DG_OK;
 }
 
@@ -1074,6 +1090,119 @@ dg_status dg_dag_fill(const dg_graph* g, const int64_t* d_locs, int64_t n, const
     DG_HIP(hipMemcpyAsync(&bits, err, sizeof(uint32_t), hipMemcpyDeviceToHost, s), "copy flags");
     DG_HIP(hipStreamSynchronize(s), "DAG fill sync");
     return device_errors(bits);
+  });
+}
+
+namespace {
+
+// Where the one-pass DAG kernels stage a location's DAG in LDS (after the
+// walk's area) and the LDS a block then needs: node and edge slots of the
+// program's static bounds, two words each.  0 when that exceeds 64 KiB or
+// the device's limit (the call then takes the two passes).
+uint32_t dag_stage_off(const dg_graph* g) { return (g->dag.lds_bytes + 15u) & ~15u; }
+
+// Calls of at most this many locations take the one pass: it saves the
+// host round trip between the two passes, but a location costs about 2.5x
+// its two-pass time (c5: 0.15 against 0.19 ms at 1,024 locations, 3.3
+// against 1.3 ms at 262,144).  DIRIGO_DAG_ONEPASS=1 takes it whenever the
+// stage fits, DIRIGO_DAG_ONEPASS=0 never.
+constexpr int64_t kDagOnePassMax = 2048;
+bool dag_onepass_wanted(int64_t n) {
+  const char* env = std::getenv("DIRIGO_DAG_ONEPASS");
+  if (env && env[0] == '1') return true;
+  if (env && env[0] == '0') return false;
+  return n <= kDagOnePassMax;
+}
+uint32_t dag_onepass_lds(const dg_graph* g) {
+  const uint64_t words = 2ull * (uint64_t)g->dag.max_nodes + 2ull * (uint64_t)g->dag.max_edges;
+  const uint64_t lds = (uint64_t)dag_stage_off(g) + 4ull * words;
+  return lds <= std::min<uint64_t>(65536u, (uint64_t)max_lds_per_block()) ? (uint32_t)lds : 0u;
+}
+
+}  // namespace
+
+dg_status dg_dag(const dg_graph* g, const int64_t* d_locs, int64_t n, int64_t* d_node_offsets, int64_t* d_edge_offsets,
+                 uint32_t* d_nodes, uint32_t* d_node_edge, uint32_t* d_edges, uint32_t* d_mults, int64_t node_capacity,
+                 int64_t edge_capacity, void* d_ws, int64_t* h_nodes, int64_t* h_edges, void* stream) {
+  if (!g || !d_node_offsets || !d_edge_offsets || !h_nodes || !h_edges || n < 0 || n > kMaxLocations ||
+      node_capacity < 0 || edge_capacity < 0 || (n > 0 && !d_locs) ||
+      (node_capacity > 0 && (!d_nodes || !d_node_edge)) || (edge_capacity > 0 && (!d_edges || !d_mults)))
+    return set_error(DG_E_INVALID_ARG, "bad argument");
+  if (!d_ws) return set_error(DG_E_WORKSPACE, "workspace is required");
+  return guarded([&]() -> dg_status {
+    const uint8_t* dblob = nullptr;
+    dg_status st = dag_program(g, &dblob);
+    if (st != DG_OK) return st;
+    if (g->dag.lds_bytes > (uint32_t)max_lds_per_block())
+      return set_error(DG_E_CAPACITY, "one location's DAG frontiers need " + std::to_string(g->dag.lds_bytes) +
+                                          " bytes of LDS");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    if (n == 0) {
+      DG_HIP(dgk::launch_scan(d_node_offsets, 0, nullptr, s), "offsets");
+      DG_HIP(dgk::launch_scan(d_edge_offsets, 0, nullptr, s), "offsets");
+      DG_HIP(hipStreamSynchronize(s), "sync");
+      *h_nodes = 0;
+      *h_edges = 0;
+      return DG_OK;
+    }
+    const uint32_t lds = dag_onepass_wanted(n) ? dag_onepass_lds(g) : 0u;
+    if (lds == 0) {
+      // The two passes: sizes, then the fill when it fits.
+      int64_t tn = 0, te = 0;
+      st = dg_dag_sizes(g, d_locs, n, d_node_offsets, d_edge_offsets, d_ws, &tn, &te, stream);
+      if (st != DG_OK) return st;
+      *h_nodes = tn;
+      *h_edges = te;
+      if (tn > node_capacity || te > edge_capacity)
+        return set_error(DG_E_BUFFER, "the DAGs need more nodes or edges than the output buffers hold");
+      return dg_dag_fill(g, d_locs, n, d_node_offsets, d_edge_offsets, d_nodes, d_node_edge, d_edges, d_mults, d_ws,
+                         stream);
+    }
+    DagWsLayout w = dag_ws_layout(n);
+    uint8_t* ws = static_cast<uint8_t*>(d_ws);
+    uint32_t* err = reinterpret_cast<uint32_t*>(ws + w.err);
+    uint64_t* ticket = reinterpret_cast<uint64_t*>(ws + w.ticket);
+    uint64_t* st_n = reinterpret_cast<uint64_t*>(ws + w.st_nodes);
+    uint64_t* st_e = reinterpret_cast<uint64_t*>(ws + w.st_edges);
+    DG_HIP(dgk::launch_zero(err, s), "zero");
+    DG_HIP(dgk::launch_zero_u64(st_n, n, s), "zero status");
+    DG_HIP(dgk::launch_zero_u64(st_e, n, s), "zero status");
+    DG_HIP(dgk::launch_zero_u64(ticket, 1, s), "zero ticket");
+    const dg::JitModule* jm = dag_jit(g, n);
+    if (jm && !jm->dag_onepass) jm = nullptr;
+    dgc::LocSrc src{d_locs, 0};
+    uint64_t ncap = (uint64_t)node_capacity, ecap = (uint64_t)edge_capacity;
+    uint32_t stage_off = dag_stage_off(g), stage_nodes = (uint32_t)g->dag.max_nodes,
+             stage_edges = (uint32_t)g->dag.max_edges;
+    // Blocks take their locations from a ticket counter (as for
+    // dg_enumerate), so a list longer than one grid runs as several
+    // launches of the same kernel.
+    DG_HIP(per_location(n, g->dag_block,
+                        [&](int64_t, int64_t m) {
+                          if (jm) {
+                            void* args[] = {&src, &n, &d_node_offsets, &d_edge_offsets, &d_nodes, &d_node_edge,
+                                            &d_edges, &d_mults, &ncap, &ecap, &stage_off, &stage_nodes,
+                                            &stage_edges, &st_n, &st_e, &ticket, &err};
+                            return launch_module(jm->dag_onepass, m, g->dag_block, lds, s, args);
+                          }
+                          return dgk::launch_dag_onepass(dblob, src, n, m, d_node_offsets, d_edge_offsets, d_nodes,
+                                                         d_node_edge, d_edges, d_mults, ncap, ecap, stage_off,
+                                                         stage_nodes, stage_edges, st_n, st_e, ticket, err,
+                                                         g->dag_block, lds, s);
+                        }),
+           "DAG one-pass kernel");
+    int64_t tn = 0, te = 0;
+    uint32_t bits = 0;
+    DG_HIP(hipMemcpyAsync(&tn, d_node_offsets + n, sizeof(int64_t), hipMemcpyDeviceToHost, s), "copy total");
+    DG_HIP(hipMemcpyAsync(&te, d_edge_offsets + n, sizeof(int64_t), hipMemcpyDeviceToHost, s), "copy total");
+    DG_HIP(hipMemcpyAsync(&bits, err, sizeof(uint32_t), hipMemcpyDeviceToHost, s), "copy flags");
+    DG_HIP(hipStreamSynchronize(s), "DAG one-pass sync");
+    *h_nodes = tn;
+    *h_edges = te;
+    st = device_errors(bits);
+    if (st == DG_E_BUFFER)
+      return set_error(DG_E_BUFFER, "the DAGs need more nodes or edges than the output buffers hold");
+    return st;
   });
 }
 

@@ -164,4 +164,69 @@ DGC void dag_fill_body(const uint8_t* __restrict__ dblob, dgc::LocSrc locs, int6
   if (e) atomicOr(err, e);
 }
 
+// One pass over the locations for DAGs that fit in LDS: the walk writes the
+// location's nodes and edges into an LDS stage after the walk's own area
+// (stage_nodes node slots, two words each, then stage_edges edge slots, two
+// words each); a node's first edge is relative to its location, so the
+// stage does not depend on where the location's DAG lands.  The location's
+// node and edge offsets then come from two decoupled look-backs over its
+// predecessors' counts (st_nodes and st_edges, as for the single-pass
+// enumeration), and the stage is copied out when it fits the capacities.
+// Blocks take their locations from a ticket counter, so every lower index
+// belongs to a block that is already running.
+template <int BLOCK>
+DGC void dag_onepass_body(const uint8_t* __restrict__ dblob, dgc::LocSrc locs, int64_t n,
+                          int64_t* __restrict__ node_off, int64_t* __restrict__ edge_off,
+                          uint32_t* __restrict__ nodes, uint32_t* __restrict__ node_edge,
+                          uint32_t* __restrict__ edges, uint32_t* __restrict__ mults, uint64_t node_cap,
+                          uint64_t edge_cap, uint32_t stage_off, uint32_t stage_nodes, uint32_t stage_edges,
+                          uint64_t* __restrict__ st_nodes, uint64_t* __restrict__ st_edges,
+                          unsigned long long* __restrict__ ticket, uint32_t* __restrict__ err) {
+  __shared__ uint32_t wsum[BLOCK / 64];
+  __shared__ uint64_t wsum64[BLOCK / 64];
+  __shared__ int64_t sh_i;
+  __shared__ uint64_t sh_noff, sh_eoff;
+  if (threadIdx.x == 0) sh_i = (int64_t)atomicAdd(ticket, 1ull);
+  __syncthreads();
+  const int64_t i = sh_i;
+  if (i >= n) return;
+  DagDevCtx<BLOCK> c{{wsum}, wsum64};
+  uint32_t e = 0;
+  uint8_t* area = reinterpret_cast<uint8_t*>(dg_smem);
+  uint32_t* sn = reinterpret_cast<uint32_t*>(area + stage_off);
+  uint32_t* sne = sn + stage_nodes;
+  uint32_t* se = sne + stage_nodes;
+  uint32_t* sm = se + stage_edges;
+  dgc::DagOut o{sn, sne, se, sm, stage_nodes, stage_edges};
+  uint64_t nn = 0, ne = 0;
+  dgc::location_dag<DagDevCtx<BLOCK>, dgc::DAG_FILL>(c, dblob, dgc::loc_at(locs, i), area, o, &nn, &ne, &e);
+  if (nn > stage_nodes || ne > stage_edges) {
+    // (Never for a program whose static bounds size the stage.)
+    e |= DGP_ERR_CAPACITY;
+    nn = 0;
+    ne = 0;
+  }
+  __syncthreads();  // the stage is complete
+  if (threadIdx.x == 0) {
+    __hip_atomic_store(&st_nodes[i], (i == 0 ? ST_PREFIX : ST_SIZE) | nn, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&st_edges[i], (i == 0 ? ST_PREFIX : ST_SIZE) | ne, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  bool go_n = false, go_e = false;
+  LookBack<BLOCK> lb_n{st_nodes, i, n, nn, node_cap, node_off, &sh_noff, &e};
+  const uint64_t n0 = lb_n(c, &go_n);
+  LookBack<BLOCK> lb_e{st_edges, i, n, ne, edge_cap, edge_off, &sh_eoff, &e};
+  const uint64_t e0 = lb_e(c, &go_e);
+  if (go_n)
+    for (uint64_t k = threadIdx.x; k < nn; k += BLOCK) {
+      nodes[n0 + k] = sn[k];
+      node_edge[n0 + k] = sne[k];
+    }
+  if (go_e)
+    for (uint64_t k = threadIdx.x; k < ne; k += BLOCK) {
+      edges[e0 + k] = se[k];
+      mults[e0 + k] = sm[k];
+    }
+  if (e) atomicOr(err, e);
+}
+
 }  // namespace dgk_dev

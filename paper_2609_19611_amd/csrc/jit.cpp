@@ -240,6 +240,7 @@ bool jit_load(const std::string& source, JitModule* out, std::string* log) {
   get("dg_enumerate_wide", &out->enumerate_wide);
   get("dg_dag_sizes", &out->dag_sizes);
   get("dg_dag_fill", &out->dag_fill);
+  get("dg_dag_onepass", &out->dag_onepass);
   return true;
 }
 

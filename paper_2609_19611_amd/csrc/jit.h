@@ -25,7 +25,7 @@ std::string jit_wide_source(const Plan& p, int block);
 std::string jit_compare_source(const Plan& a, const Plan& b, const dgc::PairPlan& pp, int block);
 
 // Source of the specialised expression-DAG kernels (dg_dag_sizes,
-// dg_dag_fill) of one DAG program for blocks of `block` threads: the
+// dg_dag_fill, dg_dag_onepass) of one DAG program for blocks of `block` threads: the
 // program's ops are walked unrolled, and only the ways of taking a group
 // that its groups use are compiled.
 std::string jit_dag_source(const DagProgram& p, int block);
@@ -54,7 +54,7 @@ namespace dg {
 struct JitModule {
   hipModule_t mod = nullptr;
   hipFunction_t sizes = nullptr, fill = nullptr, enumerate = nullptr, compare = nullptr, enumerate_wide = nullptr;
-  hipFunction_t dag_sizes = nullptr, dag_fill = nullptr;
+  hipFunction_t dag_sizes = nullptr, dag_fill = nullptr, dag_onepass = nullptr;
   int dev = -1;        // device the module is loaded on
   std::string source;  // its source (the key of the shared module)
 };

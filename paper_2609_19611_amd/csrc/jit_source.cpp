@@ -130,7 +130,15 @@ std::string jit_dag_source(const DagProgram& p, int block) {
     << "    const int64_t* __restrict__ node_off, const int64_t* __restrict__ edge_off, uint32_t* __restrict__ nodes,\n"
     << "    uint32_t* __restrict__ node_edge, uint32_t* __restrict__ edges, uint32_t* __restrict__ mults,\n"
     << "    uint32_t* __restrict__ err) {\n"
-    << "  dgk_dev::dag_fill_body<DG_B>(dg_dag, locs, n, node_off, edge_off, nodes, node_edge, edges, mults, err);\n}\n";
+    << "  dgk_dev::dag_fill_body<DG_B>(dg_dag, locs, n, node_off, edge_off, nodes, node_edge, edges, mults, err);\n}\n"
+    << "extern \"C\" __global__ __launch_bounds__(DG_B) void dg_dag_onepass(dgc::LocSrc locs, int64_t n,\n"
+    << "    int64_t* __restrict__ node_off, int64_t* __restrict__ edge_off, uint32_t* __restrict__ nodes,\n"
+    << "    uint32_t* __restrict__ node_edge, uint32_t* __restrict__ edges, uint32_t* __restrict__ mults,\n"
+    << "    uint64_t node_cap, uint64_t edge_cap, uint32_t stage_off, uint32_t stage_nodes, uint32_t stage_edges,\n"
+    << "    uint64_t* __restrict__ st_nodes, uint64_t* __restrict__ st_edges, unsigned long long* __restrict__ ticket,\n"
+    << "    uint32_t* __restrict__ err) {\n"
+    << "  dgk_dev::dag_onepass_body<DG_B>(dg_dag, locs, n, node_off, edge_off, nodes, node_edge, edges, mults,\n"
+    << "      node_cap, edge_cap, stage_off, stage_nodes, stage_edges, st_nodes, st_edges, ticket, err);\n}\n";
   return o.str();
 }
 

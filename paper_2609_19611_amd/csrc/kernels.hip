@@ -48,6 +48,17 @@ __global__ __launch_bounds__(BLOCK) void k_dag_fill(const uint8_t* __restrict__ 
 }
 
 template <int BLOCK>
+__global__ __launch_bounds__(BLOCK) void k_dag_onepass(
+    const uint8_t* __restrict__ dblob, dgc::LocSrc locs, int64_t n, int64_t* __restrict__ node_off,
+    int64_t* __restrict__ edge_off, uint32_t* __restrict__ nodes, uint32_t* __restrict__ node_edge,
+    uint32_t* __restrict__ edges, uint32_t* __restrict__ mults, uint64_t node_cap, uint64_t edge_cap,
+    uint32_t stage_off, uint32_t stage_nodes, uint32_t stage_edges, uint64_t* __restrict__ st_nodes,
+    uint64_t* __restrict__ st_edges, unsigned long long* __restrict__ ticket, uint32_t* __restrict__ err) {
+  dgk_dev::dag_onepass_body<BLOCK>(dblob, locs, n, node_off, edge_off, nodes, node_edge, edges, mults, node_cap,
+                                   edge_cap, stage_off, stage_nodes, stage_edges, st_nodes, st_edges, ticket, err);
+}
+
+template <int BLOCK>
 __global__ __launch_bounds__(BLOCK) void k_compare(const uint8_t* __restrict__ blob_a,
                                                    const uint8_t* __restrict__ blob_b,
                                                    const dgc::PairPlan* __restrict__ pp, dgc::LocSrc locs,
@@ -249,6 +260,30 @@ hipError_t launch_dag_sizes(const uint8_t* dblob, dgc::LocSrc locs, int64_t n, i
   } else if (block == 64) {
     if ((e = allow_lds(k_dag_sizes<64>, lds)) != hipSuccess) return e;
     hipLaunchKernelGGL(k_dag_sizes<64>, dim3((unsigned)n), dim3(64), lds, s, dblob, locs, n, nodes_n, edges_n, err);
+  } else {
+    return hipErrorInvalidConfiguration;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_dag_onepass(const uint8_t* dblob, dgc::LocSrc locs, int64_t n, int64_t blocks, int64_t* node_off,
+                              int64_t* edge_off, uint32_t* nodes, uint32_t* node_edge, uint32_t* edges,
+                              uint32_t* mults, uint64_t node_cap, uint64_t edge_cap, uint32_t stage_off,
+                              uint32_t stage_nodes, uint32_t stage_edges, uint64_t* st_nodes, uint64_t* st_edges,
+                              uint64_t* ticket, uint32_t* err, int block, uint32_t lds, hipStream_t s) {
+  if (blocks <= 0) return hipSuccess;
+  unsigned long long* t = reinterpret_cast<unsigned long long*>(ticket);
+  hipError_t e;
+  if (block == 256) {
+    if ((e = allow_lds(k_dag_onepass<256>, lds)) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_dag_onepass<256>, dim3((unsigned)blocks), dim3(256), lds, s, dblob, locs, n, node_off,
+                       edge_off, nodes, node_edge, edges, mults, node_cap, edge_cap, stage_off, stage_nodes,
+                       stage_edges, st_nodes, st_edges, t, err);
+  } else if (block == 64) {
+    if ((e = allow_lds(k_dag_onepass<64>, lds)) != hipSuccess) return e;
+    hipLaunchKernelGGL(k_dag_onepass<64>, dim3((unsigned)blocks), dim3(64), lds, s, dblob, locs, n, node_off,
+                       edge_off, nodes, node_edge, edges, mults, node_cap, edge_cap, stage_off, stage_nodes,
+                       stage_edges, st_nodes, st_edges, t, err);
   } else {
     return hipErrorInvalidConfiguration;
   }

@@ -17,7 +17,7 @@ CAT = tiny_graphs.catalogue()
 
 def test_library_exports_every_header_symbol():
     names = B.header_symbols()
-    assert len(names) == 24
+    assert len(names) == 25
     lib = ctypes.CDLL(B.LIB_PATH)
     for n in names:
         assert hasattr(lib, n), n
@@ -207,6 +207,27 @@ def test_calls_over_2_31_locations_are_rejected_before_any_work():
     ]
     for call in calls:
         assert B.STATUS_NAMES[call()] == "DG_E_INVALID_ARG"
+
+
+def test_one_call_dag_rejects_bad_arguments_before_any_work():
+    """dg_dag checks its arguments before any device work (no device is
+    needed here): too many locations, negative capacities, missing output
+    buffers for a non-zero capacity, missing totals, and no workspace."""
+    g = B.dg_graph_parse(W.CONFIGS["c1"]["text"]())
+    fake = ctypes.c_void_p(0x1000)  # never dereferenced
+    nn, ne = ctypes.c_int64(), ctypes.c_int64()
+
+    def call(n=4, ncap=8, ecap=8, nodes=fake, edges=fake, ws=fake, tot=True):
+        return B.STATUS_NAMES[B._lib.dg_dag(g.handle, fake, n, fake, fake, nodes, nodes, edges, edges, ncap, ecap, ws,
+                                            ctypes.byref(nn) if tot else None, ctypes.byref(ne), None)]
+    assert call(n=(1 << 31) + 1) == "DG_E_INVALID_ARG"
+    assert call(n=-1) == "DG_E_INVALID_ARG"
+    assert call(ncap=-1) == "DG_E_INVALID_ARG"
+    assert call(ecap=-1) == "DG_E_INVALID_ARG"
+    assert call(nodes=None) == "DG_E_INVALID_ARG"
+    assert call(edges=None) == "DG_E_INVALID_ARG"
+    assert call(tot=False) == "DG_E_INVALID_ARG"
+    assert call(ws=None) == "DG_E_WORKSPACE"
 
 
 def test_count_bound_is_an_exact_integer():

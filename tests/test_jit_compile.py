@@ -115,7 +115,7 @@ def test_dag_kernels_compile(name, block):
     src = _source(hostemu.lib().dgh_jit_dag_source, t, len(t), block)
     assert "#define DG_DAG_BOX 0" in src and "#define DG_DAG_NOPS" in src
     notes = _kernel_notes(_compile(src))
-    assert sorted(n for n, _ in notes) == ["dg_dag_fill", "dg_dag_sizes"]
+    assert sorted(n for n, _ in notes) == ["dg_dag_fill", "dg_dag_onepass", "dg_dag_sizes"]
     assert all(p == 0 for _, p in notes), notes
 
 
