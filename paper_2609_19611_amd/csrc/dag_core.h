@@ -311,8 +311,38 @@ DGC uint32_t box_unique(C& c, const DgdTensor& X, uint32_t* F, uint32_t n, uint3
   return (uint32_t)total;
 }
 
+// An index function at the calling thread's variables, as ifn_eval; in a
+// specialised kernel its terms are unrolled, so that each term's variable,
+// coefficient and divisor are constants (a division by a constant divisor
+// instead of the general sequence).
+DGC bool ifn_eval_dag(const DgpIFn& f, const int32_t* vt, int nt, int32_t* out) {
+#ifdef DG_DAG_NOPS
+  int32_t x = f.c;
+  DG_DAG_UNROLL
+  for (int q = 0; q < DGP_MAX_FTERMS; ++q) {
+    if (q < f.nterm) {
+      int32_t vv = vt[f.var[q] * nt];
+      const int32_t d = f.vdiv[q];
+      if (d != 1) vv = vv / d;  // variables are non-negative
+      x += f.coef[q] * vv;
+    }
+  }
+  if (f.mode == 1) {
+    if (x % f.s != 0) return false;
+    x = x / f.s;
+  } else if (f.mode == 2) {
+    x = fdiv(x, f.s);
+  }
+  *out = x;
+  return x >= 0 && x < f.size;
+#else
+  return ifn_eval(f, vt, nt, out);
+#endif
+}
+
 // Coordinates of element e of X into the calling thread's variables 0..R-1.
 DGC void node_coords(const DgdTensor& X, uint32_t e, int32_t* vt, int nt) {
+  DG_DAG_UNROLL
   for (int d = DGP_MAX_RANK - 1; d >= 0; --d) {
     if (d < X.rank) {
       const uint32_t q = magic_div(e, X.magic[d]);
@@ -327,10 +357,11 @@ DGC void node_coords(const DgdTensor& X, uint32_t e, int32_t* vt, int nt) {
 DGC bool operand_flat(const DgdOperand& P, const DgdTensor& Ta, const int32_t* vt, int nt, uint32_t* flat) {
   uint32_t f = 0;
   bool ok = true;
+  DG_DAG_UNROLL
   for (int d = 0; d < DGP_MAX_RANK; ++d) {
     if (d < Ta.rank) {
       int32_t v = 0;
-      ok = ifn_eval(P.idx[d], vt, nt, &v) && ok;
+      ok = ifn_eval_dag(P.idx[d], vt, nt, &v) && ok;
       f += Ta.stride[d] * (uint32_t)v;
     }
   }
@@ -342,6 +373,7 @@ DGC bool operand_flat(const DgdOperand& P, const DgdTensor& Ta, const int32_t* v
 // variable with index `wv`).
 DGC void ifn_linear(const DgpIFn& f, int wv, const int32_t* vt, int nt, int32_t* c0, int32_t* k) {
   int32_t c = f.c, kk = 0;
+  DG_DAG_UNROLL
   for (int t = 0; t < DGP_MAX_FTERMS; ++t) {
     if (t < f.nterm) {
       if (f.var[t] == wv) {
@@ -384,16 +416,19 @@ template <class C>
 DGC uint32_t pointwise_node(C& c, const DagCtx& x, const DgdOp& op, uint64_t pos, const DagOut& o, bool emit,
                             bool append) {
   uint32_t k = 0;
+  DG_DAG_UNROLL
   for (int q = 0; q < op.ng; ++q) {
     const DgdGroup& G = x.Gs[op.g0 + q];
     if (G.points == 0) continue;
     bool ok = true;
+    DG_DAG_UNROLL
     for (int a = 0; a < G.nop; ++a) {
       const DgdOperand& P = x.Ps[G.op0 + a];
       uint32_t f;
       ok = operand_flat(P, x.T[P.tensor], x.vt, x.nt, &f) && ok;
     }
     if (!ok) continue;
+    DG_DAG_UNROLL
     for (int a = 0; a < G.nop; ++a) {
       const DgdOperand& P = x.Ps[G.op0 + a];
       const DgdTensor& Ta = x.T[P.tensor];
@@ -523,7 +558,7 @@ DGC uint64_t ap_setup(const DagCtx& x, const DgdGroup& G, int R, const Slots& S,
     const DgpIFn& f = P.idx[pr.d];
     if (pr.q < 0) {
       int32_t v;
-      if (!ifn_eval(f, x.vt, x.nt, &v)) bad = true;
+      if (!ifn_eval_dag(f, x.vt, x.nt, &v)) bad = true;
       continue;
     }
     const int q = pr.q;
@@ -575,7 +610,7 @@ DGC uint64_t ap_setup(const DagCtx& x, const DgdGroup& G, int R, const Slots& S,
     const DgpIFn& f = P.idx[pr.d];
     int32_t v = 0;
     if (pr.q < 0) {
-      ifn_eval(f, x.vt, x.nt, &v);
+      ifn_eval_dag(f, x.vt, x.nt, &v);
     } else {
       int32_t c0, k;
       ifn_linear(f, R + pr.q, x.vt, x.nt, &c0, &k);
@@ -617,7 +652,7 @@ DGC uint64_t ap_setup_reg(const DagCtx& x, const DgdGroup& G, int R, bool bases,
     const DgpIFn& f = x.Ps[G.op0 + pr.a].idx[pr.d];
     if (pr.q < 0) {
       int32_t v;
-      if (!ifn_eval(f, x.vt, x.nt, &v)) bad = true;
+      if (!ifn_eval_dag(f, x.vt, x.nt, &v)) bad = true;
       continue;
     }
     int32_t c0, k;
@@ -680,7 +715,7 @@ DGC uint64_t ap_setup_reg(const DagCtx& x, const DgdGroup& G, int R, bool bases,
     const DgpIFn& f = x.Ps[G.op0 + pr.a].idx[pr.d];
     int32_t v = 0;
     if (pr.q < 0) {
-      ifn_eval(f, x.vt, x.nt, &v);
+      ifn_eval_dag(f, x.vt, x.nt, &v);
     } else {
       int32_t c0, k;
       ifn_linear(f, R + pr.q, x.vt, x.nt, &c0, &k);
