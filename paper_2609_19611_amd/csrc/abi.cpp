@@ -1102,10 +1102,11 @@ namespace {
 uint32_t dag_stage_off(const dg_graph* g) { return (g->dag.lds_bytes + 15u) & ~15u; }
 
 // Calls of at most this many locations take the one pass: it saves the
-// host round trip between the two passes, but a location costs about 2.5x
-// its two-pass time (c5: 0.15 against 0.19 ms at 1,024 locations, 3.3
-// against 1.3 ms at 262,144).  DIRIGO_DAG_ONEPASS=1 takes it whenever the
-// stage fits, DIRIGO_DAG_ONEPASS=0 never.
+// host round trip between the two passes, but a location costs more than
+// its two passes at scale (c5: 0.15 against 0.19 ms at 1,024 locations,
+// 0.23 against 0.21 ms at 4,096, 3.3 against 0.97 ms at 262,144).
+// DIRIGO_DAG_ONEPASS=1 takes it whenever the stage fits,
+// DIRIGO_DAG_ONEPASS=0 never.
 constexpr int64_t kDagOnePassMax = 2048;
 bool dag_onepass_wanted(int64_t n) {
   const char* env = std::getenv("DIRIGO_DAG_ONEPASS");
