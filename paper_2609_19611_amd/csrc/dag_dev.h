@@ -123,44 +123,53 @@ struct DagDevCtx : DevCtx<BLOCK> {
 // offsets); the fill pass writes location i's nodes at node_off[i] and its
 // edges at edge_off[i].
 template <int BLOCK>
-DGC void dag_sizes_body(const uint8_t* __restrict__ dblob, dgc::LocSrc locs, int64_t n, int64_t* __restrict__ nodes_n,
-                        int64_t* __restrict__ edges_n, uint32_t* __restrict__ err) {
+// A block takes `per_block` consecutive locations, one after another (small
+// DAGs: a block's writes then form one longer run, and its start and end
+// are paid once for them all).
+DGC void dag_sizes_body(const uint8_t* __restrict__ dblob, dgc::LocSrc locs, int64_t n, int per_block,
+                        int64_t* __restrict__ nodes_n, int64_t* __restrict__ edges_n, uint32_t* __restrict__ err) {
   __shared__ uint32_t wsum[BLOCK / 64];
   __shared__ uint64_t wsum64[BLOCK / 64];
-  const int64_t i = blockIdx.x;
-  if (i >= n) return;
+  const int64_t i0 = (int64_t)blockIdx.x * per_block;
+  const int64_t i1 = i0 + per_block < n ? i0 + per_block : n;
   DagDevCtx<BLOCK> c{{wsum}, wsum64};
   uint32_t e = 0;
   uint8_t* area = reinterpret_cast<uint8_t*>(dg_smem);
   dgc::DagOut o{nullptr, nullptr, nullptr, nullptr, 0, 0};
-  uint64_t nn = 0, ne = 0;
-  dgc::location_dag<DagDevCtx<BLOCK>, dgc::DAG_COUNT>(c, dblob, dgc::loc_at(locs, i), area, o, &nn, &ne, &e);
-  if (threadIdx.x == 0) {
-    nodes_n[i + 1] = (int64_t)nn;
-    edges_n[i + 1] = (int64_t)ne;
+  for (int64_t i = i0; i < i1; ++i) {
+    uint64_t nn = 0, ne = 0;
+    dgc::location_dag<DagDevCtx<BLOCK>, dgc::DAG_COUNT>(c, dblob, dgc::loc_at(locs, i), area, o, &nn, &ne, &e);
+    if (threadIdx.x == 0) {
+      nodes_n[i + 1] = (int64_t)nn;
+      edges_n[i + 1] = (int64_t)ne;
+    }
+    __syncthreads();  // the next location reuses the LDS area
   }
   if (e) atomicOr(err, e);
 }
 
 template <int BLOCK>
-DGC void dag_fill_body(const uint8_t* __restrict__ dblob, dgc::LocSrc locs, int64_t n,
+DGC void dag_fill_body(const uint8_t* __restrict__ dblob, dgc::LocSrc locs, int64_t n, int per_block,
                        const int64_t* __restrict__ node_off, const int64_t* __restrict__ edge_off,
                        uint32_t* __restrict__ nodes, uint32_t* __restrict__ node_edge, uint32_t* __restrict__ edges,
                        uint32_t* __restrict__ mults, uint32_t* __restrict__ err) {
   __shared__ uint32_t wsum[BLOCK / 64];
   __shared__ uint64_t wsum64[BLOCK / 64];
-  const int64_t i = blockIdx.x;
-  if (i >= n) return;
+  const int64_t i0 = (int64_t)blockIdx.x * per_block;
+  const int64_t i1 = i0 + per_block < n ? i0 + per_block : n;
   DagDevCtx<BLOCK> c{{wsum}, wsum64};
   uint32_t e = 0;
   uint8_t* area = reinterpret_cast<uint8_t*>(dg_smem);
-  const int64_t n0 = node_off[i], e0 = edge_off[i];
-  const int64_t rn = node_off[i + 1] - n0, re = edge_off[i + 1] - e0;
-  dgc::DagOut o{nodes + n0, node_edge + n0, edges + e0, mults + e0, rn > 0 ? (uint64_t)rn : 0ull,
-                re > 0 ? (uint64_t)re : 0ull};
-  uint64_t nn = 0, ne = 0;
-  dgc::location_dag<DagDevCtx<BLOCK>, dgc::DAG_FILL>(c, dblob, dgc::loc_at(locs, i), area, o, &nn, &ne, &e);
-  if (threadIdx.x == 0 && ((int64_t)nn != rn || (int64_t)ne != re)) e |= DGP_ERR_SIZE;
+  for (int64_t i = i0; i < i1; ++i) {
+    const int64_t n0 = node_off[i], e0 = edge_off[i];
+    const int64_t rn = node_off[i + 1] - n0, re = edge_off[i + 1] - e0;
+    dgc::DagOut o{nodes + n0, node_edge + n0, edges + e0, mults + e0, rn > 0 ? (uint64_t)rn : 0ull,
+                  re > 0 ? (uint64_t)re : 0ull};
+    uint64_t nn = 0, ne = 0;
+    dgc::location_dag<DagDevCtx<BLOCK>, dgc::DAG_FILL>(c, dblob, dgc::loc_at(locs, i), area, o, &nn, &ne, &e);
+    if (threadIdx.x == 0 && ((int64_t)nn != rn || (int64_t)ne != re)) e |= DGP_ERR_SIZE;
+    __syncthreads();  // the next location reuses the LDS area
+  }
   if (e) atomicOr(err, e);
 }
 

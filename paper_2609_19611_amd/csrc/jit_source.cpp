@@ -123,14 +123,15 @@ std::string jit_dag_source(const DagProgram& p, int block) {
     << "#include \"dag_dev.h\"\n";
   emit_bytes(o, "dg_dag", p.blob);
   o << "#define DG_B " << block << "\n"
-    << "extern \"C\" __global__ __launch_bounds__(DG_B) void dg_dag_sizes(dgc::LocSrc locs, int64_t n,\n"
+    << "extern \"C\" __global__ __launch_bounds__(DG_B) void dg_dag_sizes(dgc::LocSrc locs, int64_t n, int per_block,\n"
     << "    int64_t* __restrict__ nodes_n, int64_t* __restrict__ edges_n, uint32_t* __restrict__ err) {\n"
-    << "  dgk_dev::dag_sizes_body<DG_B>(dg_dag, locs, n, nodes_n, edges_n, err);\n}\n"
-    << "extern \"C\" __global__ __launch_bounds__(DG_B) void dg_dag_fill(dgc::LocSrc locs, int64_t n,\n"
+    << "  dgk_dev::dag_sizes_body<DG_B>(dg_dag, locs, n, per_block, nodes_n, edges_n, err);\n}\n"
+    << "extern \"C\" __global__ __launch_bounds__(DG_B) void dg_dag_fill(dgc::LocSrc locs, int64_t n, int per_block,\n"
     << "    const int64_t* __restrict__ node_off, const int64_t* __restrict__ edge_off, uint32_t* __restrict__ nodes,\n"
     << "    uint32_t* __restrict__ node_edge, uint32_t* __restrict__ edges, uint32_t* __restrict__ mults,\n"
     << "    uint32_t* __restrict__ err) {\n"
-    << "  dgk_dev::dag_fill_body<DG_B>(dg_dag, locs, n, node_off, edge_off, nodes, node_edge, edges, mults, err);\n}\n"
+    << "  dgk_dev::dag_fill_body<DG_B>(dg_dag, locs, n, per_block, node_off, edge_off, nodes, node_edge, edges, mults,\n"
+    << "      err);\n}\n"
     << "extern \"C\" __global__ __launch_bounds__(DG_B) void dg_dag_onepass(dgc::LocSrc locs, int64_t n,\n"
     << "    int64_t* __restrict__ node_off, int64_t* __restrict__ edge_off, uint32_t* __restrict__ nodes,\n"
     << "    uint32_t* __restrict__ node_edge, uint32_t* __restrict__ edges, uint32_t* __restrict__ mults,\n"

@@ -38,9 +38,10 @@ hipError_t launch_enumerate_wide(const uint8_t* blob, dgc::LocSrc locs, int64_t 
                                  uint64_t* ticket, uint32_t* err, int block, uint32_t lds, hipStream_t s);
 // Expression DAGs (dag_program.h, DgdHeader; lds: the program's lds_bytes):
 // node and edge counts of location i into nodes_n[i + 1], edges_n[i + 1];
-// then nodes and edges at node_off[i], edge_off[i].
-hipError_t launch_dag_sizes(const uint8_t* dblob, dgc::LocSrc locs, int64_t n, int64_t* nodes_n, int64_t* edges_n,
-                            uint32_t* err, int block, uint32_t lds, hipStream_t s);
+// then nodes and edges at node_off[i], edge_off[i]; each block takes
+// per_block consecutive locations.
+hipError_t launch_dag_sizes(const uint8_t* dblob, dgc::LocSrc locs, int64_t n, int per_block, int64_t* nodes_n,
+                            int64_t* edges_n, uint32_t* err, int block, uint32_t lds, hipStream_t s);
 // One pass (sizes, offsets by look-back, DAGs) over n locations in a grid
 // of `blocks` blocks taking tickets (a list longer than one grid runs as
 // several launches); the stage follows the walk's LDS area.
@@ -49,7 +50,7 @@ hipError_t launch_dag_onepass(const uint8_t* dblob, dgc::LocSrc locs, int64_t n,
                               uint32_t* mults, uint64_t node_cap, uint64_t edge_cap, uint32_t stage_off,
                               uint32_t stage_nodes, uint32_t stage_edges, uint64_t* st_nodes, uint64_t* st_edges,
                               uint64_t* ticket, uint32_t* err, int block, uint32_t lds, hipStream_t s);
-hipError_t launch_dag_fill(const uint8_t* dblob, dgc::LocSrc locs, int64_t n, const int64_t* node_off,
+hipError_t launch_dag_fill(const uint8_t* dblob, dgc::LocSrc locs, int64_t n, int per_block, const int64_t* node_off,
                            const int64_t* edge_off, uint32_t* nodes, uint32_t* node_edge, uint32_t* edges,
                            uint32_t* mults, uint32_t* err, int block, uint32_t lds, hipStream_t s);
 // Location order: positions [first, first + count) of the keyed

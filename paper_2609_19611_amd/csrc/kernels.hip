@@ -33,18 +33,18 @@ __global__ __launch_bounds__(BLOCK) void k_fill(const uint8_t* __restrict__ blob
 
 template <int BLOCK>
 __global__ __launch_bounds__(BLOCK) void k_dag_sizes(const uint8_t* __restrict__ dblob, dgc::LocSrc locs, int64_t n,
-                                                     int64_t* __restrict__ nodes_n, int64_t* __restrict__ edges_n,
-                                                     uint32_t* __restrict__ err) {
-  dgk_dev::dag_sizes_body<BLOCK>(dblob, locs, n, nodes_n, edges_n, err);
+                                                     int per_block, int64_t* __restrict__ nodes_n,
+                                                     int64_t* __restrict__ edges_n, uint32_t* __restrict__ err) {
+  dgk_dev::dag_sizes_body<BLOCK>(dblob, locs, n, per_block, nodes_n, edges_n, err);
 }
 
 template <int BLOCK>
 __global__ __launch_bounds__(BLOCK) void k_dag_fill(const uint8_t* __restrict__ dblob, dgc::LocSrc locs, int64_t n,
-                                                    const int64_t* __restrict__ node_off,
+                                                    int per_block, const int64_t* __restrict__ node_off,
                                                     const int64_t* __restrict__ edge_off, uint32_t* __restrict__ nodes,
                                                     uint32_t* __restrict__ node_edge, uint32_t* __restrict__ edges,
                                                     uint32_t* __restrict__ mults, uint32_t* __restrict__ err) {
-  dgk_dev::dag_fill_body<BLOCK>(dblob, locs, n, node_off, edge_off, nodes, node_edge, edges, mults, err);
+  dgk_dev::dag_fill_body<BLOCK>(dblob, locs, n, per_block, node_off, edge_off, nodes, node_edge, edges, mults, err);
 }
 
 template <int BLOCK>
@@ -250,16 +250,20 @@ hipError_t launch_fill(const uint8_t* blob, dgc::LocSrc locs, int64_t n, const i
   return hipGetLastError();
 }
 
-hipError_t launch_dag_sizes(const uint8_t* dblob, dgc::LocSrc locs, int64_t n, int64_t* nodes_n, int64_t* edges_n,
-                            uint32_t* err, int block, uint32_t lds, hipStream_t s) {
+hipError_t launch_dag_sizes(const uint8_t* dblob, dgc::LocSrc locs, int64_t n, int per_block, int64_t* nodes_n,
+                            int64_t* edges_n, uint32_t* err, int block, uint32_t lds, hipStream_t s) {
   if (n <= 0) return hipSuccess;
+  if (per_block < 1) return hipErrorInvalidValue;
+  const unsigned grid = (unsigned)((n + per_block - 1) / per_block);
   hipError_t e;
   if (block == 256) {
     if ((e = allow_lds(k_dag_sizes<256>, lds)) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_dag_sizes<256>, dim3((unsigned)n), dim3(256), lds, s, dblob, locs, n, nodes_n, edges_n, err);
+    hipLaunchKernelGGL(k_dag_sizes<256>, dim3(grid), dim3(256), lds, s, dblob, locs, n, per_block, nodes_n, edges_n,
+                       err);
   } else if (block == 64) {
     if ((e = allow_lds(k_dag_sizes<64>, lds)) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_dag_sizes<64>, dim3((unsigned)n), dim3(64), lds, s, dblob, locs, n, nodes_n, edges_n, err);
+    hipLaunchKernelGGL(k_dag_sizes<64>, dim3(grid), dim3(64), lds, s, dblob, locs, n, per_block, nodes_n, edges_n,
+                       err);
   } else {
     return hipErrorInvalidConfiguration;
   }
@@ -290,18 +294,20 @@ hipError_t launch_dag_onepass(const uint8_t* dblob, dgc::LocSrc locs, int64_t n,
   return hipGetLastError();
 }
 
-hipError_t launch_dag_fill(const uint8_t* dblob, dgc::LocSrc locs, int64_t n, const int64_t* node_off,
+hipError_t launch_dag_fill(const uint8_t* dblob, dgc::LocSrc locs, int64_t n, int per_block, const int64_t* node_off,
                            const int64_t* edge_off, uint32_t* nodes, uint32_t* node_edge, uint32_t* edges,
                            uint32_t* mults, uint32_t* err, int block, uint32_t lds, hipStream_t s) {
   if (n <= 0) return hipSuccess;
+  if (per_block < 1) return hipErrorInvalidValue;
+  const unsigned grid = (unsigned)((n + per_block - 1) / per_block);
   hipError_t e;
   if (block == 256) {
     if ((e = allow_lds(k_dag_fill<256>, lds)) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_dag_fill<256>, dim3((unsigned)n), dim3(256), lds, s, dblob, locs, n, node_off, edge_off,
+    hipLaunchKernelGGL(k_dag_fill<256>, dim3(grid), dim3(256), lds, s, dblob, locs, n, per_block, node_off, edge_off,
                        nodes, node_edge, edges, mults, err);
   } else if (block == 64) {
     if ((e = allow_lds(k_dag_fill<64>, lds)) != hipSuccess) return e;
-    hipLaunchKernelGGL(k_dag_fill<64>, dim3((unsigned)n), dim3(64), lds, s, dblob, locs, n, node_off, edge_off,
+    hipLaunchKernelGGL(k_dag_fill<64>, dim3(grid), dim3(64), lds, s, dblob, locs, n, per_block, node_off, edge_off,
                        nodes, node_edge, edges, mults, err);
   } else {
     return hipErrorInvalidConfiguration;
