@@ -275,8 +275,9 @@ const dg::JitModule* dag_jit(const dg_graph* cg, int64_t n) {
 // Consecutive locations per block of the DAG sizes and fill kernels: 8 for
 // small DAGs in one-wave blocks (at most 4,096 edges per location, static
 // bound), whose one-block rows are too short for a block's start and end to
-// vanish beside its writes (a plain writer of c5-sized rows, 4.6 KB per
-// array: 3.7 TB/s with one row per block, 5.0 with 8), else 1.
+// vanish beside its writes (a plain writer of 4.6 KB rows in two arrays,
+// the size of a 3x3, 64-channel conv2d node's DAG: 3.7 TB/s with one row per
+// block, 5.0 with 8), else 1.
 int dag_per_block(const dg_graph* g) { return g->dag_block == 64 && g->dag.max_edges <= 4096 ? 8 : 1; }
 
 // Leaf ids of g fit 32 bits.
@@ -1114,8 +1115,9 @@ uint32_t dag_stage_off(const dg_graph* g) { return (g->dag.lds_bytes + 15u) & ~1
 
 // Calls of at most this many locations take the one pass: it saves the
 // host round trip between the two passes, but a location costs more than
-// its two passes at scale (c5: 0.15 against 0.19 ms at 1,024 locations,
-// 0.23 against 0.21 ms at 4,096, 3.3 against 0.97 ms at 262,144).
+// its two passes at scale (the DAGs of a 3x3, 64-channel conv2d with an
+// affine and a relu: 0.15 against 0.19 ms at 1,024 locations, 0.23 against
+// 0.21 ms at 4,096, 3.3 against 0.97 ms at 262,144).
 // DIRIGO_DAG_ONEPASS=1 takes it whenever the stage fits,
 // DIRIGO_DAG_ONEPASS=0 never.
 constexpr int64_t kDagOnePassMax = 2048;
