@@ -145,6 +145,23 @@ def test_one_call_default_choice(B, monkeypatch):
     _check(B, text, W.config_locations("c5")[1::256])     # 4,096 locations
 
 
+@pytest.mark.parametrize("chunk", range(2))
+def test_one_call_fuzz(B, chunk):
+    """Seeded random graphs (as the fuzz tests build them): every output
+    location's DAG in one call, against the oracle."""
+    import fuzz_graphs
+    done = 0
+    for seed in range(chunk * 20, (chunk + 1) * 20):
+        text = fuzz_graphs.random_graph(seed)
+        try:
+            B.dg_graph_parse(text)
+        except B.DgError:
+            continue
+        _check(B, text, list(range(oracle.Graph(text).output_numel))[::-1])
+        done += 1
+    assert done >= 15
+
+
 def test_one_call_edge_cases(B):
     text = W.c2_text()
     (nn, ne), out = _call(B, text, [], 1, 1)
